@@ -1,0 +1,337 @@
+"""CPU oracle for the DeepReduce sparse-tensor codec (arXiv 2102.03112).
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only ``tests/``, the smoke check in
+``__graft_entry__`` and the CPU-baseline leg of ``bench.py`` may import this
+package.  The heavy loops live in ``drref.c`` (plain C99, single-threaded);
+this module marshals numpy arrays into it and strings the steps of one codec
+round trip together in the paper's order.  It shares no code with the GPU
+library and never imports it.
+
+Parity status of each function is recorded in its docstring; every function
+here is pinned by a test in ``tests/test_oracle_*.py`` against something other
+than itself (a worked example from the paper, a closed form, published test
+vectors, brute force, or an independent library routine).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libdrref.so")
+_lib = None
+
+OK, EINVAL, ECAPACITY = 0, -1, -2
+R_NONZERO = (1 << 64) - 1  # "select every nonzero" instead of a top-r count
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _build
+
+        _build.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    u8p = ctypes.POINTER(ctypes.c_uint8)
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    f32p = ctypes.POINTER(ctypes.c_float)
+    f64p = ctypes.POINTER(ctypes.c_double)
+    u32, u64 = ctypes.c_uint32, ctypes.c_uint64
+    sig = {
+        "drref_murmur3_32": (u32, [u8p, u64, u32]),
+        "drref_bloom_pos": (u64, [u32, u32, u64]),
+        "drref_bloom_pos_many": (None, [u32p, u64, u32, u64, u64p]),
+        "drref_bloom_params": (ctypes.c_int, [u64, ctypes.c_double, u64p, u32p]),
+        "drref_topr": (ctypes.c_int, [f32p, u64, u64, u32p]),
+        "drref_nonzero": (ctypes.c_int, [f32p, u64, u32p, u64, u64p]),
+        "drref_bloom_encode": (ctypes.c_int, [u32p, u64, u64, u32, u32p]),
+        "drref_bloom_query": (ctypes.c_int, [u32p, u64, u32, u64, u32p, u64, u64p]),
+        "drref_sort_desc": (ctypes.c_int, [f32p, u64, u32p]),
+        "drref_lsq_fit": (ctypes.c_int, [f64p, f64p, u64, u32, f64p]),
+        "drref_fit_shape": (None, [u64, u32, u32, u32p, u32p]),
+        "drref_sigma_bits": (u32, [u64]),
+        "drref_sigma_words": (u64, [u64]),
+        "drref_curvefit_encode": (
+            ctypes.c_int,
+            [f32p, u64, u32, u32, f32p, f64p, u32p, u32p, u32p, u32p],
+        ),
+        "drref_curvefit_decode": (ctypes.c_int, [f32p, u32p, u64, u32, u32, f32p]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def _check(st: int, what: str):
+    if st != OK:
+        raise OracleError(f"{what}: status {st}")
+
+
+# --------------------------------------------------------------------------
+# hash family and Bloom parameters
+# --------------------------------------------------------------------------
+
+
+def murmur3_32(data: bytes, seed: int) -> int:
+    """MurmurHash3_x86_32 of a byte string (Section 2 asks for k independent
+    hash functions; this codec takes murmur3 with seeds 0..k-1)."""
+    lib = _load()
+    buf = (ctypes.c_uint8 * max(1, len(data))).from_buffer_copy(data or b"\0")
+    return int(lib.drref_murmur3_32(buf, len(data), seed & 0xFFFFFFFF))
+
+
+def bloom_pos(idx, j: int, m: int) -> np.ndarray:
+    """Bit positions h_j(i) * m >> 32 for an array of indices."""
+    lib = _load()
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    out = np.empty(idx.size, dtype=np.uint64)
+    lib.drref_bloom_pos_many(_ptr(idx, ctypes.c_uint32), idx.size, j, m, _ptr(out, ctypes.c_uint64))
+    return out
+
+
+def bloom_params(n: int, fpr: float) -> tuple[int, int]:
+    """(m, k) from Remark 2 of Section 10.2, rounded as drref.c states."""
+    lib = _load()
+    m = ctypes.c_uint64()
+    k = ctypes.c_uint32()
+    _check(lib.drref_bloom_params(n, fpr, ctypes.byref(m), ctypes.byref(k)), "bloom_params")
+    return int(m.value), int(k.value)
+
+
+# --------------------------------------------------------------------------
+# sparsification
+# --------------------------------------------------------------------------
+
+
+def ratio_count(d: int, num: int, den: int) -> int:
+    """r = ceil(d * num / den) in integer arithmetic (the paper states r as a
+    percentage of d, Section 6; rounding up is this codec's reading)."""
+    return (d * num + den - 1) // den
+
+
+def topr(g: np.ndarray, r: int) -> np.ndarray:
+    """Indices of the r largest-magnitude entries, ascending (Section 10.2)."""
+    lib = _load()
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    S = np.empty(max(r, 1), dtype=np.uint32)
+    _check(lib.drref_topr(_ptr(g, ctypes.c_float), g.size, r, _ptr(S, ctypes.c_uint32)), "topr")
+    return S[:r]
+
+
+def nonzero(g: np.ndarray) -> np.ndarray:
+    """Support {i : g[i] != 0} of an inherently sparse gradient (Section 3)."""
+    lib = _load()
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    S = np.empty(max(g.size, 1), dtype=np.uint32)
+    n = ctypes.c_uint64()
+    _check(
+        lib.drref_nonzero(_ptr(g, ctypes.c_float), g.size, _ptr(S, ctypes.c_uint32), g.size, ctypes.byref(n)),
+        "nonzero",
+    )
+    return S[: n.value].copy()
+
+
+# --------------------------------------------------------------------------
+# Bloom filter
+# --------------------------------------------------------------------------
+
+
+def bloom_encode(S: np.ndarray, m: int, k: int) -> np.ndarray:
+    """m-bit filter (m/32 LSB-first u32 words) holding every index of S."""
+    lib = _load()
+    S = np.ascontiguousarray(S, dtype=np.uint32)
+    words = np.zeros(m // 32, dtype=np.uint32)
+    _check(lib.drref_bloom_encode(_ptr(S, ctypes.c_uint32), S.size, m, k, _ptr(words, ctypes.c_uint32)), "bloom_encode")
+    return words
+
+
+def bloom_query(words: np.ndarray, m: int, k: int, d: int) -> np.ndarray:
+    """Policy P0's set P: every i in [0, d) the filter reports, ascending."""
+    lib = _load()
+    words = np.ascontiguousarray(words, dtype=np.uint32)
+    cap = max(d, 1)
+    P = np.empty(cap, dtype=np.uint32)
+    n = ctypes.c_uint64()
+    _check(
+        lib.drref_bloom_query(_ptr(words, ctypes.c_uint32), m, k, d, _ptr(P, ctypes.c_uint32), cap, ctypes.byref(n)),
+        "bloom_query",
+    )
+    return P[: n.value].copy()
+
+
+# --------------------------------------------------------------------------
+# curve fitting of the values
+# --------------------------------------------------------------------------
+
+
+def sort_desc(V: np.ndarray) -> np.ndarray:
+    """perm[rank] = q: stable, signed descending order of V (Section 5)."""
+    lib = _load()
+    V = np.ascontiguousarray(V, dtype=np.float32)
+    perm = np.empty(max(V.size, 1), dtype=np.uint32)
+    _check(lib.drref_sort_desc(_ptr(V, ctypes.c_float), V.size, _ptr(perm, ctypes.c_uint32)), "sort_desc")
+    return perm[: V.size]
+
+
+def lsq_fit(x, y, D: int) -> np.ndarray:
+    """Least-squares polynomial coefficients (increasing powers) of degree D
+    through (x_j, y_j), normal equations in double (Section 5)."""
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.ascontiguousarray(y, dtype=np.float64)
+    c = np.zeros(D + 1, dtype=np.float64)
+    _check(lib.drref_lsq_fit(_ptr(x, ctypes.c_double), _ptr(y, ctypes.c_double), x.size, D, _ptr(c, ctypes.c_double)), "lsq_fit")
+    return c
+
+
+def fit_shape(n: int, D: int, S: int) -> tuple[int, int]:
+    lib = _load()
+    se = ctypes.c_uint32()
+    de = ctypes.c_uint32()
+    lib.drref_fit_shape(n, D, S, ctypes.byref(se), ctypes.byref(de))
+    return int(se.value), int(de.value)
+
+
+def sigma_bits(n: int) -> int:
+    return int(_load().drref_sigma_bits(n))
+
+
+def sigma_words(n: int) -> int:
+    return int(_load().drref_sigma_words(n))
+
+
+@dataclass
+class FitPayload:
+    coef: np.ndarray  # fp32, n_seg rows of degree+1
+    coef64: np.ndarray  # the double-precision solution the fp32 rows round
+    sigma: np.ndarray  # packed reorder map, u32 words
+    n: int
+    degree: int
+    n_seg: int
+    S_eff: int
+    D_eff: int
+    b: int
+
+
+def curvefit_encode(V: np.ndarray, degree: int, n_seg: int) -> FitPayload:
+    """Sort, segment, fit, and pack the reorder map (Sections 5 and 5.1)."""
+    lib = _load()
+    V = np.ascontiguousarray(V, dtype=np.float32)
+    n = V.size
+    coef = np.zeros(n_seg * (degree + 1), dtype=np.float32)
+    coef64 = np.zeros(n_seg * (degree + 1), dtype=np.float64)
+    sigma = np.zeros(max(sigma_words(n), 1), dtype=np.uint32)
+    se, de, b = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
+    _check(
+        lib.drref_curvefit_encode(
+            _ptr(V, ctypes.c_float), n, degree, n_seg, _ptr(coef, ctypes.c_float), _ptr(coef64, ctypes.c_double),
+            _ptr(sigma, ctypes.c_uint32), ctypes.byref(se), ctypes.byref(de), ctypes.byref(b),
+        ),
+        "curvefit_encode",
+    )
+    return FitPayload(coef, coef64, sigma[: sigma_words(n)], n, degree, n_seg, int(se.value), int(de.value), int(b.value))
+
+
+def curvefit_decode(coef: np.ndarray, sigma: np.ndarray, n: int, degree: int, n_seg: int) -> np.ndarray:
+    """Reconstruct the n values from the coefficients and reorder map."""
+    lib = _load()
+    coef = np.ascontiguousarray(coef, dtype=np.float32)
+    sigma = np.ascontiguousarray(sigma, dtype=np.uint32)
+    if sigma.size == 0:
+        sigma = np.zeros(1, dtype=np.uint32)
+    out = np.empty(max(n, 1), dtype=np.float32)
+    _check(
+        lib.drref_curvefit_decode(_ptr(coef, ctypes.c_float), _ptr(sigma, ctypes.c_uint32), n, degree, n_seg, _ptr(out, ctypes.c_float)),
+        "curvefit_decode",
+    )
+    return out[:n]
+
+
+def sigma_unpack(sigma: np.ndarray, n: int) -> np.ndarray:
+    """Read the n packed b-bit entries of a reorder map (plain bit loop)."""
+    b = sigma_bits(n)
+    bits = np.unpackbits(np.ascontiguousarray(sigma, dtype="<u4").view(np.uint8), bitorder="little")
+    out = np.zeros(n, dtype=np.uint64)
+    for t in range(b):
+        out |= bits[np.arange(n, dtype=np.int64) * b + t].astype(np.uint64) << np.uint64(t)
+    return out
+
+
+# --------------------------------------------------------------------------
+# one round trip over one tensor, in the paper's order
+# --------------------------------------------------------------------------
+
+
+@dataclass
+class TensorResult:
+    d: int
+    S: np.ndarray  # selected indices (sender), ascending
+    m: int
+    k: int
+    bits: np.ndarray  # Bloom filter words
+    P: np.ndarray  # sender-side P0 positives, ascending
+    V: np.ndarray  # g[P], from the dense original
+    fit: FitPayload
+    P_dec: np.ndarray  # receiver-side positives, from the filter words only
+    vals: np.ndarray  # reconstructed values, one per P_dec entry
+    dense: np.ndarray | None = field(default=None)
+
+    def payload_bits(self) -> dict:
+        """Bits that cross the network (Figure 3's container): the filter, the
+        fp32 coefficients actually used, and the reorder map."""
+        idx = self.m
+        val = 32 * self.fit.S_eff * (self.fit.D_eff + 1) if self.fit.n else 0
+        sig = self.fit.n * self.fit.b if self.fit.n else 0
+        return {"index": idx, "values": val, "sigma": sig}
+
+
+def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True) -> TensorResult:
+    """Sender: top-r (or support) -> Bloom insert -> P0 query -> V = g[P]
+    (values from the dense gradient, Section 4) -> curve-fit encode.
+    Receiver: P0 query from the filter words -> curve-fit decode -> scatter
+    into a dense gradient that is zero off P (Section 4's reconstruction).
+    ``r`` is an int or R_NONZERO."""
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    d = g.size
+    S = nonzero(g) if r == R_NONZERO else topr(g, int(r))
+    m, k = bloom_params(S.size, fpr)
+    bits = bloom_encode(S, m, k)
+    P = bloom_query(bits, m, k, d)
+    V = g[P.astype(np.int64)]
+    fit = curvefit_encode(V, degree, n_seg)
+    P_dec = bloom_query(bits, m, k, d)
+    vals = curvefit_decode(fit.coef, fit.sigma, P_dec.size, degree, n_seg)
+    dense = None
+    if want_dense:
+        dense = np.zeros(d, dtype=np.float32)
+        dense[P_dec.astype(np.int64)] = vals
+    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense)
+
+
+def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True):
+    """Code every tensor g[offsets[t]:offsets[t+1]] independently on local
+    indices.  ``ratio`` is (num, den) for top-r with r = ceil(d_t num / den),
+    or None for the support of an inherently sparse gradient."""
+    out = []
+    for t in range(len(offsets) - 1):
+        gt = g[offsets[t]: offsets[t + 1]]
+        r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
+        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense))
+    return out

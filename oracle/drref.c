@@ -1,0 +1,559 @@
+/*
+ * drref.c -- CPU oracle for the DeepReduce sparse-tensor codec
+ * (Kostopoulou et al., "DeepReduce: A Sparse-tensor Communication Framework
+ * for Distributed Deep Learning", arXiv 2102.03112).
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke
+ * check and the benchmark's CPU-baseline leg may load this library.  It is a
+ * plain, slow, single-threaded statement of what the codec computes, written
+ * so that each function can be checked against the paper by eye: no blocking,
+ * no fusion, no reordering beyond what the definitions state.  It shares no
+ * source, header, table or helper with the GPU library.
+ *
+ * Readings of the paper that this file fixes where the paper is silent
+ * (index base, tie order, rounding of the Bloom parameters, the hash family,
+ * the position map, the sort key, the abscissa, the segmentation rule and the
+ * width of the reorder map) are stated at the function that applies them.
+ *
+ * Status codes: 0 ok, -1 invalid argument, -2 output capacity too small
+ * (the required count is still reported).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define DRREF_OK 0
+#define DRREF_EINVAL (-1)
+#define DRREF_ECAPACITY (-2)
+
+/* ------------------------------------------------------------------------ */
+/* Hash family.                                                              */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The paper asks only for k independent hash functions (Section 2, "Bloom
+ * Filter"; Section 4).  This codec uses MurmurHash3_x86_32 (A. Appleby,
+ * SMHasher, public domain) with seeds 0..k-1.  The function below is the
+ * published algorithm for a byte string of any length; the codec only ever
+ * hashes the 4-byte little-endian encoding of a 0-based index.
+ */
+static uint32_t rotl32(uint32_t x, int r) { return (x << r) | (x >> (32 - r)); }
+
+uint32_t drref_murmur3_32(const uint8_t *data, uint64_t len, uint32_t seed)
+{
+    const uint32_t c1 = 0xcc9e2d51u;
+    const uint32_t c2 = 0x1b873593u;
+    uint32_t h = seed;
+    uint64_t nblocks = len / 4;
+    for (uint64_t b = 0; b < nblocks; ++b) {
+        const uint8_t *p = data + 4 * b;
+        uint32_t k = (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) |
+                     ((uint32_t)p[3] << 24);
+        k *= c1;
+        k = rotl32(k, 15);
+        k *= c2;
+        h ^= k;
+        h = rotl32(h, 13);
+        h = h * 5u + 0xe6546b64u;
+    }
+    const uint8_t *tail = data + 4 * nblocks;
+    uint32_t k = 0;
+    switch (len & 3) {
+    case 3:
+        k ^= (uint32_t)tail[2] << 16; /* fall through */
+    case 2:
+        k ^= (uint32_t)tail[1] << 8; /* fall through */
+    case 1:
+        k ^= (uint32_t)tail[0];
+        k *= c1;
+        k = rotl32(k, 15);
+        k *= c2;
+        h ^= k;
+    }
+    h ^= (uint32_t)len;
+    /* final avalanche */
+    h ^= h >> 16;
+    h *= 0x85ebca6bu;
+    h ^= h >> 13;
+    h *= 0xc2b2ae35u;
+    h ^= h >> 16;
+    return h;
+}
+
+/*
+ * Bit position of hash function j for index i in an m-bit filter.
+ * h_j(i) is the hash of the 4-byte little-endian encoding of i with seed j.
+ * It is mapped to [0, m) by floor(h * m / 2^32) (Lemire's multiply-shift
+ * range reduction), which needs m < 2^32.
+ */
+uint64_t drref_bloom_pos(uint32_t i, uint32_t j, uint64_t m)
+{
+    uint8_t le[4] = {(uint8_t)(i & 0xff), (uint8_t)((i >> 8) & 0xff), (uint8_t)((i >> 16) & 0xff),
+                     (uint8_t)((i >> 24) & 0xff)};
+    uint32_t h = drref_murmur3_32(le, 4, j);
+    return ((uint64_t)h * m) >> 32;
+}
+
+void drref_bloom_pos_many(const uint32_t *idx, uint64_t n, uint32_t j, uint64_t m, uint64_t *out)
+{
+    for (uint64_t q = 0; q < n; ++q)
+        out[q] = drref_bloom_pos(idx[q], j, m);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Bloom filter parameters (Lemma 2 and Remark 2, Section 10.2).             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Remark 2 gives the optimal real-valued size m = -n ln(eps) / (ln 2)^2 and
+ * hash count k = -ln(eps) / ln 2.  Integer reading used here:
+ *   k = max(1, round-half-away(-ln(eps) / ln 2))
+ *   C = -ln(eps) / (ln 2 * ln 2);  m = 32 * ceil(ceil(n * C) / 32), at least 32.
+ * Everything is IEEE double with the C library's log.
+ */
+int drref_bloom_params(uint64_t n, double fpr, uint64_t *m_out, uint32_t *k_out)
+{
+    if (!(fpr > 0.0 && fpr < 1.0) || !m_out || !k_out)
+        return DRREF_EINVAL;
+    double ln2 = log(2.0);
+    double kk = -log(fpr) / ln2;
+    long kr = lround(kk);
+    if (kr < 1)
+        kr = 1;
+    double C = -log(fpr) / (ln2 * ln2);
+    double raw = ceil((double)n * C);
+    uint64_t m = (uint64_t)raw;
+    m = ((m + 31) / 32) * 32;
+    if (m < 32)
+        m = 32;
+    if (m >= ((uint64_t)1 << 32))
+        return DRREF_EINVAL;
+    *m_out = m;
+    *k_out = (uint32_t)kr;
+    return DRREF_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Top-r sparsification (Section 2 "Sparsification"; Section 10.2).         */
+/* ------------------------------------------------------------------------ */
+
+/* Magnitude key: the IEEE bit pattern with the sign cleared.  For non-NaN
+ * floats it orders exactly like |x|, and +0 and -0 both map to 0. */
+static uint32_t mag_key(float x)
+{
+    uint32_t u;
+    memcpy(&u, &x, 4);
+    return u & 0x7fffffffu;
+}
+
+typedef struct {
+    uint32_t key;
+    uint32_t idx;
+} key_idx;
+
+/* key descending, then index ascending: a strict total order */
+static int cmp_key_desc_idx_asc(const void *a, const void *b)
+{
+    const key_idx *x = (const key_idx *)a, *y = (const key_idx *)b;
+    if (x->key != y->key)
+        return x->key > y->key ? -1 : 1;
+    if (x->idx != y->idx)
+        return x->idx < y->idx ? -1 : 1;
+    return 0;
+}
+
+static int cmp_u32_asc(const void *a, const void *b)
+{
+    uint32_t x = *(const uint32_t *)a, y = *(const uint32_t *)b;
+    return (x > y) - (x < y);
+}
+
+static int has_nonfinite(const float *g, uint64_t d)
+{
+    for (uint64_t i = 0; i < d; ++i)
+        if (!isfinite(g[i]))
+            return 1;
+    return 0;
+}
+
+/*
+ * Top-r: S holds the indices of the r entries of largest magnitude.  Ties in
+ * magnitude are broken by smaller index first (the paper does not say).  S is
+ * returned in ascending index order, which is the order the receiver's loop
+ * over [d] visits them (Section 4).  Indices are 0-based.
+ * Non-finite input is rejected.
+ */
+int drref_topr(const float *g, uint64_t d, uint64_t r, uint32_t *S_out)
+{
+    if ((!g && d) || (!S_out && r) || r > d || d >= ((uint64_t)1 << 32))
+        return DRREF_EINVAL;
+    if (has_nonfinite(g, d))
+        return DRREF_EINVAL;
+    if (r == 0)
+        return DRREF_OK;
+    key_idx *a = (key_idx *)malloc(sizeof(key_idx) * d);
+    if (!a)
+        return DRREF_EINVAL;
+    for (uint64_t i = 0; i < d; ++i) {
+        a[i].key = mag_key(g[i]);
+        a[i].idx = (uint32_t)i;
+    }
+    qsort(a, d, sizeof(key_idx), cmp_key_desc_idx_asc);
+    for (uint64_t q = 0; q < r; ++q)
+        S_out[q] = a[q].idx;
+    free(a);
+    qsort(S_out, r, sizeof(uint32_t), cmp_u32_asc);
+    return DRREF_OK;
+}
+
+/*
+ * Inherently sparse input (Section 3; the NCF experiment of Section 6.3):
+ * S is the support {i : g[i] != 0}, ascending.  -0.0 counts as zero.
+ */
+int drref_nonzero(const float *g, uint64_t d, uint32_t *S_out, uint64_t cap, uint64_t *n_out)
+{
+    if ((!g && d) || !n_out || d >= ((uint64_t)1 << 32))
+        return DRREF_EINVAL;
+    if (has_nonfinite(g, d))
+        return DRREF_EINVAL;
+    uint64_t n = 0;
+    for (uint64_t i = 0; i < d; ++i) {
+        if (g[i] != 0.0f) {
+            if (n < cap)
+                S_out[n] = (uint32_t)i;
+            ++n;
+        }
+    }
+    *n_out = n;
+    return n > cap ? DRREF_ECAPACITY : DRREF_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Bloom filter insert and full-range query (Sections 2 and 4).              */
+/* ------------------------------------------------------------------------ */
+
+/* Bit p of the filter lives in 32-bit word p/32 at bit p%32 (LSB first). */
+static int get_bit(const uint32_t *w, uint64_t p) { return (int)((w[p >> 5] >> (p & 31)) & 1u); }
+static void set_bit(uint32_t *w, uint64_t p) { w[p >> 5] |= 1u << (p & 31); }
+
+/* Insert every s in S: set bit h_j(s) for j = 0..k-1 (Section 2). */
+int drref_bloom_encode(const uint32_t *S, uint64_t n, uint64_t m, uint32_t k, uint32_t *words)
+{
+    if ((!S && n) || !words || m < 32 || (m & 31) || m >= ((uint64_t)1 << 32) || k < 1 || k > 32)
+        return DRREF_EINVAL;
+    memset(words, 0, sizeof(uint32_t) * (m / 32));
+    for (uint64_t q = 0; q < n; ++q)
+        for (uint32_t j = 0; j < k; ++j)
+            set_bit(words, drref_bloom_pos(S[q], j, m));
+    return DRREF_OK;
+}
+
+/* Membership: i is reported iff all k of its bits are set (Section 4,
+ * "Implementation on GPUs and CPUs": the k looked-up bits sum to k). */
+static int bloom_member(const uint32_t *words, uint64_t m, uint32_t k, uint32_t i)
+{
+    for (uint32_t j = 0; j < k; ++j)
+        if (!get_bit(words, drref_bloom_pos(i, j, m)))
+            return 0;
+    return 1;
+}
+
+/*
+ * Full-range query, policy P0 (Section 4, "No-error approach"): visit every
+ * i of the gradient's index range in increasing order and collect the
+ * positives, true and false, into P.  P is therefore ascending.
+ */
+int drref_bloom_query(const uint32_t *words, uint64_t m, uint32_t k, uint64_t d, uint32_t *P_out,
+                      uint64_t cap, uint64_t *n_out)
+{
+    if (!words || !n_out || m < 32 || (m & 31) || m >= ((uint64_t)1 << 32) || k < 1 || k > 32 ||
+        d >= ((uint64_t)1 << 32))
+        return DRREF_EINVAL;
+    uint64_t n = 0;
+    for (uint64_t i = 0; i < d; ++i) {
+        if (bloom_member(words, m, k, (uint32_t)i)) {
+            if (n < cap)
+                P_out[n] = (uint32_t)i;
+            ++n;
+        }
+    }
+    *n_out = n;
+    return n > cap ? DRREF_ECAPACITY : DRREF_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Curve fitting of the values (Section 5; Section 5.1 for the reorder map). */
+/* ------------------------------------------------------------------------ */
+
+/* Order-preserving map of a float to u32 (unsigned order == float order,
+ * with -0 just below +0). */
+static uint32_t order_key(float x)
+{
+    uint32_t u;
+    memcpy(&u, &x, 4);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+/*
+ * Descending sort of the values (Section 5: the nonzero values are sorted in
+ * descending order).  Signed order; equal values keep their original order.
+ * perm_out[rank] = original position q of the value with that rank.
+ */
+int drref_sort_desc(const float *V, uint64_t n, uint32_t *perm_out)
+{
+    if ((!V || !perm_out) && n)
+        return DRREF_EINVAL;
+    if (n == 0)
+        return DRREF_OK;
+    key_idx *a = (key_idx *)malloc(sizeof(key_idx) * n);
+    if (!a)
+        return DRREF_EINVAL;
+    for (uint64_t q = 0; q < n; ++q) {
+        a[q].key = order_key(V[q]);
+        a[q].idx = (uint32_t)q;
+    }
+    qsort(a, n, sizeof(key_idx), cmp_key_desc_idx_asc); /* order key descending, q ascending */
+    for (uint64_t q = 0; q < n; ++q)
+        perm_out[q] = a[q].idx;
+    free(a);
+    return DRREF_OK;
+}
+
+/*
+ * Least-squares polynomial of degree D through the points (x_j, y_j)
+ * (Section 5, "Polynomial regression"): minimise sum_j (y_j - sum_p c_p x_j^p)^2.
+ * Normal equations G c = b with G[p][q] = sum_j x_j^(p+q), b[p] = sum_j x_j^p y_j,
+ * accumulated in double in increasing j, solved by Gaussian elimination with
+ * partial pivoting.  coef_out[p] multiplies x^p.
+ */
+#define DRREF_MAX_DEG 7
+int drref_lsq_fit(const double *x, const double *y, uint64_t n, uint32_t D, double *coef_out)
+{
+    if (D > DRREF_MAX_DEG || n < (uint64_t)D + 1 || !x || !y || !coef_out)
+        return DRREF_EINVAL;
+    const int N = (int)D + 1;
+    double powsum[2 * DRREF_MAX_DEG + 1];
+    double rhs[DRREF_MAX_DEG + 1];
+    for (int e = 0; e <= 2 * (int)D; ++e)
+        powsum[e] = 0.0;
+    for (int p = 0; p < N; ++p)
+        rhs[p] = 0.0;
+    for (uint64_t j = 0; j < n; ++j) {
+        double tp = 1.0;
+        for (int e = 0; e <= 2 * (int)D; ++e) {
+            powsum[e] += tp;
+            if (e < N)
+                rhs[e] += tp * y[j];
+            tp *= x[j];
+        }
+    }
+    double A[DRREF_MAX_DEG + 1][DRREF_MAX_DEG + 2];
+    for (int p = 0; p < N; ++p) {
+        for (int q = 0; q < N; ++q)
+            A[p][q] = powsum[p + q];
+        A[p][N] = rhs[p];
+    }
+    for (int col = 0; col < N; ++col) {
+        int piv = col;
+        for (int row = col + 1; row < N; ++row)
+            if (fabs(A[row][col]) > fabs(A[piv][col]))
+                piv = row;
+        if (A[piv][col] == 0.0)
+            return DRREF_EINVAL;
+        if (piv != col)
+            for (int c = 0; c <= N; ++c) {
+                double t = A[col][c];
+                A[col][c] = A[piv][c];
+                A[piv][c] = t;
+            }
+        for (int row = col + 1; row < N; ++row) {
+            double f = A[row][col] / A[col][col];
+            for (int c = col; c <= N; ++c)
+                A[row][c] -= f * A[col][c];
+        }
+    }
+    for (int p = N - 1; p >= 0; --p) {
+        double s = A[p][N];
+        for (int q = p + 1; q < N; ++q)
+            s -= A[p][q] * coef_out[q];
+        coef_out[p] = s / A[p][p];
+    }
+    return DRREF_OK;
+}
+
+/*
+ * Segmentation and degree actually used for n sorted values, requested
+ * degree D and requested segment count S.  Segments hold equal counts of
+ * consecutive sorted values; a segment is never given fewer than D+1 points
+ * (Section 5 stops splitting below n'+1 points):
+ *   S_eff = min(S, max(1, floor(n / (D+1)))),
+ *   D_eff = D if n >= D+1, else n-1 (interpolation through all points).
+ * Segment s covers ranks [floor(s n / S_eff), floor((s+1) n / S_eff)).
+ */
+void drref_fit_shape(uint64_t n, uint32_t D, uint32_t S, uint32_t *S_eff, uint32_t *D_eff)
+{
+    if (n == 0) {
+        *S_eff = 0;
+        *D_eff = 0;
+        return;
+    }
+    uint64_t cap = n / ((uint64_t)D + 1);
+    if (cap < 1)
+        cap = 1;
+    *S_eff = (uint32_t)((uint64_t)S < cap ? (uint64_t)S : cap);
+    *D_eff = n >= (uint64_t)D + 1 ? D : (uint32_t)(n - 1);
+}
+
+static uint64_t seg_lo(uint64_t s, uint64_t n, uint64_t S_eff) { return s * n / S_eff; }
+
+/*
+ * Abscissa of local rank j in a segment of n_s points.  The paper fits the
+ * points (i, C_S(g)[i]) with i the rank (Section 5).  The same least-squares
+ * problem is posed here in the affine image t = (2j - (n_s - 1)) / (n_s - 1)
+ * of the rank, which maps the segment onto [-1, 1] and keeps the normal
+ * equations well conditioned; the fitted curve is the same function of the
+ * rank.  t = 0 for a one-point segment.
+ */
+static double abscissa(uint64_t j, uint64_t n_s)
+{
+    if (n_s <= 1)
+        return 0.0;
+    return (double)(2 * (int64_t)j - (int64_t)(n_s - 1)) / (double)(n_s - 1);
+}
+
+/* Width of one reorder-map entry (Section 5.1): the smallest b >= 1 with
+ * 2^b >= n, i.e. ceil(log2 n) bits per value. */
+uint32_t drref_sigma_bits(uint64_t n)
+{
+    uint32_t b = 1;
+    while (b < 63 && ((uint64_t)1 << b) < n)
+        ++b;
+    return b;
+}
+
+uint64_t drref_sigma_words(uint64_t n)
+{
+    return (n * drref_sigma_bits(n) + 31) / 32;
+}
+
+/*
+ * Value encoder (Section 5 and 5.1).  Sort V descending; split the sorted
+ * curve into equal-count segments; fit each by least squares in double;
+ * store the coefficients as fp32, S_eff rows of stride D+1 with unused
+ * entries zero.  The reorder map sigma[q] = rank of V[q] in the sorted order
+ * (original position -> final position) is packed LSB-first, b bits per
+ * entry, entry q in bits [q b, (q+1) b) of the word stream.
+ * coef64_out (optional) receives the double-precision coefficients.
+ */
+int drref_curvefit_encode(const float *V, uint64_t n, uint32_t D, uint32_t S, float *coef_out,
+                          double *coef64_out, uint32_t *sigma_out, uint32_t *S_eff_out,
+                          uint32_t *D_eff_out, uint32_t *b_out)
+{
+    if ((!V && n) || D > DRREF_MAX_DEG || S < 1 || !coef_out || (!sigma_out && n) || !S_eff_out ||
+        !D_eff_out || !b_out)
+        return DRREF_EINVAL;
+    for (uint64_t q = 0; q < n; ++q)
+        if (!isfinite(V[q]))
+            return DRREF_EINVAL;
+    uint32_t S_eff, D_eff;
+    drref_fit_shape(n, D, S, &S_eff, &D_eff);
+    *S_eff_out = S_eff;
+    *D_eff_out = D_eff;
+    *b_out = drref_sigma_bits(n);
+    for (uint64_t c = 0; c < (uint64_t)S * (D + 1); ++c) {
+        coef_out[c] = 0.0f;
+        if (coef64_out)
+            coef64_out[c] = 0.0;
+    }
+    if (n == 0)
+        return DRREF_OK;
+
+    uint32_t *perm = (uint32_t *)malloc(sizeof(uint32_t) * n);
+    double *xs = (double *)malloc(sizeof(double) * n);
+    double *ys = (double *)malloc(sizeof(double) * n);
+    if (!perm || !xs || !ys) {
+        free(perm);
+        free(xs);
+        free(ys);
+        return DRREF_EINVAL;
+    }
+    int st = drref_sort_desc(V, n, perm);
+    for (uint32_t s = 0; st == DRREF_OK && s < S_eff; ++s) {
+        uint64_t lo = seg_lo(s, n, S_eff), hi = seg_lo(s + 1, n, S_eff);
+        uint64_t ns = hi - lo;
+        for (uint64_t j = 0; j < ns; ++j) {
+            xs[j] = abscissa(j, ns);
+            ys[j] = (double)V[perm[lo + j]];
+        }
+        double c[DRREF_MAX_DEG + 1];
+        st = drref_lsq_fit(xs, ys, ns, D_eff, c);
+        for (uint32_t p = 0; st == DRREF_OK && p <= D_eff; ++p) {
+            coef_out[(uint64_t)s * (D + 1) + p] = (float)c[p];
+            if (coef64_out)
+                coef64_out[(uint64_t)s * (D + 1) + p] = c[p];
+        }
+    }
+    if (st == DRREF_OK) {
+        uint32_t b = *b_out;
+        uint64_t nw = (n * b + 31) / 32;
+        memset(sigma_out, 0, sizeof(uint32_t) * nw);
+        for (uint64_t rank = 0; rank < n; ++rank) {
+            uint64_t q = perm[rank];
+            /* write value `rank` into bits [q b, (q+1) b) */
+            for (uint32_t t = 0; t < b; ++t)
+                if ((rank >> t) & 1u)
+                    set_bit(sigma_out, q * b + t);
+        }
+    }
+    free(perm);
+    free(xs);
+    free(ys);
+    return st;
+}
+
+/* Read entry q of a packed b-bit stream. */
+static uint64_t sigma_get(const uint32_t *sigma, uint64_t q, uint32_t b)
+{
+    uint64_t v = 0;
+    for (uint32_t t = 0; t < b; ++t)
+        v |= (uint64_t)get_bit(sigma, q * b + t) << t;
+    return v;
+}
+
+/*
+ * Value decoder.  For each position q: read its rank from sigma, find the
+ * segment holding that rank and the rank's local index, and evaluate that
+ * segment's polynomial at the abscissa by Horner's rule in double on the
+ * fp32 coefficients; round to fp32.  A rank outside [0, n) is an invalid
+ * payload.
+ */
+int drref_curvefit_decode(const float *coef, const uint32_t *sigma, uint64_t n, uint32_t D, uint32_t S,
+                          float *vals_out)
+{
+    if ((!coef || !sigma || !vals_out) && n)
+        return DRREF_EINVAL;
+    if (D > DRREF_MAX_DEG || S < 1)
+        return DRREF_EINVAL;
+    if (n == 0)
+        return DRREF_OK;
+    uint32_t S_eff, D_eff;
+    drref_fit_shape(n, D, S, &S_eff, &D_eff);
+    uint32_t b = drref_sigma_bits(n);
+    for (uint64_t q = 0; q < n; ++q) {
+        uint64_t rank = sigma_get(sigma, q, b);
+        if (rank >= n)
+            return DRREF_EINVAL;
+        uint32_t s = 0;
+        while (s + 1 < S_eff && seg_lo(s + 1, n, S_eff) <= rank)
+            ++s;
+        uint64_t lo = seg_lo(s, n, S_eff), hi = seg_lo(s + 1, n, S_eff);
+        double t = abscissa(rank - lo, hi - lo);
+        const float *c = coef + (uint64_t)s * (D + 1);
+        double y = (double)c[D_eff];
+        for (int p = (int)D_eff - 1; p >= 0; --p)
+            y = y * t + (double)c[p];
+        vals_out[q] = (float)y;
+    }
+    return DRREF_OK;
+}

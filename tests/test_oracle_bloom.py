@@ -1,0 +1,174 @@
+"""Pins for the oracle's hash family, Bloom parameters, insert and query.
+
+Each test checks the oracle against something other than itself: published
+hash test vectors, the closed forms of Section 10.2 (Lemma 2, Remark 2),
+the no-false-negative property of Section 2, the false-positive rate of
+Lemma 2, the size of P from Lemma 5 (as an expectation), and brute force.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2102_03112_amd import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_murmur3_known_answer_vectors():
+    spec = json.load(open(os.path.join(GOLDEN, "murmur3_x86_32_vectors.json")))
+    for v in spec["vectors"]:
+        assert oracle.murmur3_32(bytes.fromhex(v["hex"]), v["seed"]) == int(v["hash"], 16), v
+
+
+def test_murmur3_smhasher_verification_value():
+    # SMHasher's VerificationTest: hash keys {0}, {0,1}, ..., {0..254} with
+    # seed 256 - len, concatenate the 4-byte little-endian hashes, hash that
+    # with seed 0; the low 32 bits are the verification value.
+    spec = json.load(open(os.path.join(GOLDEN, "murmur3_x86_32_vectors.json")))
+    key = bytes(range(256))
+    hashes = b"".join(
+        oracle.murmur3_32(key[:i], 256 - i).to_bytes(4, "little") for i in range(256)
+    )
+    assert oracle.murmur3_32(hashes, 0) == int(spec["smhasher_verification"], 16)
+
+
+def test_bloom_pos_is_murmur_of_le_index_scaled():
+    # pos_j(i) = floor(h_j(i) * m / 2^32) with h_j the hash of i's 4 LE bytes
+    rng = np.random.default_rng(5)
+    idx = rng.integers(0, 2**32, 64, dtype=np.uint64).astype(np.uint32)
+    for m in (32, 150_784, 3_674_496, 2**32 - 32):
+        for j in (0, 1, 9, 12):
+            got = oracle.bloom_pos(idx, j, m)
+            for i, p in zip(idx.tolist(), got.tolist()):
+                h = oracle.murmur3_32(int(i).to_bytes(4, "little"), j)
+                assert p == (h * m) >> 32
+                assert 0 <= p < m
+
+
+@pytest.mark.parametrize(
+    "n,fpr,m,k",
+    [
+        # sizes of the workloads (top-1% of 1,048,576 / 25,557,032 / each 1/24 share
+        # of 354,823,168 and top-0.1% of 138,357,544)
+        (10_486, 1e-3, 150_784, 10),
+        (255_571, 1e-3, 3_674_496, 10),
+        (138_358, 1e-3, 1_989_280, 10),
+        (147_843, 1e-3, 2_125_632, 10),
+        (0, 1e-3, 32, 10),
+        (1, 1e-4, 32, 13),
+    ],
+)
+def test_bloom_params_closed_form(n, fpr, m, k):
+    got_m, got_k = oracle.bloom_params(n, fpr)
+    assert (got_m, got_k) == (m, k)
+    # Remark 2: m = -n ln(eps) / (ln 2)^2 and k = -ln(eps) / ln 2, rounded
+    exact_m = -n * math.log(fpr) / math.log(2) ** 2
+    assert exact_m <= got_m < max(exact_m, 0) + 33
+    assert got_m % 32 == 0
+    assert abs(got_k - (-math.log(fpr) / math.log(2))) <= 0.5
+
+
+def test_bloom_params_rejects_bad_rate():
+    for bad in (0.0, 1.0, -0.1, float("nan")):
+        with pytest.raises(oracle.OracleError):
+            oracle.bloom_params(100, bad)
+
+
+def _bits_by_numpy(S, m, k):
+    """Independent construction of the filter words: a boolean array of m
+    bits, set at every position, packed LSB-first into little-endian u32."""
+    flags = np.zeros(m, dtype=bool)
+    for j in range(k):
+        flags[oracle.bloom_pos(S, j, m).astype(np.int64)] = True
+    return np.packbits(flags, bitorder="little").view("<u4")
+
+
+def test_bloom_encode_matches_bit_array_construction():
+    S = workloads.random_indices(200_000, 3_000, seed=11)
+    m, k = oracle.bloom_params(S.size, 1e-3)
+    words = oracle.bloom_encode(S, m, k)
+    assert words.dtype == np.uint32 and words.size == m // 32
+    np.testing.assert_array_equal(words, _bits_by_numpy(S, m, k))
+
+
+def test_bloom_encode_order_independent_and_popcount_bound():
+    S = workloads.random_indices(1 << 20, 10_486, seed=12)
+    m, k = oracle.bloom_params(S.size, 1e-3)
+    w1 = oracle.bloom_encode(S, m, k)
+    w2 = oracle.bloom_encode(np.random.default_rng(3).permutation(S), m, k)
+    np.testing.assert_array_equal(w1, w2)
+    pop = int(np.unpackbits(w1.view(np.uint8)).sum())
+    assert pop <= min(m, S.size * k)
+    # fill fraction within 5 sigma of 1 - exp(-k n / m) (Lemma 2's model)
+    p = 1.0 - math.exp(-k * S.size / m)
+    sig = math.sqrt(p * (1 - p) / m)
+    assert abs(pop / m - p) < 5 * sig
+
+
+def test_query_no_false_negatives_and_brute_force():
+    d = 50_000
+    S = workloads.random_indices(d, 500, seed=13)
+    m, k = oracle.bloom_params(S.size, 1e-2)
+    words = oracle.bloom_encode(S, m, k)
+    P = oracle.bloom_query(words, m, k, d)
+    assert np.all(np.diff(P.astype(np.int64)) > 0)  # ascending, no repeats
+    assert np.isin(S, P).all()  # Section 2: no false negatives
+    # brute force over every index with numpy bit tests
+    bits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+    all_i = np.arange(d, dtype=np.uint32)
+    member = np.ones(d, dtype=bool)
+    for j in range(k):
+        member &= bits[oracle.bloom_pos(all_i, j, m).astype(np.int64)]
+    np.testing.assert_array_equal(P, np.flatnonzero(member).astype(np.uint32))
+
+
+def test_query_false_positive_rate_matches_lemma2():
+    # a gradient of 2^20 entries with 1% selected, FPR target 1e-3
+    d = 1 << 20
+    S = workloads.random_indices(d, 10_486, seed=14)
+    m, k = oracle.bloom_params(S.size, 1e-3)
+    words = oracle.bloom_encode(S, m, k)
+    P = oracle.bloom_query(words, m, k, d)
+    fp = P.size - S.size
+    nonmembers = d - S.size
+    rho = np.unpackbits(words.view(np.uint8)).sum() / m
+    # conditional on the fill, each non-member is positive with prob rho^k
+    q = rho**k
+    assert abs(fp - q * nonmembers) < 5 * math.sqrt(nonmembers * q * (1 - q))
+    # Lemma 2's approximation (1 - e^{-kn/m})^k, and the target itself
+    eps = (1 - math.exp(-k * S.size / m)) ** k
+    assert abs(fp / nonmembers - eps) / eps < 0.15
+    assert abs(eps - 1e-3) / 1e-3 < 0.01
+    # Lemma 5: E|P| = r + eps (d - r), an expectation rather than a bound
+    assert abs(P.size - (S.size + eps * nonmembers)) < 5 * math.sqrt(nonmembers * eps)
+
+
+def test_query_capacity_error_reports_count():
+    d = 4096
+    S = workloads.random_indices(d, 100, seed=15)
+    m, k = oracle.bloom_params(S.size, 0.5)
+    words = oracle.bloom_encode(S, m, k)
+    lib = oracle._load()
+    import ctypes
+
+    out = np.zeros(10, dtype=np.uint32)
+    n = ctypes.c_uint64()
+    st = lib.drref_bloom_query(
+        words.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), m, k, d,
+        out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), 10, ctypes.byref(n),
+    )
+    assert st == oracle.ECAPACITY and n.value >= 100
+    np.testing.assert_array_equal(out, oracle.bloom_query(words, m, k, d)[:10])
+
+
+def test_empty_filter_and_full_filter():
+    m, k = 64, 3
+    empty = np.zeros(m // 32, dtype=np.uint32)
+    assert oracle.bloom_query(empty, m, k, 1000).size == 0
+    full = np.full(m // 32, 0xFFFFFFFF, dtype=np.uint32)
+    np.testing.assert_array_equal(oracle.bloom_query(full, m, k, 1000), np.arange(1000, dtype=np.uint32))
+    assert oracle.bloom_encode(np.zeros(0, dtype=np.uint32), m, k).sum() == 0
