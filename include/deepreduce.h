@@ -1,0 +1,217 @@
+/*
+ * deepreduce.h -- C ABI of the MI355X (gfx950) DeepReduce sparse-tensor codec.
+ *
+ * The codec follows Kostopoulou et al., "DeepReduce: A Sparse-tensor
+ * Communication Framework for Distributed Deep Learning" (arXiv 2102.03112):
+ * a gradient is sparsified (top-r, or the support of an inherently sparse
+ * gradient), its index set is compressed with a Bloom filter (Section 4) and
+ * decoded with the no-error policy P0 (Section 4, "No-error approach"), and
+ * its values are compressed by sorting them and fitting a piecewise
+ * least-squares polynomial (Section 5), with a bit-packed reorder map
+ * (Section 5.1).
+ *
+ * Conventions for every call below:
+ *  - Pointers are DEVICE pointers unless the parameter name ends in _h.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream), except the host-only helpers marked so.
+ *    Arguments are validated on the host before anything is launched; an
+ *    invalid argument returns DR_EINVAL and launches nothing.
+ *  - Counts produced by one call and consumed by the next stay in device
+ *    memory (`uint64_t*` device scalars), so calls chain without host syncs.
+ *    A `*_cap` argument is a host upper bound of such a device count; it
+ *    only sizes grids and scratch.  Every item below the device count is
+ *    processed even if the count exceeds the bound, EXCEPT where an output
+ *    capacity is named: entries beyond an output capacity are dropped and
+ *    the full count is still reported, so the caller detects overflow by
+ *    comparing the count with the capacity after synchronising.
+ *  - Indices are 0-based u32 (the paper's [d] is 1-based, Section 2), so a
+ *    gradient tensor holds fewer than 2^32 elements.
+ *  - The caller owns all memory.  Scratch comes from `ws`, at least
+ *    dr_workspace_bytes() bytes, device memory aligned to 256 bytes; its
+ *    contents are undefined between calls and it must not be shared by calls
+ *    that run concurrently.  The library keeps no state between calls.
+ *  - Non-finite gradient values are outside the codec's contract: the
+ *    results are then unspecified but every kernel still terminates, and the
+ *    round trip reports them in its flags word (DR_FLAG_NONFINITE).
+ *  - Hash family: MurmurHash3_x86_32 of the 4-byte little-endian index with
+ *    seeds 0..k-1; bit position floor(h * m / 2^32); bit p of the filter is
+ *    bit (p mod 32) of 32-bit word p / 32.
+ */
+#ifndef DEEPREDUCE_H
+#define DEEPREDUCE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define DR_EXPORT __attribute__((visibility("default")))
+#else
+#define DR_EXPORT
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DR_OK = 0,
+    DR_EINVAL = -1,    /* invalid argument; nothing was launched */
+    DR_ECAPACITY = -2, /* a capacity given on the host is too small */
+    DR_EDEVICE = -3,   /* a HIP runtime call failed; see dr_last_error() */
+    DR_ENOTSUP = -4    /* a requested option is not implemented */
+} dr_status;
+
+/* r sentinel: select every element that is not +-0 (an inherently sparse
+ * gradient, Section 3 and the NCF experiment of Section 6.3). */
+#define DR_R_NONZERO UINT64_MAX
+
+#define DR_MAX_DEGREE 7      /* highest polynomial degree per segment */
+#define DR_MAX_SEGMENTS 4096 /* most segments per tensor */
+#define DR_MAX_TENSORS 65536 /* most tensors in one round trip */
+
+/* Round-trip flags word bits (dr_roundtrip / dr_payload_encode counts). */
+#define DR_FLAG_NONFINITE 1u /* the tensor held NaN or Inf */
+
+/* ---------------------------------------------------------------------- */
+/* Host-only helpers                                                       */
+/* ---------------------------------------------------------------------- */
+
+/* Bloom filter size and hash count for n_items and a target false-positive
+ * rate fpr in (0, 1), from Remark 2 of Section 10.2 (m = -n ln(fpr)/(ln 2)^2,
+ * k = -ln(fpr)/ln 2), rounded as: k = max(1, round(-ln fpr / ln 2));
+ * m = 32 * ceil(ceil(n * C) / 32) with C = -ln(fpr) / (ln 2 * ln 2), at least
+ * 32.  Returns DR_EINVAL for fpr outside (0, 1) or m >= 2^32. */
+DR_EXPORT dr_status dr_bloom_params(uint64_t n_items, double fpr, uint64_t *m_bits_h, uint32_t *k_h);
+
+/* Bits per reorder-map entry for n values (Section 5.1): the smallest
+ * b >= 1 with 2^b >= n. */
+DR_EXPORT uint32_t dr_sigma_bits(uint64_t n);
+
+/* Scratch bytes sufficient for any call of this library on a gradient of at
+ * most d elements split into at most n_tensors tensors. */
+DR_EXPORT size_t dr_workspace_bytes(uint64_t d, uint64_t n_tensors);
+
+/* Message of the last failure on the calling host thread ("" if none). */
+DR_EXPORT const char *dr_last_error(void);
+
+/* ---------------------------------------------------------------------- */
+/* Sparsification (Section 2 "Sparsification"; Section 10.2)               */
+/* ---------------------------------------------------------------------- */
+
+/* Top-r: the indices of the r entries of g[0..d) of largest magnitude, ties
+ * broken by smaller index, written in ascending index order to idx_out
+ * (capacity r); val_out (nullable, capacity r) receives g at those indices;
+ * *n_out (device) receives r.  With r == DR_R_NONZERO, every entry that is
+ * not +-0 is selected instead, idx_out and val_out need capacity d, and
+ * *n_out receives their number.  EINVAL: d >= 2^32, r > d, null pointers,
+ * workspace too small. */
+DR_EXPORT dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx_out, float *val_out,
+                           uint64_t *n_out, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------- */
+/* Bloom-filter index compression (Sections 2 and 4)                       */
+/* ---------------------------------------------------------------------- */
+
+/* Insert the *n (device count, at most n_cap in the usual case) indices
+ * idx[0..*n) into an m_bits-bit filter with k hash functions: set bit
+ * h_j(x) for every x and j < k.  bits_out receives all m_bits/32 words (the
+ * callee clears them first).  m_bits must be a positive multiple of 32 below
+ * 2^32; 1 <= k <= 32.  Indices must be below 2^32. */
+DR_EXPORT dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap, uint64_t m_bits, uint32_t k,
+                          uint32_t *bits_out, void *ws, size_t ws_bytes, void *stream);
+
+/* Full-range query of policy P0 (Section 4): every i in [0, d) whose k bits
+ * are all set in `bits`, written in ascending order to idx_out (at most cap
+ * entries; the full count goes to *n_out, device).  True and false
+ * positives are both reported; a filter never yields a false negative. */
+DR_EXPORT dr_status dr_bloom_decode(const uint32_t *bits, uint64_t m_bits, uint32_t k, uint64_t d, uint32_t *idx_out,
+                          uint64_t cap, uint64_t *n_out, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------- */
+/* Curve-fitting value compression (Section 5; reorder map Section 5.1)    */
+/* ---------------------------------------------------------------------- */
+
+/* Compress vals[0..*n) (device count, n_cap its host bound): sort the values
+ * in descending order (signed; +0 before -0; equal values keep their
+ * order), split the sorted sequence into S_eff = min(n_seg, max(1,
+ * floor(n/(degree+1)))) runs of equal count (run s holds sorted ranks
+ * [floor(s n / S_eff), floor((s+1) n / S_eff))), and fit each run by least
+ * squares with a polynomial of degree D_eff = degree (or n-1 if n < degree+1)
+ * in t = (2j - (n_s - 1)) / (n_s - 1) for local rank j of n_s points (t = 0
+ * when n_s = 1), solved in double precision.
+ * coef_out (n_seg*(degree+1) floats) receives run s's coefficient of t^p at
+ * [s*(degree+1) + p] rounded to fp32, zeros elsewhere.
+ * sigma_out receives the reorder map sigma[q] = sorted rank of vals[q] in
+ * b = dr_sigma_bits(n) bits per entry, entry q at bits [q b, (q+1) b) of the
+ * LSB-first 32-bit word stream; capacity ceil(n_cap * dr_sigma_bits(n_cap)
+ * / 32) words.  EINVAL: degree > DR_MAX_DEGREE, n_seg == 0 or
+ * > DR_MAX_SEGMENTS, n_cap >= 2^32. */
+DR_EXPORT dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_cap, uint32_t degree, uint32_t n_seg,
+                             float *coef_out, uint32_t *sigma_out, void *ws, size_t ws_bytes, void *stream);
+
+/* Reconstruct *n values from coef and sigma as written by
+ * dr_curvefit_encode: value q is run s's polynomial, evaluated by Horner's
+ * rule in double at the abscissa of rank sigma[q], rounded to fp32. */
+DR_EXPORT dr_status dr_curvefit_decode(const float *coef, const uint32_t *sigma, const uint64_t *n, uint64_t n_cap,
+                             uint32_t degree, uint32_t n_seg, float *vals_out, void *ws, size_t ws_bytes,
+                             void *stream);
+
+/* ---------------------------------------------------------------------- */
+/* The whole codec over a gradient split into tensors (Figure 3)           */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+    uint64_t n_tensors;        /* >= 1, at most DR_MAX_TENSORS */
+    const uint64_t *offsets_h; /* host, n_tensors+1 nondecreasing offsets, [0] = 0; tensor t is
+                                  g[offsets_h[t] .. offsets_h[t+1]), fewer than 2^32 elements */
+    uint64_t ratio_num;        /* top-r: r_t = ceil(d_t * ratio_num / ratio_den) <= d_t;         */
+    uint64_t ratio_den;        /*   ratio_num == DR_R_NONZERO selects every nonzero instead      */
+    double fpr;                /* Bloom target false-positive rate, in (0, 1)                    */
+    uint32_t degree;           /* polynomial degree per run, <= DR_MAX_DEGREE                    */
+    uint32_t n_seg;            /* runs per tensor, 1 .. DR_MAX_SEGMENTS                          */
+} dr_config;
+
+/* Payload container (Figure 3's "container"): one record per tensor at byte
+ * offset rec_off_h[t] (multiples of 256) of the payload buffer.  A record is
+ * a 64-byte header followed by the filter words, the fp32 coefficients of
+ * the S_eff x (D_eff+1) fitted polynomials, and the packed reorder map, each
+ * section padded to 4 bytes and packed back to back.  Header layout
+ * (little-endian): u32 magic 0x31435244 ("DRC1"), u32 header bytes (64),
+ * u64 d, u64 n_selected, u64 n_values (= |P|), u64 m_bits, u32 k,
+ * u32 hash id (1 = MurmurHash3_x86_32), u32 D_eff, u32 S_eff,
+ * u32 sigma bits, u32 record bytes (header + sections; what would be sent).
+ * Returns the total payload capacity in bytes; fills rec_off_h (nullable,
+ * n_tensors+1 entries) with the record offsets and the end.  Returns 0 for
+ * an invalid configuration. */
+DR_EXPORT size_t dr_payload_layout(const dr_config *cfg_h, uint64_t *rec_off_h);
+
+/* Sender side over the whole gradient g: per tensor, select (top-r or
+ * support), insert into a Bloom filter sized by dr_bloom_params, run the
+ * full-range P0 query, take V = g[P] from the dense gradient (Section 4),
+ * sort and fit V, and write the record into `payload` (capacity
+ * payload_bytes, at least dr_payload_layout()).  counts_out (device,
+ * nullable) receives 4 u64 per tensor: n_selected, |P|, 0, flags. */
+DR_EXPORT dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
+                            uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream);
+
+/* Receiver side: from the payload alone, recover P by the full-range query
+ * of each tensor's filter, evaluate the fitted values at the ranks the
+ * reorder map gives, and write the dense gradient dense_out (d floats, zero
+ * off P).  idx_out / val_out (nullable, d entries) receive tensor t's
+ * positives (local indices) and their values at [offsets_h[t], offsets_h[t]
+ * + |P_t|).  counts_out (nullable): slot 2 of each tensor receives the
+ * receiver's |P|; slot 3 gains bit 2 if it disagrees with the header. */
+DR_EXPORT dr_status dr_payload_decode(const uint8_t *payload, const dr_config *cfg_h, float *dense_out, uint32_t *idx_out,
+                            float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream);
+
+/* dr_payload_encode followed by dr_payload_decode on one stream: one codec
+ * round trip of the whole gradient. */
+DR_EXPORT dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
+                       float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
+                       size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DEEPREDUCE_H */

@@ -1,0 +1,604 @@
+// api.hip -- the C ABI (include/deepreduce.h): argument checks, the
+// per-tensor plan, the workspace carve, and the launch sequence of each
+// entry point.  Everything here runs on the host; all arithmetic of the
+// codec runs in the kernels.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/deepreduce.h"
+#include "launch.hpp"
+
+using namespace dr;
+
+namespace {
+
+thread_local std::string g_err;
+
+dr_status fail(dr_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+dr_status hip_fail(hipError_t e, const char *where) {
+    return fail(DR_EDEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define DR_HIP(call)                                       \
+    do {                                                   \
+        hipError_t e_ = (call);                            \
+        if (e_ != hipSuccess) return hip_fail(e_, #call);  \
+    } while (0)
+
+constexpr uint32_t MAX_SLICES = 16384;  // 2^30-bit filters: LDS counters of the insert
+constexpr uint32_t POS_PER_ELEM = 12;   // Bloom positions the workspace holds per padded element
+
+uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+uint64_t align_up(uint64_t a, uint64_t b) { return ceil_div(a, b) * b; }
+
+// Remark 2 of Section 10.2, rounded (see deepreduce.h)
+bool bloom_params_host(uint64_t n, double fpr, uint64_t *m, uint32_t *k) {
+    if (!(fpr > 0.0 && fpr < 1.0)) return false;
+    const double ln2 = log(2.0);
+    long kr = lround(-log(fpr) / ln2);
+    if (kr < 1) kr = 1;
+    const double C = -log(fpr) / (ln2 * ln2);
+    uint64_t mm = (uint64_t)ceil((double)n * C);
+    mm = align_up(mm, 32);
+    if (mm < 32) mm = 32;
+    if (mm >= (1ull << 32) || kr > 32) return false;
+    *m = mm;
+    *k = (uint32_t)kr;
+    return true;
+}
+
+uint32_t sigma_bits_host(uint64_t n) {
+    uint32_t b = 1;
+    while (b < 63 && (1ull << b) < n) ++b;
+    return b;
+}
+
+int persist_grid(int per_cu) {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            cus = v;
+        else
+            cus = 256;
+    }
+    return cus * per_cu;
+}
+
+// Workspace regions, in carve order.  Element-sized regions have `slots`
+// entries (padded elements); the last six are contiguous so the Bloom insert
+// can borrow them for its position buffer before the value path needs them.
+struct Carve {
+    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0;
+    size_t bytes = 0;
+    size_t o_td, o_glob, o_tickets, o_done, o_lb, o_hpart, o_hist, o_sel, o_ckey, o_cidx, o_S, o_P, o_V, o_shist,
+        o_fit, o_btab, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
+
+    void plan() {
+        size_t at = 0;
+        auto take = [&](size_t sz) {
+            size_t r = at;
+            at = align_up(at + sz, 256);
+            return r;
+        };
+        o_td = take(sizeof(TDesc) * ntensors);
+        o_glob = take(sizeof(Glob));
+        o_tickets = take(64);
+        o_done = take(4 * ntensors);
+        o_lb = take(4 * 8 * ntiles);
+        o_hpart = take(4ull * HIST1_BINS * hist_blocks);
+        o_hist = take(4ull * HIST1_BINS * ntensors);
+        o_sel = take(slots / 8);
+        o_ckey = take(4 * slots);
+        o_cidx = take(4 * slots);
+        o_S = take(4 * slots);
+        o_P = take(4 * slots);
+        o_V = take(4 * slots);
+        o_shist = take(4ull * SORT_BINS * ntiles);
+        o_fit = take(8ull * NMOM * fit_blocks);
+        o_btab = take(4 * btab);
+        o_keyA = take(4 * slots);
+        o_keyB = take(4 * slots);
+        o_valA = take(4 * slots);
+        o_valB = take(4 * slots);
+        o_sig = take(4 * slots);
+        o_vs = take(4 * slots);
+        bytes = at;
+    }
+
+    Work view(uint8_t *ws) const {
+        Work w{};
+        w.td = (TDesc *)(ws + o_td);
+        w.glob = (Glob *)(ws + o_glob);
+        w.ntensors = (uint32_t)ntensors;
+        w.ntiles_total = (uint32_t)ntiles;
+        w.slots = slots;
+        w.tickets = (uint32_t *)(ws + o_tickets);
+        w.done = (uint32_t *)(ws + o_done);
+        unsigned long long *lb = (unsigned long long *)(ws + o_lb);
+        w.lb0 = lb;
+        w.lb1 = lb + ntiles;
+        w.lb2 = lb + 2 * ntiles;
+        w.lb3 = lb + 3 * ntiles;
+        w.hist_part = (uint32_t *)(ws + o_hpart);
+        w.hist = (uint32_t *)(ws + o_hist);
+        w.selbits = (uint32_t *)(ws + o_sel);
+        w.cand_key = (uint32_t *)(ws + o_ckey);
+        w.cand_idx = (uint32_t *)(ws + o_cidx);
+        w.S = (uint32_t *)(ws + o_S);
+        w.P = (uint32_t *)(ws + o_P);
+        w.V = (float *)(ws + o_V);
+        w.shist = (uint32_t *)(ws + o_shist);
+        w.fit_part = (double *)(ws + o_fit);
+        w.btab = (uint32_t *)(ws + o_btab);
+        w.keyA = (uint32_t *)(ws + o_keyA);
+        w.keyB = (uint32_t *)(ws + o_keyB);
+        w.valA = (uint32_t *)(ws + o_valA);
+        w.valB = (uint32_t *)(ws + o_valB);
+        w.sig = (uint32_t *)(ws + o_sig);
+        w.vsorted = (float *)(ws + o_vs);
+        w.bpos = (uint16_t *)(ws + o_keyA);  // borrows keyA .. vsorted
+        return w;
+    }
+
+    uint64_t pos_capacity() const { return (o_vs + 4 * slots - o_keyA) / 2; }
+};
+
+// Generic bound used by dr_workspace_bytes: one fit block per element at most.
+Carve bound_carve(uint64_t d, uint64_t n_tensors) {
+    Carve c;
+    c.ntensors = n_tensors;
+    c.ntiles = ceil_div(d, TILE) + n_tensors;
+    c.slots = c.ntiles * TILE;
+    c.hist_blocks = c.ntiles / 8 + 2 * n_tensors;
+    const uint64_t runs = n_tensors * (uint64_t)DR_MAX_SEGMENTS;
+    c.fit_blocks = (runs < d + n_tensors ? runs : d + n_tensors) * FIT_CHUNKS;
+    // Bloom table: per tensor (slices x chunks) with chunks <= 257 and
+    // m <= 2 k n <= 2 POS_PER_ELEM slots bits; plus one filter of MAX_SLICES
+    // for a standalone insert whose filter is larger than its item count
+    c.btab = (2 * c.slots * POS_PER_ELEM / SLICE_BITS + 2 * n_tensors) * 257 + 257ull * MAX_SLICES;
+    c.plan();
+    return c;
+}
+
+struct Plan {
+    std::vector<TInit> t;
+    std::vector<uint64_t> bl_ncap;  // Bloom items reserved per tensor
+    Carve carve;
+    uint32_t bl_chunks = 0, bl_slices = 0, max_slices = 0, hash_per_round = 1, kmax = 0;
+    uint64_t bl_items = 0;
+    bool any_topr = false;
+};
+
+// Per-tensor Bloom insert layout for at most n_cap items and m_cap_bits.
+void plan_bloom(TInit &in, uint64_t n_cap, uint64_t m_cap_bits, Plan &p) {
+    p.bl_ncap.push_back(n_cap);
+    const uint64_t chunk = n_cap / 256 > 1024 ? ceil_div(n_cap, 256) : 1024;
+    in.bl_chunk = (uint32_t)chunk;
+    in.bl_nchunks = (uint32_t)(n_cap ? ceil_div(n_cap, chunk) : 0);
+    in.bl_nslices = (uint32_t)ceil_div(m_cap_bits, SLICE_BITS);
+    in.bl_chunk0 = p.bl_chunks;
+    in.bl_slice0 = p.bl_slices;
+    in.bl_tab0 = p.carve.btab;
+    p.bl_chunks += in.bl_nchunks;
+    p.bl_slices += in.bl_nslices;
+    p.carve.btab += (uint64_t)in.bl_nchunks * in.bl_nslices;
+    p.bl_items += n_cap;
+    if (in.bl_nslices > p.max_slices) p.max_slices = in.bl_nslices;
+}
+
+// After the carve: how many hash functions one insert round can bucket (the
+// position buffer holds n_cap positions per hash per tensor), and each
+// tensor's place in that buffer.
+void plan_bloom_rounds(Plan &p, uint32_t k) {
+    p.kmax = k;
+    const uint64_t cap = p.carve.pos_capacity();
+    uint64_t h = p.bl_items ? cap / p.bl_items : k;
+    if (h < 1) h = 1;
+    if (h > k) h = k;
+    p.hash_per_round = (uint32_t)h;
+    uint64_t at = 0;
+    for (size_t i = 0; i < p.t.size(); ++i) {
+        p.t[i].bl_pos0 = at;
+        at += p.bl_ncap[i] * h;
+    }
+}
+
+dr_status check_cfg(const dr_config *cfg) {
+    if (!cfg) return fail(DR_EINVAL, "cfg is null");
+    if (cfg->n_tensors < 1 || cfg->n_tensors > DR_MAX_TENSORS) return fail(DR_EINVAL, "n_tensors out of range");
+    if (!cfg->offsets_h) return fail(DR_EINVAL, "offsets_h is null");
+    if (cfg->offsets_h[0] != 0) return fail(DR_EINVAL, "offsets_h[0] must be 0");
+    for (uint64_t t = 0; t < cfg->n_tensors; ++t) {
+        if (cfg->offsets_h[t + 1] < cfg->offsets_h[t]) return fail(DR_EINVAL, "offsets_h must be nondecreasing");
+        if (cfg->offsets_h[t + 1] - cfg->offsets_h[t] >= (1ull << 32))
+            return fail(DR_EINVAL, "tensor %llu has 2^32 or more elements", (unsigned long long)t);
+    }
+    if (cfg->ratio_num != DR_R_NONZERO) {
+        if (cfg->ratio_den == 0 || cfg->ratio_den >= (1ull << 32) || cfg->ratio_num > cfg->ratio_den)
+            return fail(DR_EINVAL, "ratio must satisfy 0 <= num <= den < 2^32");
+    }
+    if (!(cfg->fpr > 0.0 && cfg->fpr < 1.0)) return fail(DR_EINVAL, "fpr must be in (0, 1)");
+    if (cfg->degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
+    if (cfg->n_seg < 1 || cfg->n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
+    return DR_OK;
+}
+
+uint64_t record_capacity(uint64_t d, uint64_t n_cap, double fpr, uint32_t degree, uint32_t nseg) {
+    uint64_t m = 0;
+    uint32_t k = 0;
+    bloom_params_host(n_cap, fpr, &m, &k);
+    const uint64_t sig_words = ceil_div(d * sigma_bits_host(d ? d : 1), 32);
+    return HDR_BYTES + m / 8 + 4ull * nseg * (degree + 1) + 4 * sig_words;
+}
+
+// The per-tensor plan of a round trip (sender and receiver use the same one).
+dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_off) {
+    dr_status st = check_cfg(cfg);
+    if (st != DR_OK) return st;
+    const uint64_t T = cfg->n_tensors;
+    const bool nz = cfg->ratio_num == DR_R_NONZERO;
+    const double ln2 = log(2.0);
+    const double mC = -log(cfg->fpr) / (ln2 * ln2);
+    uint64_t m_any = 0;
+    uint32_t k = 0;
+    if (!bloom_params_host(1, cfg->fpr, &m_any, &k)) return fail(DR_EINVAL, "fpr gives more than 32 hashes");
+    p.t.resize(T);
+    rec_off.assign(T + 1, 0);
+    uint64_t tiles = 0, hist_blocks = 0, fit_blocks = 0;
+    p.carve = Carve();
+    for (uint64_t t = 0; t < T; ++t) {
+        TInit &in = p.t[t];
+        memset(&in, 0, sizeof in);
+        const uint64_t d = cfg->offsets_h[t + 1] - cfg->offsets_h[t];
+        const uint64_t r = nz ? 0 : ceil_div(d * cfg->ratio_num, cfg->ratio_den);
+        const uint64_t n_cap = nz ? d : r;
+        uint64_t m_cap = 0;
+        uint32_t kk = 0;
+        if (!bloom_params_host(n_cap, cfg->fpr, &m_cap, &kk))
+            return fail(DR_ENOTSUP, "tensor %llu: filter of %llu items needs 2^32 bits or more",
+                        (unsigned long long)t, (unsigned long long)n_cap);
+        if (ceil_div(m_cap, SLICE_BITS) > MAX_SLICES)
+            return fail(DR_ENOTSUP, "tensor %llu: filter larger than 2^30 bits", (unsigned long long)t);
+        in.off = cfg->offsets_h[t];
+        in.d = (uint32_t)d;
+        in.r = nz ? R_NONZERO : (uint32_t)r;
+        in.ntiles = (uint32_t)(d ? ceil_div(d, TILE) : 1);
+        in.tile0 = (uint32_t)tiles;
+        in.slot = tiles * TILE;
+        tiles += in.ntiles;
+        in.k = kk;
+        in.degree = cfg->degree;
+        in.nseg = cfg->n_seg;
+        in.m_words_in = 0;
+        in.mC = mC;
+        const uint64_t runs_cap = std::min<uint64_t>(cfg->n_seg, std::max<uint64_t>(1, d / (cfg->degree + 1)));
+        in.fit_blk0 = (uint32_t)fit_blocks;
+        fit_blocks += runs_cap * FIT_CHUNKS;
+        if (!nz) {
+            const uint64_t ht = std::max<uint64_t>(8, ceil_div(in.ntiles, 512));
+            in.hb0 = (uint32_t)hist_blocks;
+            in.hbn = (uint32_t)ceil_div(in.ntiles, ht);
+            hist_blocks += in.hbn;
+        } else {
+            in.hb0 = (uint32_t)hist_blocks;
+            in.hbn = 0;
+        }
+        plan_bloom(in, n_cap, m_cap, p);
+        rec_off[t + 1] = rec_off[t] + align_up(record_capacity(d, n_cap, cfg->fpr, cfg->degree, cfg->n_seg), 256);
+    }
+    p.any_topr = !nz;
+    p.carve.ntensors = T;
+    p.carve.ntiles = tiles;
+    p.carve.slots = tiles * TILE;
+    p.carve.hist_blocks = hist_blocks;
+    p.carve.fit_blocks = fit_blocks;
+    p.carve.plan();
+    plan_bloom_rounds(p, k);
+    return DR_OK;
+}
+
+hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s) {
+    for (size_t f = 0; f < t.size(); f += INIT_CHUNK) {
+        InitArgs a;
+        memset(&a, 0, sizeof a);
+        a.first = (uint32_t)f;
+        a.count = (uint32_t)std::min<size_t>(INIT_CHUNK, t.size() - f);
+        for (uint32_t i = 0; i < a.count; ++i) a.t[i] = t[f + i];
+        hipError_t e = launch_init(w, a, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t run_zero_state(const Work &w, hipStream_t s) {
+    ZeroArgs z;
+    memset(&z, 0, sizeof z);
+    z.z[0] = {w.tickets, 16};
+    z.z[1] = {w.done, w.ntensors};
+    z.z[2] = {w.lb0, 4ull * 2 * w.ntiles_total};
+    z.z[3] = {w.glob, sizeof(Glob) / 4};
+    z.n = 4;
+    return launch_zero(z, s);
+}
+
+bool ws_ok(void *ws, size_t ws_bytes, size_t need) {
+    return ws && ws_bytes >= need && ((uintptr_t)ws & 255u) == 0;
+}
+
+dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
+                      uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+    Plan p;
+    std::vector<uint64_t> rec_off;
+    dr_status st = plan_config(cfg, p, rec_off);
+    if (st != DR_OK) return st;
+    if (!g && cfg->offsets_h[cfg->n_tensors] > 0) return fail(DR_EINVAL, "g is null");
+    if (!payload || payload_bytes < rec_off.back()) return fail(DR_EINVAL, "payload buffer too small");
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    for (size_t t = 0; t < p.t.size(); ++t) {
+        p.t[t].rec_off = rec_off[t];
+        p.t[t].rec_cap = rec_off[t + 1] - rec_off[t];
+        p.t[t].rec = payload + rec_off[t];
+        p.t[t].bits = (uint32_t *)(payload + rec_off[t] + HDR_BYTES);
+        p.t[t].coef = nullptr;
+        p.t[t].sigma = nullptr;
+    }
+    const Work w = p.carve.view((uint8_t *)ws);
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(run_zero_state(w, s));
+    if (p.any_topr)
+        DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
+    else
+        DR_HIP(launch_nonzero(w, g, persist_grid(8), s));
+    DR_HIP(launch_compact_selection(w, g, nullptr, persist_grid(8), s));
+    DR_HIP(launch_params(w, s));
+    DR_HIP(launch_bloom_insert(w, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
+    DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
+    DR_HIP(launch_value_setup(w, true, s));
+    DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, persist_grid(4), s));
+    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
+    DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
+    if (counts_out) DR_HIP(launch_counts(w, counts_out, 0, s));
+    return DR_OK;
+}
+
+dr_status decode_impl(const uint8_t *payload, const dr_config *cfg, float *dense_out, uint32_t *idx_out,
+                      float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+    Plan p;
+    std::vector<uint64_t> rec_off;
+    dr_status st = plan_config(cfg, p, rec_off);
+    if (st != DR_OK) return st;
+    if (!payload) return fail(DR_EINVAL, "payload is null");
+    if (!dense_out && cfg->offsets_h[cfg->n_tensors] > 0) return fail(DR_EINVAL, "dense_out is null");
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    for (size_t t = 0; t < p.t.size(); ++t) {
+        p.t[t].rec_off = rec_off[t];
+        p.t[t].rec_cap = rec_off[t + 1] - rec_off[t];
+        p.t[t].rec = const_cast<uint8_t *>(payload) + rec_off[t];
+        p.t[t].bits = nullptr;
+    }
+    const Work w = p.carve.view((uint8_t *)ws);
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(run_zero_state(w, s));
+    DR_HIP(launch_query_decode(w, payload, dense_out, idx_out, val_out, persist_grid(4), s));
+    if (counts_out) DR_HIP(launch_counts(w, counts_out, 1, s));
+    return DR_OK;
+}
+
+// A single-tensor plan for the standalone calls.
+Plan single_plan(uint64_t d) {
+    Plan p;
+    p.t.resize(1);
+    TInit &in = p.t[0];
+    memset(&in, 0, sizeof in);
+    in.d = (uint32_t)d;
+    in.ntiles = (uint32_t)(d ? ceil_div(d, TILE) : 1);
+    in.tile0 = 0;
+    in.slot = 0;
+    p.carve.ntensors = 1;
+    p.carve.ntiles = in.ntiles;
+    p.carve.slots = (uint64_t)in.ntiles * TILE;
+    return p;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char *dr_last_error(void) { return g_err.c_str(); }
+
+dr_status dr_bloom_params(uint64_t n_items, double fpr, uint64_t *m_bits_h, uint32_t *k_h) {
+    if (!m_bits_h || !k_h) return fail(DR_EINVAL, "null output pointer");
+    if (!bloom_params_host(n_items, fpr, m_bits_h, k_h)) return fail(DR_EINVAL, "fpr outside (0, 1) or m >= 2^32");
+    return DR_OK;
+}
+
+uint32_t dr_sigma_bits(uint64_t n) { return sigma_bits_host(n); }
+
+size_t dr_workspace_bytes(uint64_t d, uint64_t n_tensors) {
+    if (n_tensors < 1) n_tensors = 1;
+    return bound_carve(d, n_tensors).bytes;
+}
+
+size_t dr_payload_layout(const dr_config *cfg_h, uint64_t *rec_off_h) {
+    Plan p;
+    std::vector<uint64_t> rec_off;
+    if (plan_config(cfg_h, p, rec_off) != DR_OK) return 0;
+    if (rec_off_h)
+        for (size_t i = 0; i < rec_off.size(); ++i) rec_off_h[i] = rec_off[i];
+    return rec_off.back();
+}
+
+dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
+                            uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream) {
+    return encode_impl(g, cfg_h, payload, payload_bytes, counts_out, ws, ws_bytes, (hipStream_t)stream);
+}
+
+dr_status dr_payload_decode(const uint8_t *payload, const dr_config *cfg_h, float *dense_out, uint32_t *idx_out,
+                            float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream) {
+    return decode_impl(payload, cfg_h, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, (hipStream_t)stream);
+}
+
+dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
+                       float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
+                       size_t ws_bytes, void *stream) {
+    dr_status st = encode_impl(g, cfg_h, payload, payload_bytes, counts_out, ws, ws_bytes, (hipStream_t)stream);
+    if (st != DR_OK) return st;
+    return decode_impl(payload, cfg_h, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, (hipStream_t)stream);
+}
+
+dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx_out, float *val_out,
+                           uint64_t *n_out, void *ws, size_t ws_bytes, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (d >= (1ull << 32)) return fail(DR_EINVAL, "d >= 2^32");
+    const bool nz = r == DR_R_NONZERO;
+    if (!nz && r > d) return fail(DR_EINVAL, "r > d");
+    if ((!g && d) || !n_out || (!idx_out && (nz ? d : r) > 0)) return fail(DR_EINVAL, "null pointer");
+    Plan p = single_plan(d);
+    TInit &in = p.t[0];
+    in.r = nz ? R_NONZERO : (uint32_t)r;
+    if (!nz) {
+        const uint64_t ht = std::max<uint64_t>(8, ceil_div(in.ntiles, 512));
+        in.hb0 = 0;
+        in.hbn = (uint32_t)ceil_div(in.ntiles, ht);
+        p.carve.hist_blocks = in.hbn;
+    }
+    p.carve.plan();
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    Work w = p.carve.view((uint8_t *)ws);
+    w.S = idx_out;  // single tensor: slot 0 is the caller's list
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(run_zero_state(w, s));
+    if (!nz)
+        DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
+    else
+        DR_HIP(launch_nonzero(w, g, persist_grid(8), s));
+    DR_HIP(launch_compact_selection(w, g, val_out, persist_grid(8), s));
+    DR_HIP(launch_export_n(w, n_out, 0, s));
+    return DR_OK;
+}
+
+dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap, uint64_t m_bits, uint32_t k,
+                          uint32_t *bits_out, void *ws, size_t ws_bytes, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (!n || !bits_out || (!idx && n_cap)) return fail(DR_EINVAL, "null pointer");
+    if (m_bits < 32 || (m_bits & 31) || m_bits >= (1ull << 32)) return fail(DR_EINVAL, "bad m_bits");
+    if (k < 1 || k > 32) return fail(DR_EINVAL, "k must be in [1, 32]");
+    if (n_cap >= (1ull << 32)) return fail(DR_EINVAL, "n_cap >= 2^32");
+    if (ceil_div(m_bits, SLICE_BITS) > MAX_SLICES) return fail(DR_ENOTSUP, "filter larger than 2^30 bits");
+    Plan p = single_plan(n_cap);
+    TInit &in = p.t[0];
+    in.k = k;
+    in.m_words_in = (uint32_t)(m_bits / 32);
+    in.bits = bits_out;
+    plan_bloom(in, n_cap, m_bits, p);
+    p.carve.plan();
+    plan_bloom_rounds(p, k);
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    Work w = p.carve.view((uint8_t *)ws);
+    w.S = const_cast<uint32_t *>(idx);
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(run_zero_state(w, s));
+    DR_HIP(launch_import_n(w, n, n_cap, s));
+    DR_HIP(launch_params(w, s));
+    DR_HIP(launch_bloom_insert(w, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
+    return DR_OK;
+}
+
+dr_status dr_bloom_decode(const uint32_t *bits, uint64_t m_bits, uint32_t k, uint64_t d, uint32_t *idx_out,
+                          uint64_t cap, uint64_t *n_out, void *ws, size_t ws_bytes, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (!bits || !n_out || (!idx_out && cap)) return fail(DR_EINVAL, "null pointer");
+    if (m_bits < 32 || (m_bits & 31) || m_bits >= (1ull << 32)) return fail(DR_EINVAL, "bad m_bits");
+    if (k < 1 || k > 32) return fail(DR_EINVAL, "k must be in [1, 32]");
+    if (d >= (1ull << 32)) return fail(DR_EINVAL, "d >= 2^32");
+    Plan p = single_plan(d);
+    TInit &in = p.t[0];
+    in.k = k;
+    in.m_words_in = (uint32_t)(m_bits / 32);
+    in.bits = const_cast<uint32_t *>(bits);
+    p.carve.plan();
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    const Work w = p.carve.view((uint8_t *)ws);
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(run_zero_state(w, s));
+    DR_HIP(launch_params(w, s));
+    DR_HIP(launch_query_plain(w, idx_out, cap, n_out, persist_grid(4), s));
+    return DR_OK;
+}
+
+dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_cap, uint32_t degree, uint32_t n_seg,
+                             float *coef_out, uint32_t *sigma_out, void *ws, size_t ws_bytes, void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (!n || !coef_out || ((!vals || !sigma_out) && n_cap)) return fail(DR_EINVAL, "null pointer");
+    if (degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
+    if (n_seg < 1 || n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
+    if (n_cap >= (1ull << 32)) return fail(DR_EINVAL, "n_cap >= 2^32");
+    Plan p = single_plan(n_cap);
+    TInit &in = p.t[0];
+    in.degree = degree;
+    in.nseg = n_seg;
+    in.coef = coef_out;
+    in.coef_stride = degree + 1;
+    in.sigma = sigma_out;
+    in.fit_blk0 = 0;
+    p.carve.fit_blocks = (uint64_t)n_seg * FIT_CHUNKS;
+    p.carve.plan();
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    const Work w = p.carve.view((uint8_t *)ws);
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(run_zero_state(w, s));
+    DR_HIP(launch_keygen(w, vals, n, n_cap, persist_grid(4), s));
+    DR_HIP(launch_value_setup(w, false, s));
+    DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, persist_grid(4), s));
+    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
+    DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
+    return DR_OK;
+}
+
+dr_status dr_curvefit_decode(const float *coef, const uint32_t *sigma, const uint64_t *n, uint64_t n_cap,
+                             uint32_t degree, uint32_t n_seg, float *vals_out, void *ws, size_t ws_bytes,
+                             void *stream) {
+    hipStream_t s = (hipStream_t)stream;
+    if (!n || ((!coef || !sigma || !vals_out) && n_cap)) return fail(DR_EINVAL, "null pointer");
+    if (degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
+    if (n_seg < 1 || n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
+    if (n_cap >= (1ull << 32)) return fail(DR_EINVAL, "n_cap >= 2^32");
+    Plan p = single_plan(0);
+    TInit &in = p.t[0];
+    in.degree = degree;
+    in.nseg = n_seg;
+    p.carve.plan();
+    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
+    const Work w = p.carve.view((uint8_t *)ws);
+    DR_HIP(run_init(w, p.t, s));
+    DR_HIP(launch_curvefit_decode(w, coef, sigma, n, n_cap, vals_out, persist_grid(4), s));
+    return DR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,330 @@
+// dr_common.hpp -- device-side building blocks shared by the codec's kernels.
+//
+// Layout conventions
+//  * A gradient is split into tensors; tensor t covers global elements
+//    [off, off + d).  Every tensor is also given a padded "slot" of
+//    ntiles * TILE elements starting at tile0 * TILE in the per-element work
+//    arrays, so per-tensor buffers never overlap and tiles never straddle
+//    tensors.
+//  * Work is split into tiles of TILE consecutive elements of one tensor.
+//    Kernels that must emit results in ascending index order take tiles in
+//    order from a ticket counter and chain the per-tile counts with a
+//    decoupled look-back, so each tile learns its output offset in one pass.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dr {
+
+constexpr uint32_t TILE = 4096;               // elements per tile
+constexpr uint32_t TILE_WORDS = TILE / 32;    // bitmap words per tile
+constexpr uint32_t NTHREADS = 256;            // threads per block (4 waves of 64)
+constexpr uint32_t NWAVES = NTHREADS / 64;
+constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
+constexpr uint32_t SLICE_LOG2 = 16;           // Bloom fill slice: 2^16 bits (8 KiB of LDS)
+constexpr uint32_t SLICE_BITS = 1u << SLICE_LOG2;
+constexpr uint32_t SLICE_WORDS = SLICE_BITS / 32;
+constexpr uint32_t HIST1_BITS = 11;           // first top-r digit: key bits 30..20
+constexpr uint32_t HIST1_BINS = 1u << HIST1_BITS;
+constexpr uint32_t HIST1_SHIFT = 20;
+constexpr uint32_t SORT_BINS = 256;           // 8-bit LSD radix digits
+constexpr uint32_t FIT_CHUNKS = 8;            // partial-moment blocks per fitted run
+constexpr uint32_t MAX_DEG = 7;
+constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
+constexpr uint32_t HDR_BYTES = 64;
+constexpr uint32_t HDR_MAGIC = 0x31435244u;   // "DRC1"
+
+// Static per-tensor set-up, written by the host (through kernel arguments).
+struct TInit {
+    uint64_t off;        // first element of the tensor in g / dense_out
+    uint64_t rec_off;    // byte offset of the tensor's payload record
+    uint64_t slot;       // first element of the tensor's padded slot (= tile0 * TILE)
+    uint64_t bl_pos0;    // first entry of this tensor in the Bloom position buffer
+    uint64_t bl_tab0;    // first entry of this tensor in the Bloom count table
+    uint32_t *bits;      // filter words (payload record or caller buffer)
+    float *coef;         // coefficient output; null: the payload record
+    uint32_t *sigma;     // reorder-map output; null: the payload record
+    uint8_t *rec;        // payload record, or null
+    double mC;           // -ln(fpr) / (ln 2)^2: m = 32 ceil(ceil(n mC) / 32)
+    uint32_t d;          // elements
+    uint32_t r;          // requested count, or R_NONZERO
+    uint32_t tile0;      // first tile
+    uint32_t ntiles;     // ceil(d / TILE), at least 1
+    uint32_t k;          // hash functions
+    uint32_t degree;     // requested polynomial degree
+    uint32_t nseg;       // requested runs
+    uint32_t m_words_in; // filter words fixed by the caller, or 0: derive from n
+    uint32_t fit_blk0;   // first block of this tensor in the fit grid
+    uint32_t bl_chunk;   // Bloom insert: items per chunk
+    uint32_t bl_chunk0;  // first Bloom chunk of this tensor
+    uint32_t bl_nchunks; // Bloom chunks reserved for this tensor
+    uint32_t bl_slice0;  // first Bloom slice of this tensor
+    uint32_t bl_nslices; // Bloom slices reserved (covers the largest possible filter)
+    uint32_t hb0, hbn;   // top-r histogram blocks of this tensor
+    uint32_t coef_stride;// floats per run in `coef` when it is given
+    uint32_t pad_;
+    uint64_t rec_cap;    // payload record capacity in bytes (receiver checks the header against it)
+};
+
+// Per-tensor descriptor, in device memory.
+struct TDesc {
+    TInit in;
+    // --- produced on the device ---
+    uint32_t n;          // |S|
+    uint32_t m_words;    // filter words
+    uint32_t nv;         // |P| on the sender
+    uint32_t nv_dec;     // |P| on the receiver
+    uint32_t seff, deff; // runs and degree actually used
+    uint32_t b;          // reorder-map bits per entry
+    uint32_t flags;      // DR_FLAG_* bits (+ internal error bits)
+    uint32_t b1;         // top-r: first-digit bin holding the threshold
+    uint32_t need1;      // top-r: how many to take from bin b1
+    uint32_t ncand;      // top-r: elements in bin b1
+    uint32_t T;          // top-r: exact threshold key
+    uint32_t needT;      // top-r: how many elements with key == T to take
+    uint32_t ntie;       // top-r: elements with key == T
+    uint32_t idx_star;   // top-r: largest index taken among key == T (when ties split)
+    uint32_t stile0;     // value sort: first tile
+    uint32_t sntiles;    // value sort: tiles
+    uint32_t sw0;        // reorder map: first word in the packing grid
+    uint32_t swords;     // reorder map: words
+    uint32_t coef_off;   // payload record: byte offset of the coefficients
+    uint32_t sigma_off;  // payload record: byte offset of the reorder map
+    uint32_t rec_bytes;  // payload record: bytes in use
+    uint32_t pad_;
+};
+
+// device-wide totals produced on the device
+struct Glob {
+    uint32_t sort_tiles;   // value-sort tiles over all tensors
+    uint32_t sigma_words;  // reorder-map words over all tensors
+    uint32_t values;       // sum of |P|
+    uint32_t pad_;
+};
+
+// internal flag bits (besides DR_FLAG_NONFINITE = 1)
+constexpr uint32_t FLAG_NONFINITE = 1u;
+constexpr uint32_t FLAG_DEC_MISMATCH = 2u;   // receiver |P| differs from the header
+constexpr uint32_t FLAG_COUNT = 4u;          // selection count differs from r
+constexpr uint32_t FLAG_CAPACITY = 8u;       // a device-side capacity was exceeded
+
+// Views of the workspace carved on the host.
+struct Work {
+    TDesc *td;
+    Glob *glob;
+    uint32_t ntensors;
+    uint32_t ntiles_total;    // sum of ntiles
+    uint64_t slots;           // padded elements = ntiles_total * TILE
+    uint32_t *tickets;        // ordered-tile ticket counters (zeroed at set-up)
+    uint32_t *done;           // per-tensor completion counters (zeroed at set-up)
+    unsigned long long *lb0;  // look-back state, one array of ntiles_total per ordered pass
+    unsigned long long *lb1;
+    unsigned long long *lb2;
+    unsigned long long *lb3;
+    uint32_t *hist_part;      // top-r first-digit partial histograms
+    uint32_t *hist;           // top-r first-digit histogram per tensor
+    uint32_t *selbits;        // selection bitmap (paper's d-bit string B), slots / 32 words
+    uint32_t *cand_key;       // top-r candidates (keys), per tensor slot
+    uint32_t *cand_idx;       // top-r candidates (indices)
+    uint32_t *S;              // selected indices, per tensor slot
+    uint32_t *P;              // sender's positives, per tensor slot
+    float *V;                 // g[P]
+    uint32_t *keyA, *keyB;    // sort keys
+    uint32_t *valA, *valB;    // sort payloads
+    uint32_t *shist;          // sort: per-tile digit counts (SORT_BINS per tile)
+    uint32_t *srow;           // sort: per tensor digit totals
+    uint32_t *sig;            // unpacked reorder map, per tensor slot
+    float *vsorted;           // values in sorted order, per tensor slot
+    double *fit_part;         // fit: partial moments
+    uint16_t *bpos;           // Bloom insert: bucketed in-slice positions
+    uint32_t *btab;           // Bloom insert: per (slice, chunk) counts then offsets
+};
+
+// ---------------------------------------------------------------------------
+// MurmurHash3_x86_32 of the 4-byte little-endian encoding of an index.
+// The key-dependent part is computed once per index and reused for every
+// seed, since it does not depend on the seed.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t rotl32(uint32_t x, uint32_t r) { return (x << r) | (x >> (32u - r)); }
+
+__device__ __forceinline__ uint32_t mm3_key(uint32_t i) {
+    uint32_t k = i * 0xcc9e2d51u;
+    k = rotl32(k, 15);
+    return k * 0x1b873593u;
+}
+
+__device__ __forceinline__ uint32_t mm3_seed(uint32_t kmix, uint32_t seed) {
+    uint32_t h = seed ^ kmix;
+    h = rotl32(h, 13);
+    h = h * 5u + 0xe6546b64u;
+    h ^= 4u;  // input length in bytes
+    h ^= h >> 16;
+    h *= 0x85ebca6bu;
+    h ^= h >> 13;
+    h *= 0xc2b2ae35u;
+    h ^= h >> 16;
+    return h;
+}
+
+// Bit position of hash j for a key mix in an m-bit filter: floor(h m / 2^32).
+__device__ __forceinline__ uint32_t bloom_pos(uint32_t kmix, uint32_t j, uint32_t m_bits) {
+    return __umulhi(mm3_seed(kmix, j), m_bits);
+}
+
+__device__ __forceinline__ uint32_t test_bit(const uint32_t *w, uint32_t p) { return (w[p >> 5] >> (p & 31u)) & 1u; }
+
+// ---------------------------------------------------------------------------
+// Wave (64-lane) primitives.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+// number of set bits of `mask` in lanes below this one
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ uint32_t popc64(uint64_t m) { return (uint32_t)__popcll(m); }
+
+// inclusive prefix sum across the wave
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+    const uint32_t lane = lane_id();
+#pragma unroll
+    for (uint32_t o = 1; o < 64; o <<= 1) {
+        uint32_t t = __shfl_up(v, o, 64);
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+#pragma unroll
+    for (uint32_t o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+    for (uint32_t o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Exclusive scan of one value per thread over a block of NT threads.
+// `scratch` holds NT/64+1 words of LDS; returns the block total in *total.
+// Contains barriers: every thread of the block must call it.
+template <uint32_t NT>
+__device__ __forceinline__ uint32_t block_excl_scan_n(uint32_t v, uint32_t *scratch, uint32_t *total) {
+    constexpr uint32_t NW = NT / 64;
+    const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
+    uint32_t inc = wave_incl_scan(v);
+    if (lane == 63) scratch[w] = inc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t s = 0;
+        for (uint32_t i = 0; i < NW; ++i) {
+            uint32_t t = scratch[i];
+            scratch[i] = s;
+            s += t;
+        }
+        scratch[NW] = s;
+    }
+    __syncthreads();
+    uint32_t r = scratch[w] + inc - v;
+    *total = scratch[NW];
+    __syncthreads();
+    return r;
+}
+
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *scratch, uint32_t *total) {
+    return block_excl_scan_n<NTHREADS>(v, scratch, total);
+}
+
+// ---------------------------------------------------------------------------
+// Tiles.
+// ---------------------------------------------------------------------------
+// tensor holding global tile `tile` (tiles of a tensor are contiguous)
+__device__ __forceinline__ uint32_t tensor_of_tile(const TDesc *td, uint32_t ntensors, uint32_t tile) {
+    uint32_t lo = 0, hi = ntensors;  // td[lo].tile0 <= tile < td[hi].tile0
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (td[mid].in.tile0 <= tile)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// ---------------------------------------------------------------------------
+// Decoupled look-back over the tiles of one tensor.  Each tile publishes its
+// own count, then walks back over its predecessors until one has published
+// an inclusive prefix.  Tiles are handed out in increasing order by a ticket
+// counter, so every predecessor belongs to a block that is already running
+// and the walk always ends.
+// ---------------------------------------------------------------------------
+constexpr unsigned long long LB_AGG = 1ull << 62;
+constexpr unsigned long long LB_INC = 2ull << 62;
+constexpr unsigned long long LB_VAL = (1ull << 62) - 1;
+
+__device__ __forceinline__ void lb_store(unsigned long long *p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long lb_load(unsigned long long *p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Called by one thread.  Returns the exclusive prefix of `count` over the
+// tiles [first, tile) of the tensor.
+__device__ inline uint64_t lookback(unsigned long long *st, uint32_t tile, uint32_t first, uint64_t count) {
+    if (tile == first) {
+        lb_store(&st[tile], LB_INC | count);
+        return 0;
+    }
+    lb_store(&st[tile], LB_AGG | count);
+    uint64_t excl = 0;
+    uint32_t j = tile - 1;
+    for (;;) {
+        unsigned long long v = lb_load(&st[j]);
+        while ((v >> 62) == 0) {
+            __builtin_amdgcn_s_sleep(1);
+            v = lb_load(&st[j]);
+        }
+        excl += v & LB_VAL;
+        if ((v & LB_INC) || j == first) break;
+        --j;
+    }
+    lb_store(&st[tile], LB_INC | (excl + count));
+    return excl;
+}
+
+// Take the next tile in order from a ticket counter (thread 0), broadcast.
+__device__ __forceinline__ uint32_t next_ticket(uint32_t *ctr, uint32_t *lds_slot) {
+    if (threadIdx.x == 0) *lds_slot = atomicAdd(ctr, 1u);
+    __syncthreads();
+    uint32_t t = *lds_slot;
+    __syncthreads();
+    return t;
+}
+
+// Magnitude key: IEEE bits with the sign cleared (orders like |x|).
+__device__ __forceinline__ uint32_t mag_key(float x) { return __float_as_uint(x) & 0x7fffffffu; }
+
+// Order-preserving u32 image of a float (unsigned order == float order).
+__device__ __forceinline__ uint32_t order_key(float x) {
+    uint32_t u = __float_as_uint(x);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float order_key_inv(uint32_t k) {
+    uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+    return __uint_as_float(u);
+}
+
+// Width of one reorder-map entry: smallest b >= 1 with 2^b >= n.
+__device__ __forceinline__ uint32_t sigma_bits(uint32_t n) {
+    if (n <= 2) return 1;
+    return 32u - __clz(n - 1u);
+}
+
+}  // namespace dr

@@ -1,0 +1,62 @@
+// launch.hpp -- host-side launchers of the codec's kernels (one per .hip file
+// that defines them), called by the C ABI in api.hip.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dr_common.hpp"
+
+namespace dr {
+
+constexpr int INIT_CHUNK = 16;  // tensors per set-up launch (kernel argument size)
+
+struct InitArgs {
+    uint32_t first, count;
+    TInit t[INIT_CHUNK];
+};
+
+struct ZeroRange {
+    void *p;
+    uint64_t words;  // 32-bit words to clear
+};
+struct ZeroArgs {
+    ZeroRange z[8];
+    uint32_t n;
+};
+
+// select.hip
+hipError_t launch_init(const Work &w, const InitArgs &a, hipStream_t s);
+hipError_t launch_zero(const ZeroArgs &a, hipStream_t s);
+hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int grid_persist, bool any_topr,
+                       hipStream_t s);
+hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s);
+hipError_t launch_compact_selection(const Work &w, const float *g, float *val_out, int grid_persist, hipStream_t s);
+hipError_t launch_params(const Work &w, hipStream_t s);
+
+// bloom.hip
+// Insert in rounds of `hash_per_round` hash functions (the position buffer
+// holds that many positions per reserved item).
+hipError_t launch_bloom_insert(const Work &w, uint32_t total_chunks, uint32_t total_slices, uint32_t max_slices,
+                               uint32_t hash_per_round, uint32_t kmax, hipStream_t s);
+hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s);
+hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,
+                              hipStream_t s);
+hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *dense_out, uint32_t *idx_out,
+                               float *val_out, int grid_persist, hipStream_t s);
+
+// valuefit.hip
+hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
+                         hipStream_t s);
+hipError_t launch_value_setup(const Work &w, bool payload, hipStream_t s);
+hipError_t launch_sort(const Work &w, uint32_t cap_tiles, int grid_persist, hipStream_t s);
+hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s);
+hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s);
+hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
+                                  uint64_t n_cap, float *vals_out, int grid_persist, hipStream_t s);
+// device count <-> tensor 0's descriptor (standalone calls)
+hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, hipStream_t s);
+hipError_t launch_export_n(const Work &w, uint64_t *n_out, int field, hipStream_t s);
+hipError_t launch_counts(const Work &w, uint64_t *counts_out, int which, hipStream_t s);
+
+}  // namespace dr

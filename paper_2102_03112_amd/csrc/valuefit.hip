@@ -1,0 +1,560 @@
+// valuefit.hip -- curve-fitting value compression (Section 5) and the
+// reorder map (Section 5.1).
+//
+//  * Sort: the values of each tensor are sorted in descending order by an
+//    LSD radix sort (four 8-bit digits) of the order-preserving u32 image,
+//    complemented so that ascending order of the key is descending order of
+//    the value.  Each pass is stable (ranks within a tile come from wave
+//    ballots in element order), so equal values keep their original order.
+//  * Fit: each run of equal count is fitted by least squares in double: the
+//    normal-equation sums are accumulated per block and reduced in a fixed
+//    order, then a Gaussian elimination with partial pivoting solves the
+//    (D+1) x (D+1) system.  No MFMA: this is a small reduction.
+//  * Reorder map: sigma[q] = sorted rank of value q, packed b bits per entry.
+#include "launch.hpp"
+
+namespace dr {
+
+__device__ __forceinline__ void fit_shape(uint32_t nv, uint32_t degree, uint32_t nseg, uint32_t *seff,
+                                          uint32_t *deff) {
+    if (nv == 0) {
+        *seff = 0;
+        *deff = 0;
+        return;
+    }
+    uint32_t cap = nv / (degree + 1u);
+    if (cap < 1) cap = 1;
+    *seff = nseg < cap ? nseg : cap;
+    *deff = nv >= degree + 1u ? degree : nv - 1u;
+}
+
+// standalone value path: keys from the caller's values
+__global__ __launch_bounds__(NTHREADS) void k_keygen(Work w, const float *__restrict__ vals, const uint64_t *n,
+                                                     uint64_t n_cap) {
+    const uint64_t n64 = *n;
+    const uint32_t nv = (uint32_t)(n64 < n_cap ? n64 : n_cap);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        w.td[0].nv = nv;
+        if (n64 > n_cap) atomicOr(&w.td[0].flags, FLAG_CAPACITY);
+    }
+    for (uint32_t q = blockIdx.x * NTHREADS + threadIdx.x; q < nv; q += gridDim.x * NTHREADS) {
+        w.keyA[q] = ~order_key(vals[q]);
+        w.valA[q] = q;
+    }
+}
+
+hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
+                         hipStream_t s) {
+    k_keygen<<<grid_persist, NTHREADS, 0, s>>>(w, vals, n, n_cap);
+    return hipGetLastError();
+}
+
+// After |P| is known: run shape, reorder-map width, sort tiling, record
+// layout and header.  One block walks the tensors in chunks.
+constexpr uint32_t SETUP_THREADS = 1024;
+
+__global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int payload) {
+    __shared__ uint32_t scratch[SETUP_THREADS / 64 + 1];
+    __shared__ uint32_t carry_tiles, carry_words, carry_vals;
+    if (threadIdx.x == 0) {
+        carry_tiles = 0;
+        carry_words = 0;
+        carry_vals = 0;
+    }
+    __syncthreads();
+    for (uint32_t t0 = 0; t0 < w.ntensors; t0 += SETUP_THREADS) {
+        const uint32_t t = t0 + threadIdx.x;
+        uint32_t ntl = 0, nwd = 0, nv = 0;
+        if (t < w.ntensors) {
+            TDesc &td = w.td[t];
+            nv = td.nv;
+            uint32_t seff, deff;
+            fit_shape(nv, td.in.degree, td.in.nseg, &seff, &deff);
+            td.seff = seff;
+            td.deff = deff;
+            const uint32_t b = sigma_bits(nv);
+            td.b = b;
+            ntl = (nv + TILE - 1) / TILE;
+            nwd = (uint32_t)(((uint64_t)nv * b + 31u) / 32u);
+            td.sntiles = ntl;
+            td.swords = nwd;
+            if (payload) {
+                const uint32_t coef_off = HDR_BYTES + td.m_words * 4u;
+                const uint32_t sigma_off = coef_off + seff * (deff + 1u) * 4u;
+                const uint32_t rec_bytes = sigma_off + nwd * 4u;
+                td.coef_off = coef_off;
+                td.sigma_off = sigma_off;
+                td.rec_bytes = rec_bytes;
+                uint8_t *rec = td.in.rec;
+                uint32_t *h = (uint32_t *)rec;
+                h[0] = HDR_MAGIC;
+                h[1] = HDR_BYTES;
+                *(uint64_t *)(rec + 8) = td.in.d;
+                *(uint64_t *)(rec + 16) = td.n;
+                *(uint64_t *)(rec + 24) = nv;
+                *(uint64_t *)(rec + 32) = (uint64_t)td.m_words * 32u;
+                h[10] = td.in.k;
+                h[11] = 1u;  // MurmurHash3_x86_32, seeds 0..k-1
+                h[12] = deff;
+                h[13] = seff;
+                h[14] = b;
+                h[15] = rec_bytes;
+            }
+        }
+        uint32_t tot_t, tot_w, tot_v;
+        const uint32_t bt = carry_tiles, bw = carry_words, bv = carry_vals;
+        const uint32_t ex_t = block_excl_scan_n<SETUP_THREADS>(ntl, scratch, &tot_t);
+        const uint32_t ex_w = block_excl_scan_n<SETUP_THREADS>(nwd, scratch, &tot_w);
+        const uint32_t ex_v = block_excl_scan_n<SETUP_THREADS>(nv, scratch, &tot_v);
+        (void)ex_v;
+        if (t < w.ntensors) {
+            w.td[t].stile0 = bt + ex_t;
+            w.td[t].sw0 = bw + ex_w;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            carry_tiles = bt + tot_t;
+            carry_words = bw + tot_w;
+            carry_vals = bv + tot_v;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        w.glob->sort_tiles = carry_tiles;
+        w.glob->sigma_words = carry_words;
+        w.glob->values = carry_vals;
+    }
+}
+
+hipError_t launch_value_setup(const Work &w, bool payload, hipStream_t s) {
+    k_value_setup<<<1, SETUP_THREADS, 0, s>>>(w, payload ? 1 : 0);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// LSD radix sort, segmented by tensor
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t tensor_of_stile(const Work &w, uint32_t g) {
+    uint32_t lo = 0, hi = w.ntensors;
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (w.td[mid].stile0 <= g)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(NTHREADS) void k_sort_hist(Work w, const uint32_t *__restrict__ keys, uint32_t shift) {
+    __shared__ uint32_t h[SORT_BINS];
+    const uint32_t total = w.glob->sort_tiles;
+    for (uint32_t gt = blockIdx.x; gt < total; gt += gridDim.x) {
+        const uint32_t t = tensor_of_stile(w, gt);
+        const TDesc &td = w.td[t];
+        const uint32_t lt = gt - td.stile0;
+        h[threadIdx.x] = 0;
+        __syncthreads();
+        const uint32_t q0 = lt * TILE, q1 = min(td.nv, q0 + TILE);
+        const uint32_t *kt = keys + td.in.slot;
+        for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) atomicAdd(&h[(kt[q] >> shift) & 255u], 1u);
+        __syncthreads();
+        w.shist[(uint64_t)SORT_BINS * td.stile0 + (uint64_t)threadIdx.x * td.sntiles + lt] = h[threadIdx.x];
+        __syncthreads();
+    }
+}
+
+// per tensor: digit totals, digit bases, and each digit row's running offsets
+__global__ __launch_bounds__(SORT_BINS) void k_sort_scan(Work w) {
+    const TDesc &td = w.td[blockIdx.x];
+    const uint32_t nt = td.sntiles;
+    if (nt == 0) return;
+    __shared__ uint32_t scratch[SORT_BINS / 64 + 1];
+    uint32_t *row = w.shist + (uint64_t)SORT_BINS * td.stile0 + (uint64_t)threadIdx.x * nt;
+    uint32_t sum = 0;
+    for (uint32_t q = 0; q < nt; ++q) sum += row[q];
+    uint32_t tot;
+    uint32_t run = block_excl_scan_n<SORT_BINS>(sum, scratch, &tot);
+    for (uint32_t q = 0; q < nt; ++q) {
+        const uint32_t c = row[q];
+        row[q] = run;
+        run += c;
+    }
+}
+
+// Stable scatter of one tile.  Element order inside the tile is
+// e = c * 256 + threadIdx.x (c = 0..15); for each c and wave, lanes holding
+// the same digit find each other with 8 ballots, and per-(c, wave, digit)
+// counts in LDS give each element its place among equal digits.
+__global__ __launch_bounds__(NTHREADS) void k_sort_scatter(Work w, const uint32_t *__restrict__ kin,
+                                                           const uint32_t *__restrict__ vin,
+                                                           uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
+                                                           uint32_t shift, int last) {
+    __shared__ uint16_t cnt[16][NWAVES][SORT_BINS];
+    __shared__ uint32_t goff[SORT_BINS];
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    const uint32_t total = w.glob->sort_tiles;
+    for (uint32_t gt = blockIdx.x; gt < total; gt += gridDim.x) {
+        const uint32_t t = tensor_of_stile(w, gt);
+        const TDesc &td = w.td[t];
+        const uint32_t lt = gt - td.stile0;
+        uint32_t *c32 = (uint32_t *)&cnt[0][0][0];
+        for (uint32_t i = threadIdx.x; i < 16 * NWAVES * SORT_BINS / 2; i += NTHREADS) c32[i] = 0;
+        goff[threadIdx.x] = w.shist[(uint64_t)SORT_BINS * td.stile0 + (uint64_t)threadIdx.x * td.sntiles + lt];
+        __syncthreads();
+        const uint32_t q0 = lt * TILE;
+        const uint32_t nv = td.nv;
+        const uint32_t *kt = kin + td.in.slot;
+        const uint32_t *vt = vin + td.in.slot;
+        uint32_t key[16], val[16], rnk[16];
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const uint32_t q = q0 + c * NTHREADS + threadIdx.x;
+            const bool valid = q < nv;
+            key[c] = valid ? kt[q] : 0u;
+            val[c] = valid ? vt[q] : 0u;
+            const uint32_t dg = (key[c] >> shift) & 255u;
+            uint64_t peers = ballot(valid);
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                const bool bit = (dg >> b) & 1u;
+                const uint64_t m = ballot(bit);
+                peers &= bit ? m : ~m;
+            }
+            const uint32_t below = lanes_below(peers);
+            rnk[c] = below;
+            if (valid && below == 0) cnt[c][wv][dg] = (uint16_t)popc64(peers);
+        }
+        __syncthreads();
+        {
+            // exclusive prefix over (c, wave) for digit = threadIdx.x
+            const uint32_t dg = threadIdx.x;
+            uint32_t run = 0;
+            for (int c = 0; c < 16; ++c)
+                for (uint32_t q = 0; q < NWAVES; ++q) {
+                    const uint32_t x = cnt[c][q][dg];
+                    cnt[c][q][dg] = (uint16_t)run;
+                    run += x;
+                }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const uint32_t q = q0 + c * NTHREADS + threadIdx.x;
+            const uint32_t dg = (key[c] >> shift) & 255u;
+            const uint32_t pos = goff[dg] + cnt[c][wv][dg] + rnk[c];
+            if (q < nv && pos < nv && val[c] < nv) {
+                if (last) {
+                    w.sig[td.in.slot + val[c]] = pos;  // reorder map: value q has rank pos
+                    w.vsorted[td.in.slot + pos] = order_key_inv(~key[c]);
+                } else {
+                    kout[td.in.slot + pos] = key[c];
+                    vout[td.in.slot + pos] = val[c];
+                }
+            }
+        }
+        __syncthreads();
+    }
+    (void)lane;
+}
+
+hipError_t launch_sort(const Work &w, uint32_t cap_tiles, int grid_persist, hipStream_t s) {
+    (void)cap_tiles;
+    uint32_t *kin = w.keyA, *vin = w.valA, *kout = w.keyB, *vout = w.valB;
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t shift = 8u * p;
+        k_sort_hist<<<grid_persist, NTHREADS, 0, s>>>(w, kin, shift);
+        k_sort_scan<<<w.ntensors, SORT_BINS, 0, s>>>(w);
+        k_sort_scatter<<<grid_persist, NTHREADS, 0, s>>>(w, kin, vin, kout, vout, shift, p == 3);
+        uint32_t *tk = kin, *tv = vin;
+        kin = kout;
+        vin = vout;
+        kout = tk;
+        vout = tv;
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Least-squares fit of each run
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t tensor_of_fit_block(const Work &w, uint32_t b) {
+    uint32_t lo = 0, hi = w.ntensors;
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (w.td[mid].in.fit_blk0 <= b)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// abscissa of local rank j in a run of ns points
+__device__ __forceinline__ double abscissa(uint64_t j, uint64_t ns) {
+    return ns > 1 ? (double)(2 * (int64_t)j - (int64_t)(ns - 1)) / (double)(ns - 1) : 0.0;
+}
+
+template <int D>
+__device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, uint64_t j0, uint64_t j1,
+                                 double *out) {
+    constexpr int NP = 2 * D + 1;
+    double pw[NP], rh[D + 1];
+#pragma unroll
+    for (int e = 0; e < NP; ++e) pw[e] = 0.0;
+#pragma unroll
+    for (int e = 0; e <= D; ++e) rh[e] = 0.0;
+    for (uint64_t j = j0 + threadIdx.x; j < j1; j += NTHREADS) {
+        const double t = abscissa(j, ns);
+        const double v = (double)y[lo_run + j];
+        double tp = 1.0;
+#pragma unroll
+        for (int e = 0; e < NP; ++e) {
+            pw[e] += tp;
+            if (e <= D) rh[e] += tp * v;
+            tp *= t;
+        }
+    }
+    __shared__ double red[NWAVES][NP + D + 1];
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+#pragma unroll
+    for (int e = 0; e < NP; ++e) {
+        const double s = wave_sum_f64(pw[e]);
+        if (lane == 0) red[wv][e] = s;
+    }
+#pragma unroll
+    for (int e = 0; e <= D; ++e) {
+        const double s = wave_sum_f64(rh[e]);
+        if (lane == 0) red[wv][NP + e] = s;
+    }
+    __syncthreads();
+    if (threadIdx.x < (uint32_t)(NP + D + 1)) {
+        double s = 0.0;
+        for (uint32_t q = 0; q < NWAVES; ++q) s += red[q][threadIdx.x];
+        out[threadIdx.x < (uint32_t)NP ? threadIdx.x : (2 * MAX_DEG + 1) + (threadIdx.x - NP)] = s;
+    }
+}
+
+__global__ __launch_bounds__(NTHREADS) void k_fit_moments(Work w) {
+    const uint32_t t = tensor_of_fit_block(w, blockIdx.x);
+    const TDesc &td = w.td[t];
+    const uint32_t local = blockIdx.x - td.in.fit_blk0;
+    const uint32_t s = local / FIT_CHUNKS, ch = local % FIT_CHUNKS;
+    if (s >= td.seff) return;
+    const uint64_t nv = td.nv, S = td.seff;
+    const uint64_t lo = s * nv / S, hi = (s + 1) * nv / S, ns = hi - lo;
+    const uint64_t j0 = ns * ch / FIT_CHUNKS, j1 = ns * (ch + 1) / FIT_CHUNKS;
+    const float *y = w.vsorted + td.in.slot;
+    double *out = w.fit_part + (uint64_t)blockIdx.x * NMOM;
+    switch (td.deff) {
+        case 0: fit_moments_body<0>(y, lo, ns, j0, j1, out); break;
+        case 1: fit_moments_body<1>(y, lo, ns, j0, j1, out); break;
+        case 2: fit_moments_body<2>(y, lo, ns, j0, j1, out); break;
+        case 3: fit_moments_body<3>(y, lo, ns, j0, j1, out); break;
+        case 4: fit_moments_body<4>(y, lo, ns, j0, j1, out); break;
+        case 5: fit_moments_body<5>(y, lo, ns, j0, j1, out); break;
+        case 6: fit_moments_body<6>(y, lo, ns, j0, j1, out); break;
+        default: fit_moments_body<7>(y, lo, ns, j0, j1, out); break;
+    }
+}
+
+// one thread per (tensor, run): sum the partial moments in chunk order and
+// solve the normal equations by Gaussian elimination with partial pivoting
+__global__ void k_fit_solve(Work w, uint32_t total_runs) {
+    const uint32_t gs = blockIdx.x * blockDim.x + threadIdx.x;
+    if (gs >= total_runs) return;
+    const uint32_t t = tensor_of_fit_block(w, gs * FIT_CHUNKS);
+    const TDesc &td = w.td[t];
+    const uint32_t s = gs - td.in.fit_blk0 / FIT_CHUNKS;
+    if (s >= td.in.nseg) return;
+    const bool standalone = td.in.coef != nullptr;
+    const uint32_t D = td.deff, N = D + 1;
+    float *row;
+    if (standalone) {
+        row = td.in.coef + (uint64_t)s * td.in.coef_stride;
+        if (s >= td.seff) {
+            for (uint32_t p = 0; p < td.in.coef_stride; ++p) row[p] = 0.0f;
+            return;
+        }
+        for (uint32_t p = N; p < td.in.coef_stride; ++p) row[p] = 0.0f;
+    } else {
+        if (s >= td.seff) return;
+        row = (float *)(td.in.rec + td.coef_off) + (uint64_t)s * N;
+    }
+    double mom[NMOM];
+    for (uint32_t e = 0; e < NMOM; ++e) mom[e] = 0.0;
+    const double *part = w.fit_part + (uint64_t)(td.in.fit_blk0 + s * FIT_CHUNKS) * NMOM;
+    for (uint32_t c = 0; c < FIT_CHUNKS; ++c)
+        for (uint32_t e = 0; e < NMOM; ++e) mom[e] += part[c * NMOM + e];
+    double A[MAX_DEG + 1][MAX_DEG + 2];
+    for (uint32_t p = 0; p < N; ++p) {
+        for (uint32_t q = 0; q < N; ++q) A[p][q] = mom[p + q];
+        A[p][N] = mom[2 * MAX_DEG + 1 + p];
+    }
+    bool ok = true;
+    for (uint32_t col = 0; col < N; ++col) {
+        uint32_t piv = col;
+        for (uint32_t r = col + 1; r < N; ++r)
+            if (fabs(A[r][col]) > fabs(A[piv][col])) piv = r;
+        if (A[piv][col] == 0.0) {
+            ok = false;
+            break;
+        }
+        if (piv != col)
+            for (uint32_t c = 0; c <= N; ++c) {
+                const double tmp = A[col][c];
+                A[col][c] = A[piv][c];
+                A[piv][c] = tmp;
+            }
+        for (uint32_t r = col + 1; r < N; ++r) {
+            const double f = A[r][col] / A[col][col];
+            for (uint32_t c = col; c <= N; ++c) A[r][c] -= f * A[col][c];
+        }
+    }
+    double x[MAX_DEG + 1];
+    for (int p = (int)N - 1; p >= 0; --p) {
+        double acc = A[p][N];
+        for (uint32_t q = p + 1; q < N; ++q) acc -= A[p][q] * x[q];
+        x[p] = ok ? acc / A[p][p] : 0.0;
+    }
+    for (uint32_t p = 0; p < N; ++p) row[p] = (float)x[p];
+}
+
+hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s) {
+    if (fit_blocks == 0) return hipSuccess;
+    k_fit_moments<<<fit_blocks, NTHREADS, 0, s>>>(w);
+    const uint32_t runs = fit_blocks / FIT_CHUNKS;
+    k_fit_solve<<<(runs + 63) / 64, 64, 0, s>>>(w, runs);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Reorder map packing: each output word gathers the entries it overlaps.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t tensor_of_sword(const Work &w, uint32_t g) {
+    uint32_t lo = 0, hi = w.ntensors;
+    while (hi - lo > 1) {
+        uint32_t mid = (lo + hi) >> 1;
+        if (w.td[mid].sw0 <= g)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(NTHREADS) void k_sigma_pack(Work w) {
+    const uint32_t total = w.glob->sigma_words;
+    for (uint32_t gw = blockIdx.x * NTHREADS + threadIdx.x; gw < total; gw += gridDim.x * NTHREADS) {
+        const uint32_t t = tensor_of_sword(w, gw);
+        const TDesc &td = w.td[t];
+        const uint32_t wl = gw - td.sw0;
+        const uint32_t b = td.b, nv = td.nv;
+        const uint64_t bit0 = (uint64_t)wl * 32u;
+        const uint64_t qa = bit0 / b;
+        uint64_t qb = (bit0 + 31u) / b;
+        if (qb > nv - 1u) qb = nv - 1u;
+        const uint32_t *sg = w.sig + td.in.slot;
+        uint32_t v = 0;
+        for (uint64_t q = qa; q <= qb; ++q) {
+            const int64_t sh = (int64_t)(q * b) - (int64_t)bit0;
+            const uint64_t e = sg[q];
+            if (sh >= 0)
+                v |= (uint32_t)(e << sh);
+            else
+                v |= (uint32_t)(e >> (-sh));
+        }
+        uint32_t *out = td.in.sigma ? td.in.sigma : (uint32_t *)(td.in.rec + td.sigma_off);
+        out[wl] = v;
+    }
+}
+
+hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s) {
+    k_sigma_pack<<<grid_persist, NTHREADS, 0, s>>>(w);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Standalone value decode: sigma and coefficients in the caller's layout
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(NTHREADS) void k_curvefit_decode(Work w, const float *__restrict__ coef,
+                                                              const uint32_t *__restrict__ sigma,
+                                                              const uint64_t *n, uint64_t n_cap,
+                                                              float *__restrict__ out) {
+    const TDesc &td = w.td[0];
+    const uint64_t n64 = *n;
+    const uint32_t nv = (uint32_t)(n64 < n_cap ? n64 : n_cap);
+    uint32_t seff, deff;
+    fit_shape(nv, td.in.degree, td.in.nseg, &seff, &deff);
+    const uint32_t b = sigma_bits(nv);
+    const uint32_t stride = td.in.degree + 1u;
+    for (uint32_t q = blockIdx.x * NTHREADS + threadIdx.x; q < nv; q += gridDim.x * NTHREADS) {
+        const uint64_t bit = (uint64_t)q * b;
+        const uint32_t w0 = sigma[bit >> 5], sh = (uint32_t)(bit & 31u);
+        uint64_t v = w0 >> sh;
+        if (sh + b > 32u) v |= (uint64_t)sigma[(bit >> 5) + 1] << (32u - sh);
+        const uint32_t rank = (uint32_t)(v & ((1ull << b) - 1ull));
+        float y = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range rank
+        if (rank < nv) {
+            const uint64_t s = (((uint64_t)rank + 1u) * seff - 1u) / nv;
+            const uint64_t lo = s * nv / seff, hi = (s + 1) * nv / seff;
+            const double tt = abscissa(rank - lo, hi - lo);
+            const float *c = coef + s * stride;
+            double acc = (double)c[deff];
+            for (int p = (int)deff - 1; p >= 0; --p) acc = acc * tt + (double)c[p];
+            y = (float)acc;
+        }
+        out[q] = y;
+    }
+}
+
+hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
+                                  uint64_t n_cap, float *vals_out, int grid_persist, hipStream_t s) {
+    k_curvefit_decode<<<grid_persist, NTHREADS, 0, s>>>(w, coef, sigma, n, n_cap, vals_out);
+    return hipGetLastError();
+}
+
+__global__ void k_import_n(Work w, const uint64_t *n, uint64_t n_cap) {
+    const uint64_t v = *n;
+    w.td[0].n = (uint32_t)(v < n_cap ? v : n_cap);
+    if (v > n_cap) w.td[0].flags |= FLAG_CAPACITY;
+}
+
+__global__ void k_export_n(Work w, uint64_t *n_out, int field) {
+    const TDesc &td = w.td[0];
+    *n_out = field == 0 ? td.n : td.nv;
+}
+
+hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, hipStream_t s) {
+    k_import_n<<<1, 1, 0, s>>>(w, n, n_cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_export_n(const Work &w, uint64_t *n_out, int field, hipStream_t s) {
+    k_export_n<<<1, 1, 0, s>>>(w, n_out, field);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Per-tensor counts for the caller
+// ---------------------------------------------------------------------------
+__global__ void k_counts(Work w, uint64_t *out, int which) {
+    const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= w.ntensors) return;
+    const TDesc &td = w.td[t];
+    if (which == 0) {
+        out[4 * t + 0] = td.n;
+        out[4 * t + 1] = td.nv;
+        out[4 * t + 3] = td.flags;
+    } else {
+        out[4 * t + 2] = td.nv_dec;
+        out[4 * t + 3] |= td.flags & FLAG_DEC_MISMATCH;
+    }
+}
+
+hipError_t launch_counts(const Work &w, uint64_t *counts_out, int which, hipStream_t s) {
+    k_counts<<<(w.ntensors + 255) / 256, 256, 0, s>>>(w, counts_out, which);
+    return hipGetLastError();
+}
+
+}  // namespace dr

@@ -1,0 +1,72 @@
+"""Helpers shared by the GPU parity tests (not collected by pytest)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev_tensor(a: np.ndarray):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t) -> np.ndarray:
+    return t.detach().cpu().numpy()
+
+
+def u64_scalar():
+    import torch
+
+    return torch.zeros(1, dtype=torch.int64, device="cuda")
+
+
+def coef_close(c_gpu: np.ndarray, c_ref64: np.ndarray, rows: int, stride: int, ncoef: int, tol: float = 1e-4):
+    """Norm-wise per run: ||c_gpu - c_ref||_inf <= tol ||c_ref||_inf."""
+    for s in range(rows):
+        a = c_gpu[s * stride: s * stride + ncoef].astype(np.float64)
+        b = c_ref64[s * stride: s * stride + ncoef]
+        scale = np.max(np.abs(b))
+        err = np.max(np.abs(a - b)) if a.size else 0.0
+        assert err <= tol * max(scale, 1e-300), f"run {s}: |dc| {err:.3e} > {tol} * {scale:.3e}"
+
+
+def values_close(y_gpu: np.ndarray, y_ref: np.ndarray, ranks: np.ndarray, n: int, seff: int, tol: float = 1e-5):
+    """|dy_q| <= tol * max(|y_ref_q|, max |y_ref| over q's run)."""
+    if n == 0:
+        return
+    ranks = ranks.astype(np.int64)
+    s = ((ranks + 1) * seff - 1) // n
+    run_max = np.zeros(seff)
+    np.maximum.at(run_max, s, np.abs(y_ref.astype(np.float64)))
+    bound = tol * np.maximum(np.abs(y_ref.astype(np.float64)), run_max[s])
+    err = np.abs(y_gpu.astype(np.float64) - y_ref.astype(np.float64))
+    bad = np.flatnonzero(err > bound)
+    assert bad.size == 0, f"{bad.size} values off, first q={bad[0]} gpu={y_gpu[bad[0]]} ref={y_ref[bad[0]]}"
+
+
+def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
+    """A GPU payload record against the oracle's result for the same tensor:
+    bit-exact filter and reorder map, header fields, coefficients within
+    1e-4 of the oracle's double-precision solution."""
+    assert rec.d == ref.d
+    assert rec.n_selected == ref.S.size
+    assert rec.n_values == ref.P.size
+    assert (rec.m_bits, rec.k, rec.hash_id) == (ref.m, ref.k, 1)
+    assert (rec.seg_eff, rec.deg_eff, rec.sigma_b) == (ref.fit.S_eff, ref.fit.D_eff, ref.fit.b)
+    np.testing.assert_array_equal(rec.bits, ref.bits)
+    np.testing.assert_array_equal(rec.sigma, ref.fit.sigma)
+    nc = ref.fit.D_eff + 1
+    c_gpu = rec.coef.reshape(rec.seg_eff, nc) if rec.seg_eff else rec.coef
+    c_ref = ref.fit.coef64.reshape(n_seg, degree + 1)[: rec.seg_eff, :nc]
+    coef_close(np.ascontiguousarray(c_gpu).ravel(), np.ascontiguousarray(c_ref).ravel(), rec.seg_eff, nc, nc)
+    words = (ref.fit.n * ref.fit.b + 31) // 32
+    assert rec.rec_bytes == 64 + ref.m // 8 + 4 * rec.seg_eff * nc + 4 * words

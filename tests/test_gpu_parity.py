@@ -1,0 +1,306 @@
+"""GPU parity: every C-ABI entry point against the CPU oracle, element by
+element, on seeded inputs that span several tiles and a ragged tail.
+
+Bit-exact: selected indices, filter words, positives, reorder maps, header
+fields.  Floating point: fit coefficients within 1e-4 (norm-wise per run) of
+the oracle's double-precision solution; reconstructed values within 1e-5 of
+the oracle's reconstruction from the same payload (floor: the run's largest
+magnitude, which guards zero crossings).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2102_03112_amd import binding as B
+from paper_2102_03112_amd import workloads as W
+from _gpu_util import check_record, coef_close, dev_tensor, host, log, u64_scalar, values_close
+
+pytestmark = pytest.mark.gpu
+
+_WS = {}
+
+
+def ws_for(d, n_tensors=1):
+    need = B.workspace_bytes(d, n_tensors)
+    cur = _WS.get("ws")
+    if cur is None or cur.numel() < need:
+        _WS["ws"] = None
+        _WS["ws"] = B.workspace(max(d, 1 << 20), n_tensors)
+    return _WS["ws"]
+
+
+def sync():
+    import torch
+
+    torch.cuda.synchronize()
+
+
+def gen(kind, d, seed):
+    if kind == "normal":
+        return W.normal(d, seed)
+    if kind == "tied":
+        return W.tied_values(d, seed)
+    if kind == "coarse":
+        rng = np.random.default_rng(seed)
+        return (rng.integers(-20, 21, d) * 0.25).astype(np.float32)
+    if kind == "equal":
+        return np.full(d, 0.5, dtype=np.float32)
+    if kind == "sparse":
+        return W.sparse_normal(d, seed, 0.4)
+    if kind == "zeros":
+        g = np.zeros(d, dtype=np.float32)
+        g[::3] = -0.0
+        return g
+    raise ValueError(kind)
+
+
+# ---------------------------------------------------------------------------
+# dr_sparsify_topr
+# ---------------------------------------------------------------------------
+TOPR_CASES = [
+    (1, 1, "normal"), (1, 0, "normal"), (100, 7, "tied"), (4096, 41, "normal"), (4097, 4097, "tied"),
+    (3 * 4096 + 17, 1000, "tied"), (70000, 7000, "normal"), (70000, 1, "tied"), (200_000, 2000, "coarse"),
+    (10_000, 333, "equal"), (123_457, 61_000, "coarse"), (50_000, 25_000, "zeros"),
+]
+
+
+@pytest.mark.parametrize("d,r,kind", TOPR_CASES)
+def test_topr_parity(d, r, kind):
+    import torch
+
+    log(f"topr d={d} r={r} kind={kind}")
+    g = gen(kind, d, seed=d + r)
+    gd = dev_tensor(g)
+    cap = max(r, 1)
+    idx = torch.full((cap,), -1, dtype=torch.int32, device="cuda")
+    val = torch.zeros(cap, dtype=torch.float32, device="cuda")
+    n = u64_scalar()
+    B.sparsify_topr(gd, r, idx, val, n, ws_for(d))
+    sync()
+    ref = oracle.topr(g, r)
+    assert int(host(n)[0]) == r
+    np.testing.assert_array_equal(host(idx)[:r].view(np.uint32), ref)
+    np.testing.assert_array_equal(host(val)[:r], g[ref.astype(np.int64)])
+
+
+@pytest.mark.parametrize("d,kind", [(50_000, "sparse"), (10_000, "zeros"), (5000, "normal"), (3 * 4096 + 1, "sparse")])
+def test_support_parity(d, kind):
+    import torch
+
+    log(f"support d={d} kind={kind}")
+    g = gen(kind, d, seed=d)
+    gd = dev_tensor(g)
+    idx = torch.full((d,), -1, dtype=torch.int32, device="cuda")
+    n = u64_scalar()
+    B.sparsify_topr(gd, B.R_NONZERO, idx, None, n, ws_for(d))
+    sync()
+    ref = oracle.nonzero(g)
+    assert int(host(n)[0]) == ref.size
+    np.testing.assert_array_equal(host(idx)[: ref.size].view(np.uint32), ref)
+
+
+# ---------------------------------------------------------------------------
+# dr_bloom_encode / dr_bloom_decode
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize(
+    "d,n,fpr",
+    [(1000, 0, 1e-3), (1000, 1, 1e-3), (36_864, 369, 1e-3), (1 << 20, 10_486, 1e-3), (8192, 8192, 1e-4),
+     (300_000, 100_000, 1e-9), (200_000, 5000, 0.5), (25_557_032, 255_571, 1e-3)],
+)
+def test_bloom_encode_parity(d, n, fpr):
+    log(f"bloom_encode d={d} n={n} fpr={fpr}")
+    S = W.random_indices(d, n, seed=n + 3)
+    m, k = oracle.bloom_params(n, fpr)
+    ref = oracle.bloom_encode(S, m, k)
+    import torch
+
+    Sd = dev_tensor(S.view(np.int32)) if n else torch.zeros(1, dtype=torch.int32, device="cuda")
+    nd = dev_tensor(np.array([n], dtype=np.int64))
+    bits = torch.full((m // 32,), 0x5A5A5A5A, dtype=torch.int32, device="cuda")
+    B.bloom_encode(Sd, nd, n, m, k, bits, ws_for(max(n, 1)))
+    sync()
+    np.testing.assert_array_equal(host(bits).view(np.uint32), ref)
+
+
+@pytest.mark.parametrize(
+    "d,n,fpr",
+    [(1, 1, 1e-3), (4095, 40, 1e-3), (4096, 41, 1e-2), (4097, 41, 1e-3), (3 * 4096 + 5, 200, 1e-3),
+     (100_000, 1000, 1e-3), (1 << 20, 10_486, 1e-3), (250_000, 150_000, 1e-4)],
+)
+def test_bloom_decode_parity(d, n, fpr):
+    import torch
+
+    log(f"bloom_decode d={d} n={n} fpr={fpr}")
+    S = W.random_indices(d, n, seed=d)
+    m, k = oracle.bloom_params(n, fpr)
+    bits = oracle.bloom_encode(S, m, k)
+    ref = oracle.bloom_query(bits, m, k, d)
+    idx = torch.full((d,), -1, dtype=torch.int32, device="cuda")
+    nd = u64_scalar()
+    B.bloom_decode(dev_tensor(bits.view(np.int32)), m, k, d, idx, d, nd, ws_for(d))
+    sync()
+    assert int(host(nd)[0]) == ref.size
+    np.testing.assert_array_equal(host(idx)[: ref.size].view(np.uint32), ref)
+
+
+def test_bloom_decode_full_empty_and_capacity():
+    import torch
+
+    d, m, k = 10_000, 256, 3
+    ws = ws_for(d)
+    idx = torch.full((d,), -1, dtype=torch.int32, device="cuda")
+    nd = u64_scalar()
+    full = np.full(m // 32, 0xFFFFFFFF, dtype=np.uint32)
+    B.bloom_decode(dev_tensor(full.view(np.int32)), m, k, d, idx, d, nd, ws)
+    sync()
+    assert int(host(nd)[0]) == d
+    np.testing.assert_array_equal(host(idx).view(np.uint32), np.arange(d, dtype=np.uint32))
+    empty = np.zeros(m // 32, dtype=np.uint32)
+    B.bloom_decode(dev_tensor(empty.view(np.int32)), m, k, d, idx, d, nd, ws)
+    sync()
+    assert int(host(nd)[0]) == 0
+    # output capacity smaller than the count: the first `cap` entries and the full count
+    S = W.random_indices(d, 500, seed=1)
+    m2, k2 = oracle.bloom_params(500, 0.05)
+    bits = oracle.bloom_encode(S, m2, k2)
+    ref = oracle.bloom_query(bits, m2, k2, d)
+    small = torch.full((100,), -1, dtype=torch.int32, device="cuda")
+    B.bloom_decode(dev_tensor(bits.view(np.int32)), m2, k2, d, small, 100, nd, ws)
+    sync()
+    assert int(host(nd)[0]) == ref.size
+    np.testing.assert_array_equal(host(small).view(np.uint32), ref[:100])
+
+
+# ---------------------------------------------------------------------------
+# dr_curvefit_encode / dr_curvefit_decode
+# ---------------------------------------------------------------------------
+CURVE_CASES = [
+    (0, 5, 8), (1, 5, 8), (2, 5, 8), (5, 5, 8), (6, 5, 8), (7, 5, 8), (47, 5, 8), (48, 5, 8), (1000, 5, 8),
+    (4096, 5, 1), (4097, 5, 8), (40_000, 5, 8), (12, 1, 6), (5000, 3, 16), (300_000, 5, 8), (100_000, 7, 64),
+]
+
+
+@pytest.mark.parametrize("n,D,S", CURVE_CASES)
+def test_curvefit_parity(n, D, S):
+    import torch
+
+    log(f"curvefit n={n} D={D} S={S}")
+    rng = np.random.default_rng(n + D)
+    V = (rng.laplace(0, 5e-4, n)).astype(np.float32)
+    if n > 100:
+        V[::17] = V[5]  # exact ties
+    ref = oracle.curvefit_encode(V, D, S)
+    nw = max(1, oracle.sigma_words(n))
+    Vd = dev_tensor(V) if n else torch.zeros(1, dtype=torch.float32, device="cuda")
+    nd = dev_tensor(np.array([n], dtype=np.int64))
+    coef = torch.full((S * (D + 1),), 7.0, dtype=torch.float32, device="cuda")
+    sig = torch.zeros(nw, dtype=torch.int32, device="cuda")
+    ws = ws_for(max(n, 1))
+    B.curvefit_encode(Vd, nd, n, D, S, coef, sig, ws)
+    out = torch.zeros(max(n, 1), dtype=torch.float32, device="cuda")
+    B.curvefit_decode(coef, sig, nd, n, D, S, out, ws)
+    sync()
+    c_gpu = host(coef)
+    s_gpu = host(sig).view(np.uint32)[: oracle.sigma_words(n)]
+    np.testing.assert_array_equal(s_gpu, ref.sigma)
+    coef_close(c_gpu, ref.coef64, ref.S_eff, D + 1, ref.D_eff + 1)
+    # everything outside the fitted rows and degrees is zero
+    mask = np.ones(S * (D + 1), bool)
+    for s in range(ref.S_eff):
+        mask[s * (D + 1): s * (D + 1) + ref.D_eff + 1] = False
+    assert np.all(c_gpu[mask] == 0)
+    # decode: GPU vs oracle on the same (GPU) payload
+    y_ref = oracle.curvefit_decode(c_gpu, s_gpu, n, D, S)
+    if n:
+        ranks = oracle.sigma_unpack(s_gpu, n)
+        values_close(host(out)[:n], y_ref, ranks, n, ref.S_eff)
+
+
+# ---------------------------------------------------------------------------
+# dr_roundtrip over a gradient split into tensors
+# ---------------------------------------------------------------------------
+def run_roundtrip(g, cfg: B.Config):
+    import torch
+
+    total, rec_off = B.payload_layout(cfg)
+    d = cfg.d
+    gd = dev_tensor(g) if d else torch.zeros(1, dtype=torch.float32, device="cuda")
+    payload = torch.zeros(total, dtype=torch.uint8, device="cuda")
+    dense = torch.full((max(d, 1),), 9.0, dtype=torch.float32, device="cuda")
+    idx = torch.full((max(d, 1),), -1, dtype=torch.int32, device="cuda")
+    val = torch.zeros(max(d, 1), dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4 * cfg.n_tensors, dtype=torch.int64, device="cuda")
+    ws = ws_for(max(d, 1), cfg.n_tensors)
+    B.roundtrip(gd, cfg, payload, dense, idx, val, counts, ws)
+    sync()
+    return dict(payload=host(payload), rec_off=rec_off, dense=host(dense)[:d], idx=host(idx)[:d].view(np.uint32),
+                val=host(val)[:d], counts=host(counts).reshape(cfg.n_tensors, 4))
+
+
+def check_roundtrip(g, cfg: B.Config, out, refs):
+    off = cfg.offsets
+    for t, ref in enumerate(refs):
+        a, b = int(off[t]), int(off[t + 1])
+        rec = B.parse_record(out["payload"], out["rec_off"][t])
+        check_record(rec, ref, cfg.degree, cfg.n_seg)
+        n_sel, nv, nv_dec, flags = [int(x) for x in out["counts"][t]]
+        assert (n_sel, nv, nv_dec, flags) == (ref.S.size, ref.P.size, ref.P.size, 0)
+        np.testing.assert_array_equal(out["idx"][a: a + nv], ref.P_dec)
+        # receiver values vs the oracle's decode of this very payload
+        y_same = oracle.curvefit_decode(rec.coef if rec.seg_eff else np.zeros(0, np.float32),
+                                        rec.sigma, nv, rec.deg_eff, max(rec.seg_eff, 1)) if nv else np.zeros(0)
+        if nv:
+            ranks = oracle.sigma_unpack(rec.sigma, nv)
+            values_close(out["val"][a: a + nv], y_same, ranks, nv, rec.seg_eff)
+            # and vs the oracle's own end-to-end reconstruction
+            values_close(out["val"][a: a + nv], ref.vals, ranks, nv, rec.seg_eff)
+        dense = out["dense"][a:b]
+        pos = ref.P_dec.astype(np.int64)
+        np.testing.assert_array_equal(dense[pos], out["val"][a: a + nv])
+        offp = np.ones(b - a, bool)
+        offp[pos] = False
+        assert np.all(dense[offp] == 0)
+
+
+RT_CASES = {
+    "resnet20_conv_37k": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 8),
+    "student_t_3x": (None, None, (1, 100), 1e-3, 5, 8),
+    "support_50k": (W.sparse_normal(50_000, 7, 0.4), [0, 50_000], None, 1e-4, 3, 16),
+    # empty, 1-, 5-, 4096-, 4097-element, empty and 4-element tensors
+    "ragged_tensors": (W.normal(8203, 8), [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8),
+    "take_all": (W.normal(5000, 9), [0, 5000], (1, 1), 1e-3, 2, 4),
+}
+
+
+@pytest.mark.parametrize("name", list(RT_CASES))
+def test_roundtrip_parity(name):
+    g, off, ratio, fpr, D, S = RT_CASES[name]
+    if name == "student_t_3x":
+        w = W.Workload("t", 100_001, 3, ratio, fpr, D, S, "student_t3", 77)
+        g, off = W.generate(w), w.offsets()
+    log(f"roundtrip {name} d={g.size} tensors={len(off) - 1}")
+    assert off[-1] == g.size
+    cfg = B.Config(off, ratio, fpr, D, S)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, D, S)
+    check_roundtrip(g, cfg, out, refs)
+
+
+def test_roundtrip_normal_1m_full_size():
+    w = W.WORKLOADS["normal_1m"]
+    log("roundtrip normal_1m")
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg)
+    check_roundtrip(g, cfg, out, refs)
+
+
+def test_roundtrip_is_deterministic():
+    w = W.Workload("t", 300_000, 2, (1, 100), 1e-3, 5, 8, "laplace_5e-4", 5)
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w)
+    a = run_roundtrip(g, cfg)
+    b = run_roundtrip(g, cfg)
+    np.testing.assert_array_equal(a["payload"], b["payload"])
+    np.testing.assert_array_equal(a["dense"], b["dense"])
