@@ -1,0 +1,230 @@
+"""Benchmark: one codec round trip (sender encode + receiver decode) of a
+synthetic gradient per step, on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Prints one JSON line.  `value` is Gelem/s of dense gradient (d / step time)
+with the inputs already in device memory; `hbm_frac` is the round trip's
+algorithmic bytes (read g, write and read the payload, write the dense
+gradient) per step time over the 8 TB/s HBM peak; `roofline` describes the
+kernel that takes the largest share of the step, timed with HIP events on
+the library's stream; `cpu_baseline` times the CPU oracle on the same
+workload on one host core.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "codec round-trip Gelem/s of dense gradient + % HBM peak; bits/element"
+HBM_PEAK = 8.0e12            # B/s, MI355X HBM3E
+INT_PEAK = 256 * 64 * 2.4e9  # 32-bit integer lane-ops/s: 256 CUs x 64 lanes/clk x 2.4 GHz
+MALL_BYTES = 256 << 20       # last-level cache; inputs rotate through more than this
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_models(d, payload_bytes, n_sel, n_val, k, fill):
+    """Algorithmic work of the dominant-kernel candidates, per launch.
+
+    HBM kernels: bytes the step must move.  The full-range query is integer
+    arithmetic: each index costs the seed-free half of MurmurHash3 (3 ops:
+    multiply, rotate, multiply) plus, per probe, the seeded half and the bit
+    test (seed xor, rotate, multiply-add, length xor, three xor-shifts, two
+    multiplies, the range multiply, shift and mask: 16 ops).  A non-member
+    is probed until its first clear bit, (1 - f^k)/(1 - f) probes for filter
+    fill f; a positive takes k probes."""
+    probes_nonmember = (1 - fill**k) / (1 - fill) if fill < 1 else k
+    query_ops = d * 3 + (d - n_val) * 16 * probes_nonmember + n_val * 16 * k
+    return {
+        "k_topr_hist": ("hbm", 4.0 * d),
+        "k_select_filter": ("hbm", 4.0 * d + d / 8.0),
+        "k_query<Q_DECODE>": ("hbm", 4.0 * d + payload_bytes),
+        "k_query<Q_ENCODE>": ("alu", query_ops),
+        "k_query<Q_DECODE>:alu": ("alu", query_ops),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="resnet50_25m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=30.0, help="bound on the oracle's CPU time")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this codec benchmark runs on one GPU; --gpus must be 1 (the exchange of "
+                                   "payloads between GPUs is not part of this build)"}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2102_03112_amd import binding as B
+    from paper_2102_03112_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    B.lib()  # fail loudly if the HIP library is missing
+    w = W.WORKLOADS[args.workload]
+    d = w.d
+    log(f"bench: workload {w.name} d={d} tensors={w.n_tensors}")
+    t0 = time.time()
+    g_host = W.generate(w)
+    log(f"bench: generated input in {time.time() - t0:.1f}s sha256={W.sha256(g_host)[:16]}")
+
+    cfg = B.Config.from_workload(w)
+    total, rec_off = B.payload_layout(cfg)
+    n_copies = max(1, min(64, math.ceil(3 * MALL_BYTES / max(1, 4 * d)))) if 4 * d < 2 * MALL_BYTES else 1
+    g_dev = [torch.from_numpy(g_host).cuda()]
+    for _ in range(n_copies - 1):
+        g_dev.append(g_dev[0].clone())
+    payload = torch.zeros(total, dtype=torch.uint8, device="cuda")
+    dense = torch.empty(d, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4 * w.n_tensors, dtype=torch.int64, device="cuda")
+    ws = B.workspace(d, w.n_tensors)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        B.roundtrip(g_dev[i % n_copies], cfg, payload, dense, None, None, counts, ws, stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    log(f"bench: {args.steps} steps, {ms:.4f} ms/step (wall {1e3 * wall / args.steps:.4f} ms/step)")
+
+    # payload accounting from the records
+    pay = payload.cpu().numpy()
+    cnt = counts.cpu().numpy().reshape(w.n_tensors, 4)
+    flags = int(np.bitwise_or.reduce(cnt[:, 3])) if w.n_tensors else 0
+    used = idx_bits = val_bits = sig_bits = 0
+    fills = []
+    n_sel = n_val = 0
+    kk = 0
+    for t in range(w.n_tensors):
+        rec = B.parse_record(pay, rec_off[t])
+        used += rec.rec_bytes
+        idx_bits += rec.m_bits
+        val_bits += 32 * rec.seg_eff * (rec.deg_eff + 1)
+        sig_bits += rec.n_values * rec.sigma_b
+        n_sel += rec.n_selected
+        n_val += rec.n_values
+        kk = rec.k
+        fills.append(float(np.unpackbits(rec.bits.view(np.uint8)).mean()))
+    fill = float(np.mean(fills)) if fills else 0.0
+    b_alg = 4.0 * d + 2.0 * used + 4.0 * d
+    value = d / (ms * 1e-3) / 1e9
+
+    # per-kernel durations from HIP events on the library's stream
+    B.trace_begin(stream)
+    for i in range(args.steps):
+        step(i)
+    tr = B.trace_end()
+    kern = {name: (cnt_, tot / cnt_) for name, (cnt_, tot) in tr.items()}  # avg ms per launch
+    per_step = {name: tot / args.steps for name, (cnt_, tot) in tr.items()}
+    dom = max(per_step, key=per_step.get)
+    models = kernel_models(d, used, n_sel, n_val, kk, fill)
+    roof = None
+    if dom in models:
+        bound, work = models[dom]
+        avg_s = kern[dom][1] * 1e-3
+        if bound == "hbm":
+            ach = work / avg_s / 1e9
+            roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9,
+                    "unit": "GB/s", "frac": round(ach / (HBM_PEAK / 1e9), 4), "traffic": None}
+        else:
+            ach = work / avg_s / 1e9
+            roof = {"kernel": dom, "bound": "alu", "achieved": round(ach, 1), "peak": INT_PEAK / 1e9,
+                    "unit": "Gop/s", "frac": round(ach / (INT_PEAK / 1e9), 4), "traffic": None}
+    else:
+        roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
+                "traffic": None}
+    log("bench: kernel ms per step: " + ", ".join(f"{k}={v:.4f}" for k, v in sorted(per_step.items(),
+                                                                                      key=lambda x: -x[1])))
+
+    # CPU oracle baseline on one host core
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        # a prefix of the gradient with the same per-tensor settings, sized so
+        # the oracle (about 3 Melem/s on one core) stays within the budget
+        elems = min(d, int(args.cpu_budget_s * 2.5e6))
+        off = [o for o in w.offsets() if o < elems] + [elems]
+        t0 = time.perf_counter()
+        oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, w.n_seg)
+        tc = time.perf_counter() - t0
+        sample = "full workload" if elems == d else f"first {elems} elements ({len(off) - 1} tensors) of the workload"
+        cpu = {"value": round(elems / tc / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
+               "sample": f"{sample}, 1 round trip, {tc:.2f} s", "cpu": _cpu_model()}
+        log(f"bench: oracle {elems} elements in {tc:.2f}s")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 4),
+        "unit": "Gelem/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "d": d, "tensors": w.n_tensors,
+                   "ratio": None if w.ratio is None else f"{w.ratio[0]}/{w.ratio[1]}", "fpr": w.fpr,
+                   "degree": w.degree, "n_seg": w.n_seg, "input_copies": n_copies},
+        "hbm_frac": round(b_alg / (ms * 1e-3) / HBM_PEAK, 4),
+        "bytes_alg": int(b_alg),
+        "bits_per_elem": round(8.0 * used / d, 4),
+        "bits_split": {"index": round(idx_bits / d, 4), "values": round(val_bits / d, 6),
+                       "sigma": round(sig_bits / d, 4)},
+        "selected": n_sel,
+        "positives": n_val,
+        "flags": flags,
+        "roofline": roof,
+        "kernels_ms_per_step": {k: round(v, 5) for k, v in per_step.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip() + f" ({os.cpu_count()} threads visible)"
+    except OSError:
+        pass
+    return None
+
+
+if __name__ == "__main__":
+    main()

@@ -210,6 +210,24 @@ DR_EXPORT dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t
                        float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------------- */
+/* Per-kernel timing (the paper reports encode/decode wall time, Section   */
+/* 6.4; this breaks it down by kernel)                                     */
+/* ---------------------------------------------------------------------- */
+
+/* Start timing on the calling host thread: an event is recorded on `stream`
+ * now, at the start of every later entry point, and after every kernel the
+ * library launches from this thread, until dr_trace_end.  Events add a few
+ * microseconds per kernel; time the codec itself with tracing off.
+ * EINVAL if tracing is already on for this thread. */
+DR_EXPORT dr_status dr_trace_begin(void *stream);
+
+/* Stop timing, wait for the recorded events, and write one line per kernel
+ * name into buf_h (NUL-terminated, truncated to buf_bytes): "<kernel>
+ * <launches> <total milliseconds>\n".  Idle time between entry points is
+ * not attributed to any kernel.  EINVAL if tracing was not begun. */
+DR_EXPORT dr_status dr_trace_end(char *buf_h, size_t buf_bytes);
+
 #ifdef __cplusplus
 }
 #endif

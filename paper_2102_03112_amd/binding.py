@@ -27,7 +27,7 @@ HEADER_MAGIC = 0x31435244
 EXPORTS = [
     "dr_bloom_params", "dr_sigma_bits", "dr_workspace_bytes", "dr_last_error", "dr_sparsify_topr",
     "dr_bloom_encode", "dr_bloom_decode", "dr_curvefit_encode", "dr_curvefit_decode", "dr_payload_layout",
-    "dr_payload_encode", "dr_payload_decode", "dr_roundtrip",
+    "dr_payload_encode", "dr_payload_decode", "dr_roundtrip", "dr_trace_begin", "dr_trace_end",
 ]
 
 
@@ -76,6 +76,8 @@ def lib():
         "dr_payload_encode": (st, [vp, cfgp, vp, sz, vp, vp, sz, vp]),
         "dr_payload_decode": (st, [vp, cfgp, vp, vp, vp, vp, vp, sz, vp]),
         "dr_roundtrip": (st, [vp, cfgp, vp, sz, vp, vp, vp, vp, vp, sz, vp]),
+        "dr_trace_begin": (st, [vp]),
+        "dr_trace_end": (st, [ctypes.c_char_p, sz]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -213,6 +215,21 @@ def roundtrip(g, cfg: Config, payload, dense_out, idx_out, val_out, counts_out, 
     _check("dr_roundtrip", lib().dr_roundtrip(
         _ptr(g), ctypes.byref(cfg.c), _ptr(payload), payload.numel(), _ptr(dense_out), _ptr(idx_out),
         _ptr(val_out), _ptr(counts_out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def trace_begin(stream=None):
+    _check("dr_trace_begin", lib().dr_trace_begin(_stream(stream)))
+
+
+def trace_end() -> dict:
+    """{kernel: (launches, total_ms)} for the kernels launched since trace_begin."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    _check("dr_trace_end", lib().dr_trace_end(buf, len(buf)))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.rsplit(" ", 2)
+        out[name] = (int(cnt), float(ms))
+    return out
 
 
 # ---------------------------------------------------------------------------

@@ -19,6 +19,8 @@ namespace {
 
 thread_local std::string g_err;
 
+void trace_call(hipStream_t s);  // per-kernel timing, defined below
+
 dr_status fail(dr_status st, const char *fmt, ...) {
     char buf[512];
     va_list ap;
@@ -39,7 +41,7 @@ dr_status hip_fail(hipError_t e, const char *where) {
         if (e_ != hipSuccess) return hip_fail(e_, #call);  \
     } while (0)
 
-constexpr uint32_t MAX_SLICES = 16384;  // 2^30-bit filters: LDS counters of the insert
+constexpr uint32_t MAX_SLICES = 16384;  // LDS counters of the insert: filters up to 2^30 bits
 constexpr uint32_t POS_PER_ELEM = 12;   // Bloom positions the workspace holds per padded element
 
 uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
@@ -84,10 +86,10 @@ int persist_grid(int per_cu) {
 // entries (padded elements); the last six are contiguous so the Bloom insert
 // can borrow them for its position buffer before the value path needs them.
 struct Carve {
-    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0;
+    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0;
     size_t bytes = 0;
-    size_t o_td, o_glob, o_tickets, o_done, o_lb, o_hpart, o_hist, o_sel, o_ckey, o_cidx, o_S, o_P, o_V, o_shist,
-        o_fit, o_btab, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
+    size_t o_td, o_glob, o_done, o_histA, o_fitdone, o_tcnt, o_toff, o_ccnt, o_hpart, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
+        o_V, o_shist, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
 
     void plan() {
         size_t at = 0;
@@ -98,12 +100,15 @@ struct Carve {
         };
         o_td = take(sizeof(TDesc) * ntensors);
         o_glob = take(sizeof(Glob));
-        o_tickets = take(64);
         o_done = take(4 * ntensors);
-        o_lb = take(4 * 8 * ntiles);
+        o_tcnt = take(4 * ntiles);
+        o_toff = take(4 * ntiles);
+        o_ccnt = take(4 * ntiles);
         o_hpart = take(4ull * HIST1_BINS * hist_blocks);
         o_hist = take(4ull * HIST1_BINS * ntensors);
+        o_histA = take(4ull * 1024 * hist_blocks);
         o_sel = take(slots / 8);
+        o_pbits = take(slots / 8);
         o_ckey = take(4 * slots);
         o_cidx = take(4 * slots);
         o_S = take(4 * slots);
@@ -111,7 +116,9 @@ struct Carve {
         o_V = take(4 * slots);
         o_shist = take(4ull * SORT_BINS * ntiles);
         o_fit = take(8ull * NMOM * fit_blocks);
+        o_fitdone = take(4ull * (fit_blocks / FIT_CHUNKS + 1));
         o_btab = take(4 * btab);
+        o_brow = take(8 * bslices);
         o_keyA = take(4 * slots);
         o_keyB = take(4 * slots);
         o_valA = take(4 * slots);
@@ -128,24 +135,29 @@ struct Carve {
         w.ntensors = (uint32_t)ntensors;
         w.ntiles_total = (uint32_t)ntiles;
         w.slots = slots;
-        w.tickets = (uint32_t *)(ws + o_tickets);
         w.done = (uint32_t *)(ws + o_done);
-        unsigned long long *lb = (unsigned long long *)(ws + o_lb);
-        w.lb0 = lb;
-        w.lb1 = lb + ntiles;
-        w.lb2 = lb + 2 * ntiles;
-        w.lb3 = lb + 3 * ntiles;
+        w.tcnt = (uint32_t *)(ws + o_tcnt);
+        w.toff = (uint32_t *)(ws + o_toff);
+        w.ccnt = (uint32_t *)(ws + o_ccnt);
+        w.pbits = (uint32_t *)(ws + o_pbits);
         w.hist_part = (uint32_t *)(ws + o_hpart);
         w.hist = (uint32_t *)(ws + o_hist);
         w.selbits = (uint32_t *)(ws + o_sel);
         w.cand_key = (uint32_t *)(ws + o_ckey);
         w.cand_idx = (uint32_t *)(ws + o_cidx);
+        w.histA_part = (uint32_t *)(ws + o_histA);
         w.S = (uint32_t *)(ws + o_S);
         w.P = (uint32_t *)(ws + o_P);
         w.V = (float *)(ws + o_V);
+        w.sub_key = (uint32_t *)(ws + o_P);  // short list of the top-r select, before P exists
+        w.sub_idx = (uint32_t *)(ws + o_V);
         w.shist = (uint32_t *)(ws + o_shist);
         w.fit_part = (double *)(ws + o_fit);
+        w.fit_done = (uint32_t *)(ws + o_fitdone);
+        w.fit_runs = (uint32_t)(fit_blocks / FIT_CHUNKS);
         w.btab = (uint32_t *)(ws + o_btab);
+        w.brow = (uint32_t *)(ws + o_brow);
+        w.bslices = (uint32_t)bslices;
         w.keyA = (uint32_t *)(ws + o_keyA);
         w.keyB = (uint32_t *)(ws + o_keyB);
         w.valA = (uint32_t *)(ws + o_valA);
@@ -159,19 +171,25 @@ struct Carve {
     uint64_t pos_capacity() const { return (o_vs + 4 * slots - o_keyA) / 2; }
 };
 
+// Tiles per top-r histogram block (1024 threads): about 256 blocks over the
+// whole gradient, at least 16 tiles each (each block writes a partial
+// histogram, so fewer blocks mean less to reduce).
+uint64_t hist_tiles_per_block(uint64_t all_tiles) { return std::max<uint64_t>(16, ceil_div(all_tiles, 256)); }
+
 // Generic bound used by dr_workspace_bytes: one fit block per element at most.
 Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     Carve c;
     c.ntensors = n_tensors;
     c.ntiles = ceil_div(d, TILE) + n_tensors;
     c.slots = c.ntiles * TILE;
-    c.hist_blocks = c.ntiles / 8 + 2 * n_tensors;
+    c.hist_blocks = c.ntiles / 16 + 2 * n_tensors;
     const uint64_t runs = n_tensors * (uint64_t)DR_MAX_SEGMENTS;
     c.fit_blocks = (runs < d + n_tensors ? runs : d + n_tensors) * FIT_CHUNKS;
-    // Bloom table: per tensor (slices x chunks) with chunks <= 257 and
+    // Bloom table: per tensor (slices x chunks) with chunks <= max(257, tiles/16 + 1) and
     // m <= 2 k n <= 2 POS_PER_ELEM slots bits; plus one filter of MAX_SLICES
     // for a standalone insert whose filter is larger than its item count
-    c.btab = (2 * c.slots * POS_PER_ELEM / SLICE_BITS + 2 * n_tensors) * 257 + 257ull * MAX_SLICES;
+    c.bslices = 2 * c.slots * POS_PER_ELEM / (1u << 14) + 2 * n_tensors + MAX_SLICES;
+    c.btab = c.bslices * (257 + c.ntiles / CHUNK_TILES);
     c.plan();
     return c;
 }
@@ -186,17 +204,28 @@ struct Plan {
 };
 
 // Per-tensor Bloom insert layout for at most n_cap items and m_cap_bits.
-void plan_bloom(TInit &in, uint64_t n_cap, uint64_t m_cap_bits, Plan &p) {
+// From the bitmap, a chunk is CHUNK_TILES tiles of it; from a list, a chunk
+// is bl_chunk items.
+
+void plan_bloom(TInit &in, uint64_t n_cap, uint64_t m_cap_bits, bool from_bitmap, Plan &p) {
     p.bl_ncap.push_back(n_cap);
-    const uint64_t chunk = n_cap / 256 > 1024 ? ceil_div(n_cap, 256) : 1024;
-    in.bl_chunk = (uint32_t)chunk;
-    in.bl_nchunks = (uint32_t)(n_cap ? ceil_div(n_cap, chunk) : 0);
-    in.bl_nslices = (uint32_t)ceil_div(m_cap_bits, SLICE_BITS);
+    if (from_bitmap) {
+        in.bl_chunk = 0;
+        in.bl_nchunks = (uint32_t)ceil_div(in.ntiles, CHUNK_TILES);
+    } else {
+        const uint64_t chunk = n_cap / 256 > 1024 ? ceil_div(n_cap, 256) : 1024;
+        in.bl_chunk = (uint32_t)chunk;
+        in.bl_nchunks = (uint32_t)(n_cap ? ceil_div(n_cap, chunk) : 0);
+    }
+    // smaller slices give the fill more blocks; large filters need 2^16-bit slices
+    in.slice_log2 = ceil_div(m_cap_bits, 1u << 14) <= MAX_SLICES ? 14 : SLICE_LOG2_MAX;
+    in.bl_nslices = (uint32_t)ceil_div(m_cap_bits, 1ull << in.slice_log2);
     in.bl_chunk0 = p.bl_chunks;
     in.bl_slice0 = p.bl_slices;
     in.bl_tab0 = p.carve.btab;
     p.bl_chunks += in.bl_nchunks;
     p.bl_slices += in.bl_nslices;
+    p.carve.bslices += in.bl_nslices;
     p.carve.btab += (uint64_t)in.bl_nchunks * in.bl_nslices;
     p.bl_items += n_cap;
     if (in.bl_nslices > p.max_slices) p.max_slices = in.bl_nslices;
@@ -215,6 +244,7 @@ void plan_bloom_rounds(Plan &p, uint32_t k) {
     uint64_t at = 0;
     for (size_t i = 0; i < p.t.size(); ++i) {
         p.t[i].bl_pos0 = at;
+        p.t[i].bl_poscap = p.bl_ncap[i] * h;
         at += p.bl_ncap[i] * h;
     }
 }
@@ -262,6 +292,12 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     rec_off.assign(T + 1, 0);
     uint64_t tiles = 0, hist_blocks = 0, fit_blocks = 0;
     p.carve = Carve();
+    uint64_t all_tiles = 0;
+    for (uint64_t t = 0; t < T; ++t) {
+        const uint64_t d = cfg->offsets_h[t + 1] - cfg->offsets_h[t];
+        all_tiles += d ? ceil_div(d, TILE) : 1;
+    }
+    const uint64_t ht = hist_tiles_per_block(all_tiles);
     for (uint64_t t = 0; t < T; ++t) {
         TInit &in = p.t[t];
         memset(&in, 0, sizeof in);
@@ -273,7 +309,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         if (!bloom_params_host(n_cap, cfg->fpr, &m_cap, &kk))
             return fail(DR_ENOTSUP, "tensor %llu: filter of %llu items needs 2^32 bits or more",
                         (unsigned long long)t, (unsigned long long)n_cap);
-        if (ceil_div(m_cap, SLICE_BITS) > MAX_SLICES)
+        if (ceil_div(m_cap, 1ull << SLICE_LOG2_MAX) > MAX_SLICES)
             return fail(DR_ENOTSUP, "tensor %llu: filter larger than 2^30 bits", (unsigned long long)t);
         in.off = cfg->offsets_h[t];
         in.d = (uint32_t)d;
@@ -285,13 +321,13 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.k = kk;
         in.degree = cfg->degree;
         in.nseg = cfg->n_seg;
-        in.m_words_in = 0;
         in.mC = mC;
+        // top-r: |S| = r is known, so the filter size is too
+        in.m_words_in = nz ? 0u : (uint32_t)(m_cap / 32);
         const uint64_t runs_cap = std::min<uint64_t>(cfg->n_seg, std::max<uint64_t>(1, d / (cfg->degree + 1)));
         in.fit_blk0 = (uint32_t)fit_blocks;
         fit_blocks += runs_cap * FIT_CHUNKS;
         if (!nz) {
-            const uint64_t ht = std::max<uint64_t>(8, ceil_div(in.ntiles, 512));
             in.hb0 = (uint32_t)hist_blocks;
             in.hbn = (uint32_t)ceil_div(in.ntiles, ht);
             hist_blocks += in.hbn;
@@ -299,7 +335,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
             in.hb0 = (uint32_t)hist_blocks;
             in.hbn = 0;
         }
-        plan_bloom(in, n_cap, m_cap, p);
+        plan_bloom(in, n_cap, m_cap, true, p);
         rec_off[t + 1] = rec_off[t] + align_up(record_capacity(d, n_cap, cfg->fpr, cfg->degree, cfg->n_seg), 256);
     }
     p.any_topr = !nz;
@@ -313,28 +349,25 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     return DR_OK;
 }
 
+// descriptors (chunks of INIT_CHUNK tensors) and the per-call state cleared
 hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s) {
+    ZeroArgs z;
+    memset(&z, 0, sizeof z);
+    z.z[0] = {w.done, w.ntensors};
+    z.z[1] = {w.glob, sizeof(Glob) / 4};
+    z.z[2] = {w.fit_done, w.fit_runs};
+    z.n = 3;
     for (size_t f = 0; f < t.size(); f += INIT_CHUNK) {
         InitArgs a;
         memset(&a, 0, sizeof a);
         a.first = (uint32_t)f;
         a.count = (uint32_t)std::min<size_t>(INIT_CHUNK, t.size() - f);
         for (uint32_t i = 0; i < a.count; ++i) a.t[i] = t[f + i];
-        hipError_t e = launch_init(w, a, s);
+        hipError_t e = launch_init(w, a, z, s);
         if (e != hipSuccess) return e;
+        z.n = 0;  // cleared once
     }
     return hipSuccess;
-}
-
-hipError_t run_zero_state(const Work &w, hipStream_t s) {
-    ZeroArgs z;
-    memset(&z, 0, sizeof z);
-    z.z[0] = {w.tickets, 16};
-    z.z[1] = {w.done, w.ntensors};
-    z.z[2] = {w.lb0, 4ull * 2 * w.ntiles_total};
-    z.z[3] = {w.glob, sizeof(Glob) / 4};
-    z.n = 4;
-    return launch_zero(z, s);
 }
 
 bool ws_ok(void *ws, size_t ws_bytes, size_t need) {
@@ -360,21 +393,18 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
         p.t[t].sigma = nullptr;
     }
     const Work w = p.carve.view((uint8_t *)ws);
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(run_zero_state(w, s));
     if (p.any_topr)
         DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
     else
         DR_HIP(launch_nonzero(w, g, persist_grid(8), s));
-    DR_HIP(launch_compact_selection(w, g, nullptr, persist_grid(8), s));
-    DR_HIP(launch_params(w, s));
-    DR_HIP(launch_bloom_insert(w, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
+    DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
     DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
-    DR_HIP(launch_value_setup(w, true, s));
+    DR_HIP(launch_value_setup(w, true, counts_out, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, persist_grid(4), s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
-    if (counts_out) DR_HIP(launch_counts(w, counts_out, 0, s));
     return DR_OK;
 }
 
@@ -395,10 +425,9 @@ dr_status decode_impl(const uint8_t *payload, const dr_config *cfg, float *dense
         p.t[t].bits = nullptr;
     }
     const Work w = p.carve.view((uint8_t *)ws);
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(run_zero_state(w, s));
-    DR_HIP(launch_query_decode(w, payload, dense_out, idx_out, val_out, persist_grid(4), s));
-    if (counts_out) DR_HIP(launch_counts(w, counts_out, 1, s));
+    DR_HIP(launch_query_decode(w, payload, dense_out, idx_out, val_out, counts_out, persist_grid(4), s));
     return DR_OK;
 }
 
@@ -418,7 +447,44 @@ Plan single_plan(uint64_t d) {
     return p;
 }
 
+// ---------------------------------------------------------------------------
+// Opt-in per-kernel timing
+// ---------------------------------------------------------------------------
+struct TraceMark {
+    const char *name;  // null: boundary at the start of an entry point (its interval is idle time)
+    hipEvent_t ev;
+};
+struct Tracer {
+    bool on = false;
+    std::vector<TraceMark> marks;
+    std::vector<hipEvent_t> pool;
+};
+thread_local Tracer g_trace;
+
+void trace_record(hipStream_t s, const char *name) {
+    if (!g_trace.on) return;
+    hipEvent_t ev;
+    if (!g_trace.pool.empty()) {
+        ev = g_trace.pool.back();
+        g_trace.pool.pop_back();
+    } else if (hipEventCreate(&ev) != hipSuccess) {
+        return;
+    }
+    if (hipEventRecord(ev, s) != hipSuccess) {
+        g_trace.pool.push_back(ev);
+        return;
+    }
+    g_trace.marks.push_back({name, ev});
+}
+
+// every entry point that launches work marks its start
+void trace_call(hipStream_t s) { trace_record(s, nullptr); }
+
 }  // namespace
+
+namespace dr {
+void trace_mark(hipStream_t s, const char *kernel) { trace_record(s, kernel); }
+}  // namespace dr
 
 // ---------------------------------------------------------------------------
 // C ABI
@@ -426,6 +492,55 @@ Plan single_plan(uint64_t d) {
 extern "C" {
 
 const char *dr_last_error(void) { return g_err.c_str(); }
+
+dr_status dr_trace_begin(void *stream) {
+    if (g_trace.on) return fail(DR_EINVAL, "tracing already begun on this thread");
+    g_trace.on = true;
+    g_trace.marks.clear();
+    trace_record((hipStream_t)stream, nullptr);
+    return DR_OK;
+}
+
+dr_status dr_trace_end(char *buf_h, size_t buf_bytes) {
+    if (!g_trace.on) return fail(DR_EINVAL, "tracing was not begun on this thread");
+    g_trace.on = false;
+    std::vector<std::string> names;
+    std::vector<double> total;
+    std::vector<uint64_t> count;
+    dr_status st = DR_OK;
+    if (!g_trace.marks.empty()) {
+        hipError_t e = hipEventSynchronize(g_trace.marks.back().ev);
+        if (e != hipSuccess) st = hip_fail(e, "hipEventSynchronize");
+    }
+    for (size_t i = 1; st == DR_OK && i < g_trace.marks.size(); ++i) {
+        if (!g_trace.marks[i].name) continue;
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, g_trace.marks[i - 1].ev, g_trace.marks[i].ev) != hipSuccess) continue;
+        size_t j = 0;
+        while (j < names.size() && names[j] != g_trace.marks[i].name) ++j;
+        if (j == names.size()) {
+            names.push_back(g_trace.marks[i].name);
+            total.push_back(0.0);
+            count.push_back(0);
+        }
+        total[j] += ms;
+        count[j] += 1;
+    }
+    for (const TraceMark &m : g_trace.marks) g_trace.pool.push_back(m.ev);
+    g_trace.marks.clear();
+    std::string out;
+    char line[256];
+    for (size_t j = 0; j < names.size(); ++j) {
+        snprintf(line, sizeof line, "%s %llu %.6f\n", names[j].c_str(), (unsigned long long)count[j], total[j]);
+        out += line;
+    }
+    if (buf_h && buf_bytes) {
+        const size_t n = std::min(out.size(), buf_bytes - 1);
+        memcpy(buf_h, out.data(), n);
+        buf_h[n] = 0;
+    }
+    return st;
+}
 
 dr_status dr_bloom_params(uint64_t n_items, double fpr, uint64_t *m_bits_h, uint32_t *k_h) {
     if (!m_bits_h || !k_h) return fail(DR_EINVAL, "null output pointer");
@@ -478,7 +593,7 @@ dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx
     TInit &in = p.t[0];
     in.r = nz ? R_NONZERO : (uint32_t)r;
     if (!nz) {
-        const uint64_t ht = std::max<uint64_t>(8, ceil_div(in.ntiles, 512));
+        const uint64_t ht = hist_tiles_per_block(in.ntiles);
         in.hb0 = 0;
         in.hbn = (uint32_t)ceil_div(in.ntiles, ht);
         p.carve.hist_blocks = in.hbn;
@@ -488,8 +603,8 @@ dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx
         return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
     Work w = p.carve.view((uint8_t *)ws);
     w.S = idx_out;  // single tensor: slot 0 is the caller's list
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(run_zero_state(w, s));
     if (!nz)
         DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
     else
@@ -506,24 +621,23 @@ dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap
     if (m_bits < 32 || (m_bits & 31) || m_bits >= (1ull << 32)) return fail(DR_EINVAL, "bad m_bits");
     if (k < 1 || k > 32) return fail(DR_EINVAL, "k must be in [1, 32]");
     if (n_cap >= (1ull << 32)) return fail(DR_EINVAL, "n_cap >= 2^32");
-    if (ceil_div(m_bits, SLICE_BITS) > MAX_SLICES) return fail(DR_ENOTSUP, "filter larger than 2^30 bits");
+    if (ceil_div(m_bits, 1ull << SLICE_LOG2_MAX) > MAX_SLICES) return fail(DR_ENOTSUP, "filter larger than 2^30 bits");
     Plan p = single_plan(n_cap);
     TInit &in = p.t[0];
     in.k = k;
     in.m_words_in = (uint32_t)(m_bits / 32);
     in.bits = bits_out;
-    plan_bloom(in, n_cap, m_bits, p);
+    plan_bloom(in, n_cap, m_bits, false, p);
     p.carve.plan();
     plan_bloom_rounds(p, k);
     if (!ws_ok(ws, ws_bytes, p.carve.bytes))
         return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
     Work w = p.carve.view((uint8_t *)ws);
     w.S = const_cast<uint32_t *>(idx);
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(run_zero_state(w, s));
     DR_HIP(launch_import_n(w, n, n_cap, s));
-    DR_HIP(launch_params(w, s));
-    DR_HIP(launch_bloom_insert(w, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
+    DR_HIP(launch_bloom_insert(w, false, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
     return DR_OK;
 }
 
@@ -543,9 +657,8 @@ dr_status dr_bloom_decode(const uint32_t *bits, uint64_t m_bits, uint32_t k, uin
     if (!ws_ok(ws, ws_bytes, p.carve.bytes))
         return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
     const Work w = p.carve.view((uint8_t *)ws);
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(run_zero_state(w, s));
-    DR_HIP(launch_params(w, s));
     DR_HIP(launch_query_plain(w, idx_out, cap, n_out, persist_grid(4), s));
     return DR_OK;
 }
@@ -570,10 +683,10 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
     if (!ws_ok(ws, ws_bytes, p.carve.bytes))
         return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
     const Work w = p.carve.view((uint8_t *)ws);
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(run_zero_state(w, s));
     DR_HIP(launch_keygen(w, vals, n, n_cap, persist_grid(4), s));
-    DR_HIP(launch_value_setup(w, false, s));
+    DR_HIP(launch_value_setup(w, false, nullptr, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, persist_grid(4), s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
@@ -596,6 +709,7 @@ dr_status dr_curvefit_decode(const float *coef, const uint32_t *sigma, const uin
     if (!ws_ok(ws, ws_bytes, p.carve.bytes))
         return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
     const Work w = p.carve.view((uint8_t *)ws);
+    trace_call(s);
     DR_HIP(run_init(w, p.t, s));
     DR_HIP(launch_curvefit_decode(w, coef, sigma, n, n_cap, vals_out, persist_grid(4), s));
     return DR_OK;

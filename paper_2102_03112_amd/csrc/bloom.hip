@@ -21,6 +21,10 @@ namespace dr {
 // ---------------------------------------------------------------------------
 // Insert
 // ---------------------------------------------------------------------------
+// The items come either from the selection bitmap (the round trip: chunk c
+// of a tensor is its bitmap tiles [c * CHUNK_TILES, (c+1) * CHUNK_TILES))
+// or from a list of indices (chunk c is items [c * bl_chunk, ...)).
+
 __device__ __forceinline__ uint32_t tensor_of_chunk(const Work &w, uint32_t c) {
     uint32_t lo = 0, hi = w.ntensors;
     while (hi - lo > 1) {
@@ -45,140 +49,195 @@ __device__ __forceinline__ uint32_t tensor_of_slice(const Work &w, uint32_t s) {
     return lo;
 }
 
-// items of chunk c of tensor td: [c * chunk, min(n, (c+1) * chunk))
+// Calls f(index) for every item of chunk c of tensor td (block-strided).
+template <bool FROM_BITMAP, typename F>
+__device__ __forceinline__ void for_chunk_items(const Work &w, const TDesc &td, uint32_t c, F f) {
+    if (FROM_BITMAP) {
+        const uint32_t w0 = c * CHUNK_TILES * TILE_WORDS;
+        const uint32_t w1 = min(td.in.ntiles * TILE_WORDS, w0 + CHUNK_TILES * TILE_WORDS);
+        const uint32_t *sb = w.selbits + (td.in.slot >> 5);
+        for (uint32_t x = w0 + threadIdx.x; x < w1; x += NTHREADS) {
+            uint32_t word = sb[x];
+            while (word) {
+                const uint32_t b = __ffs(word) - 1;
+                word &= word - 1;
+                f(x * 32u + b);
+            }
+        }
+    } else {
+        const uint32_t n = td.n, chunk = td.in.bl_chunk;
+        const uint32_t q0 = c * chunk, q1 = min(n, q0 + chunk);
+        const uint32_t *S = w.S + td.in.slot;
+        for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) f(S[q]);
+    }
+}
+
+__device__ __forceinline__ uint32_t active_chunks(const TDesc &td, bool from_bitmap) {
+    if (from_bitmap) return td.in.bl_nchunks;
+    return (td.n + td.in.bl_chunk - 1) / td.in.bl_chunk;
+}
+
+template <bool FROM_BITMAP>
 __global__ __launch_bounds__(NTHREADS) void k_bloom_count(Work w, uint32_t j0, uint32_t j1) {
     extern __shared__ uint32_t lh[];
     const uint32_t t = tensor_of_chunk(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t c = blockIdx.x - td.in.bl_chunk0;
-    if (c >= td.in.bl_nchunks) return;
-    const uint32_t n = td.n, chunk = td.in.bl_chunk;
-    const uint32_t nact = (n + chunk - 1) / chunk;
-    if (c >= nact) return;
+    if (c >= td.in.bl_nchunks || c >= active_chunks(td, FROM_BITMAP)) return;
     const uint32_t m_bits = td.m_words * 32u;
-    const uint32_t nsl = (m_bits + SLICE_BITS - 1) >> SLICE_LOG2;
+    const uint32_t sl2 = td.in.slice_log2;
+    const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
     for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) lh[s] = 0;
     __syncthreads();
-    const uint32_t q0 = c * chunk, q1 = min(n, q0 + chunk);
-    const uint32_t *S = w.S + td.in.slot;
     const uint32_t je = min(j1, td.in.k);
-    if (je <= j0) return;
-    for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) {
-        const uint32_t km = mm3_key(S[q]);
-        for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[bloom_pos(km, j, m_bits) >> SLICE_LOG2], 1u);
+    if (je > j0) {
+        for_chunk_items<FROM_BITMAP>(w, td, c, [&](uint32_t x) {
+            const uint32_t km = mm3_key(x);
+            for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[bloom_pos(km, j, m_bits) >> sl2], 1u);
+        });
     }
     __syncthreads();
     uint32_t *tab = w.btab + td.in.bl_tab0;
     for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) tab[(uint64_t)s * td.in.bl_nchunks + c] = lh[s];
 }
 
-constexpr uint32_t SCAN_THREADS = 1024;
-
-// per tensor: exclusive scan of the (slice, chunk) counts in slice-major order
-__global__ __launch_bounds__(SCAN_THREADS) void k_bloom_scan(Work w, uint32_t j0, uint32_t j1) {
-    const TDesc &td = w.td[blockIdx.x];
-    __shared__ uint32_t scratch[SCAN_THREADS / 64 + 1];
-    __shared__ uint32_t carry;
-    if (j0 >= td.in.k) return;
-    (void)j1;
-    const uint32_t n = td.n, chunk = td.in.bl_chunk;
-    const uint32_t nact = (n + chunk - 1) / chunk;
-    const uint32_t nsl = (td.m_words * 32u + SLICE_BITS - 1) >> SLICE_LOG2;
-    const uint32_t nch = td.in.bl_nchunks;
-    uint32_t *tab = w.btab + td.in.bl_tab0;
-    const uint64_t total = (uint64_t)nsl * nact;
-    if (threadIdx.x == 0) carry = 0;
-    __syncthreads();
-    for (uint64_t f0 = 0; f0 < total; f0 += SCAN_THREADS) {
-        const uint64_t f = f0 + threadIdx.x;
-        uint64_t a = 0;
-        uint32_t v = 0;
-        if (f < total) {
-            a = (f / nact) * nch + (f % nact);
-            v = tab[a];
-        }
+// Row scan: for slice s of a tensor (one block each), offsets of its chunks
+// within the slice's bucket, and the bucket's size.
+__global__ __launch_bounds__(NTHREADS) void k_bloom_rowscan(Work w, uint32_t j0, int from_bitmap) {
+    __shared__ uint32_t scratch[NWAVES + 1];
+    const uint32_t t = tensor_of_slice(w, blockIdx.x);
+    const TDesc &td = w.td[t];
+    const uint32_t s = blockIdx.x - td.in.bl_slice0;
+    if (s >= td.in.bl_nslices || j0 >= td.in.k) return;
+    const uint32_t sl2 = td.in.slice_log2;
+    const uint32_t nsl = (td.m_words * 32u + (1u << sl2) - 1) >> sl2;
+    if (s >= nsl) return;
+    const uint32_t nact = active_chunks(td, from_bitmap != 0);
+    uint32_t *row = w.btab + td.in.bl_tab0 + (uint64_t)s * td.in.bl_nchunks;
+    uint32_t carry = 0;
+    for (uint32_t c0 = 0; c0 < nact; c0 += NTHREADS) {
+        const uint32_t c = c0 + threadIdx.x;
+        const uint32_t v = c < nact ? row[c] : 0u;
         uint32_t tot;
-        const uint32_t base = carry;
-        const uint32_t ex = block_excl_scan_n<SCAN_THREADS>(v, scratch, &tot);
-        if (f < total) tab[a] = base + ex;
-        if (threadIdx.x == 0) carry = base + tot;
-        __syncthreads();
+        const uint32_t ex = block_excl_scan(v, scratch, &tot);
+        if (c < nact) row[c] = carry + ex;
+        carry += tot;
     }
+    if (threadIdx.x == 0) w.brow[blockIdx.x] = carry;
 }
 
+constexpr uint32_t SCAN_THREADS = 1024;
+
+// per tensor: start of each slice's bucket; the end of the last goes to bl_end
+__global__ __launch_bounds__(SCAN_THREADS) void k_bloom_rowbase(Work w, uint32_t j0) {
+    TDesc &td = w.td[blockIdx.x];
+    if (j0 >= td.in.k) return;
+    __shared__ uint32_t scratch[SCAN_THREADS / 64 + 1];
+    const uint32_t sl2 = td.in.slice_log2;
+    const uint32_t nsl = (td.m_words * 32u + (1u << sl2) - 1) >> sl2;
+    const uint32_t *tot = w.brow + td.in.bl_slice0;
+    uint32_t *base = w.brow + w.bslices + td.in.bl_slice0;
+    uint32_t carry = 0;
+    for (uint32_t q0 = 0; q0 < nsl; q0 += SCAN_THREADS) {
+        const uint32_t q = q0 + threadIdx.x;
+        const uint32_t v = q < nsl ? tot[q] : 0u;
+        uint32_t sum;
+        const uint32_t ex = block_excl_scan_n<SCAN_THREADS>(v, scratch, &sum);
+        if (q < nsl) base[q] = carry + ex;
+        carry += sum;
+    }
+    if (threadIdx.x == 0) td.bl_end = carry;
+}
+
+// Scatter: each position goes to its slice's bucket, after the chunk's
+// offset within that bucket.
+template <bool FROM_BITMAP>
 __global__ __launch_bounds__(NTHREADS) void k_bloom_scatter(Work w, uint32_t j0, uint32_t j1) {
     extern __shared__ uint32_t lc[];
     const uint32_t t = tensor_of_chunk(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t c = blockIdx.x - td.in.bl_chunk0;
-    if (c >= td.in.bl_nchunks) return;
-    const uint32_t n = td.n, chunk = td.in.bl_chunk;
-    const uint32_t nact = (n + chunk - 1) / chunk;
-    if (c >= nact) return;
-    const uint32_t m_bits = td.m_words * 32u;
-    const uint32_t nsl = (m_bits + SLICE_BITS - 1) >> SLICE_LOG2;
-    const uint32_t *tab = w.btab + td.in.bl_tab0;
-    for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) lc[s] = tab[(uint64_t)s * td.in.bl_nchunks + c];
-    __syncthreads();
-    const uint32_t q0 = c * chunk, q1 = min(n, q0 + chunk);
-    const uint32_t *S = w.S + td.in.slot;
+    if (c >= td.in.bl_nchunks || c >= active_chunks(td, FROM_BITMAP)) return;
     const uint32_t je = min(j1, td.in.k);
+    if (je <= j0) return;
+    const uint32_t m_bits = td.m_words * 32u;
+    const uint32_t sl2 = td.in.slice_log2;
+    const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
+    const uint32_t *tab = w.btab + td.in.bl_tab0;
+    const uint32_t *base = w.brow + w.bslices + td.in.bl_slice0;
+    for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) lc[s] = base[s] + tab[(uint64_t)s * td.in.bl_nchunks + c];
+    __syncthreads();
     uint16_t *pos = w.bpos + td.in.bl_pos0;
-    for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) {
-        const uint32_t km = mm3_key(S[q]);
+    const uint32_t mask = (1u << sl2) - 1;
+    for_chunk_items<FROM_BITMAP>(w, td, c, [&](uint32_t x) {
+        const uint32_t km = mm3_key(x);
         for (uint32_t j = j0; j < je; ++j) {
             const uint32_t p = bloom_pos(km, j, m_bits);
-            const uint32_t at = atomicAdd(&lc[p >> SLICE_LOG2], 1u);
-            pos[at] = (uint16_t)(p & (SLICE_BITS - 1));
+            const uint32_t at = atomicAdd(&lc[p >> sl2], 1u);
+            if (at < td.in.bl_poscap) pos[at] = (uint16_t)(p & mask);
         }
-    }
+    });
 }
 
 __global__ __launch_bounds__(NTHREADS) void k_bloom_fill(Work w, uint32_t j0, uint32_t j1) {
-    __shared__ uint32_t words[SLICE_WORDS];
+    __shared__ uint32_t words[SLICE_WORDS_MAX];
     const uint32_t t = tensor_of_slice(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t s = blockIdx.x - td.in.bl_slice0;
     if (s >= td.in.bl_nslices) return;
     const uint32_t m_words = td.m_words;
     const uint32_t m_bits = m_words * 32u;
-    const uint32_t nsl = (m_bits + SLICE_BITS - 1) >> SLICE_LOG2;
+    const uint32_t sl2 = td.in.slice_log2;
+    const uint32_t slice_words = (1u << sl2) / 32u;
+    const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
     if (s >= nsl) return;
-    uint32_t *out = td.in.bits + (uint64_t)s * SLICE_WORDS;
-    const uint32_t lim = min(SLICE_WORDS, m_words - s * SLICE_WORDS);
+    uint32_t *out = td.in.bits + (uint64_t)s * slice_words;
+    const uint32_t lim = min(slice_words, m_words - s * slice_words);
     // the first round starts from an empty slice, later rounds add to it
-    for (uint32_t i = threadIdx.x; i < SLICE_WORDS; i += NTHREADS) words[i] = (j0 > 0 && i < lim) ? out[i] : 0u;
+    for (uint32_t i = threadIdx.x; i < slice_words; i += NTHREADS) words[i] = (j0 > 0 && i < lim) ? out[i] : 0u;
     __syncthreads();
     const uint32_t je = min(j1, td.in.k);
-    const uint32_t n = td.n, chunk = td.in.bl_chunk;
-    const uint32_t nact = (n + chunk - 1) / chunk;
-    if (nact > 0 && je > j0) {
-        const uint32_t *tab = w.btab + td.in.bl_tab0;
-        const uint32_t start = tab[(uint64_t)s * td.in.bl_nchunks];
-        const uint32_t end = (s + 1 < nsl) ? tab[(uint64_t)(s + 1) * td.in.bl_nchunks] : n * (je - j0);
+    if (je > j0) {
+        const uint32_t start = w.brow[w.bslices + blockIdx.x];
+        uint32_t end = start + w.brow[blockIdx.x];
+        if (end > td.in.bl_poscap) end = (uint32_t)td.in.bl_poscap;
         const uint16_t *pos = w.bpos + td.in.bl_pos0;
-        for (uint32_t q = start + threadIdx.x; q < end; q += NTHREADS) {
-            const uint32_t p = pos[q];
-            atomicOr(&words[p >> 5], 1u << (p & 31u));
+        if (td.in.bl_nchunks > 0) {
+            for (uint32_t q = start + threadIdx.x; q < end; q += NTHREADS) {
+                const uint32_t p = pos[q];
+                atomicOr(&words[p >> 5], 1u << (p & 31u));
+            }
         }
     }
     __syncthreads();
     for (uint32_t i = threadIdx.x; i < lim; i += NTHREADS) out[i] = words[i];
 }
 
-hipError_t launch_bloom_insert(const Work &w, uint32_t total_chunks, uint32_t total_slices, uint32_t max_slices,
-                               uint32_t hash_per_round, uint32_t kmax, hipStream_t s) {
+hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_chunks, uint32_t total_slices,
+                               uint32_t max_slices, uint32_t hash_per_round, uint32_t kmax, hipStream_t s) {
     // LDS for one counter per slice of the largest filter
     const size_t lds = (size_t)max_slices * 4u;
     uint32_t j0 = 0;
     do {
         const uint32_t j1 = j0 + hash_per_round;
         if (total_chunks) {
-            k_bloom_count<<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
-            k_bloom_scan<<<w.ntensors, SCAN_THREADS, 0, s>>>(w, j0, j1);
-            k_bloom_scatter<<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+            if (from_bitmap)
+                k_bloom_count<true><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+            else
+                k_bloom_count<false><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+            trace_mark(s, "k_bloom_count");
+            k_bloom_rowscan<<<total_slices, NTHREADS, 0, s>>>(w, j0, from_bitmap ? 1 : 0);
+            trace_mark(s, "k_bloom_rowscan");
+            k_bloom_rowbase<<<w.ntensors, SCAN_THREADS, 0, s>>>(w, j0);
+            trace_mark(s, "k_bloom_rowbase");
+            if (from_bitmap)
+                k_bloom_scatter<true><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+            else
+                k_bloom_scatter<false><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+            trace_mark(s, "k_bloom_scatter");
         }
         k_bloom_fill<<<total_slices, NTHREADS, 0, s>>>(w, j0, j1);
+        trace_mark(s, "k_bloom_fill");
         j0 = j1;
     } while (j0 < kmax);
     return hipGetLastError();
@@ -197,6 +256,7 @@ struct QueryOut {
     const uint8_t *payload; // decode: payload base
     float *dense_out;       // decode: dense gradient
     float *val_out;         // decode: optional values
+    uint64_t *counts_out;   // decode: optional per-tensor counts (flags word)
 };
 
 struct RecordView {
@@ -262,19 +322,17 @@ __device__ __forceinline__ float eval_rank(const float *coef, uint32_t rank, uin
 
 constexpr uint32_t QWAVE = 1024;  // indices per wave per tile
 
+// Probe pass: the positives of each tile as a bitmap (pbits) and a count
+// (tcnt).  The sender already knows that its selected indices are
+// positives (S is a subset of P, Section 4), so it skips probing them.
 template <int MODE>
-__global__ __launch_bounds__(NTHREADS) void k_query(Work w, QueryOut o) {
+__global__ __launch_bounds__(NTHREADS) void k_probe(Work w, QueryOut o) {
     __shared__ uint16_t qe[NWAVES][QWAVE];
     __shared__ uint32_t qk[NWAVES][QWAVE];
-    __shared__ float stage[MODE == Q_DECODE ? TILE : 1];
+    __shared__ uint32_t lw[NWAVES][QWAVE / 32];
     __shared__ uint32_t wcount[NWAVES];
-    __shared__ uint32_t tkt, tile_excl;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
-    uint32_t *ticket = &w.tickets[MODE == Q_DECODE ? 3 : 2];
-    unsigned long long *lb = MODE == Q_DECODE ? w.lb3 : w.lb2;
-    for (;;) {
-        const uint32_t tile = next_ticket(ticket, &tkt);
-        if (tile >= w.ntiles_total) break;
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
         const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
         TDesc &td = w.td[t];
         const uint32_t lt = tile - td.in.tile0;
@@ -294,75 +352,125 @@ __global__ __launch_bounds__(NTHREADS) void k_query(Work w, QueryOut o) {
         const uint32_t wbase = lt * TILE + wv * QWAVE;  // first index of this wave
         uint16_t *me = qe[wv];
         uint32_t *mk = qk[wv];
-        // probe 0 over the wave's 1024 indices
-        uint32_t cnt = 0;
+        uint32_t *mw = lw[wv];
+        if (lane < QWAVE / 32) mw[lane] = 0;
+        __builtin_amdgcn_wave_barrier();
+        // probe 0 over the wave's 1024 indices: 16 per lane, all gathers in
+        // flight before any is tested
+        uint32_t cnt = 0, known = 0;
+        uint32_t kmv[QWAVE / 64], wrd[QWAVE / 64], sel[QWAVE / 64];
+#pragma unroll
+        for (uint32_t c = 0; c < QWAVE / 64; ++c) {
+            const uint32_t i = wbase + c * 64 + lane;
+            kmv[c] = mm3_key(i);
+            const uint32_t p = bloom_pos(kmv[c], 0, m_bits);
+            // unconditional loads (p < m_bits, and i stays inside the tensor's
+            // slot), masked afterwards, so the compiler can batch them
+            const uint32_t word = bits[p >> 5] >> (p & 31u);
+            wrd[c] = (i < d && k > 0) ? word : 0u;
+            if (MODE == Q_ENCODE) {
+                const uint32_t sw = w.selbits[(td.in.slot + i) >> 5];
+                sel[c] = i < d ? sw : 0u;
+            }
+        }
+#pragma unroll
         for (uint32_t c = 0; c < QWAVE / 64; ++c) {
             const uint32_t e = c * 64 + lane;
             const uint32_t i = wbase + e;
-            const bool valid = i < d && k > 0;
-            const uint32_t km = mm3_key(i);
-            bool hit = false;
-            if (valid) hit = test_bit(bits, bloom_pos(km, 0, m_bits));
+            bool in_s = false;
+            if (MODE == Q_ENCODE) in_s = (sel[c] >> (i & 31u)) & 1u;
+            const bool hit = !in_s && (wrd[c] & 1u);
+            if (MODE == Q_ENCODE) {
+                const uint64_t sm = ballot(in_s);
+                if (lane < 2) mw[c * 2 + lane] |= (uint32_t)(sm >> (32 * lane));
+                known += popc64(sm);
+            }
             const uint64_t mask = ballot(hit);
             if (hit) {
                 const uint32_t at = cnt + lanes_below(mask);
                 me[at] = (uint16_t)e;
-                mk[at] = km;
+                mk[at] = kmv[c];
             }
             cnt += popc64(mask);
         }
-        // probes 1..k-1 over the survivors, compacting in place
+        // probes 1..k-1 over the survivors, compacting in place; four
+        // groups of 64 queue entries have their gathers in flight together
+        constexpr uint32_t G = 4;
         for (uint32_t j = 1; j < k && cnt > 0; ++j) {
             __builtin_amdgcn_wave_barrier();
             const uint32_t L = cnt;
             cnt = 0;
-            for (uint32_t b0 = 0; b0 < L; b0 += 64) {
-                const uint32_t x = b0 + lane;
-                const bool act = x < L;
-                uint32_t e = 0, km = 0;
-                if (act) {
-                    e = me[x];
-                    km = mk[x];
+            for (uint32_t b0 = 0; b0 < L; b0 += 64 * G) {
+                uint32_t ev[G], kv[G], bw[G];
+#pragma unroll
+                for (uint32_t u = 0; u < G; ++u) {
+                    const uint32_t x = b0 + u * 64 + lane;
+                    ev[u] = x < L ? me[x] : 0u;
+                    kv[u] = x < L ? mk[x] : 0u;
                 }
-                const bool hit = act && test_bit(bits, bloom_pos(km, j, m_bits));
-                const uint64_t mask = ballot(hit);
+#pragma unroll
+                for (uint32_t u = 0; u < G; ++u) {
+                    const uint32_t p = bloom_pos(kv[u], j, m_bits);
+                    const uint32_t word = bits[p >> 5] >> (p & 31u);
+                    bw[u] = (b0 + u * 64 + lane < L) ? word : 0u;
+                }
                 __builtin_amdgcn_wave_barrier();
-                if (hit) {
-                    const uint32_t at = cnt + lanes_below(mask);
-                    me[at] = (uint16_t)e;
-                    mk[at] = km;
+#pragma unroll
+                for (uint32_t u = 0; u < G; ++u) {
+                    const bool hit = bw[u] & 1u;
+                    const uint64_t mask = ballot(hit);
+                    if (hit) {
+                        const uint32_t at = cnt + lanes_below(mask);
+                        me[at] = (uint16_t)ev[u];
+                        mk[at] = kv[u];
+                    }
+                    cnt += popc64(mask);
                 }
-                cnt += popc64(mask);
                 __builtin_amdgcn_wave_barrier();
             }
         }
-        if (lane == 0) wcount[wv] = cnt;
-        if (MODE == Q_DECODE) {
-            for (uint32_t e = threadIdx.x; e < TILE; e += NTHREADS) stage[e] = 0.0f;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t tot = 0;
-            for (uint32_t q = 0; q < NWAVES; ++q) tot += wcount[q];
-            tile_excl = (uint32_t)lookback(lb, tile, td.in.tile0, tot);
-            if (lt == td.in.ntiles - 1) {
-                const uint32_t nv = tile_excl + tot;
-                if (MODE == Q_ENCODE) td.nv = nv;
-                if (MODE == Q_PLAIN) *o.n_out = nv;
-                if (MODE == Q_DECODE) {
-                    td.nv_dec = nv;
-                    if (nv != rv.nv) atomicOr(&td.flags, FLAG_DEC_MISMATCH);
-                }
-            }
-        }
-        __syncthreads();
-        uint32_t wpre = 0;
-        for (uint32_t q = 0; q < wv; ++q) wpre += wcount[q];
-        const uint32_t qbase = tile_excl + wpre;
+        __builtin_amdgcn_wave_barrier();
         for (uint32_t x = lane; x < cnt; x += 64) {
             const uint32_t e = me[x];
-            const uint32_t i = wbase + e;
-            const uint32_t q = qbase + x;
+            atomicOr(&mw[e >> 5], 1u << (e & 31u));
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane < QWAVE / 32) w.pbits[(uint64_t)tile * TILE_WORDS + wv * (QWAVE / 32) + lane] = mw[lane];
+        if (lane == 0) wcount[wv] = cnt + known;
+        __syncthreads();
+        if (threadIdx.x == 0) w.tcnt[tile] = wcount[0] + wcount[1] + wcount[2] + wcount[3];
+        __syncthreads();
+    }
+}
+
+// Emit pass: positives in ascending order at their tensor-wide ranks.
+// Threads 0..127 own one positives word of the tile each.
+template <int MODE>
+__global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
+    __shared__ uint32_t scratch[NWAVES + 1];
+    __shared__ __attribute__((aligned(16))) float stage[MODE == Q_DECODE ? TILE : 4];
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
+        TDesc &td = w.td[t];
+        const uint32_t lt = tile - td.in.tile0;
+        const uint32_t d = td.in.d;
+        RecordView rv;
+        if (MODE == Q_DECODE) {
+            bool ok = true;
+            rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, d, &ok);
+            for (uint32_t e = threadIdx.x; e < TILE; e += NTHREADS) stage[e] = 0.0f;
+
+        }
+        uint32_t word = 0;
+        if (threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
+        uint32_t q = w.toff[tile] + ex;
+        while (word) {
+            const uint32_t b = __ffs(word) - 1;
+            word &= word - 1;
+            const uint32_t e = threadIdx.x * 32u + b;
+            const uint32_t i = lt * TILE + e;
             if (MODE == Q_ENCODE) {
                 const float v = o.g[td.in.off + i];
                 const uint64_t at = td.in.slot + q;
@@ -374,33 +482,50 @@ __global__ __launch_bounds__(NTHREADS) void k_query(Work w, QueryOut o) {
                 if (q < o.cap) o.idx_out[q] = i;
             } else {
                 float y = 0.0f;
-                if (rv.nv > 0 && q < rv.nv) {
+                if (q < rv.nv) {
                     const uint32_t rank = sigma_get(rv.sigma, q, rv.b);
-                    if (rank < rv.nv)
+                    if (rank < rv.nv) {
                         y = eval_rank(rv.coef, rank, rv.nv, rv.seff, rv.deff);
-                    else
+                    } else {
                         atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+                        if (o.counts_out) atomicOr((unsigned long long *)&o.counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
+                    }
                 }
-                stage[wv * QWAVE + e] = y;
+                stage[e] = y;
                 const uint64_t at = td.in.off + q;
                 if (o.idx_out) o.idx_out[at] = i;
                 if (o.val_out) o.val_out[at] = y;
             }
+            ++q;
         }
         if (MODE == Q_DECODE) {
             __syncthreads();
             float *dst = o.dense_out + td.in.off + (uint64_t)lt * TILE;
             const uint32_t lim = min(TILE, d - lt * TILE);
-            for (uint32_t e = threadIdx.x; e < lim; e += NTHREADS) dst[e] = stage[e];
+            if (lim == TILE && ((uintptr_t)dst & 15u) == 0) {
+                // whole, aligned tile: 16-byte stores
+                const float4 *src4 = (const float4 *)stage;
+                float4 *dst4 = (float4 *)dst;
+#pragma unroll
+                for (uint32_t u = 0; u < TILE / 4 / NTHREADS; ++u) dst4[u * NTHREADS + threadIdx.x] = src4[u * NTHREADS + threadIdx.x];
+            } else {
+                for (uint32_t e = threadIdx.x; e < lim; e += NTHREADS) dst[e] = stage[e];
+            }
         }
         __syncthreads();
     }
 }
 
+
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     QueryOut o{};
     o.g = g;
-    k_query<Q_ENCODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_probe<Q_ENCODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_probe<Q_ENCODE>");
+    hipError_t e = launch_tile_scan(w, 1, nullptr, s);
+    if (e != hipSuccess) return e;
+    k_emit<Q_ENCODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_emit<Q_ENCODE>");
     return hipGetLastError();
 }
 
@@ -410,18 +535,29 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     o.idx_out = idx_out;
     o.cap = cap;
     o.n_out = n_out;
-    k_query<Q_PLAIN><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_probe<Q_PLAIN><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_probe<Q_PLAIN>");
+    hipError_t e = launch_tile_scan(w, 3, n_out, s);
+    if (e != hipSuccess) return e;
+    k_emit<Q_PLAIN><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_emit<Q_PLAIN>");
     return hipGetLastError();
 }
 
 hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *dense_out, uint32_t *idx_out,
-                               float *val_out, int grid_persist, hipStream_t s) {
+                               float *val_out, uint64_t *counts_out, int grid_persist, hipStream_t s) {
     QueryOut o{};
+    o.counts_out = counts_out;
     o.payload = payload;
     o.dense_out = dense_out;
     o.idx_out = idx_out;
     o.val_out = val_out;
-    k_query<Q_DECODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_probe<Q_DECODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_probe<Q_DECODE>");
+    hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out, payload);
+    if (e != hipSuccess) return e;
+    k_emit<Q_DECODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_emit<Q_DECODE>");
     return hipGetLastError();
 }
 

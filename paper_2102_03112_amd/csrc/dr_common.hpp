@@ -7,9 +7,10 @@
 //    arrays, so per-tensor buffers never overlap and tiles never straddle
 //    tensors.
 //  * Work is split into tiles of TILE consecutive elements of one tensor.
-//    Kernels that must emit results in ascending index order take tiles in
-//    order from a ticket counter and chain the per-tile counts with a
-//    decoupled look-back, so each tile learns its output offset in one pass.
+//    A pass that must emit results in ascending index order first records,
+//    per tile, a bitmap of what it keeps and a count; a per-tensor scan of
+//    the counts gives each tile its output offset; an emit pass then writes
+//    the results in order.  No tile ever waits on another.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -22,9 +23,9 @@ constexpr uint32_t TILE_WORDS = TILE / 32;    // bitmap words per tile
 constexpr uint32_t NTHREADS = 256;            // threads per block (4 waves of 64)
 constexpr uint32_t NWAVES = NTHREADS / 64;
 constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
-constexpr uint32_t SLICE_LOG2 = 16;           // Bloom fill slice: 2^16 bits (8 KiB of LDS)
-constexpr uint32_t SLICE_BITS = 1u << SLICE_LOG2;
-constexpr uint32_t SLICE_WORDS = SLICE_BITS / 32;
+constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: tiles per chunk
+constexpr uint32_t SLICE_LOG2_MAX = 16;       // Bloom fill slices: at most 2^16 bits (8 KiB of LDS)
+constexpr uint32_t SLICE_WORDS_MAX = (1u << SLICE_LOG2_MAX) / 32;
 constexpr uint32_t HIST1_BITS = 11;           // first top-r digit: key bits 30..20
 constexpr uint32_t HIST1_BINS = 1u << HIST1_BITS;
 constexpr uint32_t HIST1_SHIFT = 20;
@@ -63,8 +64,9 @@ struct TInit {
     uint32_t bl_nslices; // Bloom slices reserved (covers the largest possible filter)
     uint32_t hb0, hbn;   // top-r histogram blocks of this tensor
     uint32_t coef_stride;// floats per run in `coef` when it is given
-    uint32_t pad_;
+    uint32_t slice_log2; // Bloom fill slice size (bits, log2)
     uint64_t rec_cap;    // payload record capacity in bytes (receiver checks the header against it)
+    uint64_t bl_poscap;  // Bloom insert: positions reserved for this tensor per round    // payload record capacity in bytes (receiver checks the header against it)
 };
 
 // Per-tensor descriptor, in device memory.
@@ -85,6 +87,9 @@ struct TDesc {
     uint32_t needT;      // top-r: how many elements with key == T to take
     uint32_t ntie;       // top-r: elements with key == T
     uint32_t idx_star;   // top-r: largest index taken among key == T (when ties split)
+    uint32_t bA;         // top-r: bin of key bits 19..10 holding the threshold (~0: all of b1)
+    uint32_t needA;      // top-r: how many to take from bin bA
+    uint32_t nsub;       // top-r: candidates in bin bA (the short list)
     uint32_t stile0;     // value sort: first tile
     uint32_t sntiles;    // value sort: tiles
     uint32_t sw0;        // reorder map: first word in the packing grid
@@ -92,8 +97,10 @@ struct TDesc {
     uint32_t coef_off;   // payload record: byte offset of the coefficients
     uint32_t sigma_off;  // payload record: byte offset of the reorder map
     uint32_t rec_bytes;  // payload record: bytes in use
-    uint32_t pad_;
+    uint32_t bl_end;     // Bloom insert: positions bucketed in the current round
 };
+
+static_assert(sizeof(TInit) % 4 == 0 && sizeof(TDesc) % 4 == 0, "descriptor layout");
 
 // device-wide totals produced on the device
 struct Glob {
@@ -116,17 +123,19 @@ struct Work {
     uint32_t ntensors;
     uint32_t ntiles_total;    // sum of ntiles
     uint64_t slots;           // padded elements = ntiles_total * TILE
-    uint32_t *tickets;        // ordered-tile ticket counters (zeroed at set-up)
     uint32_t *done;           // per-tensor completion counters (zeroed at set-up)
-    unsigned long long *lb0;  // look-back state, one array of ntiles_total per ordered pass
-    unsigned long long *lb1;
-    unsigned long long *lb2;
-    unsigned long long *lb3;
+    uint32_t *tcnt;           // per-tile counts of the current ordered pass
+    uint32_t *toff;           // per-tile exclusive offsets within the tensor
+    uint32_t *ccnt;           // top-r candidates per tile
+    uint32_t *pbits;          // positives of a full-range query, one bit per index (slots / 32 words)
     uint32_t *hist_part;      // top-r first-digit partial histograms
     uint32_t *hist;           // top-r first-digit histogram per tensor
     uint32_t *selbits;        // selection bitmap (paper's d-bit string B), slots / 32 words
     uint32_t *cand_key;       // top-r candidates (keys), per tensor slot
     uint32_t *cand_idx;       // top-r candidates (indices)
+    uint32_t *histA_part;     // top-r: candidates' histogram of key bits 19..10, one row per histogram block
+    uint32_t *sub_key;        // top-r short list (borrows P, which is written later)
+    uint32_t *sub_idx;        // top-r short list (borrows V)
     uint32_t *S;              // selected indices, per tensor slot
     uint32_t *P;              // sender's positives, per tensor slot
     float *V;                 // g[P]
@@ -137,8 +146,12 @@ struct Work {
     uint32_t *sig;            // unpacked reorder map, per tensor slot
     float *vsorted;           // values in sorted order, per tensor slot
     double *fit_part;         // fit: partial moments
+    uint32_t *fit_done;       // fit: chunks finished per run (zeroed at set-up)
+    uint32_t fit_runs;
     uint16_t *bpos;           // Bloom insert: bucketed in-slice positions
-    uint32_t *btab;           // Bloom insert: per (slice, chunk) counts then offsets
+    uint32_t *btab;           // Bloom insert: per (slice, chunk) counts, then offsets within the slice
+    uint32_t *brow;           // Bloom insert: per reserved slice, its count; brow + bslices: its start
+    uint32_t bslices;         // Bloom insert: reserved slices over all tensors
 };
 
 // ---------------------------------------------------------------------------
@@ -257,57 +270,6 @@ __device__ __forceinline__ uint32_t tensor_of_tile(const TDesc *td, uint32_t nte
     return lo;
 }
 
-// ---------------------------------------------------------------------------
-// Decoupled look-back over the tiles of one tensor.  Each tile publishes its
-// own count, then walks back over its predecessors until one has published
-// an inclusive prefix.  Tiles are handed out in increasing order by a ticket
-// counter, so every predecessor belongs to a block that is already running
-// and the walk always ends.
-// ---------------------------------------------------------------------------
-constexpr unsigned long long LB_AGG = 1ull << 62;
-constexpr unsigned long long LB_INC = 2ull << 62;
-constexpr unsigned long long LB_VAL = (1ull << 62) - 1;
-
-__device__ __forceinline__ void lb_store(unsigned long long *p, unsigned long long v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ unsigned long long lb_load(unsigned long long *p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Called by one thread.  Returns the exclusive prefix of `count` over the
-// tiles [first, tile) of the tensor.
-__device__ inline uint64_t lookback(unsigned long long *st, uint32_t tile, uint32_t first, uint64_t count) {
-    if (tile == first) {
-        lb_store(&st[tile], LB_INC | count);
-        return 0;
-    }
-    lb_store(&st[tile], LB_AGG | count);
-    uint64_t excl = 0;
-    uint32_t j = tile - 1;
-    for (;;) {
-        unsigned long long v = lb_load(&st[j]);
-        while ((v >> 62) == 0) {
-            __builtin_amdgcn_s_sleep(1);
-            v = lb_load(&st[j]);
-        }
-        excl += v & LB_VAL;
-        if ((v & LB_INC) || j == first) break;
-        --j;
-    }
-    lb_store(&st[tile], LB_INC | (excl + count));
-    return excl;
-}
-
-// Take the next tile in order from a ticket counter (thread 0), broadcast.
-__device__ __forceinline__ uint32_t next_ticket(uint32_t *ctr, uint32_t *lds_slot) {
-    if (threadIdx.x == 0) *lds_slot = atomicAdd(ctr, 1u);
-    __syncthreads();
-    uint32_t t = *lds_slot;
-    __syncthreads();
-    return t;
-}
-
 // Magnitude key: IEEE bits with the sign cleared (orders like |x|).
 __device__ __forceinline__ uint32_t mag_key(float x) { return __float_as_uint(x) & 0x7fffffffu; }
 
@@ -319,6 +281,21 @@ __device__ __forceinline__ uint32_t order_key(float x) {
 __device__ __forceinline__ float order_key_inv(uint32_t k) {
     uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
     return __uint_as_float(u);
+}
+
+// Filter words for |S| = n (Remark 2 of Section 10.2): m = 32 ceil(ceil(n mC)
+// / 32), at least 32 bits, at most the words reserved for the tensor.
+__device__ __forceinline__ uint32_t filter_words(TDesc &td) {
+    if (td.in.m_words_in) return td.in.m_words_in;
+    const double raw = ceil((double)td.n * td.in.mC);
+    uint64_t words = ((uint64_t)raw + 31u) / 32u;
+    if (words < 1) words = 1;
+    const uint64_t cap = ((uint64_t)td.in.bl_nslices << td.in.slice_log2) / 32u;
+    if (words > cap) {
+        atomicOr(&td.flags, FLAG_CAPACITY);
+        words = cap;
+    }
+    return (uint32_t)words;
 }
 
 // Width of one reorder-map entry: smallest b >= 1 with 2^b >= n.

@@ -9,6 +9,11 @@
 
 namespace dr {
 
+// Opt-in per-kernel timing (dr_trace_begin / dr_trace_end): when tracing is
+// on for the calling host thread, an event is recorded on the stream after
+// each kernel launch; the time between consecutive events is that kernel's.
+void trace_mark(hipStream_t s, const char *kernel);
+
 constexpr int INIT_CHUNK = 16;  // tensors per set-up launch (kernel argument size)
 
 struct InitArgs {
@@ -26,29 +31,34 @@ struct ZeroArgs {
 };
 
 // select.hip
-hipError_t launch_init(const Work &w, const InitArgs &a, hipStream_t s);
-hipError_t launch_zero(const ZeroArgs &a, hipStream_t s);
+// descriptors of one chunk of tensors, plus clearing the zero ranges
+hipError_t launch_init(const Work &w, const InitArgs &a, const ZeroArgs &z, hipStream_t s);
 hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int grid_persist, bool any_topr,
                        hipStream_t s);
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s);
 hipError_t launch_compact_selection(const Work &w, const float *g, float *val_out, int grid_persist, hipStream_t s);
-hipError_t launch_params(const Work &w, hipStream_t s);
+hipError_t launch_tile_popc(const Work &w, const uint32_t *bits, int grid_persist, hipStream_t s);
+// which: 0 |S| (and the filter size), 1 sender |P|, 2 receiver |P| (also
+// into counts_out, checked against the payload header), 3 into *n_out
+hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out = nullptr,
+                            const uint8_t *payload = nullptr);
 
 // bloom.hip
 // Insert in rounds of `hash_per_round` hash functions (the position buffer
-// holds that many positions per reserved item).
-hipError_t launch_bloom_insert(const Work &w, uint32_t total_chunks, uint32_t total_slices, uint32_t max_slices,
-                               uint32_t hash_per_round, uint32_t kmax, hipStream_t s);
+// holds that many positions per reserved item); items come from the
+// selection bitmap or from the list w.S.
+hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_chunks, uint32_t total_slices,
+                               uint32_t max_slices, uint32_t hash_per_round, uint32_t kmax, hipStream_t s);
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s);
 hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,
                               hipStream_t s);
 hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *dense_out, uint32_t *idx_out,
-                               float *val_out, int grid_persist, hipStream_t s);
+                               float *val_out, uint64_t *counts_out, int grid_persist, hipStream_t s);
 
 // valuefit.hip
 hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
                          hipStream_t s);
-hipError_t launch_value_setup(const Work &w, bool payload, hipStream_t s);
+hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s);
 hipError_t launch_sort(const Work &w, uint32_t cap_tiles, int grid_persist, hipStream_t s);
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s);
 hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s);
@@ -57,6 +67,5 @@ hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32
 // device count <-> tensor 0's descriptor (standalone calls)
 hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, hipStream_t s);
 hipError_t launch_export_n(const Work &w, uint64_t *n_out, int field, hipStream_t s);
-hipError_t launch_counts(const Work &w, uint64_t *counts_out, int which, hipStream_t s);
 
 }  // namespace dr

@@ -18,50 +18,33 @@
 
 namespace dr {
 
-__global__ __launch_bounds__(NTHREADS) void k_init(Work w, InitArgs a) {
-    uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= a.count) return;
-    TDesc &t = w.td[a.first + i];
-    t.in = a.t[i];
-    t.n = 0;
-    t.m_words = 0;
-    t.nv = 0;
-    t.nv_dec = 0;
-    t.seff = 0;
-    t.deff = 0;
-    t.b = 0;
-    t.flags = 0;
-    t.b1 = 0;
-    t.need1 = 0;
-    t.ncand = 0;
-    t.T = 0;
-    t.needT = 0;
-    t.ntie = 0;
-    t.idx_star = 0;
-    t.stile0 = 0;
-    t.sntiles = 0;
-    t.sw0 = 0;
-    t.swords = 0;
-    t.coef_off = 0;
-    t.sigma_off = 0;
-    t.rec_bytes = 0;
-}
-
-__global__ __launch_bounds__(NTHREADS) void k_zero(ZeroArgs a) {
-    uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    for (uint32_t r = 0; r < a.n; ++r) {
-        uint32_t *p = (uint32_t *)a.z[r].p;
-        for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < a.z[r].words; i += stride) p[i] = 0u;
+// Set-up: block 0 writes the tensor descriptors of this chunk (the
+// device-produced fields start at zero); every block clears its share of
+// the zero ranges.
+__global__ __launch_bounds__(NTHREADS) void k_init(Work w, InitArgs a, ZeroArgs z) {
+    if (blockIdx.x == 0 && threadIdx.x < a.count) {
+        TDesc &t = w.td[a.first + threadIdx.x];
+        uint32_t *dev = (uint32_t *)&t + sizeof(TInit) / 4;
+        for (uint32_t q = 0; q < (sizeof(TDesc) - sizeof(TInit)) / 4; ++q) dev[q] = 0u;
+        t.in = a.t[threadIdx.x];
+        // known before any data is seen: |S| = r for top-r, and a filter size
+        // given by the caller or computed on the host from r
+        if (t.in.r != R_NONZERO) t.n = t.in.r;
+        t.m_words = t.in.m_words_in;
+    }
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint32_t r = 0; r < z.n; ++r) {
+        uint32_t *p = (uint32_t *)z.z[r].p;
+        for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < z.z[r].words; i += stride) p[i] = 0u;
     }
 }
 
-hipError_t launch_init(const Work &w, const InitArgs &a, hipStream_t s) {
-    k_init<<<1, INIT_CHUNK <= NTHREADS ? NTHREADS : INIT_CHUNK, 0, s>>>(w, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_zero(const ZeroArgs &a, hipStream_t s) {
-    k_zero<<<1024, NTHREADS, 0, s>>>(a);
+hipError_t launch_init(const Work &w, const InitArgs &a, const ZeroArgs &z, hipStream_t s) {
+    uint64_t words = 0;
+    for (uint32_t r = 0; r < z.n; ++r) words += z.z[r].words;
+    const uint64_t blocks = words / (NTHREADS * 8) + 1;
+    k_init<<<blocks < 1024 ? (uint32_t)blocks : 1024u, NTHREADS, 0, s>>>(w, a, z);
+    trace_mark(s, "k_init");
     return hipGetLastError();
 }
 
@@ -84,10 +67,13 @@ __device__ __forceinline__ int tensor_of_hist_block(const Work &w, uint32_t b) {
     return (int)lo;
 }
 
-__global__ __launch_bounds__(NTHREADS) void k_topr_hist(Work w, const float *__restrict__ g) {
-    __shared__ uint32_t h[HIST1_BINS];
+constexpr uint32_t HIST_THREADS = 1024;
+constexpr uint32_t HIST_SUB = 4;  // sub-histograms, to spread LDS atomics on popular bins
+
+__global__ __launch_bounds__(HIST_THREADS) void k_topr_hist(Work w, const float *__restrict__ g) {
+    __shared__ uint32_t h[HIST_SUB][HIST1_BINS];
     __shared__ uint32_t bad;
-    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += NTHREADS) h[i] = 0;
+    for (uint32_t i = threadIdx.x; i < HIST_SUB * HIST1_BINS; i += HIST_THREADS) (&h[0][0])[i] = 0;
     if (threadIdx.x == 0) bad = 0;
     __syncthreads();
     const int t = tensor_of_hist_block(w, blockIdx.x);
@@ -98,16 +84,29 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_hist(Work w, const float *__r
     const uint64_t lo = lb * span;
     const uint64_t hi = lo + span < in.d ? lo + span : in.d;
     const float *gt = g + in.off;
+    uint32_t *mine = h[(threadIdx.x >> 6) % HIST_SUB];
     uint32_t nonfinite = 0;
-    for (uint64_t i = lo + threadIdx.x; i < hi; i += NTHREADS) {
-        uint32_t key = mag_key(gt[i]);
-        nonfinite |= key >= 0x7f800000u;
-        atomicAdd(&h[key >> HIST1_SHIFT], 1u);
+    // 8 loads in flight per thread before any is used
+    for (uint64_t b0 = lo; b0 < hi; b0 += 8 * HIST_THREADS) {
+        uint32_t key[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint64_t i = b0 + u * HIST_THREADS + threadIdx.x;
+            key[u] = mag_key(gt[i < hi ? i : hi - 1]);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint64_t i = b0 + u * HIST_THREADS + threadIdx.x;
+            if (i < hi) {
+                nonfinite |= key[u] >= 0x7f800000u;
+                atomicAdd(&mine[key[u] >> HIST1_SHIFT], 1u);
+            }
+        }
     }
     if (nonfinite) bad = 1;
     __syncthreads();
     uint32_t *out = w.hist_part + (uint64_t)blockIdx.x * HIST1_BINS;
-    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += NTHREADS) out[i] = h[i];
+    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += HIST_THREADS) out[i] = h[0][i] + h[1][i] + h[2][i] + h[3][i];
     if (threadIdx.x == 0 && bad) atomicOr(&w.td[t].flags, FLAG_NONFINITE);
 }
 
@@ -154,24 +153,37 @@ __device__ void find_from_top(const uint32_t *cnt, uint32_t need, uint32_t *res_
     __syncthreads();
 }
 
-// Sum the partial histograms; the last block of each tensor picks b1.
+// Sum the partial histograms (each block: 32 bins, 8 row groups of 32
+// threads); the last block of each tensor picks b1.
+constexpr uint32_t RED_BINS = 32;
+constexpr uint32_t RED_BLOCKS = HIST1_BINS / RED_BINS;
+
 __global__ __launch_bounds__(NTHREADS) void k_topr_reduce(Work w) {
-    const uint32_t t = blockIdx.x / (HIST1_BINS / NTHREADS);
-    const uint32_t part = blockIdx.x % (HIST1_BINS / NTHREADS);
+    const uint32_t t = blockIdx.x / RED_BLOCKS;
+    const uint32_t part = blockIdx.x % RED_BLOCKS;
     TDesc &td = w.td[t];
     if (td.in.r == R_NONZERO) return;
-    const uint32_t bin = part * NTHREADS + threadIdx.x;
-    uint32_t s = 0;
-    for (uint32_t q = 0; q < td.in.hbn; ++q) s += w.hist_part[(uint64_t)(td.in.hb0 + q) * HIST1_BINS + bin];
-    uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
-    hist[bin] = s;
-    __threadfence();
+    __shared__ uint32_t acc[NTHREADS / RED_BINS][RED_BINS];
     __shared__ uint32_t ticket, res_bin, res_above;
     __shared__ uint32_t scratch[NWAVES + 1];
+    const uint32_t bin = part * RED_BINS + (threadIdx.x % RED_BINS);
+    const uint32_t grp = threadIdx.x / RED_BINS;
+    uint32_t s = 0;
+    for (uint32_t q = grp; q < td.in.hbn; q += NTHREADS / RED_BINS)
+        s += w.hist_part[(uint64_t)(td.in.hb0 + q) * HIST1_BINS + bin];
+    acc[grp][threadIdx.x % RED_BINS] = s;
+    __syncthreads();
+    uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
+    if (threadIdx.x < RED_BINS) {
+        uint32_t tot = 0;
+        for (uint32_t g2 = 0; g2 < NTHREADS / RED_BINS; ++g2) tot += acc[g2][threadIdx.x];
+        hist[part * RED_BINS + threadIdx.x] = tot;
+    }
+    __threadfence();
     __syncthreads();
     if (threadIdx.x == 0) ticket = atomicAdd(&w.done[t], 1u);
     __syncthreads();
-    if (ticket != HIST1_BINS / NTHREADS - 1) return;
+    if (ticket != RED_BLOCKS - 1) return;
     __threadfence();
     const uint32_t r = td.in.r;
     if (r == 0) {
@@ -196,36 +208,48 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_reduce(Work w) {
 }
 
 // ---------------------------------------------------------------------------
-// top-r step 2 / support: bitmap of definite selections + ordered candidates
+// top-r step 2 / support: bitmap of definite selections + per-tile candidates
 // ---------------------------------------------------------------------------
 // Elements of a tile are visited as e = j * 256 + threadIdx.x (j = 0..15):
 // each load instruction reads 256 consecutive floats, and one wave ballot
-// covers 64 consecutive elements, i.e. two whole bitmap words.
+// covers 64 consecutive elements, i.e. two whole bitmap words.  Candidates
+// (top-r: key in bin b1) are kept in index order in the tile's own stretch
+// of the candidate arrays, with their number in ccnt[tile].  For the
+// support, tcnt[tile] receives the number of selected elements.
 __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float *__restrict__ g) {
-    __shared__ uint32_t tkt;
     __shared__ uint32_t wcnt[16 * NWAVES];
     __shared__ uint32_t woff[16 * NWAVES];
-    __shared__ uint32_t tile_excl, bad;
+    __shared__ uint32_t dcnt[NWAVES];
+    __shared__ uint32_t bad;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     if (threadIdx.x == 0) bad = 0;
-    for (;;) {
-        const uint32_t tile = next_ticket(&w.tickets[0], &tkt);
-        if (tile >= w.ntiles_total) break;
+    __syncthreads();
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
         const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
         TDesc &td = w.td[t];
         const uint32_t lt = tile - td.in.tile0;
         const uint32_t base = lt * TILE;
+        const uint32_t d = td.in.d;
+        const uint64_t slot = td.in.slot;
         const bool nz = td.in.r == R_NONZERO;
         const uint32_t b1 = nz ? 0u : td.b1;
         const float *gt = g + td.in.off;
         uint32_t keys[16];
         uint64_t cmask[16];
-        uint32_t nonfinite = 0;
+        uint32_t nonfinite = 0, ndef = 0;
+        // all 16 loads in flight before any is used (clamped inside the tensor)
+        const uint32_t last = d ? d - 1 : 0;
+        float x[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const uint32_t i = base + j * NTHREADS + threadIdx.x;
-            const bool valid = i < td.in.d;
-            const uint32_t key = valid ? mag_key(gt[i]) : 0u;
+            x[j] = d ? gt[i < d ? i : last] : 0.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const uint32_t i = base + j * NTHREADS + threadIdx.x;
+            const bool valid = i < d;
+            const uint32_t key = valid ? mag_key(x[j]) : 0u;
             nonfinite |= key >= 0x7f800000u;
             const uint32_t bin = key >> HIST1_SHIFT;
             const bool def = valid && (nz ? key != 0u : bin > b1);
@@ -233,27 +257,34 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
             const uint64_t dm = ballot(def);
             cmask[j] = ballot(cand);
             keys[j] = key;
+            ndef += popc64(dm);
             if (lane == 0 || lane == 32) {
-                const uint32_t word = (uint32_t)((td.in.slot + base + j * NTHREADS + wv * 64 + lane) >> 5);
+                const uint32_t word = (uint32_t)((slot + base + j * NTHREADS + wv * 64 + lane) >> 5);
                 w.selbits[word] = lane == 0 ? (uint32_t)dm : (uint32_t)(dm >> 32);
             }
             if (lane == 0) wcnt[j * NWAVES + wv] = popc64(cmask[j]);
         }
         if (nonfinite) bad = 1;
+        if (lane == 0) dcnt[wv] = ndef;
         __syncthreads();
         if (threadIdx.x < 64) {
-            // (j, wave) counts in element order -> exclusive offsets
-            uint32_t c = wcnt[threadIdx.x];
-            uint32_t inc = wave_incl_scan(c);
+            // (j, wave) candidate counts in element order -> exclusive offsets
+            const uint32_t c = wcnt[threadIdx.x];
+            const uint32_t inc = wave_incl_scan(c);
             woff[threadIdx.x] = inc - c;
-            if (threadIdx.x == 63) tile_excl = (uint32_t)lookback(w.lb0, tile, td.in.tile0, inc);
+            if (threadIdx.x == 63) {
+                w.ccnt[tile] = inc;
+                uint32_t nd = 0;
+                for (uint32_t q = 0; q < NWAVES; ++q) nd += dcnt[q];
+                w.tcnt[tile] = nd;
+            }
         }
         __syncthreads();
         if (threadIdx.x == 0 && bad) {
             atomicOr(&td.flags, FLAG_NONFINITE);
             bad = 0;
         }
-        const uint64_t cbase = td.in.slot + tile_excl;
+        const uint64_t cbase = slot + base;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             if ((cmask[j] >> lane) & 1ull) {
@@ -262,82 +293,189 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
                 w.cand_idx[q] = base + j * NTHREADS + threadIdx.x;
             }
         }
+        __syncthreads();
     }
 }
 
 // ---------------------------------------------------------------------------
-// top-r step 3: exact select among the candidates, one block per tensor
+// top-r step 3: finish the select on the candidates' low 20 key bits.
+//  a. one block per tensor picks the bin bA of key bits 19..10 from the
+//     histogram the filter pass built;
+//  b. a pass over the candidates marks those above bA and gathers those in
+//     bA (usually a few dozen) into a short list;
+//  c. one block per tensor finishes on the short list: bin of bits 9..0,
+//     then, if equal keys straddle the cut, the smallest indices among them.
 // ---------------------------------------------------------------------------
 constexpr uint32_t SEL_THREADS = 1024;
 
-__global__ __launch_bounds__(SEL_THREADS) void k_topr_select(Work w) {
+// Histogram of key bits 19..10 of the candidates, one partial row per
+// top-r histogram block (same tile ranges as the first pass); one wave
+// takes one tile's candidates at a time.
+__global__ __launch_bounds__(SEL_THREADS) void k_topr_candhist(Work w) {
+    __shared__ uint32_t h[1024];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int t = tensor_of_hist_block(w, blockIdx.x);
+    if (t < 0) return;
+    const TDesc &td = w.td[t];
+    const uint32_t lb = blockIdx.x - td.in.hb0;
+    const uint32_t per = (td.in.ntiles + td.in.hbn - 1) / td.in.hbn;
+    const uint32_t tl0 = lb * per, tl1 = min(td.in.ntiles, tl0 + per);
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    if (td.ncand > 0) {
+        for (uint32_t tl = tl0 + wv; tl < tl1; tl += SEL_THREADS / 64) {
+            const uint32_t c = w.ccnt[td.in.tile0 + tl];
+            const uint32_t *ck = w.cand_key + td.in.slot + (uint64_t)tl * TILE;
+            for (uint32_t j = lane; j < c; j += 64) atomicAdd(&h[(ck[j] >> 10) & 1023u], 1u);
+        }
+    }
+    __syncthreads();
+    w.histA_part[(uint64_t)blockIdx.x * 1024u + threadIdx.x] = h[threadIdx.x];
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
     TDesc &td = w.td[blockIdx.x];
     if (td.in.r == R_NONZERO || td.ncand == 0) return;
-    __shared__ uint32_t h[1024];
     __shared__ uint32_t scratch[SEL_THREADS / 64 + 1];
-    __shared__ uint32_t res_bin, res_above, found, run_total;
-    const uint32_t nc = td.ncand, need1 = td.need1;
-    const uint32_t *ck = w.cand_key + td.in.slot;
-    const uint32_t *ci = w.cand_idx + td.in.slot;
-    uint32_t T, needT, ntie, idx_star = 0xFFFFFFFFu;
+    __shared__ uint32_t res_bin, res_above;
+    if (td.need1 == td.ncand) {  // the whole bin b1 is taken
+        if (threadIdx.x == 0) {
+            td.bA = 0xFFFFFFFFu;
+            td.needA = 0;
+        }
+        return;
+    }
     if (threadIdx.x == 0) {
         res_bin = 0;
         res_above = 0;
     }
     __syncthreads();
-    if (need1 == nc) {
-        // the whole bin is taken: every candidate is selected
-        T = td.b1 << HIST1_SHIFT;
-        needT = 0;
-        ntie = 0;
-    } else {
-        // digit A: key bits 19..10
-        h[threadIdx.x] = 0;
-        __syncthreads();
-        for (uint32_t q = threadIdx.x; q < nc; q += SEL_THREADS) atomicAdd(&h[(ck[q] >> 10) & 1023u], 1u);
-        __syncthreads();
-        find_from_top<1024, SEL_THREADS>(h, need1, &res_bin, &res_above, scratch);
-        const uint32_t bA = res_bin, needA = need1 - res_above;
-        // digit B: key bits 9..0 among candidates in bin bA
-        h[threadIdx.x] = 0;
-        __syncthreads();
-        for (uint32_t q = threadIdx.x; q < nc; q += SEL_THREADS) {
-            uint32_t k = ck[q];
-            if (((k >> 10) & 1023u) == bA) atomicAdd(&h[k & 1023u], 1u);
-        }
-        __syncthreads();
-        find_from_top<1024, SEL_THREADS>(h, needA, &res_bin, &res_above, scratch);
-        const uint32_t bB = res_bin;
-        needT = needA - res_above;
-        ntie = h[bB];
-        T = (td.b1 << HIST1_SHIFT) | (bA << 10) | bB;
-        if (needT < ntie) {
-            // ties split: take the needT smallest indices among key == T;
-            // the list is in index order, so find the needT-th such entry
-            if (threadIdx.x == 0) {
-                found = 0xFFFFFFFFu;
-                run_total = 0;
+    __shared__ uint32_t histA[1024];
+    uint32_t sum = 0;
+    const uint32_t *rows = w.histA_part + (uint64_t)td.in.hb0 * 1024u + threadIdx.x;
+    uint32_t q = 0;
+    for (; q + 16 <= td.in.hbn; q += 16) {  // 16 rows in flight
+        uint32_t v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = rows[(uint64_t)(q + u) * 1024u];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) sum += v[u];
+    }
+    for (; q < td.in.hbn; ++q) sum += rows[(uint64_t)q * 1024u];
+    histA[threadIdx.x] = sum;
+    __syncthreads();
+    find_from_top<1024, SEL_THREADS>(histA, td.need1, &res_bin, &res_above, scratch);
+    if (threadIdx.x == 0) {
+        td.bA = res_bin;
+        td.needA = td.need1 - res_above;
+        td.nsub = 0;
+    }
+}
+
+// candidates above bin bA are selected; those in bA go to the short list
+__global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+        const uint32_t c = w.ccnt[tile];
+        if (c == 0) continue;
+        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
+        TDesc &td = w.td[t];
+        if (td.in.r == R_NONZERO) continue;
+        const uint32_t bA = td.bA;
+        const uint64_t b0 = td.in.slot + (uint64_t)(tile - td.in.tile0) * TILE;
+        uint32_t *sb = w.selbits + (td.in.slot >> 5);
+        for (uint32_t j0 = 0; j0 < c; j0 += NTHREADS) {
+            const uint32_t j = j0 + threadIdx.x;
+            const bool act = j < c;
+            const uint32_t k = act ? w.cand_key[b0 + j] : 0u, i = act ? w.cand_idx[b0 + j] : 0u;
+            const uint32_t dA = (k >> 10) & 1023u;
+            const bool take = act && (bA == 0xFFFFFFFFu || dA > bA);
+            const bool sub = act && bA != 0xFFFFFFFFu && dA == bA;
+            if (take) atomicOr(&sb[i >> 5], 1u << (i & 31u));
+            // wave-aggregated append to the tensor's short list
+            const uint64_t m = ballot(sub);
+            if (m) {
+                uint32_t at0 = 0;
+                if (lane_id() == (uint32_t)__ffsll((unsigned long long)m) - 1) at0 = atomicAdd(&td.nsub, popc64(m));
+                at0 = __shfl(at0, __ffsll((unsigned long long)m) - 1, 64);
+                if (sub) {
+                    const uint64_t q = td.in.slot + at0 + lanes_below(m);
+                    w.sub_key[q] = k;
+                    w.sub_idx[q] = i;
+                }
             }
-            __syncthreads();
-            for (uint32_t q0 = 0; q0 < nc; q0 += SEL_THREADS) {
-                const uint32_t q = q0 + threadIdx.x;
-                const uint32_t f = (q < nc && ck[q] == T) ? 1u : 0u;
-                uint32_t tot;
-                const uint32_t before = run_total;
-                const uint32_t ex = block_excl_scan_n<SEL_THREADS>(f, scratch, &tot);
-                if (f && before + ex + 1 == needT) found = ci[q];
-                __syncthreads();
-                if (threadIdx.x == 0) run_total = before + tot;
-                __syncthreads();
-                if (found != 0xFFFFFFFFu) break;
-            }
-            idx_star = found;
         }
     }
-    // mark the selected candidates in the bitmap
+}
+
+// Among the short list (unordered), take the needA largest by key, ties to
+// the smaller index; set their bits.
+__global__ __launch_bounds__(SEL_THREADS) void k_topr_final(Work w) {
+    TDesc &td = w.td[blockIdx.x];
+    if (td.in.r == R_NONZERO || td.ncand == 0 || td.bA == 0xFFFFFFFFu) return;
+    __shared__ uint32_t h[2048];
+    __shared__ uint32_t scratch[SEL_THREADS / 64 + 1];
+    __shared__ uint32_t res_bin, res_above;
+    const uint32_t ns = td.nsub, needA = td.needA;
+    const uint32_t *sk = w.sub_key + td.in.slot;
+    const uint32_t *si = w.sub_idx + td.in.slot;
+    // bits 9..0 of the key
+    h[threadIdx.x] = 0;
+    if (threadIdx.x == 0) {
+        res_bin = 0;
+        res_above = 0;
+    }
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < ns; q += SEL_THREADS) atomicAdd(&h[sk[q] & 1023u], 1u);
+    __syncthreads();
+    find_from_top<1024, SEL_THREADS>(h, needA, &res_bin, &res_above, scratch);
+    const uint32_t bB = res_bin;
+    const uint32_t needT = needA - res_above, ntie = h[bB];
+    const uint32_t T = (td.b1 << HIST1_SHIFT) | (td.bA << 10) | bB;
+    __syncthreads();
+    uint32_t idx_star = 0xFFFFFFFFu;
+    if (needT < ntie) {
+        // the needT smallest indices among key == T: radix select on the
+        // index, 11 + 11 + 10 bits, counting from the bottom
+        uint32_t prefix = 0, need = needT;
+        for (int pass = 0; pass < 3; ++pass) {
+            const uint32_t shift = pass == 0 ? 21u : (pass == 1 ? 10u : 0u);
+            const uint32_t nb = pass == 2 ? 1024u : 2048u;
+            for (uint32_t i = threadIdx.x; i < 2048; i += SEL_THREADS) h[i] = 0;
+            __syncthreads();
+            for (uint32_t q = threadIdx.x; q < ns; q += SEL_THREADS) {
+                const uint32_t ix = si[q];
+                const bool match = sk[q] == T && (pass == 0 || (ix >> (shift + (pass == 1 ? 11u : 10u))) == prefix);
+                if (match) atomicAdd(&h[(ix >> shift) & (nb - 1u)], 1u);
+            }
+            __syncthreads();
+            // find from the bottom: the bin where the running count reaches `need`
+            const uint32_t per = nb / SEL_THREADS;  // 2 or 1 bins per thread
+            uint32_t sum = 0;
+            for (uint32_t u = 0; u < per; ++u) sum += h[threadIdx.x * per + u];
+            uint32_t tot;
+            const uint32_t ex = block_excl_scan_n<SEL_THREADS>(sum, scratch, &tot);
+            if (ex < need && need <= ex + sum) {
+                uint32_t run = ex;
+                for (uint32_t u = 0; u < per; ++u) {
+                    const uint32_t bin = threadIdx.x * per + u;
+                    if (run + h[bin] >= need) {
+                        res_bin = bin;
+                        res_above = run;
+                        break;
+                    }
+                    run += h[bin];
+                }
+            }
+            __syncthreads();
+            prefix = (prefix << (pass == 2 ? 10u : 11u)) | res_bin;
+            need -= res_above;
+            __syncthreads();
+        }
+        idx_star = prefix;
+    }
     uint32_t *sb = w.selbits + (td.in.slot >> 5);
-    for (uint32_t q = threadIdx.x; q < nc; q += SEL_THREADS) {
-        const uint32_t k = ck[q], i = ci[q];
+    for (uint32_t q = threadIdx.x; q < ns; q += SEL_THREADS) {
+        const uint32_t k = sk[q], i = si[q];
         const bool sel = k > T || (k == T && (needT == ntie || i <= idx_star));
         if (sel) atomicOr(&sb[i >> 5], 1u << (i & 31u));
     }
@@ -352,43 +490,126 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_select(Work w) {
 hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int grid_persist, bool any_topr,
                        hipStream_t s) {
     if (any_topr) {
-        k_topr_hist<<<hist_blocks, NTHREADS, 0, s>>>(w, g);
-        k_topr_reduce<<<w.ntensors * (HIST1_BINS / NTHREADS), NTHREADS, 0, s>>>(w);
+        k_topr_hist<<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
+        trace_mark(s, "k_topr_hist");
+        k_topr_reduce<<<w.ntensors * RED_BLOCKS, NTHREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_reduce");
     }
     k_select_filter<<<grid_persist, NTHREADS, 0, s>>>(w, g);
-    if (any_topr) k_topr_select<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
-    return hipGetLastError();
-}
-
-hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s) {
-    k_select_filter<<<grid_persist, NTHREADS, 0, s>>>(w, g);
+    trace_mark(s, "k_select_filter");
+    if (any_topr) {
+        k_topr_candhist<<<hist_blocks, SEL_THREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_candhist");
+        k_topr_pickA<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_pickA");
+        k_topr_candpass<<<grid_persist, NTHREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_candpass");
+        k_topr_final<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_final");
+    }
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Ordered compaction of the selection bitmap into S (ascending indices).
+// Ordered passes: per-tile counts -> per-tensor offsets -> emit in order
+// ---------------------------------------------------------------------------
+// tcnt[tile] = set bits of the tile's words of `bits`
+__global__ __launch_bounds__(NTHREADS) void k_tile_popc(Work w, const uint32_t *__restrict__ bits) {
+    __shared__ uint32_t part[NWAVES];
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+        uint32_t c = 0;
+        if (threadIdx.x < TILE_WORDS) c = __popc(bits[(uint64_t)tile * TILE_WORDS + threadIdx.x]);
+        c = wave_sum(c);
+        if ((threadIdx.x & 63u) == 0) part[threadIdx.x >> 6] = c;
+        __syncthreads();
+        if (threadIdx.x == 0) w.tcnt[tile] = part[0] + part[1] + part[2] + part[3];
+        __syncthreads();
+    }
+}
+
+// toff = exclusive scan of tcnt over the tiles of each tensor; the total
+// goes to the tensor's field `which` (0: n, 1: nv, 2: nv_dec, 3: *n_out)
+constexpr uint32_t TSCAN_THREADS = 1024;
+constexpr uint32_t TSCAN_PER = 8;  // counts per thread per step, loaded together
+
+__global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, uint64_t *n_out,
+                                                             uint64_t *counts_out, const uint8_t *payload) {
+    TDesc &td = w.td[blockIdx.x];
+    __shared__ uint32_t scratch[TSCAN_THREADS / 64 + 1];
+    const uint32_t nt = td.in.ntiles;
+    const uint32_t *cnt = w.tcnt + td.in.tile0;
+    uint32_t *off = w.toff + td.in.tile0;
+    uint32_t carry = 0;
+    // thread x owns counts [x * PER, (x+1) * PER) of each step of PER * 1024
+    for (uint32_t q0 = 0; q0 < nt; q0 += TSCAN_THREADS * TSCAN_PER) {
+        uint32_t v[TSCAN_PER];
+        const uint32_t b = q0 + threadIdx.x * TSCAN_PER;
+#pragma unroll
+        for (uint32_t u = 0; u < TSCAN_PER; ++u) v[u] = b + u < nt ? cnt[b + u] : 0u;
+        uint32_t sum = 0;
+#pragma unroll
+        for (uint32_t u = 0; u < TSCAN_PER; ++u) sum += v[u];
+        uint32_t tot;
+        uint32_t run = carry + block_excl_scan_n<TSCAN_THREADS>(sum, scratch, &tot);
+#pragma unroll
+        for (uint32_t u = 0; u < TSCAN_PER; ++u) {
+            if (b + u < nt) off[b + u] = run;
+            run += v[u];
+        }
+        carry += tot;
+    }
+    if (threadIdx.x == 0) {
+        if (which == 0) {
+            const uint32_t cap = td.in.r != R_NONZERO ? td.in.r : td.in.d;
+            td.n = carry < cap ? carry : cap;
+            if (td.in.r != R_NONZERO && carry != td.in.r) atomicOr(&td.flags, FLAG_COUNT);
+            td.m_words = filter_words(td);
+        } else if (which == 1) {
+            td.nv = carry;
+        } else if (which == 2) {
+            td.nv_dec = carry;
+            if (counts_out) {
+                counts_out[4 * blockIdx.x + 2] = carry;
+                const uint8_t *rec = payload + td.in.rec_off;
+                const uint64_t hdr_nv = *(const uint64_t *)(rec + 24);
+                uint32_t f = td.flags;
+                if (carry != hdr_nv) f |= FLAG_DEC_MISMATCH;
+                counts_out[4 * blockIdx.x + 3] |= f & FLAG_DEC_MISMATCH;
+            }
+        } else if (n_out) {
+            *n_out = carry;
+        }
+    }
+}
+
+hipError_t launch_tile_popc(const Work &w, const uint32_t *bits, int grid_persist, hipStream_t s) {
+    k_tile_popc<<<grid_persist, NTHREADS, 0, s>>>(w, bits);
+    trace_mark(s, "k_tile_popc");
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out,
+                            const uint8_t *payload) {
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, which, n_out, counts_out, payload);
+    trace_mark(s, "k_tile_scan");
+    return hipGetLastError();
+}
+
+// S = the selection bitmap's set bits in ascending order (val_out: g there).
 // Threads 0..127 of a block own one bitmap word of the tile each.
-// ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NTHREADS) void k_compact_selection(Work w, const float *__restrict__ g,
                                                                 float *__restrict__ val_out) {
-    __shared__ uint32_t tkt;
     __shared__ uint32_t scratch[NWAVES + 1];
-    __shared__ uint32_t tile_excl;
-    for (;;) {
-        const uint32_t tile = next_ticket(&w.tickets[1], &tkt);
-        if (tile >= w.ntiles_total) break;
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
         const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
-        TDesc &td = w.td[t];
+        const TDesc &td = w.td[t];
         const uint32_t lt = tile - td.in.tile0;
         uint32_t word = 0;
-        if (threadIdx.x < TILE_WORDS) word = w.selbits[((td.in.slot + (uint64_t)lt * TILE) >> 5) + threadIdx.x];
+        if (threadIdx.x < TILE_WORDS) word = w.selbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
         uint32_t tot;
-        uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
-        if (threadIdx.x == 0) tile_excl = (uint32_t)lookback(w.lb1, tile, td.in.tile0, tot);
-        __syncthreads();
-        // output capacity: r entries for top-r, d for the support
+        const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
         const uint32_t cap = td.in.r != R_NONZERO ? td.in.r : td.in.d;
-        uint32_t rank = tile_excl + ex;
+        uint32_t rank = w.toff[tile] + ex;
         const uint32_t i0 = lt * TILE + threadIdx.x * 32;
         while (word) {
             const uint32_t b = __ffs(word) - 1;
@@ -400,45 +621,26 @@ __global__ __launch_bounds__(NTHREADS) void k_compact_selection(Work w, const fl
             }
             ++rank;
         }
-        if (threadIdx.x == 0 && lt == td.in.ntiles - 1) {
-            const uint32_t n = tile_excl + tot;
-            td.n = n < cap ? n : cap;
-            if (td.in.r != R_NONZERO && n != td.in.r) atomicOr(&td.flags, FLAG_COUNT);
-        }
-        __syncthreads();
     }
 }
 
 hipError_t launch_compact_selection(const Work &w, const float *g, float *val_out, int grid_persist,
                                     hipStream_t s) {
+    k_tile_popc<<<grid_persist, NTHREADS, 0, s>>>(w, w.selbits);
+    trace_mark(s, "k_tile_popc");
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr, nullptr);
+    trace_mark(s, "k_tile_scan");
     k_compact_selection<<<grid_persist, NTHREADS, 0, s>>>(w, g, val_out);
+    trace_mark(s, "k_compact_selection");
     return hipGetLastError();
 }
 
-// ---------------------------------------------------------------------------
-// Per-tensor Bloom parameters from |S| (Remark 2 of Section 10.2).
-// ---------------------------------------------------------------------------
-__global__ void k_params(Work w) {
-    const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= w.ntensors) return;
-    TDesc &td = w.td[t];
-    uint32_t mw = td.in.m_words_in;
-    if (mw == 0) {
-        const double raw = ceil((double)td.n * td.in.mC);
-        uint64_t words = ((uint64_t)raw + 31u) / 32u;
-        if (words < 1) words = 1;
-        const uint64_t cap = (uint64_t)td.in.bl_nslices * SLICE_WORDS;
-        if (words > cap) {
-            atomicOr(&td.flags, FLAG_CAPACITY);
-            words = cap;
-        }
-        mw = (uint32_t)words;
-    }
-    td.m_words = mw;
-}
-
-hipError_t launch_params(const Work &w, hipStream_t s) {
-    k_params<<<(w.ntensors + 255) / 256, 256, 0, s>>>(w);
+hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s) {
+    k_select_filter<<<grid_persist, NTHREADS, 0, s>>>(w, g);
+    trace_mark(s, "k_select_filter");
+    // |S| from the per-tile counts of the filter pass
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr, nullptr);
+    trace_mark(s, "k_tile_scan");
     return hipGetLastError();
 }
 

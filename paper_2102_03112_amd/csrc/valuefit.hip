@@ -46,6 +46,7 @@ __global__ __launch_bounds__(NTHREADS) void k_keygen(Work w, const float *__rest
 hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
                          hipStream_t s) {
     k_keygen<<<grid_persist, NTHREADS, 0, s>>>(w, vals, n, n_cap);
+    trace_mark(s, "k_keygen");
     return hipGetLastError();
 }
 
@@ -53,7 +54,7 @@ hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, ui
 // layout and header.  One block walks the tensors in chunks.
 constexpr uint32_t SETUP_THREADS = 1024;
 
-__global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int payload) {
+__global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int payload, uint64_t *counts_out) {
     __shared__ uint32_t scratch[SETUP_THREADS / 64 + 1];
     __shared__ uint32_t carry_tiles, carry_words, carry_vals;
     if (threadIdx.x == 0) {
@@ -78,6 +79,12 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
             nwd = (uint32_t)(((uint64_t)nv * b + 31u) / 32u);
             td.sntiles = ntl;
             td.swords = nwd;
+            if (counts_out) {
+                counts_out[4 * t + 0] = td.n;
+                counts_out[4 * t + 1] = nv;
+                counts_out[4 * t + 2] = 0;
+                counts_out[4 * t + 3] = td.flags;
+            }
             if (payload) {
                 const uint32_t coef_off = HDR_BYTES + td.m_words * 4u;
                 const uint32_t sigma_off = coef_off + seff * (deff + 1u) * 4u;
@@ -126,8 +133,9 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
     }
 }
 
-hipError_t launch_value_setup(const Work &w, bool payload, hipStream_t s) {
-    k_value_setup<<<1, SETUP_THREADS, 0, s>>>(w, payload ? 1 : 0);
+hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s) {
+    k_value_setup<<<1, SETUP_THREADS, 0, s>>>(w, payload ? 1 : 0, counts_out);
+    trace_mark(s, "k_value_setup");
     return hipGetLastError();
 }
 
@@ -159,25 +167,46 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_hist(Work w, const uint32_t *
         const uint32_t *kt = keys + td.in.slot;
         for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) atomicAdd(&h[(kt[q] >> shift) & 255u], 1u);
         __syncthreads();
-        w.shist[(uint64_t)SORT_BINS * td.stile0 + (uint64_t)threadIdx.x * td.sntiles + lt] = h[threadIdx.x];
+        w.shist[(uint64_t)SORT_BINS * (td.stile0 + lt) + threadIdx.x] = h[threadIdx.x];
         __syncthreads();
     }
 }
 
-// per tensor: digit totals, digit bases, and each digit row's running offsets
+// Per tensor: digit totals, digit bases, and the running offset of each
+// (tile, digit).  Counts are stored tile-major, so each step over the tiles
+// is one coalesced load per block.
 __global__ __launch_bounds__(SORT_BINS) void k_sort_scan(Work w) {
     const TDesc &td = w.td[blockIdx.x];
     const uint32_t nt = td.sntiles;
     if (nt == 0) return;
     __shared__ uint32_t scratch[SORT_BINS / 64 + 1];
-    uint32_t *row = w.shist + (uint64_t)SORT_BINS * td.stile0 + (uint64_t)threadIdx.x * nt;
+    uint32_t *col = w.shist + (uint64_t)SORT_BINS * td.stile0 + threadIdx.x;
     uint32_t sum = 0;
-    for (uint32_t q = 0; q < nt; ++q) sum += row[q];
+    uint32_t q = 0;
+    for (; q + 8 <= nt; q += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = col[(uint64_t)(q + u) * SORT_BINS];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += v[u];
+    }
+    for (; q < nt; ++q) sum += col[(uint64_t)q * SORT_BINS];
     uint32_t tot;
     uint32_t run = block_excl_scan_n<SORT_BINS>(sum, scratch, &tot);
-    for (uint32_t q = 0; q < nt; ++q) {
-        const uint32_t c = row[q];
-        row[q] = run;
+    q = 0;
+    for (; q + 8 <= nt; q += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = col[(uint64_t)(q + u) * SORT_BINS];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            col[(uint64_t)(q + u) * SORT_BINS] = run;
+            run += v[u];
+        }
+    }
+    for (; q < nt; ++q) {
+        const uint32_t c = col[(uint64_t)q * SORT_BINS];
+        col[(uint64_t)q * SORT_BINS] = run;
         run += c;
     }
 }
@@ -200,7 +229,7 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_scatter(Work w, const uint32_
         const uint32_t lt = gt - td.stile0;
         uint32_t *c32 = (uint32_t *)&cnt[0][0][0];
         for (uint32_t i = threadIdx.x; i < 16 * NWAVES * SORT_BINS / 2; i += NTHREADS) c32[i] = 0;
-        goff[threadIdx.x] = w.shist[(uint64_t)SORT_BINS * td.stile0 + (uint64_t)threadIdx.x * td.sntiles + lt];
+        goff[threadIdx.x] = w.shist[(uint64_t)SORT_BINS * (td.stile0 + lt) + threadIdx.x];
         __syncthreads();
         const uint32_t q0 = lt * TILE;
         const uint32_t nv = td.nv;
@@ -264,8 +293,11 @@ hipError_t launch_sort(const Work &w, uint32_t cap_tiles, int grid_persist, hipS
     for (int p = 0; p < 4; ++p) {
         const uint32_t shift = 8u * p;
         k_sort_hist<<<grid_persist, NTHREADS, 0, s>>>(w, kin, shift);
+        trace_mark(s, "k_sort_hist");
         k_sort_scan<<<w.ntensors, SORT_BINS, 0, s>>>(w);
+        trace_mark(s, "k_sort_scan");
         k_sort_scatter<<<grid_persist, NTHREADS, 0, s>>>(w, kin, vin, kout, vout, shift, p == 3);
+        trace_mark(s, "k_sort_scatter");
         uint32_t *tk = kin, *tv = vin;
         kin = kout;
         vin = vout;
@@ -335,12 +367,21 @@ __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, u
     }
 }
 
+__device__ void solve_run(const TDesc &td, uint32_t s, const double *mom);
+
+// Moments of one chunk of one run; the last chunk of a run to finish sums
+// the run's partial moments in chunk order and solves.
 __global__ __launch_bounds__(NTHREADS) void k_fit_moments(Work w) {
     const uint32_t t = tensor_of_fit_block(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t local = blockIdx.x - td.in.fit_blk0;
     const uint32_t s = local / FIT_CHUNKS, ch = local % FIT_CHUNKS;
-    if (s >= td.seff) return;
+    if (s >= td.seff) {
+        // caller-owned coefficient rows beyond the fitted runs are zero
+        if (td.in.coef && ch == 0 && s < td.in.nseg && threadIdx.x < td.in.coef_stride)
+            td.in.coef[(uint64_t)s * td.in.coef_stride + threadIdx.x] = 0.0f;
+        return;
+    }
     const uint64_t nv = td.nv, S = td.seff;
     const uint64_t lo = s * nv / S, hi = (s + 1) * nv / S, ns = hi - lo;
     const uint64_t j0 = ns * ch / FIT_CHUNKS, j1 = ns * (ch + 1) / FIT_CHUNKS;
@@ -356,75 +397,106 @@ __global__ __launch_bounds__(NTHREADS) void k_fit_moments(Work w) {
         case 6: fit_moments_body<6>(y, lo, ns, j0, j1, out); break;
         default: fit_moments_body<7>(y, lo, ns, j0, j1, out); break;
     }
+    __shared__ uint32_t ticket;
+    __shared__ double mom[NMOM];
+    __threadfence();
+    __syncthreads();
+    const uint32_t run = td.in.fit_blk0 / FIT_CHUNKS + s;
+    if (threadIdx.x == 0) ticket = atomicAdd(&w.fit_done[run], 1u);
+    __syncthreads();
+    if (ticket != FIT_CHUNKS - 1) return;
+    __threadfence();
+    if (threadIdx.x < NMOM) {
+        const double *part = w.fit_part + (uint64_t)(td.in.fit_blk0 + s * FIT_CHUNKS) * NMOM;
+        double acc = 0.0;
+        for (uint32_t c = 0; c < FIT_CHUNKS; ++c) acc += part[c * NMOM + threadIdx.x];
+        mom[threadIdx.x] = acc;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) solve_run(td, s, mom);
 }
 
-// one thread per (tensor, run): sum the partial moments in chunk order and
-// solve the normal equations by Gaussian elimination with partial pivoting
-__global__ void k_fit_solve(Work w, uint32_t total_runs) {
-    const uint32_t gs = blockIdx.x * blockDim.x + threadIdx.x;
-    if (gs >= total_runs) return;
-    const uint32_t t = tensor_of_fit_block(w, gs * FIT_CHUNKS);
-    const TDesc &td = w.td[t];
-    const uint32_t s = gs - td.in.fit_blk0 / FIT_CHUNKS;
-    if (s >= td.in.nseg) return;
-    const bool standalone = td.in.coef != nullptr;
-    const uint32_t D = td.deff, N = D + 1;
-    float *row;
-    if (standalone) {
-        row = td.in.coef + (uint64_t)s * td.in.coef_stride;
-        if (s >= td.seff) {
-            for (uint32_t p = 0; p < td.in.coef_stride; ++p) row[p] = 0.0f;
-            return;
-        }
-        for (uint32_t p = N; p < td.in.coef_stride; ++p) row[p] = 0.0f;
-    } else {
-        if (s >= td.seff) return;
-        row = (float *)(td.in.rec + td.coef_off) + (uint64_t)s * N;
-    }
-    double mom[NMOM];
-    for (uint32_t e = 0; e < NMOM; ++e) mom[e] = 0.0;
-    const double *part = w.fit_part + (uint64_t)(td.in.fit_blk0 + s * FIT_CHUNKS) * NMOM;
-    for (uint32_t c = 0; c < FIT_CHUNKS; ++c)
-        for (uint32_t e = 0; e < NMOM; ++e) mom[e] += part[c * NMOM + e];
-    double A[MAX_DEG + 1][MAX_DEG + 2];
-    for (uint32_t p = 0; p < N; ++p) {
-        for (uint32_t q = 0; q < N; ++q) A[p][q] = mom[p + q];
+// Normal equations of degree D from the summed moments, solved by Gaussian
+// elimination with partial pivoting; the system lives in registers.
+template <int D>
+__device__ void solve_normal(const double *mom, float *row) {
+    constexpr int N = D + 1;
+    double A[N][N + 1];
+#pragma unroll
+    for (int p = 0; p < N; ++p) {
+#pragma unroll
+        for (int q = 0; q < N; ++q) A[p][q] = mom[p + q];
         A[p][N] = mom[2 * MAX_DEG + 1 + p];
     }
     bool ok = true;
-    for (uint32_t col = 0; col < N; ++col) {
-        uint32_t piv = col;
-        for (uint32_t r = col + 1; r < N; ++r)
+#pragma unroll
+    for (int col = 0; col < N; ++col) {
+        int piv = col;
+#pragma unroll
+        for (int r = col + 1; r < N; ++r)
             if (fabs(A[r][col]) > fabs(A[piv][col])) piv = r;
-        if (A[piv][col] == 0.0) {
-            ok = false;
-            break;
-        }
-        if (piv != col)
-            for (uint32_t c = 0; c <= N; ++c) {
-                const double tmp = A[col][c];
-                A[col][c] = A[piv][c];
-                A[piv][c] = tmp;
+        if (A[piv][col] == 0.0) ok = false;
+        // swap rows col and piv without dynamic register indexing
+#pragma unroll
+        for (int r = col + 1; r < N; ++r) {
+            if (r == piv) {
+#pragma unroll
+                for (int c = 0; c <= N; ++c) {
+                    const double tmp = A[col][c];
+                    A[col][c] = A[r][c];
+                    A[r][c] = tmp;
+                }
             }
-        for (uint32_t r = col + 1; r < N; ++r) {
-            const double f = A[r][col] / A[col][col];
-            for (uint32_t c = col; c <= N; ++c) A[r][c] -= f * A[col][c];
+        }
+        if (A[col][col] != 0.0) {
+#pragma unroll
+            for (int r = col + 1; r < N; ++r) {
+                const double f = A[r][col] / A[col][col];
+#pragma unroll
+                for (int c = col; c <= N; ++c) A[r][c] -= f * A[col][c];
+            }
         }
     }
-    double x[MAX_DEG + 1];
-    for (int p = (int)N - 1; p >= 0; --p) {
+    double x[N];
+#pragma unroll
+    for (int p = N - 1; p >= 0; --p) {
         double acc = A[p][N];
-        for (uint32_t q = p + 1; q < N; ++q) acc -= A[p][q] * x[q];
+#pragma unroll
+        for (int q = p + 1; q < N; ++q) acc -= A[p][q] * x[q];
         x[p] = ok ? acc / A[p][p] : 0.0;
     }
-    for (uint32_t p = 0; p < N; ++p) row[p] = (float)x[p];
+#pragma unroll
+    for (int p = 0; p < N; ++p) row[p] = (float)x[p];
+}
+
+// Solve run s of a tensor and write its coefficient row (fp32).
+__device__ void solve_run(const TDesc &td, uint32_t s, const double *mom) {
+    const uint32_t D = td.deff, N = D + 1;
+    float *row;
+    if (td.in.coef) {
+        row = td.in.coef + (uint64_t)s * td.in.coef_stride;
+        for (uint32_t p = N; p < td.in.coef_stride; ++p) row[p] = 0.0f;
+    } else {
+        row = (float *)(td.in.rec + td.coef_off) + (uint64_t)s * N;
+    }
+    double m[NMOM];
+    for (uint32_t e = 0; e < NMOM; ++e) m[e] = mom[e];
+    switch (D) {
+        case 0: solve_normal<0>(m, row); break;
+        case 1: solve_normal<1>(m, row); break;
+        case 2: solve_normal<2>(m, row); break;
+        case 3: solve_normal<3>(m, row); break;
+        case 4: solve_normal<4>(m, row); break;
+        case 5: solve_normal<5>(m, row); break;
+        case 6: solve_normal<6>(m, row); break;
+        default: solve_normal<7>(m, row); break;
+    }
 }
 
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s) {
     if (fit_blocks == 0) return hipSuccess;
     k_fit_moments<<<fit_blocks, NTHREADS, 0, s>>>(w);
-    const uint32_t runs = fit_blocks / FIT_CHUNKS;
-    k_fit_solve<<<(runs + 63) / 64, 64, 0, s>>>(w, runs);
+    trace_mark(s, "k_fit_moments");
     return hipGetLastError();
 }
 
@@ -471,6 +543,7 @@ __global__ __launch_bounds__(NTHREADS) void k_sigma_pack(Work w) {
 
 hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s) {
     k_sigma_pack<<<grid_persist, NTHREADS, 0, s>>>(w);
+    trace_mark(s, "k_sigma_pack");
     return hipGetLastError();
 }
 
@@ -511,6 +584,7 @@ __global__ __launch_bounds__(NTHREADS) void k_curvefit_decode(Work w, const floa
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
                                   uint64_t n_cap, float *vals_out, int grid_persist, hipStream_t s) {
     k_curvefit_decode<<<grid_persist, NTHREADS, 0, s>>>(w, coef, sigma, n, n_cap, vals_out);
+    trace_mark(s, "k_curvefit_decode");
     return hipGetLastError();
 }
 
@@ -527,33 +601,13 @@ __global__ void k_export_n(Work w, uint64_t *n_out, int field) {
 
 hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, hipStream_t s) {
     k_import_n<<<1, 1, 0, s>>>(w, n, n_cap);
+    trace_mark(s, "k_import_n");
     return hipGetLastError();
 }
 
 hipError_t launch_export_n(const Work &w, uint64_t *n_out, int field, hipStream_t s) {
     k_export_n<<<1, 1, 0, s>>>(w, n_out, field);
-    return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Per-tensor counts for the caller
-// ---------------------------------------------------------------------------
-__global__ void k_counts(Work w, uint64_t *out, int which) {
-    const uint32_t t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= w.ntensors) return;
-    const TDesc &td = w.td[t];
-    if (which == 0) {
-        out[4 * t + 0] = td.n;
-        out[4 * t + 1] = td.nv;
-        out[4 * t + 3] = td.flags;
-    } else {
-        out[4 * t + 2] = td.nv_dec;
-        out[4 * t + 3] |= td.flags & FLAG_DEC_MISMATCH;
-    }
-}
-
-hipError_t launch_counts(const Work &w, uint64_t *counts_out, int which, hipStream_t s) {
-    k_counts<<<(w.ntensors + 255) / 256, 256, 0, s>>>(w, counts_out, which);
+    trace_mark(s, "k_export_n");
     return hipGetLastError();
 }
 

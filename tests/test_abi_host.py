@@ -36,7 +36,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 15
     assert sorted(names) == sorted(B.EXPORTS)
     for n in names:
         assert hasattr(L, n), n
@@ -151,6 +151,10 @@ def test_standalone_calls_reject_bad_arguments(L):
     assert L.dr_curvefit_encode(FAKE, FAKE, 1 << 32, 5, 8, FAKE, FAKE, FAKE, big, None) == B.DR_EINVAL
     assert L.dr_curvefit_decode(FAKE, FAKE, FAKE, 10, 8, 1, FAKE, FAKE, big, None) == B.DR_EINVAL
     assert L.dr_curvefit_decode(FAKE, FAKE, None, 10, 5, 1, FAKE, FAKE, big, None) == B.DR_EINVAL
+
+
+def test_trace_end_without_begin_is_rejected(L):
+    assert L.dr_trace_end(None, 0) == B.DR_EINVAL
 
 
 def test_parse_record_roundtrips_a_synthetic_header():
