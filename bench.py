@@ -37,22 +37,63 @@ def log(*a):
 def kernel_models(d, payload_bytes, n_sel, n_val, k, fill):
     """Algorithmic work of the dominant-kernel candidates, per launch.
 
-    HBM kernels: bytes the step must move.  The full-range query is integer
-    arithmetic: each index costs the seed-free half of MurmurHash3 (3 ops:
-    multiply, rotate, multiply) plus, per probe, the seeded half and the bit
-    test (seed xor, rotate, multiply-add, length xor, three xor-shifts, two
-    multiplies, the range multiply, shift and mask: 16 ops).  A non-member
-    is probed until its first clear bit, (1 - f^k)/(1 - f) probes for filter
-    fill f; a positive takes k probes."""
-    probes_nonmember = (1 - fill**k) / (1 - fill) if fill < 1 else k
-    query_ops = d * 3 + (d - n_val) * 16 * probes_nonmember + n_val * 16 * k
+    Streaming kernels are priced in the bytes they must move.  The two
+    full-range queries are priced in 32-bit integer lane operations: each
+    index costs the seed-free half of MurmurHash3 (multiply, rotate,
+    multiply: 3 ops) and each probe the seeded half plus the bit test (seed
+    xor, rotate, multiply-add, length xor, three xor-shifts, two multiplies,
+    the range multiply, word shift, bit shift and mask: 16 ops).  A
+    non-member is probed until its first clear bit, (1 - f^k)/(1 - f) probes
+    at filter fill f; a positive takes all k.  The sender skips the selected
+    set S, whose members it already knows."""
+    pn = (1 - fill**k) / (1 - fill) if fill < 1 else k
+    enc_ops = (d - n_sel) * 3 + (d - n_val) * 16 * pn + (n_val - n_sel) * 16 * k
+    dec_ops = d * 3 + (d - n_val) * 16 * pn + n_val * 16 * k
     return {
+        "k_probe<Q_ENCODE>": ("alu", enc_ops),
+        "k_probe<Q_DECODE>": ("alu", dec_ops),
         "k_topr_hist": ("hbm", 4.0 * d),
         "k_select_filter": ("hbm", 4.0 * d + d / 8.0),
-        "k_query<Q_DECODE>": ("hbm", 4.0 * d + payload_bytes),
-        "k_query<Q_ENCODE>": ("alu", query_ops),
-        "k_query<Q_DECODE>:alu": ("alu", query_ops),
+        "k_emit<Q_DECODE>": ("hbm", 4.0 * d + d / 8.0 + payload_bytes),
     }
+
+
+def read_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload`, from the committed
+    rocprofv3 counter summary, if that summary was taken on the current
+    kernel sources; None otherwise."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"pmc_{_slug(kernel)}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(" "):
+            key, val = line.split(":", 1)
+            fields[key.strip()] = val.strip()
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2102_03112_amd", "csrc"))):
+        h.update(open(os.path.join(ROOT, "paper_2102_03112_amd", "csrc", f), "rb").read())
+    if fields.get("csrc_sha256") != h.hexdigest()[:16] or "traffic_bytes_per_launch" not in fields:
+        return None
+    return float(fields["traffic_bytes_per_launch"])
+
+
+def _slug(kernel):
+    return kernel.replace("<", "_").replace(">", "").replace("Q_", "").lower()
+
+
+def copy_calibration(n_bytes=1 << 30, reps=5):
+    """A plain device copy of known size, for scaling the HBM counters."""
+    import torch
+
+    x = torch.ones(n_bytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n_bytes, "copy_bytes_written": n_bytes, "reps": reps}), flush=True)
 
 
 def main():
@@ -63,6 +104,8 @@ def main():
     ap.add_argument("--workload", default="resnet50_25m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=30.0, help="bound on the oracle's CPU time")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (the reference kernel for HBM counter scaling)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -78,6 +121,9 @@ def main():
 
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
+    if args.copy_calibration:
+        copy_calibration()
+        return
     B.lib()  # fail loudly if the HIP library is missing
     w = W.WORKLOADS[args.workload]
     d = w.d
@@ -150,21 +196,17 @@ def main():
     per_step = {name: tot / args.steps for name, (cnt_, tot) in tr.items()}
     dom = max(per_step, key=per_step.get)
     models = kernel_models(d, used, n_sel, n_val, kk, fill)
-    roof = None
+    roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
+            "traffic": None}
     if dom in models:
         bound, work = models[dom]
         avg_s = kern[dom][1] * 1e-3
-        if bound == "hbm":
-            ach = work / avg_s / 1e9
-            roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9,
-                    "unit": "GB/s", "frac": round(ach / (HBM_PEAK / 1e9), 4), "traffic": None}
-        else:
-            ach = work / avg_s / 1e9
-            roof = {"kernel": dom, "bound": "alu", "achieved": round(ach, 1), "peak": INT_PEAK / 1e9,
-                    "unit": "Gop/s", "frac": round(ach / (INT_PEAK / 1e9), 4), "traffic": None}
-    else:
-        roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
-                "traffic": None}
+        ach = work / avg_s / 1e9
+        peak = HBM_PEAK / 1e9 if bound == "hbm" else INT_PEAK / 1e9
+        roof.update(bound=bound, achieved=round(ach, 1), peak=peak, unit="GB/s" if bound == "hbm" else "Gop/s",
+                    frac=round(ach / peak, 4), work_per_launch=work, avg_launch_ms=round(kern[dom][1], 5),
+                    launches_per_step=kern[dom][0] / args.steps)
+    roof["traffic"] = read_traffic(dom, w.name)
     log("bench: kernel ms per step: " + ", ".join(f"{k}={v:.4f}" for k, v in sorted(per_step.items(),
                                                                                       key=lambda x: -x[1])))
 

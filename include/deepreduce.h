@@ -69,8 +69,11 @@ typedef enum {
 #define DR_MAX_SEGMENTS 4096 /* most segments per tensor */
 #define DR_MAX_TENSORS 65536 /* most tensors in one round trip */
 
-/* Round-trip flags word bits (dr_roundtrip / dr_payload_encode counts). */
-#define DR_FLAG_NONFINITE 1u /* the tensor held NaN or Inf */
+/* Bits of the per-tensor flags word (slot 3 of counts_out). */
+#define DR_FLAG_NONFINITE 1u    /* the tensor held NaN or Inf */
+#define DR_FLAG_DEC_MISMATCH 2u /* receiver: the record is invalid, or its |P| differs from the header */
+#define DR_FLAG_COUNT 4u        /* sender: the selection does not hold exactly r elements */
+#define DR_FLAG_CAPACITY 8u     /* a device-side capacity was exceeded; the output is incomplete */
 
 /* ---------------------------------------------------------------------- */
 /* Host-only helpers                                                       */
@@ -200,7 +203,8 @@ DR_EXPORT dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, ui
  * off P).  idx_out / val_out (nullable, d entries) receive tensor t's
  * positives (local indices) and their values at [offsets_h[t], offsets_h[t]
  * + |P_t|).  counts_out (nullable): slot 2 of each tensor receives the
- * receiver's |P|; slot 3 gains bit 2 if it disagrees with the header. */
+ * receiver's |P|; slot 3 gains DR_FLAG_DEC_MISMATCH if it disagrees with
+ * the header or the record is invalid (an invalid record decodes as empty). */
 DR_EXPORT dr_status dr_payload_decode(const uint8_t *payload, const dr_config *cfg_h, float *dense_out, uint32_t *idx_out,
                             float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream);
 

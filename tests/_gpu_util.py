@@ -6,6 +6,7 @@ import sys
 import numpy as np
 
 import oracle
+from paper_2102_03112_amd import binding as B
 
 
 def log(*a):
@@ -17,6 +18,12 @@ def dev_tensor(a: np.ndarray):
     import torch
 
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def sync():
+    import torch
+
+    torch.cuda.synchronize()
 
 
 def host(t) -> np.ndarray:
@@ -70,3 +77,71 @@ def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     coef_close(np.ascontiguousarray(c_gpu).ravel(), np.ascontiguousarray(c_ref).ravel(), rec.seg_eff, nc, nc)
     words = (ref.fit.n * ref.fit.b + 31) // 32
     assert rec.rec_bytes == 64 + ref.m // 8 + 4 * rec.seg_eff * nc + 4 * words
+
+
+_WS = {}
+
+
+def workspace(d, n_tensors=1):
+    """A cached device workspace of at least dr_workspace_bytes(d, n_tensors)."""
+    need = B.workspace_bytes(d, n_tensors)
+    cur = _WS.get("ws")
+    if cur is None or cur.numel() < need:
+        _WS["ws"] = None
+        import torch
+
+        torch.cuda.empty_cache()
+        _WS["ws"] = B.workspace(max(d, 1 << 20), n_tensors)
+    return _WS["ws"]
+
+
+def release_workspace():
+    _WS.clear()
+    import torch
+
+    torch.cuda.empty_cache()
+
+
+def run_roundtrip(g, cfg: B.Config):
+    import torch
+
+    total, rec_off = B.payload_layout(cfg)
+    d = cfg.d
+    gd = dev_tensor(g) if d else torch.zeros(1, dtype=torch.float32, device="cuda")
+    payload = torch.zeros(total, dtype=torch.uint8, device="cuda")
+    dense = torch.full((max(d, 1),), 9.0, dtype=torch.float32, device="cuda")
+    idx = torch.full((max(d, 1),), -1, dtype=torch.int32, device="cuda")
+    val = torch.zeros(max(d, 1), dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4 * cfg.n_tensors, dtype=torch.int64, device="cuda")
+    ws = workspace(max(d, 1), cfg.n_tensors)
+    B.roundtrip(gd, cfg, payload, dense, idx, val, counts, ws)
+    sync()
+    return dict(payload=host(payload), rec_off=rec_off, dense=host(dense)[:d], idx=host(idx)[:d].view(np.uint32),
+                val=host(val)[:d], counts=host(counts).reshape(cfg.n_tensors, 4))
+
+
+def check_roundtrip(g, cfg: B.Config, out, refs):
+    off = cfg.offsets
+    for t, ref in enumerate(refs):
+        a, b = int(off[t]), int(off[t + 1])
+        rec = B.parse_record(out["payload"], out["rec_off"][t])
+        check_record(rec, ref, cfg.degree, cfg.n_seg)
+        n_sel, nv, nv_dec, flags = [int(x) for x in out["counts"][t]]
+        assert (n_sel, nv, nv_dec, flags) == (ref.S.size, ref.P.size, ref.P.size, 0)
+        np.testing.assert_array_equal(out["idx"][a: a + nv], ref.P_dec)
+        # receiver values vs the oracle's decode of this very payload
+        y_same = oracle.curvefit_decode(rec.coef if rec.seg_eff else np.zeros(0, np.float32),
+                                        rec.sigma, nv, rec.deg_eff, max(rec.seg_eff, 1)) if nv else np.zeros(0)
+        if nv:
+            ranks = oracle.sigma_unpack(rec.sigma, nv)
+            values_close(out["val"][a: a + nv], y_same, ranks, nv, rec.seg_eff)
+            # and vs the oracle's own end-to-end reconstruction
+            values_close(out["val"][a: a + nv], ref.vals, ranks, nv, rec.seg_eff)
+        dense = out["dense"][a:b]
+        pos = ref.P_dec.astype(np.int64)
+        np.testing.assert_array_equal(dense[pos], out["val"][a: a + nv])
+        offp = np.ones(b - a, bool)
+        offp[pos] = False
+        assert np.all(dense[offp] == 0)
+
+

@@ -13,26 +13,13 @@ import pytest
 import oracle
 from paper_2102_03112_amd import binding as B
 from paper_2102_03112_amd import workloads as W
-from _gpu_util import check_record, coef_close, dev_tensor, host, log, u64_scalar, values_close
+from _gpu_util import (check_roundtrip, coef_close, dev_tensor, host, log, run_roundtrip, sync, u64_scalar,
+                       values_close, workspace)
 
 pytestmark = pytest.mark.gpu
 
-_WS = {}
-
-
 def ws_for(d, n_tensors=1):
-    need = B.workspace_bytes(d, n_tensors)
-    cur = _WS.get("ws")
-    if cur is None or cur.numel() < need:
-        _WS["ws"] = None
-        _WS["ws"] = B.workspace(max(d, 1 << 20), n_tensors)
-    return _WS["ws"]
-
-
-def sync():
-    import torch
-
-    torch.cuda.synchronize()
+    return workspace(d, n_tensors)
 
 
 def gen(kind, d, seed):
@@ -219,49 +206,6 @@ def test_curvefit_parity(n, D, S):
 # ---------------------------------------------------------------------------
 # dr_roundtrip over a gradient split into tensors
 # ---------------------------------------------------------------------------
-def run_roundtrip(g, cfg: B.Config):
-    import torch
-
-    total, rec_off = B.payload_layout(cfg)
-    d = cfg.d
-    gd = dev_tensor(g) if d else torch.zeros(1, dtype=torch.float32, device="cuda")
-    payload = torch.zeros(total, dtype=torch.uint8, device="cuda")
-    dense = torch.full((max(d, 1),), 9.0, dtype=torch.float32, device="cuda")
-    idx = torch.full((max(d, 1),), -1, dtype=torch.int32, device="cuda")
-    val = torch.zeros(max(d, 1), dtype=torch.float32, device="cuda")
-    counts = torch.zeros(4 * cfg.n_tensors, dtype=torch.int64, device="cuda")
-    ws = ws_for(max(d, 1), cfg.n_tensors)
-    B.roundtrip(gd, cfg, payload, dense, idx, val, counts, ws)
-    sync()
-    return dict(payload=host(payload), rec_off=rec_off, dense=host(dense)[:d], idx=host(idx)[:d].view(np.uint32),
-                val=host(val)[:d], counts=host(counts).reshape(cfg.n_tensors, 4))
-
-
-def check_roundtrip(g, cfg: B.Config, out, refs):
-    off = cfg.offsets
-    for t, ref in enumerate(refs):
-        a, b = int(off[t]), int(off[t + 1])
-        rec = B.parse_record(out["payload"], out["rec_off"][t])
-        check_record(rec, ref, cfg.degree, cfg.n_seg)
-        n_sel, nv, nv_dec, flags = [int(x) for x in out["counts"][t]]
-        assert (n_sel, nv, nv_dec, flags) == (ref.S.size, ref.P.size, ref.P.size, 0)
-        np.testing.assert_array_equal(out["idx"][a: a + nv], ref.P_dec)
-        # receiver values vs the oracle's decode of this very payload
-        y_same = oracle.curvefit_decode(rec.coef if rec.seg_eff else np.zeros(0, np.float32),
-                                        rec.sigma, nv, rec.deg_eff, max(rec.seg_eff, 1)) if nv else np.zeros(0)
-        if nv:
-            ranks = oracle.sigma_unpack(rec.sigma, nv)
-            values_close(out["val"][a: a + nv], y_same, ranks, nv, rec.seg_eff)
-            # and vs the oracle's own end-to-end reconstruction
-            values_close(out["val"][a: a + nv], ref.vals, ranks, nv, rec.seg_eff)
-        dense = out["dense"][a:b]
-        pos = ref.P_dec.astype(np.int64)
-        np.testing.assert_array_equal(dense[pos], out["val"][a: a + nv])
-        offp = np.ones(b - a, bool)
-        offp[pos] = False
-        assert np.all(dense[offp] == 0)
-
-
 RT_CASES = {
     "resnet20_conv_37k": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 8),
     "student_t_3x": (None, None, (1, 100), 1e-3, 5, 8),
@@ -304,3 +248,61 @@ def test_roundtrip_is_deterministic():
     b = run_roundtrip(g, cfg)
     np.testing.assert_array_equal(a["payload"], b["payload"])
     np.testing.assert_array_equal(a["dense"], b["dense"])
+
+
+def test_sender_and_receiver_separately():
+    """dr_payload_encode then dr_payload_decode into fresh buffers: the
+    receiver needs nothing but the payload and the tensor layout."""
+    import torch
+
+    w = W.Workload("t", 200_003, 2, (1, 100), 1e-3, 5, 8, "laplace_5e-4", 11)
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w)
+    total, rec_off = B.payload_layout(cfg)
+    ws = workspace(w.d, 2)
+    payload = torch.zeros(total, dtype=torch.uint8, device="cuda")
+    counts = torch.zeros(8, dtype=torch.int64, device="cuda")
+    B.payload_encode(dev_tensor(g), cfg, payload, counts, ws)
+    sync()
+    sent = host(payload).copy()
+    # a different workspace and a copy of the payload on the receiver side
+    ws2 = B.workspace(w.d, 2)
+    payload2 = dev_tensor(sent)
+    dense = torch.full((w.d,), 3.0, dtype=torch.float32, device="cuda")
+    counts2 = torch.zeros(8, dtype=torch.int64, device="cuda")
+    B.payload_decode(payload2, cfg, dense, None, None, counts2, ws2)
+    sync()
+    rt = run_roundtrip(g, cfg)
+    np.testing.assert_array_equal(host(dense), rt["dense"])
+    np.testing.assert_array_equal(sent, rt["payload"])
+    c1, c2 = host(counts).reshape(2, 4), host(counts2).reshape(2, 4)
+    np.testing.assert_array_equal(c2[:, 2], c1[:, 1])
+    assert np.all(c2[:, 3] == 0)
+
+
+def test_receiver_flags_a_damaged_header():
+    import torch
+
+    w = W.Workload("t", 50_000, 1, (1, 100), 1e-3, 5, 8, "normal_1e-3", 12)
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w)
+    rt = run_roundtrip(g, cfg)
+    bad = rt["payload"].copy()
+    bad[0] ^= 0xFF  # magic
+    dense = torch.full((w.d,), 3.0, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    B.payload_decode(dev_tensor(bad), cfg, dense, None, None, counts, workspace(w.d))
+    sync()
+    assert int(host(counts)[3]) & B.FLAG_DEC_MISMATCH
+    assert np.all(host(dense) == 0)  # an invalid record decodes as empty
+
+
+def test_per_kernel_trace():
+    w = W.WORKLOADS["resnet20_conv_37k"]
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w)
+    B.trace_begin()
+    run_roundtrip(g, cfg)
+    tr = B.trace_end()
+    assert "k_probe<Q_ENCODE>" in tr and "k_emit<Q_DECODE>" in tr
+    assert all(n >= 1 and ms >= 0 for n, ms in tr.values())
