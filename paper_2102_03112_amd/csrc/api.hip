@@ -42,7 +42,6 @@ dr_status hip_fail(hipError_t e, const char *where) {
     } while (0)
 
 constexpr uint32_t MAX_SLICES = 16384;  // LDS counters of the insert: filters up to 2^30 bits
-constexpr uint32_t POS_PER_ELEM = 12;   // Bloom positions the workspace holds per padded element
 
 uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
 uint64_t align_up(uint64_t a, uint64_t b) { return ceil_div(a, b) * b; }
@@ -185,11 +184,12 @@ Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     c.hist_blocks = c.ntiles / 16 + 2 * n_tensors;
     const uint64_t runs = n_tensors * (uint64_t)DR_MAX_SEGMENTS;
     c.fit_blocks = (runs < d + n_tensors ? runs : d + n_tensors) * FIT_CHUNKS;
-    // Bloom table: per tensor (slices x chunks) with chunks <= max(257, tiles/16 + 1) and
-    // m <= 2 k n <= 2 POS_PER_ELEM slots bits; plus one filter of MAX_SLICES
+    // Bloom table: per tensor (slices x chunks) with at most MAX_CHUNKS
+    // chunks and ceil(m / 2^14) slices, where m <= 47 n + 32 (k <= 32 gives
+    // -ln(fpr) / (ln 2)^2 < 47 bits per item); plus one filter of MAX_SLICES
     // for a standalone insert whose filter is larger than its item count
-    c.bslices = 2 * c.slots * POS_PER_ELEM / (1u << 14) + 2 * n_tensors + MAX_SLICES;
-    c.btab = c.bslices * (257 + c.ntiles / CHUNK_TILES);
+    c.bslices = 47 * c.slots / (1u << 14) + 2 * n_tensors + MAX_SLICES;
+    c.btab = c.bslices * MAX_CHUNKS;
     c.plan();
     return c;
 }
@@ -203,17 +203,18 @@ struct Plan {
     bool any_topr = false;
 };
 
-// Per-tensor Bloom insert layout for at most n_cap items and m_cap_bits.
-// From the bitmap, a chunk is CHUNK_TILES tiles of it; from a list, a chunk
-// is bl_chunk items.
+// Per-tensor Bloom insert layout for at most n_cap items and m_cap_bits:
+// at most MAX_CHUNKS chunks of items, each a run of bitmap tiles (at least
+// CHUNK_TILES) or of list entries (at least 1024).
 
 void plan_bloom(TInit &in, uint64_t n_cap, uint64_t m_cap_bits, bool from_bitmap, Plan &p) {
     p.bl_ncap.push_back(n_cap);
     if (from_bitmap) {
-        in.bl_chunk = 0;
-        in.bl_nchunks = (uint32_t)ceil_div(in.ntiles, CHUNK_TILES);
+        const uint64_t chunk = std::max<uint64_t>(CHUNK_TILES, ceil_div(in.ntiles, MAX_CHUNKS));
+        in.bl_chunk = (uint32_t)chunk;
+        in.bl_nchunks = (uint32_t)ceil_div(in.ntiles, chunk);
     } else {
-        const uint64_t chunk = n_cap / 256 > 1024 ? ceil_div(n_cap, 256) : 1024;
+        const uint64_t chunk = std::max<uint64_t>(1024, ceil_div(n_cap, MAX_CHUNKS));
         in.bl_chunk = (uint32_t)chunk;
         in.bl_nchunks = (uint32_t)(n_cap ? ceil_div(n_cap, chunk) : 0);
     }

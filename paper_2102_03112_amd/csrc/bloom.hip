@@ -2,10 +2,10 @@
 //
 // Insert: every selected index s sets bits h_j(s), j < k.  Device-wide
 // atomics into a filter larger than a CU's LDS are slow on this GPU, so the
-// insert buckets the k n bit positions by 2^16-bit slice of the filter
-// (count, scan, scatter), and one block per slice then sets its bits in
-// LDS and writes the slice out whole.  OR is commutative, so the filter
-// does not depend on the order of any of this.
+// insert buckets the k n bit positions by slice of the filter (2^14 or
+// 2^16 bits; count, scan, scatter), and one block per slice then sets its
+// bits in LDS and writes the slice out whole.  OR is commutative, so the
+// filter does not depend on the order of any of this.
 //
 // Query (policy P0, Section 4): every i of the tensor's index range whose k
 // bits are all set is a positive, reported in ascending order.  Each wave
@@ -13,7 +13,9 @@
 // j only the indices still alive are kept, compacted into an LDS queue in
 // index order (ballot + mbcnt), so lanes do not idle while a few indices
 // need many probes.  The key-dependent half of MurmurHash3 is computed once
-// per index.  Tiles chain their positive counts with a decoupled look-back.
+// per index.  The probe kernel writes a positives bitmap and per-tile
+// counts; after a per-tensor scan of the counts, the emit kernel writes the
+// positives in order.
 #include "launch.hpp"
 
 namespace dr {
@@ -22,8 +24,8 @@ namespace dr {
 // Insert
 // ---------------------------------------------------------------------------
 // The items come either from the selection bitmap (the round trip: chunk c
-// of a tensor is its bitmap tiles [c * CHUNK_TILES, (c+1) * CHUNK_TILES))
-// or from a list of indices (chunk c is items [c * bl_chunk, ...)).
+// of a tensor is its bitmap tiles [c * bl_chunk, (c+1) * bl_chunk)) or from
+// a list of indices (chunk c is items [c * bl_chunk, (c+1) * bl_chunk)).
 
 __device__ __forceinline__ uint32_t tensor_of_chunk(const Work &w, uint32_t c) {
     uint32_t lo = 0, hi = w.ntensors;
@@ -53,8 +55,8 @@ __device__ __forceinline__ uint32_t tensor_of_slice(const Work &w, uint32_t s) {
 template <bool FROM_BITMAP, typename F>
 __device__ __forceinline__ void for_chunk_items(const Work &w, const TDesc &td, uint32_t c, F f) {
     if (FROM_BITMAP) {
-        const uint32_t w0 = c * CHUNK_TILES * TILE_WORDS;
-        const uint32_t w1 = min(td.in.ntiles * TILE_WORDS, w0 + CHUNK_TILES * TILE_WORDS);
+        const uint32_t w0 = c * td.in.bl_chunk * TILE_WORDS;
+        const uint32_t w1 = min(td.in.ntiles * TILE_WORDS, w0 + td.in.bl_chunk * TILE_WORDS);
         const uint32_t *sb = w.selbits + (td.in.slot >> 5);
         for (uint32_t x = w0 + threadIdx.x; x < w1; x += NTHREADS) {
             uint32_t word = sb[x];

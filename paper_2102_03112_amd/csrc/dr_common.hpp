@@ -23,7 +23,8 @@ constexpr uint32_t TILE_WORDS = TILE / 32;    // bitmap words per tile
 constexpr uint32_t NTHREADS = 256;            // threads per block (4 waves of 64)
 constexpr uint32_t NWAVES = NTHREADS / 64;
 constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
-constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: tiles per chunk
+constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: fewest tiles per chunk
+constexpr uint32_t MAX_CHUNKS = 256;          // Bloom insert: most item chunks per tensor
 constexpr uint32_t SLICE_LOG2_MAX = 16;       // Bloom fill slices: at most 2^16 bits (8 KiB of LDS)
 constexpr uint32_t SLICE_WORDS_MAX = (1u << SLICE_LOG2_MAX) / 32;
 constexpr uint32_t HIST1_BITS = 11;           // first top-r digit: key bits 30..20
@@ -57,7 +58,7 @@ struct TInit {
     uint32_t nseg;       // requested runs
     uint32_t m_words_in; // filter words fixed by the caller, or 0: derive from n
     uint32_t fit_blk0;   // first block of this tensor in the fit grid
-    uint32_t bl_chunk;   // Bloom insert: items per chunk
+    uint32_t bl_chunk;   // Bloom insert: bitmap tiles (from the bitmap) or items (from a list) per chunk
     uint32_t bl_chunk0;  // first Bloom chunk of this tensor
     uint32_t bl_nchunks; // Bloom chunks reserved for this tensor
     uint32_t bl_slice0;  // first Bloom slice of this tensor
