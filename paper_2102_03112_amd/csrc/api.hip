@@ -68,18 +68,7 @@ uint32_t sigma_bits_host(uint64_t n) {
     return b;
 }
 
-int persist_grid(int per_cu) {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-            cus = v;
-        else
-            cus = 256;
-    }
-    return cus * per_cu;
-}
+int persist_grid(int per_cu) { return dr::device_cus() * per_cu; }
 
 // Workspace regions, in carve order.  Element-sized regions have `slots`
 // entries (padded elements); the last six are contiguous so the Bloom insert
@@ -484,6 +473,20 @@ void trace_call(hipStream_t s) { trace_record(s, nullptr); }
 }  // namespace
 
 namespace dr {
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static int cus[64] = {0};
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    const int slot = dev < 64 ? dev : 63;
+    if (cus[slot] == 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            cus[slot] = v;
+        else
+            cus[slot] = 256;
+    }
+    return cus[slot];
+}
 void trace_mark(hipStream_t s, const char *kernel) { trace_record(s, kernel); }
 }  // namespace dr
 

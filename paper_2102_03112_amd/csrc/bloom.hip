@@ -322,126 +322,191 @@ __device__ __forceinline__ float eval_rank(const float *coef, uint32_t rank, uin
     return (float)y;
 }
 
-constexpr uint32_t QWAVE = 1024;  // indices per wave per tile
+constexpr uint32_t QWAVE = 1024;             // indices per wave per step
+constexpr uint32_t PB_THREADS = 1024;        // probe block: 16 waves, one block per CU
+constexpr uint32_t PB_WAVES = PB_THREADS / 64;
+constexpr uint32_t PB_TILES = PB_WAVES * QWAVE / TILE;  // tiles one block probes per step
+constexpr uint32_t FC_WORDS = 30720;         // filter words kept in LDS (120 KiB)
+
+// The filter a tile is probed against: the sender's freshly built filter,
+// the caller's (plain decode), or the payload record's (receiver).
+__device__ __forceinline__ RecordView query_filter(const Work &w, const QueryOut &o, TDesc &td, int mode, bool *ok) {
+    RecordView rv;
+    *ok = true;
+    if (mode == Q_DECODE) {
+        rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, td.in.d, ok);
+    } else {
+        rv.bits = td.in.bits;
+        rv.m_bits = td.m_words * 32u;
+        rv.k = td.in.k;
+    }
+    return rv;
+}
+
+// Raw buffer view of a tensor's filter words.  A buffer load whose offset
+// lies past the view returns 0 without touching memory, which lets the probe
+// issue its global reads unconditionally, in batches, and still skip the
+// words it holds in LDS.
+// The caller guarantees that bits and m_bits are the same on every lane of
+// the wave; readfirstlane states it, so the descriptor lives in scalar
+// registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t filter_rsrc(const uint32_t *bits, uint32_t m_bits) {
+    const uint64_t a = (uint64_t)(uintptr_t)bits;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    uint32_t *p = (uint32_t *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)__builtin_amdgcn_readfirstlane(m_bits / 8u),
+                                             BUFFER_RSRC_WORD3);
+}
+
+// One filter word: from the LDS copy of the filter's first `fcw` words, else
+// from global memory (an L2 hit: the filter is small and read by every CU).
+__device__ __forceinline__ uint32_t filter_word(const uint32_t *fc, uint32_t fcw, __amdgpu_buffer_rsrc_t rs,
+                                                uint32_t wi) {
+    const bool in_lds = wi < fcw;
+    const uint32_t l = fc[in_lds ? wi : 0u];
+    const uint32_t g = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, in_lds ? 0xfffffff0u : wi * 4u, 0, 0);
+    return in_lds ? l : g;
+}
 
 // Probe pass: the positives of each tile as a bitmap (pbits) and a count
 // (tcnt).  The sender already knows that its selected indices are
 // positives (S is a subset of P, Section 4), so it skips probing them.
+//
+// The random filter reads are this kernel's cost: they are L2 hits, and
+// the L2-to-CU line transfers bound it.  One 1024-thread block runs per CU
+// and keeps the first 120 KiB of the current tensor's filter in LDS, so
+// that share of the probes never leaves the CU (all of them for filters up
+// to 983,040 bits).  Each block owns a contiguous range of tiles, cut into
+// runs that stay inside one tensor; the LDS copy is reloaded only when a
+// run enters a new tensor.  Inside a run, waves take quarter tiles (1024
+// indices) from a shared counter, so they stay busy until the run ends.
+constexpr uint32_t RUN_TILES = 512;  // most tiles per run (LDS tile counters)
+
 template <int MODE>
-__global__ __launch_bounds__(NTHREADS) void k_probe(Work w, QueryOut o) {
-    __shared__ uint16_t qe[NWAVES][QWAVE];
-    __shared__ uint32_t qk[NWAVES][QWAVE];
-    __shared__ uint32_t lw[NWAVES][QWAVE / 32];
-    __shared__ uint32_t wcount[NWAVES];
-    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
-    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
+__global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
+    __shared__ uint32_t fc[FC_WORDS];
+    __shared__ uint16_t qe[PB_WAVES][QWAVE];
+    __shared__ uint32_t lw[PB_WAVES][QWAVE / 32];
+    __shared__ uint32_t tcl[RUN_TILES];
+    __shared__ uint32_t next;
+    // the wave index is uniform across the wave; saying so keeps everything
+    // derived from it in scalar registers
+    const uint32_t lane = threadIdx.x & 63u, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    constexpr uint32_t QPT = TILE / QWAVE;  // quarters per tile
+    const uint32_t per = (w.ntiles_total + gridDim.x - 1) / gridDim.x;
+    const uint32_t t_begin = min(w.ntiles_total, blockIdx.x * per);
+    const uint32_t t_end = min(w.ntiles_total, t_begin + per);
+    uint32_t cached = 0xffffffffu, fcw = 0;
+    for (uint32_t rb = t_begin; rb < t_end;) {
+        const uint32_t t = tensor_of_tile(w.td, w.ntensors, rb);
         TDesc &td = w.td[t];
-        const uint32_t lt = tile - td.in.tile0;
-        const uint32_t d = td.in.d;
-        RecordView rv;
-        if (MODE == Q_DECODE) {
-            bool ok = true;
-            rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, d, &ok);
-            if (!ok && threadIdx.x == 0) atomicOr(&td.flags, FLAG_DEC_MISMATCH);
-        } else {
-            rv.bits = td.in.bits;
-            rv.m_bits = td.m_words * 32u;
-            rv.k = td.in.k;
+        const uint32_t re = min(min(t_end, td.in.tile0 + td.in.ntiles), rb + RUN_TILES);
+        const uint32_t nq = (re - rb) * QPT;
+        bool ok;
+        const RecordView rv = query_filter(w, o, td, MODE, &ok);
+        __syncthreads();  // the previous run is finished with fc, tcl and next
+        if (t != cached) {
+            fcw = min(rv.m_bits / 32u, FC_WORDS);
+            for (uint32_t x = threadIdx.x; x < fcw; x += PB_THREADS) fc[x] = rv.bits[x];
+            cached = t;
         }
-        const uint32_t m_bits = rv.m_bits, k = rv.k;
-        const uint32_t *bits = rv.bits;
-        const uint32_t wbase = lt * TILE + wv * QWAVE;  // first index of this wave
+        for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) tcl[x] = 0;
+        if (threadIdx.x == 0) {
+            next = 0;
+            if (MODE == Q_DECODE && !ok) atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+        }
+        __syncthreads();
+        const uint32_t m_bits = rv.m_bits, k = rv.k, d = td.in.d;
+        const __amdgpu_buffer_rsrc_t bits = filter_rsrc(rv.bits, m_bits);
         uint16_t *me = qe[wv];
-        uint32_t *mk = qk[wv];
         uint32_t *mw = lw[wv];
-        if (lane < QWAVE / 32) mw[lane] = 0;
-        __builtin_amdgcn_wave_barrier();
-        // probe 0 over the wave's 1024 indices: 16 per lane, all gathers in
-        // flight before any is tested
-        uint32_t cnt = 0, known = 0;
-        uint32_t kmv[QWAVE / 64], wrd[QWAVE / 64], sel[QWAVE / 64];
-#pragma unroll
-        for (uint32_t c = 0; c < QWAVE / 64; ++c) {
-            const uint32_t i = wbase + c * 64 + lane;
-            kmv[c] = mm3_key(i);
-            const uint32_t p = bloom_pos(kmv[c], 0, m_bits);
-            // unconditional loads (p < m_bits, and i stays inside the tensor's
-            // slot), masked afterwards, so the compiler can batch them
-            const uint32_t word = bits[p >> 5] >> (p & 31u);
-            wrd[c] = (i < d && k > 0) ? word : 0u;
-            if (MODE == Q_ENCODE) {
-                const uint32_t sw = w.selbits[(td.in.slot + i) >> 5];
-                sel[c] = i < d ? sw : 0u;
-            }
-        }
-#pragma unroll
-        for (uint32_t c = 0; c < QWAVE / 64; ++c) {
-            const uint32_t e = c * 64 + lane;
-            const uint32_t i = wbase + e;
-            bool in_s = false;
-            if (MODE == Q_ENCODE) in_s = (sel[c] >> (i & 31u)) & 1u;
-            const bool hit = !in_s && (wrd[c] & 1u);
-            if (MODE == Q_ENCODE) {
-                const uint64_t sm = ballot(in_s);
-                if (lane < 2) mw[c * 2 + lane] |= (uint32_t)(sm >> (32 * lane));
-                known += popc64(sm);
-            }
-            const uint64_t mask = ballot(hit);
-            if (hit) {
-                const uint32_t at = cnt + lanes_below(mask);
-                me[at] = (uint16_t)e;
-                mk[at] = kmv[c];
-            }
-            cnt += popc64(mask);
-        }
-        // probes 1..k-1 over the survivors, compacting in place; four
-        // groups of 64 queue entries have their gathers in flight together
-        constexpr uint32_t G = 4;
-        for (uint32_t j = 1; j < k && cnt > 0; ++j) {
+        for (;;) {
+            uint32_t qi = 0;
+            if (lane == 0) qi = atomicAdd(&next, 1u);
+            qi = __builtin_amdgcn_readfirstlane(qi);
+            if (qi >= nq) break;
+            const uint32_t tile = rb + qi / QPT;
+            const uint32_t wbase = (tile - td.in.tile0) * TILE + (qi % QPT) * QWAVE;  // first index
+            if (lane < QWAVE / 32) mw[lane] = 0;
             __builtin_amdgcn_wave_barrier();
-            const uint32_t L = cnt;
-            cnt = 0;
-            for (uint32_t b0 = 0; b0 < L; b0 += 64 * G) {
-                uint32_t ev[G], kv[G], bw[G];
+            // probe 0 over the quarter's 1024 indices: 16 per lane, all
+            // reads in flight before any is tested
+            uint32_t cnt = 0, known = 0;
+            uint32_t wrd[QWAVE / 64], sel[QWAVE / 64];
 #pragma unroll
-                for (uint32_t u = 0; u < G; ++u) {
-                    const uint32_t x = b0 + u * 64 + lane;
-                    ev[u] = x < L ? me[x] : 0u;
-                    kv[u] = x < L ? mk[x] : 0u;
+            for (uint32_t c = 0; c < QWAVE / 64; ++c) {
+                const uint32_t i = wbase + c * 64 + lane;
+                const uint32_t p = bloom_pos(mm3_key(i), 0, m_bits);
+                // p < m_bits always, so the read is in bounds; i past the
+                // tensor's end stays inside its slot and is masked below
+                const uint32_t word = filter_word(fc, fcw, bits, p >> 5) >> (p & 31u);
+                wrd[c] = (i < d && k > 0) ? word : 0u;
+                if (MODE == Q_ENCODE) {
+                    const uint32_t sw = w.selbits[(td.in.slot + i) >> 5];
+                    sel[c] = i < d ? sw : 0u;
                 }
-#pragma unroll
-                for (uint32_t u = 0; u < G; ++u) {
-                    const uint32_t p = bloom_pos(kv[u], j, m_bits);
-                    const uint32_t word = bits[p >> 5] >> (p & 31u);
-                    bw[u] = (b0 + u * 64 + lane < L) ? word : 0u;
-                }
-                __builtin_amdgcn_wave_barrier();
-#pragma unroll
-                for (uint32_t u = 0; u < G; ++u) {
-                    const bool hit = bw[u] & 1u;
-                    const uint64_t mask = ballot(hit);
-                    if (hit) {
-                        const uint32_t at = cnt + lanes_below(mask);
-                        me[at] = (uint16_t)ev[u];
-                        mk[at] = kv[u];
-                    }
-                    cnt += popc64(mask);
-                }
-                __builtin_amdgcn_wave_barrier();
             }
+#pragma unroll
+            for (uint32_t c = 0; c < QWAVE / 64; ++c) {
+                const uint32_t e = c * 64 + lane;
+                bool in_s = false;
+                if (MODE == Q_ENCODE) in_s = (sel[c] >> (e & 31u)) & 1u;
+                const bool hit = !in_s && (wrd[c] & 1u);
+                if (MODE == Q_ENCODE) {
+                    const uint64_t sm = ballot(in_s);
+                    if (lane < 2) mw[c * 2 + lane] |= (uint32_t)(sm >> (32 * lane));
+                    known += popc64(sm);
+                }
+                const uint64_t mask = ballot(hit);
+                if (hit) me[cnt + lanes_below(mask)] = (uint16_t)e;
+                cnt += popc64(mask);
+            }
+            // probes 1..k-1 over the survivors, compacted in place in index
+            // order; four groups of 64 queue entries have their reads in
+            // flight together
+            constexpr uint32_t G = 4;
+            for (uint32_t j = 1; j < k && cnt > 0; ++j) {
+                __builtin_amdgcn_wave_barrier();
+                const uint32_t L = cnt;
+                cnt = 0;
+                for (uint32_t b0 = 0; b0 < L; b0 += 64 * G) {
+                    uint32_t ev[G], bw[G];
+#pragma unroll
+                    for (uint32_t u = 0; u < G; ++u) {
+                        const uint32_t x = b0 + u * 64 + lane;
+                        ev[u] = x < L ? me[x] : 0u;
+                    }
+#pragma unroll
+                    for (uint32_t u = 0; u < G; ++u) {
+                        const uint32_t p = bloom_pos(mm3_key(wbase + ev[u]), j, m_bits);
+                        const uint32_t word = filter_word(fc, fcw, bits, p >> 5) >> (p & 31u);
+                        bw[u] = (b0 + u * 64 + lane < L) ? word : 0u;
+                    }
+                    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                    for (uint32_t u = 0; u < G; ++u) {
+                        const bool hit = bw[u] & 1u;
+                        const uint64_t mask = ballot(hit);
+                        if (hit) me[cnt + lanes_below(mask)] = (uint16_t)ev[u];
+                        cnt += popc64(mask);
+                    }
+                    __builtin_amdgcn_wave_barrier();
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+            for (uint32_t x = lane; x < cnt; x += 64) {
+                const uint32_t e = me[x];
+                atomicOr(&mw[e >> 5], 1u << (e & 31u));
+            }
+            __builtin_amdgcn_wave_barrier();
+            if (lane < QWAVE / 32) w.pbits[(uint64_t)tile * TILE_WORDS + (qi % QPT) * (QWAVE / 32) + lane] = mw[lane];
+            if (lane == 0) atomicAdd(&tcl[qi / QPT], cnt + known);
+            __builtin_amdgcn_wave_barrier();
         }
-        __builtin_amdgcn_wave_barrier();
-        for (uint32_t x = lane; x < cnt; x += 64) {
-            const uint32_t e = me[x];
-            atomicOr(&mw[e >> 5], 1u << (e & 31u));
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (lane < QWAVE / 32) w.pbits[(uint64_t)tile * TILE_WORDS + wv * (QWAVE / 32) + lane] = mw[lane];
-        if (lane == 0) wcount[wv] = cnt + known;
         __syncthreads();
-        if (threadIdx.x == 0) w.tcnt[tile] = wcount[0] + wcount[1] + wcount[2] + wcount[3];
-        __syncthreads();
+        for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) w.tcnt[rb + x] = tcl[x];
+        rb = re;
     }
 }
 
@@ -519,10 +584,18 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
 }
 
 
+// One probe block per CU (its LDS holds a filter copy), each owning at
+// least PB_TILES tiles so that all of its waves have work.
+static int probe_grid(const Work &w) {
+    const uint32_t cus = (uint32_t)device_cus();
+    const uint32_t by_tiles = (w.ntiles_total + PB_TILES - 1) / PB_TILES;
+    return (int)max(1u, min(cus, by_tiles));
+}
+
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     QueryOut o{};
     o.g = g;
-    k_probe<Q_ENCODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_probe<Q_ENCODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_ENCODE>");
     hipError_t e = launch_tile_scan(w, 1, nullptr, s);
     if (e != hipSuccess) return e;
@@ -537,7 +610,7 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     o.idx_out = idx_out;
     o.cap = cap;
     o.n_out = n_out;
-    k_probe<Q_PLAIN><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_probe<Q_PLAIN><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_PLAIN>");
     hipError_t e = launch_tile_scan(w, 3, n_out, s);
     if (e != hipSuccess) return e;
@@ -554,7 +627,7 @@ hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *den
     o.dense_out = dense_out;
     o.idx_out = idx_out;
     o.val_out = val_out;
-    k_probe<Q_DECODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_probe<Q_DECODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_DECODE>");
     hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out, payload);
     if (e != hipSuccess) return e;

@@ -24,7 +24,8 @@ constexpr uint32_t NTHREADS = 256;            // threads per block (4 waves of 6
 constexpr uint32_t NWAVES = NTHREADS / 64;
 constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
 constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: fewest tiles per chunk
-constexpr uint32_t MAX_CHUNKS = 256;          // Bloom insert: most item chunks per tensor
+constexpr uint32_t MAX_CHUNKS = 256;
+constexpr int BUFFER_RSRC_WORD3 = 0x00020000;  // gfx9 buffer descriptor word 3 (32-bit dword format)          // Bloom insert: most item chunks per tensor
 constexpr uint32_t SLICE_LOG2_MAX = 16;       // Bloom fill slices: at most 2^16 bits (8 KiB of LDS)
 constexpr uint32_t SLICE_WORDS_MAX = (1u << SLICE_LOG2_MAX) / 32;
 constexpr uint32_t HIST1_BITS = 11;           // first top-r digit: key bits 30..20

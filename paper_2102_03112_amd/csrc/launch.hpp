@@ -9,6 +9,8 @@
 
 namespace dr {
 
+int device_cus();  // compute units of the current device
+
 // Opt-in per-kernel timing (dr_trace_begin / dr_trace_end): when tracing is
 // on for the calling host thread, an event is recorded on the stream after
 // each kernel launch; the time between consecutive events is that kernel's.
