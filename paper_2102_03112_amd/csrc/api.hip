@@ -14,6 +14,7 @@
 #include "launch.hpp"
 
 using namespace dr;
+static_assert(MAX_SEG == DR_MAX_SEGMENTS && MAX_DEG == DR_MAX_DEGREE, "limits of the header and the kernels");
 
 namespace {
 

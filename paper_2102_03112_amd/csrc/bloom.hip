@@ -289,37 +289,27 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     const uint64_t nv64 = *(const uint64_t *)(rec + 24);
     *ok = h[0] == HDR_MAGIC && h[1] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && m_bits < (1ull << 32) &&
           v.k >= 1 && v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && nv64 <= d &&
-          (v.nv == 0 || (v.seff >= 1 && v.seff <= v.nv && v.b >= sigma_bits(v.nv))) && need <= cap;
-    if (!*ok) {
+          (v.nv == 0 || (v.seff >= 1 && v.seff <= v.nv && v.seff <= MAX_SEG && v.b >= sigma_bits(v.nv))) &&
+          need <= cap;
+    if (!*ok) {  // nothing of an invalid record is read past its first filter word
         v.k = 0;
         v.nv = 0;
         v.m_bits = 32;
+        v.seff = 0;
+        v.deff = 0;
+        v.b = 1;
+        v.coef = (const float *)(rec + HDR_BYTES + 4);
     }
-    v.sigma = (const uint32_t *)(rec + coef_off + v.seff * (v.deff + 1u) * 4u);
+    v.sigma = (const uint32_t *)((const uint8_t *)v.coef + v.seff * (v.deff + 1u) * 4u);
     return v;
 }
 
-// entry q of a packed b-bit stream (b <= 32)
-__device__ __forceinline__ uint32_t sigma_get(const uint32_t *sig, uint32_t q, uint32_t b) {
-    const uint64_t bit = (uint64_t)q * b;
+// the b-bit entry at bit offset `bit` of a packed LSB-first stream (b <= 32)
+__device__ __forceinline__ uint32_t sigma_get(const uint32_t *sig, uint64_t bit, uint32_t b) {
     const uint32_t w0 = sig[bit >> 5], sh = (uint32_t)(bit & 31u);
     uint64_t v = w0 >> sh;
     if (sh + b > 32u) v |= (uint64_t)sig[(bit >> 5) + 1] << (32u - sh);
     return b == 32u ? (uint32_t)v : (uint32_t)(v & ((1ull << b) - 1ull));
-}
-
-// value of sorted rank `rank` among nv values fitted in seff runs of degree deff
-__device__ __forceinline__ float eval_rank(const float *coef, uint32_t rank, uint32_t nv, uint32_t seff,
-                                           uint32_t deff) {
-    // run s is the largest with floor(s nv / seff) <= rank
-    const uint64_t s = (((uint64_t)rank + 1u) * seff - 1u) / nv;
-    const uint64_t lo = s * nv / seff, hi = (s + 1) * nv / seff;
-    const uint64_t ns = hi - lo, j = rank - lo;
-    const double t = ns > 1 ? (double)(2 * (int64_t)j - (int64_t)(ns - 1)) / (double)(ns - 1) : 0.0;
-    const float *c = coef + s * (deff + 1u);
-    double y = (double)c[deff];
-    for (int p = (int)deff - 1; p >= 0; --p) y = y * t + (double)c[p];
-    return (float)y;
 }
 
 constexpr uint32_t QWAVE = 1024;             // indices per wave per step
@@ -343,29 +333,14 @@ __device__ __forceinline__ RecordView query_filter(const Work &w, const QueryOut
     return rv;
 }
 
-// Raw buffer view of a tensor's filter words.  A buffer load whose offset
-// lies past the view returns 0 without touching memory, which lets the probe
-// issue its global reads unconditionally, in batches, and still skip the
-// words it holds in LDS.
-// The caller guarantees that bits and m_bits are the same on every lane of
-// the wave; readfirstlane states it, so the descriptor lives in scalar
-// registers.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t filter_rsrc(const uint32_t *bits, uint32_t m_bits) {
-    const uint64_t a = (uint64_t)(uintptr_t)bits;
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-    uint32_t *p = (uint32_t *)(uintptr_t)(((uint64_t)hi << 32) | lo);
-    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)__builtin_amdgcn_readfirstlane(m_bits / 8u),
-                                             BUFFER_RSRC_WORD3);
-}
-
 // One filter word: from the LDS copy of the filter's first `fcw` words, else
 // from global memory (an L2 hit: the filter is small and read by every CU).
 __device__ __forceinline__ uint32_t filter_word(const uint32_t *fc, uint32_t fcw, __amdgpu_buffer_rsrc_t rs,
                                                 uint32_t wi) {
     const bool in_lds = wi < fcw;
     const uint32_t l = fc[in_lds ? wi : 0u];
-    const uint32_t g = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, in_lds ? 0xfffffff0u : wi * 4u, 0, 0);
+    // the offset of a word held in LDS lies past the view: no memory access
+    const uint32_t g = buffer_u32(rs, in_lds ? 0xfffffff0u : wi * 4u);
     return in_lds ? l : g;
 }
 
@@ -418,7 +393,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         }
         __syncthreads();
         const uint32_t m_bits = rv.m_bits, k = rv.k, d = td.in.d;
-        const __amdgpu_buffer_rsrc_t bits = filter_rsrc(rv.bits, m_bits);
+        const __amdgpu_buffer_rsrc_t bits = buffer_view(rv.bits, m_bits / 8u);
         uint16_t *me = qe[wv];
         uint32_t *mw = lw[wv];
         for (;;) {
@@ -511,78 +486,129 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 }
 
 // Emit pass: positives in ascending order at their tensor-wide ranks.
-// Threads 0..127 own one positives word of the tile each.
+//  A. the tile's 128 positives words and their prefix counts (block scan);
+//     each thread lists the positives among its 16 elements at their
+//     tile-local ranks;
+//  B. thread p takes positives p, p + 256, ...: consecutive threads handle
+//     consecutive ranks, so the reorder-map reads and every output write
+//     are coalesced;
+//  C. (receiver) the dense tile, 16-byte stores, zeros included.
+// The next tile's positives words are read before this tile's B and C run.
+constexpr uint32_t EMIT_COEF = 512;  // coefficients staged in LDS (else read from the payload)
+
 template <int MODE>
 __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     __shared__ uint32_t scratch[NWAVES + 1];
-    __shared__ __attribute__((aligned(16))) float stage[MODE == Q_DECODE ? TILE : 4];
-    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+    __shared__ uint32_t pw[TILE_WORDS];
+    __shared__ uint32_t pre[TILE_WORDS];
+    __shared__ uint32_t slot[TILE];  // A: local index of the positive of rank p; B: its value (receiver)
+    __shared__ float cf[MODE == Q_DECODE ? EMIT_COEF : 1];
+    constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);  // 4 groups of 4 elements per thread
+    uint32_t coef_t = 0xffffffffu;                     // tensor whose coefficients cf holds
+    uint32_t tile = blockIdx.x;
+    uint32_t word = 0;
+    if (tile < w.ntiles_total && threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
+    for (; tile < w.ntiles_total; tile += gridDim.x) {
         const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
         TDesc &td = w.td[t];
         const uint32_t lt = tile - td.in.tile0;
         const uint32_t d = td.in.d;
+        const uint32_t q0 = w.toff[tile];
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
+        if (threadIdx.x < TILE_WORDS) {
+            pw[threadIdx.x] = word;
+            pre[threadIdx.x] = ex;
+        }
         RecordView rv;
+        uint32_t ncoef = 0;
         if (MODE == Q_DECODE) {
             bool ok = true;
             rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, d, &ok);
-            for (uint32_t e = threadIdx.x; e < TILE; e += NTHREADS) stage[e] = 0.0f;
-
+            ncoef = rv.seff * (rv.deff + 1u);
+            if (t != coef_t && ncoef <= EMIT_COEF) {
+                for (uint32_t x = threadIdx.x; x < ncoef; x += NTHREADS) cf[x] = rv.coef[x];
+                coef_t = t;
+            }
         }
-        uint32_t word = 0;
-        if (threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
-        uint32_t tot;
-        const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
-        uint32_t q = w.toff[tile] + ex;
-        while (word) {
-            const uint32_t b = __ffs(word) - 1;
-            word &= word - 1;
-            const uint32_t e = threadIdx.x * 32u + b;
-            const uint32_t i = lt * TILE + e;
+        __syncthreads();
+        // A: list the positives
+        uint32_t nib[GROUPS], rank0[GROUPS];
+#pragma unroll
+        for (uint32_t u = 0; u < GROUPS; ++u) {
+            const uint32_t e0 = u * 4 * NTHREADS + threadIdx.x * 4;
+            const uint32_t wd = pw[e0 >> 5], sh = e0 & 31u;
+            nib[u] = (wd >> sh) & 0xfu;
+            rank0[u] = pre[e0 >> 5] + __popc(sh ? wd << (32u - sh) : 0u);
+            uint32_t r = rank0[u];
+#pragma unroll
+            for (uint32_t v = 0; v < 4; ++v)
+                if ((nib[u] >> v) & 1u) slot[r++] = e0 + v;
+        }
+        // the next tile's positives words, in flight during B and C
+        const uint32_t nt = tile + gridDim.x;
+        word = 0;
+        if (nt < w.ntiles_total && threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)nt * TILE_WORDS + threadIdx.x];
+        __syncthreads();
+        // B: one positive per thread
+        const uint32_t base = lt * TILE;
+        for (uint32_t p = threadIdx.x; p < tot; p += NTHREADS) {
+            const uint32_t i = base + slot[p];
+            const uint32_t q = q0 + p;
             if (MODE == Q_ENCODE) {
-                const float v = o.g[td.in.off + i];
+                const float x = o.g[td.in.off + i];
                 const uint64_t at = td.in.slot + q;
                 w.P[at] = i;
-                w.V[at] = v;
-                w.keyA[at] = ~order_key(v);  // ascending order of ~key = descending values
+                w.V[at] = x;
+                w.keyA[at] = ~order_key(x);  // ascending order of ~key = descending values
                 w.valA[at] = q;
             } else if (MODE == Q_PLAIN) {
                 if (q < o.cap) o.idx_out[q] = i;
             } else {
                 float y = 0.0f;
                 if (q < rv.nv) {
-                    const uint32_t rank = sigma_get(rv.sigma, q, rv.b);
+                    const uint32_t rank = sigma_get(rv.sigma, (uint64_t)q * rv.b, rv.b);
                     if (rank < rv.nv) {
-                        y = eval_rank(rv.coef, rank, rv.nv, rv.seff, rv.deff);
+                        uint32_t s, lo, ns;
+                        run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);
+                        const double tt = abscissa(rank - lo, ns);
+                        y = ncoef <= EMIT_COEF ? horner(cf + s * (rv.deff + 1u), rv.deff, tt)
+                                               : horner(rv.coef + s * (rv.deff + 1u), rv.deff, tt);
                     } else {
                         atomicOr(&td.flags, FLAG_DEC_MISMATCH);
                         if (o.counts_out) atomicOr((unsigned long long *)&o.counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
                     }
                 }
-                stage[e] = y;
+                slot[p] = __float_as_uint(y);
                 const uint64_t at = td.in.off + q;
                 if (o.idx_out) o.idx_out[at] = i;
                 if (o.val_out) o.val_out[at] = y;
             }
-            ++q;
         }
         if (MODE == Q_DECODE) {
             __syncthreads();
-            float *dst = o.dense_out + td.in.off + (uint64_t)lt * TILE;
-            const uint32_t lim = min(TILE, d - lt * TILE);
-            if (lim == TILE && ((uintptr_t)dst & 15u) == 0) {
-                // whole, aligned tile: 16-byte stores
-                const float4 *src4 = (const float4 *)stage;
-                float4 *dst4 = (float4 *)dst;
+            // C: the dense tile
 #pragma unroll
-                for (uint32_t u = 0; u < TILE / 4 / NTHREADS; ++u) dst4[u * NTHREADS + threadIdx.x] = src4[u * NTHREADS + threadIdx.x];
-            } else {
-                for (uint32_t e = threadIdx.x; e < lim; e += NTHREADS) dst[e] = stage[e];
+            for (uint32_t u = 0; u < GROUPS; ++u) {
+                const uint32_t e0 = u * 4 * NTHREADS + threadIdx.x * 4;
+                float y4[4];
+                uint32_t r = rank0[u];
+#pragma unroll
+                for (uint32_t v = 0; v < 4; ++v) y4[v] = ((nib[u] >> v) & 1u) ? __uint_as_float(slot[r++]) : 0.0f;
+                float *dst = o.dense_out + td.in.off + (uint64_t)base + e0;
+                const uint32_t ie = base + e0;
+                if (ie + 4 <= d && ((uintptr_t)dst & 15u) == 0) {
+                    *(float4 *)dst = make_float4(y4[0], y4[1], y4[2], y4[3]);
+                } else {
+#pragma unroll
+                    for (uint32_t v = 0; v < 4; ++v)
+                        if (ie + v < d) dst[v] = y4[v];
+                }
             }
         }
-        __syncthreads();
+        __syncthreads();  // pw, pre and slot are rewritten by the next tile
     }
 }
-
 
 // One probe block per CU (its LDS holds a filter copy), each owning at
 // least PB_TILES tiles so that all of its waves have work.
@@ -592,6 +618,13 @@ static int probe_grid(const Work &w) {
     return (int)max(1u, min(cus, by_tiles));
 }
 
+// Enough emit blocks to fill every CU's wave slots; each walks its tiles
+// with the next tile's read in flight.
+static int emit_grid(const Work &w) {
+    const uint32_t cap = (uint32_t)device_cus() * 8u;
+    return (int)max(1u, min(cap, w.ntiles_total));
+}
+
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     QueryOut o{};
     o.g = g;
@@ -599,7 +632,7 @@ hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, 
     trace_mark(s, "k_probe<Q_ENCODE>");
     hipError_t e = launch_tile_scan(w, 1, nullptr, s);
     if (e != hipSuccess) return e;
-    k_emit<Q_ENCODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_emit<Q_ENCODE><<<emit_grid(w), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_ENCODE>");
     return hipGetLastError();
 }
@@ -614,7 +647,7 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     trace_mark(s, "k_probe<Q_PLAIN>");
     hipError_t e = launch_tile_scan(w, 3, n_out, s);
     if (e != hipSuccess) return e;
-    k_emit<Q_PLAIN><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_emit<Q_PLAIN><<<emit_grid(w), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_PLAIN>");
     return hipGetLastError();
 }
@@ -631,7 +664,7 @@ hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *den
     trace_mark(s, "k_probe<Q_DECODE>");
     hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out, payload);
     if (e != hipSuccess) return e;
-    k_emit<Q_DECODE><<<grid_persist, NTHREADS, 0, s>>>(w, o);
+    k_emit<Q_DECODE><<<emit_grid(w), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_DECODE>");
     return hipGetLastError();
 }

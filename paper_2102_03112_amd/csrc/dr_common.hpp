@@ -34,6 +34,7 @@ constexpr uint32_t HIST1_SHIFT = 20;
 constexpr uint32_t SORT_BINS = 256;           // 8-bit LSD radix digits
 constexpr uint32_t FIT_CHUNKS = 8;            // partial-moment blocks per fitted run
 constexpr uint32_t MAX_DEG = 7;
+constexpr uint32_t MAX_SEG = 4096;            // most runs per tensor
 constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
 constexpr uint32_t HDR_BYTES = 64;
 constexpr uint32_t HDR_MAGIC = 0x31435244u;   // "DRC1"
@@ -259,6 +260,63 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *scratc
 // ---------------------------------------------------------------------------
 // Tiles.
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Equal-count runs of the value fit (rank -> run, abscissa, polynomial).
+// ---------------------------------------------------------------------------
+// floor(a / b) for a < 2^53, b >= 1: a double-precision estimate, then one
+// integer correction step (the estimate is off by at most one).
+__device__ __forceinline__ uint64_t udiv53(uint64_t a, uint32_t b) {
+    uint64_t q = (uint64_t)((double)a / (double)b);
+    if (q * b > a)
+        --q;
+    else if ((q + 1) * b <= a)
+        ++q;
+    return q;
+}
+
+// Run s holds sorted ranks [floor(s n / S), floor((s+1) n / S)); the run of
+// `rank` is the largest s with floor(s n / S) <= rank, i.e.
+// floor(((rank + 1) S - 1) / n).  n < 2^32 and S <= 4096 keep every
+// product below 2^53.
+__device__ __forceinline__ void run_of_rank(uint32_t rank, uint32_t n, uint32_t seff, uint32_t *s, uint32_t *lo,
+                                            uint32_t *ns) {
+    const uint32_t r = (uint32_t)udiv53(((uint64_t)rank + 1u) * seff - 1u, n);
+    const uint32_t a = (uint32_t)udiv53((uint64_t)r * n, seff);
+    const uint32_t b = (uint32_t)udiv53(((uint64_t)r + 1u) * n, seff);
+    *s = r;
+    *lo = a;
+    *ns = b - a;
+}
+
+// abscissa of local rank j in a run of ns points: (2j - (ns-1)) / (ns-1)
+__device__ __forceinline__ double abscissa(uint64_t j, uint64_t ns) {
+    return ns > 1 ? (double)(2 * (int64_t)j - (int64_t)(ns - 1)) / (double)(ns - 1) : 0.0;
+}
+
+// Horner's rule in double on fp32 coefficients c[0..deg], rounded to fp32
+__device__ __forceinline__ float horner(const float *c, uint32_t deg, double t) {
+    double y = (double)c[deg];
+    for (int p = (int)deg - 1; p >= 0; --p) y = y * t + (double)c[p];
+    return (float)y;
+}
+
+// Raw buffer view of `bytes` bytes at p (both the same on every lane of the
+// wave; readfirstlane states it, so the descriptor sits in scalar
+// registers).  A load at an offset past the view returns 0 and touches no
+// memory, so bounds checks need neither branches nor clamps.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_view(const void *p, uint32_t bytes) {
+    const uint64_t a = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    void *q = (void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(q, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes),
+                                             BUFFER_RSRC_WORD3);
+}
+
+__device__ __forceinline__ uint32_t buffer_u32(__amdgpu_buffer_rsrc_t v, uint32_t byte_off) {
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(v, byte_off, 0, 0);
+}
+
 // tensor holding global tile `tile` (tiles of a tensor are contiguous)
 __device__ __forceinline__ uint32_t tensor_of_tile(const TDesc *td, uint32_t ntensors, uint32_t tile) {
     uint32_t lo = 0, hi = ntensors;  // td[lo].tile0 <= tile < td[hi].tile0

@@ -237,14 +237,15 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         uint32_t keys[16];
         uint64_t cmask[16];
         uint32_t nonfinite = 0, ndef = 0;
-        // all 16 loads in flight before any is used (clamped inside the tensor)
-        const uint32_t last = d ? d - 1 : 0;
+        // all 16 loads in flight before any is used; reads past the tensor's
+        // end return 0 through the buffer view
+        const __amdgpu_buffer_rsrc_t gv = buffer_view(gt + base, 4u * min(TILE, d - min(d, base)));
         float x[16];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const uint32_t i = base + j * NTHREADS + threadIdx.x;
-            x[j] = d ? gt[i < d ? i : last] : 0.0f;
-        }
+        for (int j = 0; j < 16; ++j) x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * NTHREADS + threadIdx.x)));
+        // keeps the scheduler from sinking each load next to its use (it
+        // otherwise trades the 16 reads in flight for registers)
+        asm volatile("" ::: "memory");
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const uint32_t i = base + j * NTHREADS + threadIdx.x;

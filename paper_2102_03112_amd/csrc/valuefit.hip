@@ -322,11 +322,6 @@ __device__ __forceinline__ uint32_t tensor_of_fit_block(const Work &w, uint32_t 
     return lo;
 }
 
-// abscissa of local rank j in a run of ns points
-__device__ __forceinline__ double abscissa(uint64_t j, uint64_t ns) {
-    return ns > 1 ? (double)(2 * (int64_t)j - (int64_t)(ns - 1)) / (double)(ns - 1) : 0.0;
-}
-
 template <int D>
 __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, uint64_t j0, uint64_t j1,
                                  double *out) {
@@ -569,13 +564,9 @@ __global__ __launch_bounds__(NTHREADS) void k_curvefit_decode(Work w, const floa
         const uint32_t rank = (uint32_t)(v & ((1ull << b) - 1ull));
         float y = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range rank
         if (rank < nv) {
-            const uint64_t s = (((uint64_t)rank + 1u) * seff - 1u) / nv;
-            const uint64_t lo = s * nv / seff, hi = (s + 1) * nv / seff;
-            const double tt = abscissa(rank - lo, hi - lo);
-            const float *c = coef + s * stride;
-            double acc = (double)c[deff];
-            for (int p = (int)deff - 1; p >= 0; --p) acc = acc * tt + (double)c[p];
-            y = (float)acc;
+            uint32_t s, lo, ns;
+            run_of_rank(rank, nv, seff, &s, &lo, &ns);
+            y = horner(coef + (uint64_t)s * stride, deff, abscissa(rank - lo, ns));
         }
         out[q] = y;
     }
