@@ -74,6 +74,7 @@ typedef enum {
 #define DR_FLAG_DEC_MISMATCH 2u /* receiver: the record is invalid, or its |P| differs from the header */
 #define DR_FLAG_COUNT 4u        /* sender: the selection does not hold exactly r elements */
 #define DR_FLAG_CAPACITY 8u     /* a device-side capacity was exceeded; the output is incomplete */
+#define DR_FLAG_STALLED 16u     /* an internal bounded wait gave up; the output is wrong (a bug) */
 
 /* ---------------------------------------------------------------------- */
 /* Host-only helpers                                                       */

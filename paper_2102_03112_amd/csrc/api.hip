@@ -77,8 +77,8 @@ int persist_grid(int per_cu) { return dr::device_cus() * per_cu; }
 struct Carve {
     uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0;
     size_t bytes = 0;
-    size_t o_td, o_glob, o_done, o_histA, o_fitdone, o_tcnt, o_toff, o_ccnt, o_hpart, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
-        o_V, o_shist, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
+    size_t o_td, o_glob, o_done, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
+        o_V, o_sstat, o_sdig, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
 
     void plan() {
         size_t at = 0;
@@ -93,9 +93,8 @@ struct Carve {
         o_tcnt = take(4 * ntiles);
         o_toff = take(4 * ntiles);
         o_ccnt = take(4 * ntiles);
-        o_hpart = take(4ull * HIST1_BINS * hist_blocks);
         o_hist = take(4ull * HIST1_BINS * ntensors);
-        o_histA = take(4ull * 1024 * hist_blocks);
+        o_histA = take(4ull * 1024 * ntensors);
         o_sel = take(slots / 8);
         o_pbits = take(slots / 8);
         o_ckey = take(4 * slots);
@@ -103,9 +102,9 @@ struct Carve {
         o_S = take(4 * slots);
         o_P = take(4 * slots);
         o_V = take(4 * slots);
-        o_shist = take(4ull * SORT_BINS * ntiles);
+        o_sstat = take(8ull * 4 * SORT_BINS * ntiles);
+        o_sdig = take(4ull * 4 * SORT_BINS * ntensors);
         o_fit = take(8ull * NMOM * fit_blocks);
-        o_fitdone = take(4ull * (fit_blocks / FIT_CHUNKS + 1));
         o_btab = take(4 * btab);
         o_brow = take(8 * bslices);
         o_keyA = take(4 * slots);
@@ -129,20 +128,19 @@ struct Carve {
         w.toff = (uint32_t *)(ws + o_toff);
         w.ccnt = (uint32_t *)(ws + o_ccnt);
         w.pbits = (uint32_t *)(ws + o_pbits);
-        w.hist_part = (uint32_t *)(ws + o_hpart);
         w.hist = (uint32_t *)(ws + o_hist);
         w.selbits = (uint32_t *)(ws + o_sel);
         w.cand_key = (uint32_t *)(ws + o_ckey);
         w.cand_idx = (uint32_t *)(ws + o_cidx);
-        w.histA_part = (uint32_t *)(ws + o_histA);
+        w.histA = (uint32_t *)(ws + o_histA);
         w.S = (uint32_t *)(ws + o_S);
         w.P = (uint32_t *)(ws + o_P);
         w.V = (float *)(ws + o_V);
         w.sub_key = (uint32_t *)(ws + o_P);  // short list of the top-r select, before P exists
         w.sub_idx = (uint32_t *)(ws + o_V);
-        w.shist = (uint32_t *)(ws + o_shist);
+        w.sstat = (uint64_t *)(ws + o_sstat);
+        w.sdig = (uint32_t *)(ws + o_sdig);
         w.fit_part = (double *)(ws + o_fit);
-        w.fit_done = (uint32_t *)(ws + o_fitdone);
         w.fit_runs = (uint32_t)(fit_blocks / FIT_CHUNKS);
         w.btab = (uint32_t *)(ws + o_btab);
         w.brow = (uint32_t *)(ws + o_brow);
@@ -346,8 +344,10 @@ hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s) {
     memset(&z, 0, sizeof z);
     z.z[0] = {w.done, w.ntensors};
     z.z[1] = {w.glob, sizeof(Glob) / 4};
-    z.z[2] = {w.fit_done, w.fit_runs};
-    z.n = 3;
+    z.z[2] = {w.sdig, 4ull * SORT_BINS * w.ntensors};
+    z.z[3] = {w.hist, (uint64_t)HIST1_BINS * w.ntensors};
+    z.z[4] = {w.histA, 1024ull * w.ntensors};
+    z.n = 5;
     for (size_t f = 0; f < t.size(); f += INIT_CHUNK) {
         InitArgs a;
         memset(&a, 0, sizeof a);
@@ -383,7 +383,8 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
         p.t[t].coef = nullptr;
         p.t[t].sigma = nullptr;
     }
-    const Work w = p.carve.view((uint8_t *)ws);
+    Work w = p.carve.view((uint8_t *)ws);
+    w.counts_out = counts_out;
     trace_call(s);
     DR_HIP(run_init(w, p.t, s));
     if (p.any_topr)
@@ -393,7 +394,7 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
     DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
     DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, true, counts_out, s));
-    DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, persist_grid(4), s));
+    DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;
@@ -692,7 +693,7 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
     DR_HIP(run_init(w, p.t, s));
     DR_HIP(launch_keygen(w, vals, n, n_cap, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, false, nullptr, s));
-    DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, persist_grid(4), s));
+    DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;

@@ -107,10 +107,11 @@ static_assert(sizeof(TInit) % 4 == 0 && sizeof(TDesc) % 4 == 0, "descriptor layo
 
 // device-wide totals produced on the device
 struct Glob {
-    uint32_t sort_tiles;   // value-sort tiles over all tensors
-    uint32_t sigma_words;  // reorder-map words over all tensors
-    uint32_t values;       // sum of |P|
+    uint32_t sort_tiles;      // value-sort tiles over all tensors
+    uint32_t sigma_words;     // reorder-map words over all tensors
+    uint32_t values;          // sum of |P|
     uint32_t pad_;
+    uint32_t sort_ticket[4];  // value sort: next tile of each pass, in start order
 };
 
 // internal flag bits (besides DR_FLAG_NONFINITE = 1)
@@ -118,11 +119,13 @@ constexpr uint32_t FLAG_NONFINITE = 1u;
 constexpr uint32_t FLAG_DEC_MISMATCH = 2u;   // receiver |P| differs from the header
 constexpr uint32_t FLAG_COUNT = 4u;          // selection count differs from r
 constexpr uint32_t FLAG_CAPACITY = 8u;       // a device-side capacity was exceeded
+constexpr uint32_t FLAG_STALLED = 16u;       // a bounded wait gave up (internal error)
 
 // Views of the workspace carved on the host.
 struct Work {
     TDesc *td;
     Glob *glob;
+    uint64_t *counts_out;     // the round trip's per-tensor counts (nullable): late flags go here too
     uint32_t ntensors;
     uint32_t ntiles_total;    // sum of ntiles
     uint64_t slots;           // padded elements = ntiles_total * TILE
@@ -131,12 +134,11 @@ struct Work {
     uint32_t *toff;           // per-tile exclusive offsets within the tensor
     uint32_t *ccnt;           // top-r candidates per tile
     uint32_t *pbits;          // positives of a full-range query, one bit per index (slots / 32 words)
-    uint32_t *hist_part;      // top-r first-digit partial histograms
     uint32_t *hist;           // top-r first-digit histogram per tensor
     uint32_t *selbits;        // selection bitmap (paper's d-bit string B), slots / 32 words
     uint32_t *cand_key;       // top-r candidates (keys), per tensor slot
     uint32_t *cand_idx;       // top-r candidates (indices)
-    uint32_t *histA_part;     // top-r: candidates' histogram of key bits 19..10, one row per histogram block
+    uint32_t *histA;          // top-r: per-tensor histogram of the candidates' key bits 19..10 (1024 bins)
     uint32_t *sub_key;        // top-r short list (borrows P, which is written later)
     uint32_t *sub_idx;        // top-r short list (borrows V)
     uint32_t *S;              // selected indices, per tensor slot
@@ -144,12 +146,12 @@ struct Work {
     float *V;                 // g[P]
     uint32_t *keyA, *keyB;    // sort keys
     uint32_t *valA, *valB;    // sort payloads
-    uint32_t *shist;          // sort: per-tile digit counts (SORT_BINS per tile)
+    uint64_t *sstat;          // sort look-back: (flag << 32 | count) per pass, tile and digit
+    uint32_t *sdig;           // sort: per-tensor totals of each pass's digits (4 x SORT_BINS)
     uint32_t *srow;           // sort: per tensor digit totals
     uint32_t *sig;            // unpacked reorder map, per tensor slot
     float *vsorted;           // values in sorted order, per tensor slot
     double *fit_part;         // fit: partial moments
-    uint32_t *fit_done;       // fit: chunks finished per run (zeroed at set-up)
     uint32_t fit_runs;
     uint16_t *bpos;           // Bloom insert: bucketed in-slice positions
     uint32_t *btab;           // Bloom insert: per (slice, chunk) counts, then offsets within the slice

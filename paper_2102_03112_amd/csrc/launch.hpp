@@ -61,7 +61,7 @@ hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *den
 hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
                          hipStream_t s);
 hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s);
-hipError_t launch_sort(const Work &w, uint32_t cap_tiles, int grid_persist, hipStream_t s);
+hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s);
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s);
 hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s);
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,

@@ -105,8 +105,13 @@ __global__ __launch_bounds__(HIST_THREADS) void k_topr_hist(Work w, const float 
     }
     if (nonfinite) bad = 1;
     __syncthreads();
-    uint32_t *out = w.hist_part + (uint64_t)blockIdx.x * HIST1_BINS;
-    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += HIST_THREADS) out[i] = h[0][i] + h[1][i] + h[2][i] + h[3][i];
+    // the tensor's histogram: integer sums, so the order of the adds does
+    // not matter
+    uint32_t *out = w.hist + (uint64_t)t * HIST1_BINS;
+    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += HIST_THREADS) {
+        const uint32_t c = h[0][i] + h[1][i] + h[2][i] + h[3][i];
+        if (c) atomicAdd(&out[i], c);
+    }
     if (threadIdx.x == 0 && bad) atomicOr(&w.td[t].flags, FLAG_NONFINITE);
 }
 
@@ -153,38 +158,12 @@ __device__ void find_from_top(const uint32_t *cnt, uint32_t need, uint32_t *res_
     __syncthreads();
 }
 
-// Sum the partial histograms (each block: 32 bins, 8 row groups of 32
-// threads); the last block of each tensor picks b1.
-constexpr uint32_t RED_BINS = 32;
-constexpr uint32_t RED_BLOCKS = HIST1_BINS / RED_BINS;
-
-__global__ __launch_bounds__(NTHREADS) void k_topr_reduce(Work w) {
-    const uint32_t t = blockIdx.x / RED_BLOCKS;
-    const uint32_t part = blockIdx.x % RED_BLOCKS;
-    TDesc &td = w.td[t];
+// One block per tensor: the bin b1 that holds the r-th largest magnitude.
+__global__ __launch_bounds__(NTHREADS) void k_topr_pick(Work w) {
+    TDesc &td = w.td[blockIdx.x];
     if (td.in.r == R_NONZERO) return;
-    __shared__ uint32_t acc[NTHREADS / RED_BINS][RED_BINS];
-    __shared__ uint32_t ticket, res_bin, res_above;
+    __shared__ uint32_t res_bin, res_above;
     __shared__ uint32_t scratch[NWAVES + 1];
-    const uint32_t bin = part * RED_BINS + (threadIdx.x % RED_BINS);
-    const uint32_t grp = threadIdx.x / RED_BINS;
-    uint32_t s = 0;
-    for (uint32_t q = grp; q < td.in.hbn; q += NTHREADS / RED_BINS)
-        s += w.hist_part[(uint64_t)(td.in.hb0 + q) * HIST1_BINS + bin];
-    acc[grp][threadIdx.x % RED_BINS] = s;
-    __syncthreads();
-    uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
-    if (threadIdx.x < RED_BINS) {
-        uint32_t tot = 0;
-        for (uint32_t g2 = 0; g2 < NTHREADS / RED_BINS; ++g2) tot += acc[g2][threadIdx.x];
-        hist[part * RED_BINS + threadIdx.x] = tot;
-    }
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) ticket = atomicAdd(&w.done[t], 1u);
-    __syncthreads();
-    if (ticket != RED_BLOCKS - 1) return;
-    __threadfence();
     const uint32_t r = td.in.r;
     if (r == 0) {
         if (threadIdx.x == 0) {
@@ -199,6 +178,7 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_reduce(Work w) {
         res_above = 0;
     }
     __syncthreads();
+    const uint32_t *hist = w.hist + (uint64_t)blockIdx.x * HIST1_BINS;
     find_from_top<HIST1_BINS, NTHREADS>(hist, r, &res_bin, &res_above, scratch);
     if (threadIdx.x == 0) {
         td.b1 = res_bin;
@@ -331,7 +311,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_candhist(Work w) {
         }
     }
     __syncthreads();
-    w.histA_part[(uint64_t)blockIdx.x * 1024u + threadIdx.x] = h[threadIdx.x];
+    if (h[threadIdx.x]) atomicAdd(&w.histA[(uint64_t)t * 1024u + threadIdx.x], h[threadIdx.x]);
 }
 
 __global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
@@ -351,20 +331,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
         res_above = 0;
     }
     __syncthreads();
-    __shared__ uint32_t histA[1024];
-    uint32_t sum = 0;
-    const uint32_t *rows = w.histA_part + (uint64_t)td.in.hb0 * 1024u + threadIdx.x;
-    uint32_t q = 0;
-    for (; q + 16 <= td.in.hbn; q += 16) {  // 16 rows in flight
-        uint32_t v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = rows[(uint64_t)(q + u) * 1024u];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) sum += v[u];
-    }
-    for (; q < td.in.hbn; ++q) sum += rows[(uint64_t)q * 1024u];
-    histA[threadIdx.x] = sum;
-    __syncthreads();
+    const uint32_t *histA = w.histA + (uint64_t)blockIdx.x * 1024u;
     find_from_top<1024, SEL_THREADS>(histA, td.need1, &res_bin, &res_above, scratch);
     if (threadIdx.x == 0) {
         td.bA = res_bin;
@@ -373,38 +340,97 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
     }
 }
 
-// candidates above bin bA are selected; those in bA go to the short list
+// Candidates above bin bA are selected; those in bA go to the short list.
+// A block takes CP_TILES tiles at a time and treats their candidates as one
+// flat range (a scan of the tiles' counts), so the work per thread does not
+// depend on how the candidates fall into tiles; each thread handles
+// CP_BATCH of them with all their reads in flight.
+constexpr uint32_t CP_BATCH = 4;
+constexpr uint32_t CP_TILES = 32;
+
 __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
-    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-        const uint32_t c = w.ccnt[tile];
-        if (c == 0) continue;
-        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
-        TDesc &td = w.td[t];
-        if (td.in.r == R_NONZERO) continue;
-        const uint32_t bA = td.bA;
-        const uint64_t b0 = td.in.slot + (uint64_t)(tile - td.in.tile0) * TILE;
-        uint32_t *sb = w.selbits + (td.in.slot >> 5);
-        for (uint32_t j0 = 0; j0 < c; j0 += NTHREADS) {
-            const uint32_t j = j0 + threadIdx.x;
-            const bool act = j < c;
-            const uint32_t k = act ? w.cand_key[b0 + j] : 0u, i = act ? w.cand_idx[b0 + j] : 0u;
-            const uint32_t dA = (k >> 10) & 1023u;
-            const bool take = act && (bA == 0xFFFFFFFFu || dA > bA);
-            const bool sub = act && bA != 0xFFFFFFFFu && dA == bA;
-            if (take) atomicOr(&sb[i >> 5], 1u << (i & 31u));
-            // wave-aggregated append to the tensor's short list
-            const uint64_t m = ballot(sub);
-            if (m) {
-                uint32_t at0 = 0;
-                if (lane_id() == (uint32_t)__ffsll((unsigned long long)m) - 1) at0 = atomicAdd(&td.nsub, popc64(m));
-                at0 = __shfl(at0, __ffsll((unsigned long long)m) - 1, 64);
+    __shared__ uint32_t pre[CP_TILES];
+    __shared__ uint32_t tten[CP_TILES];
+    __shared__ uint64_t tbase[CP_TILES];  // workspace offset of the tile's first candidate
+    __shared__ uint32_t tbA[CP_TILES];
+    __shared__ uint32_t gtot;
+    for (uint32_t g0 = blockIdx.x * CP_TILES; g0 < w.ntiles_total; g0 += gridDim.x * CP_TILES) {
+        if (threadIdx.x < 64) {  // the first wave scans the group's counts
+            const uint32_t tile = g0 + threadIdx.x;
+            uint32_t c = 0, t = 0;
+            if (threadIdx.x < CP_TILES && tile < w.ntiles_total) {
+                t = tensor_of_tile(w.td, w.ntensors, tile);
+                const TDesc &td = w.td[t];
+                c = td.in.r == R_NONZERO ? 0u : w.ccnt[tile];
+                tbase[threadIdx.x] = td.in.slot + (uint64_t)(tile - td.in.tile0) * TILE;
+                tbA[threadIdx.x] = td.bA;
+            }
+            const uint32_t inc = wave_incl_scan(c);
+            if (threadIdx.x < CP_TILES) {
+                pre[threadIdx.x] = inc - c;
+                tten[threadIdx.x] = t;
+            }
+            if (threadIdx.x == 63) gtot = inc;
+        }
+        __syncthreads();
+        const uint32_t tot = gtot;
+        for (uint32_t e0 = 0; e0 < tot; e0 += NTHREADS * CP_BATCH) {
+            uint32_t key[CP_BATCH], idx[CP_BATCH], tix[CP_BATCH];
+#pragma unroll
+            for (uint32_t u = 0; u < CP_BATCH; ++u) {
+                const uint32_t e = e0 + u * NTHREADS + threadIdx.x;
+                // the tile holding flat candidate e: the last x with pre[x] <= e
+                uint32_t lo = 0, hi = CP_TILES;
+                while (hi - lo > 1) {
+                    const uint32_t mid = (lo + hi) >> 1;
+                    if (pre[mid] <= e)
+                        lo = mid;
+                    else
+                        hi = mid;
+                }
+                tix[u] = lo;
+                const uint64_t at = e < tot ? tbase[lo] + (e - pre[lo]) : 0u;  // past the end: any valid slot
+                key[u] = w.cand_key[at];
+                idx[u] = w.cand_idx[at];
+            }
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (uint32_t u = 0; u < CP_BATCH; ++u) {
+                const uint32_t e = e0 + u * NTHREADS + threadIdx.x;
+                const bool act = e < tot;
+                const uint32_t x = tix[u];
+                const uint32_t bA = tbA[x], k = key[u], i = idx[u];
+                const uint32_t dA = (k >> 10) & 1023u;
+                const bool take = act && (bA == 0xFFFFFFFFu || dA > bA);
+                const bool sub = act && bA != 0xFFFFFFFFu && dA == bA;
+                // i lies in tile x, whose first element sits at slot tbase[x]
+                if (take) atomicOr(&w.selbits[(tbase[x] + (i % TILE)) >> 5], 1u << (i & 31u));
                 if (sub) {
-                    const uint64_t q = td.in.slot + at0 + lanes_below(m);
+                    // appends to the tensor's short list; a wave's lanes of
+                    // one tensor share one atomic
+                    const uint32_t tt = tten[x];
+                    TDesc &td = w.td[tt];
+                    const uint64_t m = ballot(sub);
+                    const uint32_t first = (uint32_t)__ffsll((unsigned long long)m) - 1;
+                    const uint32_t t_first = __shfl(tt, first, 64);
+                    const uint64_t same = ballot(tt == t_first) & m;
+                    uint32_t at0;
+                    uint64_t q;
+                    if (tt == t_first) {
+                        at0 = 0;
+                        if (lane_id() == first) at0 = atomicAdd(&td.nsub, popc64(same));
+                        at0 = __shfl(at0, first, 64);
+                        q = td.in.slot + at0 + lanes_below(same);
+                    } else {
+                        at0 = atomicAdd(&td.nsub, 1u);
+                        q = td.in.slot + at0;
+                    }
                     w.sub_key[q] = k;
                     w.sub_idx[q] = i;
                 }
             }
         }
+        __syncthreads();  // the group's tables are rewritten by the next group
     }
 }
 
@@ -493,8 +519,8 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
     if (any_topr) {
         k_topr_hist<<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
         trace_mark(s, "k_topr_hist");
-        k_topr_reduce<<<w.ntensors * RED_BLOCKS, NTHREADS, 0, s>>>(w);
-        trace_mark(s, "k_topr_reduce");
+        k_topr_pick<<<w.ntensors, NTHREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_pick");
     }
     k_select_filter<<<grid_persist, NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
@@ -538,7 +564,7 @@ __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, 
     TDesc &td = w.td[blockIdx.x];
     __shared__ uint32_t scratch[TSCAN_THREADS / 64 + 1];
     const uint32_t nt = td.in.ntiles;
-    const uint32_t *cnt = w.tcnt + td.in.tile0;
+    const __amdgpu_buffer_rsrc_t cv = buffer_view(w.tcnt + td.in.tile0, 4u * nt);  // past the end: 0
     uint32_t *off = w.toff + td.in.tile0;
     uint32_t carry = 0;
     // thread x owns counts [x * PER, (x+1) * PER) of each step of PER * 1024
@@ -546,7 +572,7 @@ __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, 
         uint32_t v[TSCAN_PER];
         const uint32_t b = q0 + threadIdx.x * TSCAN_PER;
 #pragma unroll
-        for (uint32_t u = 0; u < TSCAN_PER; ++u) v[u] = b + u < nt ? cnt[b + u] : 0u;
+        for (uint32_t u = 0; u < TSCAN_PER; ++u) v[u] = buffer_u32(cv, 4u * (b + u));
         uint32_t sum = 0;
 #pragma unroll
         for (uint32_t u = 0; u < TSCAN_PER; ++u) sum += v[u];

@@ -4,8 +4,10 @@
 //  * Sort: the values of each tensor are sorted in descending order by an
 //    LSD radix sort (four 8-bit digits) of the order-preserving u32 image,
 //    complemented so that ascending order of the key is descending order of
-//    the value.  Each pass is stable (ranks within a tile come from wave
-//    ballots in element order), so equal values keep their original order.
+//    the value.  One pass counts all four digits; each digit pass is then a
+//    single kernel whose tiles chain their offsets by decoupled look-back.
+//    Each pass is stable (ranks within a tile come from wave ballots in
+//    element order), so equal values keep their original order.
 //  * Fit: each run of equal count is fitted by least squares in double: the
 //    normal-equation sums are accumulated per block and reduced in a fixed
 //    order, then a Gaussian elimination with partial pivoting solves the
@@ -154,94 +156,104 @@ __device__ __forceinline__ uint32_t tensor_of_stile(const Work &w, uint32_t g) {
     return lo;
 }
 
-__global__ __launch_bounds__(NTHREADS) void k_sort_hist(Work w, const uint32_t *__restrict__ keys, uint32_t shift) {
-    __shared__ uint32_t h[SORT_BINS];
+// Before the passes: each tensor's totals of all four digits, and the
+// look-back status of every sort tile cleared.  Blocks own contiguous tile
+// ranges and add their LDS counts to the tensor's totals when the tensor
+// changes and at the end.
+__global__ __launch_bounds__(NTHREADS) void k_sort_upfront(Work w, const uint32_t *__restrict__ keys) {
+    __shared__ uint32_t h[4][SORT_BINS];
     const uint32_t total = w.glob->sort_tiles;
-    for (uint32_t gt = blockIdx.x; gt < total; gt += gridDim.x) {
+    const uint32_t per = (total + gridDim.x - 1) / gridDim.x;
+    const uint32_t g0 = min(total, blockIdx.x * per), g1 = min(total, g0 + per);
+    uint32_t cur = 0xffffffffu;
+    for (uint32_t gt = g0; gt < g1; ++gt) {
         const uint32_t t = tensor_of_stile(w, gt);
+        if (t != cur) {
+            if (cur != 0xffffffffu) {
+                __syncthreads();
+                for (uint32_t p = 0; p < 4; ++p)
+                    if (h[p][threadIdx.x]) atomicAdd(&w.sdig[(cur * 4 + p) * SORT_BINS + threadIdx.x], h[p][threadIdx.x]);
+            }
+            __syncthreads();
+            for (uint32_t p = 0; p < 4; ++p) h[p][threadIdx.x] = 0;
+            __syncthreads();
+            cur = t;
+        }
         const TDesc &td = w.td[t];
         const uint32_t lt = gt - td.stile0;
-        h[threadIdx.x] = 0;
-        __syncthreads();
-        const uint32_t q0 = lt * TILE, q1 = min(td.nv, q0 + TILE);
-        const uint32_t *kt = keys + td.in.slot;
-        for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) atomicAdd(&h[(kt[q] >> shift) & 255u], 1u);
-        __syncthreads();
-        w.shist[(uint64_t)SORT_BINS * (td.stile0 + lt) + threadIdx.x] = h[threadIdx.x];
-        __syncthreads();
-    }
-}
-
-// Per tensor: digit totals, digit bases, and the running offset of each
-// (tile, digit).  Counts are stored tile-major, so each step over the tiles
-// is one coalesced load per block.
-__global__ __launch_bounds__(SORT_BINS) void k_sort_scan(Work w) {
-    const TDesc &td = w.td[blockIdx.x];
-    const uint32_t nt = td.sntiles;
-    if (nt == 0) return;
-    __shared__ uint32_t scratch[SORT_BINS / 64 + 1];
-    uint32_t *col = w.shist + (uint64_t)SORT_BINS * td.stile0 + threadIdx.x;
-    uint32_t sum = 0;
-    uint32_t q = 0;
-    for (; q + 8 <= nt; q += 8) {
-        uint32_t v[8];
+        const uint32_t q0 = lt * TILE, nq = min(TILE, td.nv - min(td.nv, q0));
+        const __amdgpu_buffer_rsrc_t kv = buffer_view(keys + td.in.slot + q0, 4u * nq);
+        uint32_t k16[TILE / NTHREADS];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = col[(uint64_t)(q + u) * SORT_BINS];
+        for (uint32_t c = 0; c < TILE / NTHREADS; ++c) k16[c] = buffer_u32(kv, 4u * (c * NTHREADS + threadIdx.x));
+        asm volatile("" ::: "memory");
 #pragma unroll
-        for (int u = 0; u < 8; ++u) sum += v[u];
-    }
-    for (; q < nt; ++q) sum += col[(uint64_t)q * SORT_BINS];
-    uint32_t tot;
-    uint32_t run = block_excl_scan_n<SORT_BINS>(sum, scratch, &tot);
-    q = 0;
-    for (; q + 8 <= nt; q += 8) {
-        uint32_t v[8];
+        for (uint32_t c = 0; c < TILE / NTHREADS; ++c) {
+            if (c * NTHREADS + threadIdx.x < nq) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = col[(uint64_t)(q + u) * SORT_BINS];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            col[(uint64_t)(q + u) * SORT_BINS] = run;
-            run += v[u];
+                for (uint32_t p = 0; p < 4; ++p) atomicAdd(&h[p][(k16[c] >> (8 * p)) & 255u], 1u);
+            }
         }
+        uint64_t *st = w.sstat + (uint64_t)gt * SORT_BINS;
+        for (uint32_t p = 0; p < 4; ++p) st[(uint64_t)p * w.ntiles_total * SORT_BINS + threadIdx.x] = 0;
     }
-    for (; q < nt; ++q) {
-        const uint32_t c = col[(uint64_t)q * SORT_BINS];
-        col[(uint64_t)q * SORT_BINS] = run;
-        run += c;
+    if (cur != 0xffffffffu) {
+        __syncthreads();
+        for (uint32_t p = 0; p < 4; ++p)
+            if (h[p][threadIdx.x]) atomicAdd(&w.sdig[(cur * 4 + p) * SORT_BINS + threadIdx.x], h[p][threadIdx.x]);
     }
 }
 
-// Stable scatter of one tile.  Element order inside the tile is
-// e = c * 256 + threadIdx.x (c = 0..15); for each c and wave, lanes holding
-// the same digit find each other with 8 ballots, and per-(c, wave, digit)
-// counts in LDS give each element its place among equal digits.
-__global__ __launch_bounds__(NTHREADS) void k_sort_scatter(Work w, const uint32_t *__restrict__ kin,
-                                                           const uint32_t *__restrict__ vin,
-                                                           uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
-                                                           uint32_t shift, int last) {
+// One stable pass of the digit at bits [8 pass, 8 pass + 8): tiles are
+// taken in ticket order, so a tile only ever waits for tiles that running
+// blocks hold.  A tile ranks its elements locally (lanes with equal digits
+// find each other with 8 ballots; per-(chunk, wave, digit) counts in LDS
+// order them), publishes its digit counts at once, then adds up the counts
+// of the tensor's earlier tiles (decoupled look-back: a tile that already
+// knows its inclusive prefix ends the walk) and scatters.
+constexpr uint64_t ST_AGG = 1ull << 32, ST_INC = 2ull << 32;
+constexpr uint32_t SPIN_LIMIT = 1u << 20;
+constexpr uint32_t LB_WIN = 32;  // look-back window (tiles read together)
+
+__global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *__restrict__ kin,
+                                                        const uint32_t *__restrict__ vin,
+                                                        uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
+                                                        uint32_t pass) {
     __shared__ uint16_t cnt[16][NWAVES][SORT_BINS];
     __shared__ uint32_t goff[SORT_BINS];
+    __shared__ uint32_t scratch[NWAVES + 1];
+    __shared__ uint32_t ticket;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     const uint32_t total = w.glob->sort_tiles;
-    for (uint32_t gt = blockIdx.x; gt < total; gt += gridDim.x) {
-        const uint32_t t = tensor_of_stile(w, gt);
-        const TDesc &td = w.td[t];
-        const uint32_t lt = gt - td.stile0;
+    if (blockIdx.x >= total) return;
+    const uint32_t shift = 8u * pass;
+    uint64_t *stat = w.sstat + (uint64_t)pass * w.ntiles_total * SORT_BINS;
+    for (;;) {
+        if (threadIdx.x == 0) ticket = atomicAdd(&w.glob->sort_ticket[pass], 1u);
         uint32_t *c32 = (uint32_t *)&cnt[0][0][0];
         for (uint32_t i = threadIdx.x; i < 16 * NWAVES * SORT_BINS / 2; i += NTHREADS) c32[i] = 0;
-        goff[threadIdx.x] = w.shist[(uint64_t)SORT_BINS * (td.stile0 + lt) + threadIdx.x];
         __syncthreads();
-        const uint32_t q0 = lt * TILE;
+        const uint32_t gt = ticket;
+        if (gt >= total) break;
+        const uint32_t t = tensor_of_stile(w, gt);
+        TDesc &td = w.td[t];
+        const uint32_t lt = gt - td.stile0;
         const uint32_t nv = td.nv;
-        const uint32_t *kt = kin + td.in.slot;
-        const uint32_t *vt = vin + td.in.slot;
-        uint32_t key[16], val[16], rnk[16];
+        const uint32_t q0 = lt * TILE, nq = min(TILE, nv - min(nv, q0));
+        const __amdgpu_buffer_rsrc_t kv = buffer_view(kin + td.in.slot + q0, 4u * nq);
+        const __amdgpu_buffer_rsrc_t vv = buffer_view(vin + td.in.slot + q0, 4u * nq);
+        uint32_t rnk4[4] = {0, 0, 0, 0};  // four 6-bit ranks per word, 8 bits apart
+        uint32_t key[16];
+#pragma unroll
+        for (int c = 0; c < 16; ++c) key[c] = buffer_u32(kv, 4u * (c * NTHREADS + threadIdx.x));
+        asm volatile("" ::: "memory");
+        // the tensor's base of each digit of this pass
+        uint32_t dtot;
+        const uint32_t dbase =
+            block_excl_scan(w.sdig[(t * 4 + pass) * SORT_BINS + threadIdx.x], scratch, &dtot);
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
-            const uint32_t q = q0 + c * NTHREADS + threadIdx.x;
-            const bool valid = q < nv;
-            key[c] = valid ? kt[q] : 0u;
-            val[c] = valid ? vt[q] : 0u;
+            const bool valid = c * NTHREADS + threadIdx.x < nq;
             const uint32_t dg = (key[c] >> shift) & 255u;
             uint64_t peers = ballot(valid);
 #pragma unroll
@@ -251,29 +263,80 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_scatter(Work w, const uint32_
                 peers &= bit ? m : ~m;
             }
             const uint32_t below = lanes_below(peers);
-            rnk[c] = below;
+            rnk4[c >> 2] |= below << (8 * (c & 3));
             if (valid && below == 0) cnt[c][wv][dg] = (uint16_t)popc64(peers);
         }
         __syncthreads();
-        {
-            // exclusive prefix over (c, wave) for digit = threadIdx.x
-            const uint32_t dg = threadIdx.x;
-            uint32_t run = 0;
-            for (int c = 0; c < 16; ++c)
-                for (uint32_t q = 0; q < NWAVES; ++q) {
-                    const uint32_t x = cnt[c][q][dg];
-                    cnt[c][q][dg] = (uint16_t)run;
-                    run += x;
+        // digit = threadIdx.x: exclusive prefix over (chunk, wave) in element
+        // order, and the tile's count of the digit
+        const uint32_t dg = threadIdx.x;
+        uint32_t agg = 0;
+        for (int c = 0; c < 16; ++c)
+            for (uint32_t q = 0; q < NWAVES; ++q) {
+                const uint32_t x = cnt[c][q][dg];
+                cnt[c][q][dg] = (uint16_t)agg;
+                agg += x;
+            }
+        uint64_t *me = stat + (uint64_t)gt * SORT_BINS + dg;
+        uint32_t excl = 0;
+        if (lt == 0) {
+            __hip_atomic_store(me, ST_INC | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            __hip_atomic_store(me, ST_AGG | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // walk back over the tensor's earlier tiles LB_WIN at a time, all
+            // of a window's reads in flight together; a tile that has not
+            // published yet ends the window, and the next window starts at it
+            uint32_t j = gt - 1, rounds = 0;
+            for (;;) {
+                const uint32_t nwin = min(LB_WIN, j - td.stile0 + 1);
+                uint64_t sv[LB_WIN];
+#pragma unroll
+                for (uint32_t u = 0; u < LB_WIN; ++u)
+                    sv[u] = u < nwin ? __hip_atomic_load(stat + (uint64_t)(j - u) * SORT_BINS + dg, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)
+                                     : 0ull;
+                uint32_t used = nwin;
+                bool inc = false;
+#pragma unroll
+                for (uint32_t u = 0; u < LB_WIN; ++u) {
+                    if (u < used && !inc) {
+                        if ((sv[u] >> 32) == 0) {
+                            used = u;  // not published yet
+                        } else {
+                            excl += (uint32_t)sv[u];
+                            inc = (sv[u] & ST_INC) != 0;
+                        }
+                    }
                 }
+                if (inc || (used == nwin && j - td.stile0 + 1 == nwin)) break;  // prefix complete
+                j -= used;
+                if (used == 0) {
+                    if (++rounds >= SPIN_LIMIT) {  // cannot happen; never hang the device on a bug
+                        atomicOr(&td.flags, FLAG_STALLED);
+                        if (w.counts_out) atomicOr((unsigned long long *)&w.counts_out[4 * t + 3], FLAG_STALLED);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            __hip_atomic_store(me, ST_INC | (uint64_t)(excl + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        goff[dg] = dbase + excl;
+        // keys again (an L2 hit; holding them through the look-back would
+        // cost the registers of its window) and the values
+        uint32_t val[16];
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            key[c] = buffer_u32(kv, 4u * (c * NTHREADS + threadIdx.x));
+            val[c] = buffer_u32(vv, 4u * (c * NTHREADS + threadIdx.x));
         }
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
-            const uint32_t q = q0 + c * NTHREADS + threadIdx.x;
-            const uint32_t dg = (key[c] >> shift) & 255u;
-            const uint32_t pos = goff[dg] + cnt[c][wv][dg] + rnk[c];
-            if (q < nv && pos < nv && val[c] < nv) {
-                if (last) {
+            const uint32_t d8 = (key[c] >> shift) & 255u;
+            const uint32_t pos = goff[d8] + cnt[c][wv][d8] + ((rnk4[c >> 2] >> (8 * (c & 3))) & 255u);
+            if (c * NTHREADS + threadIdx.x < nq && pos < nv && val[c] < nv) {
+                if (pass == 3) {
                     w.sig[td.in.slot + val[c]] = pos;  // reorder map: value q has rank pos
                     w.vsorted[td.in.slot + pos] = order_key_inv(~key[c]);
                 } else {
@@ -282,22 +345,20 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_scatter(Work w, const uint32_
                 }
             }
         }
-        __syncthreads();
+        __syncthreads();  // cnt, goff and ticket are rewritten by the next tile
     }
     (void)lane;
 }
 
-hipError_t launch_sort(const Work &w, uint32_t cap_tiles, int grid_persist, hipStream_t s) {
-    (void)cap_tiles;
+hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s) {
+    const uint32_t cus = (uint32_t)device_cus();
+    k_sort_upfront<<<cus, NTHREADS, 0, s>>>(w, w.keyA);
+    trace_mark(s, "k_sort_upfront");
+    const int grid = (int)max(1u, min(cap_tiles, cus * 4u));
     uint32_t *kin = w.keyA, *vin = w.valA, *kout = w.keyB, *vout = w.valB;
-    for (int p = 0; p < 4; ++p) {
-        const uint32_t shift = 8u * p;
-        k_sort_hist<<<grid_persist, NTHREADS, 0, s>>>(w, kin, shift);
-        trace_mark(s, "k_sort_hist");
-        k_sort_scan<<<w.ntensors, SORT_BINS, 0, s>>>(w);
-        trace_mark(s, "k_sort_scan");
-        k_sort_scatter<<<grid_persist, NTHREADS, 0, s>>>(w, kin, vin, kout, vout, shift, p == 3);
-        trace_mark(s, "k_sort_scatter");
+    for (uint32_t p = 0; p < 4; ++p) {
+        k_sort_pass<<<grid, NTHREADS, 0, s>>>(w, kin, vin, kout, vout, p);
+        trace_mark(s, "k_sort_pass");
         uint32_t *tk = kin, *tv = vin;
         kin = kout;
         vin = vout;
@@ -322,6 +383,12 @@ __device__ __forceinline__ uint32_t tensor_of_fit_block(const Work &w, uint32_t 
     return lo;
 }
 
+// Moments of one chunk of a run: sums of t^e (e <= 2D) and t^e y (e <= D)
+// over local ranks [j0, j1) of a run of ns points starting at lo_run.
+// Each thread reads FIT_BATCH values before it uses any.
+constexpr uint32_t FIT_THREADS = 1024;
+constexpr uint32_t FIT_BATCH = 8;
+
 template <int D>
 __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, uint64_t j0, uint64_t j1,
                                  double *out) {
@@ -331,18 +398,33 @@ __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, u
     for (int e = 0; e < NP; ++e) pw[e] = 0.0;
 #pragma unroll
     for (int e = 0; e <= D; ++e) rh[e] = 0.0;
-    for (uint64_t j = j0 + threadIdx.x; j < j1; j += NTHREADS) {
-        const double t = abscissa(j, ns);
-        const double v = (double)y[lo_run + j];
-        double tp = 1.0;
+    const double inv = ns > 1 ? 1.0 / (double)(ns - 1) : 0.0;
+    const double off = (double)(ns - 1);
+    for (uint64_t jb = j0; jb < j1; jb += (uint64_t)FIT_THREADS * FIT_BATCH) {
+        float v[FIT_BATCH];
 #pragma unroll
-        for (int e = 0; e < NP; ++e) {
-            pw[e] += tp;
-            if (e <= D) rh[e] += tp * v;
-            tp *= t;
+        for (uint32_t u = 0; u < FIT_BATCH; ++u) {
+            const uint64_t j = jb + (uint64_t)u * FIT_THREADS + threadIdx.x;
+            v[u] = j < j1 ? y[lo_run + j] : 0.0f;
+        }
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (uint32_t u = 0; u < FIT_BATCH; ++u) {
+            const uint64_t j = jb + (uint64_t)u * FIT_THREADS + threadIdx.x;
+            if (j >= j1) break;
+            const double t = ((double)(2 * j) - off) * inv;
+            const double yv = (double)v[u];
+            double tp = 1.0;
+#pragma unroll
+            for (int e = 0; e < NP; ++e) {
+                pw[e] += tp;
+                if (e <= D) rh[e] += tp * yv;
+                tp *= t;
+            }
         }
     }
-    __shared__ double red[NWAVES][NP + D + 1];
+    constexpr uint32_t NW = FIT_THREADS / 64;
+    __shared__ double red[NW][NP + D + 1];
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
 #pragma unroll
     for (int e = 0; e < NP; ++e) {
@@ -357,26 +439,20 @@ __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, u
     __syncthreads();
     if (threadIdx.x < (uint32_t)(NP + D + 1)) {
         double s = 0.0;
-        for (uint32_t q = 0; q < NWAVES; ++q) s += red[q][threadIdx.x];
+        for (uint32_t q = 0; q < NW; ++q) s += red[q][threadIdx.x];
         out[threadIdx.x < (uint32_t)NP ? threadIdx.x : (2 * MAX_DEG + 1) + (threadIdx.x - NP)] = s;
     }
 }
 
 __device__ void solve_run(const TDesc &td, uint32_t s, const double *mom);
 
-// Moments of one chunk of one run; the last chunk of a run to finish sums
-// the run's partial moments in chunk order and solves.
-__global__ __launch_bounds__(NTHREADS) void k_fit_moments(Work w) {
+// Moments of one chunk of one run.
+__global__ __launch_bounds__(FIT_THREADS) void k_fit_moments(Work w) {
     const uint32_t t = tensor_of_fit_block(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t local = blockIdx.x - td.in.fit_blk0;
     const uint32_t s = local / FIT_CHUNKS, ch = local % FIT_CHUNKS;
-    if (s >= td.seff) {
-        // caller-owned coefficient rows beyond the fitted runs are zero
-        if (td.in.coef && ch == 0 && s < td.in.nseg && threadIdx.x < td.in.coef_stride)
-            td.in.coef[(uint64_t)s * td.in.coef_stride + threadIdx.x] = 0.0f;
-        return;
-    }
+    if (s >= td.seff) return;
     const uint64_t nv = td.nv, S = td.seff;
     const uint64_t lo = s * nv / S, hi = (s + 1) * nv / S, ns = hi - lo;
     const uint64_t j0 = ns * ch / FIT_CHUNKS, j1 = ns * (ch + 1) / FIT_CHUNKS;
@@ -392,17 +468,24 @@ __global__ __launch_bounds__(NTHREADS) void k_fit_moments(Work w) {
         case 6: fit_moments_body<6>(y, lo, ns, j0, j1, out); break;
         default: fit_moments_body<7>(y, lo, ns, j0, j1, out); break;
     }
-    __shared__ uint32_t ticket;
+}
+
+// One run per block: its chunks' moments summed in chunk order, then the
+// solve (one thread; the system is at most 8 x 8).  Caller-owned
+// coefficient rows past the fitted runs are zeroed.
+__global__ __launch_bounds__(64) void k_fit_solve(Work w) {
+    const uint32_t blk = blockIdx.x * FIT_CHUNKS;
+    const uint32_t t = tensor_of_fit_block(w, blk);
+    const TDesc &td = w.td[t];
+    const uint32_t s = (blk - td.in.fit_blk0) / FIT_CHUNKS;
+    if (s >= td.seff) {
+        if (td.in.coef && s < td.in.nseg && threadIdx.x < td.in.coef_stride)
+            td.in.coef[(uint64_t)s * td.in.coef_stride + threadIdx.x] = 0.0f;
+        return;
+    }
     __shared__ double mom[NMOM];
-    __threadfence();
-    __syncthreads();
-    const uint32_t run = td.in.fit_blk0 / FIT_CHUNKS + s;
-    if (threadIdx.x == 0) ticket = atomicAdd(&w.fit_done[run], 1u);
-    __syncthreads();
-    if (ticket != FIT_CHUNKS - 1) return;
-    __threadfence();
     if (threadIdx.x < NMOM) {
-        const double *part = w.fit_part + (uint64_t)(td.in.fit_blk0 + s * FIT_CHUNKS) * NMOM;
+        const double *part = w.fit_part + (uint64_t)blk * NMOM;
         double acc = 0.0;
         for (uint32_t c = 0; c < FIT_CHUNKS; ++c) acc += part[c * NMOM + threadIdx.x];
         mom[threadIdx.x] = acc;
@@ -490,8 +573,10 @@ __device__ void solve_run(const TDesc &td, uint32_t s, const double *mom) {
 
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s) {
     if (fit_blocks == 0) return hipSuccess;
-    k_fit_moments<<<fit_blocks, NTHREADS, 0, s>>>(w);
+    k_fit_moments<<<fit_blocks, FIT_THREADS, 0, s>>>(w);
     trace_mark(s, "k_fit_moments");
+    k_fit_solve<<<fit_blocks / FIT_CHUNKS, 64, 0, s>>>(w);
+    trace_mark(s, "k_fit_solve");
     return hipGetLastError();
 }
 
