@@ -59,6 +59,10 @@ def lib():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2102_03112_amd.build`")
+    # torch carries its own HIP runtime; loading it first makes the library
+    # bind to that same runtime, so torch's device pointers and streams are
+    # valid in the library's calls
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     vp, u32, u64, sz, st = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t, ctypes.c_int
     cfgp = ctypes.POINTER(DrConfig)

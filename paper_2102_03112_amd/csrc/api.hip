@@ -10,7 +10,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/deepreduce.h"
+#include "deepreduce.h"
 #include "launch.hpp"
 
 using namespace dr;

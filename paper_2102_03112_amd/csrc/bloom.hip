@@ -511,8 +511,11 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     for (; tile < w.ntiles_total; tile += gridDim.x) {
         const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
         TDesc &td = w.td[t];
+        // descriptor fields in registers (the output stores could alias
+        // them for all the compiler knows)
         const uint32_t lt = tile - td.in.tile0;
         const uint32_t d = td.in.d;
+        const uint64_t toff_el = td.in.off, tslot = td.in.slot;
         const uint32_t q0 = w.toff[tile];
         uint32_t tot;
         const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
@@ -556,8 +559,8 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             const uint32_t i = base + slot[p];
             const uint32_t q = q0 + p;
             if (MODE == Q_ENCODE) {
-                const float x = o.g[td.in.off + i];
-                const uint64_t at = td.in.slot + q;
+                const float x = o.g[toff_el + i];
+                const uint64_t at = tslot + q;
                 w.P[at] = i;
                 w.V[at] = x;
                 w.keyA[at] = ~order_key(x);  // ascending order of ~key = descending values
@@ -580,7 +583,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
                     }
                 }
                 slot[p] = __float_as_uint(y);
-                const uint64_t at = td.in.off + q;
+                const uint64_t at = toff_el + q;
                 if (o.idx_out) o.idx_out[at] = i;
                 if (o.val_out) o.val_out[at] = y;
             }
@@ -595,7 +598,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
                 uint32_t r = rank0[u];
 #pragma unroll
                 for (uint32_t v = 0; v < 4; ++v) y4[v] = ((nib[u] >> v) & 1u) ? __uint_as_float(slot[r++]) : 0.0f;
-                float *dst = o.dense_out + td.in.off + (uint64_t)base + e0;
+                float *dst = o.dense_out + toff_el + (uint64_t)base + e0;
                 const uint32_t ie = base + e0;
                 if (ie + 4 <= d && ((uintptr_t)dst & 15u) == 0) {
                     *(float4 *)dst = make_float4(y4[0], y4[1], y4[2], y4[3]);

@@ -206,95 +206,121 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_upfront(Work w, const uint32_
 
 // One stable pass of the digit at bits [8 pass, 8 pass + 8): tiles are
 // taken in ticket order, so a tile only ever waits for tiles that running
-// blocks hold.  A tile ranks its elements locally (lanes with equal digits
-// find each other with 8 ballots; per-(chunk, wave, digit) counts in LDS
-// order them), publishes its digit counts at once, then adds up the counts
-// of the tensor's earlier tiles (decoupled look-back: a tile that already
-// knows its inclusive prefix ends the walk) and scatters.
+// blocks hold.  A tile
+//  1. reads its keys (wave w holds elements [1024 w, 1024 w + 1024) of the
+//     tile, 64 consecutive per step) and counts its digits in LDS;
+//  2. publishes the counts at once and starts reading the counts of the
+//     tensor's earlier tiles (decoupled look-back, LB_WIN tiles per read
+//     round; a tile that already knows its inclusive prefix ends the walk);
+//  3. while those reads are in flight, ranks its elements: lanes with equal
+//     digits find each other with 8 ballots, and each wave keeps running
+//     per-digit counts, so ranks follow element order (a stable pass);
+//  4. finishes the look-back, publishes its inclusive prefix, and scatters.
 constexpr uint64_t ST_AGG = 1ull << 32, ST_INC = 2ull << 32;
 constexpr uint32_t SPIN_LIMIT = 1u << 20;
-constexpr uint32_t LB_WIN = 32;  // look-back window (tiles read together)
+constexpr uint32_t LB_WIN = 16;  // look-back window (tiles read together)
+constexpr uint32_t SORT_STEPS = TILE / NTHREADS;  // 16 keys per thread
 
 __global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *__restrict__ kin,
                                                         const uint32_t *__restrict__ vin,
                                                         uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
                                                         uint32_t pass) {
-    __shared__ uint16_t cnt[16][NWAVES][SORT_BINS];
+    __shared__ uint32_t hist[SORT_BINS];
+    __shared__ uint32_t run[NWAVES][SORT_BINS];  // per-wave running counts, then per-wave bases
     __shared__ uint32_t goff[SORT_BINS];
     __shared__ uint32_t scratch[NWAVES + 1];
     __shared__ uint32_t ticket;
-    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    const uint32_t lane = threadIdx.x & 63u, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t total = w.glob->sort_tiles;
     if (blockIdx.x >= total) return;
     const uint32_t shift = 8u * pass;
     uint64_t *stat = w.sstat + (uint64_t)pass * w.ntiles_total * SORT_BINS;
     for (;;) {
         if (threadIdx.x == 0) ticket = atomicAdd(&w.glob->sort_ticket[pass], 1u);
-        uint32_t *c32 = (uint32_t *)&cnt[0][0][0];
-        for (uint32_t i = threadIdx.x; i < 16 * NWAVES * SORT_BINS / 2; i += NTHREADS) c32[i] = 0;
+        hist[threadIdx.x] = 0;
+#pragma unroll
+        for (uint32_t q = 0; q < NWAVES; ++q) run[q][threadIdx.x] = 0;
         __syncthreads();
         const uint32_t gt = ticket;
         if (gt >= total) break;
         const uint32_t t = tensor_of_stile(w, gt);
         TDesc &td = w.td[t];
-        const uint32_t lt = gt - td.stile0;
+        // descriptor fields in registers: the scatter's stores could alias
+        // them for all the compiler knows, which would reload them per store
+        const uint32_t stile0 = td.stile0;
+        const uint32_t lt = gt - stile0;
         const uint32_t nv = td.nv;
+        const uint64_t slot = td.in.slot;
         const uint32_t q0 = lt * TILE, nq = min(TILE, nv - min(nv, q0));
-        const __amdgpu_buffer_rsrc_t kv = buffer_view(kin + td.in.slot + q0, 4u * nq);
-        const __amdgpu_buffer_rsrc_t vv = buffer_view(vin + td.in.slot + q0, 4u * nq);
-        uint32_t rnk4[4] = {0, 0, 0, 0};  // four 6-bit ranks per word, 8 bits apart
-        uint32_t key[16];
+        const __amdgpu_buffer_rsrc_t kv = buffer_view(kin + slot + q0, 4u * nq);
+        const __amdgpu_buffer_rsrc_t vv = buffer_view(vin + slot + q0, 4u * nq);
+        const uint32_t ebase = wv * (SORT_STEPS * 64) + lane;  // element of step c: ebase + 64 c
+        uint32_t key[SORT_STEPS];
 #pragma unroll
-        for (int c = 0; c < 16; ++c) key[c] = buffer_u32(kv, 4u * (c * NTHREADS + threadIdx.x));
+        for (uint32_t c = 0; c < SORT_STEPS; ++c) key[c] = buffer_u32(kv, 4u * (ebase + 64 * c));
         asm volatile("" ::: "memory");
         // the tensor's base of each digit of this pass
         uint32_t dtot;
-        const uint32_t dbase =
-            block_excl_scan(w.sdig[(t * 4 + pass) * SORT_BINS + threadIdx.x], scratch, &dtot);
+        const uint32_t dbase = block_excl_scan(w.sdig[(t * 4 + pass) * SORT_BINS + threadIdx.x], scratch, &dtot);
+        // 1. the tile's digit counts
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
-            const bool valid = c * NTHREADS + threadIdx.x < nq;
-            const uint32_t dg = (key[c] >> shift) & 255u;
+        for (uint32_t c = 0; c < SORT_STEPS; ++c)
+            if (ebase + 64 * c < nq) atomicAdd(&hist[(key[c] >> shift) & 255u], 1u);
+        __syncthreads();
+        // 2. publish; first look-back window in flight
+        const uint32_t dg = threadIdx.x;
+        const uint32_t agg = hist[dg];
+        uint64_t *me = stat + (uint64_t)gt * SORT_BINS + dg;
+        __hip_atomic_store(me, (lt == 0 ? ST_INC : ST_AGG) | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint32_t j = gt - 1;  // next earlier tile to read (valid while lt > 0)
+        uint32_t nwin = lt == 0 ? 0u : min(LB_WIN, j - stile0 + 1);
+        uint64_t sv[LB_WIN];
+#pragma unroll
+        for (uint32_t u = 0; u < LB_WIN; ++u)
+            sv[u] = u < nwin ? __hip_atomic_load(stat + (uint64_t)(j - u) * SORT_BINS + dg, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT)
+                             : 0ull;
+        // 3. ranks within the wave, in element order
+        uint32_t rk[SORT_STEPS / 2];  // two 16-bit ranks per word
+#pragma unroll
+        for (uint32_t c = 0; c < SORT_STEPS / 2; ++c) rk[c] = 0;
+#pragma unroll
+        for (uint32_t c = 0; c < SORT_STEPS; ++c) {
+            const bool valid = ebase + 64 * c < nq;
+            const uint32_t d8 = (key[c] >> shift) & 255u;
             uint64_t peers = ballot(valid);
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const bool bit = (dg >> b) & 1u;
+            for (int bb = 0; bb < 8; ++bb) {
+                const bool bit = (d8 >> bb) & 1u;
                 const uint64_t m = ballot(bit);
                 peers &= bit ? m : ~m;
             }
-            const uint32_t below = lanes_below(peers);
-            rnk4[c >> 2] |= below << (8 * (c & 3));
-            if (valid && below == 0) cnt[c][wv][dg] = (uint16_t)popc64(peers);
+            const uint32_t leader = (uint32_t)__ffsll((unsigned long long)peers) - 1u;
+            uint32_t r0 = 0;
+            if (valid && lane == leader) {
+                r0 = run[wv][d8];
+                run[wv][d8] = r0 + popc64(peers);
+            }
+            r0 = __shfl(r0, leader, 64);
+            rk[c >> 1] |= (r0 + lanes_below(peers)) << (16 * (c & 1));
         }
         __syncthreads();
-        // digit = threadIdx.x: exclusive prefix over (chunk, wave) in element
-        // order, and the tile's count of the digit
-        const uint32_t dg = threadIdx.x;
-        uint32_t agg = 0;
-        for (int c = 0; c < 16; ++c)
-            for (uint32_t q = 0; q < NWAVES; ++q) {
-                const uint32_t x = cnt[c][q][dg];
-                cnt[c][q][dg] = (uint16_t)agg;
-                agg += x;
-            }
-        uint64_t *me = stat + (uint64_t)gt * SORT_BINS + dg;
-        uint32_t excl = 0;
-        if (lt == 0) {
-            __hip_atomic_store(me, ST_INC | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            __hip_atomic_store(me, ST_AGG | agg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            // walk back over the tensor's earlier tiles LB_WIN at a time, all
-            // of a window's reads in flight together; a tile that has not
-            // published yet ends the window, and the next window starts at it
-            uint32_t j = gt - 1, rounds = 0;
-            for (;;) {
-                const uint32_t nwin = min(LB_WIN, j - td.stile0 + 1);
-                uint64_t sv[LB_WIN];
+        // per-wave bases of each digit (waves in element order)
+        {
+            uint32_t acc = 0;
 #pragma unroll
-                for (uint32_t u = 0; u < LB_WIN; ++u)
-                    sv[u] = u < nwin ? __hip_atomic_load(stat + (uint64_t)(j - u) * SORT_BINS + dg, __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT)
-                                     : 0ull;
+            for (uint32_t q = 0; q < NWAVES; ++q) {
+                const uint32_t x = run[q][dg];
+                run[q][dg] = acc;
+                acc += x;
+            }
+        }
+        // 4. finish the look-back: a tile that has not published yet ends
+        // the window, and the next window starts at it
+        uint32_t excl = 0;
+        if (lt > 0) {
+            uint32_t rounds = 0;
+            for (;;) {
                 uint32_t used = nwin;
                 bool inc = false;
 #pragma unroll
@@ -308,7 +334,7 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *
                         }
                     }
                 }
-                if (inc || (used == nwin && j - td.stile0 + 1 == nwin)) break;  // prefix complete
+                if (inc || (used == nwin && j - stile0 + 1 == nwin)) break;  // prefix complete
                 j -= used;
                 if (used == 0) {
                     if (++rounds >= SPIN_LIMIT) {  // cannot happen; never hang the device on a bug
@@ -318,36 +344,41 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *
                     }
                     __builtin_amdgcn_s_sleep(1);
                 }
+                nwin = min(LB_WIN, j - stile0 + 1);
+#pragma unroll
+                for (uint32_t u = 0; u < LB_WIN; ++u)
+                    sv[u] = u < nwin ? __hip_atomic_load(stat + (uint64_t)(j - u) * SORT_BINS + dg, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)
+                                     : 0ull;
             }
             __hip_atomic_store(me, ST_INC | (uint64_t)(excl + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         goff[dg] = dbase + excl;
         // keys again (an L2 hit; holding them through the look-back would
-        // cost the registers of its window) and the values
-        uint32_t val[16];
+        // cost registers) and the values
+        uint32_t val[SORT_STEPS];
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
-            key[c] = buffer_u32(kv, 4u * (c * NTHREADS + threadIdx.x));
-            val[c] = buffer_u32(vv, 4u * (c * NTHREADS + threadIdx.x));
+        for (uint32_t c = 0; c < SORT_STEPS; ++c) {
+            key[c] = buffer_u32(kv, 4u * (ebase + 64 * c));
+            val[c] = buffer_u32(vv, 4u * (ebase + 64 * c));
         }
         __syncthreads();
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
+        for (uint32_t c = 0; c < SORT_STEPS; ++c) {
             const uint32_t d8 = (key[c] >> shift) & 255u;
-            const uint32_t pos = goff[d8] + cnt[c][wv][d8] + ((rnk4[c >> 2] >> (8 * (c & 3))) & 255u);
-            if (c * NTHREADS + threadIdx.x < nq && pos < nv && val[c] < nv) {
+            const uint32_t pos = goff[d8] + run[wv][d8] + ((rk[c >> 1] >> (16 * (c & 1))) & 0xffffu);
+            if (ebase + 64 * c < nq && pos < nv && val[c] < nv) {
                 if (pass == 3) {
-                    w.sig[td.in.slot + val[c]] = pos;  // reorder map: value q has rank pos
-                    w.vsorted[td.in.slot + pos] = order_key_inv(~key[c]);
+                    w.sig[slot + val[c]] = pos;  // reorder map: value q has rank pos
+                    w.vsorted[slot + pos] = order_key_inv(~key[c]);
                 } else {
-                    kout[td.in.slot + pos] = key[c];
-                    vout[td.in.slot + pos] = val[c];
+                    kout[slot + pos] = key[c];
+                    vout[slot + pos] = val[c];
                 }
             }
         }
-        __syncthreads();  // cnt, goff and ticket are rewritten by the next tile
+        __syncthreads();  // hist, run, goff and ticket are rewritten by the next tile
     }
-    (void)lane;
 }
 
 hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s) {
