@@ -621,13 +621,6 @@ static int probe_grid(const Work &w) {
     return (int)max(1u, min(cus, by_tiles));
 }
 
-// Enough emit blocks to fill every CU's wave slots; each walks its tiles
-// with the next tile's read in flight.
-static int emit_grid(const Work &w) {
-    const uint32_t cap = (uint32_t)device_cus() * 8u;
-    return (int)max(1u, min(cap, w.ntiles_total));
-}
-
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     QueryOut o{};
     o.g = g;
@@ -635,7 +628,7 @@ hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, 
     trace_mark(s, "k_probe<Q_ENCODE>");
     hipError_t e = launch_tile_scan(w, 1, nullptr, s);
     if (e != hipSuccess) return e;
-    k_emit<Q_ENCODE><<<emit_grid(w), NTHREADS, 0, s>>>(w, o);
+    k_emit<Q_ENCODE><<<resident_grid(k_emit<Q_ENCODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_ENCODE>");
     return hipGetLastError();
 }
@@ -650,7 +643,7 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     trace_mark(s, "k_probe<Q_PLAIN>");
     hipError_t e = launch_tile_scan(w, 3, n_out, s);
     if (e != hipSuccess) return e;
-    k_emit<Q_PLAIN><<<emit_grid(w), NTHREADS, 0, s>>>(w, o);
+    k_emit<Q_PLAIN><<<resident_grid(k_emit<Q_PLAIN>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_PLAIN>");
     return hipGetLastError();
 }
@@ -667,7 +660,7 @@ hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *den
     trace_mark(s, "k_probe<Q_DECODE>");
     hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out, payload);
     if (e != hipSuccess) return e;
-    k_emit<Q_DECODE><<<emit_grid(w), NTHREADS, 0, s>>>(w, o);
+    k_emit<Q_DECODE><<<resident_grid(k_emit<Q_DECODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_DECODE>");
     return hipGetLastError();
 }

@@ -11,6 +11,24 @@ namespace dr {
 
 int device_cus();  // compute units of the current device
 
+// A grid of persistent blocks: as many as can be resident at once on the
+// current device (so every block starts at once and none waits for another
+// to finish), but no more than `work` units.  Cached per kernel and device.
+template <typename K>
+int resident_grid(K kernel, int threads, uint32_t work) {
+    static int per_cu[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    const int slot = dev < 64 ? dev : 63;
+    if (per_cu[slot] == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
+        per_cu[slot] = n;
+    }
+    const uint32_t g = (uint32_t)(per_cu[slot] * device_cus());
+    return (int)(work < g ? (work ? work : 1u) : g);
+}
+
 // Opt-in per-kernel timing (dr_trace_begin / dr_trace_end): when tracing is
 // on for the calling host thread, an event is recorded on the stream after
 // each kernel launch; the time between consecutive events is that kernel's.

@@ -86,20 +86,31 @@ __global__ __launch_bounds__(HIST_THREADS) void k_topr_hist(Work w, const float 
     const float *gt = g + in.off;
     uint32_t *mine = h[(threadIdx.x >> 6) % HIST_SUB];
     uint32_t nonfinite = 0;
-    // 8 loads in flight per thread before any is used
-    for (uint64_t b0 = lo; b0 < hi; b0 += 8 * HIST_THREADS) {
-        uint32_t key[8];
+    // 8 values per thread per step; the next step's values are in flight
+    // while this step's are counted.  Reads past the block's range return 0
+    // through the buffer view and are not counted.
+    constexpr uint32_t STEP = 8 * HIST_THREADS;
+    const uint32_t n = (uint32_t)(hi > lo ? hi - lo : 0);
+    const __amdgpu_buffer_rsrc_t gv = buffer_view(gt + lo, 4u * n);
+    uint32_t vn[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const uint64_t i = b0 + u * HIST_THREADS + threadIdx.x;
-            key[u] = mag_key(gt[i < hi ? i : hi - 1]);
+    for (int u = 0; u < 8; ++u) vn[u] = buffer_u32(gv, 4u * (u * HIST_THREADS + threadIdx.x));
+    for (uint32_t b0 = 0; b0 < n; b0 += STEP) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = vn[u];
+        if (b0 + STEP < n) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) vn[u] = buffer_u32(gv, 4u * (b0 + STEP + u * HIST_THREADS + threadIdx.x));
         }
+        asm volatile("" ::: "memory");
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-            const uint64_t i = b0 + u * HIST_THREADS + threadIdx.x;
-            if (i < hi) {
-                nonfinite |= key[u] >= 0x7f800000u;
-                atomicAdd(&mine[key[u] >> HIST1_SHIFT], 1u);
+            const uint32_t i = b0 + u * HIST_THREADS + threadIdx.x;
+            if (i < n) {
+                const uint32_t key = mag_key(__uint_as_float(v[u]));
+                nonfinite |= key >= 0x7f800000u;
+                atomicAdd(&mine[key >> HIST1_SHIFT], 1u);
             }
         }
     }
@@ -196,36 +207,72 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_pick(Work w) {
 // (top-r: key in bin b1) are kept in index order in the tile's own stretch
 // of the candidate arrays, with their number in ccnt[tile].  For the
 // support, tcnt[tile] receives the number of selected elements.
+// What the filter pass needs of a tile's tensor.  Descriptors are read with
+// vector loads (kernels write them), so a tile's fields are read before the
+// next tile's values are requested: waiting for them afterwards would also
+// wait for those values.
+struct FilterTile {
+    uint32_t t, base, d, b1;
+    uint64_t slot, off;
+    bool nz;
+};
+
+__device__ __forceinline__ FilterTile filter_tile(const Work &w, uint32_t tile) {
+    FilterTile f;
+    f.t = tensor_of_tile(w.td, w.ntensors, tile);
+    const TDesc &td = w.td[f.t];
+    f.base = (tile - td.in.tile0) * TILE;
+    f.d = td.in.d;
+    f.slot = td.in.slot;
+    f.off = td.in.off;
+    f.nz = td.in.r == R_NONZERO;
+    f.b1 = f.nz ? 0u : td.b1;
+    return f;
+}
+
+// The 16 values of a thread for a tile, read through a raw buffer view
+// (reads past the tensor's end return 0 and touch no memory).
+__device__ __forceinline__ void filter_load(const float *g, const FilterTile &f, float x[16]) {
+    const __amdgpu_buffer_rsrc_t gv = buffer_view(g + f.off + f.base, 4u * min(TILE, f.d - min(f.d, f.base)));
+#pragma unroll
+    for (int j = 0; j < 16; ++j) x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * NTHREADS + threadIdx.x)));
+}
+
 __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float *__restrict__ g) {
     __shared__ uint32_t wcnt[16 * NWAVES];
     __shared__ uint32_t woff[16 * NWAVES];
     __shared__ uint32_t dcnt[NWAVES];
+    __shared__ uint32_t sbw[TILE_WORDS];
     __shared__ uint32_t bad;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     if (threadIdx.x == 0) bad = 0;
     __syncthreads();
+    // the next tile's values are in flight while this tile is classified
+    float xn[16];
+    FilterTile fn{};
+    if (blockIdx.x < w.ntiles_total) {
+        fn = filter_tile(w, blockIdx.x);
+        filter_load(g, fn, xn);
+    }
     for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
-        TDesc &td = w.td[t];
-        const uint32_t lt = tile - td.in.tile0;
-        const uint32_t base = lt * TILE;
-        const uint32_t d = td.in.d;
-        const uint64_t slot = td.in.slot;
-        const bool nz = td.in.r == R_NONZERO;
-        const uint32_t b1 = nz ? 0u : td.b1;
-        const float *gt = g + td.in.off;
+        const FilterTile f = fn;
+        const bool more = tile + gridDim.x < w.ntiles_total;
+        if (more) fn = filter_tile(w, tile + gridDim.x);
+        float x[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) x[j] = xn[j];
+        if (more) filter_load(g, fn, xn);
+        // keeps the scheduler from sinking the loads next to their uses
+        asm volatile("" ::: "memory");
+        const uint32_t base = f.base, d = f.d, b1 = f.b1;
+        const uint64_t slot = f.slot;
+        const bool nz = f.nz;
         uint32_t keys[16];
         uint64_t cmask[16];
         uint32_t nonfinite = 0, ndef = 0;
-        // all 16 loads in flight before any is used; reads past the tensor's
-        // end return 0 through the buffer view
-        const __amdgpu_buffer_rsrc_t gv = buffer_view(gt + base, 4u * min(TILE, d - min(d, base)));
-        float x[16];
-#pragma unroll
-        for (int j = 0; j < 16; ++j) x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * NTHREADS + threadIdx.x)));
-        // keeps the scheduler from sinking each load next to its use (it
-        // otherwise trades the 16 reads in flight for registers)
-        asm volatile("" ::: "memory");
+        // lane 2j + h ends up holding half h of step j's bitmap ballot, and
+        // lane j the candidate count of step j: selects, not branches
+        uint32_t myword = 0, mycand = 0;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const uint32_t i = base + j * NTHREADS + threadIdx.x;
@@ -233,18 +280,21 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
             const uint32_t key = valid ? mag_key(x[j]) : 0u;
             nonfinite |= key >= 0x7f800000u;
             const uint32_t bin = key >> HIST1_SHIFT;
-            const bool def = valid && (nz ? key != 0u : bin > b1);
-            const bool cand = valid && !nz && bin == b1;
+            // bitwise, not short-circuit: no branches per step
+            const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > b1)));
+            const bool cand = valid & !nz & (bin == b1);
             const uint64_t dm = ballot(def);
             cmask[j] = ballot(cand);
             keys[j] = key;
             ndef += popc64(dm);
-            if (lane == 0 || lane == 32) {
-                const uint32_t word = (uint32_t)((slot + base + j * NTHREADS + wv * 64 + lane) >> 5);
-                w.selbits[word] = lane == 0 ? (uint32_t)dm : (uint32_t)(dm >> 32);
-            }
-            if (lane == 0) wcnt[j * NWAVES + wv] = popc64(cmask[j]);
+            myword = lane == 2u * j ? (uint32_t)dm : (lane == 2u * j + 1u ? (uint32_t)(dm >> 32) : myword);
+            mycand = lane == (uint32_t)j ? popc64(cmask[j]) : mycand;
         }
+        // the tile's bitmap words are staged in LDS and written by one
+        // coalesced store after the barrier (two-lane stores per step cost a
+        // third of the pass's read bandwidth)
+        if (lane < 32) sbw[(lane >> 1) * (NTHREADS / 32) + wv * 2 + (lane & 1)] = myword;
+        if (lane < 16) wcnt[lane * NWAVES + wv] = mycand;
         if (nonfinite) bad = 1;
         if (lane == 0) dcnt[wv] = ndef;
         __syncthreads();
@@ -262,9 +312,10 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         }
         __syncthreads();
         if (threadIdx.x == 0 && bad) {
-            atomicOr(&td.flags, FLAG_NONFINITE);
+            atomicOr(&w.td[f.t].flags, FLAG_NONFINITE);
             bad = 0;
         }
+        if (threadIdx.x < TILE_WORDS) w.selbits[((slot + base) >> 5) + threadIdx.x] = sbw[threadIdx.x];
         const uint64_t cbase = slot + base;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
@@ -522,14 +573,14 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
         k_topr_pick<<<w.ntensors, NTHREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_pick");
     }
-    k_select_filter<<<grid_persist, NTHREADS, 0, s>>>(w, g);
+    k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     if (any_topr) {
         k_topr_candhist<<<hist_blocks, SEL_THREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_candhist");
         k_topr_pickA<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_pickA");
-        k_topr_candpass<<<grid_persist, NTHREADS, 0, s>>>(w);
+        k_topr_candpass<<<resident_grid(k_topr_candpass, NTHREADS, (w.ntiles_total + CP_TILES - 1) / CP_TILES), NTHREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_candpass");
         k_topr_final<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_final");
@@ -663,7 +714,8 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
 }
 
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s) {
-    k_select_filter<<<grid_persist, NTHREADS, 0, s>>>(w, g);
+    (void)grid_persist;
+    k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     // |S| from the per-tile counts of the filter pass
     k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr, nullptr);
