@@ -78,7 +78,7 @@ struct Carve {
     uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0;
     size_t bytes = 0;
     size_t o_td, o_glob, o_done, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
-        o_V, o_sstat, o_sdig, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
+        o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
 
     void plan() {
         size_t at = 0;
@@ -104,6 +104,7 @@ struct Carve {
         o_V = take(4 * slots);
         o_sstat = take(8ull * 4 * SORT_BINS * ntiles);
         o_sdig = take(4ull * 4 * SORT_BINS * ntensors);
+        o_ttab = take(4ull * ntiles);
         o_fit = take(8ull * NMOM * fit_blocks);
         o_btab = take(4 * btab);
         o_brow = take(8 * bslices);
@@ -140,6 +141,7 @@ struct Carve {
         w.sub_idx = (uint32_t *)(ws + o_V);
         w.sstat = (uint64_t *)(ws + o_sstat);
         w.sdig = (uint32_t *)(ws + o_sdig);
+        w.tile_tensor = (uint32_t *)(ws + o_ttab);
         w.fit_part = (double *)(ws + o_fit);
         w.fit_runs = (uint32_t)(fit_blocks / FIT_CHUNKS);
         w.btab = (uint32_t *)(ws + o_btab);

@@ -374,7 +374,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
     const uint32_t t_end = min(w.ntiles_total, t_begin + per);
     uint32_t cached = 0xffffffffu, fcw = 0;
     for (uint32_t rb = t_begin; rb < t_end;) {
-        const uint32_t t = tensor_of_tile(w.td, w.ntensors, rb);
+        const uint32_t t = tensor_of_tile(w, rb);
         TDesc &td = w.td[t];
         const uint32_t re = min(min(t_end, td.in.tile0 + td.in.ntiles), rb + RUN_TILES);
         const uint32_t nq = (re - rb) * QPT;
@@ -403,6 +403,20 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
             if (qi >= nq) break;
             const uint32_t tile = rb + qi / QPT;
             const uint32_t wbase = (tile - td.in.tile0) * TILE + (qi % QPT) * QWAVE;  // first index
+            if (MODE == Q_DECODE) {
+                // the receiver's dense output starts as zeros here, written
+                // while the filter reads (an L2-bound loop) are in flight;
+                // the emit pass then stores only the positives
+                float *dz = o.dense_out + td.in.off + wbase;
+                if (wbase + QWAVE <= d && ((uintptr_t)dz & 15u) == 0) {
+#pragma unroll
+                    for (uint32_t u = 0; u < QWAVE / 256; ++u)
+                        ((float4 *)dz)[u * 64 + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                } else {
+                    for (uint32_t e = lane; e < QWAVE; e += 64)
+                        if (wbase + e < d) dz[e] = 0.0f;
+                }
+            }
             if (lane < QWAVE / 32) mw[lane] = 0;
             __builtin_amdgcn_wave_barrier();
             // probe 0 over the quarter's 1024 indices: 16 per lane, all
@@ -490,9 +504,9 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 //     each thread lists the positives among its 16 elements at their
 //     tile-local ranks;
 //  B. thread p takes positives p, p + 256, ...: consecutive threads handle
-//     consecutive ranks, so the reorder-map reads and every output write
-//     are coalesced;
-//  C. (receiver) the dense tile, 16-byte stores, zeros included.
+//     consecutive ranks, so the reorder-map reads and the list outputs are
+//     coalesced; the receiver also stores each value into the dense output,
+//     which the probe pass has already zeroed.
 // The next tile's positives words are read before this tile's B and C run.
 constexpr uint32_t EMIT_COEF = 512;  // coefficients staged in LDS (else read from the payload)
 
@@ -506,17 +520,20 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);  // 4 groups of 4 elements per thread
     uint32_t coef_t = 0xffffffffu;                     // tensor whose coefficients cf holds
     uint32_t tile = blockIdx.x;
-    uint32_t word = 0;
-    if (tile < w.ntiles_total && threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
+    uint32_t word = 0, q0n = 0;
+    if (tile < w.ntiles_total) {
+        q0n = w.toff[tile];
+        if (threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
+    }
     for (; tile < w.ntiles_total; tile += gridDim.x) {
-        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
+        const uint32_t t = tensor_of_tile(w, tile);
         TDesc &td = w.td[t];
         // descriptor fields in registers (the output stores could alias
         // them for all the compiler knows)
         const uint32_t lt = tile - td.in.tile0;
         const uint32_t d = td.in.d;
         const uint64_t toff_el = td.in.off, tslot = td.in.slot;
-        const uint32_t q0 = w.toff[tile];
+        const uint32_t q0 = q0n;
         uint32_t tot;
         const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
         if (threadIdx.x < TILE_WORDS) {
@@ -551,7 +568,10 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
         // the next tile's positives words, in flight during B and C
         const uint32_t nt = tile + gridDim.x;
         word = 0;
-        if (nt < w.ntiles_total && threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)nt * TILE_WORDS + threadIdx.x];
+        if (nt < w.ntiles_total) {
+            q0n = w.toff[nt];
+            if (threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)nt * TILE_WORDS + threadIdx.x];
+        }
         __syncthreads();
         // B: one positive per thread
         const uint32_t base = lt * TILE;
@@ -582,31 +602,10 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
                         if (o.counts_out) atomicOr((unsigned long long *)&o.counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
                     }
                 }
-                slot[p] = __float_as_uint(y);
+                o.dense_out[toff_el + i] = y;  // zeros elsewhere come from the probe pass
                 const uint64_t at = toff_el + q;
                 if (o.idx_out) o.idx_out[at] = i;
                 if (o.val_out) o.val_out[at] = y;
-            }
-        }
-        if (MODE == Q_DECODE) {
-            __syncthreads();
-            // C: the dense tile
-#pragma unroll
-            for (uint32_t u = 0; u < GROUPS; ++u) {
-                const uint32_t e0 = u * 4 * NTHREADS + threadIdx.x * 4;
-                float y4[4];
-                uint32_t r = rank0[u];
-#pragma unroll
-                for (uint32_t v = 0; v < 4; ++v) y4[v] = ((nib[u] >> v) & 1u) ? __uint_as_float(slot[r++]) : 0.0f;
-                float *dst = o.dense_out + toff_el + (uint64_t)base + e0;
-                const uint32_t ie = base + e0;
-                if (ie + 4 <= d && ((uintptr_t)dst & 15u) == 0) {
-                    *(float4 *)dst = make_float4(y4[0], y4[1], y4[2], y4[3]);
-                } else {
-#pragma unroll
-                    for (uint32_t v = 0; v < 4; ++v)
-                        if (ie + v < d) dst[v] = y4[v];
-                }
             }
         }
         __syncthreads();  // pw, pre and slot are rewritten by the next tile

@@ -126,6 +126,7 @@ struct Work {
     TDesc *td;
     Glob *glob;
     uint64_t *counts_out;     // the round trip's per-tensor counts (nullable): late flags go here too
+    uint32_t *tile_tensor;    // tensor of each tile (filled by k_init)
     uint32_t ntensors;
     uint32_t ntiles_total;    // sum of ntiles
     uint64_t slots;           // padded elements = ntiles_total * TILE
@@ -319,18 +320,8 @@ __device__ __forceinline__ uint32_t buffer_u32(__amdgpu_buffer_rsrc_t v, uint32_
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(v, byte_off, 0, 0);
 }
 
-// tensor holding global tile `tile` (tiles of a tensor are contiguous)
-__device__ __forceinline__ uint32_t tensor_of_tile(const TDesc *td, uint32_t ntensors, uint32_t tile) {
-    uint32_t lo = 0, hi = ntensors;  // td[lo].tile0 <= tile < td[hi].tile0
-    while (hi - lo > 1) {
-        uint32_t mid = (lo + hi) >> 1;
-        if (td[mid].in.tile0 <= tile)
-            lo = mid;
-        else
-            hi = mid;
-    }
-    return lo;
-}
+// tensor holding global tile `tile` (one read of the table k_init fills)
+__device__ __forceinline__ uint32_t tensor_of_tile(const Work &w, uint32_t tile) { return w.tile_tensor[tile]; }
 
 // Magnitude key: IEEE bits with the sign cleared (orders like |x|).
 __device__ __forceinline__ uint32_t mag_key(float x) { return __float_as_uint(x) & 0x7fffffffu; }

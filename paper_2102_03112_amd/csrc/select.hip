@@ -33,6 +33,11 @@ __global__ __launch_bounds__(NTHREADS) void k_init(Work w, InitArgs a, ZeroArgs 
         t.m_words = t.in.m_words_in;
     }
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint32_t c = 0; c < a.count; ++c) {
+        const TInit &in = a.t[c];
+        for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < in.ntiles; i += stride)
+            w.tile_tensor[in.tile0 + i] = a.first + c;
+    }
     for (uint32_t r = 0; r < z.n; ++r) {
         uint32_t *p = (uint32_t *)z.z[r].p;
         for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < z.z[r].words; i += stride) p[i] = 0u;
@@ -219,7 +224,7 @@ struct FilterTile {
 
 __device__ __forceinline__ FilterTile filter_tile(const Work &w, uint32_t tile) {
     FilterTile f;
-    f.t = tensor_of_tile(w.td, w.ntensors, tile);
+    f.t = tensor_of_tile(w, tile);
     const TDesc &td = w.td[f.t];
     f.base = (tile - td.in.tile0) * TILE;
     f.d = td.in.d;
@@ -410,7 +415,7 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
             const uint32_t tile = g0 + threadIdx.x;
             uint32_t c = 0, t = 0;
             if (threadIdx.x < CP_TILES && tile < w.ntiles_total) {
-                t = tensor_of_tile(w.td, w.ntensors, tile);
+                t = tensor_of_tile(w, tile);
                 const TDesc &td = w.td[t];
                 c = td.in.r == R_NONZERO ? 0u : w.ccnt[tile];
                 tbase[threadIdx.x] = td.in.slot + (uint64_t)(tile - td.in.tile0) * TILE;
@@ -679,7 +684,7 @@ __global__ __launch_bounds__(NTHREADS) void k_compact_selection(Work w, const fl
                                                                 float *__restrict__ val_out) {
     __shared__ uint32_t scratch[NWAVES + 1];
     for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-        const uint32_t t = tensor_of_tile(w.td, w.ntensors, tile);
+        const uint32_t t = tensor_of_tile(w, tile);
         const TDesc &td = w.td[t];
         const uint32_t lt = tile - td.in.tile0;
         uint32_t word = 0;
