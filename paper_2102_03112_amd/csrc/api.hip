@@ -190,7 +190,10 @@ struct Plan {
     Carve carve;
     uint32_t bl_chunks = 0, bl_slices = 0, max_slices = 0, hash_per_round = 1, kmax = 0;
     uint64_t bl_items = 0;
+    std::vector<uint64_t> bl_mcap;  // planned filter bits per tensor
     bool any_topr = false;
+    bool direct = false;  // every filter small enough for the direct insert
+    uint32_t dir_blocks = 0, dir_slices = 0;
 };
 
 // Per-tensor Bloom insert layout for at most n_cap items and m_cap_bits:
@@ -199,6 +202,7 @@ struct Plan {
 
 void plan_bloom(TInit &in, uint64_t n_cap, uint64_t m_cap_bits, bool from_bitmap, Plan &p) {
     p.bl_ncap.push_back(n_cap);
+    p.bl_mcap.push_back(m_cap_bits);
     if (from_bitmap) {
         const uint64_t chunk = std::max<uint64_t>(CHUNK_TILES, ceil_div(in.ntiles, MAX_CHUNKS));
         in.bl_chunk = (uint32_t)chunk;
@@ -238,6 +242,47 @@ void plan_bloom_rounds(Plan &p, uint32_t k) {
         p.t[i].bl_poscap = p.bl_ncap[i] * h;
         at += p.bl_ncap[i] * h;
     }
+}
+
+// The direct insert, when every planned filter has at most DIR_MAX_BITS bits
+// and the partial slices fit in the position buffer: G item chunks per
+// slice, about 1024 blocks in all (at most 64 chunks).
+void plan_bloom_direct(Plan &p, bool from_bitmap) {
+    p.direct = false;
+    uint64_t nsl_all = 0;
+    for (uint64_t m : p.bl_mcap) {
+        if (m > DIR_MAX_BITS) return;
+        nsl_all += ceil_div(m / 32, DIR_SLICE_WORDS);
+    }
+    if (nsl_all == 0) return;
+    uint64_t G = std::max<uint64_t>(1, std::min<uint64_t>(64, 1024 / nsl_all));
+    auto words = [&](uint64_t g) {
+        uint64_t tot = 0;
+        for (uint64_t m : p.bl_mcap) tot += ceil_div(m / 32, DIR_SLICE_WORDS) * g * std::min<uint64_t>(DIR_SLICE_WORDS, m / 32);
+        return tot;
+    };
+    const uint64_t cap_words = p.carve.pos_capacity() / 2;  // the position buffer, as 32-bit words
+    while (G > 1 && words(G) > cap_words) G /= 2;
+    if (words(G) > cap_words) return;
+    uint64_t blk = 0, sl = 0, pb = 0;
+    for (size_t i = 0; i < p.t.size(); ++i) {
+        TInit &in = p.t[i];
+        const uint64_t mw = p.bl_mcap[i] / 32;
+        in.dir_nsl = (uint32_t)ceil_div(mw, DIR_SLICE_WORDS);
+        in.dir_g = (uint32_t)G;
+        in.dir_sw = (uint32_t)std::min<uint64_t>(DIR_SLICE_WORDS, mw);
+        in.dir_blk0 = (uint32_t)blk;
+        in.dir_sl0 = (uint32_t)sl;
+        in.dir_pb = pb;
+        in.dir_per = from_bitmap ? (uint32_t)ceil_div(in.ntiles, G)
+                                 : (uint32_t)std::max<uint64_t>(1, ceil_div(p.bl_ncap[i], G));
+        blk += (uint64_t)in.dir_nsl * G;
+        sl += in.dir_nsl;
+        pb += (uint64_t)in.dir_nsl * G * in.dir_sw;
+    }
+    p.direct = true;
+    p.dir_blocks = (uint32_t)blk;
+    p.dir_slices = (uint32_t)sl;
 }
 
 dr_status check_cfg(const dr_config *cfg) {
@@ -337,6 +382,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     p.carve.fit_blocks = fit_blocks;
     p.carve.plan();
     plan_bloom_rounds(p, k);
+    plan_bloom_direct(p, true);
     return DR_OK;
 }
 
@@ -393,7 +439,10 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
         DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
     else
         DR_HIP(launch_nonzero(w, g, persist_grid(8), s));
-    DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
+    if (p.direct)
+        DR_HIP(launch_bloom_direct(w, true, p.dir_blocks, p.dir_slices, s));
+    else
+        DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
     DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, true, counts_out, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
@@ -638,6 +687,7 @@ dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap
     plan_bloom(in, n_cap, m_bits, false, p);
     p.carve.plan();
     plan_bloom_rounds(p, k);
+    plan_bloom_direct(p, false);
     if (!ws_ok(ws, ws_bytes, p.carve.bytes))
         return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
     Work w = p.carve.view((uint8_t *)ws);
@@ -645,7 +695,10 @@ dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap
     trace_call(s);
     DR_HIP(run_init(w, p.t, s));
     DR_HIP(launch_import_n(w, n, n_cap, s));
-    DR_HIP(launch_bloom_insert(w, false, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
+    if (p.direct)
+        DR_HIP(launch_bloom_direct(w, false, p.dir_blocks, p.dir_slices, s));
+    else
+        DR_HIP(launch_bloom_insert(w, false, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
     return DR_OK;
 }
 

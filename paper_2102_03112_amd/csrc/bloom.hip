@@ -215,6 +215,168 @@ __global__ __launch_bounds__(NTHREADS) void k_bloom_fill(Work w, uint32_t j0, ui
     for (uint32_t i = threadIdx.x; i < lim; i += NTHREADS) out[i] = words[i];
 }
 
+// ---------------------------------------------------------------------------
+// Direct insert, for filters of at most DIR_MAX_BITS bits: block (s, c) of
+// a tensor hashes the items of chunk c, sets the bits that fall in slice s
+// in a 128 KiB LDS copy, and writes that copy to its own partial slice; a
+// second kernel ORs each slice's partials.  OR is commutative, so the
+// filter is the same as any other insertion order gives.  Two launches and
+// no position buffer: the hashing is repeated once per slice, which is
+// cheap for the few slices such filters have.
+// ---------------------------------------------------------------------------
+constexpr uint32_t DIR_THREADS = 1024;
+
+__device__ __forceinline__ uint32_t tensor_of_dir_block(const Work &w, uint32_t b) {
+    uint32_t lo = 0, hi = w.ntensors;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (w.td[mid].in.dir_blk0 <= b)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint32_t tensor_of_dir_slice(const Work &w, uint32_t s) {
+    uint32_t lo = 0, hi = w.ntensors;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (w.td[mid].in.dir_sl0 <= s)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+template <bool FROM_BITMAP>
+__global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct(Work w) {
+    __shared__ __attribute__((aligned(16))) uint32_t sl[DIR_SLICE_WORDS];
+    __shared__ uint32_t queue[DIR_THREADS / 64][128];  // per wave: selected indices waiting to be hashed
+    const uint32_t t = tensor_of_dir_block(w, blockIdx.x);
+    const TDesc &td = w.td[t];
+    const uint32_t local = blockIdx.x - td.in.dir_blk0;
+    const uint32_t G = td.in.dir_g;
+    if (local >= td.in.dir_nsl * G) return;
+    const uint32_t s = local / G, c = local % G;
+    const uint32_t m_words = td.m_words, m_bits = m_words * 32u, k = td.in.k;
+    const uint32_t w0 = s * DIR_SLICE_WORDS;
+    if (w0 >= m_words) return;  // past the filter this call built
+    const uint32_t nw = min(DIR_SLICE_WORDS, m_words - w0);
+    const uint32_t b0 = w0 * 32u, nb = nw * 32u;
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    for (uint32_t i = threadIdx.x; i < DIR_SLICE_WORDS / 4; i += DIR_THREADS) ((uint4 *)sl)[i] = make_uint4(0, 0, 0, 0);
+    __syncthreads();
+    auto add = [&](uint32_t x) {
+        const uint32_t km = mm3_key(x);
+        for (uint32_t j = 0; j < k; ++j) {
+            const uint32_t p = bloom_pos(km, j, m_bits) - b0;  // wraps for positions below the slice
+            if (p < nb) atomicOr(&sl[p >> 5], 1u << (p & 31u));
+        }
+    };
+    if (FROM_BITMAP) {
+        const uint32_t per = td.in.dir_per;
+        // chunk c's bitmap words [wa, wb); chunks past the tensor's tiles
+        // (more chunks than tiles) are empty
+        const uint32_t wb = min(td.in.ntiles, (c + 1) * per) * TILE_WORDS;
+        const uint32_t wa = min(c * per * TILE_WORDS, wb);
+        // eight bitmap words per thread in flight, read through a buffer
+        // view of the chunk (reads past it return 0).  A wave's selected
+        // indices go through its queue, and are hashed 64 at a time, so all
+        // lanes work however sparse the bitmap is.
+        const __amdgpu_buffer_rsrc_t sv = buffer_view(w.selbits + (td.in.slot >> 5) + wa, 4u * (wb - wa));
+        uint32_t *q = queue[wv];
+        uint32_t qn = 0;
+        for (uint32_t x0 = 0; x0 < wb - wa; x0 += 8 * DIR_THREADS) {
+            uint32_t wd[8];
+#pragma unroll
+            for (uint32_t u = 0; u < 8; ++u) wd[u] = buffer_u32(sv, 4u * (x0 + u * DIR_THREADS + threadIdx.x));
+#pragma unroll
+            for (uint32_t u = 0; u < 8; ++u) {
+                uint32_t word = wd[u];
+                const uint32_t base = (wa + x0 + u * DIR_THREADS + threadIdx.x) * 32u;
+                while (ballot(word != 0u)) {
+                    const bool has = word != 0u;
+                    const uint32_t item = base + (has ? (uint32_t)(__ffs(word) - 1) : 0u);
+                    word &= word - 1u;
+                    const uint64_t m = ballot(has);
+                    if (has) q[qn + lanes_below(m)] = item;
+                    qn += popc64(m);
+                    __builtin_amdgcn_wave_barrier();
+                    if (qn >= 64) {  // the last 64 entries, one per lane
+                        const uint32_t x = q[qn - 64 + lane];
+                        __builtin_amdgcn_wave_barrier();
+                        qn -= 64;
+                        add(x);
+                    }
+                }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane < qn) add(q[lane]);
+    } else {
+        const uint32_t per = td.in.dir_per, n = td.n;
+        const uint32_t qa = c * per, qb = min(n, qa + per);
+        const __amdgpu_buffer_rsrc_t iv = buffer_view(w.S + td.in.slot + qa, 4u * (qb - min(qa, qb)));
+        for (uint32_t x0 = 0; qa + x0 < qb; x0 += 8 * DIR_THREADS) {
+            uint32_t it[8];
+#pragma unroll
+            for (uint32_t u = 0; u < 8; ++u) it[u] = buffer_u32(iv, 4u * (x0 + u * DIR_THREADS + threadIdx.x));
+#pragma unroll
+            for (uint32_t u = 0; u < 8; ++u)
+                if (qa + x0 + u * DIR_THREADS + threadIdx.x < qb) add(it[u]);
+        }
+    }
+    __syncthreads();
+    uint32_t *part = (uint32_t *)w.bpos + td.in.dir_pb + (uint64_t)local * td.in.dir_sw;
+    if ((((uintptr_t)part) & 15u) == 0) {
+        for (uint32_t i = threadIdx.x; i < nw / 4; i += DIR_THREADS) ((uint4 *)part)[i] = ((const uint4 *)sl)[i];
+        for (uint32_t i = (nw & ~3u) + threadIdx.x; i < nw; i += DIR_THREADS) part[i] = sl[i];
+    } else {
+        for (uint32_t i = threadIdx.x; i < nw; i += DIR_THREADS) part[i] = sl[i];
+    }
+}
+
+// One thread per filter word: the OR of the word's partials, in chunk order.
+__global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct_or(Work w) {
+    const uint32_t gs = blockIdx.x / (DIR_SLICE_WORDS / DIR_THREADS);  // slice over all tensors
+    const uint32_t part_of_slice = blockIdx.x % (DIR_SLICE_WORDS / DIR_THREADS);
+    const uint32_t t = tensor_of_dir_slice(w, gs);
+    const TDesc &td = w.td[t];
+    const uint32_t s = gs - td.in.dir_sl0;
+    if (s >= td.in.dir_nsl) return;
+    const uint32_t wi = part_of_slice * DIR_THREADS + threadIdx.x;  // word within the slice
+    const uint32_t m_words = td.m_words;
+    const uint32_t w0 = s * DIR_SLICE_WORDS;
+    if (w0 >= m_words || wi >= min(DIR_SLICE_WORDS, m_words - w0)) return;
+    const uint32_t G = td.in.dir_g, sw = td.in.dir_sw;
+    const uint32_t *part = (const uint32_t *)w.bpos + td.in.dir_pb + (uint64_t)s * G * sw + wi;
+    uint32_t acc = 0;
+    uint32_t c = 0;
+    for (; c + 8 <= G; c += 8) {  // eight partials in flight
+        uint32_t v[8];
+#pragma unroll
+        for (uint32_t u = 0; u < 8; ++u) v[u] = part[(uint64_t)(c + u) * sw];
+#pragma unroll
+        for (uint32_t u = 0; u < 8; ++u) acc |= v[u];
+    }
+    for (; c < G; ++c) acc |= part[(uint64_t)c * sw];
+    td.in.bits[w0 + wi] = acc;
+}
+
+hipError_t launch_bloom_direct(const Work &w, bool from_bitmap, uint32_t blocks, uint32_t slices, hipStream_t s) {
+    if (blocks == 0) return hipSuccess;
+    if (from_bitmap)
+        k_bloom_direct<true><<<blocks, DIR_THREADS, 0, s>>>(w);
+    else
+        k_bloom_direct<false><<<blocks, DIR_THREADS, 0, s>>>(w);
+    trace_mark(s, "k_bloom_direct");
+    k_bloom_direct_or<<<slices * (DIR_SLICE_WORDS / DIR_THREADS), DIR_THREADS, 0, s>>>(w);
+    trace_mark(s, "k_bloom_direct_or");
+    return hipGetLastError();
+}
+
 hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_chunks, uint32_t total_slices,
                                uint32_t max_slices, uint32_t hash_per_round, uint32_t kmax, hipStream_t s) {
     // LDS for one counter per slice of the largest filter

@@ -25,6 +25,9 @@ constexpr uint32_t NWAVES = NTHREADS / 64;
 constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
 constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: fewest tiles per chunk
 constexpr uint32_t MAX_CHUNKS = 256;
+constexpr uint32_t DIR_SLICE_LOG2 = 20;        // direct insert: 2^20-bit (128 KiB) slices in LDS
+constexpr uint32_t DIR_SLICE_WORDS = 1u << (DIR_SLICE_LOG2 - 5);
+constexpr uint64_t DIR_MAX_BITS = 8ull << DIR_SLICE_LOG2;  // at most 8 slices per tensor
 constexpr int BUFFER_RSRC_WORD3 = 0x00020000;  // gfx9 buffer descriptor word 3 (32-bit dword format)          // Bloom insert: most item chunks per tensor
 constexpr uint32_t SLICE_LOG2_MAX = 16;       // Bloom fill slices: at most 2^16 bits (8 KiB of LDS)
 constexpr uint32_t SLICE_WORDS_MAX = (1u << SLICE_LOG2_MAX) / 32;
@@ -69,7 +72,17 @@ struct TInit {
     uint32_t coef_stride;// floats per run in `coef` when it is given
     uint32_t slice_log2; // Bloom fill slice size (bits, log2)
     uint64_t rec_cap;    // payload record capacity in bytes (receiver checks the header against it)
-    uint64_t bl_poscap;  // Bloom insert: positions reserved for this tensor per round    // payload record capacity in bytes (receiver checks the header against it)
+    uint64_t bl_poscap;  // Bloom insert: positions reserved for this tensor per round
+    // direct insert (filters of at most DIR_MAX_BITS bits): block (s, c) sets
+    // the bits of slice s from item chunk c in LDS and writes them to its
+    // own partial slice; an OR over the chunks then gives the filter
+    uint64_t dir_pb;     // first partial word of this tensor
+    uint32_t dir_blk0;   // first direct-insert block of this tensor
+    uint32_t dir_sl0;    // first slice of this tensor (over all tensors)
+    uint32_t dir_nsl;    // slices planned (covers the largest possible filter)
+    uint32_t dir_g;      // item chunks
+    uint32_t dir_sw;     // words per partial slice: min(DIR_SLICE_WORDS, planned filter words)
+    uint32_t dir_per;    // bitmap tiles (from the bitmap) or items (from a list) per chunk
 };
 
 // Per-tensor descriptor, in device memory.

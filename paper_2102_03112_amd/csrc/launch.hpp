@@ -67,6 +67,7 @@ hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream
 // Insert in rounds of `hash_per_round` hash functions (the position buffer
 // holds that many positions per reserved item); items come from the
 // selection bitmap or from the list w.S.
+hipError_t launch_bloom_direct(const Work &w, bool from_bitmap, uint32_t blocks, uint32_t slices, hipStream_t s);
 hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_chunks, uint32_t total_slices,
                                uint32_t max_slices, uint32_t hash_per_round, uint32_t kmax, hipStream_t s);
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s);
