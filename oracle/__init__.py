@@ -26,6 +26,9 @@ _lib = None
 
 OK, EINVAL, ECAPACITY = 0, -1, -2
 R_NONZERO = (1 << 64) - 1  # "select every nonzero" instead of a top-r count
+# index policies (Section 4; Sections 10.4, 10.5)
+POLICY_P0, POLICY_RANDOM, POLICY_LEFTMOST, POLICY_MIDDLE, POLICY_RIGHTMOST = 0, 1, 2, 3, 4
+NO_SLOT = 0xFFFFFFFF
 
 
 class OracleError(RuntimeError):
@@ -66,6 +69,8 @@ def _load():
             [f32p, u64, u32, u32, f32p, f64p, u32p, u32p, u32p, u32p],
         ),
         "drref_curvefit_decode": (ctypes.c_int, [f32p, u32p, u64, u32, u32, f32p]),
+        "drref_perm": (u32, [u32, u64, u32]),
+        "drref_policy_slots": (ctypes.c_int, [u64, u64, u32, u32, u32p, u64p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -275,6 +280,26 @@ def sigma_unpack(sigma: np.ndarray, n: int) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
+# index policies
+# --------------------------------------------------------------------------
+
+
+def perm(q: int, N: int, seed: int) -> int:
+    """The keyed permutation of the ranks [0, N) that policy P1 uses."""
+    return int(_load().drref_perm(q, N, seed))
+
+
+def policy_slots(npos: int, r: int, policy: int, seed: int) -> tuple[np.ndarray, int]:
+    """Value number of each positive rank (NO_SLOT when the policy drops it)
+    and the number of values kept."""
+    out = np.zeros(max(npos, 1), dtype=np.uint32)
+    nc = ctypes.c_uint64()
+    _check(_load().drref_policy_slots(npos, r, policy, seed, _ptr(out, ctypes.c_uint32), ctypes.byref(nc)),
+           "drref_policy_slots")
+    return out[:npos], int(nc.value)
+
+
+# --------------------------------------------------------------------------
 # one round trip over one tensor, in the paper's order
 # --------------------------------------------------------------------------
 
@@ -286,12 +311,15 @@ class TensorResult:
     m: int
     k: int
     bits: np.ndarray  # Bloom filter words
-    P: np.ndarray  # sender-side P0 positives, ascending
-    V: np.ndarray  # g[P], from the dense original
+    P: np.ndarray  # sender-side positives, ascending
+    V: np.ndarray  # coded values in value order: g at the kept positives (Section 4)
     fit: FitPayload
     P_dec: np.ndarray  # receiver-side positives, from the filter words only
-    vals: np.ndarray  # reconstructed values, one per P_dec entry
+    vals: np.ndarray  # reconstructed value of each P_dec entry (0 where the policy dropped it)
     dense: np.ndarray | None = field(default=None)
+    policy: int = 0
+    seed: int = 0
+    slots: np.ndarray | None = field(default=None)  # value number of each positive rank, or NO_SLOT
 
     def payload_bits(self) -> dict:
         """Bits that cross the network (Figure 3's container): the filter, the
@@ -302,30 +330,41 @@ class TensorResult:
         return {"index": idx, "values": val, "sigma": sig}
 
 
-def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True) -> TensorResult:
-    """Sender: top-r (or support) -> Bloom insert -> P0 query -> V = g[P]
+def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
+                     policy: int = POLICY_P0, seed: int = 0) -> TensorResult:
+    """Sender: top-r (or support) -> Bloom insert -> full-range query (P) ->
+    the policy keeps all of P (P0) or r of it -> V = g at the kept positives
     (values from the dense gradient, Section 4) -> curve-fit encode.
-    Receiver: P0 query from the filter words -> curve-fit decode -> scatter
-    into a dense gradient that is zero off P (Section 4's reconstruction).
-    ``r`` is an int or R_NONZERO."""
+    Receiver: the same query from the filter words -> the same policy ->
+    curve-fit decode -> scatter into a dense gradient that is zero elsewhere
+    (Section 4's reconstruction).  ``r`` is an int or R_NONZERO."""
     g = np.ascontiguousarray(g, dtype=np.float32)
     d = g.size
     S = nonzero(g) if r == R_NONZERO else topr(g, int(r))
     m, k = bloom_params(S.size, fpr)
     bits = bloom_encode(S, m, k)
     P = bloom_query(bits, m, k, d)
-    V = g[P.astype(np.int64)]
+    slots, ncoded = policy_slots(P.size, S.size, policy, seed)
+    kept = slots != NO_SLOT
+    V = np.zeros(ncoded, dtype=np.float32)
+    V[slots[kept].astype(np.int64)] = g[P[kept].astype(np.int64)]
     fit = curvefit_encode(V, degree, n_seg)
+    # receiver: its own query and the same policy over its own positives
     P_dec = bloom_query(bits, m, k, d)
-    vals = curvefit_decode(fit.coef, fit.sigma, P_dec.size, degree, n_seg)
+    slots_dec, nc_dec = policy_slots(P_dec.size, ncoded, policy, seed)
+    y = curvefit_decode(fit.coef, fit.sigma, nc_dec, degree, n_seg)
+    vals = np.zeros(P_dec.size, dtype=np.float32)
+    keep_dec = slots_dec != NO_SLOT
+    vals[keep_dec] = y[slots_dec[keep_dec].astype(np.int64)]
     dense = None
     if want_dense:
         dense = np.zeros(d, dtype=np.float32)
         dense[P_dec.astype(np.int64)] = vals
-    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense)
+    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense, policy, seed, slots)
 
 
-def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True):
+def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
+              policy: int = POLICY_P0, seed: int = 0):
     """Code every tensor g[offsets[t]:offsets[t+1]] independently on local
     indices.  ``ratio`` is (num, den) for top-r with r = ceil(d_t num / den),
     or None for the support of an inherently sparse gradient."""
@@ -333,5 +372,5 @@ def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int
     for t in range(len(offsets) - 1):
         gt = g[offsets[t]: offsets[t + 1]]
         r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
-        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense))
+        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed))
     return out

@@ -557,3 +557,116 @@ int drref_curvefit_decode(const float *coef, const uint32_t *sigma, uint64_t n, 
     }
     return DRREF_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Index policies (Section 4; Sections 10.4 and 10.5).                       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Policy P0 keeps every positive of the query (Section 4, "No-error
+ * approach").  The other policies keep r of the |P| positives, so that only
+ * r values are sent: policy P1 picks them at random (Section 4, "Random
+ * approach"; Section 10.5), the deterministic policies of Section 10.4 take
+ * the leftmost, middle or rightmost r of P in index order.
+ *
+ * Sender and receiver must pick the same r positives without exchanging
+ * them.  Both run the same query, so P is the same on both sides, and P1 is
+ * made reproducible by a keyed pseudo-random permutation pi of the ranks
+ * [0, |P|) that both evaluate: the positive of rank q is kept iff
+ * pi(q) < r, and its value is value number pi(q).  For the deterministic
+ * policies the value number is the rank within the kept run.  (The paper
+ * leaves the source of randomness open; this keyed permutation is this
+ * codec's reading.)
+ *
+ * pi is a 4-round Feistel network on 2h-bit words (h = ceil(ceil(log2 N)/2),
+ * at least 1), with round function F_j(x) = MurmurHash3_x86_32 of the
+ * 4-byte little-endian x with seed (seed + j), reduced to h bits, and cycle
+ * walking (Black and Rogaway, "Ciphers with arbitrary finite domains",
+ * CT-RSA 2002) to stay inside [0, N): the network is applied again until
+ * the value falls below N.  A Feistel network is a bijection of the 2h-bit
+ * words for any round function, and cycle walking restricts a bijection to
+ * a bijection of [0, N).
+ */
+#define DRREF_POLICY_P0 0u
+#define DRREF_POLICY_RANDOM 1u
+#define DRREF_POLICY_LEFTMOST 2u
+#define DRREF_POLICY_MIDDLE 3u
+#define DRREF_POLICY_RIGHTMOST 4u
+#define DRREF_NO_SLOT 0xffffffffu
+
+static uint32_t feistel_round(uint32_t x, uint32_t seed, uint32_t j, uint32_t mask)
+{
+    uint8_t le[4] = {(uint8_t)(x & 0xff), (uint8_t)((x >> 8) & 0xff), (uint8_t)((x >> 16) & 0xff),
+                     (uint8_t)((x >> 24) & 0xff)};
+    return drref_murmur3_32(le, 4, seed + j) & mask;
+}
+
+static uint32_t feistel(uint32_t x, uint32_t h, uint32_t seed)
+{
+    const uint32_t mask = (h >= 32) ? 0xffffffffu : ((1u << h) - 1u);
+    uint32_t L = (x >> h) & mask, R = x & mask;
+    for (uint32_t j = 0; j < 4; ++j) {
+        uint32_t t = L ^ feistel_round(R, seed, j, mask);
+        L = R;
+        R = t;
+    }
+    return (L << h) | R;
+}
+
+/* half width h for a domain of N values: 2h >= ceil(log2 N), h >= 1 */
+static uint32_t feistel_half(uint64_t N)
+{
+    uint32_t bits = 0;
+    while (bits < 32 && (1ull << bits) < N) ++bits;
+    uint32_t h = (bits + 1) / 2;
+    return h < 1 ? 1 : h;
+}
+
+/* pi(q) for q < N (N >= 1, N <= 2^32) */
+uint32_t drref_perm(uint32_t q, uint64_t N, uint32_t seed)
+{
+    const uint32_t h = feistel_half(N);
+    uint32_t y = q;
+    do {
+        y = feistel(y, h, seed);
+    } while ((uint64_t)y >= N);
+    return y;
+}
+
+/*
+ * For each rank q of the |P| = npos positives: the value number it gets, or
+ * DRREF_NO_SLOT if the policy drops it.  The number of kept positives goes to
+ * *ncoded (npos for P0, min(r, npos) otherwise).
+ */
+int drref_policy_slots(uint64_t npos, uint64_t r, uint32_t policy, uint32_t seed, uint32_t *slot_out,
+                       uint64_t *ncoded)
+{
+    if (policy > DRREF_POLICY_RIGHTMOST || npos > 0xffffffffull) return DRREF_EINVAL;
+    const uint64_t keep = policy == DRREF_POLICY_P0 ? npos : (r < npos ? r : npos);
+    *ncoded = keep;
+    const uint64_t mid0 = (npos - keep) / 2, right0 = npos - keep;
+    for (uint64_t q = 0; q < npos; ++q) {
+        uint64_t slot = DRREF_NO_SLOT;
+        switch (policy) {
+        case DRREF_POLICY_P0:
+            slot = q;
+            break;
+        case DRREF_POLICY_RANDOM: {
+            const uint32_t p = drref_perm((uint32_t)q, npos, seed);
+            if (p < keep) slot = p;
+            break;
+        }
+        case DRREF_POLICY_LEFTMOST:
+            if (q < keep) slot = q;
+            break;
+        case DRREF_POLICY_MIDDLE:
+            if (q >= mid0 && q < mid0 + keep) slot = q - mid0;
+            break;
+        default: /* rightmost */
+            if (q >= right0) slot = q - right0;
+            break;
+        }
+        slot_out[q] = (uint32_t)slot;
+    }
+    return DRREF_OK;
+}
