@@ -96,12 +96,18 @@ def copy_calibration(n_bytes=1 << 30, reps=5):
     print(json.dumps({"copy_bytes_read": n_bytes, "copy_bytes_written": n_bytes, "reps": reps}), flush=True)
 
 
+POLICY_NAMES = {0: "P0", 1: "P1", 2: "leftmost", 3: "middle", 4: "rightmost"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="resnet50_25m")
+    ap.add_argument("--policy", type=int, default=0, help="index policy: 0 = P0 (no error), 1 = P1 (random r of P), "
+                                                      "2/3/4 = leftmost/middle/rightmost r of P")
+    ap.add_argument("--policy-seed", type=int, default=20210205, help="key of policy 1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=30.0, help="bound on the oracle's CPU time")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -132,7 +138,7 @@ def main():
     g_host = W.generate(w)
     log(f"bench: generated input in {time.time() - t0:.1f}s sha256={W.sha256(g_host)[:16]}")
 
-    cfg = B.Config.from_workload(w)
+    cfg = B.Config.from_workload(w, args.policy, args.policy_seed)
     total, rec_off = B.payload_layout(cfg)
     n_copies = max(1, min(64, math.ceil(3 * MALL_BYTES / max(1, 4 * d)))) if 4 * d < 2 * MALL_BYTES else 1
     g_dev = [torch.from_numpy(g_host).cuda()]
@@ -220,7 +226,8 @@ def main():
         elems = min(d, int(args.cpu_budget_s * 2.5e6))
         off = [o for o in w.offsets() if o < elems] + [elems]
         t0 = time.perf_counter()
-        oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, w.n_seg)
+        oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, w.n_seg, policy=args.policy,
+                         seed=args.policy_seed)
         tc = time.perf_counter() - t0
         sample = "full workload" if elems == d else f"first {elems} elements ({len(off) - 1} tensors) of the workload"
         cpu = {"value": round(elems / tc / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
@@ -242,7 +249,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "d": d, "tensors": w.n_tensors,
                    "ratio": None if w.ratio is None else f"{w.ratio[0]}/{w.ratio[1]}", "fpr": w.fpr,
-                   "degree": w.degree, "n_seg": w.n_seg, "input_copies": n_copies},
+                   "degree": w.degree, "n_seg": w.n_seg, "policy": POLICY_NAMES[args.policy],
+                   "input_copies": n_copies},
         "hbm_frac": round(b_alg / (ms * 1e-3) / HBM_PEAK, 4),
         "bytes_alg": int(b_alg),
         "bits_per_elem": round(8.0 * used / d, 4),

@@ -5,8 +5,10 @@
  * Communication Framework for Distributed Deep Learning" (arXiv 2102.03112):
  * a gradient is sparsified (top-r, or the support of an inherently sparse
  * gradient), its index set is compressed with a Bloom filter (Section 4) and
- * decoded with the no-error policy P0 (Section 4, "No-error approach"), and
- * its values are compressed by sorting them and fitting a piecewise
+ * decoded with the no-error policy P0 (Section 4, "No-error approach") or a
+ * policy that codes only r of the positives (P1 of Section 4 and Section
+ * 10.5; the deterministic policies of Section 10.4), and its values are
+ * compressed by sorting them and fitting a piecewise
  * least-squares polynomial (Section 5), with a bit-packed reorder map
  * (Section 5.1).
  *
@@ -68,6 +70,18 @@ typedef enum {
 #define DR_MAX_DEGREE 7      /* highest polynomial degree per segment */
 #define DR_MAX_SEGMENTS 4096 /* most segments per tensor */
 #define DR_MAX_TENSORS 65536 /* most tensors in one round trip */
+
+/* Index policies (Section 4; Sections 10.4 and 10.5): which of the filter's
+ * positives P (ascending) get a value.  P0 codes all of them.  The others
+ * code r = min(n_selected, |P|) of them: P1 a pseudo-random r-subset (see
+ * dr_config.seed), LEFTMOST / MIDDLE / RIGHTMOST the first r, the r starting
+ * at rank floor((|P| - r) / 2), or the last r.  A positive that is not coded
+ * is received as 0. */
+#define DR_POLICY_P0 0u
+#define DR_POLICY_RANDOM 1u
+#define DR_POLICY_LEFTMOST 2u
+#define DR_POLICY_MIDDLE 3u
+#define DR_POLICY_RIGHTMOST 4u
 
 /* Bits of the per-tensor flags word (slot 3 of counts_out). */
 #define DR_FLAG_NONFINITE 1u    /* the tensor held NaN or Inf */
@@ -173,17 +187,24 @@ typedef struct {
     double fpr;                /* Bloom target false-positive rate, in (0, 1)                    */
     uint32_t degree;           /* polynomial degree per run, <= DR_MAX_DEGREE                    */
     uint32_t n_seg;            /* runs per tensor, 1 .. DR_MAX_SEGMENTS                          */
+    uint32_t policy;           /* DR_POLICY_*; the receiver takes it from each record's header   */
+    uint32_t seed;             /* key of DR_POLICY_RANDOM (ignored by the others): positive q of
+                                  P is coded iff pi(q) < r, as value number pi(q), where pi is a
+                                  permutation of [0, |P|): a 4-round Feistel network on 2h-bit
+                                  words (h = max(1, ceil(ceil(log2 |P|) / 2))) whose round j
+                                  XORs MurmurHash3_x86_32(LE half, seed + j) mod 2^h into the
+                                  other half, restricted to [0, |P|) by cycle walking */
 } dr_config;
 
 /* Payload container (Figure 3's "container"): one record per tensor at byte
  * offset rec_off_h[t] (multiples of 256) of the payload buffer.  A record is
  * a 64-byte header followed by the filter words, the fp32 coefficients of
  * the S_eff x (D_eff+1) fitted polynomials, and the packed reorder map, each
- * section padded to 4 bytes and packed back to back.  Header layout
- * (little-endian): u32 magic 0x31435244 ("DRC1"), u32 header bytes (64),
- * u64 d, u64 n_selected, u64 n_values (= |P|), u64 m_bits, u32 k,
- * u32 hash id (1 = MurmurHash3_x86_32), u32 D_eff, u32 S_eff,
- * u32 sigma bits, u32 record bytes (header + sections; what would be sent).
+ * section padded to 4 bytes and packed back to back.  Header layout: 16
+ * little-endian u32 words: magic 0x31435244 ("DRC1"), header bytes (64), d,
+ * n_selected, n_positives (|P|), n_values (values coded: |P| under P0),
+ * m_bits, k, hash id (1 = MurmurHash3_x86_32), policy, seed, D_eff, S_eff,
+ * sigma bits, record bytes (header + sections; what would be sent), 0.
  * Returns the total payload capacity in bytes; fills rec_off_h (nullable,
  * n_tensors+1 entries) with the record offsets and the end.  Returns 0 for
  * an invalid configuration. */
@@ -191,8 +212,9 @@ DR_EXPORT size_t dr_payload_layout(const dr_config *cfg_h, uint64_t *rec_off_h);
 
 /* Sender side over the whole gradient g: per tensor, select (top-r or
  * support), insert into a Bloom filter sized by dr_bloom_params, run the
- * full-range P0 query, take V = g[P] from the dense gradient (Section 4),
- * sort and fit V, and write the record into `payload` (capacity
+ * full-range query (P), let the policy pick the positives to code, take
+ * their values from the dense gradient (V = g[P] under P0, Section 4), sort
+ * and fit V, and write the record into `payload` (capacity
  * payload_bytes, at least dr_payload_layout()).  counts_out (device,
  * nullable) receives 4 u64 per tensor: n_selected, |P|, 0, flags. */
 DR_EXPORT dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
@@ -200,8 +222,9 @@ DR_EXPORT dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, ui
 
 /* Receiver side: from the payload alone, recover P by the full-range query
  * of each tensor's filter, evaluate the fitted values at the ranks the
- * reorder map gives, and write the dense gradient dense_out (d floats, zero
- * off P).  idx_out / val_out (nullable, d entries) receive tensor t's
+ * reorder map gives (through the record's policy: a positive the policy
+ * did not code is 0), and write the dense gradient dense_out (d floats,
+ * zero off P).  idx_out / val_out (nullable, d entries) receive tensor t's
  * positives (local indices) and their values at [offsets_h[t], offsets_h[t]
  * + |P_t|).  counts_out (nullable): slot 2 of each tensor receives the
  * receiver's |P|; slot 3 gains DR_FLAG_DEC_MISMATCH if it disagrees with

@@ -46,6 +46,8 @@ class DrConfig(ctypes.Structure):
         ("fpr", ctypes.c_double),
         ("degree", ctypes.c_uint32),
         ("n_seg", ctypes.c_uint32),
+        ("policy", ctypes.c_uint32),
+        ("seed", ctypes.c_uint32),
     ]
 
 
@@ -175,12 +177,13 @@ def curvefit_decode(coef, sigma, n_dev, n_cap: int, degree: int, n_seg: int, val
 class Config:
     """A dr_config together with the host offsets array it points to."""
 
-    def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int):
+    def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int, policy: int = 0, seed: int = 0):
         self.offsets = np.ascontiguousarray(np.asarray(offsets, dtype=np.uint64))
         self._off_c = (ctypes.c_uint64 * self.offsets.size)(*[int(x) for x in self.offsets])
         num, den = (R_NONZERO, 1) if ratio is None else ratio
-        self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg)
+        self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg, policy, seed)
         self.ratio, self.fpr, self.degree, self.n_seg = ratio, fpr, degree, n_seg
+        self.policy, self.seed = policy, seed
 
     @property
     def n_tensors(self) -> int:
@@ -191,8 +194,8 @@ class Config:
         return int(self.offsets[-1])
 
     @classmethod
-    def from_workload(cls, w):
-        return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg)
+    def from_workload(cls, w, policy: int = 0, seed: int = 0):
+        return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg, policy, seed)
 
 
 def payload_layout(cfg: Config) -> tuple[int, list]:
@@ -245,10 +248,13 @@ def trace_end() -> dict:
 class Record:
     d: int
     n_selected: int
+    n_positives: int
     n_values: int
     m_bits: int
     k: int
     hash_id: int
+    policy: int
+    seed: int
     deg_eff: int
     seg_eff: int
     sigma_b: int
@@ -262,7 +268,8 @@ def parse_record(buf: bytes | np.ndarray, start: int) -> Record:
     """Split one payload record (header layout in include/deepreduce.h)."""
     b = np.asarray(buf, dtype=np.uint8)
     hdr = bytes(b[start:start + HEADER_BYTES])
-    magic, hbytes, d, n_sel, n_v, m_bits, k, hid, de, se, sb, rb = struct.unpack("<IIQQQQIIIIII", hdr)
+    (magic, hbytes, d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb,
+     _reserved) = struct.unpack("<16I", hdr)
     if magic != HEADER_MAGIC or hbytes != HEADER_BYTES:
         raise ValueError(f"bad record header at {start}")
     at = start + HEADER_BYTES
@@ -273,4 +280,4 @@ def parse_record(buf: bytes | np.ndarray, start: int) -> Record:
     at += 4 * ncoef
     nw = (n_v * sb + 31) // 32
     sigma = b[at: at + 4 * nw].view("<u4").copy()
-    return Record(d, n_sel, n_v, m_bits, k, hid, de, se, sb, rb, bits, coef, sigma)
+    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, bits, coef, sigma)

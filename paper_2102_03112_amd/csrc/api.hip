@@ -14,6 +14,9 @@
 #include "launch.hpp"
 
 using namespace dr;
+static_assert(POLICY_P0 == DR_POLICY_P0 && POLICY_RANDOM == DR_POLICY_RANDOM && POLICY_LEFTMOST == DR_POLICY_LEFTMOST &&
+                  POLICY_MIDDLE == DR_POLICY_MIDDLE && POLICY_RIGHTMOST == DR_POLICY_RIGHTMOST,
+              "index policy ids");
 static_assert(MAX_SEG == DR_MAX_SEGMENTS && MAX_DEG == DR_MAX_DEGREE, "limits of the header and the kernels");
 
 namespace {
@@ -302,6 +305,7 @@ dr_status check_cfg(const dr_config *cfg) {
     if (!(cfg->fpr > 0.0 && cfg->fpr < 1.0)) return fail(DR_EINVAL, "fpr must be in (0, 1)");
     if (cfg->degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
     if (cfg->n_seg < 1 || cfg->n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
+    if (cfg->policy > DR_POLICY_RIGHTMOST) return fail(DR_EINVAL, "unknown index policy %u", cfg->policy);
     return DR_OK;
 }
 
@@ -357,6 +361,8 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.k = kk;
         in.degree = cfg->degree;
         in.nseg = cfg->n_seg;
+        in.policy = cfg->policy;
+        in.seed = cfg->seed;
         in.mC = mC;
         // top-r: |S| = r is known, so the filter size is too
         in.m_words_in = nz ? 0u : (uint32_t)(m_cap / 32);

@@ -427,7 +427,7 @@ struct RecordView {
     const uint32_t *bits;
     const float *coef;
     const uint32_t *sigma;
-    uint32_t m_bits, k, nv, deff, seff, b;
+    uint32_t m_bits, k, npos, nv, policy, seed, deff, seff, b;
 };
 
 // Reads a record header and checks it against the record's capacity and
@@ -436,26 +436,31 @@ struct RecordView {
 __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t cap, uint32_t d, bool *ok) {
     RecordView v;
     const uint32_t *h = (const uint32_t *)rec;
-    const uint64_t m_bits = *(const uint64_t *)(rec + 32);
+    const uint64_t m_bits = h[H_MBITS];
     v.m_bits = (uint32_t)m_bits;
-    v.nv = (uint32_t)(*(const uint64_t *)(rec + 24));
-    v.k = h[10];
-    v.deff = h[12];
-    v.seff = h[13];
-    v.b = h[14];
+    v.npos = h[H_NPOS];
+    v.nv = h[H_NVAL];
+    v.policy = h[H_POLICY];
+    v.seed = h[H_SEED];
+    v.k = h[H_K];
+    v.deff = h[H_DEFF];
+    v.seff = h[H_SEFF];
+    v.b = h[H_B];
     v.bits = (const uint32_t *)(rec + HDR_BYTES);
     const uint32_t coef_off = HDR_BYTES + (v.m_bits / 32u) * 4u;
     v.coef = (const float *)(rec + coef_off);
     const uint64_t need = (uint64_t)HDR_BYTES + m_bits / 8u + 4ull * v.seff * (v.deff + 1ull) +
                           4ull * (((uint64_t)v.nv * v.b + 31u) / 32u);
-    const uint64_t nv64 = *(const uint64_t *)(rec + 24);
-    *ok = h[0] == HDR_MAGIC && h[1] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && m_bits < (1ull << 32) &&
-          v.k >= 1 && v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && nv64 <= d &&
+    *ok = h[H_MAGIC] == HDR_MAGIC && h[H_BYTES] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && v.k >= 1 &&
+          v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && v.npos <= d && v.nv <= v.npos &&
+          v.policy <= POLICY_RIGHTMOST && (v.policy != POLICY_P0 || v.nv == v.npos) &&
           (v.nv == 0 || (v.seff >= 1 && v.seff <= v.nv && v.seff <= MAX_SEG && v.b >= sigma_bits(v.nv))) &&
           need <= cap;
     if (!*ok) {  // nothing of an invalid record is read past its first filter word
         v.k = 0;
+        v.npos = 0;
         v.nv = 0;
+        v.policy = POLICY_P0;
         v.m_bits = 32;
         v.seff = 0;
         v.deff = 0;
@@ -704,10 +709,23 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
         }
         RecordView rv;
         uint32_t ncoef = 0;
+        // the policy's view of this tensor: positives, values coded, key
+        uint32_t npos = 0, ncoded = 0, policy = POLICY_P0, pseed = 0;
+        if (MODE == Q_ENCODE) {
+            npos = td.npos;
+            ncoded = td.nv;
+            policy = td.in.policy;
+            pseed = td.in.seed;
+        }
         if (MODE == Q_DECODE) {
             bool ok = true;
             rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, d, &ok);
             ncoef = rv.seff * (rv.deff + 1u);
+            // the receiver's own positives, and the header's values count
+            npos = td.nv_dec;
+            ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
+            policy = rv.policy;
+            pseed = rv.seed;
             if (t != coef_t && ncoef <= EMIT_COEF) {
                 for (uint32_t x = threadIdx.x; x < ncoef; x += NTHREADS) cf[x] = rv.coef[x];
                 coef_t = t;
@@ -741,18 +759,21 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             const uint32_t i = base + slot[p];
             const uint32_t q = q0 + p;
             if (MODE == Q_ENCODE) {
-                const float x = o.g[toff_el + i];
-                const uint64_t at = tslot + q;
-                w.P[at] = i;
-                w.V[at] = x;
-                w.keyA[at] = ~order_key(x);  // ascending order of ~key = descending values
-                w.valA[at] = q;
+                const uint32_t vn = policy_slot(q, npos, ncoded, policy, pseed);
+                if (vn != NO_SLOT) {
+                    const float x = o.g[toff_el + i];
+                    const uint64_t at = tslot + vn;
+                    w.V[at] = x;
+                    w.keyA[at] = ~order_key(x);  // ascending order of ~key = descending values
+                    w.valA[at] = vn;
+                }
             } else if (MODE == Q_PLAIN) {
                 if (q < o.cap) o.idx_out[q] = i;
             } else {
                 float y = 0.0f;
-                if (q < rv.nv) {
-                    const uint32_t rank = sigma_get(rv.sigma, (uint64_t)q * rv.b, rv.b);
+                const uint32_t vn = policy_slot(q, npos, ncoded, policy, pseed);
+                if (vn < rv.nv) {
+                    const uint32_t rank = sigma_get(rv.sigma, (uint64_t)vn * rv.b, rv.b);
                     if (rank < rv.nv) {
                         uint32_t s, lo, ns;
                         run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);

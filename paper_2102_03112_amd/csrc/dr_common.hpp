@@ -38,8 +38,16 @@ constexpr uint32_t SORT_BINS = 256;           // 8-bit LSD radix digits
 constexpr uint32_t FIT_CHUNKS = 8;            // partial-moment blocks per fitted run
 constexpr uint32_t MAX_DEG = 7;
 constexpr uint32_t MAX_SEG = 4096;            // most runs per tensor
+// index policies (Section 4; Sections 10.4, 10.5)
+constexpr uint32_t POLICY_P0 = 0, POLICY_RANDOM = 1, POLICY_LEFTMOST = 2, POLICY_MIDDLE = 3, POLICY_RIGHTMOST = 4;
+constexpr uint32_t NO_SLOT = 0xffffffffu;
 constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
 constexpr uint32_t HDR_BYTES = 64;
+// payload record header: sixteen little-endian u32 words
+enum HdrWord : uint32_t {
+    H_MAGIC = 0, H_BYTES, H_D, H_NSEL, H_NPOS, H_NVAL, H_MBITS, H_K, H_HASH, H_POLICY, H_SEED, H_DEFF, H_SEFF, H_B,
+    H_RECBYTES, H_RESERVED
+};
 constexpr uint32_t HDR_MAGIC = 0x31435244u;   // "DRC1"
 
 // Static per-tensor set-up, written by the host (through kernel arguments).
@@ -83,6 +91,8 @@ struct TInit {
     uint32_t dir_g;      // item chunks
     uint32_t dir_sw;     // words per partial slice: min(DIR_SLICE_WORDS, planned filter words)
     uint32_t dir_per;    // bitmap tiles (from the bitmap) or items (from a list) per chunk
+    uint32_t policy;     // index policy (POLICY_*)
+    uint32_t seed;       // key of the random policy
 };
 
 // Per-tensor descriptor, in device memory.
@@ -91,8 +101,9 @@ struct TDesc {
     // --- produced on the device ---
     uint32_t n;          // |S|
     uint32_t m_words;    // filter words
-    uint32_t nv;         // |P| on the sender
+    uint32_t nv;         // values coded on the sender: |P| for P0, else min(|S|, |P|)
     uint32_t nv_dec;     // |P| on the receiver
+    uint32_t npos;       // |P| on the sender
     uint32_t seff, deff; // runs and degree actually used
     uint32_t b;          // reorder-map bits per entry
     uint32_t flags;      // DR_FLAG_* bits (+ internal error bits)
@@ -314,6 +325,52 @@ __device__ __forceinline__ float horner(const float *c, uint32_t deg, double t) 
     double y = (double)c[deg];
     for (int p = (int)deg - 1; p >= 0; --p) y = y * t + (double)c[p];
     return (float)y;
+}
+
+// ---------------------------------------------------------------------------
+// Index policies: which positives are coded, and as which value.
+// ---------------------------------------------------------------------------
+// P1 keeps positive q iff pi(q) < ncoded, as value pi(q): pi is a keyed
+// pseudo-random permutation of [0, npos), a 4-round Feistel network on 2h-bit
+// words (h = ceil(ceil(log2 npos) / 2), at least 1; round j is MurmurHash3 of
+// the 4-byte half with seed (seed + j), cut to h bits) restricted to
+// [0, npos) by cycle walking (Black and Rogaway, CT-RSA 2002).  The walk
+// ends: pi's cycle through q returns to q, which is in the domain.
+__device__ __forceinline__ uint32_t feistel_perm(uint32_t q, uint32_t npos, uint32_t seed) {
+    uint32_t bits = 0;
+    while (bits < 32 && (1ull << bits) < npos) ++bits;
+    const uint32_t h = max(1u, (bits + 1) / 2);
+    const uint32_t mask = h >= 32 ? 0xffffffffu : ((1u << h) - 1u);
+    uint32_t y = q;
+    do {
+        uint32_t L = (y >> h) & mask, R = y & mask;
+#pragma unroll
+        for (uint32_t j = 0; j < 4; ++j) {
+            const uint32_t t = L ^ (mm3_seed(mm3_key(R), seed + j) & mask);
+            L = R;
+            R = t;
+        }
+        y = (L << h) | R;
+    } while (y >= npos);
+    return y;
+}
+
+// value number of positive rank q under `policy`, or NO_SLOT if dropped
+__device__ __forceinline__ uint32_t policy_slot(uint32_t q, uint32_t npos, uint32_t ncoded, uint32_t policy,
+                                                uint32_t seed) {
+    switch (policy) {
+        case POLICY_P0: return q;
+        case POLICY_RANDOM: {
+            const uint32_t p = feistel_perm(q, npos, seed);
+            return p < ncoded ? p : NO_SLOT;
+        }
+        case POLICY_LEFTMOST: return q < ncoded ? q : NO_SLOT;
+        case POLICY_MIDDLE: {
+            const uint32_t s0 = (npos - ncoded) / 2;
+            return (q >= s0 && q - s0 < ncoded) ? q - s0 : NO_SLOT;
+        }
+        default: return q >= npos - ncoded ? q - (npos - ncoded) : NO_SLOT;
+    }
 }
 
 // Raw buffer view of `bytes` bytes at p (both the same on every lane of the

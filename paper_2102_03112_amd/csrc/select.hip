@@ -648,15 +648,17 @@ __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, 
             if (td.in.r != R_NONZERO && carry != td.in.r) atomicOr(&td.flags, FLAG_COUNT);
             td.m_words = filter_words(td);
         } else if (which == 1) {
-            td.nv = carry;
+            // the policy codes every positive (P0) or r of them
+            td.npos = carry;
+            td.nv = td.in.policy == POLICY_P0 ? carry : min(td.n, carry);
         } else if (which == 2) {
             td.nv_dec = carry;
             if (counts_out) {
                 counts_out[4 * blockIdx.x + 2] = carry;
                 const uint8_t *rec = payload + td.in.rec_off;
-                const uint64_t hdr_nv = *(const uint64_t *)(rec + 24);
+                const uint32_t hdr_npos = ((const uint32_t *)rec)[H_NPOS];
                 uint32_t f = td.flags;
-                if (carry != hdr_nv) f |= FLAG_DEC_MISMATCH;
+                if (carry != hdr_npos) f |= FLAG_DEC_MISMATCH;
                 counts_out[4 * blockIdx.x + 3] |= f & FLAG_DEC_MISMATCH;
             }
         } else if (n_out) {

@@ -37,6 +37,7 @@ __global__ __launch_bounds__(NTHREADS) void k_keygen(Work w, const float *__rest
     const uint32_t nv = (uint32_t)(n64 < n_cap ? n64 : n_cap);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         w.td[0].nv = nv;
+        w.td[0].npos = nv;
         if (n64 > n_cap) atomicOr(&w.td[0].flags, FLAG_CAPACITY);
     }
     for (uint32_t q = blockIdx.x * NTHREADS + threadIdx.x; q < nv; q += gridDim.x * NTHREADS) {
@@ -83,7 +84,7 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
             td.swords = nwd;
             if (counts_out) {
                 counts_out[4 * t + 0] = td.n;
-                counts_out[4 * t + 1] = nv;
+                counts_out[4 * t + 1] = td.npos;
                 counts_out[4 * t + 2] = 0;
                 counts_out[4 * t + 3] = td.flags;
             }
@@ -96,18 +97,22 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
                 td.rec_bytes = rec_bytes;
                 uint8_t *rec = td.in.rec;
                 uint32_t *h = (uint32_t *)rec;
-                h[0] = HDR_MAGIC;
-                h[1] = HDR_BYTES;
-                *(uint64_t *)(rec + 8) = td.in.d;
-                *(uint64_t *)(rec + 16) = td.n;
-                *(uint64_t *)(rec + 24) = nv;
-                *(uint64_t *)(rec + 32) = (uint64_t)td.m_words * 32u;
-                h[10] = td.in.k;
-                h[11] = 1u;  // MurmurHash3_x86_32, seeds 0..k-1
-                h[12] = deff;
-                h[13] = seff;
-                h[14] = b;
-                h[15] = rec_bytes;
+                h[H_MAGIC] = HDR_MAGIC;
+                h[H_BYTES] = HDR_BYTES;
+                h[H_D] = td.in.d;
+                h[H_NSEL] = td.n;
+                h[H_NPOS] = td.npos;
+                h[H_NVAL] = nv;
+                h[H_MBITS] = td.m_words * 32u;
+                h[H_K] = td.in.k;
+                h[H_HASH] = 1u;  // MurmurHash3_x86_32, seeds 0..k-1
+                h[H_POLICY] = td.in.policy;
+                h[H_SEED] = td.in.seed;
+                h[H_DEFF] = deff;
+                h[H_SEFF] = seff;
+                h[H_B] = b;
+                h[H_RECBYTES] = rec_bytes;
+                h[H_RESERVED] = 0u;
             }
         }
         uint32_t tot_t, tot_w, tot_v;

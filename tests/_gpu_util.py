@@ -66,8 +66,9 @@ def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     1e-4 of the oracle's double-precision solution."""
     assert rec.d == ref.d
     assert rec.n_selected == ref.S.size
-    assert rec.n_values == ref.P.size
+    assert (rec.n_positives, rec.n_values) == (ref.P.size, ref.fit.n)
     assert (rec.m_bits, rec.k, rec.hash_id) == (ref.m, ref.k, 1)
+    assert (rec.policy, rec.seed) == (ref.policy, ref.seed)
     assert (rec.seg_eff, rec.deg_eff, rec.sigma_b) == (ref.fit.S_eff, ref.fit.D_eff, ref.fit.b)
     np.testing.assert_array_equal(rec.bits, ref.bits)
     np.testing.assert_array_equal(rec.sigma, ref.fit.sigma)
@@ -129,14 +130,25 @@ def check_roundtrip(g, cfg: B.Config, out, refs):
         n_sel, nv, nv_dec, flags = [int(x) for x in out["counts"][t]]
         assert (n_sel, nv, nv_dec, flags) == (ref.S.size, ref.P.size, ref.P.size, 0)
         np.testing.assert_array_equal(out["idx"][a: a + nv], ref.P_dec)
-        # receiver values vs the oracle's decode of this very payload
-        y_same = oracle.curvefit_decode(rec.coef if rec.seg_eff else np.zeros(0, np.float32),
-                                        rec.sigma, nv, rec.deg_eff, max(rec.seg_eff, 1)) if nv else np.zeros(0)
-        if nv:
-            ranks = oracle.sigma_unpack(rec.sigma, nv)
-            values_close(out["val"][a: a + nv], y_same, ranks, nv, rec.seg_eff)
+        # the policy's choice: positives it did not code are received as 0
+        vals = out["val"][a: a + nv]
+        kept = ref.slots != oracle.NO_SLOT
+        assert np.all(vals[~kept] == 0)
+        nc = ref.fit.n
+        assert int(kept.sum()) == nc
+        if nc:
+            vn = ref.slots[kept].astype(np.int64)
+            y_gpu = np.zeros(nc, np.float32)
+            y_gpu[vn] = vals[kept]
+            y_ref = np.zeros(nc, np.float32)
+            y_ref[vn] = ref.vals[kept]
+            # receiver values vs the oracle's decode of this very payload
+            y_same = oracle.curvefit_decode(rec.coef if rec.seg_eff else np.zeros(0, np.float32),
+                                            rec.sigma, nc, rec.deg_eff, max(rec.seg_eff, 1))
+            ranks = oracle.sigma_unpack(rec.sigma, nc)
+            values_close(y_gpu, y_same, ranks, nc, rec.seg_eff)
             # and vs the oracle's own end-to-end reconstruction
-            values_close(out["val"][a: a + nv], ref.vals, ranks, nv, rec.seg_eff)
+            values_close(y_gpu, y_ref, ranks, nc, rec.seg_eff)
         dense = out["dense"][a:b]
         pos = ref.P_dec.astype(np.int64)
         np.testing.assert_array_equal(dense[pos], out["val"][a: a + nv])

@@ -90,14 +90,14 @@ def test_workspace_bound_grows_with_size(L):
 FAKE = ctypes.c_void_p(1 << 20)
 
 
-def _cfg(offsets=(0, 1000), ratio=(1, 100), fpr=1e-3, degree=5, n_seg=8):
-    return B.Config(list(offsets), ratio, fpr, degree, n_seg)
+def _cfg(offsets=(0, 1000), ratio=(1, 100), fpr=1e-3, degree=5, n_seg=8, policy=0):
+    return B.Config(list(offsets), ratio, fpr, degree, n_seg, policy)
 
 
 @pytest.mark.parametrize("bad", [
     dict(fpr=0.0), dict(fpr=1.0), dict(degree=8), dict(n_seg=0), dict(n_seg=5000),
     dict(ratio=(2, 1)), dict(ratio=(1, 0)), dict(offsets=(0, 10, 5)), dict(offsets=(1, 10)),
-    dict(offsets=(0, 1 << 32)),
+    dict(offsets=(0, 1 << 32)), dict(policy=5),
 ])
 def test_config_rejected(L, bad):
     cfg = _cfg(**bad)
@@ -159,21 +159,16 @@ def test_trace_end_without_begin_is_rejected(L):
 
 def test_parse_record_roundtrips_a_synthetic_header():
     # header layout of include/deepreduce.h, built independently with numpy
-    d, n_sel, n_v, m, k, de, se, b = 1000, 10, 12, 64, 3, 1, 2, 4
+    d, n_sel, n_pos, n_v, m, k, pol, seed, de, se, b = 1000, 10, 14, 12, 64, 3, 1, 99, 1, 2, 4
     words = (n_v * b + 31) // 32
     rb = 64 + m // 8 + 4 * se * (de + 1) + 4 * words
-    hdr = np.zeros(16, dtype="<u4")
-    hdr[0], hdr[1] = 0x31435244, 64
-    hdr[2:4] = [d, 0]
-    hdr[4:6] = [n_sel, 0]
-    hdr[6:8] = [n_v, 0]
-    hdr[8:10] = [m, 0]
-    hdr[10:16] = [k, 1, de, se, b, rb]
+    hdr = np.array([0x31435244, 64, d, n_sel, n_pos, n_v, m, k, 1, pol, seed, de, se, b, rb, 0], dtype="<u4")
     body = np.concatenate([np.arange(m // 32, dtype="<u4"), np.arange(se * (de + 1), dtype="<f4").view("<u4"),
                            np.full(words, 7, dtype="<u4")])
     buf = np.concatenate([hdr, body]).view(np.uint8)
     rec = B.parse_record(buf, 0)
-    assert (rec.d, rec.n_selected, rec.n_values, rec.m_bits, rec.k, rec.deg_eff, rec.seg_eff, rec.sigma_b,
-            rec.rec_bytes) == (d, n_sel, n_v, m, k, de, se, b, rb)
+    assert (rec.d, rec.n_selected, rec.n_positives, rec.n_values, rec.m_bits, rec.k, rec.hash_id, rec.policy,
+            rec.seed, rec.deg_eff, rec.seg_eff, rec.sigma_b, rec.rec_bytes) == (d, n_sel, n_pos, n_v, m, k, 1, pol,
+                                                                                 seed, de, se, b, rb)
     np.testing.assert_array_equal(rec.bits, [0, 1])
     np.testing.assert_array_equal(rec.sigma, [7, 7])

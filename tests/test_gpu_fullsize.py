@@ -21,15 +21,15 @@ from _gpu_util import check_roundtrip, log, release_workspace, run_roundtrip
 pytestmark = pytest.mark.gpu
 
 
-def _full(name):
+def _full(name, policy=oracle.POLICY_P0, seed=0):
     w = W.WORKLOADS[name]
-    log(f"full-size {name}: generating d={w.d}")
+    log(f"full-size {name} policy={policy}: generating d={w.d}")
     g = W.generate(w)
-    cfg = B.Config.from_workload(w)
+    cfg = B.Config.from_workload(w, policy, seed)
     log(f"full-size {name}: GPU round trip")
     out = run_roundtrip(g, cfg)
     log(f"full-size {name}: oracle")
-    refs = oracle.roundtrip(g, w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg)
+    refs = oracle.roundtrip(g, w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg, policy=policy, seed=seed)
     log(f"full-size {name}: compare")
     check_roundtrip(g, cfg, out, refs)
     release_workspace()
@@ -37,6 +37,10 @@ def _full(name):
 
 def test_resnet50_25m_full():
     _full("resnet50_25m")
+
+
+def test_resnet50_25m_random_policy_full():
+    _full("resnet50_25m", oracle.POLICY_RANDOM, 20210205)
 
 
 def test_ncf_32m_support_full():
@@ -53,7 +57,7 @@ def _properties(g, w, t, rec, counts, idx, val, dense):
     r = oracle.ratio_count(d, *w.ratio)
     n_sel, nv, nv_dec, flags = [int(x) for x in counts]
     assert (n_sel, flags) == (r, 0)
-    assert nv == nv_dec == rec.n_values and rec.n_selected == r
+    assert nv == nv_dec == rec.n_positives == rec.n_values and rec.n_selected == r
     m, k = oracle.bloom_params(r, w.fpr)
     assert (rec.m_bits, rec.k, rec.hash_id, rec.d) == (m, k, 1, d)
     assert rec.sigma_b == oracle.sigma_bits(nv)

@@ -230,6 +230,61 @@ def test_roundtrip_parity(name):
     check_roundtrip(g, cfg, out, refs)
 
 
+POLICIES = [oracle.POLICY_RANDOM, oracle.POLICY_LEFTMOST, oracle.POLICY_MIDDLE, oracle.POLICY_RIGHTMOST]
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+@pytest.mark.parametrize("name", ["resnet20_fpr_1e-2", "support_50k", "ragged_tensors"])
+def test_roundtrip_policy_parity(name, policy):
+    """Policies that code r of the positives (Section 4; Sections 10.4,
+    10.5): the same choice, value numbers and reconstruction as the oracle.
+    A false-positive rate of 1e-2 leaves many positives undecoded."""
+    if name == "resnet20_fpr_1e-2":
+        g, off, ratio, fpr, D, S = W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-2, 5, 8
+    else:
+        g, off, ratio, fpr, D, S = RT_CASES[name]
+    seed = 0x5EED0000 + policy
+    log(f"roundtrip {name} policy={policy} seed={seed:#x}")
+    cfg = B.Config(off, ratio, fpr, D, S, policy, seed)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=seed)
+    assert any(ref.P.size > ref.S.size for ref in refs)
+    check_roundtrip(g, cfg, out, refs)
+
+
+def test_receiver_takes_the_policy_from_the_record():
+    """The receiver reads policy and key from each record's header, not from
+    its own configuration."""
+    import torch
+
+    g, off = W.normal(36_864, 6), [0, 36_864]
+    enc = B.Config(off, (1, 100), 1e-2, 5, 8, oracle.POLICY_RANDOM, 1234)
+    rt = run_roundtrip(g, enc)
+    dec = B.Config(off, (1, 100), 1e-2, 5, 8, oracle.POLICY_P0, 0)
+    dense = torch.full((g.size,), 3.0, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    B.payload_decode(dev_tensor(rt["payload"]), dec, dense, None, None, counts, workspace(g.size))
+    sync()
+    np.testing.assert_array_equal(host(dense), rt["dense"])
+    assert int(host(counts)[3]) == 0
+
+
+def test_receiver_rejects_an_unknown_policy_in_the_record():
+    import torch
+
+    g, off = W.normal(36_864, 6), [0, 36_864]
+    cfg = B.Config(off, (1, 100), 1e-2, 5, 8, oracle.POLICY_LEFTMOST, 0)
+    rt = run_roundtrip(g, cfg)
+    bad = rt["payload"].copy()
+    bad[36:40] = np.array([5], dtype="<u4").view(np.uint8)  # policy word
+    dense = torch.full((g.size,), 3.0, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    B.payload_decode(dev_tensor(bad), cfg, dense, None, None, counts, workspace(g.size))
+    sync()
+    assert int(host(counts)[3]) & B.FLAG_DEC_MISMATCH
+    assert np.all(host(dense) == 0)
+
+
 def test_roundtrip_normal_1m_full_size():
     w = W.WORKLOADS["normal_1m"]
     log("roundtrip normal_1m")
