@@ -374,3 +374,22 @@ def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int
         r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
         out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed))
     return out
+
+
+def decode_sum(results_per_payload, d: int, offsets, scale: float) -> np.ndarray:
+    """The receiver of a data-parallel step (Section 2, "Compressed
+    distributed training via SGD": the aggregated gradient is the mean of the
+    workers' compressed gradients; Section 6.4 gathers the payloads, so every
+    worker decodes each of them).  ``results_per_payload[p]`` is the list of
+    per-tensor results of ``roundtrip`` for worker p.  Element i of the output
+    is scale * (g_0[i] + g_1[i] + ...), the terms added one at a time in fp32
+    in payload order starting from +0, then multiplied by scale in fp32.
+    Parity pinned by brute force over dictionaries of (index, value) pairs and
+    by the one-payload and repeated-payload special cases."""
+    acc = np.zeros(d, dtype=np.float32)
+    for res in results_per_payload:
+        dense = np.zeros(d, dtype=np.float32)
+        for t, r in enumerate(res):
+            dense[offsets[t]: offsets[t + 1]] = r.dense
+        acc = (acc + dense).astype(np.float32)
+    return (np.float32(scale) * acc).astype(np.float32)
