@@ -99,6 +99,68 @@ def copy_calibration(n_bytes=1 << 30, reps=5):
 POLICY_NAMES = {0: "P0", 1: "P1", 2: "leftmost", 3: "middle", 4: "rightmost"}
 
 
+def decode_sum_bench(w, n, steps, warmup, policy, seed):
+    """Receiver of an n-worker step: n payloads of the workload (from n
+    differently seeded gradients) decoded into one averaged dense gradient by
+    dr_payload_decode_sum, against n dr_payload_decode calls whose outputs
+    are added by torch on the same stream.  Prints its own JSON line."""
+    import dataclasses
+
+    import numpy as np
+    import torch
+
+    from paper_2102_03112_amd import binding as B
+    from paper_2102_03112_amd import workloads as W
+
+    cfg = B.Config.from_workload(w, policy, seed)
+    total, _ = B.payload_layout(cfg)
+    ws = B.workspace(w.d, w.n_tensors)
+    stream = torch.cuda.current_stream()
+    pays = []
+    for p in range(n):
+        g = torch.from_numpy(W.generate(dataclasses.replace(w, seed=w.seed + 1000 * p))).cuda()
+        pay = torch.zeros(total, dtype=torch.uint8, device="cuda")
+        B.payload_encode(g, cfg, pay, None, ws, stream)
+        pays.append(pay)
+        del g
+    torch.cuda.synchronize()
+    dense = torch.empty(w.d, dtype=torch.float32, device="cuda")
+    one = torch.empty(w.d, dtype=torch.float32, device="cuda")
+
+    def fused():
+        B.payload_decode_sum(pays, cfg, 1.0 / n, dense, None, ws, stream)
+
+    def separate():
+        dense.zero_()
+        for pay in pays:
+            B.payload_decode(pay, cfg, one, None, None, None, ws, stream)
+            dense.add_(one)
+        dense.mul_(1.0 / n)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    ms_f, ms_s = timed(fused), timed(separate)
+    log(f"decode_sum: {n} payloads fused {ms_f:.4f} ms, separate {ms_s:.4f} ms")
+    print(json.dumps({
+        "metric": "receiver Gelem/s of decoded payload elements (n payloads x d)", "value": round(n * w.d / ms_f / 1e6, 4),
+        "unit": "Gelem/s", "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": round(ms_f, 5),
+        "separate_ms_per_step": round(ms_s, 5), "speedup_vs_separate": round(ms_s / ms_f, 3),
+        "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "d": w.d, "tensors": w.n_tensors, "payloads": n,
+                   "policy": POLICY_NAMES[policy]},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +170,8 @@ def main():
     ap.add_argument("--policy", type=int, default=0, help="index policy: 0 = P0 (no error), 1 = P1 (random r of P), "
                                                       "2/3/4 = leftmost/middle/rightmost r of P")
     ap.add_argument("--policy-seed", type=int, default=20210205, help="key of policy 1")
+    ap.add_argument("--decode-sum", type=int, default=0, metavar="N",
+                    help="instead: time the summing receiver over N payloads of the workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=30.0, help="bound on the oracle's CPU time")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -132,6 +196,9 @@ def main():
         return
     B.lib()  # fail loudly if the HIP library is missing
     w = W.WORKLOADS[args.workload]
+    if args.decode_sum:
+        decode_sum_bench(w, args.decode_sum, args.steps, args.warmup, args.policy, args.policy_seed)
+        return
     d = w.d
     log(f"bench: workload {w.name} d={d} tensors={w.n_tensors}")
     t0 = time.time()

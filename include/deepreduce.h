@@ -70,6 +70,7 @@ typedef enum {
 #define DR_MAX_DEGREE 7      /* highest polynomial degree per segment */
 #define DR_MAX_SEGMENTS 4096 /* most segments per tensor */
 #define DR_MAX_TENSORS 65536 /* most tensors in one round trip */
+#define DR_MAX_SUM_PAYLOADS 64 /* most payloads summed by one dr_payload_decode_sum */
 
 /* Index policies (Section 4; Sections 10.4 and 10.5): which of the filter's
  * positives P (ascending) get a value.  P0 codes all of them.  The others
@@ -231,6 +232,27 @@ DR_EXPORT dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, ui
  * the header or the record is invalid (an invalid record decodes as empty). */
 DR_EXPORT dr_status dr_payload_decode(const uint8_t *payload, const dr_config *cfg_h, float *dense_out, uint32_t *idx_out,
                             float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream);
+
+/* Receiver side of a data-parallel step (Section 2, "Compressed distributed
+ * training via SGD": the workers' compressed gradients are averaged; Section
+ * 6.4 exchanges DeepReduce payloads by all-gather, so each worker decodes
+ * all of them).  payloads_h (host array of n_payloads device pointers, 1 ..
+ * DR_MAX_SUM_PAYLOADS) holds payloads written by dr_payload_encode with the
+ * tensor layout of cfg_h (their records at dr_payload_layout's offsets).
+ * dense_out (d floats) receives scale * (g_0 + g_1 + ... + g_{n-1}), where
+ * g_p is the dense gradient dr_payload_decode rebuilds from payload p: the
+ * terms of each element are added in fp32 in payload order, starting from
+ * +0, and the sum is then multiplied by scale in fp32 (scale = 1/n gives the
+ * average).  One pass over the dense gradient writes it once.  counts_out
+ * (device, nullable) receives 4 u64 per payload and tensor, payload-major:
+ * 0, 0, the receiver's |P|, flags (DR_FLAG_DEC_MISMATCH as for
+ * dr_payload_decode).  The workspace needs dr_workspace_bytes(d,
+ * n_tensors) bytes.  EINVAL: n_payloads out of range, a null payload
+ * pointer, dense_out null with d > 0, scale not finite, an invalid cfg_h,
+ * workspace too small. */
+DR_EXPORT dr_status dr_payload_decode_sum(const uint8_t *const *payloads_h, uint32_t n_payloads, const dr_config *cfg_h,
+                                          float scale, float *dense_out, uint64_t *counts_out, void *ws,
+                                          size_t ws_bytes, void *stream);
 
 /* dr_payload_encode followed by dr_payload_decode on one stream: one codec
  * round trip of the whole gradient. */

@@ -27,7 +27,8 @@ HEADER_MAGIC = 0x31435244
 EXPORTS = [
     "dr_bloom_params", "dr_sigma_bits", "dr_workspace_bytes", "dr_last_error", "dr_sparsify_topr",
     "dr_bloom_encode", "dr_bloom_decode", "dr_curvefit_encode", "dr_curvefit_decode", "dr_payload_layout",
-    "dr_payload_encode", "dr_payload_decode", "dr_roundtrip", "dr_trace_begin", "dr_trace_end",
+    "dr_payload_encode", "dr_payload_decode", "dr_payload_decode_sum", "dr_roundtrip", "dr_trace_begin",
+    "dr_trace_end",
 ]
 
 
@@ -81,6 +82,7 @@ def lib():
         "dr_payload_layout": (sz, [cfgp, ctypes.POINTER(u64)]),
         "dr_payload_encode": (st, [vp, cfgp, vp, sz, vp, vp, sz, vp]),
         "dr_payload_decode": (st, [vp, cfgp, vp, vp, vp, vp, vp, sz, vp]),
+        "dr_payload_decode_sum": (st, [ctypes.POINTER(vp), u32, cfgp, ctypes.c_float, vp, vp, vp, sz, vp]),
         "dr_roundtrip": (st, [vp, cfgp, vp, sz, vp, vp, vp, vp, vp, sz, vp]),
         "dr_trace_begin": (st, [vp]),
         "dr_trace_end": (st, [ctypes.c_char_p, sz]),
@@ -216,6 +218,14 @@ def payload_decode(payload, cfg: Config, dense_out, idx_out, val_out, counts_out
     _check("dr_payload_decode", lib().dr_payload_decode(
         _ptr(payload), ctypes.byref(cfg.c), _ptr(dense_out), _ptr(idx_out), _ptr(val_out), _ptr(counts_out),
         _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def payload_decode_sum(payloads, cfg: Config, scale: float, dense_out, counts_out, ws, stream=None):
+    """dense_out = scale * (sum of the dense gradients the payloads decode to)."""
+    arr = (ctypes.c_void_p * max(1, len(payloads)))(*[_ptr(p) for p in payloads])
+    _check("dr_payload_decode_sum", lib().dr_payload_decode_sum(
+        arr, len(payloads), ctypes.byref(cfg.c), scale, _ptr(dense_out), _ptr(counts_out), _ptr(ws), ws.numel(),
+        _stream(stream)))
 
 
 def roundtrip(g, cfg: Config, payload, dense_out, idx_out, val_out, counts_out, ws, stream=None):

@@ -3,6 +3,8 @@
 // entry point.  Everything here runs on the host; all arithmetic of the
 // codec runs in the kernels.
 #include <math.h>
+
+#include <cmath>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -79,6 +81,7 @@ int persist_grid(int per_cu) { return dr::device_cus() * per_cu; }
 // can borrow them for its position buffer before the value path needs them.
 struct Carve {
     uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0;
+    bool query_only = false;  // descriptors, tile counts, the positives bitmap and the tile table only
     size_t bytes = 0;
     size_t o_td, o_glob, o_done, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
         o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
@@ -90,33 +93,34 @@ struct Carve {
             at = align_up(at + sz, 256);
             return r;
         };
+        const uint64_t all = query_only ? 0 : 1;  // regions the query alone does not use
         o_td = take(sizeof(TDesc) * ntensors);
         o_glob = take(sizeof(Glob));
         o_done = take(4 * ntensors);
         o_tcnt = take(4 * ntiles);
         o_toff = take(4 * ntiles);
-        o_ccnt = take(4 * ntiles);
-        o_hist = take(4ull * HIST1_BINS * ntensors);
-        o_histA = take(4ull * 1024 * ntensors);
-        o_sel = take(slots / 8);
         o_pbits = take(slots / 8);
-        o_ckey = take(4 * slots);
-        o_cidx = take(4 * slots);
-        o_S = take(4 * slots);
-        o_P = take(4 * slots);
-        o_V = take(4 * slots);
-        o_sstat = take(8ull * 4 * SORT_BINS * ntiles);
-        o_sdig = take(4ull * 4 * SORT_BINS * ntensors);
         o_ttab = take(4ull * ntiles);
-        o_fit = take(8ull * NMOM * fit_blocks);
-        o_btab = take(4 * btab);
-        o_brow = take(8 * bslices);
-        o_keyA = take(4 * slots);
-        o_keyB = take(4 * slots);
-        o_valA = take(4 * slots);
-        o_valB = take(4 * slots);
-        o_sig = take(4 * slots);
-        o_vs = take(4 * slots);
+        o_ccnt = take(all * 4 * ntiles);
+        o_hist = take(all * 4ull * HIST1_BINS * ntensors);
+        o_histA = take(all * 4ull * 1024 * ntensors);
+        o_sel = take(all * slots / 8);
+        o_ckey = take(all * 4 * slots);
+        o_cidx = take(all * 4 * slots);
+        o_S = take(all * 4 * slots);
+        o_P = take(all * 4 * slots);
+        o_V = take(all * 4 * slots);
+        o_sstat = take(all * 8ull * 4 * SORT_BINS * ntiles);
+        o_sdig = take(all * 4ull * 4 * SORT_BINS * ntensors);
+        o_fit = take(all * 8ull * NMOM * fit_blocks);
+        o_btab = take(all * 4 * btab);
+        o_brow = take(all * 8 * bslices);
+        o_keyA = take(all * 4 * slots);
+        o_keyB = take(all * 4 * slots);
+        o_valA = take(all * 4 * slots);
+        o_valB = take(all * 4 * slots);
+        o_sig = take(all * 4 * slots);
+        o_vs = take(all * 4 * slots);
         bytes = at;
     }
 
@@ -393,15 +397,21 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
 }
 
 // descriptors (chunks of INIT_CHUNK tensors) and the per-call state cleared
-hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s) {
+// Descriptors and the zeroed regions; a query-only work has no histogram or
+// sort regions, and `extra` (words) is a caller's buffer to clear as well.
+hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s, bool query_only = false,
+                    ZeroRange extra = {nullptr, 0}) {
     ZeroArgs z;
     memset(&z, 0, sizeof z);
     z.z[0] = {w.done, w.ntensors};
     z.z[1] = {w.glob, sizeof(Glob) / 4};
-    z.z[2] = {w.sdig, 4ull * SORT_BINS * w.ntensors};
-    z.z[3] = {w.hist, (uint64_t)HIST1_BINS * w.ntensors};
-    z.z[4] = {w.histA, 1024ull * w.ntensors};
-    z.n = 5;
+    z.n = 2;
+    if (!query_only) {
+        z.z[z.n++] = {w.sdig, 4ull * SORT_BINS * w.ntensors};
+        z.z[z.n++] = {w.hist, (uint64_t)HIST1_BINS * w.ntensors};
+        z.z[z.n++] = {w.histA, 1024ull * w.ntensors};
+    }
+    if (extra.p && extra.words) z.z[z.n++] = extra;
     for (size_t f = 0; f < t.size(); f += INIT_CHUNK) {
         InitArgs a;
         memset(&a, 0, sizeof a);
@@ -476,7 +486,51 @@ dr_status decode_impl(const uint8_t *payload, const dr_config *cfg, float *dense
     const Work w = p.carve.view((uint8_t *)ws);
     trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(launch_query_decode(w, payload, dense_out, idx_out, val_out, counts_out, persist_grid(4), s));
+    DR_HIP(launch_query_decode(w, dense_out, idx_out, val_out, counts_out, s));
+    return DR_OK;
+}
+
+dr_status decode_sum_impl(const uint8_t *const *payloads, uint32_t npay, const dr_config *cfg, float scale,
+                          float *dense_out, uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+    Plan p;
+    std::vector<uint64_t> rec_off;
+    dr_status st = plan_config(cfg, p, rec_off);
+    if (st != DR_OK) return st;
+    if (npay < 1 || npay > DR_MAX_SUM_PAYLOADS) return fail(DR_EINVAL, "n_payloads must be in [1, %d]", DR_MAX_SUM_PAYLOADS);
+    if (!payloads) return fail(DR_EINVAL, "payloads_h is null");
+    for (uint32_t q = 0; q < npay; ++q)
+        if (!payloads[q]) return fail(DR_EINVAL, "payloads_h[%u] is null", q);
+    const uint64_t T = cfg->n_tensors, d = cfg->offsets_h[T];
+    if (!dense_out && d > 0) return fail(DR_EINVAL, "dense_out is null");
+    if (!std::isfinite(scale)) return fail(DR_EINVAL, "scale is not finite");
+    const uint64_t ntiles1 = p.carve.ntiles;
+    if (ntiles1 * npay >= (1ull << 32) || T * npay > (1ull << 32)) return fail(DR_ENOTSUP, "too many tiles");
+    // tensor t of payload q is descriptor q * T + t, its tiles follow payload q - 1's
+    std::vector<TInit> vt;
+    vt.reserve(T * npay);
+    for (uint32_t q = 0; q < npay; ++q)
+        for (uint64_t t = 0; t < T; ++t) {
+            TInit in = p.t[t];
+            in.tile0 = (uint32_t)(q * ntiles1 + in.tile0);
+            in.slot = q * ntiles1 * TILE + in.slot;
+            in.rec_off = rec_off[t];
+            in.rec_cap = rec_off[t + 1] - rec_off[t];
+            in.rec = const_cast<uint8_t *>(payloads[q]) + rec_off[t];
+            in.bits = nullptr;
+            vt.push_back(in);
+        }
+    Carve c;
+    c.query_only = true;
+    c.ntensors = T * npay;
+    c.ntiles = ntiles1 * npay;
+    c.slots = c.ntiles * TILE;
+    c.plan();
+    if (!ws_ok(ws, ws_bytes, c.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", c.bytes);
+    const Work w = c.view((uint8_t *)ws);
+    trace_call(s);
+    DR_HIP(run_init(w, vt, s, true, {counts_out, counts_out ? 8 * T * npay : 0}));
+    DR_HIP(launch_query_decode_sum(w, npay, (uint32_t)T, (uint32_t)ntiles1, scale, dense_out, counts_out, s));
     return DR_OK;
 }
 
@@ -635,6 +689,13 @@ dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, uint8_t *pay
 dr_status dr_payload_decode(const uint8_t *payload, const dr_config *cfg_h, float *dense_out, uint32_t *idx_out,
                             float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, void *stream) {
     return decode_impl(payload, cfg_h, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, (hipStream_t)stream);
+}
+
+dr_status dr_payload_decode_sum(const uint8_t *const *payloads_h, uint32_t n_payloads, const dr_config *cfg_h,
+                                float scale, float *dense_out, uint64_t *counts_out, void *ws, size_t ws_bytes,
+                                void *stream) {
+    return decode_sum_impl(payloads_h, n_payloads, cfg_h, scale, dense_out, counts_out, ws, ws_bytes,
+                           (hipStream_t)stream);
 }
 
 dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,

@@ -410,17 +410,22 @@ hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_c
 // ---------------------------------------------------------------------------
 // Full-range query
 // ---------------------------------------------------------------------------
-enum QueryMode { Q_ENCODE = 0, Q_PLAIN = 1, Q_DECODE = 2 };
+// Q_SUM probes like Q_DECODE but leaves the dense output to the summing
+// emit pass.
+enum QueryMode { Q_ENCODE = 0, Q_PLAIN = 1, Q_DECODE = 2, Q_SUM = 3 };
 
 struct QueryOut {
     const float *g;         // encode: dense gradient (values of the positives)
     uint32_t *idx_out;      // plain: output list; decode: optional positives
     uint64_t cap;           // plain: output capacity
     uint64_t *n_out;        // plain: device count
-    const uint8_t *payload; // decode: payload base
     float *dense_out;       // decode: dense gradient
     float *val_out;         // decode: optional values
     uint64_t *counts_out;   // decode: optional per-tensor counts (flags word)
+    float scale;            // sum: factor applied to the sum
+    uint32_t npay;          // sum: payloads
+    uint32_t ntens;         // sum: tensors per payload
+    uint32_t ntiles1;       // sum: tiles per payload
 };
 
 struct RecordView {
@@ -490,8 +495,8 @@ constexpr uint32_t FC_WORDS = 30720;         // filter words kept in LDS (120 Ki
 __device__ __forceinline__ RecordView query_filter(const Work &w, const QueryOut &o, TDesc &td, int mode, bool *ok) {
     RecordView rv;
     *ok = true;
-    if (mode == Q_DECODE) {
-        rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, td.in.d, ok);
+    if (mode == Q_DECODE || mode == Q_SUM) {
+        rv = read_record(td.in.rec, td.in.rec_cap, td.in.d, ok);
     } else {
         rv.bits = td.in.bits;
         rv.m_bits = td.m_words * 32u;
@@ -556,7 +561,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) tcl[x] = 0;
         if (threadIdx.x == 0) {
             next = 0;
-            if (MODE == Q_DECODE && !ok) atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+            if ((MODE == Q_DECODE || MODE == Q_SUM) && !ok) atomicOr(&td.flags, FLAG_DEC_MISMATCH);
         }
         __syncthreads();
         const uint32_t m_bits = rv.m_bits, k = rv.k, d = td.in.d;
@@ -666,6 +671,24 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
     }
 }
 
+// The received value of a positive whose value number is vn (NO_SLOT: not
+// coded, so 0): its run's polynomial at the abscissa of its sorted rank
+// sigma[vn].  A rank outside the record flags the tensor and reads as 0.
+__device__ __forceinline__ float positive_value(const RecordView &rv, const float *cf, bool staged, uint32_t vn,
+                                                TDesc &td, uint64_t *counts_out, uint32_t t) {
+    if (vn >= rv.nv) return 0.0f;
+    const uint32_t rank = sigma_get(rv.sigma, (uint64_t)vn * rv.b, rv.b);
+    if (rank >= rv.nv) {
+        atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+        if (counts_out) atomicOr((unsigned long long *)&counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
+        return 0.0f;
+    }
+    uint32_t s, lo, ns;
+    run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);
+    const double tt = abscissa(rank - lo, ns);
+    return staged ? horner(cf + s * (rv.deff + 1u), rv.deff, tt) : horner(rv.coef + s * (rv.deff + 1u), rv.deff, tt);
+}
+
 // Emit pass: positives in ascending order at their tensor-wide ranks.
 //  A. the tile's 128 positives words and their prefix counts (block scan);
 //     each thread lists the positives among its 16 elements at their
@@ -719,7 +742,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
         }
         if (MODE == Q_DECODE) {
             bool ok = true;
-            rv = read_record(o.payload + td.in.rec_off, td.in.rec_cap, d, &ok);
+            rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
             ncoef = rv.seff * (rv.deff + 1u);
             // the receiver's own positives, and the header's values count
             npos = td.nv_dec;
@@ -770,21 +793,8 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             } else if (MODE == Q_PLAIN) {
                 if (q < o.cap) o.idx_out[q] = i;
             } else {
-                float y = 0.0f;
-                const uint32_t vn = policy_slot(q, npos, ncoded, policy, pseed);
-                if (vn < rv.nv) {
-                    const uint32_t rank = sigma_get(rv.sigma, (uint64_t)vn * rv.b, rv.b);
-                    if (rank < rv.nv) {
-                        uint32_t s, lo, ns;
-                        run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);
-                        const double tt = abscissa(rank - lo, ns);
-                        y = ncoef <= EMIT_COEF ? horner(cf + s * (rv.deff + 1u), rv.deff, tt)
-                                               : horner(rv.coef + s * (rv.deff + 1u), rv.deff, tt);
-                    } else {
-                        atomicOr(&td.flags, FLAG_DEC_MISMATCH);
-                        if (o.counts_out) atomicOr((unsigned long long *)&o.counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
-                    }
-                }
+                const float y = positive_value(rv, cf, ncoef <= EMIT_COEF,
+                                               policy_slot(q, npos, ncoded, policy, pseed), td, o.counts_out, t);
                 o.dense_out[toff_el + i] = y;  // zeros elsewhere come from the probe pass
                 const uint64_t at = toff_el + q;
                 if (o.idx_out) o.idx_out[at] = i;
@@ -792,6 +802,78 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             }
         }
         __syncthreads();  // pw, pre and slot are rewritten by the next tile
+    }
+}
+
+// Summing emit pass: one block per tile of the dense gradient.  The tile's
+// sum is kept in LDS; the payloads are added in order p = 0, 1, ...: each
+// payload's positives in the tile are listed (as in k_emit), decoded one per
+// thread, and added to their elements, with a barrier between payloads so
+// that every element sees its terms in payload order.  The tile is then
+// scaled and written once, zeros included, by full-row stores.
+__global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
+    __shared__ uint32_t scratch[NWAVES + 1];
+    __shared__ uint32_t pw[TILE_WORDS];
+    __shared__ uint32_t pre[TILE_WORDS];
+    __shared__ uint16_t slot[TILE];
+    __shared__ float acc[TILE];
+    __shared__ float cf[EMIT_COEF];
+    constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);
+    for (uint32_t tile = blockIdx.x; tile < o.ntiles1; tile += gridDim.x) {
+        const uint32_t t = tensor_of_tile(w, tile);  // payload 0's descriptor of the tensor
+        const uint32_t lt = tile - w.td[t].in.tile0;
+        const uint32_t d = w.td[t].in.d;
+        const uint64_t toff_el = w.td[t].in.off;
+        for (uint32_t e = threadIdx.x; e < TILE; e += NTHREADS) acc[e] = 0.0f;
+        for (uint32_t p = 0; p < o.npay; ++p) {
+            const uint32_t v = p * o.ntens + t;
+            TDesc &td = w.td[v];
+            const uint32_t ptile = p * o.ntiles1 + tile;
+            const uint32_t word = threadIdx.x < TILE_WORDS ? w.pbits[(uint64_t)ptile * TILE_WORDS + threadIdx.x] : 0u;
+            const uint32_t q0 = w.toff[ptile];
+            bool ok = true;
+            const RecordView rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
+            const uint32_t ncoef = rv.seff * (rv.deff + 1u);
+            const uint32_t npos = td.nv_dec;
+            const uint32_t ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
+            uint32_t tot;
+            const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
+            if (threadIdx.x < TILE_WORDS) {
+                pw[threadIdx.x] = word;
+                pre[threadIdx.x] = ex;
+            }
+            if (ncoef <= EMIT_COEF)
+                for (uint32_t x = threadIdx.x; x < ncoef; x += NTHREADS) cf[x] = rv.coef[x];
+            __syncthreads();
+#pragma unroll
+            for (uint32_t u = 0; u < GROUPS; ++u) {
+                const uint32_t e0 = u * 4 * NTHREADS + threadIdx.x * 4;
+                const uint32_t wd = pw[e0 >> 5], sh = e0 & 31u;
+                const uint32_t nib = (wd >> sh) & 0xfu;
+                uint32_t r = pre[e0 >> 5] + __popc(sh ? wd << (32u - sh) : 0u);
+#pragma unroll
+                for (uint32_t c = 0; c < 4; ++c)
+                    if ((nib >> c) & 1u) slot[r++] = (uint16_t)(e0 + c);
+            }
+            __syncthreads();
+            for (uint32_t x = threadIdx.x; x < tot; x += NTHREADS) {
+                const uint32_t vn = policy_slot(q0 + x, npos, ncoded, rv.policy, rv.seed);
+                acc[slot[x]] += positive_value(rv, cf, ncoef <= EMIT_COEF, vn, td, o.counts_out, v);
+            }
+            __syncthreads();  // pw, pre, slot and cf are rewritten by the next payload
+        }
+        // scale and store the tile
+        float *dst = o.dense_out + toff_el + (uint64_t)lt * TILE;
+        const uint32_t n_el = min(TILE, d - lt * TILE);
+        if (n_el == TILE && ((uintptr_t)dst & 15u) == 0) {
+            for (uint32_t x = threadIdx.x; x < TILE / 4; x += NTHREADS) {
+                const float4 a = ((const float4 *)acc)[x];
+                ((float4 *)dst)[x] = make_float4(o.scale * a.x, o.scale * a.y, o.scale * a.z, o.scale * a.w);
+            }
+        } else {
+            for (uint32_t x = threadIdx.x; x < n_el; x += NTHREADS) dst[x] = o.scale * acc[x];
+        }
+        __syncthreads();  // acc is cleared for the next tile
     }
 }
 
@@ -830,20 +912,37 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     return hipGetLastError();
 }
 
-hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *dense_out, uint32_t *idx_out,
-                               float *val_out, uint64_t *counts_out, int grid_persist, hipStream_t s) {
+hipError_t launch_query_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
+                               uint64_t *counts_out, hipStream_t s) {
     QueryOut o{};
     o.counts_out = counts_out;
-    o.payload = payload;
     o.dense_out = dense_out;
     o.idx_out = idx_out;
     o.val_out = val_out;
     k_probe<Q_DECODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_DECODE>");
-    hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out, payload);
+    hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out);
     if (e != hipSuccess) return e;
     k_emit<Q_DECODE><<<resident_grid(k_emit<Q_DECODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_DECODE>");
+    return hipGetLastError();
+}
+
+hipError_t launch_query_decode_sum(const Work &w, uint32_t npay, uint32_t ntens, uint32_t ntiles1, float scale,
+                                   float *dense_out, uint64_t *counts_out, hipStream_t s) {
+    QueryOut o{};
+    o.counts_out = counts_out;
+    o.dense_out = dense_out;
+    o.scale = scale;
+    o.npay = npay;
+    o.ntens = ntens;
+    o.ntiles1 = ntiles1;
+    k_probe<Q_SUM><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_probe<Q_SUM>");
+    hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out);
+    if (e != hipSuccess) return e;
+    k_emit_sum<<<resident_grid(k_emit_sum, NTHREADS, ntiles1), NTHREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_emit_sum");
     return hipGetLastError();
 }
 

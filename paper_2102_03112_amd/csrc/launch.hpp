@@ -60,8 +60,7 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
 hipError_t launch_tile_popc(const Work &w, const uint32_t *bits, int grid_persist, hipStream_t s);
 // which: 0 |S| (and the filter size), 1 sender |P|, 2 receiver |P| (also
 // into counts_out, checked against the payload header), 3 into *n_out
-hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out = nullptr,
-                            const uint8_t *payload = nullptr);
+hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out = nullptr);
 
 // bloom.hip
 // Insert in rounds of `hash_per_round` hash functions (the position buffer
@@ -73,8 +72,12 @@ hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_c
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s);
 hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,
                               hipStream_t s);
-hipError_t launch_query_decode(const Work &w, const uint8_t *payload, float *dense_out, uint32_t *idx_out,
-                               float *val_out, uint64_t *counts_out, int grid_persist, hipStream_t s);
+hipError_t launch_query_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
+                               uint64_t *counts_out, hipStream_t s);
+// Several payloads of one tensor layout into one dense sum: the work's
+// tensors are payload-major (tensor t of payload p is p * ntens + t).
+hipError_t launch_query_decode_sum(const Work &w, uint32_t npay, uint32_t ntens, uint32_t ntiles1, float scale,
+                                   float *dense_out, uint64_t *counts_out, hipStream_t s);
 
 // valuefit.hip
 hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,

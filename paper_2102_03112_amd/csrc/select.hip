@@ -616,7 +616,7 @@ constexpr uint32_t TSCAN_THREADS = 1024;
 constexpr uint32_t TSCAN_PER = 8;  // counts per thread per step, loaded together
 
 __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, uint64_t *n_out,
-                                                             uint64_t *counts_out, const uint8_t *payload) {
+                                                             uint64_t *counts_out) {
     TDesc &td = w.td[blockIdx.x];
     __shared__ uint32_t scratch[TSCAN_THREADS / 64 + 1];
     const uint32_t nt = td.in.ntiles;
@@ -655,7 +655,7 @@ __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, 
             td.nv_dec = carry;
             if (counts_out) {
                 counts_out[4 * blockIdx.x + 2] = carry;
-                const uint8_t *rec = payload + td.in.rec_off;
+                const uint8_t *rec = td.in.rec;
                 const uint32_t hdr_npos = ((const uint32_t *)rec)[H_NPOS];
                 uint32_t f = td.flags;
                 if (carry != hdr_npos) f |= FLAG_DEC_MISMATCH;
@@ -673,9 +673,8 @@ hipError_t launch_tile_popc(const Work &w, const uint32_t *bits, int grid_persis
     return hipGetLastError();
 }
 
-hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out,
-                            const uint8_t *payload) {
-    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, which, n_out, counts_out, payload);
+hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out) {
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, which, n_out, counts_out);
     trace_mark(s, "k_tile_scan");
     return hipGetLastError();
 }
@@ -713,7 +712,7 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
                                     hipStream_t s) {
     k_tile_popc<<<grid_persist, NTHREADS, 0, s>>>(w, w.selbits);
     trace_mark(s, "k_tile_popc");
-    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr, nullptr);
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr);
     trace_mark(s, "k_tile_scan");
     k_compact_selection<<<grid_persist, NTHREADS, 0, s>>>(w, g, val_out);
     trace_mark(s, "k_compact_selection");
@@ -725,7 +724,7 @@ hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipSt
     k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     // |S| from the per-tile counts of the filter pass
-    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr, nullptr);
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr);
     trace_mark(s, "k_tile_scan");
     return hipGetLastError();
 }

@@ -60,6 +60,15 @@ def values_close(y_gpu: np.ndarray, y_ref: np.ndarray, ranks: np.ndarray, n: int
     assert bad.size == 0, f"{bad.size} values off, first q={bad[0]} gpu={y_gpu[bad[0]]} ref={y_ref[bad[0]]}"
 
 
+def unpack_sigma(words: np.ndarray, n: int, b: int) -> np.ndarray:
+    """The n packed b-bit entries of a reorder map written by the GPU (a numpy
+    reader of the LSB-first layout, so that GPU output is never fed to the
+    oracle)."""
+    bits = np.unpackbits(np.ascontiguousarray(words, dtype="<u4").view(np.uint8), bitorder="little")
+    at = np.arange(n, dtype=np.int64)[:, None] * b + np.arange(b, dtype=np.int64)[None, :]
+    return (bits[at].astype(np.uint64) << np.arange(b, dtype=np.uint64)[None, :]).sum(axis=1)
+
+
 def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     """A GPU payload record against the oracle's result for the same tensor:
     bit-exact filter and reorder map, header fields, coefficients within
@@ -142,13 +151,9 @@ def check_roundtrip(g, cfg: B.Config, out, refs):
             y_gpu[vn] = vals[kept]
             y_ref = np.zeros(nc, np.float32)
             y_ref[vn] = ref.vals[kept]
-            # receiver values vs the oracle's decode of this very payload
-            y_same = oracle.curvefit_decode(rec.coef if rec.seg_eff else np.zeros(0, np.float32),
-                                            rec.sigma, nc, rec.deg_eff, max(rec.seg_eff, 1))
-            ranks = oracle.sigma_unpack(rec.sigma, nc)
-            values_close(y_gpu, y_same, ranks, nc, rec.seg_eff)
-            # and vs the oracle's own end-to-end reconstruction
-            values_close(y_gpu, y_ref, ranks, nc, rec.seg_eff)
+            # receiver values vs the oracle's own end-to-end reconstruction
+            ranks = oracle.sigma_unpack(ref.fit.sigma, nc)
+            values_close(y_gpu, y_ref, ranks, nc, ref.fit.S_eff)
         dense = out["dense"][a:b]
         pos = ref.P_dec.astype(np.int64)
         np.testing.assert_array_equal(dense[pos], out["val"][a: a + nv])

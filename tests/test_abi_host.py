@@ -36,7 +36,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     assert sorted(names) == sorted(B.EXPORTS)
     for n in names:
         assert hasattr(L, n), n
@@ -104,6 +104,25 @@ def test_config_rejected(L, bad):
     assert L.dr_payload_layout(ctypes.byref(cfg.c), None) == 0
     st = L.dr_roundtrip(FAKE, ctypes.byref(cfg.c), FAKE, 1 << 30, FAKE, None, None, None, FAKE, 1 << 40, None)
     assert st == B.DR_EINVAL
+
+
+def test_decode_sum_rejects_bad_arguments(L):
+    cfg = _cfg()
+    big = 1 << 40
+    one = (ctypes.c_void_p * 65)(*([FAKE.value] * 65))
+    nul = (ctypes.c_void_p * 2)(FAKE.value, None)
+    f = L.dr_payload_decode_sum
+    assert f(one, 0, ctypes.byref(cfg.c), 1.0, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(one, 65, ctypes.byref(cfg.c), 1.0, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(None, 1, ctypes.byref(cfg.c), 1.0, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(nul, 2, ctypes.byref(cfg.c), 1.0, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(one, 2, ctypes.byref(cfg.c), 1.0, None, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(one, 2, ctypes.byref(cfg.c), float("nan"), FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(one, 2, ctypes.byref(cfg.c), float("inf"), FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert f(one, 2, ctypes.byref(cfg.c), 1.0, FAKE, None, FAKE, 1000, None) == B.DR_EINVAL
+    assert f(one, 2, None, 1.0, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    bad = _cfg(policy=9)
+    assert f(one, 2, ctypes.byref(bad.c), 1.0, FAKE, None, FAKE, big, None) == B.DR_EINVAL
 
 
 def test_null_config_and_zero_tensors(L):

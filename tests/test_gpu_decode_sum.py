@@ -1,0 +1,170 @@
+"""GPU parity of dr_payload_decode_sum: several payloads decoded into one
+scaled dense sum (Section 2, the aggregated gradient; Section 6.4, payloads
+gathered so that every worker decodes all of them)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2102_03112_amd import binding as B
+from paper_2102_03112_amd import workloads as W
+from _gpu_util import dev_tensor, host, log, sync, workspace
+
+pytestmark = pytest.mark.gpu
+
+EPS32 = float(np.finfo(np.float32).eps)
+
+
+def _encode_all(gs, cfg):
+    import torch
+
+    total, rec_off = B.payload_layout(cfg)
+    ws = workspace(cfg.d, cfg.n_tensors)
+    pays = []
+    for g in gs:
+        pay = torch.zeros(total, dtype=torch.uint8, device="cuda")
+        B.payload_encode(dev_tensor(g), cfg, pay, None, ws)
+        pays.append(pay)
+    sync()
+    return pays
+
+
+def _bounds(refs_per_payload, offsets, d, tol=1e-5):
+    """Per element: sum over payloads of the value tolerance of that
+    payload's received value (the run-max floor of the value check), and the
+    sum of the magnitudes (for the fp32 rounding of the sum)."""
+    vb = np.zeros(d)
+    mag = np.zeros(d)
+    for res in refs_per_payload:
+        for t, r in enumerate(res):
+            if r.P_dec.size == 0:
+                continue
+            y = np.abs(r.vals.astype(np.float64))
+            kept = r.slots != oracle.NO_SLOT
+            run_max = np.zeros(max(r.fit.S_eff, 1))
+            if r.fit.n:
+                ranks = oracle.sigma_unpack(r.fit.sigma, r.fit.n).astype(np.int64)
+                s_of_vn = ((ranks + 1) * r.fit.S_eff - 1) // r.fit.n
+                s = np.zeros(r.P_dec.size, np.int64)
+                s[kept] = s_of_vn[r.slots[kept].astype(np.int64)]
+                np.maximum.at(run_max, s[kept], y[kept])
+                floor = np.where(kept, run_max[s], 0.0)
+            else:
+                floor = np.zeros_like(y)
+            at = offsets[t] + r.P_dec.astype(np.int64)
+            vb[at] += tol * np.maximum(y, floor)
+            mag[at] += y
+    return vb, mag
+
+
+def _check(out, want, refs, offsets, d, n, scale):
+    vb, mag = _bounds(refs, offsets, d)
+    bound = abs(scale) * (vb + 4 * n * EPS32 * mag)
+    err = np.abs(out.astype(np.float64) - want.astype(np.float64))
+    bad = np.flatnonzero(err > bound)
+    assert bad.size == 0, f"{bad.size} elements off, first i={bad[0]} gpu={out[bad[0]]} ref={want[bad[0]]}"
+    # zero exactly where no payload has a positive
+    on = np.zeros(d, bool)
+    for res in refs:
+        for t, r in enumerate(res):
+            on[offsets[t] + r.P_dec.astype(np.int64)] = True
+    assert np.all(out[~on] == 0)
+
+
+CASES = {
+    # name: (d, offsets, ratio, fpr, D, S, n payloads, policy)
+    "resnet20_x8": (36_864, [0, 36_864], (1, 100), 1e-3, 5, 8, 8, oracle.POLICY_P0),
+    "ragged_x3": (8203, [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8, 3, oracle.POLICY_P0),
+    "two_tensors_x5_p1": (300_000, [0, 123_457, 300_000], (1, 100), 1e-2, 3, 4, 5, oracle.POLICY_RANDOM),
+    "support_x2": (50_000, [0, 50_000], None, 1e-4, 3, 16, 2, oracle.POLICY_P0),
+    "one_payload": (100_000, [0, 100_000], (1, 100), 1e-3, 5, 8, 1, oracle.POLICY_P0),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_decode_sum_parity(name):
+    import torch
+
+    d, off, ratio, fpr, D, S, n, policy = CASES[name]
+    log(f"decode_sum {name} d={d} payloads={n}")
+    if ratio is None:
+        gs = [W.sparse_normal(d, 300 + p, 0.4) for p in range(n)]
+    else:
+        gs = [W.normal(d, 300 + p, scale=1e-3) for p in range(n)]
+    cfg = B.Config(off, ratio, fpr, D, S, policy, 99)
+    pays = _encode_all(gs, cfg)
+    scale = 1.0 / n
+    dense = torch.full((max(d, 1),), 5.0, dtype=torch.float32, device="cuda")
+    counts = torch.full((4 * n * cfg.n_tensors,), 7, dtype=torch.int64, device="cuda")
+    B.payload_decode_sum(pays, cfg, scale, dense, counts, workspace(d, cfg.n_tensors))
+    sync()
+    out = host(dense)[:d]
+    refs = [oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=99) for g in gs]
+    want = oracle.decode_sum(refs, d, off, scale)
+    _check(out, want, refs, off, d, n, scale)
+    c = host(counts).reshape(n, cfg.n_tensors, 4)
+    for p, res in enumerate(refs):
+        for t, r in enumerate(res):
+            assert tuple(int(x) for x in c[p, t]) == (0, 0, r.P_dec.size, 0)
+
+
+def test_decode_sum_equals_the_single_decodes_added_in_order():
+    """The summing pass and n separate dr_payload_decode calls run the same
+    per-positive arithmetic: adding the single decodes in payload order in
+    fp32 gives the same bits."""
+    import torch
+
+    d, off = 200_003, [0, 77_777, 200_003]
+    cfg = B.Config(off, (1, 100), 1e-3, 5, 8)
+    gs = [W.normal(d, 500 + p, scale=1e-3) for p in range(4)]
+    pays = _encode_all(gs, cfg)
+    ws = workspace(d, 2)
+    acc = np.zeros(d, np.float32)
+    for pay in pays:
+        one = torch.zeros(d, dtype=torch.float32, device="cuda")
+        B.payload_decode(pay, cfg, one, None, None, None, ws)
+        sync()
+        acc = (acc + host(one)).astype(np.float32)
+    dense = torch.zeros(d, dtype=torch.float32, device="cuda")
+    B.payload_decode_sum(pays, cfg, 0.25, dense, None, ws)
+    sync()
+    np.testing.assert_array_equal(host(dense), (np.float32(0.25) * acc).astype(np.float32))
+
+
+def test_decode_sum_flags_a_damaged_payload_and_skips_it():
+    import torch
+
+    d, off = 40_000, [0, 40_000]
+    cfg = B.Config(off, (1, 100), 1e-3, 5, 8)
+    gs = [W.normal(d, 600 + p, scale=1e-3) for p in range(3)]
+    pays = _encode_all(gs, cfg)
+    bad = host(pays[1]).copy()
+    bad[0] ^= 0xFF  # magic
+    pays[1] = dev_tensor(bad)
+    dense = torch.zeros(d, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(12, dtype=torch.int64, device="cuda")
+    B.payload_decode_sum(pays, cfg, 1.0, dense, counts, workspace(d))
+    sync()
+    c = host(counts).reshape(3, 4)
+    assert c[1, 3] & B.FLAG_DEC_MISMATCH and c[0, 3] == 0 and c[2, 3] == 0
+    refs = [oracle.roundtrip(gs[p], off, (1, 100), 1e-3, 5, 8) for p in (0, 2)]
+    want = oracle.decode_sum(refs, d, off, 1.0)
+    _check(host(dense), want, refs, off, d, 2, 1.0)
+
+
+def test_decode_sum_at_the_payload_limit_fits_the_workspace():
+    """64 payloads of a small multi-tensor layout: the workspace sized by
+    dr_workspace_bytes(d, n_tensors) holds the summing pass's state."""
+    import torch
+
+    d, off = 9000, [0, 10, 4106, 9000]
+    cfg = B.Config(off, (1, 10), 1e-2, 2, 2)
+    n = 64
+    gs = [W.normal(d, 700 + p, scale=1e-3) for p in range(n)]
+    pays = _encode_all(gs, cfg)
+    ws = B.workspace(d, 3)
+    dense = torch.zeros(d, dtype=torch.float32, device="cuda")
+    B.payload_decode_sum(pays, cfg, 1.0 / n, dense, None, ws)
+    sync()
+    refs = [oracle.roundtrip(g, off, (1, 10), 1e-2, 2, 2) for g in gs]
+    want = oracle.decode_sum(refs, d, off, 1.0 / n)
+    _check(host(dense), want, refs, off, d, n, 1.0 / n)

@@ -186,6 +186,11 @@ def test_curvefit_parity(n, D, S):
     B.curvefit_encode(Vd, nd, n, D, S, coef, sig, ws)
     out = torch.zeros(max(n, 1), dtype=torch.float32, device="cuda")
     B.curvefit_decode(coef, sig, nd, n, D, S, out, ws)
+    # the decoder alone, on the oracle's coefficients and reorder map
+    coef_o = dev_tensor(ref.coef.astype(np.float32))
+    sig_o = dev_tensor(np.concatenate([ref.sigma.astype(np.uint32), np.zeros(1, np.uint32)]).view(np.int32))
+    out_o = torch.zeros(max(n, 1), dtype=torch.float32, device="cuda")
+    B.curvefit_decode(coef_o, sig_o, nd, n, D, S, out_o, ws)
     sync()
     c_gpu = host(coef)
     s_gpu = host(sig).view(np.uint32)[: oracle.sigma_words(n)]
@@ -196,11 +201,13 @@ def test_curvefit_parity(n, D, S):
     for s in range(ref.S_eff):
         mask[s * (D + 1): s * (D + 1) + ref.D_eff + 1] = False
     assert np.all(c_gpu[mask] == 0)
-    # decode: GPU vs oracle on the same (GPU) payload
-    y_ref = oracle.curvefit_decode(c_gpu, s_gpu, n, D, S)
+    # decode: the oracle's reconstruction from its own coefficients, against
+    # the GPU's from its own payload and from the oracle's payload
+    y_ref = oracle.curvefit_decode(ref.coef, ref.sigma, n, D, S)
     if n:
-        ranks = oracle.sigma_unpack(s_gpu, n)
+        ranks = oracle.sigma_unpack(ref.sigma, n)
         values_close(host(out)[:n], y_ref, ranks, n, ref.S_eff)
+        values_close(host(out_o)[:n], y_ref, ranks, n, ref.S_eff)
 
 
 # ---------------------------------------------------------------------------
