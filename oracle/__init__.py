@@ -29,6 +29,9 @@ R_NONZERO = (1 << 64) - 1  # "select every nonzero" instead of a top-r count
 # index policies (Section 4; Sections 10.4, 10.5)
 POLICY_P0, POLICY_RANDOM, POLICY_LEFTMOST, POLICY_MIDDLE, POLICY_RIGHTMOST = 0, 1, 2, 3, 4
 NO_SLOT = 0xFFFFFFFF
+# segmentation of the sorted values (Section 5)
+SEG_EQUAL, SEG_CHORD = 0, 1
+MAX_SEG = 4096
 
 
 class OracleError(RuntimeError):
@@ -69,6 +72,13 @@ def _load():
             [f32p, u64, u32, u32, f32p, f64p, u32p, u32p, u32p, u32p],
         ),
         "drref_curvefit_decode": (ctypes.c_int, [f32p, u32p, u64, u32, u32, f32p]),
+        "drref_segment": (ctypes.c_int, [f32p, u64, u32, u32, u32, u64p, u32p]),
+        "drref_seg_heuristic": (u32, [f32p, u64, u32]),
+        "drref_curvefit_encode_seg": (
+            ctypes.c_int,
+            [f32p, u64, u32, u32, u32, f32p, f64p, u32p, u64p, u32p, u32p, u32p],
+        ),
+        "drref_curvefit_decode_seg": (ctypes.c_int, [f32p, u32p, u64, u32, u32, u64p, f32p]),
         "drref_perm": (u32, [u32, u64, u32]),
         "drref_policy_slots": (ctypes.c_int, [u64, u64, u32, u32, u32p, u64p]),
     }
@@ -233,25 +243,66 @@ class FitPayload:
     S_eff: int
     D_eff: int
     b: int
+    seg_mode: int = SEG_EQUAL
+    bounds: np.ndarray = None  # segment starts, S_eff + 1 entries (last = n)
 
 
-def curvefit_encode(V: np.ndarray, degree: int, n_seg: int) -> FitPayload:
-    """Sort, segment, fit, and pack the reorder map (Sections 5 and 5.1)."""
+def curvefit_encode(V: np.ndarray, degree: int, n_seg: int, seg_mode: int = SEG_EQUAL) -> FitPayload:
+    """Sort, segment, fit, and pack the reorder map (Sections 5 and 5.1).
+    ``n_seg`` = 0 asks for the heuristic number of segments; ``seg_mode``
+    chooses equal-count or chord segmentation (Section 5).  The coefficient
+    rows are n_seg (MAX_SEG for the heuristic) of degree+1."""
     lib = _load()
     V = np.ascontiguousarray(V, dtype=np.float32)
     n = V.size
-    coef = np.zeros(n_seg * (degree + 1), dtype=np.float32)
-    coef64 = np.zeros(n_seg * (degree + 1), dtype=np.float64)
+    cap = n_seg if n_seg else MAX_SEG
+    coef = np.zeros(cap * (degree + 1), dtype=np.float32)
+    coef64 = np.zeros(cap * (degree + 1), dtype=np.float64)
     sigma = np.zeros(max(sigma_words(n), 1), dtype=np.uint32)
+    bounds = np.zeros(cap + 1, dtype=np.uint64)
     se, de, b = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
     _check(
-        lib.drref_curvefit_encode(
-            _ptr(V, ctypes.c_float), n, degree, n_seg, _ptr(coef, ctypes.c_float), _ptr(coef64, ctypes.c_double),
-            _ptr(sigma, ctypes.c_uint32), ctypes.byref(se), ctypes.byref(de), ctypes.byref(b),
+        lib.drref_curvefit_encode_seg(
+            _ptr(V, ctypes.c_float), n, degree, n_seg, seg_mode, _ptr(coef, ctypes.c_float),
+            _ptr(coef64, ctypes.c_double), _ptr(sigma, ctypes.c_uint32), _ptr(bounds, ctypes.c_uint64),
+            ctypes.byref(se), ctypes.byref(de), ctypes.byref(b),
         ),
         "curvefit_encode",
     )
-    return FitPayload(coef, coef64, sigma[: sigma_words(n)], n, degree, n_seg, int(se.value), int(de.value), int(b.value))
+    S_eff = int(se.value)
+    return FitPayload(coef, coef64, sigma[: sigma_words(n)], n, degree, n_seg, S_eff, int(de.value), int(b.value),
+                      seg_mode, bounds[: S_eff + 1].copy())
+
+
+def segment(C: np.ndarray, degree: int, n_seg: int, seg_mode: int) -> np.ndarray:
+    """Segment starts (S_eff + 1 entries) of already sorted values C."""
+    C = np.ascontiguousarray(C, dtype=np.float32)
+    bounds = np.zeros(n_seg + 1, dtype=np.uint64)
+    se = ctypes.c_uint32()
+    _check(_load().drref_segment(_ptr(C, ctypes.c_float), C.size, degree, n_seg, seg_mode,
+                                 _ptr(bounds, ctypes.c_uint64), ctypes.byref(se)), "segment")
+    return bounds[: int(se.value) + 1].copy()
+
+
+def seg_heuristic(C: np.ndarray, degree: int) -> int:
+    """Heuristic number of segments for sorted values C (p + 1 pieces)."""
+    C = np.ascontiguousarray(C, dtype=np.float32)
+    return int(_load().drref_seg_heuristic(_ptr(C, ctypes.c_float), C.size, degree))
+
+
+def curvefit_decode_seg(coef: np.ndarray, sigma: np.ndarray, n: int, degree: int, bounds: np.ndarray) -> np.ndarray:
+    """Reconstruct n values from coefficients, reorder map and segment starts."""
+    lib = _load()
+    coef = np.ascontiguousarray(coef, dtype=np.float32)
+    sigma = np.ascontiguousarray(sigma, dtype=np.uint32)
+    if sigma.size == 0:
+        sigma = np.zeros(1, dtype=np.uint32)
+    bounds = np.ascontiguousarray(bounds, dtype=np.uint64)
+    out = np.empty(max(n, 1), dtype=np.float32)
+    _check(lib.drref_curvefit_decode_seg(_ptr(coef, ctypes.c_float), _ptr(sigma, ctypes.c_uint32), n, degree,
+                                         max(bounds.size - 1, 0), _ptr(bounds, ctypes.c_uint64),
+                                         _ptr(out, ctypes.c_float)), "curvefit_decode_seg")
+    return out[:n]
 
 
 def curvefit_decode(coef: np.ndarray, sigma: np.ndarray, n: int, degree: int, n_seg: int) -> np.ndarray:
@@ -326,12 +377,14 @@ class TensorResult:
         fp32 coefficients actually used, and the reorder map."""
         idx = self.m
         val = 32 * self.fit.S_eff * (self.fit.D_eff + 1) if self.fit.n else 0
+        if self.fit.seg_mode == SEG_CHORD and self.fit.S_eff > 1:
+            val += 32 * (self.fit.S_eff - 1)  # the interior segment starts
         sig = self.fit.n * self.fit.b if self.fit.n else 0
         return {"index": idx, "values": val, "sigma": sig}
 
 
 def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
-                     policy: int = POLICY_P0, seed: int = 0) -> TensorResult:
+                     policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL) -> TensorResult:
     """Sender: top-r (or support) -> Bloom insert -> full-range query (P) ->
     the policy keeps all of P (P0) or r of it -> V = g at the kept positives
     (values from the dense gradient, Section 4) -> curve-fit encode.
@@ -348,11 +401,11 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     kept = slots != NO_SLOT
     V = np.zeros(ncoded, dtype=np.float32)
     V[slots[kept].astype(np.int64)] = g[P[kept].astype(np.int64)]
-    fit = curvefit_encode(V, degree, n_seg)
+    fit = curvefit_encode(V, degree, n_seg, seg_mode)
     # receiver: its own query and the same policy over its own positives
     P_dec = bloom_query(bits, m, k, d)
     slots_dec, nc_dec = policy_slots(P_dec.size, ncoded, policy, seed)
-    y = curvefit_decode(fit.coef, fit.sigma, nc_dec, degree, n_seg)
+    y = curvefit_decode_seg(fit.coef, fit.sigma, nc_dec, degree, fit.bounds)
     vals = np.zeros(P_dec.size, dtype=np.float32)
     keep_dec = slots_dec != NO_SLOT
     vals[keep_dec] = y[slots_dec[keep_dec].astype(np.int64)]
@@ -364,7 +417,7 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
 
 
 def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
-              policy: int = POLICY_P0, seed: int = 0):
+              policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL):
     """Code every tensor g[offsets[t]:offsets[t+1]] independently on local
     indices.  ``ratio`` is (num, den) for top-r with r = ceil(d_t num / den),
     or None for the support of an inherently sparse gradient."""
@@ -372,7 +425,7 @@ def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int
     for t in range(len(offsets) - 1):
         gt = g[offsets[t]: offsets[t + 1]]
         r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
-        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed))
+        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed, seg_mode))
     return out
 
 

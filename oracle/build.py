@@ -12,7 +12,7 @@ def build(verbose: bool = False) -> str:
     src = os.path.join(HERE, "drref.c")
     out = os.path.join(HERE, "libdrref.so")
     tmp = out + ".tmp"
-    cmd = ["gcc", "-O2", "-std=c99", "-Wall", "-Wextra", "-fPIC", "-shared", src, "-o", tmp, "-lm"]
+    cmd = ["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-Wall", "-Wextra", "-fPIC", "-shared", src, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

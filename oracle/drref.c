@@ -437,6 +437,150 @@ uint64_t drref_sigma_words(uint64_t n)
     return (n * drref_sigma_bits(n) + 31) / 32;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Adaptive segmentation (Section 5, "Piece-wise approximation") and the    */
+/* number of pieces (Section 5 after Lemma 1; Remark 4 of Section 10).     */
+/* ------------------------------------------------------------------------ */
+
+#define DRREF_MAX_SEG 4096
+#define DRREF_SEG_EQUAL 0u
+#define DRREF_SEG_CHORD 1u
+
+/*
+ * Distance of sorted value C[i] from the chord through the segment's first
+ * and last points (ranks a and z > a).  The paper takes the squared vertical
+ * distance; its absolute value has the same maximiser.  Evaluated in double
+ * as written, one rounding per operation (no fused multiply-add), so that
+ * any implementation that follows these steps takes the same decisions.
+ */
+static double chord_dist(const float *C, uint64_t a, uint64_t z, uint64_t i)
+{
+    const double ca = (double)C[a];
+    const double m = ((double)C[z] - ca) / (double)(z - a);
+    const double y = ca + m * (double)(i - a);
+    return fabs(y - (double)C[i]);
+}
+
+/*
+ * Farthest allowed split point of segment [a, e) for degree D: the rank i
+ * that ends the left part, over the ranks that leave both parts at least
+ * D+1 points (the paper stops below n'+1 points); ties to the smaller rank.
+ * Returns 0 and leaves *i_out alone if no split is allowed.
+ */
+static double seg_candidate(const float *C, uint64_t a, uint64_t e, uint32_t D, uint64_t *i_out)
+{
+    const uint64_t minpts = (uint64_t)D + 1;
+    if (e - a < 2 * minpts)
+        return 0.0;
+    const uint64_t z = e - 1;
+    double best = 0.0;
+    for (uint64_t i = a + D; i + minpts <= z; ++i) {
+        const double dd = chord_dist(C, a, z, i);
+        if (dd > best) {
+            best = dd;
+            *i_out = i;
+        }
+    }
+    return best;
+}
+
+/*
+ * Segment starts of the sorted values C[0..n) (descending), for degree D and
+ * at most S segments: bounds_out[0..S_eff] with bounds_out[0] = 0 and
+ * bounds_out[S_eff] = n.
+ *  - Equal-count segments: segment s covers [floor(s n / S_eff),
+ *    floor((s+1) n / S_eff)), S_eff as in drref_fit_shape.
+ *  - Chord segmentation (Section 5): the values with the sign bit clear and
+ *    the rest (positive and negative sorted values) start as separate
+ *    segments, when S >= 2 and both hold at least D+1 points.  Then, while
+ *    there are fewer than S segments, the segment whose farthest allowed
+ *    split point lies farthest from its chord (ties: the leftmost segment)
+ *    is split after that point.  It stops early when no segment has an
+ *    allowed split point off its chord.
+ */
+int drref_segment(const float *C, uint64_t n, uint32_t D, uint32_t S, uint32_t mode, uint64_t *bounds_out,
+                  uint32_t *S_eff_out)
+{
+    if ((!C && n) || !bounds_out || !S_eff_out || S < 1 || S > DRREF_MAX_SEG || mode > DRREF_SEG_CHORD ||
+        D > DRREF_MAX_DEG)
+        return DRREF_EINVAL;
+    bounds_out[0] = 0;
+    if (n == 0) {
+        *S_eff_out = 0;
+        return DRREF_OK;
+    }
+    if (mode == DRREF_SEG_EQUAL) {
+        uint32_t S_eff, D_eff;
+        drref_fit_shape(n, D, S, &S_eff, &D_eff);
+        for (uint32_t s = 0; s <= S_eff; ++s)
+            bounds_out[s] = (uint64_t)s * n / S_eff;
+        *S_eff_out = S_eff;
+        return DRREF_OK;
+    }
+    const uint64_t minpts = (uint64_t)D + 1;
+    uint64_t l = 0;
+    while (l < n && !signbit(C[l]))
+        ++l;
+    uint32_t count = 1;
+    bounds_out[1] = n;
+    if (S >= 2 && l >= minpts && n - l >= minpts) {
+        bounds_out[1] = l;
+        bounds_out[2] = n;
+        count = 2;
+    }
+    while (count < S) {
+        int64_t best_seg = -1;
+        double best = 0.0;
+        uint64_t best_i = 0;
+        for (uint32_t k = 0; k < count; ++k) {
+            uint64_t i = 0;
+            const double dd = seg_candidate(C, bounds_out[k], bounds_out[k + 1], D, &i);
+            if (dd > best) {
+                best = dd;
+                best_seg = k;
+                best_i = i;
+            }
+        }
+        if (best_seg < 0)
+            break;
+        for (uint32_t k = count + 1; k > (uint32_t)best_seg + 1; --k)
+            bounds_out[k] = bounds_out[k - 1];
+        bounds_out[best_seg + 1] = best_i + 1;
+        ++count;
+    }
+    *S_eff_out = count;
+    return DRREF_OK;
+}
+
+/*
+ * Number of segments when the caller asks for the heuristic: p + 1 pieces
+ * for p knots, with M = |(C[0] - C[1]) - (C[n-2] - C[n-1])| (the first and
+ * last differences of the sorted curve; 0 if n < 2), and
+ *  - p = ceil(2 sqrt(M)) for a fit of degree >= 1 (Section 5, from the
+ *    piece-wise linear bound 2M/p^2 of Lemma 1),
+ *  - p = ceil(M / sqrt(2) - 1) for degree 0 (Remark 4, piece-wise constant),
+ * at least 0, and at most DRREF_MAX_SEG pieces.  Each ceiling is found as the
+ * smallest p >= 0 with p^2 >= 4M, resp. 2 (p+1)^2 >= M^2, in double, which
+ * needs no square root.
+ */
+uint32_t drref_seg_heuristic(const float *C, uint64_t n, uint32_t D)
+{
+    double M = 0.0;
+    if (n >= 2)
+        M = fabs(((double)C[0] - (double)C[1]) - ((double)C[n - 2] - (double)C[n - 1]));
+    uint32_t p = 0;
+    if (D == 0) {
+        const double M2 = M * M;
+        while (p + 1 < DRREF_MAX_SEG && 2.0 * (double)(p + 1) * (double)(p + 1) < M2)
+            ++p;
+    } else {
+        const double M4 = 4.0 * M;
+        while (p + 1 < DRREF_MAX_SEG && (double)p * (double)p < M4)
+            ++p;
+    }
+    return p + 1;
+}
+
 /*
  * Value encoder (Section 5 and 5.1).  Sort V descending; split the sorted
  * curve into equal-count segments; fit each by least squares in double;
@@ -446,47 +590,75 @@ uint64_t drref_sigma_words(uint64_t n)
  * entry, entry q in bits [q b, (q+1) b) of the word stream.
  * coef64_out (optional) receives the double-precision coefficients.
  */
-int drref_curvefit_encode(const float *V, uint64_t n, uint32_t D, uint32_t S, float *coef_out,
-                          double *coef64_out, uint32_t *sigma_out, uint32_t *S_eff_out,
-                          uint32_t *D_eff_out, uint32_t *b_out)
+/*
+ * The same with a choice of segmentation: mode DRREF_SEG_EQUAL or
+ * DRREF_SEG_CHORD (drref_segment), and S = 0 for the heuristic number of
+ * segments (drref_seg_heuristic).  coef_out and coef64_out hold
+ * S_cap = (S ? S : DRREF_MAX_SEG) rows; bounds_out (optional) S_cap + 1
+ * segment starts.
+ */
+int drref_curvefit_encode_seg(const float *V, uint64_t n, uint32_t D, uint32_t S, uint32_t mode,
+                              float *coef_out, double *coef64_out, uint32_t *sigma_out, uint64_t *bounds_out,
+                              uint32_t *S_eff_out, uint32_t *D_eff_out, uint32_t *b_out)
 {
-    if ((!V && n) || D > DRREF_MAX_DEG || S < 1 || !coef_out || (!sigma_out && n) || !S_eff_out ||
-        !D_eff_out || !b_out)
+    if ((!V && n) || D > DRREF_MAX_DEG || S > DRREF_MAX_SEG || mode > DRREF_SEG_CHORD || !coef_out ||
+        (!sigma_out && n) || !S_eff_out || !D_eff_out || !b_out)
         return DRREF_EINVAL;
     for (uint64_t q = 0; q < n; ++q)
         if (!isfinite(V[q]))
             return DRREF_EINVAL;
-    uint32_t S_eff, D_eff;
-    drref_fit_shape(n, D, S, &S_eff, &D_eff);
-    *S_eff_out = S_eff;
+    const uint32_t S_cap = S ? S : DRREF_MAX_SEG;
+    uint32_t S_unused, D_eff;
+    drref_fit_shape(n, D, S_cap, &S_unused, &D_eff);
     *D_eff_out = D_eff;
     *b_out = drref_sigma_bits(n);
-    for (uint64_t c = 0; c < (uint64_t)S * (D + 1); ++c) {
+    for (uint64_t c = 0; c < (uint64_t)S_cap * (D + 1); ++c) {
         coef_out[c] = 0.0f;
         if (coef64_out)
             coef64_out[c] = 0.0;
     }
-    if (n == 0)
+    if (n == 0) {
+        *S_eff_out = 0;
+        if (bounds_out)
+            bounds_out[0] = 0;
         return DRREF_OK;
+    }
 
     uint32_t *perm = (uint32_t *)malloc(sizeof(uint32_t) * n);
     double *xs = (double *)malloc(sizeof(double) * n);
     double *ys = (double *)malloc(sizeof(double) * n);
-    if (!perm || !xs || !ys) {
+    float *C = (float *)malloc(sizeof(float) * n);
+    uint64_t *bounds = (uint64_t *)malloc(sizeof(uint64_t) * ((size_t)S_cap + 1));
+    if (!perm || !xs || !ys || !C || !bounds) {
         free(perm);
         free(xs);
         free(ys);
+        free(C);
+        free(bounds);
         return DRREF_EINVAL;
     }
     int st = drref_sort_desc(V, n, perm);
+    uint32_t S_eff = 0;
+    if (st == DRREF_OK) {
+        for (uint64_t j = 0; j < n; ++j)
+            C[j] = V[perm[j]];
+        const uint32_t S_req = S ? S : drref_seg_heuristic(C, n, D);
+        st = drref_segment(C, n, D, S_req, mode, bounds, &S_eff);
+    }
+    *S_eff_out = S_eff;
+    if (bounds_out && st == DRREF_OK)
+        for (uint32_t s = 0; s <= S_eff; ++s)
+            bounds_out[s] = bounds[s];
     for (uint32_t s = 0; st == DRREF_OK && s < S_eff; ++s) {
-        uint64_t lo = seg_lo(s, n, S_eff), hi = seg_lo(s + 1, n, S_eff);
+        uint64_t lo = bounds[s], hi = bounds[s + 1];
         uint64_t ns = hi - lo;
         for (uint64_t j = 0; j < ns; ++j) {
             xs[j] = abscissa(j, ns);
             ys[j] = (double)V[perm[lo + j]];
         }
         double c[DRREF_MAX_DEG + 1];
+        /* a chord segment holds at least D+1 points; one of an equal-count
+         * split too, unless n < D+1, when D_eff = n-1 interpolates */
         st = drref_lsq_fit(xs, ys, ns, D_eff, c);
         for (uint32_t p = 0; st == DRREF_OK && p <= D_eff; ++p) {
             coef_out[(uint64_t)s * (D + 1) + p] = (float)c[p];
@@ -509,7 +681,19 @@ int drref_curvefit_encode(const float *V, uint64_t n, uint32_t D, uint32_t S, fl
     free(perm);
     free(xs);
     free(ys);
+    free(C);
+    free(bounds);
     return st;
+}
+
+int drref_curvefit_encode(const float *V, uint64_t n, uint32_t D, uint32_t S, float *coef_out,
+                          double *coef64_out, uint32_t *sigma_out, uint32_t *S_eff_out,
+                          uint32_t *D_eff_out, uint32_t *b_out)
+{
+    if (S < 1)
+        return DRREF_EINVAL;
+    return drref_curvefit_encode_seg(V, n, D, S, DRREF_SEG_EQUAL, coef_out, coef64_out, sigma_out, NULL,
+                                     S_eff_out, D_eff_out, b_out);
 }
 
 /* Read entry q of a packed b-bit stream. */
@@ -528,6 +712,40 @@ static uint64_t sigma_get(const uint32_t *sigma, uint64_t q, uint32_t b)
  * fp32 coefficients; round to fp32.  A rank outside [0, n) is an invalid
  * payload.
  */
+int drref_curvefit_decode_seg(const float *coef, const uint32_t *sigma, uint64_t n, uint32_t D, uint32_t S_eff,
+                              const uint64_t *bounds, float *vals_out)
+{
+    if ((!coef || !sigma || !vals_out || !bounds) && n)
+        return DRREF_EINVAL;
+    if (D > DRREF_MAX_DEG || (n && S_eff < 1))
+        return DRREF_EINVAL;
+    if (n == 0)
+        return DRREF_OK;
+    if (bounds[0] != 0 || bounds[S_eff] != n)
+        return DRREF_EINVAL;
+    for (uint32_t s = 0; s < S_eff; ++s)
+        if (bounds[s + 1] <= bounds[s])
+            return DRREF_EINVAL;
+    const uint32_t D_eff = n >= (uint64_t)D + 1 ? D : (uint32_t)(n - 1);
+    const uint32_t b = drref_sigma_bits(n);
+    for (uint64_t q = 0; q < n; ++q) {
+        const uint64_t rank = sigma_get(sigma, q, b);
+        if (rank >= n)
+            return DRREF_EINVAL;
+        uint32_t s = 0;
+        while (s + 1 < S_eff && bounds[s + 1] <= rank)
+            ++s;
+        const uint64_t lo = bounds[s], hi = bounds[s + 1];
+        const double t = abscissa(rank - lo, hi - lo);
+        const float *c = coef + (uint64_t)s * (D + 1);
+        double y = (double)c[D_eff];
+        for (int p = (int)D_eff - 1; p >= 0; --p)
+            y = y * t + (double)c[p];
+        vals_out[q] = (float)y;
+    }
+    return DRREF_OK;
+}
+
 int drref_curvefit_decode(const float *coef, const uint32_t *sigma, uint64_t n, uint32_t D, uint32_t S,
                           float *vals_out)
 {
