@@ -170,6 +170,9 @@ def main():
     ap.add_argument("--policy", type=int, default=0, help="index policy: 0 = P0 (no error), 1 = P1 (random r of P), "
                                                       "2/3/4 = leftmost/middle/rightmost r of P")
     ap.add_argument("--policy-seed", type=int, default=20210205, help="key of policy 1")
+    ap.add_argument("--segmentation", type=int, default=0, help="0 = equal-count runs, 1 = chord splits")
+    ap.add_argument("--n-seg", type=int, default=None, help="runs per tensor (0 = heuristic); default: the "
+                                                            "workload's")
     ap.add_argument("--decode-sum", type=int, default=0, metavar="N",
                     help="instead: time the summing receiver over N payloads of the workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -205,7 +208,7 @@ def main():
     g_host = W.generate(w)
     log(f"bench: generated input in {time.time() - t0:.1f}s sha256={W.sha256(g_host)[:16]}")
 
-    cfg = B.Config.from_workload(w, args.policy, args.policy_seed)
+    cfg = B.Config.from_workload(w, args.policy, args.policy_seed, args.segmentation, args.n_seg)
     total, rec_off = B.payload_layout(cfg)
     n_copies = max(1, min(64, math.ceil(3 * MALL_BYTES / max(1, 4 * d)))) if 4 * d < 2 * MALL_BYTES else 1
     g_dev = [torch.from_numpy(g_host).cuda()]
@@ -293,8 +296,8 @@ def main():
         elems = min(d, int(args.cpu_budget_s * 2.5e6))
         off = [o for o in w.offsets() if o < elems] + [elems]
         t0 = time.perf_counter()
-        oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, w.n_seg, policy=args.policy,
-                         seed=args.policy_seed)
+        oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, cfg.n_seg, policy=args.policy,
+                         seed=args.policy_seed, seg_mode=args.segmentation)
         tc = time.perf_counter() - t0
         sample = "full workload" if elems == d else f"first {elems} elements ({len(off) - 1} tensors) of the workload"
         cpu = {"value": round(elems / tc / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
@@ -316,7 +319,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "d": d, "tensors": w.n_tensors,
                    "ratio": None if w.ratio is None else f"{w.ratio[0]}/{w.ratio[1]}", "fpr": w.fpr,
-                   "degree": w.degree, "n_seg": w.n_seg, "policy": POLICY_NAMES[args.policy],
+                   "degree": w.degree, "n_seg": cfg.n_seg, "policy": POLICY_NAMES[args.policy],
+                   "segmentation": ["equal", "chord"][args.segmentation],
                    "input_copies": n_copies},
         "hbm_frac": round(b_alg / (ms * 1e-3) / HBM_PEAK, 4),
         "bytes_alg": int(b_alg),

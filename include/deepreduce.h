@@ -84,6 +84,22 @@ typedef enum {
 #define DR_POLICY_MIDDLE 3u
 #define DR_POLICY_RIGHTMOST 4u
 
+/* Segmentation of the sorted values into runs fitted separately (Section 5,
+ * "Piece-wise approximation").  EQUAL: runs of equal count (as in
+ * dr_curvefit_encode).  CHORD: the paper's split at the point farthest from
+ * the chord joining a run's end points: the values with the sign bit clear
+ * and the others start as two runs (when n_seg >= 2 and each has at least
+ * degree+1 values); then, while there are fewer than n_seg runs, the run
+ * whose farthest allowed point lies farthest from its chord (ties: the
+ * leftmost run) is split after that point, a split being allowed only where
+ * both parts keep at least degree+1 values; it stops early when no allowed
+ * point lies off its chord.  The distance |C[a] + m (i - a) - C[i]| with m =
+ * (C[z] - C[a]) / (z - a) (run [a, z], C the sorted values as doubles) is
+ * evaluated in double with one rounding per operation; ties to the smaller
+ * rank. */
+#define DR_SEG_EQUAL 0u
+#define DR_SEG_CHORD 1u
+
 /* Bits of the per-tensor flags word (slot 3 of counts_out). */
 #define DR_FLAG_NONFINITE 1u    /* the tensor held NaN or Inf */
 #define DR_FLAG_DEC_MISMATCH 2u /* receiver: the record is invalid, or its |P| differs from the header */
@@ -187,7 +203,12 @@ typedef struct {
     uint64_t ratio_den;        /*   ratio_num == DR_R_NONZERO selects every nonzero instead      */
     double fpr;                /* Bloom target false-positive rate, in (0, 1)                    */
     uint32_t degree;           /* polynomial degree per run, <= DR_MAX_DEGREE                    */
-    uint32_t n_seg;            /* runs per tensor, 1 .. DR_MAX_SEGMENTS                          */
+    uint32_t n_seg;            /* runs per tensor, 1 .. DR_MAX_SEGMENTS; 0: from the sorted values,
+                                  p + 1 runs with p = ceil(2 sqrt(M)) for degree >= 1 (Section 5,
+                                  after Lemma 1) or ceil(M / sqrt(2) - 1) for degree 0 (Remark 4),
+                                  M = |(C[0] - C[1]) - (C[n-2] - C[n-1])| in double, each ceiling
+                                  taken as the smallest p >= 0 with p^2 >= 4M, resp.
+                                  2 (p+1)^2 >= M^2; at most DR_MAX_SEGMENTS runs              */
     uint32_t policy;           /* DR_POLICY_*; the receiver takes it from each record's header   */
     uint32_t seed;             /* key of DR_POLICY_RANDOM (ignored by the others): positive q of
                                   P is coded iff pi(q) < r, as value number pi(q), where pi is a
@@ -195,17 +216,20 @@ typedef struct {
                                   words (h = max(1, ceil(ceil(log2 |P|) / 2))) whose round j
                                   XORs MurmurHash3_x86_32(LE half, seed + j) mod 2^h into the
                                   other half, restricted to [0, |P|) by cycle walking */
+    uint32_t segmentation;     /* DR_SEG_EQUAL or DR_SEG_CHORD                                   */
 } dr_config;
 
 /* Payload container (Figure 3's "container"): one record per tensor at byte
  * offset rec_off_h[t] (multiples of 256) of the payload buffer.  A record is
  * a 64-byte header followed by the filter words, the fp32 coefficients of
- * the S_eff x (D_eff+1) fitted polynomials, and the packed reorder map, each
- * section padded to 4 bytes and packed back to back.  Header layout: 16
- * little-endian u32 words: magic 0x31435244 ("DRC1"), header bytes (64), d,
- * n_selected, n_positives (|P|), n_values (values coded: |P| under P0),
- * m_bits, k, hash id (1 = MurmurHash3_x86_32), policy, seed, D_eff, S_eff,
- * sigma bits, record bytes (header + sections; what would be sent), 0.
+ * the S_eff x (D_eff+1) fitted polynomials, under DR_SEG_CHORD the S_eff - 1
+ * u32 starts of runs 1 .. S_eff-1 (sorted ranks, ascending), and the packed
+ * reorder map, each section padded to 4 bytes and packed back to back.
+ * Header layout: 16 little-endian u32 words: magic 0x31435244 ("DRC1"),
+ * header bytes (64), d, n_selected, n_positives (|P|), n_values (values
+ * coded: |P| under P0), m_bits, k, hash id (1 = MurmurHash3_x86_32), policy,
+ * seed, D_eff, S_eff, sigma bits, record bytes (header + sections; what
+ * would be sent), segmentation (DR_SEG_*).
  * Returns the total payload capacity in bytes; fills rec_off_h (nullable,
  * n_tensors+1 entries) with the record offsets and the end.  Returns 0 for
  * an invalid configuration. */

@@ -49,6 +49,7 @@ class DrConfig(ctypes.Structure):
         ("n_seg", ctypes.c_uint32),
         ("policy", ctypes.c_uint32),
         ("seed", ctypes.c_uint32),
+        ("segmentation", ctypes.c_uint32),
     ]
 
 
@@ -179,13 +180,15 @@ def curvefit_decode(coef, sigma, n_dev, n_cap: int, degree: int, n_seg: int, val
 class Config:
     """A dr_config together with the host offsets array it points to."""
 
-    def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int, policy: int = 0, seed: int = 0):
+    def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int, policy: int = 0, seed: int = 0,
+                 segmentation: int = 0):
         self.offsets = np.ascontiguousarray(np.asarray(offsets, dtype=np.uint64))
         self._off_c = (ctypes.c_uint64 * self.offsets.size)(*[int(x) for x in self.offsets])
         num, den = (R_NONZERO, 1) if ratio is None else ratio
-        self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg, policy, seed)
+        self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg, policy, seed,
+                          segmentation)
         self.ratio, self.fpr, self.degree, self.n_seg = ratio, fpr, degree, n_seg
-        self.policy, self.seed = policy, seed
+        self.policy, self.seed, self.segmentation = policy, seed, segmentation
 
     @property
     def n_tensors(self) -> int:
@@ -196,8 +199,9 @@ class Config:
         return int(self.offsets[-1])
 
     @classmethod
-    def from_workload(cls, w, policy: int = 0, seed: int = 0):
-        return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg, policy, seed)
+    def from_workload(cls, w, policy: int = 0, seed: int = 0, segmentation: int = 0, n_seg=None):
+        return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg if n_seg is None else n_seg, policy, seed,
+                   segmentation)
 
 
 def payload_layout(cfg: Config) -> tuple[int, list]:
@@ -269,8 +273,10 @@ class Record:
     seg_eff: int
     sigma_b: int
     rec_bytes: int
+    seg_mode: int
     bits: np.ndarray
     coef: np.ndarray
+    knots: np.ndarray  # starts of runs 1 .. S_eff-1 (chord segmentation), else empty
     sigma: np.ndarray
 
 
@@ -279,7 +285,7 @@ def parse_record(buf: bytes | np.ndarray, start: int) -> Record:
     b = np.asarray(buf, dtype=np.uint8)
     hdr = bytes(b[start:start + HEADER_BYTES])
     (magic, hbytes, d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb,
-     _reserved) = struct.unpack("<16I", hdr)
+     seg) = struct.unpack("<16I", hdr)
     if magic != HEADER_MAGIC or hbytes != HEADER_BYTES:
         raise ValueError(f"bad record header at {start}")
     at = start + HEADER_BYTES
@@ -288,6 +294,9 @@ def parse_record(buf: bytes | np.ndarray, start: int) -> Record:
     ncoef = se * (de + 1)
     coef = b[at: at + 4 * ncoef].view("<f4").copy()
     at += 4 * ncoef
+    nkn = se - 1 if seg == 1 and se > 1 else 0
+    knots = b[at: at + 4 * nkn].view("<u4").copy()
+    at += 4 * nkn
     nw = (n_v * sb + 31) // 32
     sigma = b[at: at + 4 * nw].view("<u4").copy()
-    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, bits, coef, sigma)
+    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, seg, bits, coef, knots, sigma)

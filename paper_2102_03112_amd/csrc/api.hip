@@ -19,6 +19,7 @@ using namespace dr;
 static_assert(POLICY_P0 == DR_POLICY_P0 && POLICY_RANDOM == DR_POLICY_RANDOM && POLICY_LEFTMOST == DR_POLICY_LEFTMOST &&
                   POLICY_MIDDLE == DR_POLICY_MIDDLE && POLICY_RIGHTMOST == DR_POLICY_RIGHTMOST,
               "index policy ids");
+static_assert(SEG_EQUAL == DR_SEG_EQUAL && SEG_CHORD == DR_SEG_CHORD, "segmentation ids");
 static_assert(MAX_SEG == DR_MAX_SEGMENTS && MAX_DEG == DR_MAX_DEGREE, "limits of the header and the kernels");
 
 namespace {
@@ -80,11 +81,11 @@ int persist_grid(int per_cu) { return dr::device_cus() * per_cu; }
 // entries (padded elements); the last six are contiguous so the Bloom insert
 // can borrow them for its position buffer before the value path needs them.
 struct Carve {
-    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0;
+    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0, bnd = 0;
     bool query_only = false;  // descriptors, tile counts, the positives bitmap and the tile table only
     size_t bytes = 0;
     size_t o_td, o_glob, o_done, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
-        o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs;
+        o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs, o_bnd;
 
     void plan() {
         size_t at = 0;
@@ -115,6 +116,7 @@ struct Carve {
         o_fit = take(all * 8ull * NMOM * fit_blocks);
         o_btab = take(all * 4 * btab);
         o_brow = take(all * 8 * bslices);
+        o_bnd = take(all * 4 * bnd);
         o_keyA = take(all * 4 * slots);
         o_keyB = take(all * 4 * slots);
         o_valA = take(all * 4 * slots);
@@ -161,6 +163,7 @@ struct Carve {
         w.sig = (uint32_t *)(ws + o_sig);
         w.vsorted = (float *)(ws + o_vs);
         w.bpos = (uint16_t *)(ws + o_keyA);  // borrows keyA .. vsorted
+        w.bounds = (uint32_t *)(ws + o_bnd);
         return w;
     }
 
@@ -181,6 +184,8 @@ Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     c.hist_blocks = c.ntiles / 16 + 2 * n_tensors;
     const uint64_t runs = n_tensors * (uint64_t)DR_MAX_SEGMENTS;
     c.fit_blocks = (runs < d + n_tensors ? runs : d + n_tensors) * FIT_CHUNKS;
+    // chord run starts: at most (runs + 1) per tensor
+    c.bnd = std::min<uint64_t>(n_tensors * (uint64_t)(DR_MAX_SEGMENTS + 1), d + 2 * n_tensors);
     // Bloom table: per tensor (slices x chunks) with at most MAX_CHUNKS
     // chunks and ceil(m / 2^14) slices, where m <= 47 n + 32 (k <= 32 gives
     // -ln(fpr) / (ln 2)^2 < 47 bits per item); plus one filter of MAX_SLICES
@@ -200,6 +205,7 @@ struct Plan {
     std::vector<uint64_t> bl_mcap;  // planned filter bits per tensor
     bool any_topr = false;
     bool direct = false;  // every filter small enough for the direct insert
+    bool segment = false; // some tensor needs the segmentation pass (chord, or the heuristic count)
     uint32_t dir_blocks = 0, dir_slices = 0;
 };
 
@@ -308,17 +314,26 @@ dr_status check_cfg(const dr_config *cfg) {
     }
     if (!(cfg->fpr > 0.0 && cfg->fpr < 1.0)) return fail(DR_EINVAL, "fpr must be in (0, 1)");
     if (cfg->degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
-    if (cfg->n_seg < 1 || cfg->n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
+    if (cfg->n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
+    if (cfg->segmentation > DR_SEG_CHORD) return fail(DR_EINVAL, "unknown segmentation %u", cfg->segmentation);
     if (cfg->policy > DR_POLICY_RIGHTMOST) return fail(DR_EINVAL, "unknown index policy %u", cfg->policy);
     return DR_OK;
 }
 
-uint64_t record_capacity(uint64_t d, uint64_t n_cap, double fpr, uint32_t degree, uint32_t nseg) {
+// Most runs a tensor of d elements can be fitted with: the requested count
+// (or, for the heuristic, the most segments), never more than one per D+1
+// values.
+uint64_t runs_cap(uint64_t d, uint32_t degree, uint32_t nseg) {
+    const uint64_t req = nseg ? nseg : (uint64_t)DR_MAX_SEGMENTS;
+    return std::min<uint64_t>(req, std::max<uint64_t>(1, d / (degree + 1)));
+}
+
+uint64_t record_capacity(uint64_t d, uint64_t n_cap, double fpr, uint32_t degree, uint64_t runs, bool knots) {
     uint64_t m = 0;
     uint32_t k = 0;
     bloom_params_host(n_cap, fpr, &m, &k);
     const uint64_t sig_words = ceil_div(d * sigma_bits_host(d ? d : 1), 32);
-    return HDR_BYTES + m / 8 + 4ull * nseg * (degree + 1) + 4 * sig_words;
+    return HDR_BYTES + m / 8 + 4ull * runs * (degree + 1) + (knots ? 4ull * runs : 0) + 4 * sig_words;
 }
 
 // The per-tensor plan of a round trip (sender and receiver use the same one).
@@ -334,7 +349,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     if (!bloom_params_host(1, cfg->fpr, &m_any, &k)) return fail(DR_EINVAL, "fpr gives more than 32 hashes");
     p.t.resize(T);
     rec_off.assign(T + 1, 0);
-    uint64_t tiles = 0, hist_blocks = 0, fit_blocks = 0;
+    uint64_t tiles = 0, hist_blocks = 0, fit_blocks = 0, bnd = 0;
     p.carve = Carve();
     uint64_t all_tiles = 0;
     for (uint64_t t = 0; t < T; ++t) {
@@ -367,12 +382,18 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.nseg = cfg->n_seg;
         in.policy = cfg->policy;
         in.seed = cfg->seed;
+        in.seg_mode = cfg->segmentation;
         in.mC = mC;
         // top-r: |S| = r is known, so the filter size is too
         in.m_words_in = nz ? 0u : (uint32_t)(m_cap / 32);
-        const uint64_t runs_cap = std::min<uint64_t>(cfg->n_seg, std::max<uint64_t>(1, d / (cfg->degree + 1)));
+        const uint64_t runs = runs_cap(d, cfg->degree, cfg->n_seg);
         in.fit_blk0 = (uint32_t)fit_blocks;
-        fit_blocks += runs_cap * FIT_CHUNKS;
+        fit_blocks += runs * FIT_CHUNKS;
+        if (cfg->segmentation == DR_SEG_CHORD) {
+            in.bnd0 = (uint32_t)bnd;
+            bnd += runs + 1;
+        }
+        p.segment |= cfg->segmentation == DR_SEG_CHORD || cfg->n_seg == 0;
         if (!nz) {
             in.hb0 = (uint32_t)hist_blocks;
             in.hbn = (uint32_t)ceil_div(in.ntiles, ht);
@@ -382,7 +403,9 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
             in.hbn = 0;
         }
         plan_bloom(in, n_cap, m_cap, true, p);
-        rec_off[t + 1] = rec_off[t] + align_up(record_capacity(d, n_cap, cfg->fpr, cfg->degree, cfg->n_seg), 256);
+        rec_off[t + 1] = rec_off[t] + align_up(record_capacity(d, n_cap, cfg->fpr, cfg->degree, runs,
+                                                               cfg->segmentation == DR_SEG_CHORD),
+                                               256);
     }
     p.any_topr = !nz;
     p.carve.ntensors = T;
@@ -390,6 +413,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     p.carve.slots = tiles * TILE;
     p.carve.hist_blocks = hist_blocks;
     p.carve.fit_blocks = fit_blocks;
+    p.carve.bnd = bnd;
     p.carve.plan();
     plan_bloom_rounds(p, k);
     plan_bloom_direct(p, true);
@@ -462,6 +486,7 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
     DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, true, counts_out, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
+    if (p.segment) DR_HIP(launch_segment(w, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;

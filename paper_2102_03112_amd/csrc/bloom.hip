@@ -431,8 +431,9 @@ struct QueryOut {
 struct RecordView {
     const uint32_t *bits;
     const float *coef;
+    const uint32_t *knots;  // chord segmentation: the seff - 1 interior run starts
     const uint32_t *sigma;
-    uint32_t m_bits, k, npos, nv, policy, seed, deff, seff, b;
+    uint32_t m_bits, k, npos, nv, policy, seed, deff, seff, b, segmode;
 };
 
 // Reads a record header and checks it against the record's capacity and
@@ -451,14 +452,16 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     v.deff = h[H_DEFF];
     v.seff = h[H_SEFF];
     v.b = h[H_B];
+    v.segmode = h[H_SEGMODE];
     v.bits = (const uint32_t *)(rec + HDR_BYTES);
     const uint32_t coef_off = HDR_BYTES + (v.m_bits / 32u) * 4u;
     v.coef = (const float *)(rec + coef_off);
-    const uint64_t need = (uint64_t)HDR_BYTES + m_bits / 8u + 4ull * v.seff * (v.deff + 1ull) +
+    const uint32_t nknots = v.segmode == SEG_CHORD && v.seff > 1 ? v.seff - 1 : 0u;
+    const uint64_t need = (uint64_t)HDR_BYTES + m_bits / 8u + 4ull * v.seff * (v.deff + 1ull) + 4ull * nknots +
                           4ull * (((uint64_t)v.nv * v.b + 31u) / 32u);
     *ok = h[H_MAGIC] == HDR_MAGIC && h[H_BYTES] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && v.k >= 1 &&
           v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && v.npos <= d && v.nv <= v.npos &&
-          v.policy <= POLICY_RIGHTMOST && (v.policy != POLICY_P0 || v.nv == v.npos) &&
+          v.policy <= POLICY_RIGHTMOST && (v.policy != POLICY_P0 || v.nv == v.npos) && v.segmode <= SEG_CHORD &&
           (v.nv == 0 || (v.seff >= 1 && v.seff <= v.nv && v.seff <= MAX_SEG && v.b >= sigma_bits(v.nv))) &&
           need <= cap;
     if (!*ok) {  // nothing of an invalid record is read past its first filter word
@@ -466,13 +469,15 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
         v.npos = 0;
         v.nv = 0;
         v.policy = POLICY_P0;
+        v.segmode = SEG_EQUAL;
         v.m_bits = 32;
         v.seff = 0;
         v.deff = 0;
         v.b = 1;
         v.coef = (const float *)(rec + HDR_BYTES + 4);
     }
-    v.sigma = (const uint32_t *)((const uint8_t *)v.coef + v.seff * (v.deff + 1u) * 4u);
+    v.knots = (const uint32_t *)((const uint8_t *)v.coef + v.seff * (v.deff + 1u) * 4u);
+    v.sigma = v.knots + (*ok ? nknots : 0u);
     return v;
 }
 
@@ -673,20 +678,28 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 
 // The received value of a positive whose value number is vn (NO_SLOT: not
 // coded, so 0): its run's polynomial at the abscissa of its sorted rank
-// sigma[vn].  A rank outside the record flags the tensor and reads as 0.
-__device__ __forceinline__ float positive_value(const RecordView &rv, const float *cf, bool staged, uint32_t vn,
-                                                TDesc &td, uint64_t *counts_out, uint32_t t) {
+// sigma[vn].  A rank outside the record, or run starts that do not bracket
+// it, flag the tensor and read as 0.  kn: the run starts of a chord-
+// segmented record (staged in LDS, or the record's own).
+__device__ __forceinline__ float positive_value(const RecordView &rv, const float *cf, const uint32_t *kn,
+                                                uint32_t vn, TDesc &td, uint64_t *counts_out, uint32_t t) {
     if (vn >= rv.nv) return 0.0f;
     const uint32_t rank = sigma_get(rv.sigma, (uint64_t)vn * rv.b, rv.b);
-    if (rank >= rv.nv) {
+    uint32_t s, lo, ns;
+    bool good = rank < rv.nv;
+    if (good) {
+        if (rv.segmode == SEG_CHORD)
+            good = run_of_rank_knots(kn, rank, rv.nv, rv.seff, &s, &lo, &ns);
+        else
+            run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);
+    }
+    if (!good) {
         atomicOr(&td.flags, FLAG_DEC_MISMATCH);
         if (counts_out) atomicOr((unsigned long long *)&counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
         return 0.0f;
     }
-    uint32_t s, lo, ns;
-    run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);
     const double tt = abscissa(rank - lo, ns);
-    return staged ? horner(cf + s * (rv.deff + 1u), rv.deff, tt) : horner(rv.coef + s * (rv.deff + 1u), rv.deff, tt);
+    return horner(cf + s * (rv.deff + 1u), rv.deff, tt);
 }
 
 // Emit pass: positives in ascending order at their tensor-wide ranks.
@@ -698,7 +711,27 @@ __device__ __forceinline__ float positive_value(const RecordView &rv, const floa
 //     coalesced; the receiver also stores each value into the dense output,
 //     which the probe pass has already zeroed.
 // The next tile's positives words are read before this tile's B and C run.
-constexpr uint32_t EMIT_COEF = 512;  // coefficients staged in LDS (else read from the payload)
+constexpr uint32_t EMIT_COEF = 512;   // coefficients staged in LDS (else read from the payload)
+constexpr uint32_t EMIT_KNOTS = 256;  // chord run starts staged in LDS (else read from the payload)
+
+// Stage a record's coefficients and run starts in LDS when they fit (the
+// caller synchronises before use); the pointers to read them from: LDS or
+// the record.
+__device__ __forceinline__ void stage_record(const RecordView &rv, float *cf, uint32_t *kn, const float **cf_use,
+                                             const uint32_t **kn_use) {
+    const uint32_t ncoef = rv.seff * (rv.deff + 1u);
+    const uint32_t nkn = rv.segmode == SEG_CHORD && rv.seff > 1 ? rv.seff - 1 : 0u;
+    *cf_use = rv.coef;
+    *kn_use = rv.knots;
+    if (ncoef <= EMIT_COEF) {
+        for (uint32_t x = threadIdx.x; x < ncoef; x += blockDim.x) cf[x] = rv.coef[x];
+        *cf_use = cf;
+    }
+    if (nkn <= EMIT_KNOTS) {
+        for (uint32_t x = threadIdx.x; x < nkn; x += blockDim.x) kn[x] = rv.knots[x];
+        *kn_use = kn;
+    }
+}
 
 template <int MODE>
 __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
@@ -707,8 +740,11 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     __shared__ uint32_t pre[TILE_WORDS];
     __shared__ uint32_t slot[TILE];  // A: local index of the positive of rank p; B: its value (receiver)
     __shared__ float cf[MODE == Q_DECODE ? EMIT_COEF : 1];
+    __shared__ uint32_t kn[MODE == Q_DECODE ? EMIT_KNOTS : 1];
     constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);  // 4 groups of 4 elements per thread
     uint32_t coef_t = 0xffffffffu;                     // tensor whose coefficients cf holds
+    const float *cfu = cf;                              // its coefficients: LDS or the record
+    const uint32_t *knu = kn;                           // its run starts: LDS or the record
     uint32_t tile = blockIdx.x;
     uint32_t word = 0, q0n = 0;
     if (tile < w.ntiles_total) {
@@ -731,7 +767,6 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             pre[threadIdx.x] = ex;
         }
         RecordView rv;
-        uint32_t ncoef = 0;
         // the policy's view of this tensor: positives, values coded, key
         uint32_t npos = 0, ncoded = 0, policy = POLICY_P0, pseed = 0;
         if (MODE == Q_ENCODE) {
@@ -743,14 +778,13 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
         if (MODE == Q_DECODE) {
             bool ok = true;
             rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
-            ncoef = rv.seff * (rv.deff + 1u);
             // the receiver's own positives, and the header's values count
             npos = td.nv_dec;
             ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
             policy = rv.policy;
             pseed = rv.seed;
-            if (t != coef_t && ncoef <= EMIT_COEF) {
-                for (uint32_t x = threadIdx.x; x < ncoef; x += NTHREADS) cf[x] = rv.coef[x];
+            if (t != coef_t) {
+                stage_record(rv, cf, kn, &cfu, &knu);
                 coef_t = t;
             }
         }
@@ -793,8 +827,8 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             } else if (MODE == Q_PLAIN) {
                 if (q < o.cap) o.idx_out[q] = i;
             } else {
-                const float y = positive_value(rv, cf, ncoef <= EMIT_COEF,
-                                               policy_slot(q, npos, ncoded, policy, pseed), td, o.counts_out, t);
+                const float y =
+                    positive_value(rv, cfu, knu, policy_slot(q, npos, ncoded, policy, pseed), td, o.counts_out, t);
                 o.dense_out[toff_el + i] = y;  // zeros elsewhere come from the probe pass
                 const uint64_t at = toff_el + q;
                 if (o.idx_out) o.idx_out[at] = i;
@@ -818,6 +852,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
     __shared__ uint16_t slot[TILE];
     __shared__ float acc[TILE];
     __shared__ float cf[EMIT_COEF];
+    __shared__ uint32_t kn[EMIT_KNOTS];
     constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);
     for (uint32_t tile = blockIdx.x; tile < o.ntiles1; tile += gridDim.x) {
         const uint32_t t = tensor_of_tile(w, tile);  // payload 0's descriptor of the tensor
@@ -833,7 +868,6 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
             const uint32_t q0 = w.toff[ptile];
             bool ok = true;
             const RecordView rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
-            const uint32_t ncoef = rv.seff * (rv.deff + 1u);
             const uint32_t npos = td.nv_dec;
             const uint32_t ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
             uint32_t tot;
@@ -842,8 +876,9 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
                 pw[threadIdx.x] = word;
                 pre[threadIdx.x] = ex;
             }
-            if (ncoef <= EMIT_COEF)
-                for (uint32_t x = threadIdx.x; x < ncoef; x += NTHREADS) cf[x] = rv.coef[x];
+            const float *cfu;
+            const uint32_t *knu;
+            stage_record(rv, cf, kn, &cfu, &knu);
             __syncthreads();
 #pragma unroll
             for (uint32_t u = 0; u < GROUPS; ++u) {
@@ -858,9 +893,9 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
             __syncthreads();
             for (uint32_t x = threadIdx.x; x < tot; x += NTHREADS) {
                 const uint32_t vn = policy_slot(q0 + x, npos, ncoded, rv.policy, rv.seed);
-                acc[slot[x]] += positive_value(rv, cf, ncoef <= EMIT_COEF, vn, td, o.counts_out, v);
+                acc[slot[x]] += positive_value(rv, cfu, knu, vn, td, o.counts_out, v);
             }
-            __syncthreads();  // pw, pre, slot and cf are rewritten by the next payload
+            __syncthreads();  // pw, pre, slot, cf and kn are rewritten by the next payload
         }
         // scale and store the tile
         float *dst = o.dense_out + toff_el + (uint64_t)lt * TILE;

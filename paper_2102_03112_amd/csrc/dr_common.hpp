@@ -41,12 +41,14 @@ constexpr uint32_t MAX_SEG = 4096;            // most runs per tensor
 // index policies (Section 4; Sections 10.4, 10.5)
 constexpr uint32_t POLICY_P0 = 0, POLICY_RANDOM = 1, POLICY_LEFTMOST = 2, POLICY_MIDDLE = 3, POLICY_RIGHTMOST = 4;
 constexpr uint32_t NO_SLOT = 0xffffffffu;
+// segmentation of the sorted values (Section 5)
+constexpr uint32_t SEG_EQUAL = 0, SEG_CHORD = 1;
 constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
 constexpr uint32_t HDR_BYTES = 64;
 // payload record header: sixteen little-endian u32 words
 enum HdrWord : uint32_t {
     H_MAGIC = 0, H_BYTES, H_D, H_NSEL, H_NPOS, H_NVAL, H_MBITS, H_K, H_HASH, H_POLICY, H_SEED, H_DEFF, H_SEFF, H_B,
-    H_RECBYTES, H_RESERVED
+    H_RECBYTES, H_SEGMODE
 };
 constexpr uint32_t HDR_MAGIC = 0x31435244u;   // "DRC1"
 
@@ -93,6 +95,8 @@ struct TInit {
     uint32_t dir_per;    // bitmap tiles (from the bitmap) or items (from a list) per chunk
     uint32_t policy;     // index policy (POLICY_*)
     uint32_t seed;       // key of the random policy
+    uint32_t seg_mode;   // SEG_EQUAL or SEG_CHORD (nseg == 0: the heuristic count)
+    uint32_t bnd0;       // chord segmentation: first segment-start entry of this tensor
 };
 
 // Per-tensor descriptor, in device memory.
@@ -182,6 +186,7 @@ struct Work {
     uint32_t *btab;           // Bloom insert: per (slice, chunk) counts, then offsets within the slice
     uint32_t *brow;           // Bloom insert: per reserved slice, its count; brow + bslices: its start
     uint32_t bslices;         // Bloom insert: reserved slices over all tensors
+    uint32_t *bounds;         // chord segmentation: segment starts (S_eff + 1 per tensor)
 };
 
 // ---------------------------------------------------------------------------
@@ -313,6 +318,28 @@ __device__ __forceinline__ void run_of_rank(uint32_t rank, uint32_t n, uint32_t 
     *s = r;
     *lo = a;
     *ns = b - a;
+}
+
+// Run of a sorted rank under chord segmentation: the runs start at 0 and at
+// the seff - 1 interior starts knots[0..seff-2] (ascending), and the last
+// ends at n.  Binary search for the last start <= rank; false if the starts
+// do not bracket the rank (a damaged record).
+__device__ __forceinline__ bool run_of_rank_knots(const uint32_t *knots, uint32_t rank, uint32_t n, uint32_t seff,
+                                                  uint32_t *s, uint32_t *lo, uint32_t *ns) {
+    uint32_t a = 0, b = seff;  // the run is in [a, b)
+    while (b - a > 1) {
+        const uint32_t mid = (a + b) >> 1;
+        if (knots[mid - 1] <= rank)
+            a = mid;
+        else
+            b = mid;
+    }
+    const uint32_t st = a ? knots[a - 1] : 0u;
+    const uint32_t en = a + 1 < seff ? knots[a] : n;
+    *s = a;
+    *lo = st;
+    *ns = en - st;
+    return st <= rank && rank < en;
 }
 
 // abscissa of local rank j in a run of ns points: (2j - (ns-1)) / (ns-1)

@@ -112,7 +112,7 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
                 h[H_SEFF] = seff;
                 h[H_B] = b;
                 h[H_RECBYTES] = rec_bytes;
-                h[H_RESERVED] = 0u;
+                h[H_SEGMODE] = td.in.seg_mode;
             }
         }
         uint32_t tot_t, tot_w, tot_v;
@@ -405,8 +405,274 @@ hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
+// Segmentation of the sorted values (Section 5, "Piece-wise approximation")
+// ---------------------------------------------------------------------------
+// One block per tensor, after the sort.  Equal-count runs need nothing here
+// unless their number comes from the heuristic.  Chord segmentation keeps
+// the run starts and each run's farthest allowed split point in LDS and
+// splits greedily; each split costs one block-wide arg-max over the two new
+// runs.  Distances are evaluated as in the oracle's definition, one
+// rounding per double operation (no contraction), so both take the same
+// decisions.
+constexpr uint32_t SEG_THREADS = 1024;
+constexpr uint32_t SEG_BATCH = 8;
+
+__device__ __forceinline__ double chord_dist(double ca, double m, uint32_t a, uint32_t i, float ci) {
+#pragma clang fp contract(off)
+    const double y = ca + m * (double)(i - a);
+    return fabs(y - (double)ci);
+}
+
+// farthest allowed split point of run [a, e) for degree D, block-wide; the
+// returned distance is 0 when no split is allowed (then *i_out is unset)
+__device__ double seg_candidate(const float *C, uint32_t a, uint32_t e, uint32_t D, uint32_t *i_out, double *rd,
+                                uint32_t *ri) {
+#pragma clang fp contract(off)
+    const uint32_t minpts = D + 1u;
+    double best = 0.0;
+    uint32_t bi = 0xffffffffu;
+    if (e - a >= 2u * minpts) {
+        const uint32_t z = e - 1u;
+        const double ca = (double)C[a];
+        const double m = ((double)C[z] - ca) / (double)(z - a);
+        const uint32_t i0 = a + D, i1 = z - D;  // split points [i0, i1)
+        // SEG_BATCH reads in flight per thread; each thread's points are
+        // visited in increasing order, so a strict compare keeps the
+        // smallest rank among equal distances
+        for (uint32_t ib = i0; ib < i1; ib += SEG_THREADS * SEG_BATCH) {
+            float v[SEG_BATCH];
+#pragma unroll
+            for (uint32_t u = 0; u < SEG_BATCH; ++u) {
+                const uint32_t i = ib + u * SEG_THREADS + threadIdx.x;
+                v[u] = i < i1 ? C[i] : 0.0f;
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < SEG_BATCH; ++u) {
+                const uint32_t i = ib + u * SEG_THREADS + threadIdx.x;
+                if (i < i1) {
+                    const double dd = chord_dist(ca, m, a, i, v[u]);
+                    if (dd > best) {
+                        best = dd;
+                        bi = i;
+                    }
+                }
+            }
+        }
+    }
+    // arg-max over the block: larger distance, then smaller rank
+    for (uint32_t off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_down(best, off);
+        const uint32_t oi = __shfl_down(bi, off);
+        if (od > best || (od == best && oi < bi)) {
+            best = od;
+            bi = oi;
+        }
+    }
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    __syncthreads();  // rd and ri are free
+    if (lane == 0) {
+        rd[wv] = best;
+        ri[wv] = bi;
+    }
+    __syncthreads();
+    best = rd[0];
+    bi = ri[0];
+    for (uint32_t q = 1; q < SEG_THREADS / 64; ++q)
+        if (rd[q] > best || (rd[q] == best && ri[q] < bi)) {
+            best = rd[q];
+            bi = ri[q];
+        }
+    if (best > 0.0) *i_out = bi;
+    return best;
+}
+
+// segments for the heuristic (p + 1 pieces): p = ceil(2 sqrt(M)) for degree
+// >= 1, ceil(M / sqrt(2) - 1) for degree 0, M from the first and last
+// differences of the sorted curve; each ceiling found by the smallest p with
+// p^2 >= 4M, resp. 2 (p+1)^2 >= M^2
+__device__ uint32_t seg_heuristic(const float *C, uint32_t n, uint32_t D) {
+#pragma clang fp contract(off)
+    double M = 0.0;
+    if (n >= 2) M = fabs(((double)C[0] - (double)C[1]) - ((double)C[n - 2] - (double)C[n - 1]));
+    uint32_t p = 0;
+    if (D == 0) {
+        const double M2 = M * M;
+        while (p + 1 < MAX_SEG && 2.0 * (double)(p + 1) * (double)(p + 1) < M2) ++p;
+    } else {
+        const double M4 = 4.0 * M;
+        while (p + 1 < MAX_SEG && (double)p * (double)p < M4) ++p;
+    }
+    return p + 1;
+}
+
+__global__ __launch_bounds__(SEG_THREADS) void k_segment(Work w) {
+    TDesc &td = w.td[blockIdx.x];
+    const bool chord = td.in.seg_mode == SEG_CHORD;
+    const uint32_t n = td.nv;
+    if ((!chord && td.in.nseg != 0) || n == 0) return;
+    __shared__ uint32_t st[MAX_SEG + 1];  // run starts, st[count] = n
+    __shared__ double cd[MAX_SEG];        // each run's farthest allowed split distance (0: none)
+    __shared__ uint32_t ci[MAX_SEG];      // and the rank that would end its left part
+    __shared__ double rd[SEG_THREADS / 64];
+    __shared__ uint32_t ri[SEG_THREADS / 64];
+    __shared__ uint32_t sh_req, sh_count, sh_pick;
+    const uint32_t D = td.in.degree;
+    const float *C = w.vsorted + td.in.slot;
+    if (threadIdx.x == 0) {
+        const uint32_t req = td.in.nseg ? td.in.nseg : seg_heuristic(C, n, D);
+        sh_req = req;
+        uint32_t count = 1;
+        st[0] = 0;
+        st[1] = n;
+        if (chord) {
+            // values with the sign bit clear come first in the sorted order
+            uint32_t lo = 0, hi = n;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if (!(__float_as_uint(C[mid]) >> 31))
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            if (req >= 2 && lo >= D + 1 && n - lo >= D + 1) {
+                st[1] = lo;
+                st[2] = n;
+                count = 2;
+            }
+        }
+        sh_count = count;
+    }
+    __syncthreads();
+    uint32_t count = sh_count;
+    const uint32_t req = sh_req;
+    if (chord) {
+        for (uint32_t k = 0; k < count; ++k) {
+            uint32_t i = 0;
+            const double dd = seg_candidate(C, st[k], st[k + 1], D, &i, rd, ri);
+            if (threadIdx.x == 0) {
+                cd[k] = dd;
+                ci[k] = i;
+            }
+        }
+        __syncthreads();
+        while (count < req) {
+            // the run to split: farthest candidate, then the leftmost run
+            double best = 0.0;
+            uint32_t bk = 0xffffffffu;
+            for (uint32_t k = threadIdx.x; k < count; k += SEG_THREADS)
+                if (cd[k] > best) {
+                    best = cd[k];
+                    bk = k;
+                }
+            for (uint32_t off = 32; off > 0; off >>= 1) {
+                const double od = __shfl_down(best, off);
+                const uint32_t ok = __shfl_down(bk, off);
+                if (od > best || (od == best && ok < bk)) {
+                    best = od;
+                    bk = ok;
+                }
+            }
+            const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+            if (lane == 0) {
+                rd[wv] = best;
+                ri[wv] = bk;
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                double b = rd[0];
+                uint32_t k = ri[0];
+                for (uint32_t q = 1; q < SEG_THREADS / 64; ++q)
+                    if (rd[q] > b || (rd[q] == b && ri[q] < k)) {
+                        b = rd[q];
+                        k = ri[q];
+                    }
+                sh_pick = b > 0.0 ? k : 0xffffffffu;
+            }
+            __syncthreads();
+            const uint32_t k = sh_pick;
+            if (k == 0xffffffffu) break;
+            // insert a start after run k: entries k+1..count move one place
+            // right, in chunks from the top so that no chunk reads what
+            // another has written
+            for (int64_t top = count; top >= (int64_t)k + 1; top -= SEG_THREADS) {
+                const int64_t xx = top - (int64_t)threadIdx.x;
+                const bool mv = xx >= (int64_t)k + 1;
+                uint32_t s_v = 0, c_i = 0;
+                double c_d = 0.0;
+                if (mv) {
+                    s_v = st[xx];
+                    if (xx < count) {
+                        c_d = cd[xx];
+                        c_i = ci[xx];
+                    }
+                }
+                __syncthreads();
+                if (mv) {
+                    st[xx + 1] = s_v;
+                    if (xx < count) {
+                        cd[xx + 1] = c_d;
+                        ci[xx + 1] = c_i;
+                    }
+                }
+                __syncthreads();
+            }
+            if (threadIdx.x == 0) st[k + 1] = ci[k] + 1u;
+            ++count;
+            __syncthreads();
+            for (uint32_t kk = k; kk <= k + 1; ++kk) {
+                uint32_t i = 0;
+                const double dd = seg_candidate(C, st[kk], st[kk + 1], D, &i, rd, ri);
+                if (threadIdx.x == 0) {
+                    cd[kk] = dd;
+                    ci[kk] = i;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // the record's layout now that the run count is known
+    const uint32_t deff = td.deff;
+    const uint32_t seff = chord ? count : (req < max(1u, n / (D + 1u)) ? req : max(1u, n / (D + 1u)));
+    const uint32_t nkn = chord && seff > 1 ? seff - 1 : 0u;
+    if (chord)
+        for (uint32_t x = threadIdx.x; x <= seff; x += SEG_THREADS) w.bounds[td.in.bnd0 + x] = st[x];
+    if (td.in.rec) {
+        const uint32_t kn_off = td.coef_off + 4u * seff * (deff + 1u);
+        uint32_t *kn = (uint32_t *)(td.in.rec + kn_off);
+        for (uint32_t x = threadIdx.x; x < nkn; x += SEG_THREADS) kn[x] = st[x + 1];
+        if (threadIdx.x == 0) {
+            td.seff = seff;
+            td.sigma_off = kn_off + 4u * nkn;
+            td.rec_bytes = td.sigma_off + 4u * td.swords;
+            uint32_t *h = (uint32_t *)td.in.rec;
+            h[H_SEFF] = seff;
+            h[H_RECBYTES] = td.rec_bytes;
+        }
+    } else if (threadIdx.x == 0) {
+        td.seff = seff;
+    }
+}
+
+hipError_t launch_segment(const Work &w, hipStream_t s) {
+    k_segment<<<w.ntensors, SEG_THREADS, 0, s>>>(w);
+    trace_mark(s, "k_segment");
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Least-squares fit of each run
 // ---------------------------------------------------------------------------
+// sorted ranks [lo, hi) of run s
+__device__ __forceinline__ void run_range(const Work &w, const TDesc &td, uint32_t s, uint64_t *lo, uint64_t *hi) {
+    if (td.in.seg_mode == SEG_CHORD) {
+        *lo = w.bounds[td.in.bnd0 + s];
+        *hi = w.bounds[td.in.bnd0 + s + 1];
+    } else {
+        const uint64_t nv = td.nv, S = td.seff;
+        *lo = s * nv / S;
+        *hi = (s + 1) * nv / S;
+    }
+}
 __device__ __forceinline__ uint32_t tensor_of_fit_block(const Work &w, uint32_t b) {
     uint32_t lo = 0, hi = w.ntensors;
     while (hi - lo > 1) {
@@ -489,8 +755,9 @@ __global__ __launch_bounds__(FIT_THREADS) void k_fit_moments(Work w) {
     const uint32_t local = blockIdx.x - td.in.fit_blk0;
     const uint32_t s = local / FIT_CHUNKS, ch = local % FIT_CHUNKS;
     if (s >= td.seff) return;
-    const uint64_t nv = td.nv, S = td.seff;
-    const uint64_t lo = s * nv / S, hi = (s + 1) * nv / S, ns = hi - lo;
+    uint64_t lo, hi;
+    run_range(w, td, s, &lo, &hi);
+    const uint64_t ns = hi - lo;
     const uint64_t j0 = ns * ch / FIT_CHUNKS, j1 = ns * (ch + 1) / FIT_CHUNKS;
     const float *y = w.vsorted + td.in.slot;
     double *out = w.fit_part + (uint64_t)blockIdx.x * NMOM;

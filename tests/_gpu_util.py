@@ -46,12 +46,17 @@ def coef_close(c_gpu: np.ndarray, c_ref64: np.ndarray, rows: int, stride: int, n
         assert err <= tol * max(scale, 1e-300), f"run {s}: |dc| {err:.3e} > {tol} * {scale:.3e}"
 
 
-def values_close(y_gpu: np.ndarray, y_ref: np.ndarray, ranks: np.ndarray, n: int, seff: int, tol: float = 1e-5):
-    """|dy_q| <= tol * max(|y_ref_q|, max |y_ref| over q's run)."""
+def values_close(y_gpu: np.ndarray, y_ref: np.ndarray, ranks: np.ndarray, n: int, seff: int, tol: float = 1e-5,
+                 bounds=None):
+    """|dy_q| <= tol * max(|y_ref_q|, max |y_ref| over q's run).  Runs are
+    of equal count, or start at `bounds` (chord segmentation)."""
     if n == 0:
         return
     ranks = ranks.astype(np.int64)
-    s = ((ranks + 1) * seff - 1) // n
+    if bounds is None:
+        s = ((ranks + 1) * seff - 1) // n
+    else:
+        s = np.searchsorted(np.asarray(bounds, np.int64), ranks, side="right") - 1
     run_max = np.zeros(seff)
     np.maximum.at(run_max, s, np.abs(y_ref.astype(np.float64)))
     bound = tol * np.maximum(np.abs(y_ref.astype(np.float64)), run_max[s])
@@ -78,15 +83,18 @@ def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     assert (rec.n_positives, rec.n_values) == (ref.P.size, ref.fit.n)
     assert (rec.m_bits, rec.k, rec.hash_id) == (ref.m, ref.k, 1)
     assert (rec.policy, rec.seed) == (ref.policy, ref.seed)
+    assert rec.seg_mode == ref.fit.seg_mode
+    if ref.fit.seg_mode == oracle.SEG_CHORD:
+        np.testing.assert_array_equal(rec.knots, ref.fit.bounds[1:-1].astype(np.uint32))
     assert (rec.seg_eff, rec.deg_eff, rec.sigma_b) == (ref.fit.S_eff, ref.fit.D_eff, ref.fit.b)
     np.testing.assert_array_equal(rec.bits, ref.bits)
     np.testing.assert_array_equal(rec.sigma, ref.fit.sigma)
     nc = ref.fit.D_eff + 1
     c_gpu = rec.coef.reshape(rec.seg_eff, nc) if rec.seg_eff else rec.coef
-    c_ref = ref.fit.coef64.reshape(n_seg, degree + 1)[: rec.seg_eff, :nc]
+    c_ref = ref.fit.coef64.reshape(n_seg or oracle.MAX_SEG, degree + 1)[: rec.seg_eff, :nc]
     coef_close(np.ascontiguousarray(c_gpu).ravel(), np.ascontiguousarray(c_ref).ravel(), rec.seg_eff, nc, nc)
     words = (ref.fit.n * ref.fit.b + 31) // 32
-    assert rec.rec_bytes == 64 + ref.m // 8 + 4 * rec.seg_eff * nc + 4 * words
+    assert rec.rec_bytes == 64 + ref.m // 8 + 4 * rec.seg_eff * nc + 4 * rec.knots.size + 4 * words
 
 
 _WS = {}
@@ -153,7 +161,8 @@ def check_roundtrip(g, cfg: B.Config, out, refs):
             y_ref[vn] = ref.vals[kept]
             # receiver values vs the oracle's own end-to-end reconstruction
             ranks = oracle.sigma_unpack(ref.fit.sigma, nc)
-            values_close(y_gpu, y_ref, ranks, nc, ref.fit.S_eff)
+            values_close(y_gpu, y_ref, ranks, nc, ref.fit.S_eff,
+                         bounds=ref.fit.bounds if ref.fit.seg_mode == oracle.SEG_CHORD else None)
         dense = out["dense"][a:b]
         pos = ref.P_dec.astype(np.int64)
         np.testing.assert_array_equal(dense[pos], out["val"][a: a + nv])

@@ -90,12 +90,12 @@ def test_workspace_bound_grows_with_size(L):
 FAKE = ctypes.c_void_p(1 << 20)
 
 
-def _cfg(offsets=(0, 1000), ratio=(1, 100), fpr=1e-3, degree=5, n_seg=8, policy=0):
-    return B.Config(list(offsets), ratio, fpr, degree, n_seg, policy)
+def _cfg(offsets=(0, 1000), ratio=(1, 100), fpr=1e-3, degree=5, n_seg=8, policy=0, segmentation=0):
+    return B.Config(list(offsets), ratio, fpr, degree, n_seg, policy, 0, segmentation)
 
 
 @pytest.mark.parametrize("bad", [
-    dict(fpr=0.0), dict(fpr=1.0), dict(degree=8), dict(n_seg=0), dict(n_seg=5000),
+    dict(fpr=0.0), dict(fpr=1.0), dict(degree=8), dict(n_seg=5000), dict(segmentation=2),
     dict(ratio=(2, 1)), dict(ratio=(1, 0)), dict(offsets=(0, 10, 5)), dict(offsets=(1, 10)),
     dict(offsets=(0, 1 << 32)), dict(policy=5),
 ])

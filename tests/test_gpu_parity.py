@@ -259,6 +259,38 @@ def test_roundtrip_policy_parity(name, policy):
     check_roundtrip(g, cfg, out, refs)
 
 
+SEG_CASES = {
+    # name: (g, offsets, ratio, fpr, D, S, segmentation)
+    "resnet20_chord8": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 8, oracle.SEG_CHORD),
+    "laplace_chord16_d1": (W.generate(W.Workload("t", 300_000, 1, (1, 100), 1e-3, 1, 16, "laplace_5e-4", 13)),
+                           [0, 300_000], (1, 100), 1e-3, 1, 16, oracle.SEG_CHORD),
+    "ragged_chord8": (W.normal(8203, 8), [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8,
+                      oracle.SEG_CHORD),
+    "support_chord_auto_d0": (W.sparse_normal(50_000, 7, 0.4, scale=40.0), [0, 50_000], None, 1e-4, 0, 0,
+                              oracle.SEG_CHORD),
+    "normal_equal_auto_d1": (W.normal(200_000, 21, scale=3.0), [0, 200_000], (1, 100), 1e-3, 1, 0,
+                             oracle.SEG_EQUAL),
+    "normal_chord_auto_d1": (W.normal(200_000, 21, scale=3.0), [0, 200_000], (1, 100), 1e-3, 1, 0,
+                             oracle.SEG_CHORD),
+    "many_runs_chord": (W.normal(400_000, 22, scale=1e-3), [0, 400_000], (1, 10), 1e-3, 1, 3000,
+                        oracle.SEG_CHORD),
+}
+
+
+@pytest.mark.parametrize("name", list(SEG_CASES))
+def test_roundtrip_segmentation_parity(name):
+    """Chord segmentation and the heuristic run count (Section 5): the same
+    run starts (bit-exact) and values as the oracle."""
+    g, off, ratio, fpr, D, S, seg = SEG_CASES[name]
+    log(f"roundtrip {name} d={g.size} D={D} S={S} seg={seg}")
+    cfg = B.Config(off, ratio, fpr, D, S, 0, 0, seg)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, D, S, seg_mode=seg)
+    check_roundtrip(g, cfg, out, refs)
+    if seg == oracle.SEG_CHORD:
+        assert any(r.fit.S_eff > 1 for r in refs)
+
+
 def test_receiver_takes_the_policy_from_the_record():
     """The receiver reads policy and key from each record's header, not from
     its own configuration."""
