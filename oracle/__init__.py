@@ -32,6 +32,8 @@ NO_SLOT = 0xFFFFFFFF
 # segmentation of the sorted values (Section 5)
 SEG_EQUAL, SEG_CHORD = 0, 1
 MAX_SEG = 4096
+# value models (Section 5): polynomial, double exponential
+FIT_POLY, FIT_DEXP = 0, 1
 
 
 class OracleError(RuntimeError):
@@ -79,6 +81,12 @@ def _load():
             [f32p, u64, u32, u32, u32, f32p, f64p, u32p, u64p, u32p, u32p, u32p],
         ),
         "drref_curvefit_decode_seg": (ctypes.c_int, [f32p, u32p, u64, u32, u32, u64p, f32p]),
+        "drref_curvefit_encode_ex": (
+            ctypes.c_int,
+            [f32p, u64, u32, u32, u32, u32, f32p, f64p, u32p, u64p, u32p, u32p, u32p, u32p],
+        ),
+        "drref_curvefit_decode_ex": (ctypes.c_int, [f32p, u32p, u64, u32, u32, u64p, u32, f32p]),
+        "drref_dexp_fit": (ctypes.c_int, [f64p, f64p, u64, f64p, f64p]),
         "drref_perm": (u32, [u32, u64, u32]),
         "drref_policy_slots": (ctypes.c_int, [u64, u64, u32, u32, u32p, u64p]),
     }
@@ -245,33 +253,51 @@ class FitPayload:
     b: int
     seg_mode: int = SEG_EQUAL
     bounds: np.ndarray = None  # segment starts, S_eff + 1 entries (last = n)
+    model: int = FIT_POLY  # the model used (a DEXP request on fewer than 4 values gives POLY)
 
 
-def curvefit_encode(V: np.ndarray, degree: int, n_seg: int, seg_mode: int = SEG_EQUAL) -> FitPayload:
+def curvefit_encode(V: np.ndarray, degree: int, n_seg: int, seg_mode: int = SEG_EQUAL,
+                    model: int = FIT_POLY) -> FitPayload:
     """Sort, segment, fit, and pack the reorder map (Sections 5 and 5.1).
     ``n_seg`` = 0 asks for the heuristic number of segments; ``seg_mode``
-    chooses equal-count or chord segmentation (Section 5).  The coefficient
-    rows are n_seg (MAX_SEG for the heuristic) of degree+1."""
+    chooses equal-count or chord segmentation (Section 5); ``model`` the
+    polynomial or the double exponential (degree taken as 3: rows (a, b, c,
+    d)).  The coefficient rows are n_seg (MAX_SEG for the heuristic) of
+    degree+1."""
     lib = _load()
     V = np.ascontiguousarray(V, dtype=np.float32)
     n = V.size
+    if model == FIT_DEXP:
+        degree = 3
     cap = n_seg if n_seg else MAX_SEG
     coef = np.zeros(cap * (degree + 1), dtype=np.float32)
     coef64 = np.zeros(cap * (degree + 1), dtype=np.float64)
     sigma = np.zeros(max(sigma_words(n), 1), dtype=np.uint32)
     bounds = np.zeros(cap + 1, dtype=np.uint64)
-    se, de, b = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
+    se, de, b, mo = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
     _check(
-        lib.drref_curvefit_encode_seg(
-            _ptr(V, ctypes.c_float), n, degree, n_seg, seg_mode, _ptr(coef, ctypes.c_float),
+        lib.drref_curvefit_encode_ex(
+            _ptr(V, ctypes.c_float), n, degree, n_seg, seg_mode, model, _ptr(coef, ctypes.c_float),
             _ptr(coef64, ctypes.c_double), _ptr(sigma, ctypes.c_uint32), _ptr(bounds, ctypes.c_uint64),
-            ctypes.byref(se), ctypes.byref(de), ctypes.byref(b),
+            ctypes.byref(se), ctypes.byref(de), ctypes.byref(b), ctypes.byref(mo),
         ),
         "curvefit_encode",
     )
     S_eff = int(se.value)
     return FitPayload(coef, coef64, sigma[: sigma_words(n)], n, degree, n_seg, S_eff, int(de.value), int(b.value),
-                      seg_mode, bounds[: S_eff + 1].copy())
+                      seg_mode, bounds[: S_eff + 1].copy(), int(mo.value))
+
+
+def dexp_fit(t: np.ndarray, y: np.ndarray) -> tuple[np.ndarray, float]:
+    """(a, b, c, d) of the least-squares fit y ~ a e^(bt) + c e^(dt), and its
+    residual sum of squares."""
+    t = np.ascontiguousarray(t, dtype=np.float64)
+    y = np.ascontiguousarray(y, dtype=np.float64)
+    th = np.zeros(4)
+    rss = ctypes.c_double()
+    _check(_load().drref_dexp_fit(_ptr(t, ctypes.c_double), _ptr(y, ctypes.c_double), t.size,
+                                  _ptr(th, ctypes.c_double), ctypes.byref(rss)), "dexp_fit")
+    return th, float(rss.value)
 
 
 def segment(C: np.ndarray, degree: int, n_seg: int, seg_mode: int) -> np.ndarray:
@@ -290,7 +316,8 @@ def seg_heuristic(C: np.ndarray, degree: int) -> int:
     return int(_load().drref_seg_heuristic(_ptr(C, ctypes.c_float), C.size, degree))
 
 
-def curvefit_decode_seg(coef: np.ndarray, sigma: np.ndarray, n: int, degree: int, bounds: np.ndarray) -> np.ndarray:
+def curvefit_decode_seg(coef: np.ndarray, sigma: np.ndarray, n: int, degree: int, bounds: np.ndarray,
+                        model: int = FIT_POLY) -> np.ndarray:
     """Reconstruct n values from coefficients, reorder map and segment starts."""
     lib = _load()
     coef = np.ascontiguousarray(coef, dtype=np.float32)
@@ -299,9 +326,9 @@ def curvefit_decode_seg(coef: np.ndarray, sigma: np.ndarray, n: int, degree: int
         sigma = np.zeros(1, dtype=np.uint32)
     bounds = np.ascontiguousarray(bounds, dtype=np.uint64)
     out = np.empty(max(n, 1), dtype=np.float32)
-    _check(lib.drref_curvefit_decode_seg(_ptr(coef, ctypes.c_float), _ptr(sigma, ctypes.c_uint32), n, degree,
-                                         max(bounds.size - 1, 0), _ptr(bounds, ctypes.c_uint64),
-                                         _ptr(out, ctypes.c_float)), "curvefit_decode_seg")
+    _check(lib.drref_curvefit_decode_ex(_ptr(coef, ctypes.c_float), _ptr(sigma, ctypes.c_uint32), n, degree,
+                                        max(bounds.size - 1, 0), _ptr(bounds, ctypes.c_uint64), model,
+                                        _ptr(out, ctypes.c_float)), "curvefit_decode_seg")
     return out[:n]
 
 
@@ -384,7 +411,8 @@ class TensorResult:
 
 
 def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
-                     policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL) -> TensorResult:
+                     policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL,
+                     model: int = FIT_POLY) -> TensorResult:
     """Sender: top-r (or support) -> Bloom insert -> full-range query (P) ->
     the policy keeps all of P (P0) or r of it -> V = g at the kept positives
     (values from the dense gradient, Section 4) -> curve-fit encode.
@@ -401,11 +429,11 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     kept = slots != NO_SLOT
     V = np.zeros(ncoded, dtype=np.float32)
     V[slots[kept].astype(np.int64)] = g[P[kept].astype(np.int64)]
-    fit = curvefit_encode(V, degree, n_seg, seg_mode)
+    fit = curvefit_encode(V, degree, n_seg, seg_mode, model)
     # receiver: its own query and the same policy over its own positives
     P_dec = bloom_query(bits, m, k, d)
     slots_dec, nc_dec = policy_slots(P_dec.size, ncoded, policy, seed)
-    y = curvefit_decode_seg(fit.coef, fit.sigma, nc_dec, degree, fit.bounds)
+    y = curvefit_decode_seg(fit.coef, fit.sigma, nc_dec, fit.degree, fit.bounds, fit.model)
     vals = np.zeros(P_dec.size, dtype=np.float32)
     keep_dec = slots_dec != NO_SLOT
     vals[keep_dec] = y[slots_dec[keep_dec].astype(np.int64)]
@@ -417,7 +445,7 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
 
 
 def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
-              policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL):
+              policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL, model: int = FIT_POLY):
     """Code every tensor g[offsets[t]:offsets[t+1]] independently on local
     indices.  ``ratio`` is (num, den) for top-r with r = ceil(d_t num / den),
     or None for the support of an inherently sparse gradient."""
@@ -425,7 +453,7 @@ def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int
     for t in range(len(offsets) - 1):
         gt = g[offsets[t]: offsets[t + 1]]
         r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
-        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed, seg_mode))
+        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed, seg_mode, model))
     return out
 
 

@@ -438,6 +438,151 @@ uint64_t drref_sigma_words(uint64_t n)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Double-exponential value fit (Section 5, "Nonlinear regression").        */
+/* ------------------------------------------------------------------------ */
+
+#define DRREF_DEXP_ITERS 40
+#define DRREF_DEXP_RATE_MAX 40.0
+
+/* Solve the n x n system A x = rhs (n <= 4) by Gaussian elimination with
+ * partial pivoting; nonzero if a pivot is zero. */
+static int solve_small(int n, double A[4][5], double *x)
+{
+    for (int col = 0; col < n; ++col) {
+        int piv = col;
+        for (int row = col + 1; row < n; ++row)
+            if (fabs(A[row][col]) > fabs(A[piv][col]))
+                piv = row;
+        if (A[piv][col] == 0.0)
+            return 1;
+        if (piv != col)
+            for (int c = 0; c <= n; ++c) {
+                double t = A[col][c];
+                A[col][c] = A[piv][c];
+                A[piv][c] = t;
+            }
+        for (int row = col + 1; row < n; ++row) {
+            double f = A[row][col] / A[col][col];
+            for (int c = col; c <= n; ++c)
+                A[row][c] -= f * A[col][c];
+        }
+    }
+    for (int p = n - 1; p >= 0; --p) {
+        double s = A[p][n];
+        for (int q = p + 1; q < n; ++q)
+            s -= A[p][q] * x[q];
+        x[p] = s / A[p][p];
+    }
+    return 0;
+}
+
+/*
+ * Sums of one pass over the points for y ~ a e^(b t) + c e^(d t): the upper
+ * triangle of J^T J (row-major: 00 01 02 03 11 12 13 22 23 33), J^T r and
+ * r^T r, with J = [e^(bt), a t e^(bt), e^(dt), c t e^(dt)] and r = y - model,
+ * accumulated in double in increasing j.
+ */
+static void dexp_sums(const double *t, const double *y, uint64_t n, const double th[4], double s[15])
+{
+    for (int e = 0; e < 15; ++e)
+        s[e] = 0.0;
+    for (uint64_t j = 0; j < n; ++j) {
+        const double eb = exp(th[1] * t[j]), ed = exp(th[3] * t[j]);
+        const double J[4] = {eb, th[0] * t[j] * eb, ed, th[2] * t[j] * ed};
+        const double r = y[j] - (th[0] * eb + th[2] * ed);
+        int e = 0;
+        for (int p = 0; p < 4; ++p)
+            for (int q = p; q < 4; ++q)
+                s[e++] += J[p] * J[q];
+        for (int p = 0; p < 4; ++p)
+            s[10 + p] += J[p] * r;
+        s[14] += r * r;
+    }
+}
+
+/*
+ * Least-squares fit of y_j ~ a e^(b t_j) + c e^(d t_j) over n >= 4 points
+ * (Section 5 names the model; its fitting method is not given).  Steps:
+ *  1. start from rates b = 1, d = -1 and the amplitudes (a, c) that solve
+ *     the 2 x 2 linear least-squares problem for those rates (a = mean y,
+ *     c = 0 if it is singular);
+ *  2. DRREF_DEXP_ITERS Levenberg-Marquardt steps: solve
+ *     (J^T J + lambda diag(J^T J)) delta = J^T r, clamp the rates of
+ *     theta + delta to [-40, 40], and keep the trial point if its residual
+ *     sum of squares is smaller (lambda /= 10), else keep theta (lambda *=
+ *     10); lambda starts at 1e-3 and a singular system counts as a reject.
+ * theta_out = (a, b, c, d); *rss_out = the final residual sum of squares.
+ */
+int drref_dexp_fit(const double *t, const double *y, uint64_t n, double *theta_out, double *rss_out)
+{
+    if (!t || !y || !theta_out || n < 4)
+        return DRREF_EINVAL;
+    double th[4] = {0.0, 1.0, 0.0, -1.0};
+    {
+        double s11 = 0, s12 = 0, s22 = 0, sy1 = 0, sy2 = 0, sy = 0;
+        for (uint64_t j = 0; j < n; ++j) {
+            const double e1 = exp(t[j]), e2 = exp(-t[j]);
+            s11 += e1 * e1;
+            s12 += e1 * e2;
+            s22 += e2 * e2;
+            sy1 += y[j] * e1;
+            sy2 += y[j] * e2;
+            sy += y[j];
+        }
+        const double det = s11 * s22 - s12 * s12;
+        if (det != 0.0) {
+            th[0] = (sy1 * s22 - sy2 * s12) / det;
+            th[2] = (sy2 * s11 - sy1 * s12) / det;
+        } else {
+            th[0] = sy / (double)n;
+        }
+    }
+    double s[15], st[15];
+    dexp_sums(t, y, n, th, s);
+    double lambda = 1e-3;
+    for (int it = 0; it < DRREF_DEXP_ITERS; ++it) {
+        double A[4][5];
+        int e = 0;
+        for (int p = 0; p < 4; ++p)
+            for (int q = p; q < 4; ++q) {
+                A[p][q] = s[e];
+                A[q][p] = s[e];
+                ++e;
+            }
+        for (int p = 0; p < 4; ++p) {
+            A[p][p] += lambda * A[p][p];
+            A[p][4] = s[10 + p];
+        }
+        double delta[4];
+        if (solve_small(4, A, delta)) {
+            lambda *= 10.0;
+            continue;
+        }
+        double tt[4];
+        for (int p = 0; p < 4; ++p)
+            tt[p] = th[p] + delta[p];
+        for (int p = 1; p < 4; p += 2)
+            tt[p] = tt[p] > DRREF_DEXP_RATE_MAX ? DRREF_DEXP_RATE_MAX
+                                                : (tt[p] < -DRREF_DEXP_RATE_MAX ? -DRREF_DEXP_RATE_MAX : tt[p]);
+        dexp_sums(t, y, n, tt, st);
+        if (st[14] < s[14]) {
+            for (int p = 0; p < 4; ++p)
+                th[p] = tt[p];
+            for (int q = 0; q < 15; ++q)
+                s[q] = st[q];
+            lambda /= 10.0;
+        } else {
+            lambda *= 10.0;
+        }
+    }
+    for (int p = 0; p < 4; ++p)
+        theta_out[p] = th[p];
+    if (rss_out)
+        *rss_out = s[14];
+    return DRREF_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Adaptive segmentation (Section 5, "Piece-wise approximation") and the    */
 /* number of pieces (Section 5 after Lemma 1; Remark 4 of Section 10).     */
 /* ------------------------------------------------------------------------ */
@@ -597,9 +742,44 @@ uint32_t drref_seg_heuristic(const float *C, uint64_t n, uint32_t D)
  * S_cap = (S ? S : DRREF_MAX_SEG) rows; bounds_out (optional) S_cap + 1
  * segment starts.
  */
+#define DRREF_FIT_POLY 0u
+#define DRREF_FIT_DEXP 1u
+
+static int curvefit_encode_impl(const float *V, uint64_t n, uint32_t D, uint32_t S, uint32_t mode, uint32_t model,
+                                float *coef_out, double *coef64_out, uint32_t *sigma_out, uint64_t *bounds_out,
+                                uint32_t *S_eff_out, uint32_t *D_eff_out, uint32_t *b_out);
+
+/*
+ * The general value encoder: model DRREF_FIT_POLY (polynomials of degree D)
+ * or DRREF_FIT_DEXP (a e^(bt) + c e^(dt) per run, coefficient row (a, b, c,
+ * d); D is taken as 3, the four parameters needing at least four points per
+ * run).  A DEXP tensor of fewer than four values is coded as the polynomial
+ * through them; *model_out reports the model used.
+ */
+int drref_curvefit_encode_ex(const float *V, uint64_t n, uint32_t D, uint32_t S, uint32_t mode, uint32_t model,
+                             float *coef_out, double *coef64_out, uint32_t *sigma_out, uint64_t *bounds_out,
+                             uint32_t *S_eff_out, uint32_t *D_eff_out, uint32_t *b_out, uint32_t *model_out)
+{
+    if (model > DRREF_FIT_DEXP || !model_out)
+        return DRREF_EINVAL;
+    if (model == DRREF_FIT_DEXP)
+        D = 3;
+    *model_out = (model == DRREF_FIT_DEXP && n >= 4) ? DRREF_FIT_DEXP : DRREF_FIT_POLY;
+    return curvefit_encode_impl(V, n, D, S, mode, *model_out, coef_out, coef64_out, sigma_out, bounds_out,
+                                S_eff_out, D_eff_out, b_out);
+}
+
 int drref_curvefit_encode_seg(const float *V, uint64_t n, uint32_t D, uint32_t S, uint32_t mode,
                               float *coef_out, double *coef64_out, uint32_t *sigma_out, uint64_t *bounds_out,
                               uint32_t *S_eff_out, uint32_t *D_eff_out, uint32_t *b_out)
+{
+    return curvefit_encode_impl(V, n, D, S, mode, DRREF_FIT_POLY, coef_out, coef64_out, sigma_out, bounds_out,
+                                S_eff_out, D_eff_out, b_out);
+}
+
+static int curvefit_encode_impl(const float *V, uint64_t n, uint32_t D, uint32_t S, uint32_t mode, uint32_t model,
+                                float *coef_out, double *coef64_out, uint32_t *sigma_out, uint64_t *bounds_out,
+                                uint32_t *S_eff_out, uint32_t *D_eff_out, uint32_t *b_out)
 {
     if ((!V && n) || D > DRREF_MAX_DEG || S > DRREF_MAX_SEG || mode > DRREF_SEG_CHORD || !coef_out ||
         (!sigma_out && n) || !S_eff_out || !D_eff_out || !b_out)
@@ -659,7 +839,10 @@ int drref_curvefit_encode_seg(const float *V, uint64_t n, uint32_t D, uint32_t S
         double c[DRREF_MAX_DEG + 1];
         /* a chord segment holds at least D+1 points; one of an equal-count
          * split too, unless n < D+1, when D_eff = n-1 interpolates */
-        st = drref_lsq_fit(xs, ys, ns, D_eff, c);
+        if (model == DRREF_FIT_DEXP)
+            st = drref_dexp_fit(xs, ys, ns, c, NULL);
+        else
+            st = drref_lsq_fit(xs, ys, ns, D_eff, c);
         for (uint32_t p = 0; st == DRREF_OK && p <= D_eff; ++p) {
             coef_out[(uint64_t)s * (D + 1) + p] = (float)c[p];
             if (coef64_out)
@@ -712,9 +895,25 @@ static uint64_t sigma_get(const uint32_t *sigma, uint64_t q, uint32_t b)
  * fp32 coefficients; round to fp32.  A rank outside [0, n) is an invalid
  * payload.
  */
+int drref_curvefit_decode_ex(const float *coef, const uint32_t *sigma, uint64_t n, uint32_t D, uint32_t S_eff,
+                             const uint64_t *bounds, uint32_t model, float *vals_out);
+
 int drref_curvefit_decode_seg(const float *coef, const uint32_t *sigma, uint64_t n, uint32_t D, uint32_t S_eff,
                               const uint64_t *bounds, float *vals_out)
 {
+    return drref_curvefit_decode_ex(coef, sigma, n, D, S_eff, bounds, DRREF_FIT_POLY, vals_out);
+}
+
+/*
+ * Decoder for either model: a DEXP run's value at abscissa t is
+ * a e^(b t) + c e^(d t) in double on the fp32 row (a, b, c, d), rounded to
+ * fp32 (D is 3 for DEXP records).
+ */
+int drref_curvefit_decode_ex(const float *coef, const uint32_t *sigma, uint64_t n, uint32_t D, uint32_t S_eff,
+                             const uint64_t *bounds, uint32_t model, float *vals_out)
+{
+    if (model > DRREF_FIT_DEXP)
+        return DRREF_EINVAL;
     if ((!coef || !sigma || !vals_out || !bounds) && n)
         return DRREF_EINVAL;
     if (D > DRREF_MAX_DEG || (n && S_eff < 1))
@@ -738,9 +937,14 @@ int drref_curvefit_decode_seg(const float *coef, const uint32_t *sigma, uint64_t
         const uint64_t lo = bounds[s], hi = bounds[s + 1];
         const double t = abscissa(rank - lo, hi - lo);
         const float *c = coef + (uint64_t)s * (D + 1);
-        double y = (double)c[D_eff];
-        for (int p = (int)D_eff - 1; p >= 0; --p)
-            y = y * t + (double)c[p];
+        double y;
+        if (model == DRREF_FIT_DEXP) {
+            y = (double)c[0] * exp((double)c[1] * t) + (double)c[2] * exp((double)c[3] * t);
+        } else {
+            y = (double)c[D_eff];
+            for (int p = (int)D_eff - 1; p >= 0; --p)
+                y = y * t + (double)c[p];
+        }
         vals_out[q] = (float)y;
     }
     return DRREF_OK;
