@@ -171,6 +171,7 @@ def main():
                                                       "2/3/4 = leftmost/middle/rightmost r of P")
     ap.add_argument("--policy-seed", type=int, default=20210205, help="key of policy 1")
     ap.add_argument("--segmentation", type=int, default=0, help="0 = equal-count runs, 1 = chord splits")
+    ap.add_argument("--fit-model", type=int, default=0, help="0 = polynomial, 1 = double exponential")
     ap.add_argument("--n-seg", type=int, default=None, help="runs per tensor (0 = heuristic); default: the "
                                                             "workload's")
     ap.add_argument("--decode-sum", type=int, default=0, metavar="N",
@@ -208,7 +209,7 @@ def main():
     g_host = W.generate(w)
     log(f"bench: generated input in {time.time() - t0:.1f}s sha256={W.sha256(g_host)[:16]}")
 
-    cfg = B.Config.from_workload(w, args.policy, args.policy_seed, args.segmentation, args.n_seg)
+    cfg = B.Config.from_workload(w, args.policy, args.policy_seed, args.segmentation, args.n_seg, args.fit_model)
     total, rec_off = B.payload_layout(cfg)
     n_copies = max(1, min(64, math.ceil(3 * MALL_BYTES / max(1, 4 * d)))) if 4 * d < 2 * MALL_BYTES else 1
     g_dev = [torch.from_numpy(g_host).cuda()]
@@ -297,7 +298,7 @@ def main():
         off = [o for o in w.offsets() if o < elems] + [elems]
         t0 = time.perf_counter()
         oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, cfg.n_seg, policy=args.policy,
-                         seed=args.policy_seed, seg_mode=args.segmentation)
+                         seed=args.policy_seed, seg_mode=args.segmentation, model=args.fit_model)
         tc = time.perf_counter() - t0
         sample = "full workload" if elems == d else f"first {elems} elements ({len(off) - 1} tensors) of the workload"
         cpu = {"value": round(elems / tc / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
@@ -321,6 +322,7 @@ def main():
                    "ratio": None if w.ratio is None else f"{w.ratio[0]}/{w.ratio[1]}", "fpr": w.fpr,
                    "degree": w.degree, "n_seg": cfg.n_seg, "policy": POLICY_NAMES[args.policy],
                    "segmentation": ["equal", "chord"][args.segmentation],
+                   "fit_model": ["poly", "dexp"][args.fit_model],
                    "input_copies": n_copies},
         "hbm_frac": round(b_alg / (ms * 1e-3) / HBM_PEAK, 4),
         "bytes_alg": int(b_alg),

@@ -100,6 +100,22 @@ typedef enum {
 #define DR_SEG_EQUAL 0u
 #define DR_SEG_CHORD 1u
 
+/* Value model per run (Section 5).  POLY: the least-squares polynomial of
+ * degree `degree` (see dr_curvefit_encode).  DEXP: y = a e^(b t) + c e^(d t)
+ * on the same abscissa t in [-1, 1], coefficient row (a, b, c, d) (so a
+ * record's D_eff is 3 and runs hold at least 4 values; `degree` is not
+ * used).  The fit: rates (1, -1) with the amplitudes that solve the linear
+ * least-squares problem for them (a = mean, c = 0 if it is singular), then
+ * 40 Levenberg-Marquardt steps solving (J^T J + lambda diag(J^T J)) delta =
+ * J^T r in double, the trial rates clamped to [-40, 40], a trial kept only
+ * if it lowers the residual sum of squares (lambda from 1e-3, /10 on a kept
+ * step, x10 otherwise).  Decoding evaluates a e^(bt) + c e^(dt) in double
+ * on the fp32 row and rounds to fp32.  A tensor with fewer than 4 values is
+ * coded with the polynomial through them (the header names the model
+ * used). */
+#define DR_FIT_POLY 0u
+#define DR_FIT_DEXP 1u
+
 /* Bits of the per-tensor flags word (slot 3 of counts_out). */
 #define DR_FLAG_NONFINITE 1u    /* the tensor held NaN or Inf */
 #define DR_FLAG_DEC_MISMATCH 2u /* receiver: the record is invalid, or its |P| differs from the header */
@@ -217,6 +233,7 @@ typedef struct {
                                   XORs MurmurHash3_x86_32(LE half, seed + j) mod 2^h into the
                                   other half, restricted to [0, |P|) by cycle walking */
     uint32_t segmentation;     /* DR_SEG_EQUAL or DR_SEG_CHORD                                   */
+    uint32_t fit_model;        /* DR_FIT_POLY or DR_FIT_DEXP                                     */
 } dr_config;
 
 /* Payload container (Figure 3's "container"): one record per tensor at byte
@@ -229,7 +246,7 @@ typedef struct {
  * header bytes (64), d, n_selected, n_positives (|P|), n_values (values
  * coded: |P| under P0), m_bits, k, hash id (1 = MurmurHash3_x86_32), policy,
  * seed, D_eff, S_eff, sigma bits, record bytes (header + sections; what
- * would be sent), segmentation (DR_SEG_*).
+ * would be sent), segmentation (DR_SEG_*) | value model (DR_FIT_*) << 8.
  * Returns the total payload capacity in bytes; fills rec_off_h (nullable,
  * n_tensors+1 entries) with the record offsets and the end.  Returns 0 for
  * an invalid configuration. */

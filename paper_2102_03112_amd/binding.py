@@ -50,6 +50,7 @@ class DrConfig(ctypes.Structure):
         ("policy", ctypes.c_uint32),
         ("seed", ctypes.c_uint32),
         ("segmentation", ctypes.c_uint32),
+        ("fit_model", ctypes.c_uint32),
     ]
 
 
@@ -181,14 +182,14 @@ class Config:
     """A dr_config together with the host offsets array it points to."""
 
     def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int, policy: int = 0, seed: int = 0,
-                 segmentation: int = 0):
+                 segmentation: int = 0, fit_model: int = 0):
         self.offsets = np.ascontiguousarray(np.asarray(offsets, dtype=np.uint64))
         self._off_c = (ctypes.c_uint64 * self.offsets.size)(*[int(x) for x in self.offsets])
         num, den = (R_NONZERO, 1) if ratio is None else ratio
         self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg, policy, seed,
-                          segmentation)
+                          segmentation, fit_model)
         self.ratio, self.fpr, self.degree, self.n_seg = ratio, fpr, degree, n_seg
-        self.policy, self.seed, self.segmentation = policy, seed, segmentation
+        self.policy, self.seed, self.segmentation, self.fit_model = policy, seed, segmentation, fit_model
 
     @property
     def n_tensors(self) -> int:
@@ -199,9 +200,9 @@ class Config:
         return int(self.offsets[-1])
 
     @classmethod
-    def from_workload(cls, w, policy: int = 0, seed: int = 0, segmentation: int = 0, n_seg=None):
+    def from_workload(cls, w, policy: int = 0, seed: int = 0, segmentation: int = 0, n_seg=None, fit_model: int = 0):
         return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg if n_seg is None else n_seg, policy, seed,
-                   segmentation)
+                   segmentation, fit_model)
 
 
 def payload_layout(cfg: Config) -> tuple[int, list]:
@@ -274,6 +275,7 @@ class Record:
     sigma_b: int
     rec_bytes: int
     seg_mode: int
+    model: int
     bits: np.ndarray
     coef: np.ndarray
     knots: np.ndarray  # starts of runs 1 .. S_eff-1 (chord segmentation), else empty
@@ -294,9 +296,11 @@ def parse_record(buf: bytes | np.ndarray, start: int) -> Record:
     ncoef = se * (de + 1)
     coef = b[at: at + 4 * ncoef].view("<f4").copy()
     at += 4 * ncoef
+    seg, model = seg & 0xFF, seg >> 8
     nkn = se - 1 if seg == 1 and se > 1 else 0
     knots = b[at: at + 4 * nkn].view("<u4").copy()
     at += 4 * nkn
     nw = (n_v * sb + 31) // 32
     sigma = b[at: at + 4 * nw].view("<u4").copy()
-    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, seg, bits, coef, knots, sigma)
+    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, seg, model, bits, coef, knots,
+                  sigma)

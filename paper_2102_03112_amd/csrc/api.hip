@@ -20,6 +20,7 @@ static_assert(POLICY_P0 == DR_POLICY_P0 && POLICY_RANDOM == DR_POLICY_RANDOM && 
                   POLICY_MIDDLE == DR_POLICY_MIDDLE && POLICY_RIGHTMOST == DR_POLICY_RIGHTMOST,
               "index policy ids");
 static_assert(SEG_EQUAL == DR_SEG_EQUAL && SEG_CHORD == DR_SEG_CHORD, "segmentation ids");
+static_assert(FIT_POLY == DR_FIT_POLY && FIT_DEXP == DR_FIT_DEXP, "value model ids");
 static_assert(MAX_SEG == DR_MAX_SEGMENTS && MAX_DEG == DR_MAX_DEGREE, "limits of the header and the kernels");
 
 namespace {
@@ -206,6 +207,7 @@ struct Plan {
     bool any_topr = false;
     bool direct = false;  // every filter small enough for the direct insert
     bool segment = false; // some tensor needs the segmentation pass (chord, or the heuristic count)
+    bool dexp = false;    // some tensor fits double exponentials
     uint32_t dir_blocks = 0, dir_slices = 0;
 };
 
@@ -316,6 +318,7 @@ dr_status check_cfg(const dr_config *cfg) {
     if (cfg->degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
     if (cfg->n_seg > DR_MAX_SEGMENTS) return fail(DR_EINVAL, "n_seg out of range");
     if (cfg->segmentation > DR_SEG_CHORD) return fail(DR_EINVAL, "unknown segmentation %u", cfg->segmentation);
+    if (cfg->fit_model > DR_FIT_DEXP) return fail(DR_EINVAL, "unknown value model %u", cfg->fit_model);
     if (cfg->policy > DR_POLICY_RIGHTMOST) return fail(DR_EINVAL, "unknown index policy %u", cfg->policy);
     return DR_OK;
 }
@@ -378,7 +381,11 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.slot = tiles * TILE;
         tiles += in.ntiles;
         in.k = kk;
-        in.degree = cfg->degree;
+        // the double exponential has four parameters per run, the row of a
+        // cubic
+        const uint32_t degree = cfg->fit_model == DR_FIT_DEXP ? 3u : cfg->degree;
+        in.degree = degree;
+        in.fit_model = cfg->fit_model;
         in.nseg = cfg->n_seg;
         in.policy = cfg->policy;
         in.seed = cfg->seed;
@@ -386,7 +393,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.mC = mC;
         // top-r: |S| = r is known, so the filter size is too
         in.m_words_in = nz ? 0u : (uint32_t)(m_cap / 32);
-        const uint64_t runs = runs_cap(d, cfg->degree, cfg->n_seg);
+        const uint64_t runs = runs_cap(d, degree, cfg->n_seg);
         in.fit_blk0 = (uint32_t)fit_blocks;
         fit_blocks += runs * FIT_CHUNKS;
         if (cfg->segmentation == DR_SEG_CHORD) {
@@ -394,6 +401,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
             bnd += runs + 1;
         }
         p.segment |= cfg->segmentation == DR_SEG_CHORD || cfg->n_seg == 0;
+        p.dexp |= cfg->fit_model == DR_FIT_DEXP;
         if (!nz) {
             in.hb0 = (uint32_t)hist_blocks;
             in.hbn = (uint32_t)ceil_div(in.ntiles, ht);
@@ -403,7 +411,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
             in.hbn = 0;
         }
         plan_bloom(in, n_cap, m_cap, true, p);
-        rec_off[t + 1] = rec_off[t] + align_up(record_capacity(d, n_cap, cfg->fpr, cfg->degree, runs,
+        rec_off[t + 1] = rec_off[t] + align_up(record_capacity(d, n_cap, cfg->fpr, degree, runs,
                                                                cfg->segmentation == DR_SEG_CHORD),
                                                256);
     }
@@ -487,7 +495,7 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
     DR_HIP(launch_value_setup(w, true, counts_out, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     if (p.segment) DR_HIP(launch_segment(w, s));
-    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
+    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;
 }
@@ -841,7 +849,7 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
     DR_HIP(launch_keygen(w, vals, n, n_cap, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, false, nullptr, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
-    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, s));
+    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;
 }

@@ -433,7 +433,7 @@ struct RecordView {
     const float *coef;
     const uint32_t *knots;  // chord segmentation: the seff - 1 interior run starts
     const uint32_t *sigma;
-    uint32_t m_bits, k, npos, nv, policy, seed, deff, seff, b, segmode;
+    uint32_t m_bits, k, npos, nv, policy, seed, deff, seff, b, segmode, model;
 };
 
 // Reads a record header and checks it against the record's capacity and
@@ -452,7 +452,9 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     v.deff = h[H_DEFF];
     v.seff = h[H_SEFF];
     v.b = h[H_B];
-    v.segmode = h[H_SEGMODE];
+    const uint32_t hw15 = h[H_SEGMODE];  // segmentation | value model << 8
+    v.segmode = hw15 & 0xffu;
+    v.model = (hw15 >> 8) & 0xffu;
     v.bits = (const uint32_t *)(rec + HDR_BYTES);
     const uint32_t coef_off = HDR_BYTES + (v.m_bits / 32u) * 4u;
     v.coef = (const float *)(rec + coef_off);
@@ -462,6 +464,7 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     *ok = h[H_MAGIC] == HDR_MAGIC && h[H_BYTES] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && v.k >= 1 &&
           v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && v.npos <= d && v.nv <= v.npos &&
           v.policy <= POLICY_RIGHTMOST && (v.policy != POLICY_P0 || v.nv == v.npos) && v.segmode <= SEG_CHORD &&
+          (hw15 >> 16) == 0 && v.model <= FIT_DEXP && (v.model != FIT_DEXP || v.deff == 3) &&
           (v.nv == 0 || (v.seff >= 1 && v.seff <= v.nv && v.seff <= MAX_SEG && v.b >= sigma_bits(v.nv))) &&
           need <= cap;
     if (!*ok) {  // nothing of an invalid record is read past its first filter word
@@ -470,6 +473,7 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
         v.nv = 0;
         v.policy = POLICY_P0;
         v.segmode = SEG_EQUAL;
+        v.model = FIT_POLY;
         v.m_bits = 32;
         v.seff = 0;
         v.deff = 0;
@@ -699,7 +703,10 @@ __device__ __forceinline__ float positive_value(const RecordView &rv, const floa
         return 0.0f;
     }
     const double tt = abscissa(rank - lo, ns);
-    return horner(cf + s * (rv.deff + 1u), rv.deff, tt);
+    const float *row = cf + s * (rv.deff + 1u);
+    if (rv.model == FIT_DEXP)
+        return (float)((double)row[0] * exp((double)row[1] * tt) + (double)row[2] * exp((double)row[3] * tt));
+    return horner(row, rv.deff, tt);
 }
 
 // Emit pass: positives in ascending order at their tensor-wide ranks.

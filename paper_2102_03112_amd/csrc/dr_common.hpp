@@ -43,6 +43,8 @@ constexpr uint32_t POLICY_P0 = 0, POLICY_RANDOM = 1, POLICY_LEFTMOST = 2, POLICY
 constexpr uint32_t NO_SLOT = 0xffffffffu;
 // segmentation of the sorted values (Section 5)
 constexpr uint32_t SEG_EQUAL = 0, SEG_CHORD = 1;
+// value models (Section 5): polynomial, double exponential a e^(bt) + c e^(dt)
+constexpr uint32_t FIT_POLY = 0, FIT_DEXP = 1;
 constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
 constexpr uint32_t HDR_BYTES = 64;
 // payload record header: sixteen little-endian u32 words
@@ -96,6 +98,7 @@ struct TInit {
     uint32_t policy;     // index policy (POLICY_*)
     uint32_t seed;       // key of the random policy
     uint32_t seg_mode;   // SEG_EQUAL or SEG_CHORD (nseg == 0: the heuristic count)
+    uint32_t fit_model;  // FIT_POLY or FIT_DEXP (then degree is 3: rows (a, b, c, d))
     uint32_t bnd0;       // chord segmentation: first segment-start entry of this tensor
 };
 
@@ -129,6 +132,7 @@ struct TDesc {
     uint32_t sigma_off;  // payload record: byte offset of the reorder map
     uint32_t rec_bytes;  // payload record: bytes in use
     uint32_t bl_end;     // Bloom insert: positions bucketed in the current round
+    uint32_t model;      // value model used: FIT_DEXP needs at least 4 values, else FIT_POLY
 };
 
 static_assert(sizeof(TInit) % 4 == 0 && sizeof(TDesc) % 4 == 0, "descriptor layout");

@@ -85,7 +85,7 @@ hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, ui
 hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s);
 hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s);
 hipError_t launch_segment(const Work &w, hipStream_t s);
-hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s);
+hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s);
 hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s);
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
                                   uint64_t n_cap, float *vals_out, int grid_persist, hipStream_t s);

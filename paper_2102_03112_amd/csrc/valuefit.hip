@@ -78,6 +78,7 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
             td.deff = deff;
             const uint32_t b = sigma_bits(nv);
             td.b = b;
+            td.model = td.in.fit_model == FIT_DEXP && nv >= 4 ? FIT_DEXP : FIT_POLY;
             ntl = (nv + TILE - 1) / TILE;
             nwd = (uint32_t)(((uint64_t)nv * b + 31u) / 32u);
             td.sntiles = ntl;
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int paylo
                 h[H_SEFF] = seff;
                 h[H_B] = b;
                 h[H_RECBYTES] = rec_bytes;
-                h[H_SEGMODE] = td.in.seg_mode;
+                h[H_SEGMODE] = td.in.seg_mode | (td.model << 8);
             }
         }
         uint32_t tot_t, tot_w, tot_v;
@@ -754,7 +755,7 @@ __global__ __launch_bounds__(FIT_THREADS) void k_fit_moments(Work w) {
     const TDesc &td = w.td[t];
     const uint32_t local = blockIdx.x - td.in.fit_blk0;
     const uint32_t s = local / FIT_CHUNKS, ch = local % FIT_CHUNKS;
-    if (s >= td.seff) return;
+    if (s >= td.seff || td.model == FIT_DEXP) return;
     uint64_t lo, hi;
     run_range(w, td, s, &lo, &hi);
     const uint64_t ns = hi - lo;
@@ -786,6 +787,7 @@ __global__ __launch_bounds__(64) void k_fit_solve(Work w) {
             td.in.coef[(uint64_t)s * td.in.coef_stride + threadIdx.x] = 0.0f;
         return;
     }
+    if (td.model == FIT_DEXP) return;  // fitted by k_fit_dexp
     __shared__ double mom[NMOM];
     if (threadIdx.x < NMOM) {
         const double *part = w.fit_part + (uint64_t)blk * NMOM;
@@ -874,12 +876,246 @@ __device__ void solve_run(const TDesc &td, uint32_t s, const double *mom) {
     }
 }
 
-hipError_t launch_fit(const Work &w, uint32_t fit_blocks, hipStream_t s) {
+// ---------------------------------------------------------------------------
+// Double-exponential fit (Section 5, "Nonlinear regression"): one block per
+// run, Levenberg-Marquardt on y ~ a e^(bt) + c e^(dt) with the same steps as
+// the oracle (start at rates (1, -1) with the amplitudes of the linear
+// problem; DEXP_ITERS steps, rates clamped to [-40, 40], lambda from 1e-3,
+// x10 on a reject, /10 on an accept).  Each step is one pass over the run:
+// the 15 sums of J^T J, J^T r and r^T r at the trial point, reduced over
+// the block in a fixed order; every thread then takes the same decision and
+// solves the same 4 x 4 system.  A thread takes a contiguous range of
+// points: the abscissae are equally spaced, so e^(b t) advances by one
+// multiplication per point from one exp() at the range's start (relative
+// drift ~1e-15 over a range, far below the fit's tolerance).
+// ---------------------------------------------------------------------------
+constexpr uint32_t DEXP_THREADS = 512;
+constexpr int DEXP_ITERS = 40;
+constexpr uint32_t DEXP_BATCH = 8;
+constexpr double DEXP_RATE_MAX = 40.0;
+
+// sums over the block, in wave order, into tot[0..N) (LDS); the block is
+// synchronised on return
+template <int N>
+__device__ void block_sums(const double *v, double (*red)[15], double *tot) {
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+        const double sm = wave_sum_f64(v[e]);
+        if (lane == 0) red[wv][e] = sm;
+    }
+    __syncthreads();
+    if (threadIdx.x < (uint32_t)N) {
+        double acc = 0.0;
+        for (uint32_t q = 0; q < DEXP_THREADS / 64; ++q) acc += red[q][threadIdx.x];
+        tot[threadIdx.x] = acc;
+    }
+    __syncthreads();
+}
+
+// solve A x = rhs (4 x 4, augmented) by elimination with partial pivoting;
+// false if a pivot is zero
+// (every index is a compile-time constant once unrolled, so A stays in
+// registers: the pivot row is swapped in by selects)
+__device__ __forceinline__ bool solve4(double A[4][5], double *x) {
+#pragma unroll
+    for (int col = 0; col < 4; ++col) {
+        int piv = col;
+        double best = fabs(A[col][col]);
+#pragma unroll
+        for (int row = col + 1; row < 4; ++row)
+            if (fabs(A[row][col]) > best) {
+                best = fabs(A[row][col]);
+                piv = row;
+            }
+        if (best == 0.0) return false;
+#pragma unroll
+        for (int row = col + 1; row < 4; ++row) {
+            const bool sw = row == piv;
+#pragma unroll
+            for (int c = 0; c <= 4; ++c) {
+                const double a = A[col][c], b = A[row][c];
+                A[col][c] = sw ? b : a;
+                A[row][c] = sw ? a : b;
+            }
+        }
+#pragma unroll
+        for (int row = col + 1; row < 4; ++row) {
+            const double f = A[row][col] / A[col][col];
+#pragma unroll
+            for (int c = col; c <= 4; ++c) A[row][c] -= f * A[col][c];
+        }
+    }
+#pragma unroll
+    for (int p = 3; p >= 0; --p) {
+        double s = A[p][4];
+#pragma unroll
+        for (int q = p + 1; q < 4; ++q) s -= A[p][q] * x[q];
+        x[p] = s / A[p][p];
+    }
+    return true;
+}
+
+__global__ __launch_bounds__(DEXP_THREADS) void k_fit_dexp(Work w) {
+    const uint32_t blk = blockIdx.x * FIT_CHUNKS;
+    const uint32_t t = tensor_of_fit_block(w, blk);
+    const TDesc &td = w.td[t];
+    const uint32_t s = (blk - td.in.fit_blk0) / FIT_CHUNKS;
+    if (td.model != FIT_DEXP || s >= td.seff) return;
+    __shared__ double red[DEXP_THREADS / 64][15];
+    __shared__ double tot[15];
+    // the solver's state lives in LDS and only thread 0 changes it, which
+    // keeps the per-thread registers to one pass's sums
+    __shared__ double th_s[4], tt_s[4], cur_s[15], lambda_s;
+    __shared__ int it_s, go_s;
+    uint64_t lo, hi;
+    run_range(w, td, s, &lo, &hi);
+    const uint64_t ns = hi - lo;
+    const float *y = w.vsorted + td.in.slot + lo;
+    const double inv = ns > 1 ? 1.0 / (double)(ns - 1) : 0.0;
+    const double off = (double)(ns - 1);
+    const uint64_t per = (ns + DEXP_THREADS - 1) / DEXP_THREADS;
+    const uint64_t j0 = min(ns, threadIdx.x * per), j1 = min(ns, j0 + per);
+    const double step = 2.0 * inv;
+    // start: rates (1, -1), amplitudes from the 2 x 2 linear problem
+    {
+        double v[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+        if (j0 < j1) {
+            const double t0 = ((double)(2 * j0) - off) * inv;
+            double e1 = exp(t0), e2 = exp(-t0);
+            const double r1 = exp(step), r2 = exp(-step);
+            for (uint64_t jb = j0; jb < j1; jb += DEXP_BATCH) {
+                float yv[DEXP_BATCH];
+#pragma unroll
+                for (uint32_t u = 0; u < DEXP_BATCH; ++u) yv[u] = jb + u < j1 ? y[jb + u] : 0.0f;
+#pragma unroll
+                for (uint32_t u = 0; u < DEXP_BATCH; ++u) {
+                    if (jb + u >= j1) break;
+                    const double yj = (double)yv[u];
+                    v[0] += e1 * e1;
+                    v[1] += e1 * e2;
+                    v[2] += e2 * e2;
+                    v[3] += yj * e1;
+                    v[4] += yj * e2;
+                    v[5] += yj;
+                    e1 *= r1;
+                    e2 *= r2;
+                }
+            }
+        }
+        block_sums<6>(v, red, tot);
+        if (threadIdx.x == 0) {
+            const double det = tot[0] * tot[2] - tot[1] * tot[1];
+            th_s[1] = 1.0;
+            th_s[3] = -1.0;
+            if (det != 0.0) {
+                th_s[0] = (tot[3] * tot[2] - tot[4] * tot[1]) / det;
+                th_s[2] = (tot[4] * tot[0] - tot[3] * tot[1]) / det;
+            } else {
+                th_s[0] = tot[5] / (double)ns;
+                th_s[2] = 0.0;
+            }
+            for (int p = 0; p < 4; ++p) tt_s[p] = th_s[p];
+            lambda_s = 1e-3;
+            it_s = 0;
+        }
+        __syncthreads();
+    }
+    for (bool first = true;; first = false) {
+        // one pass at the trial point tt_s
+        const double a = tt_s[0], b = tt_s[1], c = tt_s[2], dd = tt_s[3];
+        double v[15];
+#pragma unroll
+        for (int e = 0; e < 15; ++e) v[e] = 0.0;
+        if (j0 < j1) {
+            const double t0 = ((double)(2 * j0) - off) * inv;
+            double eb = exp(b * t0), ed = exp(dd * t0);
+            const double rb = exp(b * step), rd = exp(dd * step);
+            for (uint64_t jb = j0; jb < j1; jb += DEXP_BATCH) {
+                float yv[DEXP_BATCH];
+#pragma unroll
+                for (uint32_t u = 0; u < DEXP_BATCH; ++u) yv[u] = jb + u < j1 ? y[jb + u] : 0.0f;
+#pragma unroll
+                for (uint32_t u = 0; u < DEXP_BATCH; ++u) {
+                    const uint64_t j = jb + u;
+                    if (j >= j1) break;
+                    const double tj = ((double)(2 * j) - off) * inv, yj = (double)yv[u];
+                    const double J[4] = {eb, a * tj * eb, ed, c * tj * ed};
+                    const double r = yj - (a * eb + c * ed);
+                    int e = 0;
+#pragma unroll
+                    for (int p = 0; p < 4; ++p)
+#pragma unroll
+                        for (int q = p; q < 4; ++q) v[e++] += J[p] * J[q];
+#pragma unroll
+                    for (int p = 0; p < 4; ++p) v[10 + p] += J[p] * r;
+                    v[14] += r * r;
+                    eb *= rb;
+                    ed *= rd;
+                }
+            }
+        }
+        block_sums<15>(v, red, tot);
+        if (threadIdx.x == 0) {
+            if (first) {
+                for (int e = 0; e < 15; ++e) cur_s[e] = tot[e];
+            } else if (tot[14] < cur_s[14]) {
+                for (int p = 0; p < 4; ++p) th_s[p] = tt_s[p];
+                for (int e = 0; e < 15; ++e) cur_s[e] = tot[e];
+                lambda_s /= 10.0;
+            } else {
+                lambda_s *= 10.0;
+            }
+            // the next trial point; a singular system uses up a step
+            int go = 0;
+            while (it_s < DEXP_ITERS) {
+                ++it_s;
+                double A[4][5];
+                int e = 0;
+                for (int p = 0; p < 4; ++p)
+                    for (int q = p; q < 4; ++q) {
+                        A[p][q] = cur_s[e];
+                        A[q][p] = cur_s[e];
+                        ++e;
+                    }
+                for (int p = 0; p < 4; ++p) {
+                    A[p][p] += lambda_s * A[p][p];
+                    A[p][4] = cur_s[10 + p];
+                }
+                double delta[4];
+                if (!solve4(A, delta)) {
+                    lambda_s *= 10.0;
+                    continue;
+                }
+                for (int p = 0; p < 4; ++p) tt_s[p] = th_s[p] + delta[p];
+                for (int p = 1; p < 4; p += 2)
+                    tt_s[p] = tt_s[p] > DEXP_RATE_MAX ? DEXP_RATE_MAX
+                                                      : (tt_s[p] < -DEXP_RATE_MAX ? -DEXP_RATE_MAX : tt_s[p]);
+                go = 1;
+                break;
+            }
+            go_s = go;
+        }
+        __syncthreads();
+        if (!go_s) break;
+    }
+    if (threadIdx.x < 4) {
+        float *row = td.in.coef ? td.in.coef + (uint64_t)s * td.in.coef_stride
+                                : (float *)(td.in.rec + td.coef_off) + (uint64_t)s * 4u;
+        row[threadIdx.x] = (float)th_s[threadIdx.x];
+    }
+}
+
+hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s) {
     if (fit_blocks == 0) return hipSuccess;
     k_fit_moments<<<fit_blocks, FIT_THREADS, 0, s>>>(w);
     trace_mark(s, "k_fit_moments");
     k_fit_solve<<<fit_blocks / FIT_CHUNKS, 64, 0, s>>>(w);
     trace_mark(s, "k_fit_solve");
+    if (dexp) {
+        k_fit_dexp<<<fit_blocks / FIT_CHUNKS, DEXP_THREADS, 0, s>>>(w);
+        trace_mark(s, "k_fit_dexp");
+    }
     return hipGetLastError();
 }
 

@@ -84,6 +84,7 @@ def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     assert (rec.m_bits, rec.k, rec.hash_id) == (ref.m, ref.k, 1)
     assert (rec.policy, rec.seed) == (ref.policy, ref.seed)
     assert rec.seg_mode == ref.fit.seg_mode
+    assert rec.model == ref.fit.model
     if ref.fit.seg_mode == oracle.SEG_CHORD:
         np.testing.assert_array_equal(rec.knots, ref.fit.bounds[1:-1].astype(np.uint32))
     assert (rec.seg_eff, rec.deg_eff, rec.sigma_b) == (ref.fit.S_eff, ref.fit.D_eff, ref.fit.b)
@@ -143,7 +144,7 @@ def check_roundtrip(g, cfg: B.Config, out, refs):
     for t, ref in enumerate(refs):
         a, b = int(off[t]), int(off[t + 1])
         rec = B.parse_record(out["payload"], out["rec_off"][t])
-        check_record(rec, ref, cfg.degree, cfg.n_seg)
+        check_record(rec, ref, ref.fit.degree, cfg.n_seg)
         n_sel, nv, nv_dec, flags = [int(x) for x in out["counts"][t]]
         assert (n_sel, nv, nv_dec, flags) == (ref.S.size, ref.P.size, ref.P.size, 0)
         np.testing.assert_array_equal(out["idx"][a: a + nv], ref.P_dec)

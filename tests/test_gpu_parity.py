@@ -291,6 +291,30 @@ def test_roundtrip_segmentation_parity(name):
         assert any(r.fit.S_eff > 1 for r in refs)
 
 
+DEXP_CASES = {
+    # name: (g, offsets, ratio, fpr, S, segmentation)
+    "resnet20_dexp": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 1, oracle.SEG_EQUAL),
+    "laplace_dexp8": (W.generate(W.Workload("t", 300_000, 1, (1, 100), 1e-3, 3, 8, "laplace_5e-4", 17)),
+                      [0, 300_000], (1, 100), 1e-3, 8, oracle.SEG_EQUAL),
+    "laplace_dexp_chord6": (W.generate(W.Workload("t", 300_000, 1, (1, 100), 1e-3, 3, 6, "laplace_5e-4", 18)),
+                            [0, 300_000], (1, 100), 1e-3, 6, oracle.SEG_CHORD),
+    "ragged_dexp": (W.normal(8203, 8), [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 4, oracle.SEG_EQUAL),
+}
+
+
+@pytest.mark.parametrize("name", list(DEXP_CASES))
+def test_roundtrip_dexp_parity(name):
+    """The double-exponential model (Section 5): same fitted rows (norm-wise
+    1e-4 per run) and reconstructed values as the oracle."""
+    g, off, ratio, fpr, S, seg = DEXP_CASES[name]
+    log(f"roundtrip {name} d={g.size} S={S} seg={seg}")
+    cfg = B.Config(off, ratio, fpr, 3, S, 0, 0, seg, oracle.FIT_DEXP)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, 3, S, seg_mode=seg, model=oracle.FIT_DEXP)
+    check_roundtrip(g, cfg, out, refs)
+    assert any(r.fit.model == oracle.FIT_DEXP for r in refs)
+
+
 def test_receiver_takes_the_policy_from_the_record():
     """The receiver reads policy and key from each record's header, not from
     its own configuration."""
