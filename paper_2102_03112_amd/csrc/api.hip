@@ -9,6 +9,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -461,27 +462,38 @@ bool ws_ok(void *ws, size_t ws_bytes, size_t need) {
     return ws && ws_bytes >= need && ((uintptr_t)ws & 255u) == 0;
 }
 
-dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
-                      uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+// The sender in two halves: select, insert, query and the values' layout
+// (front), then sort, segmentation, fit and reorder map (back).
+struct Encode {
     Plan p;
     std::vector<uint64_t> rec_off;
-    dr_status st = plan_config(cfg, p, rec_off);
+    Work w;
+};
+
+dr_status encode_prepare(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
+                         uint64_t *counts_out, void *ws, size_t ws_bytes, Encode &e) {
+    dr_status st = plan_config(cfg, e.p, e.rec_off);
     if (st != DR_OK) return st;
     if (!g && cfg->offsets_h[cfg->n_tensors] > 0) return fail(DR_EINVAL, "g is null");
-    if (!payload || payload_bytes < rec_off.back()) return fail(DR_EINVAL, "payload buffer too small");
-    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
-        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
-    for (size_t t = 0; t < p.t.size(); ++t) {
-        p.t[t].rec_off = rec_off[t];
-        p.t[t].rec_cap = rec_off[t + 1] - rec_off[t];
-        p.t[t].rec = payload + rec_off[t];
-        p.t[t].bits = (uint32_t *)(payload + rec_off[t] + HDR_BYTES);
-        p.t[t].coef = nullptr;
-        p.t[t].sigma = nullptr;
+    if (!payload || payload_bytes < e.rec_off.back()) return fail(DR_EINVAL, "payload buffer too small");
+    if (!ws_ok(ws, ws_bytes, e.p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", e.p.carve.bytes);
+    for (size_t t = 0; t < e.p.t.size(); ++t) {
+        e.p.t[t].rec_off = e.rec_off[t];
+        e.p.t[t].rec_cap = e.rec_off[t + 1] - e.rec_off[t];
+        e.p.t[t].rec = payload + e.rec_off[t];
+        e.p.t[t].bits = (uint32_t *)(payload + e.rec_off[t] + HDR_BYTES);
+        e.p.t[t].coef = nullptr;
+        e.p.t[t].sigma = nullptr;
     }
-    Work w = p.carve.view((uint8_t *)ws);
-    w.counts_out = counts_out;
-    trace_call(s);
+    e.w = e.p.carve.view((uint8_t *)ws);
+    e.w.counts_out = counts_out;
+    return DR_OK;
+}
+
+dr_status encode_front(Encode &e, const float *g, uint64_t *counts_out, hipStream_t s) {
+    const Plan &p = e.p;
+    const Work &w = e.w;
     DR_HIP(run_init(w, p.t, s));
     if (p.any_topr)
         DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
@@ -493,6 +505,12 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
         DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
     DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, true, counts_out, s));
+    return DR_OK;
+}
+
+dr_status encode_back(Encode &e, hipStream_t s) {
+    const Plan &p = e.p;
+    const Work &w = e.w;
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     if (p.segment) DR_HIP(launch_segment(w, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
@@ -500,27 +518,159 @@ dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, si
     return DR_OK;
 }
 
-dr_status decode_impl(const uint8_t *payload, const dr_config *cfg, float *dense_out, uint32_t *idx_out,
-                      float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+dr_status encode_impl(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
+                      uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+    Encode e;
+    dr_status st = encode_prepare(g, cfg, payload, payload_bytes, counts_out, ws, ws_bytes, e);
+    if (st != DR_OK) return st;
+    trace_call(s);
+    st = encode_front(e, g, counts_out, s);
+    if (st != DR_OK) return st;
+    return encode_back(e, s);
+}
+
+// The receiver: its own descriptors over the payload's records, in the
+// workspace at byte offset ws_off (a query-only carve there if query_only).
+struct Decode {
     Plan p;
     std::vector<uint64_t> rec_off;
-    dr_status st = plan_config(cfg, p, rec_off);
+    Work w;
+    float *dense_out;
+    uint32_t *idx_out;
+    float *val_out;
+    uint64_t *counts_out;
+};
+
+dr_status decode_prepare(const uint8_t *payload, const dr_config *cfg, float *dense_out, uint32_t *idx_out,
+                         float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, Decode &dd) {
+    dr_status st = plan_config(cfg, dd.p, dd.rec_off);
     if (st != DR_OK) return st;
     if (!payload) return fail(DR_EINVAL, "payload is null");
     if (!dense_out && cfg->offsets_h[cfg->n_tensors] > 0) return fail(DR_EINVAL, "dense_out is null");
-    if (!ws_ok(ws, ws_bytes, p.carve.bytes))
-        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", p.carve.bytes);
-    for (size_t t = 0; t < p.t.size(); ++t) {
-        p.t[t].rec_off = rec_off[t];
-        p.t[t].rec_cap = rec_off[t + 1] - rec_off[t];
-        p.t[t].rec = const_cast<uint8_t *>(payload) + rec_off[t];
-        p.t[t].bits = nullptr;
+    if (!ws_ok(ws, ws_bytes, dd.p.carve.bytes))
+        return fail(DR_EINVAL, "workspace too small or not 256-byte aligned (need %zu)", dd.p.carve.bytes);
+    for (size_t t = 0; t < dd.p.t.size(); ++t) {
+        dd.p.t[t].rec_off = dd.rec_off[t];
+        dd.p.t[t].rec_cap = dd.rec_off[t + 1] - dd.rec_off[t];
+        dd.p.t[t].rec = const_cast<uint8_t *>(payload) + dd.rec_off[t];
+        dd.p.t[t].bits = nullptr;
     }
-    const Work w = p.carve.view((uint8_t *)ws);
-    trace_call(s);
-    DR_HIP(run_init(w, p.t, s));
-    DR_HIP(launch_query_decode(w, dense_out, idx_out, val_out, counts_out, s));
+    dd.w = dd.p.carve.view((uint8_t *)ws);
+    dd.dense_out = dense_out;
+    dd.idx_out = idx_out;
+    dd.val_out = val_out;
+    dd.counts_out = counts_out;
     return DR_OK;
+}
+
+// Bytes of a receiver's query-only work for the plan's layout.
+Carve query_carve(const Plan &p) {
+    Carve c;
+    c.query_only = true;
+    c.ntensors = p.carve.ntensors;
+    c.ntiles = p.carve.ntiles;
+    c.slots = p.carve.slots;
+    c.plan();
+    return c;
+}
+
+dr_status decode_front(Decode &dd, uint32_t max_probe_blocks, bool query_only, hipStream_t s) {
+    DR_HIP(run_init(dd.w, dd.p.t, s, query_only));
+    DR_HIP(launch_probe_decode(dd.w, dd.dense_out, dd.counts_out, max_probe_blocks, s));
+    return DR_OK;
+}
+
+dr_status decode_back(Decode &dd, hipStream_t s) {
+    DR_HIP(launch_emit_decode(dd.w, dd.dense_out, dd.idx_out, dd.val_out, dd.counts_out, s));
+    return DR_OK;
+}
+
+dr_status decode_impl(const uint8_t *payload, const dr_config *cfg, float *dense_out, uint32_t *idx_out,
+                      float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
+    Decode dd;
+    dr_status st = decode_prepare(payload, cfg, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, dd);
+    if (st != DR_OK) return st;
+    trace_call(s);
+    st = decode_front(dd, 0xffffffffu, false, s);
+    if (st != DR_OK) return st;
+    return decode_back(dd, s);
+}
+
+// A second stream per device for the round trip's overlap, with the two
+// events that fork and join it; created on first use, kept until exit.
+struct SideStream {
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+SideStream g_side[64];
+
+bool side_stream(SideStream **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
+    SideStream &ss = g_side[dev];
+    if (!ss.s) {
+        if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) return false;
+        if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) {
+            ss.s = nullptr;
+            return false;
+        }
+    }
+    *out = &ss;
+    return true;
+}
+
+bool tracing_on();
+
+// dr_roundtrip: the receiver's probe pass needs only the payload's header
+// and filter, which the sender has written once its values' layout is set,
+// so it runs on a second stream while the sender sorts and fits its values
+// (the probe is bound by L2 request throughput and loses little when some
+// CUs are left to the sort and the fit).  The receiver then
+// uses its own query-only work after the sender's in the workspace; without
+// room for it, with segmentation passes that rewrite the header after the
+// sort, or while per-kernel timing is on, the two sides run one after the
+// other.
+dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
+                         float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
+                         size_t ws_bytes, hipStream_t s) {
+    Encode e;
+    dr_status st = encode_prepare(g, cfg, payload, payload_bytes, counts_out, ws, ws_bytes, e);
+    if (st != DR_OK) return st;
+    Decode dd;
+    st = decode_prepare(payload, cfg, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, dd);
+    if (st != DR_OK) return st;
+    const Carve qc = query_carve(dd.p);
+    const size_t qoff = align_up(e.p.carve.bytes, 256);
+    SideStream *ss = nullptr;
+    const bool overlap = !e.p.segment && !tracing_on() && qoff + qc.bytes <= ws_bytes && side_stream(&ss);
+    trace_call(s);
+    st = encode_front(e, g, counts_out, s);
+    if (st != DR_OK) return st;
+    if (!overlap) {
+        st = encode_back(e, s);
+        if (st != DR_OK) return st;
+        st = decode_front(dd, 0xffffffffu, false, s);
+        if (st != DR_OK) return st;
+        return decode_back(dd, s);
+    }
+    dd.w = qc.view((uint8_t *)ws + qoff);
+    std::lock_guard<std::mutex> lock(g_side_mu);  // one fork/join sequence at a time per process
+    DR_HIP(hipEventRecord(ss->fork, s));
+    DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
+    // CUs left to the sender: the sort and the fit want a few dozen when
+    // the probe pass is short; for long probe passes (large gradients) each
+    // CU taken from the probe costs more than the sender gains (measured on
+    // 25.6 M, 138 M and 355 M elements)
+    const uint32_t reserve = cfg->offsets_h[cfg->n_tensors] <= (1ull << 26) ? 32u : 8u;
+    st = decode_front(dd, (uint32_t)std::max(1, dr::device_cus() - (int)reserve), true, ss->s);
+    if (st != DR_OK) return st;
+    DR_HIP(hipEventRecord(ss->join, ss->s));
+    st = encode_back(e, s);
+    if (st != DR_OK) return st;
+    DR_HIP(hipStreamWaitEvent(s, ss->join, 0));
+    return decode_back(dd, s);
 }
 
 dr_status decode_sum_impl(const uint8_t *const *payloads, uint32_t npay, const dr_config *cfg, float scale,
@@ -615,6 +765,8 @@ void trace_record(hipStream_t s, const char *name) {
 
 // every entry point that launches work marks its start
 void trace_call(hipStream_t s) { trace_record(s, nullptr); }
+
+bool tracing_on() { return g_trace.on; }
 
 }  // namespace
 
@@ -734,9 +886,8 @@ dr_status dr_payload_decode_sum(const uint8_t *const *payloads_h, uint32_t n_pay
 dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
                        float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
                        size_t ws_bytes, void *stream) {
-    dr_status st = encode_impl(g, cfg_h, payload, payload_bytes, counts_out, ws, ws_bytes, (hipStream_t)stream);
-    if (st != DR_OK) return st;
-    return decode_impl(payload, cfg_h, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, (hipStream_t)stream);
+    return roundtrip_impl(g, cfg_h, payload, payload_bytes, dense_out, idx_out, val_out, counts_out, ws, ws_bytes,
+                          (hipStream_t)stream);
 }
 
 dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx_out, float *val_out,

@@ -954,17 +954,23 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     return hipGetLastError();
 }
 
-hipError_t launch_query_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
-                               uint64_t *counts_out, hipStream_t s) {
+hipError_t launch_probe_decode(const Work &w, float *dense_out, uint64_t *counts_out, uint32_t max_blocks,
+                               hipStream_t s) {
+    QueryOut o{};
+    o.counts_out = counts_out;
+    o.dense_out = dense_out;
+    k_probe<Q_DECODE><<<min((uint32_t)probe_grid(w), max_blocks), PB_THREADS, 0, s>>>(w, o);
+    trace_mark(s, "k_probe<Q_DECODE>");
+    return launch_tile_scan(w, 2, nullptr, s, counts_out);
+}
+
+hipError_t launch_emit_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
+                              uint64_t *counts_out, hipStream_t s) {
     QueryOut o{};
     o.counts_out = counts_out;
     o.dense_out = dense_out;
     o.idx_out = idx_out;
     o.val_out = val_out;
-    k_probe<Q_DECODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
-    trace_mark(s, "k_probe<Q_DECODE>");
-    hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out);
-    if (e != hipSuccess) return e;
     k_emit<Q_DECODE><<<resident_grid(k_emit<Q_DECODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_DECODE>");
     return hipGetLastError();

@@ -72,8 +72,12 @@ hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_c
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s);
 hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,
                               hipStream_t s);
-hipError_t launch_query_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
-                               uint64_t *counts_out, hipStream_t s);
+// the receiver's query in two halves: the probe pass (at most max_blocks
+// blocks) with the tile scan, then the emit pass
+hipError_t launch_probe_decode(const Work &w, float *dense_out, uint64_t *counts_out, uint32_t max_blocks,
+                               hipStream_t s);
+hipError_t launch_emit_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
+                              uint64_t *counts_out, hipStream_t s);
 // Several payloads of one tensor layout into one dense sum: the work's
 // tensors are payload-major (tensor t of payload p is p * ntens + t).
 hipError_t launch_query_decode_sum(const Work &w, uint32_t npay, uint32_t ntens, uint32_t ntiles1, float scale,

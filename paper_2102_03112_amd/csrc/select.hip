@@ -659,7 +659,10 @@ __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, 
                 const uint32_t hdr_npos = ((const uint32_t *)rec)[H_NPOS];
                 uint32_t f = td.flags;
                 if (carry != hdr_npos) f |= FLAG_DEC_MISMATCH;
-                counts_out[4 * blockIdx.x + 3] |= f & FLAG_DEC_MISMATCH;
+                // atomic: the sender's last passes may flag the same word
+                // while the receiver's query runs beside them
+                if (f & FLAG_DEC_MISMATCH)
+                    atomicOr((unsigned long long *)&counts_out[4 * blockIdx.x + 3], FLAG_DEC_MISMATCH);
             }
         } else if (n_out) {
             *n_out = carry;

@@ -368,6 +368,21 @@ def test_roundtrip_is_deterministic():
     np.testing.assert_array_equal(a["dense"], b["dense"])
 
 
+@pytest.mark.parametrize("name", ["resnet20_conv_37k", "ragged_tensors", "support_50k"])
+def test_overlapped_round_trip_matches_the_sequential_one(name):
+    """dr_roundtrip runs the receiver's probe pass on a second stream while
+    the sender fits its values; with per-kernel timing on it runs the two
+    sides one after the other.  Both give the same bytes."""
+    g, off, ratio, fpr, D, S = RT_CASES[name]
+    cfg = B.Config(off, ratio, fpr, D, S)
+    a = run_roundtrip(g, cfg)
+    B.trace_begin()
+    b = run_roundtrip(g, cfg)
+    B.trace_end()
+    for key in ("payload", "dense", "idx", "val", "counts"):
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+
+
 def test_sender_and_receiver_separately():
     """dr_payload_encode then dr_payload_decode into fresh buffers: the
     receiver needs nothing but the payload and the tensor layout."""
