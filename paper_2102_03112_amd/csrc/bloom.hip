@@ -959,7 +959,9 @@ hipError_t launch_probe_decode(const Work &w, float *dense_out, uint64_t *counts
     QueryOut o{};
     o.counts_out = counts_out;
     o.dense_out = dense_out;
-    k_probe<Q_DECODE><<<min((uint32_t)probe_grid(w), max_blocks), PB_THREADS, 0, s>>>(w, o);
+    // std::min: HIP's host min() takes ints, and max_blocks may be ~0u
+    const uint32_t grid = std::min<uint32_t>((uint32_t)probe_grid(w), std::max<uint32_t>(1u, max_blocks));
+    k_probe<Q_DECODE><<<grid, PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_DECODE>");
     return launch_tile_scan(w, 2, nullptr, s, counts_out);
 }
