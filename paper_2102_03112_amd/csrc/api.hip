@@ -539,6 +539,7 @@ struct Decode {
     uint32_t *idx_out;
     float *val_out;
     uint64_t *counts_out;
+    bool general;  // chord runs or the double exponential: the emit pass that handles them
 };
 
 dr_status decode_prepare(const uint8_t *payload, const dr_config *cfg, float *dense_out, uint32_t *idx_out,
@@ -560,6 +561,7 @@ dr_status decode_prepare(const uint8_t *payload, const dr_config *cfg, float *de
     dd.idx_out = idx_out;
     dd.val_out = val_out;
     dd.counts_out = counts_out;
+    dd.general = cfg->segmentation != DR_SEG_EQUAL || cfg->fit_model != DR_FIT_POLY;
     return DR_OK;
 }
 
@@ -581,7 +583,7 @@ dr_status decode_front(Decode &dd, uint32_t max_probe_blocks, bool query_only, h
 }
 
 dr_status decode_back(Decode &dd, hipStream_t s) {
-    DR_HIP(launch_emit_decode(dd.w, dd.dense_out, dd.idx_out, dd.val_out, dd.counts_out, s));
+    DR_HIP(launch_emit_decode(dd.w, dd.dense_out, dd.idx_out, dd.val_out, dd.counts_out, dd.general, s));
     return DR_OK;
 }
 

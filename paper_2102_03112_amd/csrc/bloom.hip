@@ -685,6 +685,10 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 // sigma[vn].  A rank outside the record, or run starts that do not bracket
 // it, flag the tensor and read as 0.  kn: the run starts of a chord-
 // segmented record (staged in LDS, or the record's own).
+// GEN: records may use chord runs or the double exponential; without it
+// (the usual equal runs of polynomials) the kernels stay at half the
+// registers.
+template <bool GEN>
 __device__ __forceinline__ float positive_value(const RecordView &rv, const float *cf, const uint32_t *kn,
                                                 uint32_t vn, TDesc &td, uint64_t *counts_out, uint32_t t) {
     if (vn >= rv.nv) return 0.0f;
@@ -692,7 +696,7 @@ __device__ __forceinline__ float positive_value(const RecordView &rv, const floa
     uint32_t s, lo, ns;
     bool good = rank < rv.nv;
     if (good) {
-        if (rv.segmode == SEG_CHORD)
+        if (GEN && rv.segmode == SEG_CHORD)
             good = run_of_rank_knots(kn, rank, rv.nv, rv.seff, &s, &lo, &ns);
         else
             run_of_rank(rank, rv.nv, rv.seff, &s, &lo, &ns);
@@ -704,7 +708,7 @@ __device__ __forceinline__ float positive_value(const RecordView &rv, const floa
     }
     const double tt = abscissa(rank - lo, ns);
     const float *row = cf + s * (rv.deff + 1u);
-    if (rv.model == FIT_DEXP)
+    if (GEN && rv.model == FIT_DEXP)
         return (float)((double)row[0] * exp((double)row[1] * tt) + (double)row[2] * exp((double)row[3] * tt));
     return horner(row, rv.deff, tt);
 }
@@ -740,7 +744,21 @@ __device__ __forceinline__ void stage_record(const RecordView &rv, float *cf, ui
     }
 }
 
-template <int MODE>
+// records of another layout than the kernel's (GEN) decode as empty and are
+// flagged: the receiver's configuration sizes the records, so it names the
+// segmentation and the model the sender used
+template <bool GEN>
+__device__ __forceinline__ void match_layout(RecordView &rv, TDesc &td, uint64_t *counts_out, uint32_t t) {
+    if (!GEN && (rv.segmode != SEG_EQUAL || rv.model != FIT_POLY)) {
+        rv.nv = 0;
+        if (threadIdx.x == 0) {
+            atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+            if (counts_out) atomicOr((unsigned long long *)&counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
+        }
+    }
+}
+
+template <int MODE, bool GEN = false>
 __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     __shared__ uint32_t scratch[NWAVES + 1];
     __shared__ uint32_t pw[TILE_WORDS];
@@ -785,6 +803,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
         if (MODE == Q_DECODE) {
             bool ok = true;
             rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
+            match_layout<GEN>(rv, td, o.counts_out, t);
             // the receiver's own positives, and the header's values count
             npos = td.nv_dec;
             ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
@@ -834,8 +853,8 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             } else if (MODE == Q_PLAIN) {
                 if (q < o.cap) o.idx_out[q] = i;
             } else {
-                const float y =
-                    positive_value(rv, cfu, knu, policy_slot(q, npos, ncoded, policy, pseed), td, o.counts_out, t);
+                const float y = positive_value<GEN>(rv, cfu, knu, policy_slot(q, npos, ncoded, policy, pseed), td,
+                                                    o.counts_out, t);
                 o.dense_out[toff_el + i] = y;  // zeros elsewhere come from the probe pass
                 const uint64_t at = toff_el + q;
                 if (o.idx_out) o.idx_out[at] = i;
@@ -900,7 +919,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
             __syncthreads();
             for (uint32_t x = threadIdx.x; x < tot; x += NTHREADS) {
                 const uint32_t vn = policy_slot(q0 + x, npos, ncoded, rv.policy, rv.seed);
-                acc[slot[x]] += positive_value(rv, cfu, knu, vn, td, o.counts_out, v);
+                acc[slot[x]] += positive_value<true>(rv, cfu, knu, vn, td, o.counts_out, v);
             }
             __syncthreads();  // pw, pre, slot, cf and kn are rewritten by the next payload
         }
@@ -924,7 +943,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
 static int probe_grid(const Work &w) {
     const uint32_t cus = (uint32_t)device_cus();
     const uint32_t by_tiles = (w.ntiles_total + PB_TILES - 1) / PB_TILES;
-    return (int)max(1u, min(cus, by_tiles));
+    return (int)std::max(1u, std::min(cus, by_tiles));
 }
 
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
@@ -967,13 +986,17 @@ hipError_t launch_probe_decode(const Work &w, float *dense_out, uint64_t *counts
 }
 
 hipError_t launch_emit_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
-                              uint64_t *counts_out, hipStream_t s) {
+                              uint64_t *counts_out, bool general, hipStream_t s) {
     QueryOut o{};
     o.counts_out = counts_out;
     o.dense_out = dense_out;
     o.idx_out = idx_out;
     o.val_out = val_out;
-    k_emit<Q_DECODE><<<resident_grid(k_emit<Q_DECODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
+    if (general)
+        k_emit<Q_DECODE, true><<<resident_grid(k_emit<Q_DECODE, true>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(
+            w, o);
+    else
+        k_emit<Q_DECODE><<<resident_grid(k_emit<Q_DECODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_DECODE>");
     return hipGetLastError();
 }

@@ -79,7 +79,7 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
 hipError_t launch_probe_decode(const Work &w, float *dense_out, uint64_t *counts_out, uint32_t max_blocks,
                                hipStream_t s);
 hipError_t launch_emit_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,
-                              uint64_t *counts_out, hipStream_t s);
+                              uint64_t *counts_out, bool general, hipStream_t s);
 // Several payloads of one tensor layout into one dense sum: the work's
 // tensors are payload-major (tensor t of payload p is p * ntens + t).
 hipError_t launch_query_decode_sum(const Work &w, uint32_t npay, uint32_t ntens, uint32_t ntiles1, float scale,

@@ -391,7 +391,7 @@ hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s) {
     const uint32_t cus = (uint32_t)device_cus();
     k_sort_upfront<<<cus, NTHREADS, 0, s>>>(w, w.keyA);
     trace_mark(s, "k_sort_upfront");
-    const int grid = (int)max(1u, min(cap_tiles, cus * 4u));
+    const int grid = (int)std::max(1u, std::min(cap_tiles, cus * 4u));
     uint32_t *kin = w.keyA, *vin = w.valA, *kout = w.keyB, *vout = w.valB;
     for (uint32_t p = 0; p < 4; ++p) {
         k_sort_pass<<<grid, NTHREADS, 0, s>>>(w, kin, vin, kout, vout, p);
