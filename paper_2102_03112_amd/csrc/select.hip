@@ -174,33 +174,42 @@ __device__ void find_from_top(const uint32_t *cnt, uint32_t need, uint32_t *res_
     __syncthreads();
 }
 
-// One block per tensor: the bin b1 that holds the r-th largest magnitude.
-__global__ __launch_bounds__(NTHREADS) void k_topr_pick(Work w) {
-    TDesc &td = w.td[blockIdx.x];
-    if (td.in.r == R_NONZERO) return;
-    __shared__ uint32_t res_bin, res_above;
-    __shared__ uint32_t scratch[NWAVES + 1];
+// The bin b1 that holds the r-th largest magnitude of top-r tensor t, from
+// its histogram (block-wide, every thread gets it).  Every filter block
+// finds it for its own tiles' tensor, hidden under its first tile's reads;
+// the block holding the tensor's first tile records b1, how many to take
+// from it and its size for the passes after.
+struct PickLds {
+    uint32_t res_bin, res_above;
+    uint32_t scratch[NWAVES + 1];
+};
+
+__device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) {
+    TDesc &td = w.td[t];
     const uint32_t r = td.in.r;
     if (r == 0) {
-        if (threadIdx.x == 0) {
+        if (record && threadIdx.x == 0) {
             td.b1 = HIST1_BINS;  // nothing above, nothing in the bin
             td.need1 = 0;
             td.ncand = 0;
         }
-        return;
+        return HIST1_BINS;
     }
     if (threadIdx.x == 0) {
-        res_bin = 0;
-        res_above = 0;
+        l.res_bin = 0;
+        l.res_above = 0;
     }
     __syncthreads();
-    const uint32_t *hist = w.hist + (uint64_t)blockIdx.x * HIST1_BINS;
-    find_from_top<HIST1_BINS, NTHREADS>(hist, r, &res_bin, &res_above, scratch);
-    if (threadIdx.x == 0) {
-        td.b1 = res_bin;
-        td.need1 = r - res_above;
-        td.ncand = hist[res_bin];
+    const uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
+    find_from_top<HIST1_BINS, NTHREADS>(hist, r, &l.res_bin, &l.res_above, l.scratch);
+    const uint32_t b1 = l.res_bin;
+    if (record && threadIdx.x == 0) {
+        td.b1 = b1;
+        td.need1 = r - l.res_above;
+        td.ncand = hist[b1];
     }
+    __syncthreads();  // l is reused
+    return b1;
 }
 
 // ---------------------------------------------------------------------------
@@ -217,7 +226,7 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_pick(Work w) {
 // next tile's values are requested: waiting for them afterwards would also
 // wait for those values.
 struct FilterTile {
-    uint32_t t, base, d, b1;
+    uint32_t t, base, d;
     uint64_t slot, off;
     bool nz;
 };
@@ -231,7 +240,6 @@ __device__ __forceinline__ FilterTile filter_tile(const Work &w, uint32_t tile) 
     f.slot = td.in.slot;
     f.off = td.in.off;
     f.nz = td.in.r == R_NONZERO;
-    f.b1 = f.nz ? 0u : td.b1;
     return f;
 }
 
@@ -249,9 +257,11 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
     __shared__ uint32_t dcnt[NWAVES];
     __shared__ uint32_t sbw[TILE_WORDS];
     __shared__ uint32_t bad;
+    __shared__ PickLds pl;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     if (threadIdx.x == 0) bad = 0;
     __syncthreads();
+    uint32_t b1_t = 0xffffffffu, b1_c = 0;  // tensor whose b1 the block holds, and b1
     // the next tile's values are in flight while this tile is classified
     float xn[16];
     FilterTile fn{};
@@ -269,7 +279,11 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         if (more) filter_load(g, fn, xn);
         // keeps the scheduler from sinking the loads next to their uses
         asm volatile("" ::: "memory");
-        const uint32_t base = f.base, d = f.d, b1 = f.b1;
+        if (!f.nz && f.t != b1_t) {
+            b1_c = pick_b1(w, f.t, f.base == 0, pl);
+            b1_t = f.t;
+        }
+        const uint32_t base = f.base, d = f.d, b1 = f.nz ? 0u : b1_c;
         const uint64_t slot = f.slot;
         const bool nz = f.nz;
         uint32_t keys[16];
@@ -575,8 +589,6 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
     if (any_topr) {
         k_topr_hist<<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
         trace_mark(s, "k_topr_hist");
-        k_topr_pick<<<w.ntensors, NTHREADS, 0, s>>>(w);
-        trace_mark(s, "k_topr_pick");
     }
     k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
