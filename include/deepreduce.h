@@ -295,8 +295,17 @@ DR_EXPORT dr_status dr_payload_decode_sum(const uint8_t *const *payloads_h, uint
                                           float scale, float *dense_out, uint64_t *counts_out, void *ws,
                                           size_t ws_bytes, void *stream);
 
-/* dr_payload_encode followed by dr_payload_decode on one stream: one codec
- * round trip of the whole gradient. */
+/* dr_payload_encode followed by dr_payload_decode: one codec round trip of
+ * the whole gradient, with the same results.  The receiver's query pass
+ * needs only the records' headers and filters, so once the sender has
+ * written them the library runs it on a second stream of its own (one per
+ * device, created on first use) while the sender sorts and fits its values;
+ * the second stream waits for `stream` and `stream` waits for it before the
+ * receiver's last pass, so the call stays ordered on `stream` (also under
+ * graph capture).  This needs room in `ws` for the receiver's own state
+ * after the sender's (dr_workspace_bytes leaves it for the usual layouts);
+ * otherwise, and with chord segmentation or the heuristic run count, the
+ * two sides run one after the other. */
 DR_EXPORT dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
                        float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
                        size_t ws_bytes, void *stream);
@@ -315,8 +324,12 @@ DR_EXPORT dr_status dr_trace_begin(void *stream);
 
 /* Stop timing, wait for the recorded events, and write one line per kernel
  * name into buf_h (NUL-terminated, truncated to buf_bytes): "<kernel>
- * <launches> <total milliseconds>\n".  Idle time between entry points is
- * not attributed to any kernel.  EINVAL if tracing was not begun. */
+ * <launches> <total milliseconds>\n".  A kernel's time runs from the
+ * previous event on its own stream; dr_roundtrip runs part of the receiver
+ * on a second stream beside the sender, so the times of kernels on the two
+ * streams overlap and may add up to more than the elapsed time.  Idle time
+ * between entry points is not attributed to any kernel.  EINVAL if tracing
+ * was not begun. */
 DR_EXPORT dr_status dr_trace_end(char *buf_h, size_t buf_bytes);
 
 #ifdef __cplusplus

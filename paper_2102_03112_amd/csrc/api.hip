@@ -623,17 +623,14 @@ bool side_stream(SideStream **out) {
     return true;
 }
 
-bool tracing_on();
-
 // dr_roundtrip: the receiver's probe pass needs only the payload's header
 // and filter, which the sender has written once its values' layout is set,
 // so it runs on a second stream while the sender sorts and fits its values
 // (the probe is bound by L2 request throughput and loses little when some
 // CUs are left to the sort and the fit).  The receiver then
 // uses its own query-only work after the sender's in the workspace; without
-// room for it, with segmentation passes that rewrite the header after the
-// sort, or while per-kernel timing is on, the two sides run one after the
-// other.
+// room for it, or with segmentation passes that rewrite the header after
+// the sort, the two sides run one after the other.
 dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
                          float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
                          size_t ws_bytes, hipStream_t s) {
@@ -646,7 +643,7 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     const Carve qc = query_carve(dd.p);
     const size_t qoff = align_up(e.p.carve.bytes, 256);
     SideStream *ss = nullptr;
-    const bool overlap = !e.p.segment && !tracing_on() && qoff + qc.bytes <= ws_bytes && side_stream(&ss);
+    const bool overlap = !e.p.segment && qoff + qc.bytes <= ws_bytes && side_stream(&ss);
     trace_call(s);
     st = encode_front(e, g, counts_out, s);
     if (st != DR_OK) return st;
@@ -661,6 +658,7 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     std::lock_guard<std::mutex> lock(g_side_mu);  // one fork/join sequence at a time per process
     DR_HIP(hipEventRecord(ss->fork, s));
     DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
+    trace_call(ss->s);  // per-kernel timing: the side stream's kernels count from here
     // CUs left to the sender: the sort and the fit want a few dozen when
     // the probe pass is short; for long probe passes (large gradients) each
     // CU taken from the probe costs more than the sender gains (measured on
@@ -741,6 +739,7 @@ Plan single_plan(uint64_t d) {
 struct TraceMark {
     const char *name;  // null: boundary at the start of an entry point (its interval is idle time)
     hipEvent_t ev;
+    hipStream_t s;     // a kernel's time runs from the previous mark on the same stream
 };
 struct Tracer {
     bool on = false;
@@ -762,13 +761,12 @@ void trace_record(hipStream_t s, const char *name) {
         g_trace.pool.push_back(ev);
         return;
     }
-    g_trace.marks.push_back({name, ev});
+    g_trace.marks.push_back({name, ev, s});
 }
 
 // every entry point that launches work marks its start
 void trace_call(hipStream_t s) { trace_record(s, nullptr); }
 
-bool tracing_on() { return g_trace.on; }
 
 }  // namespace
 
@@ -818,8 +816,11 @@ dr_status dr_trace_end(char *buf_h, size_t buf_bytes) {
     }
     for (size_t i = 1; st == DR_OK && i < g_trace.marks.size(); ++i) {
         if (!g_trace.marks[i].name) continue;
+        size_t p = i - 1;  // the previous mark on the kernel's stream
+        while (p > 0 && g_trace.marks[p].s != g_trace.marks[i].s) --p;
+        if (g_trace.marks[p].s != g_trace.marks[i].s) continue;
         float ms = 0.f;
-        if (hipEventElapsedTime(&ms, g_trace.marks[i - 1].ev, g_trace.marks[i].ev) != hipSuccess) continue;
+        if (hipEventElapsedTime(&ms, g_trace.marks[p].ev, g_trace.marks[i].ev) != hipSuccess) continue;
         size_t j = 0;
         while (j < names.size() && names[j] != g_trace.marks[i].name) ++j;
         if (j == names.size()) {

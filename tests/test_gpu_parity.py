@@ -371,16 +371,44 @@ def test_roundtrip_is_deterministic():
 @pytest.mark.parametrize("name", ["resnet20_conv_37k", "ragged_tensors", "support_50k"])
 def test_overlapped_round_trip_matches_the_sequential_one(name):
     """dr_roundtrip runs the receiver's probe pass on a second stream while
-    the sender fits its values; with per-kernel timing on it runs the two
-    sides one after the other.  Both give the same bytes."""
+    the sender fits its values; dr_payload_encode then dr_payload_decode run
+    the two sides one after the other.  Both give the same bytes."""
+    import torch
+
     g, off, ratio, fpr, D, S = RT_CASES[name]
     cfg = B.Config(off, ratio, fpr, D, S)
     a = run_roundtrip(g, cfg)
-    B.trace_begin()
-    b = run_roundtrip(g, cfg)
-    B.trace_end()
+    total, _ = B.payload_layout(cfg)
+    d = g.size
+    ws = workspace(max(d, 1), cfg.n_tensors)
+    payload = torch.zeros(total, dtype=torch.uint8, device="cuda")
+    dense = torch.full((max(d, 1),), 9.0, dtype=torch.float32, device="cuda")
+    idx = torch.full((max(d, 1),), -1, dtype=torch.int32, device="cuda")
+    val = torch.zeros(max(d, 1), dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4 * cfg.n_tensors, dtype=torch.int64, device="cuda")
+    gd = dev_tensor(g) if d else torch.zeros(1, dtype=torch.float32, device="cuda")
+    B.payload_encode(gd, cfg, payload, counts, ws)
+    B.payload_decode(payload, cfg, dense, idx, val, counts, ws)
+    sync()
+    b = dict(payload=host(payload), dense=host(dense)[:d], idx=host(idx)[:d].view(np.uint32), val=host(val)[:d],
+             counts=host(counts).reshape(cfg.n_tensors, 4))
     for key in ("payload", "dense", "idx", "val", "counts"):
         np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+
+
+def test_trace_attributes_both_streams():
+    """Per-kernel timing follows each stream: the receiver's probe pass on
+    the second stream is timed from the fork, not from the sender's last
+    kernel."""
+    w = W.WORKLOADS["normal_1m"]
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w)
+    run_roundtrip(g, cfg)
+    B.trace_begin()
+    run_roundtrip(g, cfg)
+    tr = B.trace_end()
+    for k in ("k_probe<Q_ENCODE>", "k_probe<Q_DECODE>", "k_sort_pass", "k_emit<Q_DECODE>"):
+        assert k in tr and tr[k][0] >= 1 and tr[k][1] > 0, k
 
 
 def test_sender_and_receiver_separately():
