@@ -670,6 +670,7 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     st = encode_back(e, s);
     if (st != DR_OK) return st;
     DR_HIP(hipStreamWaitEvent(s, ss->join, 0));
+    trace_call(s);  // per-kernel timing: the wait for the join is idle time
     return decode_back(dd, s);
 }
 
