@@ -43,7 +43,10 @@ def _bounds(refs_per_payload, offsets, d, tol=1e-5):
             run_max = np.zeros(max(r.fit.S_eff, 1))
             if r.fit.n:
                 ranks = oracle.sigma_unpack(r.fit.sigma, r.fit.n).astype(np.int64)
-                s_of_vn = ((ranks + 1) * r.fit.S_eff - 1) // r.fit.n
+                if r.fit.seg_mode == oracle.SEG_CHORD:
+                    s_of_vn = np.searchsorted(r.fit.bounds.astype(np.int64), ranks, side="right") - 1
+                else:
+                    s_of_vn = ((ranks + 1) * r.fit.S_eff - 1) // r.fit.n
                 s = np.zeros(r.P_dec.size, np.int64)
                 s[kept] = s_of_vn[r.slots[kept].astype(np.int64)]
                 np.maximum.at(run_max, s[kept], y[kept])
@@ -71,12 +74,16 @@ def _check(out, want, refs, offsets, d, n, scale):
 
 
 CASES = {
-    # name: (d, offsets, ratio, fpr, D, S, n payloads, policy)
+    # name: (d, offsets, ratio, fpr, D, S, n payloads, policy[, segmentation, model])
     "resnet20_x8": (36_864, [0, 36_864], (1, 100), 1e-3, 5, 8, 8, oracle.POLICY_P0),
     "ragged_x3": (8203, [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8, 3, oracle.POLICY_P0),
     "two_tensors_x5_p1": (300_000, [0, 123_457, 300_000], (1, 100), 1e-2, 3, 4, 5, oracle.POLICY_RANDOM),
     "support_x2": (50_000, [0, 50_000], None, 1e-4, 3, 16, 2, oracle.POLICY_P0),
     "one_payload": (100_000, [0, 100_000], (1, 100), 1e-3, 5, 8, 1, oracle.POLICY_P0),
+    "chord_dexp_x3": (120_000, [0, 50_000, 120_000], (1, 100), 1e-3, 3, 4, 3, oracle.POLICY_P0, oracle.SEG_CHORD,
+                      oracle.FIT_DEXP),
+    "chord_poly_x4": (80_000, [0, 80_000], (1, 50), 1e-3, 2, 6, 4, oracle.POLICY_P0, oracle.SEG_CHORD,
+                      oracle.FIT_POLY),
 }
 
 
@@ -84,13 +91,14 @@ CASES = {
 def test_decode_sum_parity(name):
     import torch
 
-    d, off, ratio, fpr, D, S, n, policy = CASES[name]
+    d, off, ratio, fpr, D, S, n, policy, *rest = CASES[name]
+    seg, model = rest if rest else (oracle.SEG_EQUAL, oracle.FIT_POLY)
     log(f"decode_sum {name} d={d} payloads={n}")
     if ratio is None:
         gs = [W.sparse_normal(d, 300 + p, 0.4) for p in range(n)]
     else:
         gs = [W.normal(d, 300 + p, scale=1e-3) for p in range(n)]
-    cfg = B.Config(off, ratio, fpr, D, S, policy, 99)
+    cfg = B.Config(off, ratio, fpr, D, S, policy, 99, seg, model)
     pays = _encode_all(gs, cfg)
     scale = 1.0 / n
     dense = torch.full((max(d, 1),), 5.0, dtype=torch.float32, device="cuda")
@@ -98,7 +106,8 @@ def test_decode_sum_parity(name):
     B.payload_decode_sum(pays, cfg, scale, dense, counts, workspace(d, cfg.n_tensors))
     sync()
     out = host(dense)[:d]
-    refs = [oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=99) for g in gs]
+    refs = [oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=99, seg_mode=seg, model=model)
+            for g in gs]
     want = oracle.decode_sum(refs, d, off, scale)
     _check(out, want, refs, off, d, n, scale)
     c = host(counts).reshape(n, cfg.n_tensors, 4)
