@@ -604,9 +604,10 @@ struct SideStream {
     hipStream_t s = nullptr;
     hipEvent_t fork = nullptr, join = nullptr;
 };
-std::mutex g_side_mu;
+std::mutex g_side_mu;  // guards creation and each fork/join sequence
 SideStream g_side[64];
 
+// the current device's side stream; call with g_side_mu held
 bool side_stream(SideStream **out) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return false;
@@ -642,8 +643,12 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     if (st != DR_OK) return st;
     const Carve qc = query_carve(dd.p);
     const size_t qoff = align_up(e.p.carve.bytes, 256);
+    // one fork/join sequence at a time per process, so that the two events
+    // are not re-recorded by another thread between a record and its wait
+    std::unique_lock<std::mutex> lock(g_side_mu);
     SideStream *ss = nullptr;
     const bool overlap = !e.p.segment && qoff + qc.bytes <= ws_bytes && side_stream(&ss);
+    if (!overlap) lock.unlock();
     trace_call(s);
     st = encode_front(e, g, counts_out, s);
     if (st != DR_OK) return st;
@@ -655,7 +660,6 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
         return decode_back(dd, s);
     }
     dd.w = qc.view((uint8_t *)ws + qoff);
-    std::lock_guard<std::mutex> lock(g_side_mu);  // one fork/join sequence at a time per process
     DR_HIP(hipEventRecord(ss->fork, s));
     DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
     trace_call(ss->s);  // per-kernel timing: the side stream's kernels count from here
