@@ -9,8 +9,10 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <map>
 #include <mutex>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "deepreduce.h"
@@ -791,6 +793,21 @@ int device_cus() {
     return cus[slot];
 }
 void trace_mark(hipStream_t s, const char *kernel) { trace_record(s, kernel); }
+
+int blocks_per_cu(const void *kernel, int threads) {
+    static std::mutex mu;
+    static std::map<std::tuple<const void *, int, int>, int> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+    const auto key = std::make_tuple(kernel, threads, dev);
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
+    cache[key] = n;
+    return n;
+}
 }  // namespace dr
 
 // ---------------------------------------------------------------------------

@@ -13,21 +13,17 @@ namespace dr {
 
 int device_cus();  // compute units of the current device
 
+// Resident blocks per CU of `kernel` at `threads` threads on the current
+// device (hipOccupancyMaxActiveBlocksPerMultiprocessor), cached per kernel
+// address, block size and device.
+int blocks_per_cu(const void *kernel, int threads);
+
 // A grid of persistent blocks: as many as can be resident at once on the
 // current device (so every block starts at once and none waits for another
-// to finish), but no more than `work` units.  Cached per kernel and device.
+// to finish), but no more than `work` units.
 template <typename K>
 int resident_grid(K kernel, int threads, uint32_t work) {
-    static int per_cu[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
-    const int slot = dev < 64 ? dev : 63;
-    if (per_cu[slot] == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
-        per_cu[slot] = n;
-    }
-    const uint32_t g = (uint32_t)(per_cu[slot] * device_cus());
+    const uint32_t g = (uint32_t)(blocks_per_cu((const void *)kernel, threads) * device_cus());
     return (int)(work < g ? (work ? work : 1u) : g);
 }
 
