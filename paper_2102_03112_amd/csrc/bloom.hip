@@ -516,12 +516,14 @@ __device__ __forceinline__ RecordView query_filter(const Work &w, const QueryOut
 
 // One filter word: from the LDS copy of the filter's first `fcw` words, else
 // from global memory (an L2 hit: the filter is small and read by every CU).
+// A lane that is not `live` (an empty queue slot) makes no memory request.
 __device__ __forceinline__ uint32_t filter_word(const uint32_t *fc, uint32_t fcw, __amdgpu_buffer_rsrc_t rs,
-                                                uint32_t wi) {
+                                                uint32_t wi, bool live = true) {
     const bool in_lds = wi < fcw;
     const uint32_t l = fc[in_lds ? wi : 0u];
-    // the offset of a word held in LDS lies past the view: no memory access
-    const uint32_t g = buffer_u32(rs, in_lds ? 0xfffffff0u : wi * 4u);
+    // the offset of a word held in LDS, or of a dead lane, lies past the
+    // view: no memory access
+    const uint32_t g = buffer_u32(rs, (in_lds || !live) ? 0xfffffff0u : wi * 4u);
     return in_lds ? l : g;
 }
 
@@ -537,7 +539,14 @@ __device__ __forceinline__ uint32_t filter_word(const uint32_t *fc, uint32_t fcw
 // runs that stay inside one tensor; the LDS copy is reloaded only when a
 // run enters a new tensor.  Inside a run, waves take quarter tiles (1024
 // indices) from a shared counter, so they stay busy until the run ends.
+//
+// Each probe round costs a wave one L2 round trip.  Once a quarter's
+// survivors fit in one 64-lane group (mostly positives, which take every
+// probe), the round trips, not the reads, are the cost: the next TAIL_PROBES
+// probes are then read together.  A survivor that fails the first of them
+// costs one read it did not need.
 constexpr uint32_t RUN_TILES = 512;  // most tiles per run (LDS tile counters)
+constexpr uint32_t TAIL_PROBES = 2;  // probes per round once the survivors fit one group
 
 template <int MODE>
 __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
@@ -639,6 +648,28 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
             for (uint32_t j = 1; j < k && cnt > 0; ++j) {
                 __builtin_amdgcn_wave_barrier();
                 const uint32_t L = cnt;
+                if (L <= 64) {
+                    // survivor x in lane x; probes j .. j + S - 1 in flight together
+                    const uint32_t S = min(k - j, TAIL_PROBES);
+                    const bool act = lane < L;
+                    const uint32_t e = act ? me[lane] : 0u;
+                    const uint32_t key = mm3_key(wbase + e);
+                    uint32_t all = 1u;
+#pragma unroll
+                    for (uint32_t u = 0; u < TAIL_PROBES; ++u) {
+                        if (u < S) {
+                            const uint32_t p = bloom_pos(key, j + u, m_bits);
+                            all &= filter_word(fc, fcw, bits, p >> 5, act) >> (p & 31u);
+                        }
+                    }
+                    const bool hit = act && (all & 1u);
+                    __builtin_amdgcn_wave_barrier();
+                    const uint64_t mask = ballot(hit);
+                    if (hit) me[lanes_below(mask)] = (uint16_t)e;
+                    cnt = popc64(mask);
+                    j += S - 1;
+                    continue;
+                }
                 cnt = 0;
                 for (uint32_t b0 = 0; b0 < L; b0 += 64 * G) {
                     uint32_t ev[G], bw[G];
@@ -646,16 +677,20 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
                     for (uint32_t u = 0; u < G; ++u) {
                         const uint32_t x = b0 + u * 64 + lane;
                         ev[u] = x < L ? me[x] : 0u;
+                        bw[u] = 0u;
                     }
 #pragma unroll
                     for (uint32_t u = 0; u < G; ++u) {
+                        if (b0 + u * 64 >= L) break;  // this group and the ones after it are empty
+                        const bool live = b0 + u * 64 + lane < L;
                         const uint32_t p = bloom_pos(mm3_key(wbase + ev[u]), j, m_bits);
-                        const uint32_t word = filter_word(fc, fcw, bits, p >> 5) >> (p & 31u);
-                        bw[u] = (b0 + u * 64 + lane < L) ? word : 0u;
+                        const uint32_t word = filter_word(fc, fcw, bits, p >> 5, live) >> (p & 31u);
+                        bw[u] = live ? word : 0u;
                     }
                     __builtin_amdgcn_wave_barrier();
 #pragma unroll
                     for (uint32_t u = 0; u < G; ++u) {
+                        if (b0 + u * 64 >= L) break;
                         const bool hit = bw[u] & 1u;
                         const uint64_t mask = ballot(hit);
                         if (hit) me[cnt + lanes_below(mask)] = (uint16_t)ev[u];
