@@ -802,54 +802,61 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     __shared__ float cf[MODE == Q_DECODE ? EMIT_COEF : 1];
     __shared__ uint32_t kn[MODE == Q_DECODE ? EMIT_KNOTS : 1];
     constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);  // 4 groups of 4 elements per thread
-    uint32_t coef_t = 0xffffffffu;                     // tensor whose coefficients cf holds
-    const float *cfu = cf;                              // its coefficients: LDS or the record
+    const float *cfu = cf;                              // the tensor's coefficients: LDS or the record
     const uint32_t *knu = kn;                           // its run starts: LDS or the record
+    // The next tile's positives words, first rank and tensor are read one
+    // tile ahead, and the tensor's fields (descriptor, record header) only
+    // when the tensor changes, so a tile waits on no chain of dependent
+    // reads.  The barriers order LDS only: the read-ahead and the output
+    // stores stay in flight across them.
     uint32_t tile = blockIdx.x;
-    uint32_t word = 0, q0n = 0;
+    uint32_t word = 0, q0n = 0, tn = 0;
     if (tile < w.ntiles_total) {
         q0n = w.toff[tile];
+        tn = tensor_of_tile(w, tile);
         if (threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)tile * TILE_WORDS + threadIdx.x];
     }
+    uint32_t cur_t = 0xffffffffu, tile0 = 0, d = 0;
+    uint64_t toff_el = 0, tslot = 0;
+    RecordView rv{};
+    // the policy's view of the tensor: positives, values coded, key
+    uint32_t npos = 0, ncoded = 0, policy = POLICY_P0, pseed = 0;
     for (; tile < w.ntiles_total; tile += gridDim.x) {
-        const uint32_t t = tensor_of_tile(w, tile);
+        const uint32_t t = tn;
         TDesc &td = w.td[t];
-        // descriptor fields in registers (the output stores could alias
-        // them for all the compiler knows)
-        const uint32_t lt = tile - td.in.tile0;
-        const uint32_t d = td.in.d;
-        const uint64_t toff_el = td.in.off, tslot = td.in.slot;
+        if (t != cur_t) {
+            tile0 = td.in.tile0;
+            d = td.in.d;
+            toff_el = td.in.off;
+            tslot = td.in.slot;
+            if (MODE == Q_ENCODE) {
+                npos = td.npos;
+                ncoded = td.nv;
+                policy = td.in.policy;
+                pseed = td.in.seed;
+            }
+            if (MODE == Q_DECODE) {
+                bool ok = true;
+                rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
+                match_layout<GEN>(rv, td, o.counts_out, t);
+                // the receiver's own positives, and the header's values count
+                npos = td.nv_dec;
+                ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
+                policy = rv.policy;
+                pseed = rv.seed;
+                stage_record(rv, cf, kn, &cfu, &knu);
+            }
+            cur_t = t;
+        }
+        const uint32_t lt = tile - tile0;
         const uint32_t q0 = q0n;
         uint32_t tot;
-        const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
+        const uint32_t ex = block_excl_scan_n<NTHREADS, true>(__popc(word), scratch, &tot);
         if (threadIdx.x < TILE_WORDS) {
             pw[threadIdx.x] = word;
             pre[threadIdx.x] = ex;
         }
-        RecordView rv;
-        // the policy's view of this tensor: positives, values coded, key
-        uint32_t npos = 0, ncoded = 0, policy = POLICY_P0, pseed = 0;
-        if (MODE == Q_ENCODE) {
-            npos = td.npos;
-            ncoded = td.nv;
-            policy = td.in.policy;
-            pseed = td.in.seed;
-        }
-        if (MODE == Q_DECODE) {
-            bool ok = true;
-            rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
-            match_layout<GEN>(rv, td, o.counts_out, t);
-            // the receiver's own positives, and the header's values count
-            npos = td.nv_dec;
-            ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
-            policy = rv.policy;
-            pseed = rv.seed;
-            if (t != coef_t) {
-                stage_record(rv, cf, kn, &cfu, &knu);
-                coef_t = t;
-            }
-        }
-        __syncthreads();
+        lds_barrier();
         // A: list the positives
         uint32_t nib[GROUPS], rank0[GROUPS];
 #pragma unroll
@@ -863,14 +870,15 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             for (uint32_t v = 0; v < 4; ++v)
                 if ((nib[u] >> v) & 1u) slot[r++] = e0 + v;
         }
-        // the next tile's positives words, in flight during B and C
+        // the next tile's positives words, in flight during B
         const uint32_t nt = tile + gridDim.x;
         word = 0;
         if (nt < w.ntiles_total) {
             q0n = w.toff[nt];
+            tn = tensor_of_tile(w, nt);
             if (threadIdx.x < TILE_WORDS) word = w.pbits[(uint64_t)nt * TILE_WORDS + threadIdx.x];
         }
-        __syncthreads();
+        lds_barrier();
         // B: one positive per thread
         const uint32_t base = lt * TILE;
         for (uint32_t p = threadIdx.x; p < tot; p += NTHREADS) {
@@ -896,7 +904,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
                 if (o.val_out) o.val_out[at] = y;
             }
         }
-        __syncthreads();  // pw, pre and slot are rewritten by the next tile
+        lds_barrier();  // pw, pre, slot, cf and kn are rewritten by the next tile
     }
 }
 

@@ -227,6 +227,17 @@ __device__ __forceinline__ uint32_t bloom_pos(uint32_t kmix, uint32_t j, uint32_
 __device__ __forceinline__ uint32_t test_bit(const uint32_t *w, uint32_t p) { return (w[p >> 5] >> (p & 31u)) & 1u; }
 
 // ---------------------------------------------------------------------------
+// Block barrier for LDS traffic only: waits for this wave's LDS operations,
+// not for its global loads, stores or atomics, which stay in flight across it
+// (__syncthreads also drains those).  For barriers that order LDS accesses
+// alone; not where one thread reads global memory that another thread of
+// the block wrote before the barrier.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Wave (64-lane) primitives.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
@@ -265,14 +276,18 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 
 // Exclusive scan of one value per thread over a block of NT threads.
 // `scratch` holds NT/64+1 words of LDS; returns the block total in *total.
-// Contains barriers: every thread of the block must call it.
-template <uint32_t NT>
+// Contains barriers: every thread of the block must call it.  LDS_ONLY: its
+// barriers leave the caller's global memory operations in flight.
+template <uint32_t NT, bool LDS_ONLY = false>
 __device__ __forceinline__ uint32_t block_excl_scan_n(uint32_t v, uint32_t *scratch, uint32_t *total) {
     constexpr uint32_t NW = NT / 64;
     const uint32_t lane = threadIdx.x & 63u, w = threadIdx.x >> 6;
     uint32_t inc = wave_incl_scan(v);
     if (lane == 63) scratch[w] = inc;
-    __syncthreads();
+    if (LDS_ONLY)
+        lds_barrier();
+    else
+        __syncthreads();
     if (threadIdx.x == 0) {
         uint32_t s = 0;
         for (uint32_t i = 0; i < NW; ++i) {
@@ -282,10 +297,16 @@ __device__ __forceinline__ uint32_t block_excl_scan_n(uint32_t v, uint32_t *scra
         }
         scratch[NW] = s;
     }
-    __syncthreads();
+    if (LDS_ONLY)
+        lds_barrier();
+    else
+        __syncthreads();
     uint32_t r = scratch[w] + inc - v;
     *total = scratch[NW];
-    __syncthreads();
+    if (LDS_ONLY)
+        lds_barrier();
+    else
+        __syncthreads();
     return r;
 }
 
