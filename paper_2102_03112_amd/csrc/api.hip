@@ -108,7 +108,7 @@ struct Carve {
         o_ttab = take(4ull * ntiles);
         o_ccnt = take(all * 4 * ntiles);
         o_hist = take(all * 4ull * HIST1_BINS * ntensors);
-        o_histA = take(all * 4ull * 1024 * ntensors);
+        o_histA = take(all * 4ull * 1024 * HISTA_COPIES * ntensors);
         o_sel = take(all * slots / 8);
         o_ckey = take(all * 4 * slots);
         o_cidx = take(all * 4 * slots);
@@ -444,7 +444,7 @@ hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s, b
     if (!query_only) {
         z.z[z.n++] = {w.sdig, 4ull * SORT_BINS * w.ntensors};
         z.z[z.n++] = {w.hist, (uint64_t)HIST1_BINS * w.ntensors};
-        z.z[z.n++] = {w.histA, 1024ull * w.ntensors};
+        z.z[z.n++] = {w.histA, 1024ull * HISTA_COPIES * w.ntensors};
     }
     if (extra.p && extra.words) z.z[z.n++] = extra;
     for (size_t f = 0; f < t.size(); f += INIT_CHUNK) {

@@ -34,6 +34,10 @@ constexpr uint32_t SLICE_WORDS_MAX = (1u << SLICE_LOG2_MAX) / 32;
 constexpr uint32_t HIST1_BITS = 11;           // first top-r digit: key bits 30..20
 constexpr uint32_t HIST1_BINS = 1u << HIST1_BITS;
 constexpr uint32_t HIST1_SHIFT = 20;
+// Copies of each tensor's histogram of the candidates' key bits 19..10: the
+// filter pass's blocks add to copy (block mod HISTA_COPIES), which spreads
+// their atomics over that many times more cache lines.
+constexpr uint32_t HISTA_COPIES = 8;
 constexpr uint32_t SORT_BINS = 256;           // 8-bit LSD radix digits
 constexpr uint32_t FIT_CHUNKS = 8;            // partial-moment blocks per fitted run
 constexpr uint32_t MAX_DEG = 7;
@@ -171,7 +175,7 @@ struct Work {
     uint32_t *selbits;        // selection bitmap (paper's d-bit string B), slots / 32 words
     uint32_t *cand_key;       // top-r candidates (keys), per tensor slot
     uint32_t *cand_idx;       // top-r candidates (indices)
-    uint32_t *histA;          // top-r: per-tensor histogram of the candidates' key bits 19..10 (1024 bins)
+    uint32_t *histA;          // top-r: per tensor, HISTA_COPIES histograms of the candidates' key bits 19..10 (1024 bins)
     uint32_t *sub_key;        // top-r short list (borrows P, which is written later)
     uint32_t *sub_idx;        // top-r short list (borrows V)
     uint32_t *S;              // selected indices, per tensor slot

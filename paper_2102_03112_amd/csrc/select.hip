@@ -8,10 +8,11 @@
 //      histograms, reduced without global atomics), pick the bin b1 that
 //      holds the r-th largest key;
 //   2. one pass over the tensor marks every element above b1 in the
-//      selection bitmap (the d-bit string B of Section 3) and compacts the
-//      elements of bin b1 into an index-ordered candidate list;
-//   3. one block per tensor finishes the select on the candidates' low 20
-//      key bits and resolves ties at the threshold by index order.
+//      selection bitmap (the d-bit string B of Section 3), compacts the
+//      elements of bin b1 into an index-ordered candidate list and counts
+//      them by key bits 19..10;
+//   3. the select finishes on the candidates' low 20 key bits and resolves
+//      ties at the threshold by index order.
 // The support of an inherently sparse gradient (Section 3) is the bitmap of
 // nonzeros, written by the same pass.
 #include "launch.hpp"
@@ -259,6 +260,7 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
     __shared__ uint32_t bad;
     __shared__ PickLds pl;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    const uint32_t hcopy = blockIdx.x % HISTA_COPIES;
     if (threadIdx.x == 0) bad = 0;
     __syncthreads();
     uint32_t b1_t = 0xffffffffu, b1_c = 0;  // tensor whose b1 the block holds, and b1
@@ -336,12 +338,14 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         }
         if (threadIdx.x < TILE_WORDS) w.selbits[((slot + base) >> 5) + threadIdx.x] = sbw[threadIdx.x];
         const uint64_t cbase = slot + base;
+        uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * 1024u;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             if ((cmask[j] >> lane) & 1ull) {
                 const uint64_t q = cbase + woff[j * NWAVES + wv] + lanes_below(cmask[j]);
                 w.cand_key[q] = keys[j];
                 w.cand_idx[q] = base + j * NTHREADS + threadIdx.x;
+                atomicAdd(&histA[(keys[j] >> 10) & 1023u], 1u);
             }
         }
         __syncthreads();
@@ -351,38 +355,13 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
 // ---------------------------------------------------------------------------
 // top-r step 3: finish the select on the candidates' low 20 key bits.
 //  a. one block per tensor picks the bin bA of key bits 19..10 from the
-//     histogram the filter pass built;
+//     histograms the filter pass built;
 //  b. a pass over the candidates marks those above bA and gathers those in
 //     bA (usually a few dozen) into a short list;
 //  c. one block per tensor finishes on the short list: bin of bits 9..0,
 //     then, if equal keys straddle the cut, the smallest indices among them.
 // ---------------------------------------------------------------------------
 constexpr uint32_t SEL_THREADS = 1024;
-
-// Histogram of key bits 19..10 of the candidates, one partial row per
-// top-r histogram block (same tile ranges as the first pass); one wave
-// takes one tile's candidates at a time.
-__global__ __launch_bounds__(SEL_THREADS) void k_topr_candhist(Work w) {
-    __shared__ uint32_t h[1024];
-    h[threadIdx.x] = 0;
-    __syncthreads();
-    const int t = tensor_of_hist_block(w, blockIdx.x);
-    if (t < 0) return;
-    const TDesc &td = w.td[t];
-    const uint32_t lb = blockIdx.x - td.in.hb0;
-    const uint32_t per = (td.in.ntiles + td.in.hbn - 1) / td.in.hbn;
-    const uint32_t tl0 = lb * per, tl1 = min(td.in.ntiles, tl0 + per);
-    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
-    if (td.ncand > 0) {
-        for (uint32_t tl = tl0 + wv; tl < tl1; tl += SEL_THREADS / 64) {
-            const uint32_t c = w.ccnt[td.in.tile0 + tl];
-            const uint32_t *ck = w.cand_key + td.in.slot + (uint64_t)tl * TILE;
-            for (uint32_t j = lane; j < c; j += 64) atomicAdd(&h[(ck[j] >> 10) & 1023u], 1u);
-        }
-    }
-    __syncthreads();
-    if (h[threadIdx.x]) atomicAdd(&w.histA[(uint64_t)t * 1024u + threadIdx.x], h[threadIdx.x]);
-}
 
 __global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
     TDesc &td = w.td[blockIdx.x];
@@ -401,8 +380,16 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
         res_above = 0;
     }
     __syncthreads();
-    const uint32_t *histA = w.histA + (uint64_t)blockIdx.x * 1024u;
-    find_from_top<1024, SEL_THREADS>(histA, td.need1, &res_bin, &res_above, scratch);
+    __shared__ uint32_t hsum[1024];
+    const uint32_t *histA = w.histA + (uint64_t)blockIdx.x * HISTA_COPIES * 1024u;
+    for (uint32_t b = threadIdx.x; b < 1024u; b += SEL_THREADS) {
+        uint32_t c = 0;
+#pragma unroll
+        for (uint32_t q = 0; q < HISTA_COPIES; ++q) c += histA[q * 1024u + b];
+        hsum[b] = c;
+    }
+    __syncthreads();
+    find_from_top<1024, SEL_THREADS>(hsum, td.need1, &res_bin, &res_above, scratch);
     if (threadIdx.x == 0) {
         td.bA = res_bin;
         td.needA = td.need1 - res_above;
@@ -593,8 +580,6 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
     k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     if (any_topr) {
-        k_topr_candhist<<<hist_blocks, SEL_THREADS, 0, s>>>(w);
-        trace_mark(s, "k_topr_candhist");
         k_topr_pickA<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_pickA");
         k_topr_candpass<<<resident_grid(k_topr_candpass, NTHREADS, (w.ntiles_total + CP_TILES - 1) / CP_TILES), NTHREADS, 0, s>>>(w);
