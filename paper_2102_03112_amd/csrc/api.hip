@@ -578,10 +578,20 @@ Carve query_carve(const Plan &p) {
     return c;
 }
 
-dr_status decode_front(Decode &dd, uint32_t max_probe_blocks, bool query_only, hipStream_t s) {
+dr_status decode_init(Decode &dd, bool query_only, hipStream_t s) {
     DR_HIP(run_init(dd.w, dd.p.t, s, query_only));
+    return DR_OK;
+}
+
+dr_status decode_probe(Decode &dd, uint32_t max_probe_blocks, hipStream_t s) {
     DR_HIP(launch_probe_decode(dd.w, dd.dense_out, dd.counts_out, max_probe_blocks, s));
     return DR_OK;
+}
+
+dr_status decode_front(Decode &dd, uint32_t max_probe_blocks, bool query_only, hipStream_t s) {
+    dr_status st = decode_init(dd, query_only, s);
+    if (st != DR_OK) return st;
+    return decode_probe(dd, max_probe_blocks, s);
 }
 
 dr_status decode_back(Decode &dd, hipStream_t s) {
@@ -604,7 +614,7 @@ dr_status decode_impl(const uint8_t *payload, const dr_config *cfg, float *dense
 // events that fork and join it; created on first use, kept until exit.
 struct SideStream {
     hipStream_t s = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
+    hipEvent_t start = nullptr, fork = nullptr, join = nullptr;
 };
 std::mutex g_side_mu;  // guards creation and each fork/join sequence
 SideStream g_side[64];
@@ -616,7 +626,8 @@ bool side_stream(SideStream **out) {
     SideStream &ss = g_side[dev];
     if (!ss.s) {
         if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) return false;
-        if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
+        if (hipEventCreateWithFlags(&ss.start, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
             hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) {
             ss.s = nullptr;
             return false;
@@ -652,6 +663,17 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     const bool overlap = !e.p.segment && qoff + qc.bytes <= ws_bytes && side_stream(&ss);
     if (!overlap) lock.unlock();
     trace_call(s);
+    if (overlap) {
+        // the receiver's set-up needs nothing from the sender: the side
+        // stream runs it (once the caller's earlier work on s is done) while
+        // the sender selects
+        dd.w = qc.view((uint8_t *)ws + qoff);
+        DR_HIP(hipEventRecord(ss->start, s));
+        DR_HIP(hipStreamWaitEvent(ss->s, ss->start, 0));
+        trace_call(ss->s);  // per-kernel timing: the side stream's kernels count from here
+        st = decode_init(dd, true, ss->s);
+        if (st != DR_OK) return st;
+    }
     st = encode_front(e, g, counts_out, s);
     if (st != DR_OK) return st;
     if (!overlap) {
@@ -661,16 +683,15 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
         if (st != DR_OK) return st;
         return decode_back(dd, s);
     }
-    dd.w = qc.view((uint8_t *)ws + qoff);
     DR_HIP(hipEventRecord(ss->fork, s));
     DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
-    trace_call(ss->s);  // per-kernel timing: the side stream's kernels count from here
+    trace_call(ss->s);  // per-kernel timing: the wait for the fork is idle time
     // CUs left to the sender: the sort and the fit want a few dozen when
     // the probe pass is short; for long probe passes (large gradients) each
     // CU taken from the probe costs more than the sender gains (measured on
     // 25.6 M, 138 M and 355 M elements)
     const uint32_t reserve = cfg->offsets_h[cfg->n_tensors] <= (1ull << 26) ? 32u : 8u;
-    st = decode_front(dd, (uint32_t)std::max(1, dr::device_cus() - (int)reserve), true, ss->s);
+    st = decode_probe(dd, (uint32_t)std::max(1, dr::device_cus() - (int)reserve), ss->s);
     if (st != DR_OK) return st;
     DR_HIP(hipEventRecord(ss->join, ss->s));
     st = encode_back(e, s);

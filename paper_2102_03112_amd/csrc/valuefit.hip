@@ -213,8 +213,9 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_upfront(Work w, const uint32_
 // One stable pass of the digit at bits [8 pass, 8 pass + 8): tiles are
 // taken in ticket order, so a tile only ever waits for tiles that running
 // blocks hold.  A tile
-//  1. reads its keys (wave w holds elements [1024 w, 1024 w + 1024) of the
-//     tile, 64 consecutive per step) and counts its digits in LDS;
+//  1. reads its keys and values (wave w holds elements [1024 w, 1024 w +
+//     1024) of the tile, 64 consecutive per step) and counts its digits in
+//     LDS;
 //  2. publishes the counts at once and starts reading the counts of the
 //     tensor's earlier tiles (decoupled look-back, LB_WIN tiles per read
 //     round; a tile that already knows its inclusive prefix ends the walk);
@@ -261,9 +262,14 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *
         const __amdgpu_buffer_rsrc_t kv = buffer_view(kin + slot + q0, 4u * nq);
         const __amdgpu_buffer_rsrc_t vv = buffer_view(vin + slot + q0, 4u * nq);
         const uint32_t ebase = wv * (SORT_STEPS * 64) + lane;  // element of step c: ebase + 64 c
-        uint32_t key[SORT_STEPS];
+        // keys and values read together and held until the scatter: one
+        // round trip to memory per tile
+        uint32_t key[SORT_STEPS], val[SORT_STEPS];
 #pragma unroll
-        for (uint32_t c = 0; c < SORT_STEPS; ++c) key[c] = buffer_u32(kv, 4u * (ebase + 64 * c));
+        for (uint32_t c = 0; c < SORT_STEPS; ++c) {
+            key[c] = buffer_u32(kv, 4u * (ebase + 64 * c));
+            val[c] = buffer_u32(vv, 4u * (ebase + 64 * c));
+        }
         asm volatile("" ::: "memory");
         // the tensor's base of each digit of this pass
         uint32_t dtot;
@@ -360,14 +366,6 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *
             __hip_atomic_store(me, ST_INC | (uint64_t)(excl + agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         goff[dg] = dbase + excl;
-        // keys again (an L2 hit; holding them through the look-back would
-        // cost registers) and the values
-        uint32_t val[SORT_STEPS];
-#pragma unroll
-        for (uint32_t c = 0; c < SORT_STEPS; ++c) {
-            key[c] = buffer_u32(kv, 4u * (ebase + 64 * c));
-            val[c] = buffer_u32(vv, 4u * (ebase + 64 * c));
-        }
         __syncthreads();
 #pragma unroll
         for (uint32_t c = 0; c < SORT_STEPS; ++c) {
