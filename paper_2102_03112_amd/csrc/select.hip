@@ -354,48 +354,16 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
 
 // ---------------------------------------------------------------------------
 // top-r step 3: finish the select on the candidates' low 20 key bits.
-//  a. one block per tensor picks the bin bA of key bits 19..10 from the
-//     histograms the filter pass built;
-//  b. a pass over the candidates marks those above bA and gathers those in
-//     bA (usually a few dozen) into a short list;
+//  a. each block of the candidate pass picks, for the tensors of its tiles,
+//     the bin bA of key bits 19..10 from the histograms the filter pass
+//     built (the block holding a tensor's first tile records it);
+//  b. that pass marks the candidates above bA and gathers those in bA
+//     (usually a few dozen) into a short list;
 //  c. one block per tensor finishes on the short list: bin of bits 9..0,
 //     then, if equal keys straddle the cut, the smallest indices among them.
 // ---------------------------------------------------------------------------
 constexpr uint32_t SEL_THREADS = 1024;
-
-__global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
-    TDesc &td = w.td[blockIdx.x];
-    if (td.in.r == R_NONZERO || td.ncand == 0) return;
-    __shared__ uint32_t scratch[SEL_THREADS / 64 + 1];
-    __shared__ uint32_t res_bin, res_above;
-    if (td.need1 == td.ncand) {  // the whole bin b1 is taken
-        if (threadIdx.x == 0) {
-            td.bA = 0xFFFFFFFFu;
-            td.needA = 0;
-        }
-        return;
-    }
-    if (threadIdx.x == 0) {
-        res_bin = 0;
-        res_above = 0;
-    }
-    __syncthreads();
-    __shared__ uint32_t hsum[1024];
-    const uint32_t *histA = w.histA + (uint64_t)blockIdx.x * HISTA_COPIES * 1024u;
-    for (uint32_t b = threadIdx.x; b < 1024u; b += SEL_THREADS) {
-        uint32_t c = 0;
-#pragma unroll
-        for (uint32_t q = 0; q < HISTA_COPIES; ++q) c += histA[q * 1024u + b];
-        hsum[b] = c;
-    }
-    __syncthreads();
-    find_from_top<1024, SEL_THREADS>(hsum, td.need1, &res_bin, &res_above, scratch);
-    if (threadIdx.x == 0) {
-        td.bA = res_bin;
-        td.needA = td.need1 - res_above;
-        td.nsub = 0;
-    }
-}
+constexpr uint32_t ALL_OF_B1 = 0xFFFFFFFFu;  // bA when the whole bin b1 is taken
 
 // Candidates above bin bA are selected; those in bA go to the short list.
 // A block takes CP_TILES tiles at a time and treats their candidates as one
@@ -405,30 +373,97 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_pickA(Work w) {
 constexpr uint32_t CP_BATCH = 4;
 constexpr uint32_t CP_TILES = 32;
 
+// bA of top-r tensor t (ALL_OF_B1: the whole bin b1 is taken) from the sum
+// of its histogram copies, and how many to take from bin bA.  Block-wide.
+__device__ uint32_t pick_bA(const Work &w, uint32_t t, uint32_t *hsum, PickLds &l, uint32_t *needA) {
+    const TDesc &td = w.td[t];
+    const uint32_t need1 = td.need1, ncand = td.ncand;
+    if (need1 == ncand) {
+        *needA = 0;
+        return ALL_OF_B1;
+    }
+    const uint32_t *histA = w.histA + (uint64_t)t * HISTA_COPIES * 1024u;
+    for (uint32_t b = threadIdx.x; b < 1024u; b += NTHREADS) {
+        uint32_t c = 0;
+#pragma unroll
+        for (uint32_t q = 0; q < HISTA_COPIES; ++q) c += histA[q * 1024u + b];
+        hsum[b] = c;
+    }
+    if (threadIdx.x == 0) {
+        l.res_bin = 0;
+        l.res_above = 0;
+    }
+    __syncthreads();
+    find_from_top<1024, NTHREADS>(hsum, need1, &l.res_bin, &l.res_above, l.scratch);
+    const uint32_t bA = l.res_bin;
+    *needA = need1 - l.res_above;
+    __syncthreads();  // hsum and l are reused
+    return bA;
+}
+
 __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
     __shared__ uint32_t pre[CP_TILES];
     __shared__ uint32_t tten[CP_TILES];
     __shared__ uint64_t tbase[CP_TILES];  // workspace offset of the tile's first candidate
     __shared__ uint32_t tbA[CP_TILES];
-    __shared__ uint32_t gtot;
+    __shared__ uint32_t tpk[CP_TILES];    // the tile's entry in the group's tensor list
+    __shared__ uint32_t gten[CP_TILES], gbA[CP_TILES];  // the group's tensors, in tile order, and their bA
+    __shared__ uint32_t gtot, ngten;
+    __shared__ uint32_t hsum[1024];
+    __shared__ PickLds pl;
+    uint32_t last_t = 0xFFFFFFFFu, last_bA = 0;  // the block's most recent pick
     for (uint32_t g0 = blockIdx.x * CP_TILES; g0 < w.ntiles_total; g0 += gridDim.x * CP_TILES) {
-        if (threadIdx.x < 64) {  // the first wave scans the group's counts
+        if (threadIdx.x < 64) {  // the first wave scans the group's counts and lists its tensors
             const uint32_t tile = g0 + threadIdx.x;
-            uint32_t c = 0, t = 0;
-            if (threadIdx.x < CP_TILES && tile < w.ntiles_total) {
+            const bool in = threadIdx.x < CP_TILES && tile < w.ntiles_total;
+            uint32_t c = 0, t = 0xFFFFFFFFu;
+            if (in) {
                 t = tensor_of_tile(w, tile);
                 const TDesc &td = w.td[t];
                 c = td.in.r == R_NONZERO ? 0u : w.ccnt[tile];
                 tbase[threadIdx.x] = td.in.slot + (uint64_t)(tile - td.in.tile0) * TILE;
-                tbA[threadIdx.x] = td.bA;
             }
             const uint32_t inc = wave_incl_scan(c);
-            if (threadIdx.x < CP_TILES) {
+            // tiles are in tensor order: a tile whose tensor differs from the
+            // previous tile's starts the next entry of the group's list
+            const uint32_t tprev = __shfl_up(t, 1, 64);
+            const bool fresh = in && (threadIdx.x == 0 || t != tprev);
+            const uint64_t fm = ballot(fresh);
+            const uint32_t ord = lanes_below(fm) + (fresh ? 1u : 0u);  // list entries up to this tile
+            if (fresh) gten[ord - 1] = t;
+            if (threadIdx.x < CP_TILES) {  // past the last tile: an empty tile (pre = total)
                 pre[threadIdx.x] = inc - c;
                 tten[threadIdx.x] = t;
+                tpk[threadIdx.x] = in ? ord - 1 : 0u;
             }
-            if (threadIdx.x == 63) gtot = inc;
+            if (threadIdx.x == 63) {
+                gtot = inc;
+                ngten = popc64(fm);
+            }
         }
+        __syncthreads();
+        const uint32_t ng = ngten;
+        for (uint32_t q = 0; q < ng; ++q) {  // block-uniform
+            const uint32_t t = gten[q];
+            if (t != last_t) {
+                TDesc &td = w.td[t];
+                uint32_t bA = 0, needA = 0;
+                if (td.in.r != R_NONZERO && td.ncand > 0) {
+                    bA = pick_bA(w, t, hsum, pl, &needA);
+                    // the group holding the tensor's first tile records the
+                    // pick for the final step
+                    if (td.in.tile0 >= g0 && threadIdx.x == 0) {
+                        td.bA = bA;
+                        td.needA = needA;
+                    }
+                }
+                last_t = t;
+                last_bA = bA;
+            }
+            if (threadIdx.x == 0) gbA[q] = last_bA;
+        }
+        __syncthreads();
+        if (threadIdx.x < CP_TILES && g0 + threadIdx.x < w.ntiles_total) tbA[threadIdx.x] = gbA[tpk[threadIdx.x]];
         __syncthreads();
         const uint32_t tot = gtot;
         for (uint32_t e0 = 0; e0 < tot; e0 += NTHREADS * CP_BATCH) {
@@ -458,8 +493,8 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
                 const uint32_t x = tix[u];
                 const uint32_t bA = tbA[x], k = key[u], i = idx[u];
                 const uint32_t dA = (k >> 10) & 1023u;
-                const bool take = act && (bA == 0xFFFFFFFFu || dA > bA);
-                const bool sub = act && bA != 0xFFFFFFFFu && dA == bA;
+                const bool take = act && (bA == ALL_OF_B1 || dA > bA);
+                const bool sub = act && bA != ALL_OF_B1 && dA == bA;
                 // i lies in tile x, whose first element sits at slot tbase[x]
                 if (take) atomicOr(&w.selbits[(tbase[x] + (i % TILE)) >> 5], 1u << (i & 31u));
                 if (sub) {
@@ -495,7 +530,7 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
 // the smaller index; set their bits.
 __global__ __launch_bounds__(SEL_THREADS) void k_topr_final(Work w) {
     TDesc &td = w.td[blockIdx.x];
-    if (td.in.r == R_NONZERO || td.ncand == 0 || td.bA == 0xFFFFFFFFu) return;
+    if (td.in.r == R_NONZERO || td.ncand == 0 || td.bA == ALL_OF_B1) return;
     __shared__ uint32_t h[2048];
     __shared__ uint32_t scratch[SEL_THREADS / 64 + 1];
     __shared__ uint32_t res_bin, res_above;
@@ -580,8 +615,6 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
     k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     if (any_topr) {
-        k_topr_pickA<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
-        trace_mark(s, "k_topr_pickA");
         k_topr_candpass<<<resident_grid(k_topr_candpass, NTHREADS, (w.ntiles_total + CP_TILES - 1) / CP_TILES), NTHREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_candpass");
         k_topr_final<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
