@@ -180,9 +180,18 @@ __device__ void find_from_top(const uint32_t *cnt, uint32_t need, uint32_t *res_
 // finds it for its own tiles' tensor, hidden under its first tile's reads;
 // the block holding the tensor's first tile records b1, how many to take
 // from it and its size for the passes after.
+// The filter pass's blocks: 512 threads, 8 elements of a tile each, and at
+// most 80 VGPRs so that three blocks (six waves per SIMD) fit on a CU.
+// Measured against 256 threads and 16 elements (120 VGPRs, four waves per
+// SIMD): 40 µs against 44 per pass over 25.6 M elements; seven or eight
+// waves per SIMD spill enough to be slower.
+constexpr uint32_t FILTER_THREADS = 512;
+constexpr uint32_t FILTER_WAVES = FILTER_THREADS / 64;
+constexpr uint32_t FILTER_STEPS = TILE / FILTER_THREADS;  // elements per thread per tile
+
 struct PickLds {
     uint32_t res_bin, res_above;
-    uint32_t scratch[NWAVES + 1];
+    uint32_t scratch[FILTER_WAVES + 1];  // block scans of up to FILTER_THREADS threads
 };
 
 __device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) {
@@ -202,7 +211,7 @@ __device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) 
     }
     __syncthreads();
     const uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
-    find_from_top<HIST1_BINS, NTHREADS>(hist, r, &l.res_bin, &l.res_above, l.scratch);
+    find_from_top<HIST1_BINS, FILTER_THREADS>(hist, r, &l.res_bin, &l.res_above, l.scratch);
     const uint32_t b1 = l.res_bin;
     if (record && threadIdx.x == 0) {
         td.b1 = b1;
@@ -216,8 +225,8 @@ __device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) 
 // ---------------------------------------------------------------------------
 // top-r step 2 / support: bitmap of definite selections + per-tile candidates
 // ---------------------------------------------------------------------------
-// Elements of a tile are visited as e = j * 256 + threadIdx.x (j = 0..15):
-// each load instruction reads 256 consecutive floats, and one wave ballot
+// Elements of a tile are visited as e = j * 512 + threadIdx.x (j = 0..7):
+// each load instruction reads 512 consecutive floats, and one wave ballot
 // covers 64 consecutive elements, i.e. two whole bitmap words.  Candidates
 // (top-r: key in bin b1) are kept in index order in the tile's own stretch
 // of the candidate arrays, with their number in ccnt[tile].  For the
@@ -244,18 +253,20 @@ __device__ __forceinline__ FilterTile filter_tile(const Work &w, uint32_t tile) 
     return f;
 }
 
-// The 16 values of a thread for a tile, read through a raw buffer view
-// (reads past the tensor's end return 0 and touch no memory).
-__device__ __forceinline__ void filter_load(const float *g, const FilterTile &f, float x[16]) {
+// The FILTER_STEPS values of a thread for a tile, read through a raw buffer
+// view (reads past the tensor's end return 0 and touch no memory).
+__device__ __forceinline__ void filter_load(const float *g, const FilterTile &f, float x[FILTER_STEPS]) {
     const __amdgpu_buffer_rsrc_t gv = buffer_view(g + f.off + f.base, 4u * min(TILE, f.d - min(f.d, f.base)));
 #pragma unroll
-    for (int j = 0; j < 16; ++j) x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * NTHREADS + threadIdx.x)));
+    for (uint32_t j = 0; j < FILTER_STEPS; ++j)
+        x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * FILTER_THREADS + threadIdx.x)));
 }
 
-__global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float *__restrict__ g) {
-    __shared__ uint32_t wcnt[16 * NWAVES];
-    __shared__ uint32_t woff[16 * NWAVES];
-    __shared__ uint32_t dcnt[NWAVES];
+__global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void k_select_filter(Work w, const float *__restrict__ g) {
+    static_assert(FILTER_STEPS * FILTER_WAVES == 64, "one wave scans the (step, wave) candidate counts");
+    __shared__ uint32_t wcnt[FILTER_STEPS * FILTER_WAVES];
+    __shared__ uint32_t woff[FILTER_STEPS * FILTER_WAVES];
+    __shared__ uint32_t dcnt[FILTER_WAVES];
     __shared__ uint32_t sbw[TILE_WORDS];
     __shared__ uint32_t bad;
     __shared__ PickLds pl;
@@ -265,7 +276,7 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
     __syncthreads();
     uint32_t b1_t = 0xffffffffu, b1_c = 0;  // tensor whose b1 the block holds, and b1
     // the next tile's values are in flight while this tile is classified
-    float xn[16];
+    float xn[FILTER_STEPS];
     FilterTile fn{};
     if (blockIdx.x < w.ntiles_total) {
         fn = filter_tile(w, blockIdx.x);
@@ -275,9 +286,9 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         const FilterTile f = fn;
         const bool more = tile + gridDim.x < w.ntiles_total;
         if (more) fn = filter_tile(w, tile + gridDim.x);
-        float x[16];
+        float x[FILTER_STEPS];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) x[j] = xn[j];
+        for (uint32_t j = 0; j < FILTER_STEPS; ++j) x[j] = xn[j];
         if (more) filter_load(g, fn, xn);
         // keeps the scheduler from sinking the loads next to their uses
         asm volatile("" ::: "memory");
@@ -288,15 +299,15 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         const uint32_t base = f.base, d = f.d, b1 = f.nz ? 0u : b1_c;
         const uint64_t slot = f.slot;
         const bool nz = f.nz;
-        uint32_t keys[16];
-        uint64_t cmask[16];
+        uint32_t keys[FILTER_STEPS];
+        uint64_t cmask[FILTER_STEPS];
         uint32_t nonfinite = 0, ndef = 0;
         // lane 2j + h ends up holding half h of step j's bitmap ballot, and
         // lane j the candidate count of step j: selects, not branches
         uint32_t myword = 0, mycand = 0;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const uint32_t i = base + j * NTHREADS + threadIdx.x;
+        for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
+            const uint32_t i = base + j * FILTER_THREADS + threadIdx.x;
             const bool valid = i < d;
             const uint32_t key = valid ? mag_key(x[j]) : 0u;
             nonfinite |= key >= 0x7f800000u;
@@ -309,13 +320,13 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
             keys[j] = key;
             ndef += popc64(dm);
             myword = lane == 2u * j ? (uint32_t)dm : (lane == 2u * j + 1u ? (uint32_t)(dm >> 32) : myword);
-            mycand = lane == (uint32_t)j ? popc64(cmask[j]) : mycand;
+            mycand = lane == j ? popc64(cmask[j]) : mycand;
         }
         // the tile's bitmap words are staged in LDS and written by one
         // coalesced store after the barrier (two-lane stores per step cost a
         // third of the pass's read bandwidth)
-        if (lane < 32) sbw[(lane >> 1) * (NTHREADS / 32) + wv * 2 + (lane & 1)] = myword;
-        if (lane < 16) wcnt[lane * NWAVES + wv] = mycand;
+        if (lane < 2 * FILTER_STEPS) sbw[(lane >> 1) * (FILTER_THREADS / 32) + wv * 2 + (lane & 1)] = myword;
+        if (lane < FILTER_STEPS) wcnt[lane * FILTER_WAVES + wv] = mycand;
         if (nonfinite) bad = 1;
         if (lane == 0) dcnt[wv] = ndef;
         __syncthreads();
@@ -327,7 +338,7 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
             if (threadIdx.x == 63) {
                 w.ccnt[tile] = inc;
                 uint32_t nd = 0;
-                for (uint32_t q = 0; q < NWAVES; ++q) nd += dcnt[q];
+                for (uint32_t q = 0; q < FILTER_WAVES; ++q) nd += dcnt[q];
                 w.tcnt[tile] = nd;
             }
         }
@@ -340,11 +351,11 @@ __global__ __launch_bounds__(NTHREADS) void k_select_filter(Work w, const float 
         const uint64_t cbase = slot + base;
         uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * 1024u;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
+        for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
             if ((cmask[j] >> lane) & 1ull) {
-                const uint64_t q = cbase + woff[j * NWAVES + wv] + lanes_below(cmask[j]);
+                const uint64_t q = cbase + woff[j * FILTER_WAVES + wv] + lanes_below(cmask[j]);
                 w.cand_key[q] = keys[j];
-                w.cand_idx[q] = base + j * NTHREADS + threadIdx.x;
+                w.cand_idx[q] = base + j * FILTER_THREADS + threadIdx.x;
                 atomicAdd(&histA[(keys[j] >> 10) & 1023u], 1u);
             }
         }
@@ -612,7 +623,7 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
         k_topr_hist<<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
         trace_mark(s, "k_topr_hist");
     }
-    k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
+    k_select_filter<<<resident_grid(k_select_filter, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     if (any_topr) {
         k_topr_candpass<<<resident_grid(k_topr_candpass, NTHREADS, (w.ntiles_total + CP_TILES - 1) / CP_TILES), NTHREADS, 0, s>>>(w);
@@ -754,7 +765,7 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
 
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     (void)grid_persist;
-    k_select_filter<<<resident_grid(k_select_filter, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, g);
+    k_select_filter<<<resident_grid(k_select_filter, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     // |S| from the per-tile counts of the filter pass
     k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr);
