@@ -551,6 +551,145 @@ __device__ __forceinline__ uint32_t filter_word(const uint32_t *fc, uint32_t fcw
 constexpr uint32_t RUN_TILES = 512;  // most tiles per run (LDS tile counters)
 constexpr uint32_t TAIL_PROBES = 2;  // probes per round once the survivors fit one group
 
+// The tensor totals of the probe pass: the sender's |P| and values coded,
+// or the receiver's |P| (checked against the record's header).
+template <int MODE>
+__device__ void probe_total(const Work &w, const QueryOut &o, uint32_t t, uint32_t total) {
+    TDesc &td = w.td[t];
+    if (MODE == Q_ENCODE) {
+        // the policy codes every positive (P0) or r of them
+        td.npos = total;
+        td.nv = td.in.policy == POLICY_P0 ? total : min(td.n, total);
+    } else {
+        td.nv_dec = total;
+        if (o.counts_out) {
+            o.counts_out[4 * t + 2] = total;
+            if (total != ((const uint32_t *)td.in.rec)[H_NPOS])
+                atomicOr((unsigned long long *)&o.counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
+        }
+    }
+}
+
+// The tile scan, at the end of the probe pass: toff = each tile's exclusive
+// count within its tensor, and each tensor's total where its last tile
+// lies.  Blocks own contiguous tile ranges in block order.  A block
+//  1. sums its trailing segment (its tiles of the tensor of its last tile)
+//     and publishes it: as inclusive if the block holds that tensor's first
+//     tile, else as an aggregate;
+//  2. if its first tile continues a tensor that began in an earlier block,
+//     wave 0 walks back over the preceding blocks, 64 at a time, adding
+//     aggregates until an inclusive entry (decoupled look-back); a block
+//     whose range lies inside that tensor then publishes its inclusive sum;
+//  3. scans its tiles, segmented at tensor starts.
+// A block waits only for blocks with smaller indices, which start first, so
+// every wait ends; the wait is bounded anyway and flags the tensor if it
+// gives up.  `lds` is the filter copy's LDS, free at this point.
+constexpr uint64_t PS_AGG = 1ull << 62, PS_INC = 2ull << 62;
+constexpr uint32_t PS_SPIN_LIMIT = 1u << 20;
+
+template <int MODE>
+__device__ void probe_scan(const Work &w, const QueryOut &o, uint32_t t_begin, uint32_t t_end, uint32_t *lds) {
+    if (t_end <= t_begin) return;  // block-uniform
+    const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    const uint32_t t_first = tensor_of_tile(w, t_begin), t_last = tensor_of_tile(w, t_end - 1);
+    const uint32_t tile0_first = w.td[t_first].in.tile0;
+    const uint32_t trail0 = max(t_begin, w.td[t_last].in.tile0);
+    const bool cont = t_begin > tile0_first;  // the first tensor began in an earlier block
+    // 1. the trailing segment's sum
+    uint32_t s = 0;
+    for (uint32_t t = trail0 + threadIdx.x; t < t_end; t += PB_THREADS) s += w.tcnt[t];
+    s = wave_sum(s);
+    if (lane == 0) lds[wv] = s;
+    __syncthreads();
+    s = 0;
+    for (uint32_t q = 0; q < PB_WAVES; ++q) s += lds[q];
+    uint64_t *st = w.pstat;
+    const bool trail_inc = trail0 > t_begin || !cont;
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&st[blockIdx.x], (trail_inc ? PS_INC : PS_AGG) | s, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();  // lds is rewritten below
+    // 2. look-back
+    if (cont && wv == 0) {
+        uint32_t excl = 0, j = blockIdx.x, rounds = 0;  // next window: blocks j - 1, j - 2, ...
+        for (;;) {
+            const uint32_t nwin = min(64u, j);
+            const bool inw = lane < nwin;
+            const uint64_t v = inw ? __hip_atomic_load(&st[j - 1 - lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                   : 0ull;
+            const uint64_t unpub = ballot(inw && (v >> 62) == 0);
+            const uint64_t inc = ballot(inw && (v >> 62) == 2);
+            const uint32_t first_unpub = unpub ? (uint32_t)__ffsll((unsigned long long)unpub) - 1 : 64u;
+            const uint32_t first_inc = inc ? (uint32_t)__ffsll((unsigned long long)inc) - 1 : 64u;
+            if (first_inc < first_unpub) {  // the nearest entries up to an inclusive one are all published
+                excl += wave_sum(lane <= first_inc ? (uint32_t)v : 0u);
+                break;
+            }
+            const uint32_t upto = min(first_unpub, nwin);  // published aggregates nearest first
+            excl += wave_sum(lane < upto ? (uint32_t)v : 0u);
+            j -= upto;
+            if (j == 0) break;  // cannot happen: block 0 holds the first tensor's start
+            if (upto == 0) {
+                if (++rounds >= PS_SPIN_LIMIT) {  // never hang the device on a bug
+                    if (lane == 0) {
+                        atomicOr(&w.td[t_first].flags, FLAG_STALLED);
+                        if (o.counts_out)
+                            atomicOr((unsigned long long *)&o.counts_out[4 * t_first + 3], FLAG_STALLED);
+                    }
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        if (lane == 0) {
+            lds[0] = excl;
+            if (t_first == t_last)
+                __hip_atomic_store(&st[blockIdx.x], PS_INC | (uint64_t)(excl + s), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    __syncthreads();
+    uint32_t carry = cont ? lds[0] : 0u;  // the running count of the segment entering the chunk
+    __syncthreads();
+    // 3. segmented exclusive scan, PB_THREADS tiles at a time
+    for (uint32_t c0 = t_begin; c0 < t_end; c0 += PB_THREADS) {
+        const uint32_t t = c0 + threadIdx.x;
+        const bool in = t < t_end;
+        uint32_t v = 0, tt = 0;
+        bool f = false, last = false;
+        if (in) {
+            v = w.tcnt[t];
+            tt = tensor_of_tile(w, t);
+            const TInit &ti = w.td[tt].in;
+            f = t == ti.tile0;  // a tensor starts here
+            last = t + 1 == ti.tile0 + ti.ntiles;
+        }
+        uint32_t sv = v, sf = f ? 1u : 0u;  // inclusive within the wave: (segment started, sum)
+#pragma unroll
+        for (uint32_t d = 1; d < 64; d <<= 1) {
+            const uint32_t pv = __shfl_up(sv, d, 64), pf = __shfl_up(sf, d, 64);
+            if (lane >= d) {
+                if (!sf) sv += pv;
+                sf |= pf;
+            }
+        }
+        if (lane == 63) {
+            lds[wv] = sv;
+            lds[PB_WAVES + wv] = sf;
+        }
+        __syncthreads();
+        uint32_t pre = carry;
+        for (uint32_t q = 0; q < wv; ++q) pre = lds[PB_WAVES + q] ? lds[q] : pre + lds[q];
+        const uint32_t incl = sf ? sv : pre + sv;
+        if (in) {
+            w.toff[t] = incl - v;
+            if (last) probe_total<MODE>(w, o, tt, incl);
+        }
+        for (uint32_t q = 0; q < PB_WAVES; ++q) carry = lds[PB_WAVES + q] ? lds[q] : carry + lds[q];
+        __syncthreads();  // lds is rewritten by the next chunk
+    }
+}
+
 template <int MODE>
 __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
     __shared__ uint32_t fc[FC_WORDS];
@@ -582,7 +721,10 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) tcl[x] = 0;
         if (threadIdx.x == 0) {
             next = 0;
-            if ((MODE == Q_DECODE || MODE == Q_SUM) && !ok) atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+            if ((MODE == Q_DECODE || MODE == Q_SUM) && !ok) {
+                atomicOr(&td.flags, FLAG_DEC_MISMATCH);
+                if (o.counts_out) atomicOr((unsigned long long *)&o.counts_out[4 * t + 3], FLAG_DEC_MISMATCH);
+            }
         }
         __syncthreads();
         const uint32_t m_bits = rv.m_bits, k = rv.k, d = td.in.d;
@@ -715,6 +857,10 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         __syncthreads();
         for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) w.tcnt[rb + x] = tcl[x];
         rb = re;
+    }
+    if (MODE == Q_ENCODE || MODE == Q_DECODE) {
+        __syncthreads();  // the block's tile counts are written; fc is free
+        probe_scan<MODE>(w, o, t_begin, t_end, fc);
     }
 }
 
@@ -987,7 +1133,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
 // One probe block per CU (its LDS holds a filter copy), each owning at
 // least PB_TILES tiles so that all of its waves have work.
 static int probe_grid(const Work &w) {
-    const uint32_t cus = (uint32_t)device_cus();
+    const uint32_t cus = std::min((uint32_t)device_cus(), PSTAT_MAX);  // one look-back entry per block
     const uint32_t by_tiles = (w.ntiles_total + PB_TILES - 1) / PB_TILES;
     return (int)std::max(1u, std::min(cus, by_tiles));
 }
@@ -995,10 +1141,9 @@ static int probe_grid(const Work &w) {
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     QueryOut o{};
     o.g = g;
+    // the pass also scans its tile counts (probe_scan)
     k_probe<Q_ENCODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_ENCODE>");
-    hipError_t e = launch_tile_scan(w, 1, nullptr, s);
-    if (e != hipSuccess) return e;
     k_emit<Q_ENCODE><<<resident_grid(k_emit<Q_ENCODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_ENCODE>");
     return hipGetLastError();
@@ -1026,9 +1171,10 @@ hipError_t launch_probe_decode(const Work &w, float *dense_out, uint64_t *counts
     o.dense_out = dense_out;
     // std::min: HIP's host min() takes ints, and max_blocks may be ~0u
     const uint32_t grid = std::min<uint32_t>((uint32_t)probe_grid(w), std::max<uint32_t>(1u, max_blocks));
+    // the pass also scans its tile counts (probe_scan)
     k_probe<Q_DECODE><<<grid, PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_DECODE>");
-    return launch_tile_scan(w, 2, nullptr, s, counts_out);
+    return hipGetLastError();
 }
 
 hipError_t launch_emit_decode(const Work &w, float *dense_out, uint32_t *idx_out, float *val_out,

@@ -156,6 +156,7 @@ constexpr uint32_t FLAG_DEC_MISMATCH = 2u;   // receiver |P| differs from the he
 constexpr uint32_t FLAG_COUNT = 4u;          // selection count differs from r
 constexpr uint32_t FLAG_CAPACITY = 8u;       // a device-side capacity was exceeded
 constexpr uint32_t FLAG_STALLED = 16u;       // a bounded wait gave up (internal error)
+constexpr uint32_t PSTAT_MAX = 4096;         // probe pass blocks with a look-back entry (at most)
 
 // Views of the workspace carved on the host.
 struct Work {
@@ -167,6 +168,7 @@ struct Work {
     uint32_t ntiles_total;    // sum of ntiles
     uint64_t slots;           // padded elements = ntiles_total * TILE
     uint32_t *done;           // per-tensor completion counters (zeroed at set-up)
+    uint64_t *pstat;          // probe pass look-back: per block (flag << 62 | trailing count), zeroed at set-up
     uint32_t *tcnt;           // per-tile counts of the current ordered pass
     uint32_t *toff;           // per-tile exclusive offsets within the tensor
     uint32_t *ccnt;           // top-r candidates per tile
