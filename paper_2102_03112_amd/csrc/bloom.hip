@@ -552,7 +552,8 @@ constexpr uint32_t RUN_TILES = 512;  // most tiles per run (LDS tile counters)
 constexpr uint32_t TAIL_PROBES = 2;  // probes per round once the survivors fit one group
 
 // The tensor totals of the probe pass: the sender's |P| and values coded,
-// or the receiver's |P| (checked against the record's header).
+// the plain query's count, or the receiver's |P| (checked against the
+// record's header).
 template <int MODE>
 __device__ void probe_total(const Work &w, const QueryOut &o, uint32_t t, uint32_t total) {
     TDesc &td = w.td[t];
@@ -560,6 +561,8 @@ __device__ void probe_total(const Work &w, const QueryOut &o, uint32_t t, uint32
         // the policy codes every positive (P0) or r of them
         td.npos = total;
         td.nv = td.in.policy == POLICY_P0 ? total : min(td.n, total);
+    } else if (MODE == Q_PLAIN) {
+        if (o.n_out) *o.n_out = total;  // one tensor
     } else {
         td.nv_dec = total;
         if (o.counts_out) {
@@ -858,10 +861,8 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) w.tcnt[rb + x] = tcl[x];
         rb = re;
     }
-    if (MODE == Q_ENCODE || MODE == Q_DECODE) {
-        __syncthreads();  // the block's tile counts are written; fc is free
-        probe_scan<MODE>(w, o, t_begin, t_end, fc);
-    }
+    __syncthreads();  // the block's tile counts are written; fc is free
+    probe_scan<MODE>(w, o, t_begin, t_end, fc);
 }
 
 // The received value of a positive whose value number is vn (NO_SLOT: not
@@ -1155,10 +1156,9 @@ hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, ui
     o.idx_out = idx_out;
     o.cap = cap;
     o.n_out = n_out;
+    // the pass also scans its tile counts (probe_scan)
     k_probe<Q_PLAIN><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_PLAIN>");
-    hipError_t e = launch_tile_scan(w, 3, n_out, s);
-    if (e != hipSuccess) return e;
     k_emit<Q_PLAIN><<<resident_grid(k_emit<Q_PLAIN>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_PLAIN>");
     return hipGetLastError();
@@ -1202,10 +1202,9 @@ hipError_t launch_query_decode_sum(const Work &w, uint32_t npay, uint32_t ntens,
     o.npay = npay;
     o.ntens = ntens;
     o.ntiles1 = ntiles1;
+    // the pass also scans its tile counts (probe_scan)
     k_probe<Q_SUM><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_SUM>");
-    hipError_t e = launch_tile_scan(w, 2, nullptr, s, counts_out);
-    if (e != hipSuccess) return e;
     k_emit_sum<<<resident_grid(k_emit_sum, NTHREADS, ntiles1), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit_sum");
     return hipGetLastError();
