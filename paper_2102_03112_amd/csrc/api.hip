@@ -508,8 +508,7 @@ dr_status encode_front(Encode &e, const float *g, uint64_t *counts_out, hipStrea
         DR_HIP(launch_bloom_direct(w, true, p.dir_blocks, p.dir_slices, s));
     else
         DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
-    DR_HIP(launch_query_encode(w, g, persist_grid(4), s));
-    DR_HIP(launch_value_setup(w, true, counts_out, s));
+    DR_HIP(launch_query_encode(w, g, persist_grid(4), counts_out, s));
     return DR_OK;
 }
 

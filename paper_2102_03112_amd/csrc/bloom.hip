@@ -17,6 +17,7 @@
 // counts; after a per-tensor scan of the counts, the emit kernel writes the
 // positives in order.
 #include "launch.hpp"
+#include "value_setup.hpp"
 
 namespace dr {
 
@@ -426,6 +427,7 @@ struct QueryOut {
     uint32_t npay;          // sum: payloads
     uint32_t ntens;         // sum: tensors per payload
     uint32_t ntiles1;       // sum: tiles per payload
+    int setup;              // encode: block 0 of the emit pass also runs the value set-up
 };
 
 struct RecordView {
@@ -961,6 +963,9 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     // stores stay in flight across them.
     uint32_t tile = blockIdx.x;
     uint32_t word = 0, q0n = 0, tn = 0;
+    // the sender's value set-up needs only the counts the probe pass left;
+    // block 0 runs it here instead of in a kernel of its own
+    if (MODE == Q_ENCODE && o.setup && blockIdx.x == 0) value_setup_block<NTHREADS>(w, 1, o.counts_out);
     if (tile < w.ntiles_total) {
         q0n = w.toff[tile];
         tn = tensor_of_tile(w, tile);
@@ -1139,9 +1144,11 @@ static int probe_grid(const Work &w) {
     return (int)std::max(1u, std::min(cus, by_tiles));
 }
 
-hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, hipStream_t s) {
+hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, uint64_t *counts_out, hipStream_t s) {
     QueryOut o{};
     o.g = g;
+    o.setup = 1;
+    o.counts_out = counts_out;
     // the pass also scans its tile counts (probe_scan)
     k_probe<Q_ENCODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_ENCODE>");

@@ -14,21 +14,9 @@
 //    (D+1) x (D+1) system.  No MFMA: this is a small reduction.
 //  * Reorder map: sigma[q] = sorted rank of value q, packed b bits per entry.
 #include "launch.hpp"
+#include "value_setup.hpp"
 
 namespace dr {
-
-__device__ __forceinline__ void fit_shape(uint32_t nv, uint32_t degree, uint32_t nseg, uint32_t *seff,
-                                          uint32_t *deff) {
-    if (nv == 0) {
-        *seff = 0;
-        *deff = 0;
-        return;
-    }
-    uint32_t cap = nv / (degree + 1u);
-    if (cap < 1) cap = 1;
-    *seff = nseg < cap ? nseg : cap;
-    *deff = nv >= degree + 1u ? degree : nv - 1u;
-}
 
 // standalone value path: keys from the caller's values
 __global__ __launch_bounds__(NTHREADS) void k_keygen(Work w, const float *__restrict__ vals, const uint64_t *n,
@@ -54,91 +42,11 @@ hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, ui
 }
 
 // After |P| is known: run shape, reorder-map width, sort tiling, record
-// layout and header.  One block walks the tensors in chunks.
+// layout and header (value_setup_block).
 constexpr uint32_t SETUP_THREADS = 1024;
 
 __global__ __launch_bounds__(SETUP_THREADS) void k_value_setup(Work w, int payload, uint64_t *counts_out) {
-    __shared__ uint32_t scratch[SETUP_THREADS / 64 + 1];
-    __shared__ uint32_t carry_tiles, carry_words, carry_vals;
-    if (threadIdx.x == 0) {
-        carry_tiles = 0;
-        carry_words = 0;
-        carry_vals = 0;
-    }
-    __syncthreads();
-    for (uint32_t t0 = 0; t0 < w.ntensors; t0 += SETUP_THREADS) {
-        const uint32_t t = t0 + threadIdx.x;
-        uint32_t ntl = 0, nwd = 0, nv = 0;
-        if (t < w.ntensors) {
-            TDesc &td = w.td[t];
-            nv = td.nv;
-            uint32_t seff, deff;
-            fit_shape(nv, td.in.degree, td.in.nseg, &seff, &deff);
-            td.seff = seff;
-            td.deff = deff;
-            const uint32_t b = sigma_bits(nv);
-            td.b = b;
-            td.model = td.in.fit_model == FIT_DEXP && nv >= 4 ? FIT_DEXP : FIT_POLY;
-            ntl = (nv + TILE - 1) / TILE;
-            nwd = (uint32_t)(((uint64_t)nv * b + 31u) / 32u);
-            td.sntiles = ntl;
-            td.swords = nwd;
-            if (counts_out) {
-                counts_out[4 * t + 0] = td.n;
-                counts_out[4 * t + 1] = td.npos;
-                counts_out[4 * t + 2] = 0;
-                counts_out[4 * t + 3] = td.flags;
-            }
-            if (payload) {
-                const uint32_t coef_off = HDR_BYTES + td.m_words * 4u;
-                const uint32_t sigma_off = coef_off + seff * (deff + 1u) * 4u;
-                const uint32_t rec_bytes = sigma_off + nwd * 4u;
-                td.coef_off = coef_off;
-                td.sigma_off = sigma_off;
-                td.rec_bytes = rec_bytes;
-                uint8_t *rec = td.in.rec;
-                uint32_t *h = (uint32_t *)rec;
-                h[H_MAGIC] = HDR_MAGIC;
-                h[H_BYTES] = HDR_BYTES;
-                h[H_D] = td.in.d;
-                h[H_NSEL] = td.n;
-                h[H_NPOS] = td.npos;
-                h[H_NVAL] = nv;
-                h[H_MBITS] = td.m_words * 32u;
-                h[H_K] = td.in.k;
-                h[H_HASH] = 1u;  // MurmurHash3_x86_32, seeds 0..k-1
-                h[H_POLICY] = td.in.policy;
-                h[H_SEED] = td.in.seed;
-                h[H_DEFF] = deff;
-                h[H_SEFF] = seff;
-                h[H_B] = b;
-                h[H_RECBYTES] = rec_bytes;
-                h[H_SEGMODE] = td.in.seg_mode | (td.model << 8);
-            }
-        }
-        uint32_t tot_t, tot_w, tot_v;
-        const uint32_t bt = carry_tiles, bw = carry_words, bv = carry_vals;
-        const uint32_t ex_t = block_excl_scan_n<SETUP_THREADS>(ntl, scratch, &tot_t);
-        const uint32_t ex_w = block_excl_scan_n<SETUP_THREADS>(nwd, scratch, &tot_w);
-        const uint32_t ex_v = block_excl_scan_n<SETUP_THREADS>(nv, scratch, &tot_v);
-        (void)ex_v;
-        if (t < w.ntensors) {
-            w.td[t].stile0 = bt + ex_t;
-            w.td[t].sw0 = bw + ex_w;
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            carry_tiles = bt + tot_t;
-            carry_words = bw + tot_w;
-            carry_vals = bv + tot_v;
-        }
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        w.glob->sort_tiles = carry_tiles;
-        w.glob->sigma_words = carry_words;
-        w.glob->values = carry_vals;
-    }
+    value_setup_block<SETUP_THREADS>(w, payload, counts_out);
 }
 
 hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s) {
