@@ -213,6 +213,17 @@ def test_curvefit_parity(n, D, S):
 # ---------------------------------------------------------------------------
 # dr_roundtrip over a gradient split into tensors
 # ---------------------------------------------------------------------------
+def _many_tensor_offsets():
+    """37 tensors over about 3 M elements (about 740 tiles, so the probe pass
+    gives each block two or three tiles): tensors of one element up to
+    several hundred tiles, starting anywhere in a block's range."""
+    rng = np.random.default_rng(11)
+    sizes = list(rng.integers(1, 250_000, 24)) + [1, 2, 4095, 4096, 4097, 8192, 12_289, 0, 3, 70_000, 1, 5, 640_000]
+    return [0] + list(np.cumsum(sizes).astype(int))
+
+
+_MANY = _many_tensor_offsets()
+
 RT_CASES = {
     "resnet20_conv_37k": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 8),
     "student_t_3x": (None, None, (1, 100), 1e-3, 5, 8),
@@ -220,6 +231,8 @@ RT_CASES = {
     # empty, 1-, 5-, 4096-, 4097-element, empty and 4-element tensors
     "ragged_tensors": (W.normal(8203, 8), [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8),
     "take_all": (W.normal(5000, 9), [0, 5000], (1, 1), 1e-3, 2, 4),
+    # the probe pass's per-block look-back across many tensor boundaries
+    "many_tensors_3m": (W.normal(_MANY[-1], 12), _MANY, (1, 100), 1e-3, 5, 8),
 }
 
 
@@ -368,7 +381,7 @@ def test_roundtrip_is_deterministic():
     np.testing.assert_array_equal(a["dense"], b["dense"])
 
 
-@pytest.mark.parametrize("name", ["resnet20_conv_37k", "ragged_tensors", "support_50k"])
+@pytest.mark.parametrize("name", ["resnet20_conv_37k", "ragged_tensors", "support_50k", "many_tensors_3m"])
 def test_overlapped_round_trip_matches_the_sequential_one(name):
     """dr_roundtrip runs the receiver's probe pass on a second stream while
     the sender fits its values; dr_payload_encode then dr_payload_decode run
