@@ -496,10 +496,14 @@ dr_status encode_prepare(const float *g, const dr_config *cfg, uint8_t *payload,
     return DR_OK;
 }
 
-dr_status encode_front(Encode &e, const float *g, uint64_t *counts_out, hipStream_t s) {
+// after_probe, if given, is recorded once the records' headers and filters
+// are written (the receiver's probe pass needs nothing more)
+dr_status encode_front(Encode &e, const float *g, uint64_t *counts_out, hipStream_t s,
+                       hipEvent_t after_probe = nullptr) {
     const Plan &p = e.p;
     const Work &w = e.w;
-    DR_HIP(run_init(w, p.t, s));
+    // counts_out starts as zeros (its flags words are OR-ed)
+    DR_HIP(run_init(w, p.t, s, false, {counts_out, counts_out ? 8ull * w.ntensors : 0}));
     if (p.any_topr)
         DR_HIP(launch_topr(w, g, (uint32_t)p.carve.hist_blocks, persist_grid(8), true, s));
     else
@@ -508,7 +512,7 @@ dr_status encode_front(Encode &e, const float *g, uint64_t *counts_out, hipStrea
         DR_HIP(launch_bloom_direct(w, true, p.dir_blocks, p.dir_slices, s));
     else
         DR_HIP(launch_bloom_insert(w, true, p.bl_chunks, p.bl_slices, p.max_slices, p.hash_per_round, p.kmax, s));
-    DR_HIP(launch_query_encode(w, g, persist_grid(4), counts_out, s));
+    DR_HIP(launch_query_encode(w, g, persist_grid(4), counts_out, s, after_probe));
     return DR_OK;
 }
 
@@ -676,7 +680,10 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
         st = decode_init(dd, true, ss->s);
         if (st != DR_OK) return st;
     }
-    st = encode_front(e, g, counts_out, s);
+    // the fork: once the sender's probe pass has written the records'
+    // headers and filters, the receiver's probe pass can run beside the
+    // sender's emit pass and value stage
+    st = encode_front(e, g, counts_out, s, overlap ? ss->fork : nullptr);
     if (st != DR_OK) return st;
     if (!overlap) {
         st = encode_back(e, s);
@@ -685,7 +692,6 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
         if (st != DR_OK) return st;
         return decode_back(dd, s);
     }
-    DR_HIP(hipEventRecord(ss->fork, s));
     DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
     trace_call(ss->s);  // per-kernel timing: the wait for the fork is idle time
     // CUs left to the sender: the sort and the fit want a few dozen when

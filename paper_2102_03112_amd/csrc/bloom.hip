@@ -563,6 +563,9 @@ __device__ void probe_total(const Work &w, const QueryOut &o, uint32_t t, uint32
         // the policy codes every positive (P0) or r of them
         td.npos = total;
         td.nv = td.in.policy == POLICY_P0 ? total : min(td.n, total);
+        // the record's header is complete here, so the receiver's probe
+        // pass can start as soon as this pass ends
+        value_setup_tensor(w, t, 1, o.counts_out);
     } else if (MODE == Q_PLAIN) {
         if (o.n_out) *o.n_out = total;  // one tensor
     } else {
@@ -963,9 +966,10 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     // stores stay in flight across them.
     uint32_t tile = blockIdx.x;
     uint32_t word = 0, q0n = 0, tn = 0;
-    // the sender's value set-up needs only the counts the probe pass left;
-    // block 0 runs it here instead of in a kernel of its own
-    if (MODE == Q_ENCODE && o.setup && blockIdx.x == 0) value_setup_block<NTHREADS>(w, 1, o.counts_out);
+    // the value stage's layout over the tensors needs only the per-tensor
+    // set-up the probe pass did; block 0 runs it here instead of in a kernel
+    // of its own
+    if (MODE == Q_ENCODE && o.setup && blockIdx.x == 0) value_layout_block<NTHREADS>(w);
     if (tile < w.ntiles_total) {
         q0n = w.toff[tile];
         tn = tensor_of_tile(w, tile);
@@ -1144,14 +1148,20 @@ static int probe_grid(const Work &w) {
     return (int)std::max(1u, std::min(cus, by_tiles));
 }
 
-hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, uint64_t *counts_out, hipStream_t s) {
+hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, uint64_t *counts_out, hipStream_t s,
+                               hipEvent_t after_probe) {
     QueryOut o{};
     o.g = g;
     o.setup = 1;
     o.counts_out = counts_out;
-    // the pass also scans its tile counts (probe_scan)
+    // the pass also scans its tile counts (probe_scan) and writes the
+    // records' headers
     k_probe<Q_ENCODE><<<probe_grid(w), PB_THREADS, 0, s>>>(w, o);
     trace_mark(s, "k_probe<Q_ENCODE>");
+    if (after_probe) {
+        hipError_t e = hipEventRecord(after_probe, s);
+        if (e != hipSuccess) return e;
+    }
     k_emit<Q_ENCODE><<<resident_grid(k_emit<Q_ENCODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_ENCODE>");
     return hipGetLastError();

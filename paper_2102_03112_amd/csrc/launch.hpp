@@ -67,8 +67,11 @@ hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream
 hipError_t launch_bloom_direct(const Work &w, bool from_bitmap, uint32_t blocks, uint32_t slices, hipStream_t s);
 hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_chunks, uint32_t total_slices,
                                uint32_t max_slices, uint32_t hash_per_round, uint32_t kmax, hipStream_t s);
-// the sender's query: probe, emit, and the value set-up (in the emit pass)
-hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, uint64_t *counts_out, hipStream_t s);
+// the sender's query: probe (with the per-tensor value set-up and headers),
+// then emit (with the layout over the tensors); after_probe, if given, is
+// recorded between the two
+hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, uint64_t *counts_out, hipStream_t s,
+                               hipEvent_t after_probe = nullptr);
 hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,
                               hipStream_t s);
 // the receiver's query in two halves: the probe pass (at most max_blocks
