@@ -133,10 +133,13 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_upfront(Work w, const uint32_
 //  4. finishes the look-back, publishes its inclusive prefix, and scatters.
 constexpr uint64_t ST_AGG = 1ull << 32, ST_INC = 2ull << 32;
 constexpr uint32_t SPIN_LIMIT = 1u << 20;
-constexpr uint32_t LB_WIN = 16;  // look-back window (tiles read together)
+constexpr uint32_t LB_WIN = 8;  // look-back window (tiles read together)
 constexpr uint32_t SORT_STEPS = TILE / NTHREADS;  // 16 keys per thread
 
-__global__ __launch_bounds__(NTHREADS) void k_sort_pass(Work w, const uint32_t *__restrict__ kin,
+// At most 168 VGPRs (three blocks per CU; 233 without the bound, which
+// left the 32 CUs the round trip gives the sender 64 block slots for a
+// 25.6 M-element gradient's 69 tiles, so 5 tiles waited for a second round).
+__global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(3))) void k_sort_pass(Work w, const uint32_t *__restrict__ kin,
                                                         const uint32_t *__restrict__ vin,
                                                         uint32_t *__restrict__ kout, uint32_t *__restrict__ vout,
                                                         uint32_t pass) {
