@@ -297,9 +297,10 @@ DR_EXPORT dr_status dr_payload_decode_sum(const uint8_t *const *payloads_h, uint
 
 /* dr_payload_encode followed by dr_payload_decode: one codec round trip of
  * the whole gradient, with the same results.  The receiver's query pass
- * needs only the records' headers and filters, so once the sender has
- * written them the library runs it on a second stream of its own (one per
- * device, created on first use) while the sender sorts and fits its values;
+ * needs only the records' headers and filters, so once the sender's query
+ * pass has written them the library runs it on a second stream of its own
+ * (one per device, created on first use) while the sender emits, sorts and
+ * fits its values (the receiver's set-up runs there from the start);
  * the second stream waits for `stream` and `stream` waits for it before the
  * receiver's last pass, so the call stays ordered on `stream` (also under
  * graph capture).  This needs room in `ws` for the receiver's own state

@@ -88,7 +88,7 @@ struct Carve {
     uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0, bnd = 0;
     bool query_only = false;  // descriptors, tile counts, the positives bitmap and the tile table only
     size_t bytes = 0;
-    size_t o_td, o_glob, o_done, o_pstat, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
+    size_t o_td, o_glob, o_pstat, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
         o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs, o_bnd;
 
     void plan() {
@@ -101,7 +101,6 @@ struct Carve {
         const uint64_t all = query_only ? 0 : 1;  // regions the query alone does not use
         o_td = take(sizeof(TDesc) * ntensors);
         o_glob = take(sizeof(Glob));
-        o_done = take(4 * ntensors);
         o_pstat = take(8ull * PSTAT_MAX);
         o_tcnt = take(4 * ntiles);
         o_toff = take(4 * ntiles);
@@ -138,7 +137,6 @@ struct Carve {
         w.ntensors = (uint32_t)ntensors;
         w.ntiles_total = (uint32_t)ntiles;
         w.slots = slots;
-        w.done = (uint32_t *)(ws + o_done);
         w.pstat = (uint64_t *)(ws + o_pstat);
         w.tcnt = (uint32_t *)(ws + o_tcnt);
         w.toff = (uint32_t *)(ws + o_toff);
@@ -440,10 +438,9 @@ hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s, b
                     ZeroRange extra = {nullptr, 0}) {
     ZeroArgs z;
     memset(&z, 0, sizeof z);
-    z.z[0] = {w.done, w.ntensors};
-    z.z[1] = {w.glob, sizeof(Glob) / 4};
-    z.z[2] = {w.pstat, 2ull * PSTAT_MAX};
-    z.n = 3;
+    z.z[0] = {w.glob, sizeof(Glob) / 4};
+    z.z[1] = {w.pstat, 2ull * PSTAT_MAX};
+    z.n = 2;
     if (!query_only) {
         z.z[z.n++] = {w.sdig, 4ull * SORT_BINS * w.ntensors};
         z.z[z.n++] = {w.hist, (uint64_t)HIST1_BINS * w.ntensors};
@@ -644,10 +641,11 @@ bool side_stream(SideStream **out) {
 }
 
 // dr_roundtrip: the receiver's probe pass needs only the payload's header
-// and filter, which the sender has written once its values' layout is set,
-// so it runs on a second stream while the sender sorts and fits its values
-// (the probe is bound by L2 request throughput and loses little when some
-// CUs are left to the sort and the fit).  The receiver then
+// and filter, which the sender's probe pass has written (it sets each
+// tensor's run shape and header where it learns |P|), so it runs on a
+// second stream while the sender emits, sorts and fits its values (the
+// probe is bound by L2 request throughput and loses little when some CUs
+// are left to the sender).  The receiver then
 // uses its own query-only work after the sender's in the workspace; without
 // room for it, or with segmentation passes that rewrite the header after
 // the sort, the two sides run one after the other.

@@ -167,7 +167,6 @@ struct Work {
     uint32_t ntensors;
     uint32_t ntiles_total;    // sum of ntiles
     uint64_t slots;           // padded elements = ntiles_total * TILE
-    uint32_t *done;           // per-tensor completion counters (zeroed at set-up)
     uint64_t *pstat;          // probe pass look-back: per block (flag << 62 | trailing count), zeroed at set-up
     uint32_t *tcnt;           // per-tile counts of the current ordered pass
     uint32_t *toff;           // per-tile exclusive offsets within the tensor

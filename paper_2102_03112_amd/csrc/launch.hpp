@@ -56,9 +56,6 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int 
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s);
 hipError_t launch_compact_selection(const Work &w, const float *g, float *val_out, int grid_persist, hipStream_t s);
 hipError_t launch_tile_popc(const Work &w, const uint32_t *bits, int grid_persist, hipStream_t s);
-// which: 0 |S| (and the filter size), 1 sender |P|, 2 receiver |P| (also
-// into counts_out, checked against the payload header), 3 into *n_out
-hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out = nullptr);
 
 // bloom.hip
 // Insert in rounds of `hash_per_round` hash functions (the position buffer

@@ -651,13 +651,12 @@ __global__ __launch_bounds__(NTHREADS) void k_tile_popc(Work w, const uint32_t *
     }
 }
 
-// toff = exclusive scan of tcnt over the tiles of each tensor; the total
-// goes to the tensor's field `which` (0: n, 1: nv, 2: nv_dec, 3: *n_out)
+// toff = exclusive scan of the selection's tcnt over the tiles of each
+// tensor; the total is |S| (the queries scan their counts in the probe pass)
 constexpr uint32_t TSCAN_THREADS = 1024;
 constexpr uint32_t TSCAN_PER = 8;  // counts per thread per step, loaded together
 
-__global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, uint64_t *n_out,
-                                                             uint64_t *counts_out) {
+__global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w) {
     TDesc &td = w.td[blockIdx.x];
     __shared__ uint32_t scratch[TSCAN_THREADS / 64 + 1];
     const uint32_t nt = td.in.ntiles;
@@ -683,31 +682,10 @@ __global__ __launch_bounds__(TSCAN_THREADS) void k_tile_scan(Work w, int which, 
         carry += tot;
     }
     if (threadIdx.x == 0) {
-        if (which == 0) {
-            const uint32_t cap = td.in.r != R_NONZERO ? td.in.r : td.in.d;
-            td.n = carry < cap ? carry : cap;
-            if (td.in.r != R_NONZERO && carry != td.in.r) atomicOr(&td.flags, FLAG_COUNT);
-            td.m_words = filter_words(td);
-        } else if (which == 1) {
-            // the policy codes every positive (P0) or r of them
-            td.npos = carry;
-            td.nv = td.in.policy == POLICY_P0 ? carry : min(td.n, carry);
-        } else if (which == 2) {
-            td.nv_dec = carry;
-            if (counts_out) {
-                counts_out[4 * blockIdx.x + 2] = carry;
-                const uint8_t *rec = td.in.rec;
-                const uint32_t hdr_npos = ((const uint32_t *)rec)[H_NPOS];
-                uint32_t f = td.flags;
-                if (carry != hdr_npos) f |= FLAG_DEC_MISMATCH;
-                // atomic: the sender's last passes may flag the same word
-                // while the receiver's query runs beside them
-                if (f & FLAG_DEC_MISMATCH)
-                    atomicOr((unsigned long long *)&counts_out[4 * blockIdx.x + 3], FLAG_DEC_MISMATCH);
-            }
-        } else if (n_out) {
-            *n_out = carry;
-        }
+        const uint32_t cap = td.in.r != R_NONZERO ? td.in.r : td.in.d;
+        td.n = carry < cap ? carry : cap;
+        if (td.in.r != R_NONZERO && carry != td.in.r) atomicOr(&td.flags, FLAG_COUNT);
+        td.m_words = filter_words(td);
     }
 }
 
@@ -717,11 +695,6 @@ hipError_t launch_tile_popc(const Work &w, const uint32_t *bits, int grid_persis
     return hipGetLastError();
 }
 
-hipError_t launch_tile_scan(const Work &w, int which, uint64_t *n_out, hipStream_t s, uint64_t *counts_out) {
-    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, which, n_out, counts_out);
-    trace_mark(s, "k_tile_scan");
-    return hipGetLastError();
-}
 
 // S = the selection bitmap's set bits in ascending order (val_out: g there).
 // Threads 0..127 of a block own one bitmap word of the tile each.
@@ -756,7 +729,7 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
                                     hipStream_t s) {
     k_tile_popc<<<grid_persist, NTHREADS, 0, s>>>(w, w.selbits);
     trace_mark(s, "k_tile_popc");
-    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr);
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w);
     trace_mark(s, "k_tile_scan");
     k_compact_selection<<<grid_persist, NTHREADS, 0, s>>>(w, g, val_out);
     trace_mark(s, "k_compact_selection");
@@ -768,7 +741,7 @@ hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipSt
     k_select_filter<<<resident_grid(k_select_filter, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     // |S| from the per-tile counts of the filter pass
-    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w, 0, nullptr, nullptr);
+    k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w);
     trace_mark(s, "k_tile_scan");
     return hipGetLastError();
 }
