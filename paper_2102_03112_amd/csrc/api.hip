@@ -692,11 +692,13 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     }
     DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
     trace_call(ss->s);  // per-kernel timing: the wait for the fork is idle time
-    // CUs left to the sender: the sort and the fit want a few dozen when
-    // the probe pass is short; for long probe passes (large gradients) each
-    // CU taken from the probe costs more than the sender gains (measured on
-    // 25.6 M, 138 M and 355 M elements)
-    const uint32_t reserve = cfg->offsets_h[cfg->n_tensors] <= (1ull << 26) ? 32u : 8u;
+    // CUs left to the sender: one in each of the 32 shader engines (8 XCDs
+    // of 4).  Workgroups are dealt to the engines in turn, so a kernel
+    // launched beside the probe pass needs a free CU in every engine: with
+    // fewer left, its workgroups dealt to a full engine wait for the probe
+    // pass to end, and the sender's value stage runs after it instead of
+    // beside it (seen with 8, 16 and 24 left)
+    const uint32_t reserve = 32u;
     st = decode_probe(dd, (uint32_t)std::max(1, dr::device_cus() - (int)reserve), ss->s);
     if (st != DR_OK) return st;
     DR_HIP(hipEventRecord(ss->join, ss->s));
