@@ -52,8 +52,6 @@ dr_status hip_fail(hipError_t e, const char *where) {
         if (e_ != hipSuccess) return hip_fail(e_, #call);  \
     } while (0)
 
-constexpr uint32_t MAX_SLICES = 16384;  // LDS counters of the insert: filters up to 2^30 bits
-
 uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
 uint64_t align_up(uint64_t a, uint64_t b) { return ceil_div(a, b) * b; }
 
@@ -166,12 +164,12 @@ struct Carve {
         w.valB = (uint32_t *)(ws + o_valB);
         w.sig = (uint32_t *)(ws + o_sig);
         w.vsorted = (float *)(ws + o_vs);
-        w.bpos = (uint16_t *)(ws + o_keyA);  // borrows keyA .. vsorted
+        w.bpos = (uint32_t *)(ws + o_keyA);  // borrows keyA .. vsorted
         w.bounds = (uint32_t *)(ws + o_bnd);
         return w;
     }
 
-    uint64_t pos_capacity() const { return (o_vs + 4 * slots - o_keyA) / 2; }
+    uint64_t pos_capacity() const { return (o_vs + 4 * slots - o_keyA) / 4; }
 };
 
 // Tiles per top-r histogram block (1024 threads): about 256 blocks over the
@@ -191,10 +189,11 @@ Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     // chord run starts: at most (runs + 1) per tensor
     c.bnd = std::min<uint64_t>(n_tensors * (uint64_t)(DR_MAX_SEGMENTS + 1), d + 2 * n_tensors);
     // Bloom table: per tensor (slices x chunks) with at most MAX_CHUNKS
-    // chunks and ceil(m / 2^14) slices, where m <= 47 n + 32 (k <= 32 gives
-    // -ln(fpr) / (ln 2)^2 < 47 bits per item); plus one filter of MAX_SLICES
-    // for a standalone insert whose filter is larger than its item count
-    c.bslices = 47 * c.slots / (1u << 14) + 2 * n_tensors + MAX_SLICES;
+    // chunks and at most ceil(m / 2^14) slices, where m <= 47 n + 32 (k <= 32
+    // gives -ln(fpr) / (ln 2)^2 < 47 bits per item); plus one filter of
+    // BL_MAX_SLICES for a standalone insert whose filter is larger than its
+    // item count
+    c.bslices = 47 * c.slots / (1u << SLICE_LOG2_MIN) + 2 * n_tensors + BL_MAX_SLICES;
     c.btab = c.bslices * MAX_CHUNKS;
     c.plan();
     return c;
@@ -230,8 +229,11 @@ void plan_bloom(TInit &in, uint64_t n_cap, uint64_t m_cap_bits, bool from_bitmap
         in.bl_chunk = (uint32_t)chunk;
         in.bl_nchunks = (uint32_t)(n_cap ? ceil_div(n_cap, chunk) : 0);
     }
-    // smaller slices give the fill more blocks; large filters need 2^16-bit slices
-    in.slice_log2 = ceil_div(m_cap_bits, 1u << 14) <= MAX_SLICES ? 14 : SLICE_LOG2_MAX;
+    // About 256 slices (of 2^14 to 2^20 bits): enough fill blocks, and runs
+    // of about 64 records per slice in each of the scatter's groups
+    uint32_t sl2 = SLICE_LOG2_MIN;
+    while (sl2 < SLICE_LOG2_MAX && ceil_div(m_cap_bits, 1ull << sl2) > 256) ++sl2;
+    in.slice_log2 = sl2;
     in.bl_nslices = (uint32_t)ceil_div(m_cap_bits, 1ull << in.slice_log2);
     in.bl_chunk0 = p.bl_chunks;
     in.bl_slice0 = p.bl_slices;
@@ -253,6 +255,10 @@ void plan_bloom_rounds(Plan &p, uint32_t k) {
     uint64_t h = p.bl_items ? cap / p.bl_items : k;
     if (h < 1) h = 1;
     if (h > k) h = k;
+    // a tensor's records are addressed with 32-bit offsets
+    uint64_t ncap_max = 0;
+    for (uint64_t n : p.bl_ncap) ncap_max = std::max(ncap_max, n);
+    while (h > 1 && ncap_max * h >= (1ull << 31)) --h;
     p.hash_per_round = (uint32_t)h;
     uint64_t at = 0;
     for (size_t i = 0; i < p.t.size(); ++i) {
@@ -279,7 +285,7 @@ void plan_bloom_direct(Plan &p, bool from_bitmap) {
         for (uint64_t m : p.bl_mcap) tot += ceil_div(m / 32, DIR_SLICE_WORDS) * g * std::min<uint64_t>(DIR_SLICE_WORDS, m / 32);
         return tot;
     };
-    const uint64_t cap_words = p.carve.pos_capacity() / 2;  // the position buffer, as 32-bit words
+    const uint64_t cap_words = p.carve.pos_capacity();  // the position buffer, in 32-bit words
     while (G > 1 && words(G) > cap_words) G /= 2;
     if (words(G) > cap_words) return;
     uint64_t blk = 0, sl = 0, pb = 0;
@@ -374,7 +380,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         if (!bloom_params_host(n_cap, cfg->fpr, &m_cap, &kk))
             return fail(DR_ENOTSUP, "tensor %llu: filter of %llu items needs 2^32 bits or more",
                         (unsigned long long)t, (unsigned long long)n_cap);
-        if (ceil_div(m_cap, 1ull << SLICE_LOG2_MAX) > MAX_SLICES)
+        if (ceil_div(m_cap, 1ull << SLICE_LOG2_MAX) > BL_MAX_SLICES)
             return fail(DR_ENOTSUP, "tensor %llu: filter larger than 2^30 bits", (unsigned long long)t);
         in.off = cfg->offsets_h[t];
         in.d = (uint32_t)d;
@@ -983,7 +989,7 @@ dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap
     if (m_bits < 32 || (m_bits & 31) || m_bits >= (1ull << 32)) return fail(DR_EINVAL, "bad m_bits");
     if (k < 1 || k > 32) return fail(DR_EINVAL, "k must be in [1, 32]");
     if (n_cap >= (1ull << 32)) return fail(DR_EINVAL, "n_cap >= 2^32");
-    if (ceil_div(m_bits, 1ull << SLICE_LOG2_MAX) > MAX_SLICES) return fail(DR_ENOTSUP, "filter larger than 2^30 bits");
+    if (ceil_div(m_bits, 1ull << SLICE_LOG2_MAX) > BL_MAX_SLICES) return fail(DR_ENOTSUP, "filter larger than 2^30 bits");
     Plan p = single_plan(n_cap);
     TInit &in = p.t[0];
     in.k = k;

@@ -52,14 +52,15 @@ __device__ __forceinline__ uint32_t tensor_of_slice(const Work &w, uint32_t s) {
     return lo;
 }
 
-// Calls f(index) for every item of chunk c of tensor td (block-strided).
-template <bool FROM_BITMAP, typename F>
+// Calls f(index) for every item of chunk c of tensor td (strided over the
+// block's NT threads).
+template <bool FROM_BITMAP, uint32_t NT, typename F>
 __device__ __forceinline__ void for_chunk_items(const Work &w, const TDesc &td, uint32_t c, F f) {
     if (FROM_BITMAP) {
         const uint32_t w0 = c * td.in.bl_chunk * TILE_WORDS;
         const uint32_t w1 = min(td.in.ntiles * TILE_WORDS, w0 + td.in.bl_chunk * TILE_WORDS);
         const uint32_t *sb = w.selbits + (td.in.slot >> 5);
-        for (uint32_t x = w0 + threadIdx.x; x < w1; x += NTHREADS) {
+        for (uint32_t x = w0 + threadIdx.x; x < w1; x += NT) {
             uint32_t word = sb[x];
             while (word) {
                 const uint32_t b = __ffs(word) - 1;
@@ -71,7 +72,7 @@ __device__ __forceinline__ void for_chunk_items(const Work &w, const TDesc &td, 
         const uint32_t n = td.n, chunk = td.in.bl_chunk;
         const uint32_t q0 = c * chunk, q1 = min(n, q0 + chunk);
         const uint32_t *S = w.S + td.in.slot;
-        for (uint32_t q = q0 + threadIdx.x; q < q1; q += NTHREADS) f(S[q]);
+        for (uint32_t q = q0 + threadIdx.x; q < q1; q += NT) f(S[q]);
     }
 }
 
@@ -80,8 +81,13 @@ __device__ __forceinline__ uint32_t active_chunks(const TDesc &td, bool from_bit
     return (td.n + td.in.bl_chunk - 1) / td.in.bl_chunk;
 }
 
+// The bucketed insert's kernels run 1024 threads per block: a chunk's
+// items are hashed one after another per thread, and the LDS atomics of the
+// count and scatter passes need many waves in flight to hide their latency.
+constexpr uint32_t BL_THREADS = 1024;
+
 template <bool FROM_BITMAP>
-__global__ __launch_bounds__(NTHREADS) void k_bloom_count(Work w, uint32_t j0, uint32_t j1) {
+__global__ __launch_bounds__(BL_THREADS) void k_bloom_count(Work w, uint32_t j0, uint32_t j1) {
     extern __shared__ uint32_t lh[];
     const uint32_t t = tensor_of_chunk(w, blockIdx.x);
     const TDesc &td = w.td[t];
@@ -90,18 +96,18 @@ __global__ __launch_bounds__(NTHREADS) void k_bloom_count(Work w, uint32_t j0, u
     const uint32_t m_bits = td.m_words * 32u;
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
-    for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) lh[s] = 0;
+    for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) lh[s] = 0;
     __syncthreads();
     const uint32_t je = min(j1, td.in.k);
     if (je > j0) {
-        for_chunk_items<FROM_BITMAP>(w, td, c, [&](uint32_t x) {
+        for_chunk_items<FROM_BITMAP, BL_THREADS>(w, td, c, [&](uint32_t x) {
             const uint32_t km = mm3_key(x);
             for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[bloom_pos(km, j, m_bits) >> sl2], 1u);
         });
     }
     __syncthreads();
     uint32_t *tab = w.btab + td.in.bl_tab0;
-    for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) tab[(uint64_t)s * td.in.bl_nchunks + c] = lh[s];
+    for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) tab[(uint64_t)s * td.in.bl_nchunks + c] = lh[s];
 }
 
 // Row scan: for slice s of a tensor (one block each), offsets of its chunks
@@ -153,12 +159,30 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_bloom_rowbase(Work w, uint32_t
 }
 
 // Scatter: each position goes to its slice's bucket, after the chunk's
-// offset within that bucket.
+// offset within that bucket, as a 32-bit offset within the slice.  A block
+// takes its chunk's items 4096 at a time and their positions four hashes at
+// a time (16 K positions), groups them by slice in LDS (a counting sort:
+// ranks from LDS atomics, a scan of the counts, then the placement), and
+// writes each slice's run with consecutive lanes on consecutive addresses.
+// Stored straight from the hashing lanes, each 4-byte record was an L2
+// request of its own, and the pass ran at the L2 request rate.
+constexpr uint32_t SC_ITEMS = 4096;                      // items per batch
+constexpr uint32_t SC_HASHES = 4;                        // hashes per group
+constexpr uint32_t SC_PER = SC_ITEMS / BL_THREADS;       // items per thread
+constexpr uint32_t SC_STAGE = SC_ITEMS * SC_HASHES;      // positions per group
+
 template <bool FROM_BITMAP>
-__global__ __launch_bounds__(NTHREADS) void k_bloom_scatter(Work w, uint32_t j0, uint32_t j1) {
-    extern __shared__ uint32_t lc[];
+__global__ __launch_bounds__(BL_THREADS) void k_bloom_scatter(Work w, uint32_t j0, uint32_t j1) {
+    __shared__ uint32_t gcur[BL_MAX_SLICES];  // next record of this chunk in each slice's bucket
+    __shared__ uint32_t cnt[BL_MAX_SLICES];   // the group's positions per slice
+    __shared__ uint32_t off[BL_MAX_SLICES];   // their start in the staging area
+    __shared__ uint32_t items[SC_ITEMS];
+    __shared__ uint32_t stage[SC_STAGE];
+    __shared__ uint16_t sbkt[SC_STAGE];
+    __shared__ uint32_t scratch[BL_THREADS / 64 + 1];
+    __shared__ uint32_t s_nitems;
     const uint32_t t = tensor_of_chunk(w, blockIdx.x);
-    const TDesc &td = w.td[t];
+    TDesc &td = w.td[t];
     const uint32_t c = blockIdx.x - td.in.bl_chunk0;
     if (c >= td.in.bl_nchunks || c >= active_chunks(td, FROM_BITMAP)) return;
     const uint32_t je = min(j1, td.in.k);
@@ -166,23 +190,126 @@ __global__ __launch_bounds__(NTHREADS) void k_bloom_scatter(Work w, uint32_t j0,
     const uint32_t m_bits = td.m_words * 32u;
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
+    if (nsl > BL_MAX_SLICES) {  // excluded by the plan
+        if (threadIdx.x == 0) atomicOr(&td.flags, FLAG_CAPACITY);
+        return;
+    }
     const uint32_t *tab = w.btab + td.in.bl_tab0;
     const uint32_t *base = w.brow + w.bslices + td.in.bl_slice0;
-    for (uint32_t s = threadIdx.x; s < nsl; s += NTHREADS) lc[s] = base[s] + tab[(uint64_t)s * td.in.bl_nchunks + c];
-    __syncthreads();
-    uint16_t *pos = w.bpos + td.in.bl_pos0;
+    for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) {
+        gcur[s] = base[s] + tab[(uint64_t)s * td.in.bl_nchunks + c];
+        cnt[s] = 0;
+    }
+    uint32_t *pos = w.bpos + td.in.bl_pos0;
+    const uint64_t poscap = td.in.bl_poscap;
     const uint32_t mask = (1u << sl2) - 1;
-    for_chunk_items<FROM_BITMAP>(w, td, c, [&](uint32_t x) {
-        const uint32_t km = mm3_key(x);
-        for (uint32_t j = j0; j < je; ++j) {
-            const uint32_t p = bloom_pos(km, j, m_bits);
-            const uint32_t at = atomicAdd(&lc[p >> sl2], 1u);
-            if (at < td.in.bl_poscap) pos[at] = (uint16_t)(p & mask);
+    // the chunk's items: bitmap words [x0, x1) or list entries [x0, x1)
+    uint32_t x0, x1;
+    const uint32_t *src;
+    if (FROM_BITMAP) {
+        x0 = c * td.in.bl_chunk * TILE_WORDS;
+        x1 = min(td.in.ntiles * TILE_WORDS, x0 + td.in.bl_chunk * TILE_WORDS);
+        src = w.selbits + (td.in.slot >> 5);
+    } else {
+        x0 = c * td.in.bl_chunk;
+        x1 = min(td.n, x0 + td.in.bl_chunk);
+        src = w.S + td.in.slot;
+    }
+    __syncthreads();
+    while (x0 < x1) {
+        // 1. the batch's items into LDS
+        uint32_t nitems;
+        if (FROM_BITMAP) {
+            // the longest run of words from x0 whose items fit (one word at least)
+            const uint32_t x = x0 + threadIdx.x;
+            const uint32_t word = x < x1 ? src[x] : 0u;
+            const uint32_t pc = __popc(word);
+            uint32_t tot;
+            const uint32_t ex = block_excl_scan_n<BL_THREADS, true>(pc, scratch, &tot);
+            const bool take = ex + pc <= SC_ITEMS;  // a prefix of the threads
+            if (take) {
+                uint32_t wd = word, e = ex;
+                while (wd) {
+                    items[e++] = x * 32u + (uint32_t)(__ffs(wd) - 1);
+                    wd &= wd - 1;
+                }
+            }
+            const uint32_t ntake = (uint32_t)__syncthreads_count(take);
+            if (take && threadIdx.x == ntake - 1) s_nitems = ex + pc;
+            __syncthreads();
+            nitems = s_nitems;
+            x0 += ntake;
+        } else {
+            nitems = min(SC_ITEMS, x1 - x0);
+#pragma unroll
+            for (uint32_t u = 0; u < SC_PER; ++u) {
+                const uint32_t i = u * BL_THREADS + threadIdx.x;
+                if (i < nitems) items[i] = src[x0 + i];
+            }
+            x0 += nitems;
+            __syncthreads();
         }
-    });
+        uint32_t km[SC_PER];
+#pragma unroll
+        for (uint32_t u = 0; u < SC_PER; ++u) {
+            const uint32_t i = u * BL_THREADS + threadIdx.x;
+            km[u] = i < nitems ? mm3_key(items[i]) : 0u;
+        }
+        for (uint32_t jg = j0; jg < je; jg += SC_HASHES) {
+            // 2. positions, and their ranks within their slice's group
+            uint32_t pr[SC_PER * SC_HASHES], br[SC_PER * SC_HASHES];
+#pragma unroll
+            for (uint32_t u = 0; u < SC_PER; ++u) {
+                const bool iv = u * BL_THREADS + threadIdx.x < nitems;
+#pragma unroll
+                for (uint32_t v = 0; v < SC_HASHES; ++v) {
+                    const uint32_t q = u * SC_HASHES + v;
+                    br[q] = 0xffffffffu;
+                    pr[q] = 0;
+                    if (iv && jg + v < je) {
+                        const uint32_t p = bloom_pos(km[u], jg + v, m_bits);
+                        const uint32_t b = p >> sl2;
+                        br[q] = (b << 16) | atomicAdd(&cnt[b], 1u);
+                        pr[q] = p & mask;
+                    }
+                }
+            }
+            lds_barrier();
+            // 3. each slice's place in the staging area
+            uint32_t tot;
+            const uint32_t ex = block_excl_scan_n<BL_THREADS, true>(threadIdx.x < nsl ? cnt[threadIdx.x] : 0u, scratch,
+                                                                    &tot);
+            if (threadIdx.x < nsl) off[threadIdx.x] = ex;
+            lds_barrier();
+#pragma unroll
+            for (uint32_t q = 0; q < SC_PER * SC_HASHES; ++q) {
+                if (br[q] != 0xffffffffu) {
+                    const uint32_t b = br[q] >> 16;
+                    const uint32_t at = off[b] + (br[q] & 0xffffu);
+                    stage[at] = pr[q];
+                    sbkt[at] = (uint16_t)b;
+                }
+            }
+            lds_barrier();
+            // 4. each slice's run, coalesced, after the chunk's earlier records
+            for (uint32_t i = threadIdx.x; i < tot; i += BL_THREADS) {
+                const uint32_t b = sbkt[i];
+                const uint32_t g = gcur[b] + (i - off[b]);
+                if (g < poscap) pos[g] = stage[i];
+            }
+            lds_barrier();
+            for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) {
+                gcur[s] += cnt[s];
+                cnt[s] = 0;
+            }
+            lds_barrier();
+        }
+    }
 }
 
-__global__ __launch_bounds__(NTHREADS) void k_bloom_fill(Work w, uint32_t j0, uint32_t j1) {
+// Fill: one block per slice sets its bucket's bits in an LDS copy of the
+// slice (up to 128 KiB) and writes the slice out.
+__global__ __launch_bounds__(BL_THREADS) void k_bloom_fill(Work w, uint32_t j0, uint32_t j1) {
     __shared__ uint32_t words[SLICE_WORDS_MAX];
     const uint32_t t = tensor_of_slice(w, blockIdx.x);
     const TDesc &td = w.td[t];
@@ -197,23 +324,32 @@ __global__ __launch_bounds__(NTHREADS) void k_bloom_fill(Work w, uint32_t j0, ui
     uint32_t *out = td.in.bits + (uint64_t)s * slice_words;
     const uint32_t lim = min(slice_words, m_words - s * slice_words);
     // the first round starts from an empty slice, later rounds add to it
-    for (uint32_t i = threadIdx.x; i < slice_words; i += NTHREADS) words[i] = (j0 > 0 && i < lim) ? out[i] : 0u;
+    for (uint32_t i = threadIdx.x; i < slice_words; i += BL_THREADS) words[i] = (j0 > 0 && i < lim) ? out[i] : 0u;
     __syncthreads();
     const uint32_t je = min(j1, td.in.k);
     if (je > j0) {
         const uint32_t start = w.brow[w.bslices + blockIdx.x];
         uint32_t end = start + w.brow[blockIdx.x];
         if (end > td.in.bl_poscap) end = (uint32_t)td.in.bl_poscap;
-        const uint16_t *pos = w.bpos + td.in.bl_pos0;
+        const uint32_t *pos = w.bpos + td.in.bl_pos0;
         if (td.in.bl_nchunks > 0) {
-            for (uint32_t q = start + threadIdx.x; q < end; q += NTHREADS) {
-                const uint32_t p = pos[q];
-                atomicOr(&words[p >> 5], 1u << (p & 31u));
+            // eight loads in flight per thread before their bits are set
+            constexpr uint32_t U = 8;
+            for (uint32_t q0 = start; q0 < end; q0 += U * BL_THREADS) {
+                uint32_t p[U];
+#pragma unroll
+                for (uint32_t u = 0; u < U; ++u) {
+                    const uint32_t q = q0 + u * BL_THREADS + threadIdx.x;
+                    p[u] = q < end ? pos[q] : 0xffffffffu;
+                }
+#pragma unroll
+                for (uint32_t u = 0; u < U; ++u)
+                    if (p[u] != 0xffffffffu) atomicOr(&words[p[u] >> 5], 1u << (p[u] & 31u));
             }
         }
     }
     __syncthreads();
-    for (uint32_t i = threadIdx.x; i < lim; i += NTHREADS) out[i] = words[i];
+    for (uint32_t i = threadIdx.x; i < lim; i += BL_THREADS) out[i] = words[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -330,7 +466,7 @@ __global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct(Work w) {
         }
     }
     __syncthreads();
-    uint32_t *part = (uint32_t *)w.bpos + td.in.dir_pb + (uint64_t)local * td.in.dir_sw;
+    uint32_t *part = w.bpos + td.in.dir_pb + (uint64_t)local * td.in.dir_sw;
     if ((((uintptr_t)part) & 15u) == 0) {
         for (uint32_t i = threadIdx.x; i < nw / 4; i += DIR_THREADS) ((uint4 *)part)[i] = ((const uint4 *)sl)[i];
         for (uint32_t i = (nw & ~3u) + threadIdx.x; i < nw; i += DIR_THREADS) part[i] = sl[i];
@@ -352,7 +488,7 @@ __global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct_or(Work w) {
     const uint32_t w0 = s * DIR_SLICE_WORDS;
     if (w0 >= m_words || wi >= min(DIR_SLICE_WORDS, m_words - w0)) return;
     const uint32_t G = td.in.dir_g, sw = td.in.dir_sw;
-    const uint32_t *part = (const uint32_t *)w.bpos + td.in.dir_pb + (uint64_t)s * G * sw + wi;
+    const uint32_t *part = w.bpos + td.in.dir_pb + (uint64_t)s * G * sw + wi;
     uint32_t acc = 0;
     uint32_t c = 0;
     for (; c + 8 <= G; c += 8) {  // eight partials in flight
@@ -387,21 +523,21 @@ hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_c
         const uint32_t j1 = j0 + hash_per_round;
         if (total_chunks) {
             if (from_bitmap)
-                k_bloom_count<true><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+                k_bloom_count<true><<<total_chunks, BL_THREADS, lds, s>>>(w, j0, j1);
             else
-                k_bloom_count<false><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+                k_bloom_count<false><<<total_chunks, BL_THREADS, lds, s>>>(w, j0, j1);
             trace_mark(s, "k_bloom_count");
             k_bloom_rowscan<<<total_slices, NTHREADS, 0, s>>>(w, j0, from_bitmap ? 1 : 0);
             trace_mark(s, "k_bloom_rowscan");
             k_bloom_rowbase<<<w.ntensors, SCAN_THREADS, 0, s>>>(w, j0);
             trace_mark(s, "k_bloom_rowbase");
             if (from_bitmap)
-                k_bloom_scatter<true><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+                k_bloom_scatter<true><<<total_chunks, BL_THREADS, 0, s>>>(w, j0, j1);
             else
-                k_bloom_scatter<false><<<total_chunks, NTHREADS, lds, s>>>(w, j0, j1);
+                k_bloom_scatter<false><<<total_chunks, BL_THREADS, 0, s>>>(w, j0, j1);
             trace_mark(s, "k_bloom_scatter");
         }
-        k_bloom_fill<<<total_slices, NTHREADS, 0, s>>>(w, j0, j1);
+        k_bloom_fill<<<total_slices, BL_THREADS, 0, s>>>(w, j0, j1);
         trace_mark(s, "k_bloom_fill");
         j0 = j1;
     } while (j0 < kmax);

@@ -24,13 +24,15 @@ constexpr uint32_t NTHREADS = 256;            // threads per block (4 waves of 6
 constexpr uint32_t NWAVES = NTHREADS / 64;
 constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
 constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: fewest tiles per chunk
-constexpr uint32_t MAX_CHUNKS = 256;
+constexpr uint32_t MAX_CHUNKS = 256;           // Bloom insert: most item chunks per tensor
 constexpr uint32_t DIR_SLICE_LOG2 = 20;        // direct insert: 2^20-bit (128 KiB) slices in LDS
 constexpr uint32_t DIR_SLICE_WORDS = 1u << (DIR_SLICE_LOG2 - 5);
 constexpr uint64_t DIR_MAX_BITS = 8ull << DIR_SLICE_LOG2;  // at most 8 slices per tensor
-constexpr int BUFFER_RSRC_WORD3 = 0x00020000;  // gfx9 buffer descriptor word 3 (32-bit dword format)          // Bloom insert: most item chunks per tensor
-constexpr uint32_t SLICE_LOG2_MAX = 16;       // Bloom fill slices: at most 2^16 bits (8 KiB of LDS)
+constexpr int BUFFER_RSRC_WORD3 = 0x00020000;  // gfx9 buffer descriptor word 3 (32-bit dword format)
+constexpr uint32_t SLICE_LOG2_MIN = 14;       // Bloom fill slices: 2^14 to 2^20 bits (2 to 128 KiB of LDS)
+constexpr uint32_t SLICE_LOG2_MAX = 20;
 constexpr uint32_t SLICE_WORDS_MAX = (1u << SLICE_LOG2_MAX) / 32;
+constexpr uint32_t BL_MAX_SLICES = 1024;      // Bloom insert: slices per filter (filters up to 2^30 bits)
 constexpr uint32_t HIST1_BITS = 11;           // first top-r digit: key bits 30..20
 constexpr uint32_t HIST1_BINS = 1u << HIST1_BITS;
 constexpr uint32_t HIST1_SHIFT = 20;
@@ -191,7 +193,7 @@ struct Work {
     float *vsorted;           // values in sorted order, per tensor slot
     double *fit_part;         // fit: partial moments
     uint32_t fit_runs;
-    uint16_t *bpos;           // Bloom insert: bucketed in-slice positions
+    uint32_t *bpos;           // Bloom insert: bucketed in-slice positions
     uint32_t *btab;           // Bloom insert: per (slice, chunk) counts, then offsets within the slice
     uint32_t *brow;           // Bloom insert: per reserved slice, its count; brow + bslices: its start
     uint32_t bslices;         // Bloom insert: reserved slices over all tensors

@@ -92,7 +92,10 @@ def test_support_parity(d, kind):
 @pytest.mark.parametrize(
     "d,n,fpr",
     [(1000, 0, 1e-3), (1000, 1, 1e-3), (36_864, 369, 1e-3), (1 << 20, 10_486, 1e-3), (8192, 8192, 1e-4),
-     (300_000, 100_000, 1e-9), (200_000, 5000, 0.5), (25_557_032, 255_571, 1e-3)],
+     (300_000, 100_000, 1e-9), (200_000, 5000, 0.5), (25_557_032, 255_571, 1e-3),
+     # filters above 2^23 bits take the bucketed insert: 2^16-bit slices, and
+     # 2^18-bit slices with the 13 hashes in three rounds
+     (4_000_000, 1_000_000, 1e-3), (3_000_000, 2_500_000, 1e-4)],
 )
 def test_bloom_encode_parity(d, n, fpr):
     log(f"bloom_encode d={d} n={n} fpr={fpr}")
@@ -228,6 +231,8 @@ RT_CASES = {
     "resnet20_conv_37k": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 8),
     "student_t_3x": (None, None, (1, 100), 1e-3, 5, 8),
     "support_50k": (W.sparse_normal(50_000, 7, 0.4), [0, 50_000], None, 1e-4, 3, 16),
+    # a filter planned for 1 M items: the bucketed insert, in three rounds
+    "support_1m": (W.sparse_normal(1_000_000, 13, 0.4), [0, 1_000_000], None, 1e-4, 3, 16),
     # empty, 1-, 5-, 4096-, 4097-element, empty and 4-element tensors
     "ragged_tensors": (W.normal(8203, 8), [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8),
     "take_all": (W.normal(5000, 9), [0, 5000], (1, 1), 1e-3, 2, 4),
@@ -381,7 +386,7 @@ def test_roundtrip_is_deterministic():
     np.testing.assert_array_equal(a["dense"], b["dense"])
 
 
-@pytest.mark.parametrize("name", ["resnet20_conv_37k", "ragged_tensors", "support_50k", "many_tensors_3m"])
+@pytest.mark.parametrize("name", ["resnet20_conv_37k", "ragged_tensors", "support_50k", "support_1m", "many_tensors_3m"])
 def test_overlapped_round_trip_matches_the_sequential_one(name):
     """dr_roundtrip runs the receiver's probe pass on a second stream while
     the sender fits its values; dr_payload_encode then dr_payload_decode run
