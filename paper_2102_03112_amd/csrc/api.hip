@@ -83,11 +83,13 @@ int persist_grid(int per_cu) { return dr::device_cus() * per_cu; }
 // entries (padded elements); the last six are contiguous so the Bloom insert
 // can borrow them for its position buffer before the value path needs them.
 struct Carve {
-    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0, bnd = 0;
+    uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, fit_blocks = 0, btab = 0, bslices = 0, bnd = 0,
+             segslots = 0;
     bool query_only = false;  // descriptors, tile counts, the positives bitmap and the tile table only
     size_t bytes = 0;
     size_t o_td, o_glob, o_pstat, o_histA, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
-        o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs, o_bnd;
+        o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs, o_bnd,
+        o_segst, o_segpart;
 
     void plan() {
         size_t at = 0;
@@ -119,6 +121,8 @@ struct Carve {
         o_btab = take(all * 4 * btab);
         o_brow = take(all * 8 * bslices);
         o_bnd = take(all * 4 * bnd);
+        o_segst = take(all * sizeof(SegState) * segslots);
+        o_segpart = take(all * sizeof(SegPart) * SEG_GRID_BLOCKS * segslots);
         o_keyA = take(all * 4 * slots);
         o_keyB = take(all * 4 * slots);
         o_valA = take(all * 4 * slots);
@@ -166,6 +170,8 @@ struct Carve {
         w.vsorted = (float *)(ws + o_vs);
         w.bpos = (uint32_t *)(ws + o_keyA);  // borrows keyA .. vsorted
         w.bounds = (uint32_t *)(ws + o_bnd);
+        w.segst = (SegState *)(ws + o_segst);
+        w.segpart = (SegPart *)(ws + o_segpart);
         return w;
     }
 
@@ -188,6 +194,7 @@ Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     c.fit_blocks = (runs < d + n_tensors ? runs : d + n_tensors) * FIT_CHUNKS;
     // chord run starts: at most (runs + 1) per tensor
     c.bnd = std::min<uint64_t>(n_tensors * (uint64_t)(DR_MAX_SEGMENTS + 1), d + 2 * n_tensors);
+    c.segslots = n_tensors <= SEG_GRID_TENSORS ? n_tensors : 0;
     // Bloom table: per tensor (slices x chunks) with at most MAX_CHUNKS
     // chunks and at most ceil(m / 2^14) slices, where m <= 47 n + 32 (k <= 32
     // gives -ln(fpr) / (ln 2)^2 < 47 bits per item); plus one filter of
@@ -211,6 +218,8 @@ struct Plan {
     bool segment = false; // some tensor needs the segmentation pass (chord, or the heuristic count)
     bool dexp = false;    // some tensor fits double exponentials
     uint32_t dir_blocks = 0, dir_slices = 0;
+    uint32_t seg_grid_req = 0;  // most runs requested of a tensor segmented over the grid
+    bool seg_block_pass = false;  // some tensor needs the one-block segmentation pass
 };
 
 // Per-tensor Bloom insert layout for at most n_cap items and m_cap_bits:
@@ -405,11 +414,20 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         const uint64_t runs = runs_cap(d, degree, cfg->n_seg);
         in.fit_blk0 = (uint32_t)fit_blocks;
         fit_blocks += runs * FIT_CHUNKS;
+        in.seg_slot = NO_SEG_SLOT;
         if (cfg->segmentation == DR_SEG_CHORD) {
             in.bnd0 = (uint32_t)bnd;
             bnd += runs + 1;
+            // a requested run count of at most SEG_GRID_RUNS, for a few
+            // tensors: the splits are evaluated over the whole grid
+            if (T <= SEG_GRID_TENSORS && cfg->n_seg >= 1 && cfg->n_seg <= SEG_GRID_RUNS) {
+                in.seg_slot = (uint32_t)p.carve.segslots++;
+                p.seg_grid_req = std::max(p.seg_grid_req, cfg->n_seg);
+            }
         }
-        p.segment |= cfg->segmentation == DR_SEG_CHORD || cfg->n_seg == 0;
+        const bool seg = cfg->segmentation == DR_SEG_CHORD || cfg->n_seg == 0;
+        p.segment |= seg;
+        p.seg_block_pass |= seg && in.seg_slot == NO_SEG_SLOT;
         p.dexp |= cfg->fit_model == DR_FIT_DEXP;
         if (!nz) {
             in.hb0 = (uint32_t)hist_blocks;
@@ -437,7 +455,6 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     return DR_OK;
 }
 
-// descriptors (chunks of INIT_CHUNK tensors) and the per-call state cleared
 // Descriptors and the zeroed regions; a query-only work has no histogram or
 // sort regions, and `extra` (words) is a caller's buffer to clear as well.
 hipError_t run_init(const Work &w, const std::vector<TInit> &t, hipStream_t s, bool query_only = false,
@@ -523,7 +540,7 @@ dr_status encode_back(Encode &e, hipStream_t s) {
     const Plan &p = e.p;
     const Work &w = e.w;
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
-    if (p.segment) DR_HIP(launch_segment(w, s));
+    if (p.segment) DR_HIP(launch_segment(w, p.seg_grid_req, p.seg_block_pass, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
     DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;
@@ -765,6 +782,7 @@ Plan single_plan(uint64_t d) {
     p.t.resize(1);
     TInit &in = p.t[0];
     memset(&in, 0, sizeof in);
+    in.seg_slot = NO_SEG_SLOT;
     in.d = (uint32_t)d;
     in.ntiles = (uint32_t)(d ? ceil_div(d, TILE) : 1);
     in.tile0 = 0;

@@ -106,6 +106,30 @@ struct TInit {
     uint32_t seg_mode;   // SEG_EQUAL or SEG_CHORD (nseg == 0: the heuristic count)
     uint32_t fit_model;  // FIT_POLY or FIT_DEXP (then degree is 3: rows (a, b, c, d))
     uint32_t bnd0;       // chord segmentation: first segment-start entry of this tensor
+    uint32_t seg_slot;   // chord segmentation over the whole grid: the tensor's state, or NO_SEG_SLOT
+};
+
+// Chord segmentation over the whole grid (at most SEG_GRID_RUNS runs per
+// tensor, at most SEG_GRID_TENSORS such tensors): each step evaluates the
+// runs a split has just made, in parallel over SEG_GRID_BLOCKS blocks; the
+// last block to finish picks and makes the next split.
+constexpr uint32_t NO_SEG_SLOT = 0xFFFFFFFFu;
+constexpr uint32_t SEG_GRID_RUNS = 64;
+constexpr uint32_t SEG_GRID_TENSORS = 64;
+constexpr uint32_t SEG_GRID_BLOCKS = 256;
+struct SegState {
+    double cd[SEG_GRID_RUNS];  // each run's farthest allowed split distance (0: none)
+    uint32_t ci[SEG_GRID_RUNS];  // and the rank that ends its left part
+    uint32_t count;            // runs so far (their starts are in the tensor's bounds)
+    uint32_t req;              // runs requested
+    uint32_t done;             // no further split
+    uint32_t pend;             // first of the runs to evaluate (npend of them)
+    uint32_t npend;
+    uint32_t arrive;           // blocks done with this step
+};
+struct SegPart {               // one block's farthest point of each run evaluated
+    double d[2];
+    uint32_t i[2];
 };
 
 // Per-tensor descriptor, in device memory.
@@ -198,6 +222,8 @@ struct Work {
     uint32_t *brow;           // Bloom insert: per reserved slice, its count; brow + bslices: its start
     uint32_t bslices;         // Bloom insert: reserved slices over all tensors
     uint32_t *bounds;         // chord segmentation: segment starts (S_eff + 1 per tensor)
+    SegState *segst;          // chord segmentation over the grid: per state slot
+    SegPart *segpart;         // and SEG_GRID_BLOCKS partial results per slot
 };
 
 // ---------------------------------------------------------------------------

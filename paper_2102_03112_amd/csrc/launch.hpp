@@ -87,7 +87,7 @@ hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, ui
                          hipStream_t s);
 hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s);
 hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s);
-hipError_t launch_segment(const Work &w, hipStream_t s);
+hipError_t launch_segment(const Work &w, uint32_t grid_req, bool block_pass, hipStream_t s);
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s);
 hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s);
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,

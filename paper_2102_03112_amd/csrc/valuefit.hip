@@ -415,6 +415,288 @@ __device__ uint32_t seg_heuristic(const float *C, uint32_t n, uint32_t D) {
     return p + 1;
 }
 
+// The record's layout once the run count seff is known: the knots (chord
+// runs: the seff - 1 interior starts st[1..seff-1]) and the header fields
+// that follow from the count.  Block-wide, NT threads.
+template <uint32_t NT>
+__device__ void seg_finish(TDesc &td, uint32_t seff, bool chord, const uint32_t *st) {
+    const uint32_t deff = td.deff;
+    const uint32_t nkn = chord && seff > 1 ? seff - 1 : 0u;
+    if (td.in.rec) {
+        const uint32_t kn_off = td.coef_off + 4u * seff * (deff + 1u);
+        uint32_t *kn = (uint32_t *)(td.in.rec + kn_off);
+        for (uint32_t x = threadIdx.x; x < nkn; x += NT) kn[x] = st[x + 1];
+        if (threadIdx.x == 0) {
+            td.seff = seff;
+            td.sigma_off = kn_off + 4u * nkn;
+            td.rec_bytes = td.sigma_off + 4u * td.swords;
+            uint32_t *h = (uint32_t *)td.in.rec;
+            h[H_SEFF] = seff;
+            h[H_RECBYTES] = td.rec_bytes;
+        }
+    } else if (threadIdx.x == 0) {
+        td.seff = seff;
+    }
+}
+
+// values with the sign bit clear come first in the sorted order: their count
+__device__ __forceinline__ uint32_t sign_split(const float *C, uint32_t n) {
+    uint32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (!(__float_as_uint(C[mid]) >> 31))
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// Chord segmentation over the whole grid, for tensors with a state slot.
+// k_seg_init makes the sign split and marks the first runs for evaluation.
+// In each k_seg_step every block evaluates its share of the marked runs'
+// allowed split points (the runs' ranges laid end to end), and the last
+// block to finish a tensor reduces the blocks' results, picks the run to
+// split (farthest candidate, then the leftmost run), splits it after its
+// candidate and marks the two new runs.  The host launches one step per
+// split that may be needed; steps after the last split return at once.
+// The decisions are those of the one-block loop in k_segment: the same
+// distances, evaluated the same way, and the same tie rules.
+constexpr uint32_t SEGG_THREADS = 256;
+static_assert(SEG_GRID_BLOCKS <= SEGG_THREADS, "the last block reduces one result per thread");
+
+__global__ __launch_bounds__(SEGG_THREADS) void k_seg_init(Work w) {
+    __shared__ uint32_t st[3];
+    TDesc &td = w.td[blockIdx.x];
+    if (td.in.seg_slot == NO_SEG_SLOT) return;
+    SegState &ss = w.segst[td.in.seg_slot];
+    const uint32_t n = td.nv, D = td.in.degree, req = td.in.nseg;
+    const float *C = w.vsorted + td.in.slot;
+    // the sign split, by a 256-way search: the values with the sign bit
+    // clear are a prefix of the sorted order
+    uint32_t lo = 0, hi = n;  // the first value with the sign bit set is in [lo, hi]
+    while (hi - lo > SEGG_THREADS) {
+        const uint32_t x = lo + (uint32_t)((uint64_t)(hi - lo) * threadIdx.x / SEGG_THREADS);
+        const uint32_t c = (uint32_t)__syncthreads_count(!(__float_as_uint(C[x]) >> 31));
+        // the first c probes hold values with the sign bit clear
+        const uint32_t nlo = c == 0 ? lo : lo + (uint32_t)((uint64_t)(hi - lo) * (c - 1) / SEGG_THREADS) + 1u;
+        const uint32_t nhi = c == SEGG_THREADS ? hi : lo + (uint32_t)((uint64_t)(hi - lo) * c / SEGG_THREADS);
+        lo = nlo;
+        hi = c == 0 ? lo : nhi;
+    }
+    {
+        const uint32_t x = lo + threadIdx.x;
+        lo += (uint32_t)__syncthreads_count(x < hi && !(__float_as_uint(C[x]) >> 31));
+    }
+    uint32_t count = 0;
+    if (threadIdx.x == 0) {
+        st[0] = 0;
+        st[1] = n;
+        if (n > 0) {
+            count = 1;
+            if (req >= 2 && lo >= D + 1 && n - lo >= D + 1) {
+                st[1] = lo;
+                st[2] = n;
+                count = 2;
+            }
+        }
+        uint32_t *stw = w.bounds + td.in.bnd0;
+        for (uint32_t x = 0; x <= count && n > 0; ++x) stw[x] = st[x];
+        ss.count = count;
+        ss.req = req;
+        ss.done = n == 0 || count >= req;
+        ss.pend = 0;
+        ss.npend = count;
+        ss.arrive = 0;
+    }
+    count = __shfl(count, 0, 64);  // wave 0 holds it; the other waves are done
+    if (threadIdx.x < 64 && n > 0 && count >= req) seg_finish<64>(td, count, true, st);
+}
+
+// arg-max of (distance, rank) pairs over a wave: larger distance, then the
+// smaller rank
+__device__ __forceinline__ void argmax_wave(double *d, uint32_t *i) {
+    for (uint32_t off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_down(*d, off);
+        const uint32_t oi = __shfl_down(*i, off);
+        if (od > *d || (od == *d && oi < *i)) {
+            *d = od;
+            *i = oi;
+        }
+    }
+}
+
+__global__ __launch_bounds__(SEGG_THREADS) void k_seg_step(Work w) {
+    __shared__ double rd[2][SEGG_THREADS / 64];
+    __shared__ uint32_t ri[2][SEGG_THREADS / 64];
+    __shared__ uint32_t last, s_nc, s_done;
+    __shared__ uint32_t lst[SEG_GRID_RUNS + 1];
+    __shared__ double lcd[SEG_GRID_RUNS];
+    __shared__ uint32_t lci[SEG_GRID_RUNS];
+    const uint32_t G = gridDim.x, lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    for (uint32_t t = 0; t < w.ntensors; ++t) {
+        TDesc &td = w.td[t];
+        const uint32_t slot = td.in.seg_slot;
+        if (slot == NO_SEG_SLOT) continue;
+        SegState &ss = w.segst[slot];
+        if (ss.done) continue;
+        const uint32_t D = td.in.degree;
+        const float *C = w.vsorted + td.in.slot;
+        const uint32_t *st = w.bounds + td.in.bnd0;
+        const uint32_t p0 = ss.pend, np = ss.npend;
+        // run q: split points [a + D, z - D), z = e - 1, when it holds at
+        // least 2 (D + 1) points; its chord through (a, C[a]) and (z, C[z])
+        uint32_t a[2] = {0, 0}, L[2] = {0, 0};
+        double ca[2] = {0.0, 0.0}, m[2] = {0.0, 0.0};
+#pragma unroll
+        for (uint32_t q = 0; q < 2; ++q) {
+            if (q < np) {
+                const uint32_t aq = st[p0 + q], eq = st[p0 + q + 1];
+                if (eq - aq >= 2u * (D + 1u)) {
+                    const uint32_t z = eq - 1u;
+                    a[q] = aq;
+                    L[q] = (z - D) - (aq + D);
+                    ca[q] = (double)C[aq];
+                    m[q] = ((double)C[z] - ca[q]) / (double)(z - aq);
+                }
+            }
+        }
+        const uint32_t tot = L[0] + L[1];
+        const uint32_t c0 = (uint32_t)((uint64_t)tot * blockIdx.x / G);
+        const uint32_t c1 = (uint32_t)((uint64_t)tot * (blockIdx.x + 1) / G);
+        double best[2] = {0.0, 0.0};
+        uint32_t bi[2] = {0xffffffffu, 0xffffffffu};
+        // SEG_BATCH reads in flight per thread; a thread's points come in
+        // increasing rank, so a strict compare keeps the smallest rank
+        for (uint32_t xb = c0; xb < c1; xb += SEGG_THREADS * SEG_BATCH) {
+            float v[SEG_BATCH];
+#pragma unroll
+            for (uint32_t u = 0; u < SEG_BATCH; ++u) {
+                const uint32_t x = xb + u * SEGG_THREADS + threadIdx.x;
+                const uint32_t i = x < L[0] ? a[0] + D + x : a[1] + D + (x - L[0]);
+                v[u] = x < c1 ? C[i] : 0.0f;
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < SEG_BATCH; ++u) {
+                const uint32_t x = xb + u * SEGG_THREADS + threadIdx.x;
+                if (x < c1) {
+                    const uint32_t q = x < L[0] ? 0u : 1u;
+                    const uint32_t i = q ? a[1] + D + (x - L[0]) : a[0] + D + x;
+                    const double dd = chord_dist(ca[q], m[q], a[q], i, v[u]);
+                    if (dd > best[q]) {
+                        best[q] = dd;
+                        bi[q] = i;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (uint32_t q = 0; q < 2; ++q) {
+            argmax_wave(&best[q], &bi[q]);
+            if (lane == 0) {
+                rd[q][wv] = best[q];
+                ri[q][wv] = bi[q];
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            SegPart part;
+#pragma unroll
+            for (uint32_t q = 0; q < 2; ++q) {
+                double b = rd[q][0];
+                uint32_t k = ri[q][0];
+                for (uint32_t x = 1; x < SEGG_THREADS / 64; ++x)
+                    if (rd[q][x] > b || (rd[q][x] == b && ri[q][x] < k)) {
+                        b = rd[q][x];
+                        k = ri[q][x];
+                    }
+                part.d[q] = b;
+                part.i[q] = k;
+            }
+            w.segpart[(uint64_t)slot * SEG_GRID_BLOCKS + blockIdx.x] = part;
+            __threadfence();
+            last = atomicAdd(&ss.arrive, 1u) == G - 1u;
+        }
+        __syncthreads();
+        if (last) {
+            // the last block: every block's result, then the split, made on
+            // an LDS copy of the tensor's runs
+            __threadfence();
+#pragma unroll
+            for (uint32_t q = 0; q < 2; ++q) {
+                double b = 0.0;
+                uint32_t k = 0xffffffffu;
+                if (threadIdx.x < G) {
+                    const SegPart &pp = w.segpart[(uint64_t)slot * SEG_GRID_BLOCKS + threadIdx.x];
+                    b = pp.d[q];
+                    k = pp.i[q];
+                }
+                argmax_wave(&b, &k);
+                if (lane == 0) {
+                    rd[q][wv] = b;
+                    ri[q][wv] = k;
+                }
+            }
+            uint32_t *stw = w.bounds + td.in.bnd0;
+            const uint32_t count = ss.count;
+            for (uint32_t x = threadIdx.x; x <= count; x += SEGG_THREADS) lst[x] = stw[x];
+            for (uint32_t x = threadIdx.x; x < count; x += SEGG_THREADS) {
+                lcd[x] = ss.cd[x];
+                lci[x] = ss.ci[x];
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                for (uint32_t q = 0; q < np; ++q) {
+                    double b = rd[q][0];
+                    uint32_t k = ri[q][0];
+                    for (uint32_t x = 1; x < SEGG_THREADS / 64; ++x)
+                        if (rd[q][x] > b || (rd[q][x] == b && ri[q][x] < k)) {
+                            b = rd[q][x];
+                            k = ri[q][x];
+                        }
+                    lcd[p0 + q] = b;
+                    lci[p0 + q] = b > 0.0 ? k : 0u;
+                }
+                // the run to split: farthest candidate, then the leftmost run
+                double b = 0.0;
+                uint32_t k = 0xffffffffu;
+                for (uint32_t x = 0; x < count; ++x)
+                    if (lcd[x] > b) {
+                        b = lcd[x];
+                        k = x;
+                    }
+                uint32_t nc = count;
+                if (k != 0xffffffffu) {
+                    // a start after run k: runs k+1.. move one place right
+                    for (uint32_t x = count; x >= k + 1u; --x) lst[x + 1] = lst[x];
+                    for (uint32_t x = count - 1u; x >= k + 1u && x < count; --x) {
+                        lcd[x + 1] = lcd[x];
+                        lci[x + 1] = lci[x];
+                    }
+                    lst[k + 1] = lci[k] + 1u;
+                    nc = count + 1u;
+                }
+                s_nc = nc;
+                s_done = k == 0xffffffffu || nc >= ss.req;  // no split left, or enough runs
+                ss.count = nc;
+                ss.done = s_done;
+                ss.pend = k;
+                ss.npend = 2;
+                ss.arrive = 0;
+            }
+            __syncthreads();
+            const uint32_t nc = s_nc;
+            for (uint32_t x = threadIdx.x; x <= nc; x += SEGG_THREADS) stw[x] = lst[x];
+            for (uint32_t x = threadIdx.x; x < nc; x += SEGG_THREADS) {
+                ss.cd[x] = lcd[x];
+                ss.ci[x] = lci[x];
+            }
+            if (s_done) seg_finish<SEGG_THREADS>(td, nc, true, lst);
+        }
+        __syncthreads();  // rd, ri and last are reused for the next tensor
+    }
+}
+
 __global__ __launch_bounds__(SEG_THREADS) void k_segment(Work w) {
     TDesc &td = w.td[blockIdx.x];
     const bool chord = td.in.seg_mode == SEG_CHORD;
@@ -428,6 +710,7 @@ __global__ __launch_bounds__(SEG_THREADS) void k_segment(Work w) {
     __shared__ uint32_t sh_req, sh_count, sh_pick;
     const uint32_t D = td.in.degree;
     const float *C = w.vsorted + td.in.slot;
+    if (td.in.seg_slot != NO_SEG_SLOT) return;  // segmented over the grid, layout written
     if (threadIdx.x == 0) {
         const uint32_t req = td.in.nseg ? td.in.nseg : seg_heuristic(C, n, D);
         sh_req = req;
@@ -435,15 +718,7 @@ __global__ __launch_bounds__(SEG_THREADS) void k_segment(Work w) {
         st[0] = 0;
         st[1] = n;
         if (chord) {
-            // values with the sign bit clear come first in the sorted order
-            uint32_t lo = 0, hi = n;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if (!(__float_as_uint(C[mid]) >> 31))
-                    lo = mid + 1;
-                else
-                    hi = mid;
-            }
+            const uint32_t lo = sign_split(C, n);
             if (req >= 2 && lo >= D + 1 && n - lo >= D + 1) {
                 st[1] = lo;
                 st[2] = n;
@@ -541,29 +816,24 @@ __global__ __launch_bounds__(SEG_THREADS) void k_segment(Work w) {
         }
     }
     // the record's layout now that the run count is known
-    const uint32_t deff = td.deff;
     const uint32_t seff = chord ? count : (req < max(1u, n / (D + 1u)) ? req : max(1u, n / (D + 1u)));
-    const uint32_t nkn = chord && seff > 1 ? seff - 1 : 0u;
     if (chord)
         for (uint32_t x = threadIdx.x; x <= seff; x += SEG_THREADS) w.bounds[td.in.bnd0 + x] = st[x];
-    if (td.in.rec) {
-        const uint32_t kn_off = td.coef_off + 4u * seff * (deff + 1u);
-        uint32_t *kn = (uint32_t *)(td.in.rec + kn_off);
-        for (uint32_t x = threadIdx.x; x < nkn; x += SEG_THREADS) kn[x] = st[x + 1];
-        if (threadIdx.x == 0) {
-            td.seff = seff;
-            td.sigma_off = kn_off + 4u * nkn;
-            td.rec_bytes = td.sigma_off + 4u * td.swords;
-            uint32_t *h = (uint32_t *)td.in.rec;
-            h[H_SEFF] = seff;
-            h[H_RECBYTES] = td.rec_bytes;
-        }
-    } else if (threadIdx.x == 0) {
-        td.seff = seff;
-    }
+    seg_finish<SEG_THREADS>(td, seff, chord, st);
 }
 
-hipError_t launch_segment(const Work &w, hipStream_t s) {
+// grid_req: the most runs requested of a tensor with a state slot (0: none);
+// block_pass: some tensor has no state slot and is segmented by k_segment
+hipError_t launch_segment(const Work &w, uint32_t grid_req, bool block_pass, hipStream_t s) {
+    if (grid_req > 0) {
+        k_seg_init<<<w.ntensors, SEGG_THREADS, 0, s>>>(w);
+        trace_mark(s, "k_seg_init");
+        for (uint32_t q = 1; q < grid_req; ++q) {
+            k_seg_step<<<SEG_GRID_BLOCKS, SEGG_THREADS, 0, s>>>(w);
+            trace_mark(s, "k_seg_step");
+        }
+    }
+    if (!block_pass) return hipGetLastError();
     k_segment<<<w.ntensors, SEG_THREADS, 0, s>>>(w);
     trace_mark(s, "k_segment");
     return hipGetLastError();

@@ -292,6 +292,11 @@ SEG_CASES = {
                              oracle.SEG_CHORD),
     "many_runs_chord": (W.normal(400_000, 22, scale=1e-3), [0, 400_000], (1, 10), 1e-3, 1, 3000,
                         oracle.SEG_CHORD),
+    # splits evaluated over the whole grid: 600 k values in 16 runs, and 37
+    # tensors at once
+    "support_chord16_1m": (W.sparse_normal(1_000_000, 13, 0.4), [0, 1_000_000], None, 1e-4, 3, 16,
+                           oracle.SEG_CHORD),
+    "many_tensors_chord8": (W.normal(_MANY[-1], 12), _MANY, (1, 100), 1e-3, 5, 8, oracle.SEG_CHORD),
 }
 
 
