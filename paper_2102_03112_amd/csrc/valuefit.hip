@@ -842,6 +842,24 @@ hipError_t launch_segment(const Work &w, uint32_t grid_req, bool block_pass, hip
 // ---------------------------------------------------------------------------
 // Least-squares fit of each run
 // ---------------------------------------------------------------------------
+// The double-exponential fit's state per run, after DEXP_PARTS x 15 partial
+// sums in the run's share of the fit partials (FIT_CHUNKS x NMOM doubles,
+// free once the polynomial fit has read them).
+constexpr uint32_t DEXP_PARTS = 8;  // blocks per run and pass
+struct DexpState {
+    double th[4];    // current point (a, b, c, d)
+    double tt[4];    // trial point
+    double cur[15];  // sums at the current point
+    double lambda;
+    int it;          // steps taken
+    uint32_t done;   // the fit has ended and the row is written
+    uint32_t arrive; // blocks done with this pass
+    uint32_t pad;
+};
+static_assert(DEXP_PARTS * 15 * 8 + sizeof(DexpState) <= FIT_CHUNKS * NMOM * 8, "state fits in the run's partials");
+__device__ __forceinline__ DexpState *dexp_state(const Work &w, uint32_t run) {
+    return (DexpState *)(w.fit_part + (uint64_t)run * FIT_CHUNKS * NMOM + DEXP_PARTS * 15);
+}
 // sorted ranks [lo, hi) of run s
 __device__ __forceinline__ void run_range(const Work &w, const TDesc &td, uint32_t s, uint64_t *lo, uint64_t *hi) {
     if (td.in.seg_mode == SEG_CHORD) {
@@ -966,7 +984,11 @@ __global__ __launch_bounds__(64) void k_fit_solve(Work w) {
             td.in.coef[(uint64_t)s * td.in.coef_stride + threadIdx.x] = 0.0f;
         return;
     }
-    if (td.model == FIT_DEXP) return;  // fitted by k_fit_dexp
+    if (td.model == FIT_DEXP) {  // fitted by k_dexp_pass: its state starts cleared
+        if (threadIdx.x < sizeof(DexpState) / 4)
+            ((uint32_t *)dexp_state(w, blockIdx.x))[threadIdx.x] = 0u;
+        return;
+    }
     __shared__ double mom[NMOM];
     if (threadIdx.x < NMOM) {
         const double *part = w.fit_part + (uint64_t)blk * NMOM;
@@ -1056,19 +1078,23 @@ __device__ void solve_run(const TDesc &td, uint32_t s, const double *mom) {
 }
 
 // ---------------------------------------------------------------------------
-// Double-exponential fit (Section 5, "Nonlinear regression"): one block per
-// run, Levenberg-Marquardt on y ~ a e^(bt) + c e^(dt) with the same steps as
-// the oracle (start at rates (1, -1) with the amplitudes of the linear
-// problem; DEXP_ITERS steps, rates clamped to [-40, 40], lambda from 1e-3,
-// x10 on a reject, /10 on an accept).  Each step is one pass over the run:
-// the 15 sums of J^T J, J^T r and r^T r at the trial point, reduced over
-// the block in a fixed order; every thread then takes the same decision and
-// solves the same 4 x 4 system.  A thread takes a contiguous range of
-// points: the abscissae are equally spaced, so e^(b t) advances by one
-// multiplication per point from one exp() at the range's start (relative
-// drift ~1e-15 over a range, far below the fit's tolerance).
+// Double-exponential fit (Section 5, "Nonlinear regression"):
+// Levenberg-Marquardt on y ~ a e^(bt) + c e^(dt) with the same steps as the
+// oracle (start at rates (1, -1) with the amplitudes of the linear problem;
+// DEXP_ITERS steps, rates clamped to [-40, 40], lambda from 1e-3, x10 on a
+// reject, /10 on an accept).  Each step is one pass over the run: the 15
+// sums of J^T J, J^T r and r^T r at the trial point.  A pass is one launch
+// of k_dexp_pass, with DEXP_PARTS blocks per run; each block sums its part
+// of the run and the last block to finish (a counter) adds the parts in a
+// fixed order, takes the step's decision and solves the 4 x 4 system for
+// the next trial point.  The solver's state stays in the run's share of
+// the fit partials, which the polynomial fit no longer needs.  A thread
+// takes a contiguous range of points: the abscissae are equally spaced, so
+// e^(b t) advances by one multiplication per point from one exp() at the
+// range's start (relative drift ~1e-15 over a range, far below the fit's
+// tolerance).
 // ---------------------------------------------------------------------------
-constexpr uint32_t DEXP_THREADS = 512;
+constexpr uint32_t DEXP_THREADS = 256;
 constexpr int DEXP_ITERS = 40;
 constexpr uint32_t DEXP_BATCH = 8;
 constexpr double DEXP_RATE_MAX = 40.0;
@@ -1135,30 +1161,20 @@ __device__ __forceinline__ bool solve4(double A[4][5], double *x) {
     return true;
 }
 
-__global__ __launch_bounds__(DEXP_THREADS) void k_fit_dexp(Work w) {
-    const uint32_t blk = blockIdx.x * FIT_CHUNKS;
-    const uint32_t t = tensor_of_fit_block(w, blk);
-    const TDesc &td = w.td[t];
-    const uint32_t s = (blk - td.in.fit_blk0) / FIT_CHUNKS;
-    if (td.model != FIT_DEXP || s >= td.seff) return;
-    __shared__ double red[DEXP_THREADS / 64][15];
-    __shared__ double tot[15];
-    // the solver's state lives in LDS and only thread 0 changes it, which
-    // keeps the per-thread registers to one pass's sums
-    __shared__ double th_s[4], tt_s[4], cur_s[15], lambda_s;
-    __shared__ int it_s, go_s;
-    uint64_t lo, hi;
-    run_range(w, td, s, &lo, &hi);
-    const uint64_t ns = hi - lo;
-    const float *y = w.vsorted + td.in.slot + lo;
+// one pass over block `part`'s share of run [lo, lo + ns) at (a, b, c, dd):
+// init: the 6 sums of the linear start; else the 15 sums of the step
+__device__ void dexp_part_sums(const float *y, uint64_t ns, uint32_t part, bool init, const double th[4],
+                               double (*red)[15], double *tot) {
     const double inv = ns > 1 ? 1.0 / (double)(ns - 1) : 0.0;
     const double off = (double)(ns - 1);
-    const uint64_t per = (ns + DEXP_THREADS - 1) / DEXP_THREADS;
-    const uint64_t j0 = min(ns, threadIdx.x * per), j1 = min(ns, j0 + per);
     const double step = 2.0 * inv;
-    // start: rates (1, -1), amplitudes from the 2 x 2 linear problem
-    {
-        double v[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+    const uint64_t b0 = ns * part / DEXP_PARTS, b1 = ns * (part + 1) / DEXP_PARTS;
+    const uint64_t per = (b1 - b0 + DEXP_THREADS - 1) / DEXP_THREADS;
+    const uint64_t j0 = min(b1, b0 + threadIdx.x * per), j1 = min(b1, j0 + per);
+    double v[15];
+#pragma unroll
+    for (int e = 0; e < 15; ++e) v[e] = 0.0;
+    if (init) {
         if (j0 < j1) {
             const double t0 = ((double)(2 * j0) - off) * inv;
             double e1 = exp(t0), e2 = exp(-t0);
@@ -1183,105 +1199,163 @@ __global__ __launch_bounds__(DEXP_THREADS) void k_fit_dexp(Work w) {
             }
         }
         block_sums<6>(v, red, tot);
-        if (threadIdx.x == 0) {
-            const double det = tot[0] * tot[2] - tot[1] * tot[1];
-            th_s[1] = 1.0;
-            th_s[3] = -1.0;
-            if (det != 0.0) {
-                th_s[0] = (tot[3] * tot[2] - tot[4] * tot[1]) / det;
-                th_s[2] = (tot[4] * tot[0] - tot[3] * tot[1]) / det;
-            } else {
-                th_s[0] = tot[5] / (double)ns;
-                th_s[2] = 0.0;
-            }
-            for (int p = 0; p < 4; ++p) tt_s[p] = th_s[p];
-            lambda_s = 1e-3;
-            it_s = 0;
-        }
-        __syncthreads();
+        return;
     }
-    for (bool first = true;; first = false) {
-        // one pass at the trial point tt_s
-        const double a = tt_s[0], b = tt_s[1], c = tt_s[2], dd = tt_s[3];
-        double v[15];
+    const double a = th[0], b = th[1], c = th[2], dd = th[3];
+    if (j0 < j1) {
+        const double t0 = ((double)(2 * j0) - off) * inv;
+        double eb = exp(b * t0), ed = exp(dd * t0);
+        const double rb = exp(b * step), rd = exp(dd * step);
+        for (uint64_t jb = j0; jb < j1; jb += DEXP_BATCH) {
+            float yv[DEXP_BATCH];
 #pragma unroll
-        for (int e = 0; e < 15; ++e) v[e] = 0.0;
-        if (j0 < j1) {
-            const double t0 = ((double)(2 * j0) - off) * inv;
-            double eb = exp(b * t0), ed = exp(dd * t0);
-            const double rb = exp(b * step), rd = exp(dd * step);
-            for (uint64_t jb = j0; jb < j1; jb += DEXP_BATCH) {
-                float yv[DEXP_BATCH];
+            for (uint32_t u = 0; u < DEXP_BATCH; ++u) yv[u] = jb + u < j1 ? y[jb + u] : 0.0f;
 #pragma unroll
-                for (uint32_t u = 0; u < DEXP_BATCH; ++u) yv[u] = jb + u < j1 ? y[jb + u] : 0.0f;
-#pragma unroll
-                for (uint32_t u = 0; u < DEXP_BATCH; ++u) {
-                    const uint64_t j = jb + u;
-                    if (j >= j1) break;
-                    const double tj = ((double)(2 * j) - off) * inv, yj = (double)yv[u];
-                    const double J[4] = {eb, a * tj * eb, ed, c * tj * ed};
-                    const double r = yj - (a * eb + c * ed);
-                    int e = 0;
-#pragma unroll
-                    for (int p = 0; p < 4; ++p)
-#pragma unroll
-                        for (int q = p; q < 4; ++q) v[e++] += J[p] * J[q];
-#pragma unroll
-                    for (int p = 0; p < 4; ++p) v[10 + p] += J[p] * r;
-                    v[14] += r * r;
-                    eb *= rb;
-                    ed *= rd;
-                }
-            }
-        }
-        block_sums<15>(v, red, tot);
-        if (threadIdx.x == 0) {
-            if (first) {
-                for (int e = 0; e < 15; ++e) cur_s[e] = tot[e];
-            } else if (tot[14] < cur_s[14]) {
-                for (int p = 0; p < 4; ++p) th_s[p] = tt_s[p];
-                for (int e = 0; e < 15; ++e) cur_s[e] = tot[e];
-                lambda_s /= 10.0;
-            } else {
-                lambda_s *= 10.0;
-            }
-            // the next trial point; a singular system uses up a step
-            int go = 0;
-            while (it_s < DEXP_ITERS) {
-                ++it_s;
-                double A[4][5];
+            for (uint32_t u = 0; u < DEXP_BATCH; ++u) {
+                const uint64_t j = jb + u;
+                if (j >= j1) break;
+                const double tj = ((double)(2 * j) - off) * inv, yj = (double)yv[u];
+                const double J[4] = {eb, a * tj * eb, ed, c * tj * ed};
+                const double r = yj - (a * eb + c * ed);
                 int e = 0;
+#pragma unroll
                 for (int p = 0; p < 4; ++p)
-                    for (int q = p; q < 4; ++q) {
-                        A[p][q] = cur_s[e];
-                        A[q][p] = cur_s[e];
-                        ++e;
-                    }
-                for (int p = 0; p < 4; ++p) {
-                    A[p][p] += lambda_s * A[p][p];
-                    A[p][4] = cur_s[10 + p];
-                }
-                double delta[4];
-                if (!solve4(A, delta)) {
-                    lambda_s *= 10.0;
-                    continue;
-                }
-                for (int p = 0; p < 4; ++p) tt_s[p] = th_s[p] + delta[p];
-                for (int p = 1; p < 4; p += 2)
-                    tt_s[p] = tt_s[p] > DEXP_RATE_MAX ? DEXP_RATE_MAX
-                                                      : (tt_s[p] < -DEXP_RATE_MAX ? -DEXP_RATE_MAX : tt_s[p]);
-                go = 1;
-                break;
+#pragma unroll
+                    for (int q = p; q < 4; ++q) v[e++] += J[p] * J[q];
+#pragma unroll
+                for (int p = 0; p < 4; ++p) v[10 + p] += J[p] * r;
+                v[14] += r * r;
+                eb *= rb;
+                ed *= rd;
             }
-            go_s = go;
         }
-        __syncthreads();
-        if (!go_s) break;
     }
-    if (threadIdx.x < 4) {
+    block_sums<15>(v, red, tot);
+}
+
+// Pass `pass` of every double-exponential run: 0 sums the linear start,
+// 1 evaluates the start, each later pass a trial point.  Launched
+// 2 + DEXP_ITERS times; a run whose fit has ended returns at once.
+__global__ __launch_bounds__(DEXP_THREADS) void k_dexp_pass(Work w, uint32_t pass) {
+    const uint32_t run = blockIdx.x / DEXP_PARTS, part = blockIdx.x % DEXP_PARTS;
+    const uint32_t blk = run * FIT_CHUNKS;
+    const uint32_t t = tensor_of_fit_block(w, blk);
+    const TDesc &td = w.td[t];
+    const uint32_t s = (blk - td.in.fit_blk0) / FIT_CHUNKS;
+    if (td.model != FIT_DEXP || s >= td.seff) return;
+    DexpState &st = *dexp_state(w, run);
+    if (st.done) return;
+    __shared__ double red[DEXP_THREADS / 64][15];
+    __shared__ double tot[15];
+    __shared__ uint32_t last;
+    uint64_t lo, hi;
+    run_range(w, td, s, &lo, &hi);
+    const uint64_t ns = hi - lo;
+    const float *y = w.vsorted + td.in.slot + lo;
+    double th[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) th[p] = st.tt[p];
+    dexp_part_sums(y, ns, part, pass == 0, th, red, tot);
+    double *parts = w.fit_part + (uint64_t)blk * NMOM;  // DEXP_PARTS x 15 sums
+    if (threadIdx.x < 15) parts[part * 15 + threadIdx.x] = tot[threadIdx.x];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        last = atomicAdd(&st.arrive, 1u) == DEXP_PARTS - 1u;
+    }
+    __syncthreads();
+    if (!last) return;
+    // the last block: the run's sums (parts in order) and the solver's state
+    // into LDS, read in parallel; then thread 0 takes the step's decision
+    __threadfence();
+    __shared__ double sum[15], cur[15], sth[4], stt[4], slam;
+    __shared__ int sit;
+    if (threadIdx.x < 15) {
+        double acc = 0.0;
+        for (uint32_t q = 0; q < DEXP_PARTS; ++q) acc += parts[q * 15 + threadIdx.x];
+        sum[threadIdx.x] = acc;
+        cur[threadIdx.x] = st.cur[threadIdx.x];
+    } else if (threadIdx.x < 19) {
+        sth[threadIdx.x - 15] = st.th[threadIdx.x - 15];
+        stt[threadIdx.x - 15] = st.tt[threadIdx.x - 15];
+    } else if (threadIdx.x == 19) {
+        slam = st.lambda;
+        sit = st.it;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    st.arrive = 0;
+    if (pass == 0) {
+        // start: rates (1, -1), amplitudes from the 2 x 2 linear problem
+        const double det = sum[0] * sum[2] - sum[1] * sum[1];
+        double th0, th2;
+        if (det != 0.0) {
+            th0 = (sum[3] * sum[2] - sum[4] * sum[1]) / det;
+            th2 = (sum[4] * sum[0] - sum[3] * sum[1]) / det;
+        } else {
+            th0 = sum[5] / (double)ns;
+            th2 = 0.0;
+        }
+        const double th4[4] = {th0, 1.0, th2, -1.0};
+        for (int p = 0; p < 4; ++p) {
+            st.th[p] = th4[p];
+            st.tt[p] = th4[p];
+        }
+        st.lambda = 1e-3;
+        st.it = 0;
+        return;
+    }
+    double lambda = slam;
+    if (pass == 1) {
+        for (int e = 0; e < 15; ++e) cur[e] = sum[e];
+    } else if (sum[14] < cur[14]) {
+        for (int p = 0; p < 4; ++p) sth[p] = stt[p];
+        for (int e = 0; e < 15; ++e) cur[e] = sum[e];
+        lambda /= 10.0;
+    } else {
+        lambda *= 10.0;
+    }
+    // the next trial point; a singular system uses up a step
+    int it = sit;
+    bool go = false;
+    while (it < DEXP_ITERS) {
+        ++it;
+        double A[4][5];
+        int e = 0;
+        for (int p = 0; p < 4; ++p)
+            for (int q = p; q < 4; ++q) {
+                A[p][q] = cur[e];
+                A[q][p] = cur[e];
+                ++e;
+            }
+        for (int p = 0; p < 4; ++p) {
+            A[p][p] += lambda * A[p][p];
+            A[p][4] = cur[10 + p];
+        }
+        double delta[4];
+        if (!solve4(A, delta)) {
+            lambda *= 10.0;
+            continue;
+        }
+        for (int p = 0; p < 4; ++p) stt[p] = sth[p] + delta[p];
+        for (int p = 1; p < 4; p += 2)
+            stt[p] = stt[p] > DEXP_RATE_MAX ? DEXP_RATE_MAX : (stt[p] < -DEXP_RATE_MAX ? -DEXP_RATE_MAX : stt[p]);
+        go = true;
+        break;
+    }
+    for (int p = 0; p < 4; ++p) {
+        st.th[p] = sth[p];
+        st.tt[p] = stt[p];
+    }
+    for (int e = 0; e < 15; ++e) st.cur[e] = cur[e];
+    st.lambda = lambda;
+    st.it = it;
+    if (!go) {
+        // the fit has ended: the run's row
+        st.done = 1;
         float *row = td.in.coef ? td.in.coef + (uint64_t)s * td.in.coef_stride
                                 : (float *)(td.in.rec + td.coef_off) + (uint64_t)s * 4u;
-        row[threadIdx.x] = (float)th_s[threadIdx.x];
+        for (int p = 0; p < 4; ++p) row[p] = (float)sth[p];
     }
 }
 
@@ -1292,8 +1366,10 @@ hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t
     k_fit_solve<<<fit_blocks / FIT_CHUNKS, 64, 0, s>>>(w);
     trace_mark(s, "k_fit_solve");
     if (dexp) {
-        k_fit_dexp<<<fit_blocks / FIT_CHUNKS, DEXP_THREADS, 0, s>>>(w);
-        trace_mark(s, "k_fit_dexp");
+        for (uint32_t pass = 0; pass < 2u + (uint32_t)DEXP_ITERS; ++pass) {
+            k_dexp_pass<<<(fit_blocks / FIT_CHUNKS) * DEXP_PARTS, DEXP_THREADS, 0, s>>>(w, pass);
+            trace_mark(s, "k_dexp_pass");
+        }
     }
     return hipGetLastError();
 }
