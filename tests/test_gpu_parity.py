@@ -233,6 +233,9 @@ RT_CASES = {
     "support_50k": (W.sparse_normal(50_000, 7, 0.4), [0, 50_000], None, 1e-4, 3, 16),
     # a filter planned for 1 M items: the bucketed insert, in three rounds
     "support_1m": (W.sparse_normal(1_000_000, 13, 0.4), [0, 1_000_000], None, 1e-4, 3, 16),
+    # three such tensors: the bucketed insert over several tensors' slices
+    # and chunks
+    "support_3x500k": (W.sparse_normal(1_500_001, 14, 0.4), [0, 500_000, 1_000_000, 1_500_001], None, 1e-4, 3, 8),
     # empty, 1-, 5-, 4096-, 4097-element, empty and 4-element tensors
     "ragged_tensors": (W.normal(8203, 8), [0, 0, 1, 6, 4102, 8199, 8199, 8203], (1, 2), 1e-3, 5, 8),
     "take_all": (W.normal(5000, 9), [0, 5000], (1, 1), 1e-3, 2, 4),
@@ -297,6 +300,9 @@ SEG_CASES = {
     "support_chord16_1m": (W.sparse_normal(1_000_000, 13, 0.4), [0, 1_000_000], None, 1e-4, 3, 16,
                            oracle.SEG_CHORD),
     "many_tensors_chord8": (W.normal(_MANY[-1], 12), _MANY, (1, 100), 1e-3, 5, 8, oracle.SEG_CHORD),
+    # two and one runs: the sign split alone, and no split at all
+    "resnet20_chord2": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 2, oracle.SEG_CHORD),
+    "resnet20_chord1": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-3, 5, 1, oracle.SEG_CHORD),
 }
 
 
@@ -310,7 +316,7 @@ def test_roundtrip_segmentation_parity(name):
     out = run_roundtrip(g, cfg)
     refs = oracle.roundtrip(g, off, ratio, fpr, D, S, seg_mode=seg)
     check_roundtrip(g, cfg, out, refs)
-    if seg == oracle.SEG_CHORD:
+    if seg == oracle.SEG_CHORD and S != 1:
         assert any(r.fit.S_eff > 1 for r in refs)
 
 
