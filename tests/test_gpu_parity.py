@@ -233,6 +233,8 @@ RT_CASES = {
     "support_50k": (W.sparse_normal(50_000, 7, 0.4), [0, 50_000], None, 1e-4, 3, 16),
     # a filter planned for 1 M items: the bucketed insert, in three rounds
     "support_1m": (W.sparse_normal(1_000_000, 13, 0.4), [0, 1_000_000], None, 1e-4, 3, 16),
+    # 1.5 M values: 366 sort tiles in each pass's look-back
+    "support_2500k": (W.sparse_normal(2_500_000, 15, 0.4), [0, 2_500_000], None, 1e-4, 3, 16),
     # three such tensors: the bucketed insert over several tensors' slices
     # and chunks
     "support_3x500k": (W.sparse_normal(1_500_001, 14, 0.4), [0, 500_000, 1_000_000, 1_500_001], None, 1e-4, 3, 8),
