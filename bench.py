@@ -178,6 +178,8 @@ def main():
                     help="instead: time the summing receiver over N payloads of the workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=30.0, help="bound on the oracle's CPU time")
+    ap.add_argument("--cpu-min-s", type=float, default=10.0,
+                    help="the oracle's sample is repeated until it has run this long (at most 8 times)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (the reference kernel for HBM counter scaling)")
     args = ap.parse_args()
@@ -297,13 +299,18 @@ def main():
         elems = min(d, int(args.cpu_budget_s * 2.5e6))
         off = [o for o in w.offsets() if o < elems] + [elems]
         t0 = time.perf_counter()
-        oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, cfg.n_seg, policy=args.policy,
-                         seed=args.policy_seed, seg_mode=args.segmentation, model=args.fit_model)
-        tc = time.perf_counter() - t0
+        reps = 0
+        while True:
+            oracle.roundtrip(g_host[:elems], off, w.ratio, w.fpr, w.degree, cfg.n_seg, policy=args.policy,
+                             seed=args.policy_seed, seg_mode=args.segmentation, model=args.fit_model)
+            reps += 1
+            tc = time.perf_counter() - t0
+            if tc >= args.cpu_min_s or reps >= 8:
+                break
         sample = "full workload" if elems == d else f"first {elems} elements ({len(off) - 1} tensors) of the workload"
-        cpu = {"value": round(elems / tc / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
-               "sample": f"{sample}, 1 round trip, {tc:.2f} s", "cpu": _cpu_model()}
-        log(f"bench: oracle {elems} elements in {tc:.2f}s")
+        cpu = {"value": round(elems * reps / tc / 1e9, 6), "unit": "Gelem/s", "cores": 1, "kind": "oracle",
+               "sample": f"{sample}, {reps} round trip{'s' if reps > 1 else ''}, {tc:.2f} s", "cpu": _cpu_model()}
+        log(f"bench: oracle {elems} elements x {reps} in {tc:.2f}s")
 
     out = {
         "metric": METRIC,
