@@ -34,6 +34,9 @@ SEG_EQUAL, SEG_CHORD = 0, 1
 MAX_SEG = 4096
 # value models (Section 5): polynomial, double exponential
 FIT_POLY, FIT_DEXP = 0, 1
+# where the sender takes the coded values (Section 4): the dense gradient g,
+# or the sparsified gradient (g on the selection, 0 elsewhere)
+VALUES_DENSE, VALUES_SPARSE = 0, 1
 
 
 class OracleError(RuntimeError):
@@ -398,6 +401,7 @@ class TensorResult:
     policy: int = 0
     seed: int = 0
     slots: np.ndarray | None = field(default=None)  # value number of each positive rank, or NO_SLOT
+    value_source: int = VALUES_DENSE
 
     def payload_bits(self) -> dict:
         """Bits that cross the network (Figure 3's container): the filter, the
@@ -412,10 +416,13 @@ class TensorResult:
 
 def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
                      policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL,
-                     model: int = FIT_POLY) -> TensorResult:
+                     model: int = FIT_POLY, value_source: int = VALUES_DENSE) -> TensorResult:
     """Sender: top-r (or support) -> Bloom insert -> full-range query (P) ->
-    the policy keeps all of P (P0) or r of it -> V = g at the kept positives
-    (values from the dense gradient, Section 4) -> curve-fit encode.
+    the policy keeps all of P (P0) or r of it -> V = the gradient at the kept
+    positives -> curve-fit encode.  Section 4 defines P0's values on the
+    sparsified gradient g~ (g on S, 0 elsewhere), so a false positive carries
+    0 (``value_source=VALUES_SPARSE``); it also allows reading them from the
+    dense g when the sparsifier leaves it accessible (``VALUES_DENSE``).
     Receiver: the same query from the filter words -> the same policy ->
     curve-fit decode -> scatter into a dense gradient that is zero elsewhere
     (Section 4's reconstruction).  ``r`` is an int or R_NONZERO."""
@@ -427,8 +434,15 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     P = bloom_query(bits, m, k, d)
     slots, ncoded = policy_slots(P.size, S.size, policy, seed)
     kept = slots != NO_SLOT
+    if value_source == VALUES_SPARSE:
+        g_src = np.zeros(d, dtype=np.float32)  # g~: g on the selection, +0 elsewhere
+        g_src[S.astype(np.int64)] = g[S.astype(np.int64)]
+    elif value_source == VALUES_DENSE:
+        g_src = g
+    else:
+        raise OracleError(f"unknown value source {value_source}")
     V = np.zeros(ncoded, dtype=np.float32)
-    V[slots[kept].astype(np.int64)] = g[P[kept].astype(np.int64)]
+    V[slots[kept].astype(np.int64)] = g_src[P[kept].astype(np.int64)]
     fit = curvefit_encode(V, degree, n_seg, seg_mode, model)
     # receiver: its own query and the same policy over its own positives
     P_dec = bloom_query(bits, m, k, d)
@@ -441,11 +455,12 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     if want_dense:
         dense = np.zeros(d, dtype=np.float32)
         dense[P_dec.astype(np.int64)] = vals
-    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense, policy, seed, slots)
+    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense, policy, seed, slots, value_source)
 
 
 def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
-              policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL, model: int = FIT_POLY):
+              policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL, model: int = FIT_POLY,
+              value_source: int = VALUES_DENSE):
     """Code every tensor g[offsets[t]:offsets[t+1]] independently on local
     indices.  ``ratio`` is (num, den) for top-r with r = ceil(d_t num / den),
     or None for the support of an inherently sparse gradient."""
@@ -453,7 +468,8 @@ def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int
     for t in range(len(offsets) - 1):
         gt = g[offsets[t]: offsets[t + 1]]
         r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
-        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed, seg_mode, model))
+        out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed, seg_mode, model,
+                                    value_source))
     return out
 
 

@@ -96,3 +96,49 @@ def test_empty_and_degenerate_tensors():
     g = workloads.normal(10, seed=2)
     (res,) = oracle.roundtrip(g, [0, 10], (1, 1), 1e-3, 5, 8)  # r = d
     np.testing.assert_array_equal(res.P, np.arange(10, dtype=np.uint32))
+
+
+def _topr_mask_numpy(g, r):
+    """The r largest |g|, ties to the smaller index, by numpy's lexsort."""
+    key = np.abs(g.astype(np.float64))
+    order = np.lexsort((np.arange(g.size), -key))[:r]
+    mask = np.zeros(g.size, bool)
+    mask[order] = True
+    return mask
+
+
+@pytest.mark.parametrize("source", [oracle.VALUES_DENSE, oracle.VALUES_SPARSE])
+def test_value_source_interpolating_round_trip(source):
+    """Section 4 codes P0's values from the sparsified gradient g~ (g on the
+    top-r set, 0 elsewhere), or from the dense g when the sparsifier leaves it
+    accessible.  With one value per run (degree 0 and as many runs as
+    values) every run is interpolated, so the decoded gradient is exactly
+    what was sent: g~ itself for the sparse source, g on all of P for the
+    dense one.  A false-positive rate of 0.05 leaves ~150 false positives, so
+    the two differ."""
+    g = workloads.normal(3000, seed=31, scale=1.0)
+    r = 60
+    (res,) = oracle.roundtrip(g, [0, g.size], (1, 50), 0.05, 0, oracle.MAX_SEG, value_source=source)
+    assert res.S.size == r and res.P.size > r + 50
+    assert res.fit.S_eff == res.P.size and res.fit.D_eff == 0
+    mask = _topr_mask_numpy(g, r)
+    if source == oracle.VALUES_SPARSE:
+        expect = np.where(mask, g, np.float32(0))
+        assert np.count_nonzero(res.V == 0) == res.P.size - r
+    else:
+        onP = np.zeros(g.size, bool)
+        onP[res.P.astype(np.int64)] = True
+        assert onP[mask].all()
+        expect = np.where(onP, g, np.float32(0))
+        assert np.count_nonzero(res.V == 0) == 0
+    np.testing.assert_array_equal(res.dense, expect)
+
+
+def test_value_source_sparse_equals_dense_on_support():
+    """The support of an inherently sparse gradient selects every nonzero, so
+    g~ = g and both sources code the same values."""
+    g = workloads.sparse_normal(20_000, seed=4, zero_frac=0.4)
+    a, = oracle.roundtrip(g, [0, g.size], None, 1e-2, 3, 16, value_source=oracle.VALUES_SPARSE)
+    b, = oracle.roundtrip(g, [0, g.size], None, 1e-2, 3, 16, value_source=oracle.VALUES_DENSE)
+    np.testing.assert_array_equal(a.V, b.V)
+    np.testing.assert_array_equal(a.dense, b.dense)
