@@ -20,12 +20,16 @@
  *    invalid argument returns DR_EINVAL and launches nothing.
  *  - Counts produced by one call and consumed by the next stay in device
  *    memory (`uint64_t*` device scalars), so calls chain without host syncs.
- *    A `*_cap` argument is a host upper bound of such a device count; it
- *    only sizes grids and scratch.  Every item below the device count is
- *    processed even if the count exceeds the bound, EXCEPT where an output
- *    capacity is named: entries beyond an output capacity are dropped and
- *    the full count is still reported, so the caller detects overflow by
- *    comparing the count with the capacity after synchronising.
+ *    An input count `n` comes with `n_cap`, the host-side capacity of the
+ *    items behind it (it sizes grids and scratch): a call processes the
+ *    first min(*n, n_cap) items, and its `flags_out` word (device,
+ *    nullable) receives DR_FLAG_CAPACITY when *n exceeds n_cap, else 0.
+ *    Items past n_cap are then NOT processed (a filter built from a cut
+ *    list yields false negatives for them), so a caller whose count can
+ *    exceed its capacity must check that word.  An output capacity `cap`
+ *    works the other way: entries beyond it are dropped and the full count
+ *    is still reported, so the caller detects overflow by comparing the
+ *    count with the capacity after synchronising.
  *  - Indices are 0-based u32 (the paper's [d] is 1-based, Section 2), so a
  *    gradient tensor holds fewer than 2^32 elements.
  *  - The caller owns all memory.  Scratch comes from `ws`, at least
@@ -116,6 +120,15 @@ typedef enum {
 #define DR_FIT_POLY 0u
 #define DR_FIT_DEXP 1u
 
+/* Where the sender takes the values of the positives it codes (Section 4,
+ * policy P0).  SPARSE: from the sparsified gradient g~, whose entries are
+ * g at the selected indices and 0 elsewhere, so a false positive carries
+ * the value 0 (the base definition of P0).  DENSE: from the dense gradient
+ * g, so a false positive carries its own gradient value (the variant the
+ * paper allows when the sparsifier leaves g accessible, as GRACE does). */
+#define DR_VALUES_DENSE 0u
+#define DR_VALUES_SPARSE 1u
+
 /* Bits of the per-tensor flags word (slot 3 of counts_out). */
 #define DR_FLAG_NONFINITE 1u    /* the tensor held NaN or Inf */
 #define DR_FLAG_DEC_MISMATCH 2u /* receiver: the record is invalid, or its |P| differs from the header */
@@ -145,6 +158,19 @@ DR_EXPORT size_t dr_workspace_bytes(uint64_t d, uint64_t n_tensors);
 /* Message of the last failure on the calling host thread ("" if none). */
 DR_EXPORT const char *dr_last_error(void);
 
+/* Host-only, no GPU needed.  Replays, for configuration cfg_h, the index
+ * ranges that the kernels derive from the host's plan (the Bloom insert's
+ * item chunks and partial slices, for the round trip's selection bitmap and
+ * for dr_bloom_encode's index list; the probe pass's per-block tile ranges
+ * for several grid sizes; the value sort's tiles for value counts from 0 to
+ * each tensor's size) with the same arithmetic the kernels run, and checks
+ * every range against the buffer it addresses.  *violations_h receives the
+ * number of ranges that would leave their buffer (0 for a sound plan); when
+ * it is not 0, dr_last_error() describes the first.  EINVAL: an invalid
+ * cfg_h or a null violations_h. */
+typedef struct dr_config dr_config;
+DR_EXPORT dr_status dr_check_ranges(const dr_config *cfg_h, uint64_t *violations_h);
+
 /* ---------------------------------------------------------------------- */
 /* Sparsification (Section 2 "Sparsification"; Section 10.2)               */
 /* ---------------------------------------------------------------------- */
@@ -163,13 +189,15 @@ DR_EXPORT dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uin
 /* Bloom-filter index compression (Sections 2 and 4)                       */
 /* ---------------------------------------------------------------------- */
 
-/* Insert the *n (device count, at most n_cap in the usual case) indices
- * idx[0..*n) into an m_bits-bit filter with k hash functions: set bit
- * h_j(x) for every x and j < k.  bits_out receives all m_bits/32 words (the
- * callee clears them first).  m_bits must be a positive multiple of 32 below
- * 2^32; 1 <= k <= 32.  Indices must be below 2^32. */
+/* Insert the *n (device count) indices idx[0..*n) into an m_bits-bit filter
+ * with k hash functions: set bit h_j(x) for every x and j < k.  bits_out
+ * receives all m_bits/32 words (the callee clears them first).  n_cap is
+ * the capacity of idx: at most n_cap indices are inserted, and flags_out
+ * (device, nullable) receives DR_FLAG_CAPACITY if *n > n_cap (see the
+ * conventions above), else 0.  m_bits must be a positive multiple of 32
+ * below 2^32; 1 <= k <= 32.  Indices must be below 2^32. */
 DR_EXPORT dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap, uint64_t m_bits, uint32_t k,
-                          uint32_t *bits_out, void *ws, size_t ws_bytes, void *stream);
+                          uint32_t *bits_out, uint64_t *flags_out, void *ws, size_t ws_bytes, void *stream);
 
 /* Full-range query of policy P0 (Section 4): every i in [0, d) whose k bits
  * are all set in `bits`, written in ascending order to idx_out (at most cap
@@ -182,7 +210,9 @@ DR_EXPORT dr_status dr_bloom_decode(const uint32_t *bits, uint64_t m_bits, uint3
 /* Curve-fitting value compression (Section 5; reorder map Section 5.1)    */
 /* ---------------------------------------------------------------------- */
 
-/* Compress vals[0..*n) (device count, n_cap its host bound): sort the values
+/* Compress vals[0..*n) (device count; n_cap, the capacity of vals, bounds
+ * it and flags_out, device and nullable, receives DR_FLAG_CAPACITY if *n >
+ * n_cap, else 0, as the conventions above say): sort the values
  * in descending order (signed; +0 before -0; equal values keep their
  * order), split the sorted sequence into S_eff = min(n_seg, max(1,
  * floor(n/(degree+1)))) runs of equal count (run s holds sorted ranks
@@ -198,20 +228,24 @@ DR_EXPORT dr_status dr_bloom_decode(const uint32_t *bits, uint64_t m_bits, uint3
  * / 32) words.  EINVAL: degree > DR_MAX_DEGREE, n_seg == 0 or
  * > DR_MAX_SEGMENTS, n_cap >= 2^32. */
 DR_EXPORT dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_cap, uint32_t degree, uint32_t n_seg,
-                             float *coef_out, uint32_t *sigma_out, void *ws, size_t ws_bytes, void *stream);
+                             float *coef_out, uint32_t *sigma_out, uint64_t *flags_out, void *ws, size_t ws_bytes,
+                             void *stream);
 
 /* Reconstruct *n values from coef and sigma as written by
  * dr_curvefit_encode: value q is run s's polynomial, evaluated by Horner's
- * rule in double at the abscissa of rank sigma[q], rounded to fp32. */
+ * rule in double at the abscissa of rank sigma[q], rounded to fp32.  n_cap
+ * is the capacity of vals_out: at most n_cap values are written, and
+ * flags_out (device, nullable) receives DR_FLAG_CAPACITY if *n > n_cap,
+ * else 0. */
 DR_EXPORT dr_status dr_curvefit_decode(const float *coef, const uint32_t *sigma, const uint64_t *n, uint64_t n_cap,
-                             uint32_t degree, uint32_t n_seg, float *vals_out, void *ws, size_t ws_bytes,
-                             void *stream);
+                             uint32_t degree, uint32_t n_seg, float *vals_out, uint64_t *flags_out, void *ws,
+                             size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------- */
 /* The whole codec over a gradient split into tensors (Figure 3)           */
 /* ---------------------------------------------------------------------- */
 
-typedef struct {
+struct dr_config {
     uint64_t n_tensors;        /* >= 1, at most DR_MAX_TENSORS */
     const uint64_t *offsets_h; /* host, n_tensors+1 nondecreasing offsets, [0] = 0; tensor t is
                                   g[offsets_h[t] .. offsets_h[t+1]), fewer than 2^32 elements */
@@ -234,7 +268,8 @@ typedef struct {
                                   other half, restricted to [0, |P|) by cycle walking */
     uint32_t segmentation;     /* DR_SEG_EQUAL or DR_SEG_CHORD                                   */
     uint32_t fit_model;        /* DR_FIT_POLY or DR_FIT_DEXP                                     */
-} dr_config;
+    uint32_t value_source;     /* DR_VALUES_DENSE or DR_VALUES_SPARSE                            */
+};
 
 /* Payload container (Figure 3's "container"): one record per tensor at byte
  * offset rec_off_h[t] (multiples of 256) of the payload buffer.  A record is
@@ -246,7 +281,8 @@ typedef struct {
  * header bytes (64), d, n_selected, n_positives (|P|), n_values (values
  * coded: |P| under P0), m_bits, k, hash id (1 = MurmurHash3_x86_32), policy,
  * seed, D_eff, S_eff, sigma bits, record bytes (header + sections; what
- * would be sent), segmentation (DR_SEG_*) | value model (DR_FIT_*) << 8.
+ * would be sent), segmentation (DR_SEG_*) | value model (DR_FIT_*) << 8 |
+ * value source (DR_VALUES_*) << 16.
  * Returns the total payload capacity in bytes; fills rec_off_h (nullable,
  * n_tensors+1 entries) with the record offsets and the end.  Returns 0 for
  * an invalid configuration. */
@@ -255,8 +291,10 @@ DR_EXPORT size_t dr_payload_layout(const dr_config *cfg_h, uint64_t *rec_off_h);
 /* Sender side over the whole gradient g: per tensor, select (top-r or
  * support), insert into a Bloom filter sized by dr_bloom_params, run the
  * full-range query (P), let the policy pick the positives to code, take
- * their values from the dense gradient (V = g[P] under P0, Section 4), sort
- * and fit V, and write the record into `payload` (capacity
+ * their values from the dense gradient (V = g[P] under P0) or from the
+ * sparsified one (V = g~[P]: 0 at false positives), as cfg_h->value_source
+ * says (Section 4), sort and fit V, and write the record into `payload`
+ * (capacity
  * payload_bytes, at least dr_payload_layout()).  counts_out (device,
  * nullable) receives 4 u64 per tensor: n_selected, |P|, 0, flags. */
 DR_EXPORT dr_status dr_payload_encode(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,

@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(HERE, "libdeepreduce.so")
 
 DR_OK, DR_EINVAL, DR_ECAPACITY, DR_EDEVICE, DR_ENOTSUP = 0, -1, -2, -3, -4
 R_NONZERO = (1 << 64) - 1
-FLAG_NONFINITE, FLAG_DEC_MISMATCH, FLAG_COUNT, FLAG_CAPACITY = 1, 2, 4, 8
+FLAG_NONFINITE, FLAG_DEC_MISMATCH, FLAG_COUNT, FLAG_CAPACITY, FLAG_STALLED = 1, 2, 4, 8, 16
+VALUES_DENSE, VALUES_SPARSE = 0, 1
 HEADER_BYTES = 64
 HEADER_MAGIC = 0x31435244
 
@@ -28,7 +29,7 @@ EXPORTS = [
     "dr_bloom_params", "dr_sigma_bits", "dr_workspace_bytes", "dr_last_error", "dr_sparsify_topr",
     "dr_bloom_encode", "dr_bloom_decode", "dr_curvefit_encode", "dr_curvefit_decode", "dr_payload_layout",
     "dr_payload_encode", "dr_payload_decode", "dr_payload_decode_sum", "dr_roundtrip", "dr_trace_begin",
-    "dr_trace_end",
+    "dr_trace_end", "dr_check_ranges",
 ]
 
 
@@ -51,6 +52,7 @@ class DrConfig(ctypes.Structure):
         ("seed", ctypes.c_uint32),
         ("segmentation", ctypes.c_uint32),
         ("fit_model", ctypes.c_uint32),
+        ("value_source", ctypes.c_uint32),
     ]
 
 
@@ -77,10 +79,10 @@ def lib():
         "dr_workspace_bytes": (sz, [u64, u64]),
         "dr_last_error": (ctypes.c_char_p, []),
         "dr_sparsify_topr": (st, [vp, u64, u64, vp, vp, vp, vp, sz, vp]),
-        "dr_bloom_encode": (st, [vp, vp, u64, u64, u32, vp, vp, sz, vp]),
+        "dr_bloom_encode": (st, [vp, vp, u64, u64, u32, vp, vp, vp, sz, vp]),
         "dr_bloom_decode": (st, [vp, u64, u32, u64, vp, u64, vp, vp, sz, vp]),
-        "dr_curvefit_encode": (st, [vp, vp, u64, u32, u32, vp, vp, vp, sz, vp]),
-        "dr_curvefit_decode": (st, [vp, vp, vp, u64, u32, u32, vp, vp, sz, vp]),
+        "dr_curvefit_encode": (st, [vp, vp, u64, u32, u32, vp, vp, vp, vp, sz, vp]),
+        "dr_curvefit_decode": (st, [vp, vp, vp, u64, u32, u32, vp, vp, vp, sz, vp]),
         "dr_payload_layout": (sz, [cfgp, ctypes.POINTER(u64)]),
         "dr_payload_encode": (st, [vp, cfgp, vp, sz, vp, vp, sz, vp]),
         "dr_payload_decode": (st, [vp, cfgp, vp, vp, vp, vp, vp, sz, vp]),
@@ -88,6 +90,7 @@ def lib():
         "dr_roundtrip": (st, [vp, cfgp, vp, sz, vp, vp, vp, vp, vp, sz, vp]),
         "dr_trace_begin": (st, [vp]),
         "dr_trace_end": (st, [ctypes.c_char_p, sz]),
+        "dr_check_ranges": (st, [cfgp, ctypes.POINTER(u64)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -156,9 +159,10 @@ def sparsify_topr(g, r: int, idx_out, val_out, n_out, ws, stream=None):
         _ptr(g), g.numel(), r, _ptr(idx_out), _ptr(val_out), _ptr(n_out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def bloom_encode(idx, n_dev, n_cap: int, m_bits: int, k: int, bits_out, ws, stream=None):
+def bloom_encode(idx, n_dev, n_cap: int, m_bits: int, k: int, bits_out, ws, stream=None, flags_out=None):
     _check("dr_bloom_encode", lib().dr_bloom_encode(
-        _ptr(idx), _ptr(n_dev), n_cap, m_bits, k, _ptr(bits_out), _ptr(ws), ws.numel(), _stream(stream)))
+        _ptr(idx), _ptr(n_dev), n_cap, m_bits, k, _ptr(bits_out), _ptr(flags_out), _ptr(ws), ws.numel(),
+        _stream(stream)))
 
 
 def bloom_decode(bits, m_bits: int, k: int, d: int, idx_out, cap: int, n_out, ws, stream=None):
@@ -166,30 +170,33 @@ def bloom_decode(bits, m_bits: int, k: int, d: int, idx_out, cap: int, n_out, ws
         _ptr(bits), m_bits, k, d, _ptr(idx_out), cap, _ptr(n_out), _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def curvefit_encode(vals, n_dev, n_cap: int, degree: int, n_seg: int, coef_out, sigma_out, ws, stream=None):
+def curvefit_encode(vals, n_dev, n_cap: int, degree: int, n_seg: int, coef_out, sigma_out, ws, stream=None,
+                    flags_out=None):
     _check("dr_curvefit_encode", lib().dr_curvefit_encode(
-        _ptr(vals), _ptr(n_dev), n_cap, degree, n_seg, _ptr(coef_out), _ptr(sigma_out), _ptr(ws), ws.numel(),
-        _stream(stream)))
+        _ptr(vals), _ptr(n_dev), n_cap, degree, n_seg, _ptr(coef_out), _ptr(sigma_out), _ptr(flags_out), _ptr(ws),
+        ws.numel(), _stream(stream)))
 
 
-def curvefit_decode(coef, sigma, n_dev, n_cap: int, degree: int, n_seg: int, vals_out, ws, stream=None):
+def curvefit_decode(coef, sigma, n_dev, n_cap: int, degree: int, n_seg: int, vals_out, ws, stream=None,
+                    flags_out=None):
     _check("dr_curvefit_decode", lib().dr_curvefit_decode(
-        _ptr(coef), _ptr(sigma), _ptr(n_dev), n_cap, degree, n_seg, _ptr(vals_out), _ptr(ws), ws.numel(),
-        _stream(stream)))
+        _ptr(coef), _ptr(sigma), _ptr(n_dev), n_cap, degree, n_seg, _ptr(vals_out), _ptr(flags_out), _ptr(ws),
+        ws.numel(), _stream(stream)))
 
 
 class Config:
     """A dr_config together with the host offsets array it points to."""
 
     def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int, policy: int = 0, seed: int = 0,
-                 segmentation: int = 0, fit_model: int = 0):
+                 segmentation: int = 0, fit_model: int = 0, value_source: int = VALUES_DENSE):
         self.offsets = np.ascontiguousarray(np.asarray(offsets, dtype=np.uint64))
         self._off_c = (ctypes.c_uint64 * self.offsets.size)(*[int(x) for x in self.offsets])
         num, den = (R_NONZERO, 1) if ratio is None else ratio
         self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg, policy, seed,
-                          segmentation, fit_model)
+                          segmentation, fit_model, value_source)
         self.ratio, self.fpr, self.degree, self.n_seg = ratio, fpr, degree, n_seg
         self.policy, self.seed, self.segmentation, self.fit_model = policy, seed, segmentation, fit_model
+        self.value_source = value_source
 
     @property
     def n_tensors(self) -> int:
@@ -200,9 +207,18 @@ class Config:
         return int(self.offsets[-1])
 
     @classmethod
-    def from_workload(cls, w, policy: int = 0, seed: int = 0, segmentation: int = 0, n_seg=None, fit_model: int = 0):
+    def from_workload(cls, w, policy: int = 0, seed: int = 0, segmentation: int = 0, n_seg=None, fit_model: int = 0,
+                      value_source: int = VALUES_DENSE):
         return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg if n_seg is None else n_seg, policy, seed,
-                   segmentation, fit_model)
+                   segmentation, fit_model, value_source)
+
+
+def check_ranges(cfg: Config) -> tuple[int, str]:
+    """Host-only: the number of kernel index ranges of cfg's plan that would
+    leave their buffers, and the first one's description."""
+    v = ctypes.c_uint64()
+    _check("dr_check_ranges", lib().dr_check_ranges(ctypes.byref(cfg.c), ctypes.byref(v)))
+    return int(v.value), last_error()
 
 
 def payload_layout(cfg: Config) -> tuple[int, list]:
@@ -276,6 +292,7 @@ class Record:
     rec_bytes: int
     seg_mode: int
     model: int
+    value_source: int
     bits: np.ndarray
     coef: np.ndarray
     knots: np.ndarray  # starts of runs 1 .. S_eff-1 (chord segmentation), else empty
@@ -296,11 +313,11 @@ def parse_record(buf: bytes | np.ndarray, start: int) -> Record:
     ncoef = se * (de + 1)
     coef = b[at: at + 4 * ncoef].view("<f4").copy()
     at += 4 * ncoef
-    seg, model = seg & 0xFF, seg >> 8
+    seg, model, vsrc = seg & 0xFF, (seg >> 8) & 0xFF, seg >> 16
     nkn = se - 1 if seg == 1 and se > 1 else 0
     knots = b[at: at + 4 * nkn].view("<u4").copy()
     at += 4 * nkn
     nw = (n_v * sb + 31) // 32
     sigma = b[at: at + 4 * nw].view("<u4").copy()
-    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, seg, model, bits, coef, knots,
-                  sigma)
+    return Record(d, n_sel, n_pos, n_v, m_bits, k, hid, pol, seed, de, se, sb, rb, seg, model, vsrc, bits, coef,
+                  knots, sigma)

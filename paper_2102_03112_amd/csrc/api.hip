@@ -24,6 +24,7 @@ static_assert(POLICY_P0 == DR_POLICY_P0 && POLICY_RANDOM == DR_POLICY_RANDOM && 
               "index policy ids");
 static_assert(SEG_EQUAL == DR_SEG_EQUAL && SEG_CHORD == DR_SEG_CHORD, "segmentation ids");
 static_assert(FIT_POLY == DR_FIT_POLY && FIT_DEXP == DR_FIT_DEXP, "value model ids");
+static_assert(VALUES_DENSE == DR_VALUES_DENSE && VALUES_SPARSE == DR_VALUES_SPARSE, "value source ids");
 static_assert(MAX_SEG == DR_MAX_SEGMENTS && MAX_DEG == DR_MAX_DEGREE, "limits of the header and the kernels");
 
 namespace {
@@ -338,6 +339,7 @@ dr_status check_cfg(const dr_config *cfg) {
     if (cfg->segmentation > DR_SEG_CHORD) return fail(DR_EINVAL, "unknown segmentation %u", cfg->segmentation);
     if (cfg->fit_model > DR_FIT_DEXP) return fail(DR_EINVAL, "unknown value model %u", cfg->fit_model);
     if (cfg->policy > DR_POLICY_RIGHTMOST) return fail(DR_EINVAL, "unknown index policy %u", cfg->policy);
+    if (cfg->value_source > DR_VALUES_SPARSE) return fail(DR_EINVAL, "unknown value source %u", cfg->value_source);
     return DR_OK;
 }
 
@@ -408,6 +410,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.policy = cfg->policy;
         in.seed = cfg->seed;
         in.seg_mode = cfg->segmentation;
+        in.value_src = cfg->value_source;
         in.mC = mC;
         // top-r: |S| = r is known, so the filter size is too
         in.m_words_in = nz ? 0u : (uint32_t)(m_cap / 32);
@@ -794,6 +797,177 @@ Plan single_plan(uint64_t d) {
 }
 
 // ---------------------------------------------------------------------------
+// Host-side range check: the kernels' index arithmetic (ranges.hpp) replayed
+// over every chunk, slice, block and sort tile a configuration plans.
+// ---------------------------------------------------------------------------
+struct RangeCheck {
+    uint64_t bad = 0;
+    std::string first;
+    void fail_if(bool cond, const char *fmt, ...) {
+        if (!cond) return;
+        if (bad++ == 0) {
+            char buf[512];
+            va_list ap;
+            va_start(ap, fmt);
+            vsnprintf(buf, sizeof buf, fmt, ap);
+            va_end(ap);
+            first = buf;
+        }
+    }
+};
+
+// The direct insert of a plan: every (slice, chunk) block's bitmap window
+// or list window, and its partial slice in the position buffer.
+void check_direct(const Plan &p, bool from_bitmap, const std::vector<uint64_t> &list_n, RangeCheck &rc) {
+    const Carve &c = p.carve;
+    const uint64_t sel_words = c.slots / 32, pos_cap = c.pos_capacity();
+    for (size_t t = 0; t < p.t.size(); ++t) {
+        const TInit &in = p.t[t];
+        const uint32_t G = in.dir_g, per = in.dir_per;
+        const uint64_t m_words = p.bl_mcap[t] / 32;
+        rc.fail_if(G == 0 || per == 0, "tensor %zu: direct insert with %u chunks of %u", t, G, per);
+        for (uint32_t ch = 0; ch < G; ++ch) {
+            if (from_bitmap) {
+                const Range32 cw = dir_bitmap_chunk(in.ntiles, per, ch, TILE_WORDS);
+                // the kernel's view and loop run over hi - lo words (32-bit)
+                rc.fail_if(cw.lo > cw.hi || (uint32_t)(cw.hi - cw.lo) > (uint64_t)per * TILE_WORDS,
+                           "tensor %zu chunk %u: bitmap words [%u, %u)", t, ch, cw.lo, cw.hi);
+                rc.fail_if(cw.hi > (uint64_t)in.ntiles * TILE_WORDS,
+                           "tensor %zu chunk %u: bitmap words end %u past the tensor's %u tiles", t, ch, cw.hi,
+                           in.ntiles);
+                rc.fail_if((in.slot >> 5) + cw.hi > sel_words, "tensor %zu chunk %u: bitmap words past the bitmap",
+                           t, ch);
+            } else {
+                for (uint64_t n : list_n) {
+                    const Range32 cq = dir_list_chunk((uint32_t)n, per, ch);
+                    rc.fail_if(cq.hi > n || cq.lo > cq.hi || (uint32_t)(cq.hi - cq.lo) > per,
+                               "tensor %zu chunk %u: items [%u, %u) of %llu", t, ch,
+                               cq.lo, cq.hi, (unsigned long long)n);
+                }
+                // every item below the capacity falls in some chunk
+                rc.fail_if((uint64_t)G * per < p.bl_ncap[t], "tensor %zu: %u chunks of %u cover fewer than %llu items",
+                           t, G, per, (unsigned long long)p.bl_ncap[t]);
+            }
+            for (uint32_t sl = 0; sl < in.dir_nsl; ++sl) {
+                const uint64_t w0 = (uint64_t)sl * DIR_SLICE_WORDS;
+                if (w0 >= m_words) continue;
+                const uint64_t nw = std::min<uint64_t>(DIR_SLICE_WORDS, m_words - w0);
+                const uint64_t local = (uint64_t)sl * G + ch;
+                rc.fail_if(nw > in.dir_sw, "tensor %zu slice %u: %llu words in a %u-word partial", t, sl,
+                           (unsigned long long)nw, in.dir_sw);
+                rc.fail_if(in.dir_pb + local * in.dir_sw + nw > pos_cap,
+                           "tensor %zu slice %u chunk %u: partial slice past the position buffer", t, sl, ch);
+                rc.fail_if(in.dir_blk0 + local >= p.dir_blocks, "tensor %zu: block %llu past the grid", t,
+                           (unsigned long long)(in.dir_blk0 + local));
+            }
+        }
+        // the OR pass: slice sl's partials are G consecutive runs of dir_sw words
+        rc.fail_if(in.dir_sl0 + in.dir_nsl > p.dir_slices, "tensor %zu: slices past the OR grid", t);
+    }
+}
+
+// The bucketed insert's regions of a plan.
+void check_bucketed(const Plan &p, RangeCheck &rc) {
+    const Carve &c = p.carve;
+    const uint64_t pos_cap = c.pos_capacity();
+    for (size_t t = 0; t < p.t.size(); ++t) {
+        const TInit &in = p.t[t];
+        rc.fail_if(in.bl_pos0 + in.bl_poscap > pos_cap, "tensor %zu: position records past the buffer", t);
+        rc.fail_if(in.bl_tab0 + (uint64_t)in.bl_nchunks * in.bl_nslices > c.btab, "tensor %zu: count table overrun",
+                   t);
+        rc.fail_if((uint64_t)in.bl_nslices << in.slice_log2 < p.bl_mcap[t], "tensor %zu: slices cover too few bits",
+                   t);
+    }
+}
+
+// The probe pass's block ranges for several grid sizes: contiguous, in
+// block order, covering every tile once.
+void check_probe_blocks(uint32_t ntiles, RangeCheck &rc) {
+    const uint32_t grids[] = {1u, 2u, 3u, 7u, 32u, 224u, 255u, 256u, 1024u, PSTAT_MAX};
+    for (uint32_t grid : grids) {
+        uint32_t next = 0;
+        for (uint32_t b = 0; b < grid; ++b) {
+            const Range32 r = probe_block_tiles(ntiles, grid, b);
+            rc.fail_if(r.lo > r.hi || r.hi > ntiles, "grid %u block %u: tiles [%u, %u) of %u", grid, b, r.lo, r.hi,
+                       ntiles);
+            if (r.lo < r.hi) {
+                rc.fail_if(r.lo != next, "grid %u block %u: starts at tile %u, not %u", grid, b, r.lo, next);
+                next = r.hi;
+            }
+        }
+        rc.fail_if(next != ntiles, "grid %u: blocks cover %u of %u tiles", grid, next, ntiles);
+    }
+}
+
+// The value sort's tiles for value counts from 0 to d per tensor (the count
+// is known only on the device): each tile's view lies inside the tensor's
+// slot and below the count, and the tiles of all tensors fit the look-back
+// status rows (one per tile of the gradient).
+void check_sort_tiles(const Plan &p, RangeCheck &rc) {
+    const Carve &c = p.carve;
+    uint64_t max_tiles = 0;
+    for (size_t t = 0; t < p.t.size(); ++t) {
+        const TInit &in = p.t[t];
+        const uint64_t d = in.d;
+        const uint64_t cand[] = {0, 1, TILE - 1, TILE, TILE + 1, 2 * TILE + 7, d / 2, d > 0 ? d - 1 : 0, d};
+        uint64_t most = 0;
+        for (uint64_t nv : cand) {
+            if (nv > d) continue;
+            const uint32_t ntl = (uint32_t)((nv + TILE - 1) / TILE);
+            for (uint32_t lt = 0; lt <= ntl; ++lt) {  // one past the last, as a block past the end computes it
+                const Range32 r = sort_tile_values((uint32_t)nv, lt, TILE);
+                rc.fail_if(r.lo > r.hi || r.hi > nv || r.hi - r.lo > TILE,
+                           "tensor %zu, %llu values, tile %u: values [%u, %u)", t, (unsigned long long)nv, lt, r.lo,
+                           r.hi);
+                rc.fail_if(in.slot + r.hi > c.slots, "tensor %zu, %llu values, tile %u: past the work arrays", t,
+                           (unsigned long long)nv, lt);
+            }
+            most = std::max<uint64_t>(most, ntl);
+        }
+        max_tiles += most;
+    }
+    rc.fail_if(max_tiles > c.ntiles, "sort tiles %llu exceed the %llu look-back rows", (unsigned long long)max_tiles,
+               (unsigned long long)c.ntiles);
+}
+
+dr_status check_ranges_impl(const dr_config *cfg, uint64_t *violations) {
+    if (!violations) return fail(DR_EINVAL, "violations_h is null");
+    Plan p;
+    std::vector<uint64_t> rec_off;
+    dr_status st = plan_config(cfg, p, rec_off);
+    if (st != DR_OK) return st;
+    RangeCheck rc;
+    // the round trip's plan: items from the selection bitmap
+    if (p.direct)
+        check_direct(p, true, {}, rc);
+    else
+        check_bucketed(p, rc);
+    check_probe_blocks((uint32_t)p.carve.ntiles, rc);
+    check_sort_tiles(p, rc);
+    // the standalone insert of each tensor's selection (dr_bloom_encode's
+    // plan: items from a list of n_cap entries)
+    for (size_t t = 0; t < p.t.size(); ++t) {
+        const uint64_t n_cap = p.bl_ncap[t];
+        Plan q = single_plan(n_cap);
+        TInit &in = q.t[0];
+        in.k = p.t[t].k;
+        in.m_words_in = (uint32_t)(p.bl_mcap[t] / 32);
+        plan_bloom(in, n_cap, p.bl_mcap[t], false, q);
+        q.carve.plan();
+        plan_bloom_rounds(q, in.k);
+        plan_bloom_direct(q, false);
+        if (q.direct)
+            check_direct(q, false, {0, 1, n_cap / 2, n_cap}, rc);
+        else
+            check_bucketed(q, rc);
+    }
+    *violations = rc.bad;
+    if (rc.bad) return fail(DR_OK, "%llu range violations; first: %s", (unsigned long long)rc.bad, rc.first.c_str());
+    g_err.clear();
+    return DR_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Opt-in per-kernel timing
 // ---------------------------------------------------------------------------
 struct TraceMark {
@@ -922,6 +1096,10 @@ dr_status dr_trace_end(char *buf_h, size_t buf_bytes) {
     return st;
 }
 
+dr_status dr_check_ranges(const dr_config *cfg_h, uint64_t *violations_h) {
+    return check_ranges_impl(cfg_h, violations_h);
+}
+
 dr_status dr_bloom_params(uint64_t n_items, double fpr, uint64_t *m_bits_h, uint32_t *k_h) {
     if (!m_bits_h || !k_h) return fail(DR_EINVAL, "null output pointer");
     if (!bloom_params_host(n_items, fpr, m_bits_h, k_h)) return fail(DR_EINVAL, "fpr outside (0, 1) or m >= 2^32");
@@ -1001,7 +1179,7 @@ dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx
 }
 
 dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap, uint64_t m_bits, uint32_t k,
-                          uint32_t *bits_out, void *ws, size_t ws_bytes, void *stream) {
+                          uint32_t *bits_out, uint64_t *flags_out, void *ws, size_t ws_bytes, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     if (!n || !bits_out || (!idx && n_cap)) return fail(DR_EINVAL, "null pointer");
     if (m_bits < 32 || (m_bits & 31) || m_bits >= (1ull << 32)) return fail(DR_EINVAL, "bad m_bits");
@@ -1023,7 +1201,7 @@ dr_status dr_bloom_encode(const uint32_t *idx, const uint64_t *n, uint64_t n_cap
     w.S = const_cast<uint32_t *>(idx);
     trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(launch_import_n(w, n, n_cap, s));
+    DR_HIP(launch_import_n(w, n, n_cap, flags_out, s));
     if (p.direct)
         DR_HIP(launch_bloom_direct(w, false, p.dir_blocks, p.dir_slices, s));
     else
@@ -1054,7 +1232,8 @@ dr_status dr_bloom_decode(const uint32_t *bits, uint64_t m_bits, uint32_t k, uin
 }
 
 dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_cap, uint32_t degree, uint32_t n_seg,
-                             float *coef_out, uint32_t *sigma_out, void *ws, size_t ws_bytes, void *stream) {
+                             float *coef_out, uint32_t *sigma_out, uint64_t *flags_out, void *ws, size_t ws_bytes,
+                             void *stream) {
     hipStream_t s = (hipStream_t)stream;
     if (!n || !coef_out || ((!vals || !sigma_out) && n_cap)) return fail(DR_EINVAL, "null pointer");
     if (degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
@@ -1075,7 +1254,7 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
     const Work w = p.carve.view((uint8_t *)ws);
     trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(launch_keygen(w, vals, n, n_cap, persist_grid(4), s));
+    DR_HIP(launch_keygen(w, vals, n, n_cap, flags_out, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, false, nullptr, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
@@ -1084,8 +1263,8 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
 }
 
 dr_status dr_curvefit_decode(const float *coef, const uint32_t *sigma, const uint64_t *n, uint64_t n_cap,
-                             uint32_t degree, uint32_t n_seg, float *vals_out, void *ws, size_t ws_bytes,
-                             void *stream) {
+                             uint32_t degree, uint32_t n_seg, float *vals_out, uint64_t *flags_out, void *ws,
+                             size_t ws_bytes, void *stream) {
     hipStream_t s = (hipStream_t)stream;
     if (!n || ((!coef || !sigma || !vals_out) && n_cap)) return fail(DR_EINVAL, "null pointer");
     if (degree > DR_MAX_DEGREE) return fail(DR_EINVAL, "degree > %d", DR_MAX_DEGREE);
@@ -1101,7 +1280,7 @@ dr_status dr_curvefit_decode(const float *coef, const uint32_t *sigma, const uin
     const Work w = p.carve.view((uint8_t *)ws);
     trace_call(s);
     DR_HIP(run_init(w, p.t, s));
-    DR_HIP(launch_curvefit_decode(w, coef, sigma, n, n_cap, vals_out, persist_grid(4), s));
+    DR_HIP(launch_curvefit_decode(w, coef, sigma, n, n_cap, vals_out, flags_out, persist_grid(4), s));
     return DR_OK;
 }
 

@@ -413,11 +413,10 @@ __global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct(Work w) {
         }
     };
     if (FROM_BITMAP) {
-        const uint32_t per = td.in.dir_per;
         // chunk c's bitmap words [wa, wb); chunks past the tensor's tiles
         // (more chunks than tiles) are empty
-        const uint32_t wb = min(td.in.ntiles, (c + 1) * per) * TILE_WORDS;
-        const uint32_t wa = min(c * per * TILE_WORDS, wb);
+        const Range32 cw = dir_bitmap_chunk(td.in.ntiles, td.in.dir_per, c, TILE_WORDS);
+        const uint32_t wa = cw.lo, wb = cw.hi;
         // eight bitmap words per thread in flight, read through a buffer
         // view of the chunk (reads past it return 0).  A wave's selected
         // indices go through its queue, and are hashed 64 at a time, so all
@@ -453,9 +452,9 @@ __global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct(Work w) {
         __builtin_amdgcn_wave_barrier();
         if (lane < qn) add(q[lane]);
     } else {
-        const uint32_t per = td.in.dir_per, n = td.n;
-        const uint32_t qa = c * per, qb = min(n, qa + per);
-        const __amdgpu_buffer_rsrc_t iv = buffer_view(w.S + td.in.slot + qa, 4u * (qb - min(qa, qb)));
+        const Range32 cq = dir_list_chunk(td.n, td.in.dir_per, c);
+        const uint32_t qa = cq.lo, qb = cq.hi;
+        const __amdgpu_buffer_rsrc_t iv = buffer_view(w.S + td.in.slot + qa, 4u * (qb - qa));
         for (uint32_t x0 = 0; qa + x0 < qb; x0 += 8 * DIR_THREADS) {
             uint32_t it[8];
 #pragma unroll
@@ -590,9 +589,10 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     v.deff = h[H_DEFF];
     v.seff = h[H_SEFF];
     v.b = h[H_B];
-    const uint32_t hw15 = h[H_SEGMODE];  // segmentation | value model << 8
+    const uint32_t hw15 = h[H_SEGMODE];  // segmentation | value model << 8 | value source << 16
     v.segmode = hw15 & 0xffu;
     v.model = (hw15 >> 8) & 0xffu;
+    const uint32_t vsrc = (hw15 >> 16) & 0xffu;
     v.bits = (const uint32_t *)(rec + HDR_BYTES);
     const uint32_t coef_off = HDR_BYTES + (v.m_bits / 32u) * 4u;
     v.coef = (const float *)(rec + coef_off);
@@ -602,7 +602,7 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     *ok = h[H_MAGIC] == HDR_MAGIC && h[H_BYTES] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && v.k >= 1 &&
           v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && v.npos <= d && v.nv <= v.npos &&
           v.policy <= POLICY_RIGHTMOST && (v.policy != POLICY_P0 || v.nv == v.npos) && v.segmode <= SEG_CHORD &&
-          (hw15 >> 16) == 0 && v.model <= FIT_DEXP && (v.model != FIT_DEXP || v.deff == 3) &&
+          (hw15 >> 24) == 0 && vsrc <= VALUES_SPARSE && v.model <= FIT_DEXP && (v.model != FIT_DEXP || v.deff == 3) &&
           (v.nv == 0 || (v.seff >= 1 && v.seff <= v.nv && v.seff <= MAX_SEG && v.b >= sigma_bits(v.nv))) &&
           need <= cap;
     if (!*ok) {  // nothing of an invalid record is read past its first filter word
@@ -845,9 +845,8 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
     // derived from it in scalar registers
     const uint32_t lane = threadIdx.x & 63u, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     constexpr uint32_t QPT = TILE / QWAVE;  // steps per tile
-    const uint32_t per = (w.ntiles_total + gridDim.x - 1) / gridDim.x;
-    const uint32_t t_begin = min(w.ntiles_total, blockIdx.x * per);
-    const uint32_t t_end = min(w.ntiles_total, t_begin + per);
+    const Range32 own = probe_block_tiles(w.ntiles_total, gridDim.x, blockIdx.x);
+    const uint32_t t_begin = own.lo, t_end = own.hi;
     uint32_t cached = 0xffffffffu, fcw = 0;
     for (uint32_t rb = t_begin; rb < t_end;) {
         const uint32_t t = tensor_of_tile(w, rb);
@@ -1116,6 +1115,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
     RecordView rv{};
     // the policy's view of the tensor: positives, values coded, key
     uint32_t npos = 0, ncoded = 0, policy = POLICY_P0, pseed = 0;
+    bool sparse_vals = false;  // sender: values from g~ (0 off the selection)
     for (; tile < w.ntiles_total; tile += gridDim.x) {
         const uint32_t t = tn;
         TDesc &td = w.td[t];
@@ -1129,6 +1129,7 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
                 ncoded = td.nv;
                 policy = td.in.policy;
                 pseed = td.in.seed;
+                sparse_vals = td.in.value_src == VALUES_SPARSE;
             }
             if (MODE == Q_DECODE) {
                 bool ok = true;
@@ -1182,7 +1183,10 @@ __global__ __launch_bounds__(NTHREADS) void k_emit(Work w, QueryOut o) {
             if (MODE == Q_ENCODE) {
                 const uint32_t vn = policy_slot(q, npos, ncoded, policy, pseed);
                 if (vn != NO_SLOT) {
-                    const float x = o.g[toff_el + i];
+                    float x = o.g[toff_el + i];
+                    // g~ is 0 at a false positive: i not in the selection
+                    // (tslot is a multiple of the tile, so bit i & 31)
+                    if (sparse_vals && !((w.selbits[(tslot + i) >> 5] >> (i & 31u)) & 1u)) x = 0.0f;
                     const uint64_t at = tslot + vn;
                     w.V[at] = x;
                     w.keyA[at] = ~order_key(x);  // ascending order of ~key = descending values

@@ -51,6 +51,8 @@ constexpr uint32_t NO_SLOT = 0xffffffffu;
 constexpr uint32_t SEG_EQUAL = 0, SEG_CHORD = 1;
 // value models (Section 5): polynomial, double exponential a e^(bt) + c e^(dt)
 constexpr uint32_t FIT_POLY = 0, FIT_DEXP = 1;
+// where the sender's coded values come from (Section 4): g, or g~ (0 off S)
+constexpr uint32_t VALUES_DENSE = 0, VALUES_SPARSE = 1;
 constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
 constexpr uint32_t HDR_BYTES = 64;
 // payload record header: sixteen little-endian u32 words
@@ -107,6 +109,8 @@ struct TInit {
     uint32_t fit_model;  // FIT_POLY or FIT_DEXP (then degree is 3: rows (a, b, c, d))
     uint32_t bnd0;       // chord segmentation: first segment-start entry of this tensor
     uint32_t seg_slot;   // chord segmentation over the whole grid: the tensor's state, or NO_SEG_SLOT
+    uint32_t value_src;  // VALUES_DENSE or VALUES_SPARSE
+    uint32_t pad_;
 };
 
 // Chord segmentation over the whole grid (at most SEG_GRID_RUNS runs per

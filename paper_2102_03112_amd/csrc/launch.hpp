@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include "dr_common.hpp"
+#include "ranges.hpp"
 
 namespace dr {
 
@@ -32,7 +33,7 @@ int resident_grid(K kernel, int threads, uint32_t work) {
 // each kernel launch; the time between consecutive events is that kernel's.
 void trace_mark(hipStream_t s, const char *kernel);
 
-constexpr int INIT_CHUNK = 16;  // tensors per set-up launch (kernel argument size)
+constexpr int INIT_CHUNK = 15;  // tensors per set-up launch (kernel argument size)
 
 struct InitArgs {
     uint32_t first, count;
@@ -47,6 +48,8 @@ struct ZeroArgs {
     ZeroRange z[8];
     uint32_t n;
 };
+// k_init's arguments stay within 4 KiB
+static_assert(sizeof(Work) + sizeof(InitArgs) + sizeof(ZeroArgs) <= 4096, "set-up kernel arguments");
 
 // select.hip
 // descriptors of one chunk of tensors, plus clearing the zero ranges
@@ -83,17 +86,20 @@ hipError_t launch_query_decode_sum(const Work &w, uint32_t npay, uint32_t ntens,
                                    float *dense_out, uint64_t *counts_out, hipStream_t s);
 
 // valuefit.hip
-hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
-                         hipStream_t s);
+// the standalone calls' device counts: at most n_cap items are used, and
+// flags_out (nullable) receives FLAG_CAPACITY if the count exceeds n_cap
+hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, uint64_t *flags_out,
+                         int grid_persist, hipStream_t s);
 hipError_t launch_value_setup(const Work &w, bool payload, uint64_t *counts_out, hipStream_t s);
 hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s);
 hipError_t launch_segment(const Work &w, uint32_t grid_req, bool block_pass, hipStream_t s);
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s);
 hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s);
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
-                                  uint64_t n_cap, float *vals_out, int grid_persist, hipStream_t s);
+                                  uint64_t n_cap, float *vals_out, uint64_t *flags_out, int grid_persist,
+                                  hipStream_t s);
 // device count <-> tensor 0's descriptor (standalone calls)
-hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, hipStream_t s);
+hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, uint64_t *flags_out, hipStream_t s);
 hipError_t launch_export_n(const Work &w, uint64_t *n_out, int field, hipStream_t s);
 
 }  // namespace dr

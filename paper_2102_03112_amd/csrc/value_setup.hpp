@@ -67,7 +67,7 @@ __device__ inline void value_setup_tensor(const Work &w, uint32_t t, int payload
         h[H_SEFF] = seff;
         h[H_B] = b;
         h[H_RECBYTES] = rec_bytes;
-        h[H_SEGMODE] = td.in.seg_mode | (td.model << 8);
+        h[H_SEGMODE] = td.in.seg_mode | (td.model << 8) | (td.in.value_src << 16);
     }
 }
 

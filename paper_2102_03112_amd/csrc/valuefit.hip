@@ -20,13 +20,14 @@ namespace dr {
 
 // standalone value path: keys from the caller's values
 __global__ __launch_bounds__(NTHREADS) void k_keygen(Work w, const float *__restrict__ vals, const uint64_t *n,
-                                                     uint64_t n_cap) {
+                                                     uint64_t n_cap, uint64_t *flags_out) {
     const uint64_t n64 = *n;
     const uint32_t nv = (uint32_t)(n64 < n_cap ? n64 : n_cap);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         w.td[0].nv = nv;
         w.td[0].npos = nv;
         if (n64 > n_cap) atomicOr(&w.td[0].flags, FLAG_CAPACITY);
+        if (flags_out) *flags_out = n64 > n_cap ? FLAG_CAPACITY : 0u;
     }
     for (uint32_t q = blockIdx.x * NTHREADS + threadIdx.x; q < nv; q += gridDim.x * NTHREADS) {
         w.keyA[q] = ~order_key(vals[q]);
@@ -34,9 +35,9 @@ __global__ __launch_bounds__(NTHREADS) void k_keygen(Work w, const float *__rest
     }
 }
 
-hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, int grid_persist,
-                         hipStream_t s) {
-    k_keygen<<<grid_persist, NTHREADS, 0, s>>>(w, vals, n, n_cap);
+hipError_t launch_keygen(const Work &w, const float *vals, const uint64_t *n, uint64_t n_cap, uint64_t *flags_out,
+                         int grid_persist, hipStream_t s) {
+    k_keygen<<<grid_persist, NTHREADS, 0, s>>>(w, vals, n, n_cap, flags_out);
     trace_mark(s, "k_keygen");
     return hipGetLastError();
 }
@@ -95,7 +96,8 @@ __global__ __launch_bounds__(NTHREADS) void k_sort_upfront(Work w, const uint32_
         }
         const TDesc &td = w.td[t];
         const uint32_t lt = gt - td.stile0;
-        const uint32_t q0 = lt * TILE, nq = min(TILE, td.nv - min(td.nv, q0));
+        const Range32 sr = sort_tile_values(td.nv, lt, TILE);
+        const uint32_t q0 = sr.lo, nq = sr.hi - sr.lo;
         const __amdgpu_buffer_rsrc_t kv = buffer_view(keys + td.in.slot + q0, 4u * nq);
         uint32_t k16[TILE / NTHREADS];
 #pragma unroll
@@ -169,7 +171,8 @@ __global__ __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(3))) v
         const uint32_t lt = gt - stile0;
         const uint32_t nv = td.nv;
         const uint64_t slot = td.in.slot;
-        const uint32_t q0 = lt * TILE, nq = min(TILE, nv - min(nv, q0));
+        const Range32 sr = sort_tile_values(nv, lt, TILE);
+        const uint32_t q0 = sr.lo, nq = sr.hi - sr.lo;
         const __amdgpu_buffer_rsrc_t kv = buffer_view(kin + slot + q0, 4u * nq);
         const __amdgpu_buffer_rsrc_t vv = buffer_view(vin + slot + q0, 4u * nq);
         const uint32_t ebase = wv * (SORT_STEPS * 64) + lane;  // element of step c: ebase + 64 c
@@ -1427,10 +1430,11 @@ hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s) {
 __global__ __launch_bounds__(NTHREADS) void k_curvefit_decode(Work w, const float *__restrict__ coef,
                                                               const uint32_t *__restrict__ sigma,
                                                               const uint64_t *n, uint64_t n_cap,
-                                                              float *__restrict__ out) {
+                                                              float *__restrict__ out, uint64_t *flags_out) {
     const TDesc &td = w.td[0];
     const uint64_t n64 = *n;
     const uint32_t nv = (uint32_t)(n64 < n_cap ? n64 : n_cap);
+    if (flags_out && blockIdx.x == 0 && threadIdx.x == 0) *flags_out = n64 > n_cap ? FLAG_CAPACITY : 0u;
     uint32_t seff, deff;
     fit_shape(nv, td.in.degree, td.in.nseg, &seff, &deff);
     const uint32_t b = sigma_bits(nv);
@@ -1452,16 +1456,18 @@ __global__ __launch_bounds__(NTHREADS) void k_curvefit_decode(Work w, const floa
 }
 
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
-                                  uint64_t n_cap, float *vals_out, int grid_persist, hipStream_t s) {
-    k_curvefit_decode<<<grid_persist, NTHREADS, 0, s>>>(w, coef, sigma, n, n_cap, vals_out);
+                                  uint64_t n_cap, float *vals_out, uint64_t *flags_out, int grid_persist,
+                                  hipStream_t s) {
+    k_curvefit_decode<<<grid_persist, NTHREADS, 0, s>>>(w, coef, sigma, n, n_cap, vals_out, flags_out);
     trace_mark(s, "k_curvefit_decode");
     return hipGetLastError();
 }
 
-__global__ void k_import_n(Work w, const uint64_t *n, uint64_t n_cap) {
+__global__ void k_import_n(Work w, const uint64_t *n, uint64_t n_cap, uint64_t *flags_out) {
     const uint64_t v = *n;
     w.td[0].n = (uint32_t)(v < n_cap ? v : n_cap);
     if (v > n_cap) w.td[0].flags |= FLAG_CAPACITY;
+    if (flags_out) *flags_out = v > n_cap ? FLAG_CAPACITY : 0u;
 }
 
 __global__ void k_export_n(Work w, uint64_t *n_out, int field) {
@@ -1469,8 +1475,8 @@ __global__ void k_export_n(Work w, uint64_t *n_out, int field) {
     *n_out = field == 0 ? td.n : td.nv;
 }
 
-hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, hipStream_t s) {
-    k_import_n<<<1, 1, 0, s>>>(w, n, n_cap);
+hipError_t launch_import_n(const Work &w, const uint64_t *n, uint64_t n_cap, uint64_t *flags_out, hipStream_t s) {
+    k_import_n<<<1, 1, 0, s>>>(w, n, n_cap, flags_out);
     trace_mark(s, "k_import_n");
     return hipGetLastError();
 }

@@ -85,6 +85,7 @@ def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     assert (rec.policy, rec.seed) == (ref.policy, ref.seed)
     assert rec.seg_mode == ref.fit.seg_mode
     assert rec.model == ref.fit.model
+    assert rec.value_source == ref.value_source
     if ref.fit.seg_mode == oracle.SEG_CHORD:
         np.testing.assert_array_equal(rec.knots, ref.fit.bounds[1:-1].astype(np.uint32))
     assert (rec.seg_eff, rec.deg_eff, rec.sigma_b) == (ref.fit.S_eff, ref.fit.D_eff, ref.fit.b)

@@ -36,7 +36,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == len(set(names)) == 17
     assert sorted(names) == sorted(B.EXPORTS)
     for n in names:
         assert hasattr(L, n), n
@@ -160,16 +160,16 @@ def test_standalone_calls_reject_bad_arguments(L):
     assert L.dr_sparsify_topr(FAKE, 10, 5, FAKE, None, FAKE, FAKE, 10, None) == B.DR_EINVAL
     # Bloom: m not a positive multiple of 32, k out of range
     for m, k in [(0, 3), (33, 3), (1 << 32, 3), (64, 0), (64, 33)]:
-        assert L.dr_bloom_encode(FAKE, FAKE, 10, m, k, FAKE, FAKE, big, None) == B.DR_EINVAL
+        assert L.dr_bloom_encode(FAKE, FAKE, 10, m, k, FAKE, None, FAKE, big, None) == B.DR_EINVAL
         assert L.dr_bloom_decode(FAKE, m, k, 100, FAKE, 100, FAKE, FAKE, big, None) == B.DR_EINVAL
-    assert L.dr_bloom_encode(FAKE, None, 10, 64, 3, FAKE, FAKE, big, None) == B.DR_EINVAL
+    assert L.dr_bloom_encode(FAKE, None, 10, 64, 3, FAKE, None, FAKE, big, None) == B.DR_EINVAL
     assert L.dr_bloom_decode(FAKE, 64, 3, 1 << 32, FAKE, 100, FAKE, FAKE, big, None) == B.DR_EINVAL
     # curve fit: degree, segments, sizes
-    assert L.dr_curvefit_encode(FAKE, FAKE, 10, 8, 1, FAKE, FAKE, FAKE, big, None) == B.DR_EINVAL
-    assert L.dr_curvefit_encode(FAKE, FAKE, 10, 5, 0, FAKE, FAKE, FAKE, big, None) == B.DR_EINVAL
-    assert L.dr_curvefit_encode(FAKE, FAKE, 1 << 32, 5, 8, FAKE, FAKE, FAKE, big, None) == B.DR_EINVAL
-    assert L.dr_curvefit_decode(FAKE, FAKE, FAKE, 10, 8, 1, FAKE, FAKE, big, None) == B.DR_EINVAL
-    assert L.dr_curvefit_decode(FAKE, FAKE, None, 10, 5, 1, FAKE, FAKE, big, None) == B.DR_EINVAL
+    assert L.dr_curvefit_encode(FAKE, FAKE, 10, 8, 1, FAKE, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert L.dr_curvefit_encode(FAKE, FAKE, 10, 5, 0, FAKE, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert L.dr_curvefit_encode(FAKE, FAKE, 1 << 32, 5, 8, FAKE, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert L.dr_curvefit_decode(FAKE, FAKE, FAKE, 10, 8, 1, FAKE, None, FAKE, big, None) == B.DR_EINVAL
+    assert L.dr_curvefit_decode(FAKE, FAKE, None, 10, 5, 1, FAKE, None, FAKE, big, None) == B.DR_EINVAL
 
 
 def test_trace_end_without_begin_is_rejected(L):

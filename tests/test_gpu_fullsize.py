@@ -3,10 +3,12 @@ times (one dr_roundtrip over the whole gradient, workspace from
 dr_workspace_bytes).
 
 ResNet-50-, NCF- and VGG-16-sized gradients are checked element by element
-against the full oracle (tens of seconds of CPU each).  For the
-350M-parameter transformer split into 24 tensors, the oracle codes four of
-the tensors (both tensor sizes occur among them) and every tensor is
-checked against properties that hold at any size.
+against the full oracle (tens of seconds of CPU each).  The 350M-parameter
+transformer split into 24 tensors is coded in one GPU round trip (a
+module-scoped fixture); each of its 24 tensors is then compared element by
+element against the oracle's round trip of that tensor (about two seconds
+of CPU each, one test per tensor), and every tensor is also checked against
+properties that hold at any size.
 """
 import math
 
@@ -89,30 +91,42 @@ def _properties(g, w, t, rec, counts, idx, val, dense):
     assert err < 0.5
 
 
-def test_transformer_355m_x24_full():
+@pytest.fixture(scope="module")
+def transformer_run():
     w = W.WORKLOADS["transformer_355m_x24"]
     log(f"full-size {w.name}: generating d={w.d}")
     g = W.generate(w)
     cfg = B.Config.from_workload(w)
     log(f"full-size {w.name}: GPU round trip")
     out = run_roundtrip(g, cfg)
+    release_workspace()
+    yield w, g, out
+    del g, out
+
+
+def test_transformer_355m_x24_properties(transformer_run):
+    w, g, out = transformer_run
     off = w.offsets()
     for t in range(w.n_tensors):
         a, b = off[t], off[t + 1]
         rec = B.parse_record(out["payload"], out["rec_off"][t])
         _properties(g[a:b], w, t, rec, out["counts"][t], out["idx"][a:b], out["val"][a:b], out["dense"][a:b])
     log(f"full-size {w.name}: properties hold on all {w.n_tensors} tensors")
-    pick = [0, 7, 16, 23]  # 16 tensors of 14,784,299 elements, then 8 of 14,784,298
-    for t in pick:
-        log(f"full-size {w.name}: oracle on tensor {t}")
-        a, b = off[t], off[t + 1]
-        ref = oracle.roundtrip_tensor(g[a:b], oracle.ratio_count(b - a, *w.ratio), w.fpr, w.degree, w.n_seg)
-        sub = B.Config([0, b - a], w.ratio, w.fpr, w.degree, w.n_seg)
-        one = {
-            "payload": out["payload"][out["rec_off"][t]:out["rec_off"][t + 1]],
-            "rec_off": [0, out["rec_off"][t + 1] - out["rec_off"][t]],
-            "counts": out["counts"][t:t + 1],
-            "idx": out["idx"][a:b], "val": out["val"][a:b], "dense": out["dense"][a:b],
-        }
-        check_roundtrip(g[a:b], sub, one, [ref])
-    release_workspace()
+
+
+# 16 tensors of 14,784,299 elements, then 8 of 14,784,298 (array_split order)
+@pytest.mark.parametrize("t", range(24))
+def test_transformer_355m_x24_tensor(transformer_run, t):
+    w, g, out = transformer_run
+    off = w.offsets()
+    a, b = off[t], off[t + 1]
+    log(f"full-size {w.name}: oracle on tensor {t} ({b - a} elements)")
+    ref = oracle.roundtrip_tensor(g[a:b], oracle.ratio_count(b - a, *w.ratio), w.fpr, w.degree, w.n_seg)
+    sub = B.Config([0, b - a], w.ratio, w.fpr, w.degree, w.n_seg)
+    one = {
+        "payload": out["payload"][out["rec_off"][t]:out["rec_off"][t + 1]],
+        "rec_off": [0, out["rec_off"][t + 1] - out["rec_off"][t]],
+        "counts": out["counts"][t:t + 1],
+        "idx": out["idx"][a:b], "val": out["val"][a:b], "dense": out["dense"][a:b],
+    }
+    check_roundtrip(g[a:b], sub, one, [ref])

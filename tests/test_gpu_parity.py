@@ -112,6 +112,58 @@ def test_bloom_encode_parity(d, n, fpr):
     np.testing.assert_array_equal(host(bits).view(np.uint32), ref)
 
 
+@pytest.mark.parametrize("n_dev,n_cap", [(900, 1000), (1000, 1000), (1300, 1000), (300_000, 200_000)])
+def test_bloom_encode_count_against_capacity(n_dev, n_cap):
+    """At most n_cap indices are inserted; a device count above the capacity
+    is reported in flags_out (DR_FLAG_CAPACITY), one at or below it is not."""
+    import torch
+
+    log(f"bloom_encode n_dev={n_dev} n_cap={n_cap}")
+    S = W.random_indices(4 * max(n_dev, n_cap), max(n_dev, n_cap), seed=n_dev)
+    m, k = oracle.bloom_params(n_cap, 1e-3)
+    used = min(n_dev, n_cap)
+    ref = oracle.bloom_encode(S[:used], m, k)
+    bits = torch.full((m // 32,), 0x5A5A5A5A, dtype=torch.int32, device="cuda")
+    flags = dev_tensor(np.array([0x77], dtype=np.int64))
+    B.bloom_encode(dev_tensor(S.view(np.int32)), dev_tensor(np.array([n_dev], dtype=np.int64)), n_cap, m, k, bits,
+                   ws_for(max(n_dev, n_cap)), flags_out=flags)
+    sync()
+    np.testing.assert_array_equal(host(bits).view(np.uint32), ref)
+    assert int(host(flags)[0]) == (B.FLAG_CAPACITY if n_dev > n_cap else 0)
+
+
+@pytest.mark.parametrize("n_dev,n_cap", [(5000, 6000), (6000, 6000), (7000, 6000)])
+def test_curvefit_count_against_capacity(n_dev, n_cap):
+    """The value path uses the first min(n, n_cap) values, and both calls
+    report a count above the capacity in flags_out."""
+    import torch
+
+    log(f"curvefit n_dev={n_dev} n_cap={n_cap}")
+    D, S = 3, 4
+    V = W.normal(max(n_dev, n_cap), 71)
+    used = min(n_dev, n_cap)
+    ref = oracle.curvefit_encode(V[:used], D, S)
+    nd = dev_tensor(np.array([n_dev], dtype=np.int64))
+    coef = torch.zeros(S * (D + 1), dtype=torch.float32, device="cuda")
+    nw = oracle.sigma_words(n_cap) + 1
+    sig = torch.zeros(nw, dtype=torch.int32, device="cuda")
+    f1 = dev_tensor(np.array([0x77], dtype=np.int64))
+    f2 = dev_tensor(np.array([0x77], dtype=np.int64))
+    ws = ws_for(max(n_dev, n_cap))
+    B.curvefit_encode(dev_tensor(V), nd, n_cap, D, S, coef, sig, ws, flags_out=f1)
+    out = torch.full((n_cap + 64,), 5.0, dtype=torch.float32, device="cuda")
+    B.curvefit_decode(coef, sig, nd, n_cap, D, S, out, ws, flags_out=f2)
+    sync()
+    expect = B.FLAG_CAPACITY if n_dev > n_cap else 0
+    assert int(host(f1)[0]) == expect and int(host(f2)[0]) == expect
+    np.testing.assert_array_equal(host(sig).view(np.uint32)[: oracle.sigma_words(used)], ref.sigma)
+    coef_close(host(coef), ref.coef64, ref.S_eff, D + 1, ref.D_eff + 1)
+    y = host(out)
+    assert np.all(y[used:] == 5.0)  # nothing written past the count and the capacity
+    y_ref = oracle.curvefit_decode(ref.coef, ref.sigma, used, D, S)
+    values_close(y[:used], y_ref, oracle.sigma_unpack(ref.sigma, used), used, ref.S_eff)
+
+
 @pytest.mark.parametrize(
     "d,n,fpr",
     [(1, 1, 1e-3), (4095, 40, 1e-3), (4096, 41, 1e-2), (4097, 41, 1e-3), (3 * 4096 + 5, 200, 1e-3),
@@ -280,6 +332,36 @@ def test_roundtrip_policy_parity(name, policy):
     refs = oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=seed)
     assert any(ref.P.size > ref.S.size for ref in refs)
     check_roundtrip(g, cfg, out, refs)
+
+
+VSRC_CASES = {
+    # name: (g, offsets, ratio, fpr, D, S, policy)
+    "resnet20_fpr_1e-2": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-2, 5, 8, oracle.POLICY_P0),
+    "resnet20_fpr_1e-2_p1": (W.normal(36_864, 6), [0, 36_864], (1, 100), 1e-2, 5, 8, oracle.POLICY_RANDOM),
+    "ragged_tensors": RT_CASES["ragged_tensors"] + (oracle.POLICY_P0,),
+    "support_50k": RT_CASES["support_50k"] + (oracle.POLICY_P0,),
+    "many_tensors_3m": RT_CASES["many_tensors_3m"] + (oracle.POLICY_P0,),
+    # one value per run: the decoded gradient is g~ itself
+    "interp_d0": (W.normal(3000, 31, scale=1.0), [0, 3000], (1, 50), 0.05, 0, oracle.MAX_SEG, oracle.POLICY_P0),
+}
+
+
+@pytest.mark.parametrize("name", list(VSRC_CASES))
+def test_roundtrip_sparse_value_source_parity(name):
+    """Values from the sparsified gradient (Section 4's P0: 0 at a false
+    positive): record, positives and values as the oracle's."""
+    g, off, ratio, fpr, D, S, policy = VSRC_CASES[name]
+    seed = 0x5EED0001
+    log(f"roundtrip {name} value_source=sparse policy={policy}")
+    cfg = B.Config(off, ratio, fpr, D, S, policy, seed, value_source=B.VALUES_SPARSE)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=seed,
+                            value_source=oracle.VALUES_SPARSE)
+    check_roundtrip(g, cfg, out, refs)
+    if name == "interp_d0":
+        (ref,) = refs
+        assert ref.P.size > ref.S.size
+        np.testing.assert_array_equal(out["dense"], ref.dense)
 
 
 SEG_CASES = {
