@@ -349,6 +349,26 @@ DR_EXPORT dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t
                        float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * round trip as dr_roundtrip, with the same results, but its scratch is a
+ * static device array of the library, DR_STATIC_SCRATCH_BYTES bytes on each
+ * GPU it runs on (allocated when the library's code is loaded there and held
+ * until the process ends), instead of a caller's workspace.  The caller
+ * still passes the gradient, the payload and the outputs.  The sender and
+ * the receiver run one after the other on `stream`; the call launches only
+ * kernels (no second stream, no event, no hipMalloc, hipFree or memset; keep
+ * per-kernel tracing off).  DR_ECAPACITY, before anything is launched, if
+ * the configuration needs more scratch than the array holds: 64 MiB covers
+ * the round trip of gradients up to about one million elements.  Every call
+ * on one GPU shares that GPU's array, which keeps the last call's contents
+ * (each call clears what it needs cleared): calls that overlap on one GPU
+ * (other host threads, or other streams not ordered with this one) race. */
+#define DR_STATIC_SCRATCH_BYTES (64ull << 20)
+DR_EXPORT dr_status dr_roundtrip_static(const float *g, const dr_config *cfg_h, uint8_t *payload,
+                                        size_t payload_bytes, float *dense_out, uint32_t *idx_out, float *val_out,
+                                        uint64_t *counts_out, void *stream);
+
 /* ---------------------------------------------------------------------- */
 /* Per-kernel timing (the paper reports encode/decode wall time, Section   */
 /* 6.4; this breaks it down by kernel)                                     */

@@ -29,7 +29,7 @@ EXPORTS = [
     "dr_bloom_params", "dr_sigma_bits", "dr_workspace_bytes", "dr_last_error", "dr_sparsify_topr",
     "dr_bloom_encode", "dr_bloom_decode", "dr_curvefit_encode", "dr_curvefit_decode", "dr_payload_layout",
     "dr_payload_encode", "dr_payload_decode", "dr_payload_decode_sum", "dr_roundtrip", "dr_trace_begin",
-    "dr_trace_end", "dr_check_ranges",
+    "dr_trace_end", "dr_check_ranges", "dr_roundtrip_static",
 ]
 
 
@@ -91,6 +91,7 @@ def lib():
         "dr_trace_begin": (st, [vp]),
         "dr_trace_end": (st, [ctypes.c_char_p, sz]),
         "dr_check_ranges": (st, [cfgp, ctypes.POINTER(u64)]),
+        "dr_roundtrip_static": (st, [vp, cfgp, vp, sz, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -253,6 +254,13 @@ def roundtrip(g, cfg: Config, payload, dense_out, idx_out, val_out, counts_out, 
     _check("dr_roundtrip", lib().dr_roundtrip(
         _ptr(g), ctypes.byref(cfg.c), _ptr(payload), payload.numel(), _ptr(dense_out), _ptr(idx_out),
         _ptr(val_out), _ptr(counts_out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def roundtrip_static(g, cfg: Config, payload, dense_out, idx_out, val_out, counts_out, stream=None):
+    """dr_roundtrip with the library's static scratch instead of a workspace."""
+    _check("dr_roundtrip_static", lib().dr_roundtrip_static(
+        _ptr(g), ctypes.byref(cfg.c), _ptr(payload), payload.numel(), _ptr(dense_out), _ptr(idx_out),
+        _ptr(val_out), _ptr(counts_out), _stream(stream)))
 
 
 def trace_begin(stream=None):

@@ -735,6 +735,66 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     return decode_back(dd, s);
 }
 
+// ---------------------------------------------------------------------------
+// The round trip for callers that cannot allocate: its scratch is a static
+// device array of the library, one per GPU, held until the process ends.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[DR_STATIC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;       // guards the first lookup on each device
+void *g_scratch_ptr[64] = {};  // scratch's device address, per device
+
+// The device address of `scratch` on the current device, looked up once per
+// device (each GPU holds its own copy of the array).  In host code the
+// array's name is a host-side stand-in, never a device address.
+dr_status static_scratch(void **out) {
+    int dev = 0;
+    DR_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= 64) return fail(DR_ENOTSUP, "device %d: at most 64 devices", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return DR_OK;
+}
+
+// dr_roundtrip's sender then receiver, one after the other on `s`, in the
+// static scratch: no second stream, no event, no allocation.
+dr_status roundtrip_static_impl(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
+                                float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out,
+                                hipStream_t s) {
+    {
+        Plan p;
+        std::vector<uint64_t> rec_off;
+        dr_status st = plan_config(cfg, p, rec_off);
+        if (st != DR_OK) return st;
+        if (p.carve.bytes > DR_STATIC_SCRATCH_BYTES)
+            return fail(DR_ECAPACITY, "this gradient needs %zu bytes of scratch; the static scratch holds %zu "
+                        "(use dr_roundtrip with a workspace)", p.carve.bytes, (size_t)DR_STATIC_SCRATCH_BYTES);
+    }
+    void *ws = nullptr;
+    dr_status st = static_scratch(&ws);
+    if (st != DR_OK) return st;
+    Encode e;
+    st = encode_prepare(g, cfg, payload, payload_bytes, counts_out, ws, DR_STATIC_SCRATCH_BYTES, e);
+    if (st != DR_OK) return st;
+    Decode dd;
+    st = decode_prepare(payload, cfg, dense_out, idx_out, val_out, counts_out, ws, DR_STATIC_SCRATCH_BYTES, dd);
+    if (st != DR_OK) return st;
+    trace_call(s);
+    st = encode_front(e, g, counts_out, s);
+    if (st != DR_OK) return st;
+    st = encode_back(e, s);
+    if (st != DR_OK) return st;
+    st = decode_front(dd, 0xffffffffu, false, s);
+    if (st != DR_OK) return st;
+    return decode_back(dd, s);
+}
+
 dr_status decode_sum_impl(const uint8_t *const *payloads, uint32_t npay, const dr_config *cfg, float scale,
                           float *dense_out, uint64_t *counts_out, void *ws, size_t ws_bytes, hipStream_t s) {
     Plan p;
@@ -1144,6 +1204,13 @@ dr_status dr_roundtrip(const float *g, const dr_config *cfg_h, uint8_t *payload,
                        size_t ws_bytes, void *stream) {
     return roundtrip_impl(g, cfg_h, payload, payload_bytes, dense_out, idx_out, val_out, counts_out, ws, ws_bytes,
                           (hipStream_t)stream);
+}
+
+dr_status dr_roundtrip_static(const float *g, const dr_config *cfg_h, uint8_t *payload, size_t payload_bytes,
+                              float *dense_out, uint32_t *idx_out, float *val_out, uint64_t *counts_out,
+                              void *stream) {
+    return roundtrip_static_impl(g, cfg_h, payload, payload_bytes, dense_out, idx_out, val_out, counts_out,
+                                 (hipStream_t)stream);
 }
 
 dr_status dr_sparsify_topr(const float *g, uint64_t d, uint64_t r, uint32_t *idx_out, float *val_out,
