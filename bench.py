@@ -4,9 +4,12 @@ synthetic gradient per step, on one MI355X.
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
 Prints one JSON line.  `value` is Gelem/s of dense gradient (d / step time)
-with the inputs already in device memory; `hbm_frac` is the round trip's
-algorithmic bytes (read g, write and read the payload, write the dense
-gradient) per step time over the 8 TB/s HBM peak; `roofline` describes the
+with the inputs already in device memory; `ms_median`, `ms_p10` and `ms_p90`
+are over the timed steps; `hbm_frac` is the round trip's algorithmic bytes
+(read g, write and read the payload, write the dense gradient) per step
+time over the 8 TB/s HBM peak, and `hbm_frac_of_copy` the same over the
+bandwidth a plain 1 GiB device copy reaches on the same GPU
+(`copy_ceiling_GBps`, read plus written bytes); `roofline` describes the
 kernel that takes the largest share of the step, timed with HIP events on
 the library's stream; `cpu_baseline` times the CPU oracle on the same
 workload on one host core.
@@ -58,15 +61,16 @@ def kernel_models(d, payload_bytes, n_sel, n_val, k, fill):
     }
 
 
-def read_traffic(kernel, workload):
-    """HBM bytes per launch of `kernel` on `workload`, from the committed
-    rocprofv3 counter summary, if that summary was taken on the current
-    kernel sources; None otherwise."""
+def read_profile(kernel, workload):
+    """Counter figures of `kernel` on `workload` from the committed rocprofv3
+    summary (profiles/pmc_<kernel>_<workload>.txt): HBM bytes per launch and
+    the VALU-busy fraction, if that summary was taken on the current kernel
+    sources; {} otherwise."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", f"pmc_{_slug(kernel)}_{workload}.txt")
     if not os.path.exists(path):
-        return None
+        return {}
     fields = {}
     for line in open(path):
         if ":" in line and not line.startswith(" "):
@@ -75,9 +79,34 @@ def read_traffic(kernel, workload):
     h = hashlib.sha256()
     for f in sorted(os.listdir(os.path.join(ROOT, "paper_2102_03112_amd", "csrc"))):
         h.update(open(os.path.join(ROOT, "paper_2102_03112_amd", "csrc", f), "rb").read())
-    if fields.get("csrc_sha256") != h.hexdigest()[:16] or "traffic_bytes_per_launch" not in fields:
-        return None
-    return float(fields["traffic_bytes_per_launch"])
+    if fields.get("csrc_sha256") != h.hexdigest()[:16]:
+        return {}
+    out = {}
+    for key in ("traffic_bytes_per_launch", "valu_busy"):
+        if key in fields:
+            out[key] = float(fields[key])
+    return out
+
+
+def copy_ceiling(stream, n_bytes=1 << 30, reps=5):
+    """Achievable HBM bandwidth on this part: bytes read plus bytes written
+    per second by a plain 1 GiB device-to-device copy (best of `reps`)."""
+    import torch
+
+    x = torch.ones(n_bytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        y.copy_(x)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) * 1e-3)
+    del x, y
+    torch.cuda.empty_cache()
+    return 2.0 * n_bytes / best
 
 
 def _slug(kernel):
@@ -230,19 +259,21 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # timed region
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # timed region: an event between consecutive steps gives each step's time
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    ev0.record(stream)
+    evs[0].record(stream)
     for i in range(args.steps):
         step(i)
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms = ev0.elapsed_time(ev1) / args.steps
-    log(f"bench: {args.steps} steps, {ms:.4f} ms/step (wall {1e3 * wall / args.steps:.4f} ms/step)")
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    pct = lambda q: per[min(len(per) - 1, int(round(q * (len(per) - 1))))]
+    log(f"bench: {args.steps} steps, {ms:.4f} ms/step (median {pct(0.5):.4f}, p10 {pct(0.1):.4f}, "
+        f"p90 {pct(0.9):.4f}; wall {1e3 * wall / args.steps:.4f} ms/step)")
 
     # payload accounting from the records
     pay = payload.cpu().numpy()
@@ -285,7 +316,10 @@ def main():
         roof.update(bound=bound, achieved=round(ach, 1), peak=peak, unit="GB/s" if bound == "hbm" else "Gop/s",
                     frac=round(ach / peak, 4), work_per_launch=work, avg_launch_ms=round(kern[dom][1], 5),
                     launches_per_step=kern[dom][0] / args.steps)
-    roof["traffic"] = read_traffic(dom, w.name)
+    prof = read_profile(dom, w.name)
+    roof["traffic"] = prof.get("traffic_bytes_per_launch")
+    roof["valu_busy"] = prof.get("valu_busy")
+    ceiling = copy_ceiling(stream)
     log("bench: kernel ms per step: " + ", ".join(f"{k}={v:.4f}" for k, v in sorted(per_step.items(),
                                                                                       key=lambda x: -x[1])))
 
@@ -331,7 +365,12 @@ def main():
                    "segmentation": ["equal", "chord"][args.segmentation],
                    "fit_model": ["poly", "dexp"][args.fit_model],
                    "input_copies": n_copies},
+        "ms_median": round(pct(0.5), 5),
+        "ms_p10": round(pct(0.1), 5),
+        "ms_p90": round(pct(0.9), 5),
         "hbm_frac": round(b_alg / (ms * 1e-3) / HBM_PEAK, 4),
+        "copy_ceiling_GBps": round(ceiling / 1e9, 1),
+        "hbm_frac_of_copy": round(b_alg / (ms * 1e-3) / ceiling, 4),
         "bytes_alg": int(b_alg),
         "bits_per_elem": round(8.0 * used / d, 4),
         "bits_split": {"index": round(idx_bits / d, 4), "values": round(val_bits / d, 6),
