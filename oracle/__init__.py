@@ -34,6 +34,10 @@ SEG_EQUAL, SEG_CHORD = 0, 1
 MAX_SEG = 4096
 # value models (Section 5): polynomial, double exponential
 FIT_POLY, FIT_DEXP = 0, 1
+# filter layouts: every hash over the whole array, or hash j over part j of k
+LAYOUT_STANDARD, LAYOUT_PARTITIONED = 0, 1
+# the record header's hash id of each layout
+HASH_ID = {LAYOUT_STANDARD: 1, LAYOUT_PARTITIONED: 2}
 # where the sender takes the coded values (Section 4): the dense gradient g,
 # or the sparsified gradient (g on the selection, 0 elsewhere)
 VALUES_DENSE, VALUES_SPARSE = 0, 1
@@ -67,6 +71,10 @@ def _load():
         "drref_nonzero": (ctypes.c_int, [f32p, u64, u32p, u64, u64p]),
         "drref_bloom_encode": (ctypes.c_int, [u32p, u64, u64, u32, u32p]),
         "drref_bloom_query": (ctypes.c_int, [u32p, u64, u32, u64, u32p, u64, u64p]),
+        "drref_part_start": (u64, [u32, u64, u32]),
+        "drref_bloom_pos_layout_many": (None, [u32p, u64, u32, u64, u32, u32, u64p]),
+        "drref_bloom_encode_layout": (ctypes.c_int, [u32p, u64, u64, u32, u32, u32p]),
+        "drref_bloom_query_layout": (ctypes.c_int, [u32p, u64, u32, u32, u64, u32p, u64, u64p]),
         "drref_sort_desc": (ctypes.c_int, [f32p, u64, u32p]),
         "drref_lsq_fit": (ctypes.c_int, [f64p, f64p, u64, u32, f64p]),
         "drref_fit_shape": (None, [u64, u32, u32, u32p, u32p]),
@@ -123,13 +131,24 @@ def murmur3_32(data: bytes, seed: int) -> int:
     return int(lib.drref_murmur3_32(buf, len(data), seed & 0xFFFFFFFF))
 
 
-def bloom_pos(idx, j: int, m: int) -> np.ndarray:
-    """Bit positions h_j(i) * m >> 32 for an array of indices."""
+def bloom_pos(idx, j: int, m: int, k: int = 0, layout: int = LAYOUT_STANDARD) -> np.ndarray:
+    """Bit positions of hash j for an array of indices: h_j(i) * m >> 32
+    (standard layout), or floor(j m / k) + h_j(i) * q_j >> 32 within part j
+    of size q_j (partitioned layout; needs k)."""
     lib = _load()
     idx = np.ascontiguousarray(idx, dtype=np.uint32)
     out = np.empty(idx.size, dtype=np.uint64)
-    lib.drref_bloom_pos_many(_ptr(idx, ctypes.c_uint32), idx.size, j, m, _ptr(out, ctypes.c_uint64))
+    if layout == LAYOUT_STANDARD:
+        lib.drref_bloom_pos_many(_ptr(idx, ctypes.c_uint32), idx.size, j, m, _ptr(out, ctypes.c_uint64))
+    else:
+        lib.drref_bloom_pos_layout_many(_ptr(idx, ctypes.c_uint32), idx.size, j, m, k, layout,
+                                        _ptr(out, ctypes.c_uint64))
     return out
+
+
+def part_start(j: int, m: int, k: int) -> int:
+    """First bit of part j of a partitioned filter: floor(j m / k)."""
+    return int(_load().drref_part_start(j, m, k))
 
 
 def bloom_params(n: int, fpr: float) -> tuple[int, int]:
@@ -179,26 +198,34 @@ def nonzero(g: np.ndarray) -> np.ndarray:
 # --------------------------------------------------------------------------
 
 
-def bloom_encode(S: np.ndarray, m: int, k: int) -> np.ndarray:
+def bloom_encode(S: np.ndarray, m: int, k: int, layout: int = LAYOUT_STANDARD) -> np.ndarray:
     """m-bit filter (m/32 LSB-first u32 words) holding every index of S."""
     lib = _load()
     S = np.ascontiguousarray(S, dtype=np.uint32)
     words = np.zeros(m // 32, dtype=np.uint32)
-    _check(lib.drref_bloom_encode(_ptr(S, ctypes.c_uint32), S.size, m, k, _ptr(words, ctypes.c_uint32)), "bloom_encode")
+    if layout == LAYOUT_STANDARD:
+        st = lib.drref_bloom_encode(_ptr(S, ctypes.c_uint32), S.size, m, k, _ptr(words, ctypes.c_uint32))
+    else:
+        st = lib.drref_bloom_encode_layout(_ptr(S, ctypes.c_uint32), S.size, m, k, layout,
+                                           _ptr(words, ctypes.c_uint32))
+    _check(st, "bloom_encode")
     return words
 
 
-def bloom_query(words: np.ndarray, m: int, k: int, d: int) -> np.ndarray:
+def bloom_query(words: np.ndarray, m: int, k: int, d: int, layout: int = LAYOUT_STANDARD) -> np.ndarray:
     """Policy P0's set P: every i in [0, d) the filter reports, ascending."""
     lib = _load()
     words = np.ascontiguousarray(words, dtype=np.uint32)
     cap = max(d, 1)
     P = np.empty(cap, dtype=np.uint32)
     n = ctypes.c_uint64()
-    _check(
-        lib.drref_bloom_query(_ptr(words, ctypes.c_uint32), m, k, d, _ptr(P, ctypes.c_uint32), cap, ctypes.byref(n)),
-        "bloom_query",
-    )
+    if layout == LAYOUT_STANDARD:
+        st = lib.drref_bloom_query(_ptr(words, ctypes.c_uint32), m, k, d, _ptr(P, ctypes.c_uint32), cap,
+                                   ctypes.byref(n))
+    else:
+        st = lib.drref_bloom_query_layout(_ptr(words, ctypes.c_uint32), m, k, layout, d, _ptr(P, ctypes.c_uint32),
+                                          cap, ctypes.byref(n))
+    _check(st, "bloom_query")
     return P[: n.value].copy()
 
 
@@ -402,6 +429,7 @@ class TensorResult:
     seed: int = 0
     slots: np.ndarray | None = field(default=None)  # value number of each positive rank, or NO_SLOT
     value_source: int = VALUES_DENSE
+    layout: int = LAYOUT_STANDARD
 
     def payload_bits(self) -> dict:
         """Bits that cross the network (Figure 3's container): the filter, the
@@ -416,7 +444,8 @@ class TensorResult:
 
 def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
                      policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL,
-                     model: int = FIT_POLY, value_source: int = VALUES_DENSE) -> TensorResult:
+                     model: int = FIT_POLY, value_source: int = VALUES_DENSE,
+                     layout: int = LAYOUT_STANDARD) -> TensorResult:
     """Sender: top-r (or support) -> Bloom insert -> full-range query (P) ->
     the policy keeps all of P (P0) or r of it -> V = the gradient at the kept
     positives -> curve-fit encode.  Section 4 defines P0's values on the
@@ -425,13 +454,14 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     dense g when the sparsifier leaves it accessible (``VALUES_DENSE``).
     Receiver: the same query from the filter words -> the same policy ->
     curve-fit decode -> scatter into a dense gradient that is zero elsewhere
-    (Section 4's reconstruction).  ``r`` is an int or R_NONZERO."""
+    (Section 4's reconstruction).  ``layout`` is the filter layout (the
+    record's hash id tells the receiver).  ``r`` is an int or R_NONZERO."""
     g = np.ascontiguousarray(g, dtype=np.float32)
     d = g.size
     S = nonzero(g) if r == R_NONZERO else topr(g, int(r))
     m, k = bloom_params(S.size, fpr)
-    bits = bloom_encode(S, m, k)
-    P = bloom_query(bits, m, k, d)
+    bits = bloom_encode(S, m, k, layout)
+    P = bloom_query(bits, m, k, d, layout)
     slots, ncoded = policy_slots(P.size, S.size, policy, seed)
     kept = slots != NO_SLOT
     if value_source == VALUES_SPARSE:
@@ -445,7 +475,7 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     V[slots[kept].astype(np.int64)] = g_src[P[kept].astype(np.int64)]
     fit = curvefit_encode(V, degree, n_seg, seg_mode, model)
     # receiver: its own query and the same policy over its own positives
-    P_dec = bloom_query(bits, m, k, d)
+    P_dec = bloom_query(bits, m, k, d, layout)
     slots_dec, nc_dec = policy_slots(P_dec.size, ncoded, policy, seed)
     y = curvefit_decode_seg(fit.coef, fit.sigma, nc_dec, fit.degree, fit.bounds, fit.model)
     vals = np.zeros(P_dec.size, dtype=np.float32)
@@ -455,12 +485,12 @@ def roundtrip_tensor(g: np.ndarray, r, fpr: float, degree: int, n_seg: int, want
     if want_dense:
         dense = np.zeros(d, dtype=np.float32)
         dense[P_dec.astype(np.int64)] = vals
-    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense, policy, seed, slots, value_source)
+    return TensorResult(d, S, m, k, bits, P, V, fit, P_dec, vals, dense, policy, seed, slots, value_source, layout)
 
 
 def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int, want_dense: bool = True,
               policy: int = POLICY_P0, seed: int = 0, seg_mode: int = SEG_EQUAL, model: int = FIT_POLY,
-              value_source: int = VALUES_DENSE):
+              value_source: int = VALUES_DENSE, layout: int = LAYOUT_STANDARD):
     """Code every tensor g[offsets[t]:offsets[t+1]] independently on local
     indices.  ``ratio`` is (num, den) for top-r with r = ceil(d_t num / den),
     or None for the support of an inherently sparse gradient."""
@@ -469,7 +499,7 @@ def roundtrip(g: np.ndarray, offsets, ratio, fpr: float, degree: int, n_seg: int
         gt = g[offsets[t]: offsets[t + 1]]
         r = R_NONZERO if ratio is None else ratio_count(gt.size, ratio[0], ratio[1])
         out.append(roundtrip_tensor(gt, r, fpr, degree, n_seg, want_dense, policy, seed, seg_mode, model,
-                                    value_source))
+                                    value_source, layout))
     return out
 
 

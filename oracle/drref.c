@@ -101,6 +101,42 @@ void drref_bloom_pos_many(const uint32_t *idx, uint64_t n, uint32_t j, uint64_t 
         out[q] = drref_bloom_pos(idx[q], j, m);
 }
 
+/*
+ * Filter layouts.  STANDARD (0): every hash function addresses the whole
+ * m-bit array, as above.  PARTITIONED (1): the array is cut into k parts,
+ * part j covering bits [floor(j m / k), floor((j+1) m / k)), and hash
+ * function j addresses only part j: pos_j(i) = floor(j m / k) +
+ * floor(h_j(i) q_j / 2^32) with q_j the part's size.  Section 2 asks only for
+ * k independent hash functions into the m-bit array; in the partitioned
+ * array each part receives n insertions into about m/k bits, so a part's
+ * fill is about 1 - e^{-kn/m} and the false-positive rate about
+ * (1 - e^{-kn/m})^k, the same as Lemma 2 gives for the standard array.
+ * The same Murmur hash and seeds are used.  (The partitioned layout is the
+ * one a GPU can query with its first parts held in on-chip memory.)
+ */
+#define DRREF_LAYOUT_STANDARD 0u
+#define DRREF_LAYOUT_PARTITIONED 1u
+
+uint64_t drref_part_start(uint32_t j, uint64_t m, uint32_t k) { return (uint64_t)j * m / k; }
+
+uint64_t drref_bloom_pos_layout(uint32_t i, uint32_t j, uint64_t m, uint32_t k, uint32_t layout)
+{
+    if (layout == DRREF_LAYOUT_STANDARD)
+        return drref_bloom_pos(i, j, m);
+    uint64_t lo = drref_part_start(j, m, k), hi = drref_part_start(j + 1, m, k);
+    uint8_t le[4] = {(uint8_t)(i & 0xff), (uint8_t)((i >> 8) & 0xff), (uint8_t)((i >> 16) & 0xff),
+                     (uint8_t)((i >> 24) & 0xff)};
+    uint32_t h = drref_murmur3_32(le, 4, j);
+    return lo + (((uint64_t)h * (hi - lo)) >> 32);
+}
+
+void drref_bloom_pos_layout_many(const uint32_t *idx, uint64_t n, uint32_t j, uint64_t m, uint32_t k, uint32_t layout,
+                                 uint64_t *out)
+{
+    for (uint64_t q = 0; q < n; ++q)
+        out[q] = drref_bloom_pos_layout(idx[q], j, m, k, layout);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Bloom filter parameters (Lemma 2 and Remark 2, Section 10.2).             */
 /* ------------------------------------------------------------------------ */
@@ -237,24 +273,32 @@ int drref_nonzero(const float *g, uint64_t d, uint32_t *S_out, uint64_t cap, uin
 static int get_bit(const uint32_t *w, uint64_t p) { return (int)((w[p >> 5] >> (p & 31)) & 1u); }
 static void set_bit(uint32_t *w, uint64_t p) { w[p >> 5] |= 1u << (p & 31); }
 
-/* Insert every s in S: set bit h_j(s) for j = 0..k-1 (Section 2). */
-int drref_bloom_encode(const uint32_t *S, uint64_t n, uint64_t m, uint32_t k, uint32_t *words)
+/* Insert every s in S: set bit h_j(s) for j = 0..k-1 (Section 2), in the
+ * given layout. */
+int drref_bloom_encode_layout(const uint32_t *S, uint64_t n, uint64_t m, uint32_t k, uint32_t layout,
+                              uint32_t *words)
 {
-    if ((!S && n) || !words || m < 32 || (m & 31) || m >= ((uint64_t)1 << 32) || k < 1 || k > 32)
+    if ((!S && n) || !words || m < 32 || (m & 31) || m >= ((uint64_t)1 << 32) || k < 1 || k > 32 ||
+        layout > DRREF_LAYOUT_PARTITIONED)
         return DRREF_EINVAL;
     memset(words, 0, sizeof(uint32_t) * (m / 32));
     for (uint64_t q = 0; q < n; ++q)
         for (uint32_t j = 0; j < k; ++j)
-            set_bit(words, drref_bloom_pos(S[q], j, m));
+            set_bit(words, drref_bloom_pos_layout(S[q], j, m, k, layout));
     return DRREF_OK;
+}
+
+int drref_bloom_encode(const uint32_t *S, uint64_t n, uint64_t m, uint32_t k, uint32_t *words)
+{
+    return drref_bloom_encode_layout(S, n, m, k, DRREF_LAYOUT_STANDARD, words);
 }
 
 /* Membership: i is reported iff all k of its bits are set (Section 4,
  * "Implementation on GPUs and CPUs": the k looked-up bits sum to k). */
-static int bloom_member(const uint32_t *words, uint64_t m, uint32_t k, uint32_t i)
+static int bloom_member(const uint32_t *words, uint64_t m, uint32_t k, uint32_t layout, uint32_t i)
 {
     for (uint32_t j = 0; j < k; ++j)
-        if (!get_bit(words, drref_bloom_pos(i, j, m)))
+        if (!get_bit(words, drref_bloom_pos_layout(i, j, m, k, layout)))
             return 0;
     return 1;
 }
@@ -264,15 +308,15 @@ static int bloom_member(const uint32_t *words, uint64_t m, uint32_t k, uint32_t 
  * i of the gradient's index range in increasing order and collect the
  * positives, true and false, into P.  P is therefore ascending.
  */
-int drref_bloom_query(const uint32_t *words, uint64_t m, uint32_t k, uint64_t d, uint32_t *P_out,
-                      uint64_t cap, uint64_t *n_out)
+int drref_bloom_query_layout(const uint32_t *words, uint64_t m, uint32_t k, uint32_t layout, uint64_t d,
+                             uint32_t *P_out, uint64_t cap, uint64_t *n_out)
 {
     if (!words || !n_out || m < 32 || (m & 31) || m >= ((uint64_t)1 << 32) || k < 1 || k > 32 ||
-        d >= ((uint64_t)1 << 32))
+        d >= ((uint64_t)1 << 32) || layout > DRREF_LAYOUT_PARTITIONED)
         return DRREF_EINVAL;
     uint64_t n = 0;
     for (uint64_t i = 0; i < d; ++i) {
-        if (bloom_member(words, m, k, (uint32_t)i)) {
+        if (bloom_member(words, m, k, layout, (uint32_t)i)) {
             if (n < cap)
                 P_out[n] = (uint32_t)i;
             ++n;
@@ -280,6 +324,12 @@ int drref_bloom_query(const uint32_t *words, uint64_t m, uint32_t k, uint64_t d,
     }
     *n_out = n;
     return n > cap ? DRREF_ECAPACITY : DRREF_OK;
+}
+
+int drref_bloom_query(const uint32_t *words, uint64_t m, uint32_t k, uint64_t d, uint32_t *P_out,
+                      uint64_t cap, uint64_t *n_out)
+{
+    return drref_bloom_query_layout(words, m, k, DRREF_LAYOUT_STANDARD, d, P_out, cap, n_out);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -172,3 +172,86 @@ def test_empty_filter_and_full_filter():
     full = np.full(m // 32, 0xFFFFFFFF, dtype=np.uint32)
     np.testing.assert_array_equal(oracle.bloom_query(full, m, k, 1000), np.arange(1000, dtype=np.uint32))
     assert oracle.bloom_encode(np.zeros(0, dtype=np.uint32), m, k).sum() == 0
+
+
+# ---------------------------------------------------------------------------
+# the partitioned layout: hash function j addresses only part j of k
+# ---------------------------------------------------------------------------
+P_LAYOUT = oracle.LAYOUT_PARTITIONED
+
+
+@pytest.mark.parametrize("m,k", [(32, 10), (32, 32), (64, 3), (150_784, 10), (3_674_496, 10), (366_140_544, 13),
+                                 (2**32 - 32, 7)])
+def test_partitioned_parts_tile_the_array(m, k):
+    starts = [oracle.part_start(j, m, k) for j in range(k + 1)]
+    assert starts[0] == 0 and starts[-1] == m
+    sizes = np.diff(np.asarray(starts, dtype=np.int64))
+    assert sizes.min() >= m // k and sizes.max() <= -(-m // k) and sizes.sum() == m
+
+
+def test_partitioned_with_one_part_is_the_standard_map():
+    # k = 1: the single part is the whole array, so both layouts coincide
+    idx = np.random.default_rng(8).integers(0, 2**32, 5000, dtype=np.uint64).astype(np.uint32)
+    for m in (32, 150_784, 2**32 - 32):
+        np.testing.assert_array_equal(oracle.bloom_pos(idx, 0, m, 1, P_LAYOUT), oracle.bloom_pos(idx, 0, m))
+    S = workloads.random_indices(1 << 16, 900, seed=4)
+    np.testing.assert_array_equal(oracle.bloom_encode(S, 14_400, 1, P_LAYOUT), oracle.bloom_encode(S, 14_400, 1))
+
+
+def test_partitioned_hash_j_is_uniform_in_part_j():
+    m, k = 3_674_496, 10
+    idx = np.arange(200_000, dtype=np.uint32)
+    for j in range(k):
+        lo, hi = oracle.part_start(j, m, k), oracle.part_start(j + 1, m, k)
+        p = oracle.bloom_pos(idx, j, m, k, P_LAYOUT).astype(np.int64)
+        assert p.min() >= lo and p.max() < hi
+        # uniform over 16 equal sub-ranges of the part (chi-square, 15 dof)
+        c = np.bincount((p - lo) * 16 // (hi - lo), minlength=16)
+        e = idx.size / 16
+        assert ((c - e) ** 2 / e).sum() < 50
+
+
+def test_partitioned_item_sets_one_bit_per_part():
+    m, k = 150_784, 10
+    starts = [oracle.part_start(j, m, k) for j in range(k + 1)]
+    for s in (0, 1, 12345, 2**32 - 1):
+        bits = np.unpackbits(oracle.bloom_encode(np.array([s], np.uint32), m, k, P_LAYOUT).view(np.uint8),
+                             bitorder="little")
+        assert [int(bits[starts[j]:starts[j + 1]].sum()) for j in range(k)] == [1] * k
+
+
+def test_partitioned_query_no_false_negatives_brute_force_and_order_independence():
+    d = 20_000
+    S = workloads.random_indices(d, 400, seed=6)
+    m, k = oracle.bloom_params(S.size, 1e-2)
+    words = oracle.bloom_encode(S, m, k, P_LAYOUT)
+    shuffled = np.random.default_rng(1).permutation(S)
+    np.testing.assert_array_equal(oracle.bloom_encode(shuffled, m, k, P_LAYOUT), words)
+    P = oracle.bloom_query(words, m, k, d, P_LAYOUT)
+    assert np.isin(S, P).all()
+    bits = np.unpackbits(words.view(np.uint8), bitorder="little").astype(bool)
+    all_i = np.arange(d, dtype=np.uint32)
+    member = np.ones(d, bool)
+    for j in range(k):
+        member &= bits[oracle.bloom_pos(all_i, j, m, k, P_LAYOUT).astype(np.int64)]
+    np.testing.assert_array_equal(P, np.flatnonzero(member).astype(np.uint32))
+    # differs from the standard layout's filter
+    assert not np.array_equal(words, oracle.bloom_encode(S, m, k))
+
+
+def test_partitioned_false_positive_rate_matches_lemma2():
+    d = 1 << 20
+    S = workloads.random_indices(d, 10_486, seed=14)
+    m, k = oracle.bloom_params(S.size, 1e-3)
+    words = oracle.bloom_encode(S, m, k, P_LAYOUT)
+    P = oracle.bloom_query(words, m, k, d, P_LAYOUT)
+    fp = P.size - S.size
+    nonmembers = d - S.size
+    bits = np.unpackbits(words.view(np.uint8), bitorder="little")
+    starts = [oracle.part_start(j, m, k) for j in range(k + 1)]
+    # conditional on the parts' fills, a non-member is positive with the
+    # product of the fills
+    q = float(np.prod([bits[starts[j]:starts[j + 1]].mean() for j in range(k)]))
+    assert abs(fp - q * nonmembers) < 5 * math.sqrt(nonmembers * q * (1 - q))
+    eps = (1 - math.exp(-k * S.size / m)) ** k
+    assert abs(fp / nonmembers - eps) / eps < 0.15

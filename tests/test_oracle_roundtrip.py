@@ -142,3 +142,13 @@ def test_value_source_sparse_equals_dense_on_support():
     b, = oracle.roundtrip(g, [0, g.size], None, 1e-2, 3, 16, value_source=oracle.VALUES_DENSE)
     np.testing.assert_array_equal(a.V, b.V)
     np.testing.assert_array_equal(a.dense, b.dense)
+
+
+def test_partitioned_layout_round_trip():
+    """The round trip with the partitioned filter layout: the same
+    properties as with the standard one, and a filter of the same size."""
+    g = workloads.normal(36_864, seed=9)
+    (res,) = oracle.roundtrip(g, [0, g.size], (1, 100), 1e-3, 5, 8, layout=oracle.LAYOUT_PARTITIONED)
+    _check_tensor(res, g, 369)
+    assert res.layout == oracle.LAYOUT_PARTITIONED
+    assert (res.m, res.k) == oracle.bloom_params(369, 1e-3)
