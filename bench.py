@@ -203,6 +203,10 @@ def main():
     ap.add_argument("--fit-model", type=int, default=0, help="0 = polynomial, 1 = double exponential")
     ap.add_argument("--n-seg", type=int, default=None, help="runs per tensor (0 = heuristic); default: the "
                                                             "workload's")
+    ap.add_argument("--layout", type=int, default=0, help="filter layout: 0 = standard (every hash over the whole "
+                                                          "array), 1 = partitioned (hash j over part j of k)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip timing the partitioned filter layout beside the standard one")
     ap.add_argument("--decode-sum", type=int, default=0, metavar="N",
                     help="instead: time the summing receiver over N payloads of the workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -240,7 +244,8 @@ def main():
     g_host = W.generate(w)
     log(f"bench: generated input in {time.time() - t0:.1f}s sha256={W.sha256(g_host)[:16]}")
 
-    cfg = B.Config.from_workload(w, args.policy, args.policy_seed, args.segmentation, args.n_seg, args.fit_model)
+    cfg = B.Config.from_workload(w, args.policy, args.policy_seed, args.segmentation, args.n_seg, args.fit_model,
+                                 filter_layout=args.layout)
     total, rec_off = B.payload_layout(cfg)
     n_copies = max(1, min(64, math.ceil(3 * MALL_BYTES / max(1, 4 * d)))) if 4 * d < 2 * MALL_BYTES else 1
     g_dev = [torch.from_numpy(g_host).cuda()]
@@ -323,6 +328,42 @@ def main():
     log("bench: kernel ms per step: " + ", ".join(f"{k}={v:.4f}" for k, v in sorted(per_step.items(),
                                                                                       key=lambda x: -x[1])))
 
+    # the other filter layout on the same input, timed the same way (a
+    # variant beside the headline figure, not the headline)
+    variants = {}
+    if not args.no_variants and args.layout == 0:
+        cfg_p = B.Config.from_workload(w, args.policy, args.policy_seed, args.segmentation, args.n_seg, args.fit_model,
+                                       filter_layout=1)
+
+        def step_p(i):
+            B.roundtrip(g_dev[i % n_copies], cfg_p, payload, dense, None, None, counts, ws, stream)
+
+        for i in range(args.warmup):
+            step_p(i)
+        torch.cuda.synchronize()
+        pe = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        pe[0].record(stream)
+        for i in range(args.steps):
+            step_p(i)
+            pe[i + 1].record(stream)
+        torch.cuda.synchronize()
+        ms_p = pe[0].elapsed_time(pe[-1]) / args.steps
+        per_p = sorted(pe[i].elapsed_time(pe[i + 1]) for i in range(args.steps))
+        B.trace_begin(stream)
+        for i in range(args.steps):
+            step_p(i)
+        trp = {name: tot / args.steps for name, (cnt_, tot) in B.trace_end().items()}
+        cp = counts.cpu().numpy().reshape(w.n_tensors, 4)
+        variants["filter_layout_partitioned"] = {
+            "ms_per_step": round(ms_p, 5), "ms_median": round(per_p[len(per_p) // 2], 5),
+            "value": round(d / (ms_p * 1e-3) / 1e9, 4), "unit": "Gelem/s",
+            "hbm_frac": round(b_alg / (ms_p * 1e-3) / HBM_PEAK, 4),
+            "flags": int(np.bitwise_or.reduce(cp[:, 3])) if w.n_tensors else 0,
+            "positives": int(cp[:, 1].sum()),
+            "kernels_ms_per_step": {k: round(v, 5) for k, v in trp.items()},
+        }
+        log(f"bench: partitioned filter layout {ms_p:.4f} ms/step")
+
     # CPU oracle baseline on one host core
     cpu = None
     if not args.no_cpu_baseline:
@@ -364,6 +405,7 @@ def main():
                    "degree": w.degree, "n_seg": cfg.n_seg, "policy": POLICY_NAMES[args.policy],
                    "segmentation": ["equal", "chord"][args.segmentation],
                    "fit_model": ["poly", "dexp"][args.fit_model],
+                   "filter_layout": ["standard", "partitioned"][args.layout],
                    "input_copies": n_copies},
         "ms_median": round(pct(0.5), 5),
         "ms_p10": round(pct(0.1), 5),
@@ -380,6 +422,7 @@ def main():
         "flags": flags,
         "roofline": roof,
         "kernels_ms_per_step": {k: round(v, 5) for k, v in per_step.items()},
+        "variants": variants,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

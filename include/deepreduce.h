@@ -129,6 +129,19 @@ typedef enum {
 #define DR_VALUES_DENSE 0u
 #define DR_VALUES_SPARSE 1u
 
+/* Filter layouts (the position map of the k hash functions; Section 2 asks
+ * only for k independent hash functions into the m-bit array).  STANDARD
+ * (record hash id 1): bit floor(h_j(i) m / 2^32) for every j.  PARTITIONED
+ * (record hash id 2): the array is cut into k parts, part j covering bits
+ * [floor(j m / k), floor((j+1) m / k)), and hash j sets bit floor(j m / k) +
+ * floor(h_j(i) q_j / 2^32) of its part (q_j bits).  Same m, k, hash and
+ * seeds; each part's fill is about 1 - e^{-kn/m}, so the false-positive rate
+ * is Lemma 2's (1 - e^{-kn/m})^k as for the standard layout.  The receiver
+ * takes the layout from each record.  The query of a partitioned filter
+ * reads its first parts, those of the first probes, from on-chip memory. */
+#define DR_FILTER_STANDARD 0u
+#define DR_FILTER_PARTITIONED 1u
+
 /* Bits of the per-tensor flags word (slot 3 of counts_out). */
 #define DR_FLAG_NONFINITE 1u    /* the tensor held NaN or Inf */
 #define DR_FLAG_DEC_MISMATCH 2u /* receiver: the record is invalid, or its |P| differs from the header */
@@ -269,6 +282,7 @@ struct dr_config {
     uint32_t segmentation;     /* DR_SEG_EQUAL or DR_SEG_CHORD                                   */
     uint32_t fit_model;        /* DR_FIT_POLY or DR_FIT_DEXP                                     */
     uint32_t value_source;     /* DR_VALUES_DENSE or DR_VALUES_SPARSE                            */
+    uint32_t filter_layout;    /* DR_FILTER_STANDARD or DR_FILTER_PARTITIONED                    */
 };
 
 /* Payload container (Figure 3's "container"): one record per tensor at byte
@@ -279,7 +293,8 @@ struct dr_config {
  * reorder map, each section padded to 4 bytes and packed back to back.
  * Header layout: 16 little-endian u32 words: magic 0x31435244 ("DRC1"),
  * header bytes (64), d, n_selected, n_positives (|P|), n_values (values
- * coded: |P| under P0), m_bits, k, hash id (1 = MurmurHash3_x86_32), policy,
+ * coded: |P| under P0), m_bits, k, hash id (MurmurHash3_x86_32 with seeds
+ * 0..k-1; 1 = standard filter layout, 2 = partitioned), policy,
  * seed, D_eff, S_eff, sigma bits, record bytes (header + sections; what
  * would be sent), segmentation (DR_SEG_*) | value model (DR_FIT_*) << 8 |
  * value source (DR_VALUES_*) << 16.

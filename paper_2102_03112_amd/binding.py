@@ -22,6 +22,7 @@ DR_OK, DR_EINVAL, DR_ECAPACITY, DR_EDEVICE, DR_ENOTSUP = 0, -1, -2, -3, -4
 R_NONZERO = (1 << 64) - 1
 FLAG_NONFINITE, FLAG_DEC_MISMATCH, FLAG_COUNT, FLAG_CAPACITY, FLAG_STALLED = 1, 2, 4, 8, 16
 VALUES_DENSE, VALUES_SPARSE = 0, 1
+FILTER_STANDARD, FILTER_PARTITIONED = 0, 1
 HEADER_BYTES = 64
 HEADER_MAGIC = 0x31435244
 
@@ -53,6 +54,7 @@ class DrConfig(ctypes.Structure):
         ("segmentation", ctypes.c_uint32),
         ("fit_model", ctypes.c_uint32),
         ("value_source", ctypes.c_uint32),
+        ("filter_layout", ctypes.c_uint32),
     ]
 
 
@@ -189,15 +191,17 @@ class Config:
     """A dr_config together with the host offsets array it points to."""
 
     def __init__(self, offsets, ratio, fpr: float, degree: int, n_seg: int, policy: int = 0, seed: int = 0,
-                 segmentation: int = 0, fit_model: int = 0, value_source: int = VALUES_DENSE):
+                 segmentation: int = 0, fit_model: int = 0, value_source: int = VALUES_DENSE,
+                 filter_layout: int = FILTER_STANDARD):
         self.offsets = np.ascontiguousarray(np.asarray(offsets, dtype=np.uint64))
         self._off_c = (ctypes.c_uint64 * self.offsets.size)(*[int(x) for x in self.offsets])
         num, den = (R_NONZERO, 1) if ratio is None else ratio
         self.c = DrConfig(self.offsets.size - 1, self._off_c, num, den, fpr, degree, n_seg, policy, seed,
-                          segmentation, fit_model, value_source)
+                          segmentation, fit_model, value_source, filter_layout)
         self.ratio, self.fpr, self.degree, self.n_seg = ratio, fpr, degree, n_seg
         self.policy, self.seed, self.segmentation, self.fit_model = policy, seed, segmentation, fit_model
         self.value_source = value_source
+        self.filter_layout = filter_layout
 
     @property
     def n_tensors(self) -> int:
@@ -209,9 +213,9 @@ class Config:
 
     @classmethod
     def from_workload(cls, w, policy: int = 0, seed: int = 0, segmentation: int = 0, n_seg=None, fit_model: int = 0,
-                      value_source: int = VALUES_DENSE):
+                      value_source: int = VALUES_DENSE, filter_layout: int = FILTER_STANDARD):
         return cls(w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg if n_seg is None else n_seg, policy, seed,
-                   segmentation, fit_model, value_source)
+                   segmentation, fit_model, value_source, filter_layout)
 
 
 def check_ranges(cfg: Config) -> tuple[int, str]:

@@ -25,6 +25,7 @@ static_assert(POLICY_P0 == DR_POLICY_P0 && POLICY_RANDOM == DR_POLICY_RANDOM && 
 static_assert(SEG_EQUAL == DR_SEG_EQUAL && SEG_CHORD == DR_SEG_CHORD, "segmentation ids");
 static_assert(FIT_POLY == DR_FIT_POLY && FIT_DEXP == DR_FIT_DEXP, "value model ids");
 static_assert(VALUES_DENSE == DR_VALUES_DENSE && VALUES_SPARSE == DR_VALUES_SPARSE, "value source ids");
+static_assert(LAYOUT_STANDARD == DR_FILTER_STANDARD && LAYOUT_PARTITIONED == DR_FILTER_PARTITIONED, "filter layouts");
 static_assert(MAX_SEG == DR_MAX_SEGMENTS && MAX_DEG == DR_MAX_DEGREE, "limits of the header and the kernels");
 
 namespace {
@@ -340,6 +341,8 @@ dr_status check_cfg(const dr_config *cfg) {
     if (cfg->fit_model > DR_FIT_DEXP) return fail(DR_EINVAL, "unknown value model %u", cfg->fit_model);
     if (cfg->policy > DR_POLICY_RIGHTMOST) return fail(DR_EINVAL, "unknown index policy %u", cfg->policy);
     if (cfg->value_source > DR_VALUES_SPARSE) return fail(DR_EINVAL, "unknown value source %u", cfg->value_source);
+    if (cfg->filter_layout > DR_FILTER_PARTITIONED)
+        return fail(DR_EINVAL, "unknown filter layout %u", cfg->filter_layout);
     return DR_OK;
 }
 
@@ -411,6 +414,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         in.seed = cfg->seed;
         in.seg_mode = cfg->segmentation;
         in.value_src = cfg->value_source;
+        in.layout = cfg->filter_layout;
         in.mC = mC;
         // top-r: |S| = r is known, so the filter size is too
         in.m_words_in = nz ? 0u : (uint32_t)(m_cap / 32);
@@ -545,7 +549,6 @@ dr_status encode_back(Encode &e, hipStream_t s) {
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     if (p.segment) DR_HIP(launch_segment(w, p.seg_grid_req, p.seg_block_pass, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
-    DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;
 }
 
@@ -1325,7 +1328,6 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
     DR_HIP(launch_value_setup(w, false, nullptr, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
-    DR_HIP(launch_sigma_pack(w, persist_grid(4), s));
     return DR_OK;
 }
 

@@ -96,13 +96,17 @@ __global__ __launch_bounds__(BL_THREADS) void k_bloom_count(Work w, uint32_t j0,
     const uint32_t m_bits = td.m_words * 32u;
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
+    __shared__ uint32_t ps[33];
+    const bool part = td.in.layout == LAYOUT_PARTITIONED;
+    if (part) fill_part_starts(ps, m_bits, td.in.k);
+    const PosMap pm{m_bits, part ? ps : nullptr};
     for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) lh[s] = 0;
     __syncthreads();
     const uint32_t je = min(j1, td.in.k);
     if (je > j0) {
         for_chunk_items<FROM_BITMAP, BL_THREADS>(w, td, c, [&](uint32_t x) {
             const uint32_t km = mm3_key(x);
-            for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[bloom_pos(km, j, m_bits) >> sl2], 1u);
+            for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[pm(km, j) >> sl2], 1u);
         });
     }
     __syncthreads();
@@ -188,6 +192,10 @@ __global__ __launch_bounds__(BL_THREADS) void k_bloom_scatter(Work w, uint32_t j
     const uint32_t je = min(j1, td.in.k);
     if (je <= j0) return;
     const uint32_t m_bits = td.m_words * 32u;
+    __shared__ uint32_t ps[33];
+    const bool part = td.in.layout == LAYOUT_PARTITIONED;
+    if (part) fill_part_starts(ps, m_bits, td.in.k);  // read after the barrier below
+    const PosMap pm{m_bits, part ? ps : nullptr};
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
     if (nsl > BL_MAX_SLICES) {  // excluded by the plan
@@ -267,7 +275,7 @@ __global__ __launch_bounds__(BL_THREADS) void k_bloom_scatter(Work w, uint32_t j
                     br[q] = 0xffffffffu;
                     pr[q] = 0;
                     if (iv && jg + v < je) {
-                        const uint32_t p = bloom_pos(km[u], jg + v, m_bits);
+                        const uint32_t p = pm(km[u], jg + v);
                         const uint32_t b = p >> sl2;
                         br[q] = (b << 16) | atomicAdd(&cnt[b], 1u);
                         pr[q] = p & mask;
@@ -403,12 +411,24 @@ __global__ __launch_bounds__(DIR_THREADS) void k_bloom_direct(Work w) {
     const uint32_t nw = min(DIR_SLICE_WORDS, m_words - w0);
     const uint32_t b0 = w0 * 32u, nb = nw * 32u;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
+    __shared__ uint32_t ps[33];
+    const bool parts = td.in.layout == LAYOUT_PARTITIONED;
+    if (parts) fill_part_starts(ps, m_bits, k);
+    const PosMap pm{m_bits, parts ? ps : nullptr};
     for (uint32_t i = threadIdx.x; i < DIR_SLICE_WORDS / 4; i += DIR_THREADS) ((uint4 *)sl)[i] = make_uint4(0, 0, 0, 0);
     __syncthreads();
+    // the hashes that can land in this slice: all, or (partitioned) those
+    // whose part meets [b0, b0 + nb)
+    uint32_t jlo = 0, jhi = k;
+    if (parts) {
+        while (jlo < k && ps[jlo + 1] <= b0) ++jlo;
+        jhi = jlo;
+        while (jhi < k && ps[jhi] < b0 + nb) ++jhi;
+    }
     auto add = [&](uint32_t x) {
         const uint32_t km = mm3_key(x);
-        for (uint32_t j = 0; j < k; ++j) {
-            const uint32_t p = bloom_pos(km, j, m_bits) - b0;  // wraps for positions below the slice
+        for (uint32_t j = jlo; j < jhi; ++j) {
+            const uint32_t p = pm(km, j) - b0;  // wraps for positions below the slice
             if (p < nb) atomicOr(&sl[p >> 5], 1u << (p & 31u));
         }
     };
@@ -571,6 +591,7 @@ struct RecordView {
     const uint32_t *knots;  // chord segmentation: the seff - 1 interior run starts
     const uint32_t *sigma;
     uint32_t m_bits, k, npos, nv, policy, seed, deff, seff, b, segmode, model;
+    uint32_t layout;  // LAYOUT_* of the filter (from the record's hash id)
 };
 
 // Reads a record header and checks it against the record's capacity and
@@ -586,6 +607,8 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     v.policy = h[H_POLICY];
     v.seed = h[H_SEED];
     v.k = h[H_K];
+    const uint32_t hash_id = h[H_HASH];
+    v.layout = hash_id == HASH_ID_PARTITIONED ? LAYOUT_PARTITIONED : LAYOUT_STANDARD;
     v.deff = h[H_DEFF];
     v.seff = h[H_SEFF];
     v.b = h[H_B];
@@ -600,6 +623,7 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
     const uint64_t need = (uint64_t)HDR_BYTES + m_bits / 8u + 4ull * v.seff * (v.deff + 1ull) + 4ull * nknots +
                           4ull * (((uint64_t)v.nv * v.b + 31u) / 32u);
     *ok = h[H_MAGIC] == HDR_MAGIC && h[H_BYTES] == HDR_BYTES && m_bits >= 32 && (m_bits & 31u) == 0 && v.k >= 1 &&
+          (hash_id == HASH_ID_STANDARD || hash_id == HASH_ID_PARTITIONED) &&
           v.k <= 32 && v.deff <= MAX_DEG && v.b >= 1 && v.b <= 32 && v.npos <= d && v.nv <= v.npos &&
           v.policy <= POLICY_RIGHTMOST && (v.policy != POLICY_P0 || v.nv == v.npos) && v.segmode <= SEG_CHORD &&
           (hw15 >> 24) == 0 && vsrc <= VALUES_SPARSE && v.model <= FIT_DEXP && (v.model != FIT_DEXP || v.deff == 3) &&
@@ -607,6 +631,7 @@ __device__ __forceinline__ RecordView read_record(const uint8_t *rec, uint64_t c
           need <= cap;
     if (!*ok) {  // nothing of an invalid record is read past its first filter word
         v.k = 0;
+        v.layout = LAYOUT_STANDARD;
         v.npos = 0;
         v.nv = 0;
         v.policy = POLICY_P0;
@@ -648,6 +673,7 @@ __device__ __forceinline__ RecordView query_filter(const Work &w, const QueryOut
         rv.bits = td.in.bits;
         rv.m_bits = td.m_words * 32u;
         rv.k = td.in.k;
+        rv.layout = td.in.layout;
     }
     return rv;
 }
@@ -841,6 +867,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
     __shared__ uint32_t lw[PB_WAVES][QWAVE / 32];
     __shared__ uint32_t tcl[RUN_TILES];
     __shared__ uint32_t next;
+    __shared__ uint32_t ps[33];  // part starts of a partitioned filter
     // the wave index is uniform across the wave; saying so keeps everything
     // derived from it in scalar registers
     const uint32_t lane = threadIdx.x & 63u, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -859,6 +886,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         if (t != cached) {
             fcw = min(rv.m_bits / 32u, FC_WORDS);
             for (uint32_t x = threadIdx.x; x < fcw; x += PB_THREADS) fc[x] = rv.bits[x];
+            if (rv.layout == LAYOUT_PARTITIONED) fill_part_starts(ps, rv.m_bits, rv.k);
             cached = t;
         }
         for (uint32_t x = threadIdx.x; x < re - rb; x += PB_THREADS) tcl[x] = 0;
@@ -872,6 +900,9 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         __syncthreads();
         const uint32_t m_bits = rv.m_bits, k = rv.k, d = td.in.d;
         const __amdgpu_buffer_rsrc_t bits = buffer_view(rv.bits, m_bits / 8u);
+        // with the partitioned layout the first parts, those of the first
+        // probes, are the ones held in LDS
+        const PosMap pm{m_bits, rv.layout == LAYOUT_PARTITIONED ? ps : nullptr};
         uint16_t *me = qe[wv];
         uint32_t *mw = lw[wv];
         for (;;) {
@@ -904,7 +935,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 #pragma unroll
             for (uint32_t c = 0; c < QWAVE / 64; ++c) {
                 const uint32_t i = wbase + c * 64 + lane;
-                const uint32_t p = bloom_pos(mm3_key(i), 0, m_bits);
+                const uint32_t p = pm(mm3_key(i), 0);
                 // p < m_bits always, so the read is in bounds; i past the
                 // tensor's end stays inside its slot and is masked below
                 const uint32_t word = filter_word(fc, fcw, bits, p >> 5) >> (p & 31u);
@@ -946,7 +977,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 #pragma unroll
                     for (uint32_t u = 0; u < TAIL_PROBES; ++u) {
                         if (u < S) {
-                            const uint32_t p = bloom_pos(key, j + u, m_bits);
+                            const uint32_t p = pm(key, j + u);
                             all &= filter_word(fc, fcw, bits, p >> 5, act) >> (p & 31u);
                         }
                     }
@@ -971,7 +1002,7 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
                     for (uint32_t u = 0; u < G; ++u) {
                         if (b0 + u * 64 >= L) break;  // this group and the ones after it are empty
                         const bool live = b0 + u * 64 + lane < L;
-                        const uint32_t p = bloom_pos(mm3_key(wbase + ev[u]), j, m_bits);
+                        const uint32_t p = pm(mm3_key(wbase + ev[u]), j);
                         const uint32_t word = filter_word(fc, fcw, bits, p >> 5, live) >> (p & 31u);
                         bw[u] = live ? word : 0u;
                     }

@@ -53,6 +53,10 @@ constexpr uint32_t SEG_EQUAL = 0, SEG_CHORD = 1;
 constexpr uint32_t FIT_POLY = 0, FIT_DEXP = 1;
 // where the sender's coded values come from (Section 4): g, or g~ (0 off S)
 constexpr uint32_t VALUES_DENSE = 0, VALUES_SPARSE = 1;
+// filter layouts: each hash over the whole array, or hash j over part j of k;
+// a record's hash id names the layout
+constexpr uint32_t LAYOUT_STANDARD = 0, LAYOUT_PARTITIONED = 1;
+constexpr uint32_t HASH_ID_STANDARD = 1, HASH_ID_PARTITIONED = 2;
 constexpr uint32_t NMOM = 3 * MAX_DEG + 2;    // 2D+1 power sums + D+1 right-hand sides (room for D=7)
 constexpr uint32_t HDR_BYTES = 64;
 // payload record header: sixteen little-endian u32 words
@@ -110,7 +114,7 @@ struct TInit {
     uint32_t bnd0;       // chord segmentation: first segment-start entry of this tensor
     uint32_t seg_slot;   // chord segmentation over the whole grid: the tensor's state, or NO_SEG_SLOT
     uint32_t value_src;  // VALUES_DENSE or VALUES_SPARSE
-    uint32_t pad_;
+    uint32_t layout;     // LAYOUT_STANDARD or LAYOUT_PARTITIONED
 };
 
 // Chord segmentation over the whole grid (at most SEG_GRID_RUNS runs per
@@ -262,6 +266,28 @@ __device__ __forceinline__ uint32_t bloom_pos(uint32_t kmix, uint32_t j, uint32_
 }
 
 __device__ __forceinline__ uint32_t test_bit(const uint32_t *w, uint32_t p) { return (w[p >> 5] >> (p & 31u)) & 1u; }
+
+// Bit positions of a filter in its layout.  Standard: hash j over the whole
+// m-bit array.  Partitioned: part j covers [ps[j], ps[j+1]), ps[j] =
+// floor(j m / k), and hash j maps into it by the same multiply-shift.
+struct PosMap {
+    uint32_t m_bits;
+    const uint32_t *ps;  // the k + 1 part starts (LDS) of a partitioned filter, else null
+    __device__ __forceinline__ uint32_t operator()(uint32_t kmix, uint32_t j) const {
+        const uint32_t h = mm3_seed(kmix, j);
+        if (ps) {
+            const uint32_t a = ps[j];
+            return a + __umulhi(h, ps[j + 1] - a);
+        }
+        return __umulhi(h, m_bits);
+    }
+};
+
+// Part starts floor(j m / k), j = 0..k, written by threads 0..k of the
+// block (the caller synchronises before use).
+__device__ __forceinline__ void fill_part_starts(uint32_t *ps, uint32_t m_bits, uint32_t k) {
+    if (threadIdx.x <= k && k > 0) ps[threadIdx.x] = (uint32_t)(((uint64_t)threadIdx.x * m_bits) / k);
+}
 
 // ---------------------------------------------------------------------------
 // Block barrier for LDS traffic only: waits for this wave's LDS operations,

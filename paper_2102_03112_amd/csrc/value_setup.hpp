@@ -60,7 +60,8 @@ __device__ inline void value_setup_tensor(const Work &w, uint32_t t, int payload
         h[H_NVAL] = nv;
         h[H_MBITS] = td.m_words * 32u;
         h[H_K] = td.in.k;
-        h[H_HASH] = 1u;  // MurmurHash3_x86_32, seeds 0..k-1
+        // MurmurHash3_x86_32, seeds 0..k-1, over the whole array or per part
+        h[H_HASH] = td.in.layout == LAYOUT_PARTITIONED ? HASH_ID_PARTITIONED : HASH_ID_STANDARD;
         h[H_POLICY] = td.in.policy;
         h[H_SEED] = td.in.seed;
         h[H_DEFF] = deff;

@@ -949,8 +949,16 @@ __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, u
 
 __device__ void solve_run(const TDesc &td, uint32_t s, const double *mom);
 
-// Moments of one chunk of one run.
-__global__ __launch_bounds__(FIT_THREADS) void k_fit_moments(Work w) {
+__device__ void pack_sigma_words(const Work &w, uint32_t first, uint32_t stride);
+
+// Moments of one chunk of one run (blocks [0, fit_blocks)); the blocks
+// after them pack the reorder map, which needs only the sort.
+__global__ __launch_bounds__(FIT_THREADS) void k_fit_moments(Work w, uint32_t fit_blocks) {
+    if (blockIdx.x >= fit_blocks) {
+        pack_sigma_words(w, (blockIdx.x - fit_blocks) * FIT_THREADS + threadIdx.x,
+                         (gridDim.x - fit_blocks) * FIT_THREADS);
+        return;
+    }
     const uint32_t t = tensor_of_fit_block(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t local = blockIdx.x - td.in.fit_blk0;
@@ -1363,9 +1371,11 @@ __global__ __launch_bounds__(DEXP_THREADS) void k_dexp_pass(Work w, uint32_t pas
 }
 
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s) {
-    if (fit_blocks == 0) return hipSuccess;
-    k_fit_moments<<<fit_blocks, FIT_THREADS, 0, s>>>(w);
+    // the fit's chunk blocks, then PACK_BLOCKS packing the reorder maps
+    constexpr uint32_t PACK_BLOCKS = 32;
+    k_fit_moments<<<fit_blocks + PACK_BLOCKS, FIT_THREADS, 0, s>>>(w, fit_blocks);
     trace_mark(s, "k_fit_moments");
+    if (fit_blocks == 0) return hipGetLastError();
     k_fit_solve<<<fit_blocks / FIT_CHUNKS, 64, 0, s>>>(w);
     trace_mark(s, "k_fit_solve");
     if (dexp) {
@@ -1392,9 +1402,10 @@ __device__ __forceinline__ uint32_t tensor_of_sword(const Work &w, uint32_t g) {
     return lo;
 }
 
-__global__ __launch_bounds__(NTHREADS) void k_sigma_pack(Work w) {
+// Words first, first + stride, ... of the reorder maps of all tensors.
+__device__ void pack_sigma_words(const Work &w, uint32_t first, uint32_t stride) {
     const uint32_t total = w.glob->sigma_words;
-    for (uint32_t gw = blockIdx.x * NTHREADS + threadIdx.x; gw < total; gw += gridDim.x * NTHREADS) {
+    for (uint32_t gw = first; gw < total; gw += stride) {
         const uint32_t t = tensor_of_sword(w, gw);
         const TDesc &td = w.td[t];
         const uint32_t wl = gw - td.sw0;
@@ -1416,12 +1427,6 @@ __global__ __launch_bounds__(NTHREADS) void k_sigma_pack(Work w) {
         uint32_t *out = td.in.sigma ? td.in.sigma : (uint32_t *)(td.in.rec + td.sigma_off);
         out[wl] = v;
     }
-}
-
-hipError_t launch_sigma_pack(const Work &w, int grid_persist, hipStream_t s) {
-    k_sigma_pack<<<grid_persist, NTHREADS, 0, s>>>(w);
-    trace_mark(s, "k_sigma_pack");
-    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

@@ -81,7 +81,7 @@ def check_record(rec, ref: "oracle.TensorResult", degree: int, n_seg: int):
     assert rec.d == ref.d
     assert rec.n_selected == ref.S.size
     assert (rec.n_positives, rec.n_values) == (ref.P.size, ref.fit.n)
-    assert (rec.m_bits, rec.k, rec.hash_id) == (ref.m, ref.k, 1)
+    assert (rec.m_bits, rec.k, rec.hash_id) == (ref.m, ref.k, oracle.HASH_ID[ref.layout])
     assert (rec.policy, rec.seed) == (ref.policy, ref.seed)
     assert rec.seg_mode == ref.fit.seg_mode
     assert rec.model == ref.fit.model

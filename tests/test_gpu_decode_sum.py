@@ -84,6 +84,11 @@ CASES = {
                       oracle.FIT_DEXP),
     "chord_poly_x4": (80_000, [0, 80_000], (1, 50), 1e-3, 2, 6, 4, oracle.POLICY_P0, oracle.SEG_CHORD,
                       oracle.FIT_POLY),
+    # partitioned filters, one larger than the probe pass's LDS copy
+    "partitioned_x3": (300_000, [0, 123_457, 300_000], (1, 100), 1e-3, 5, 8, 3, oracle.POLICY_P0, oracle.SEG_EQUAL,
+                       oracle.FIT_POLY, oracle.LAYOUT_PARTITIONED),
+    "partitioned_12m_x2": (12_000_000, [0, 12_000_000], (1, 100), 1e-3, 5, 8, 2, oracle.POLICY_P0, oracle.SEG_EQUAL,
+                           oracle.FIT_POLY, oracle.LAYOUT_PARTITIONED),
 }
 
 
@@ -92,13 +97,13 @@ def test_decode_sum_parity(name):
     import torch
 
     d, off, ratio, fpr, D, S, n, policy, *rest = CASES[name]
-    seg, model = rest if rest else (oracle.SEG_EQUAL, oracle.FIT_POLY)
+    seg, model, layout = (list(rest) + [oracle.SEG_EQUAL, oracle.FIT_POLY, oracle.LAYOUT_STANDARD][len(rest):])
     log(f"decode_sum {name} d={d} payloads={n}")
     if ratio is None:
         gs = [W.sparse_normal(d, 300 + p, 0.4) for p in range(n)]
     else:
         gs = [W.normal(d, 300 + p, scale=1e-3) for p in range(n)]
-    cfg = B.Config(off, ratio, fpr, D, S, policy, 99, seg, model)
+    cfg = B.Config(off, ratio, fpr, D, S, policy, 99, seg, model, filter_layout=layout)
     pays = _encode_all(gs, cfg)
     scale = 1.0 / n
     dense = torch.full((max(d, 1),), 5.0, dtype=torch.float32, device="cuda")
@@ -106,8 +111,8 @@ def test_decode_sum_parity(name):
     B.payload_decode_sum(pays, cfg, scale, dense, counts, workspace(d, cfg.n_tensors))
     sync()
     out = host(dense)[:d]
-    refs = [oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=99, seg_mode=seg, model=model)
-            for g in gs]
+    refs = [oracle.roundtrip(g, off, ratio, fpr, D, S, policy=policy, seed=99, seg_mode=seg, model=model,
+                             layout=layout) for g in gs]
     want = oracle.decode_sum(refs, d, off, scale)
     _check(out, want, refs, off, d, n, scale)
     c = host(counts).reshape(n, cfg.n_tensors, 4)

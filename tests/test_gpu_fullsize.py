@@ -45,6 +45,17 @@ def test_resnet50_25m_random_policy_full():
     _full("resnet50_25m", oracle.POLICY_RANDOM, 20210205)
 
 
+def test_resnet50_25m_partitioned_layout_full():
+    w = W.WORKLOADS["resnet50_25m"]
+    log(f"full-size {w.name} layout=partitioned: generating d={w.d}")
+    g = W.generate(w)
+    cfg = B.Config.from_workload(w, filter_layout=B.FILTER_PARTITIONED)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg, layout=oracle.LAYOUT_PARTITIONED)
+    check_roundtrip(g, cfg, out, refs)
+    release_workspace()
+
+
 def test_ncf_32m_support_full():
     _full("ncf_32m")
 

@@ -70,6 +70,34 @@ def test_topr_parity(d, r, kind):
     np.testing.assert_array_equal(host(val)[:r], g[ref.astype(np.int64)])
 
 
+# large tensors: millions of elements, r from 0.1% to a few %, and heavy ties
+LARGE_TOPR_CASES = [
+    ("normal_5m", lambda: W.normal(5_000_000, 31), 50_000),
+    ("laplace_5m_r0.1pct", lambda: W.generate(W.Workload("t", 5_000_003, 1, (1, 1000), 1e-3, 5, 8, "laplace_5e-4", 32)),
+     5001),
+    ("coarse_ties_6m", lambda: (np.random.default_rng(35).integers(-40, 41, 6_000_000) * 0.125).astype(np.float32),
+     200_000),
+]
+
+
+@pytest.mark.parametrize("name,make,r", LARGE_TOPR_CASES, ids=[c[0] for c in LARGE_TOPR_CASES])
+def test_topr_large_parity(name, make, r):
+    import torch
+
+    g = make()
+    d = g.size
+    log(f"topr large {name} d={d} r={r}")
+    ref = oracle.topr(g, r)
+    idx = torch.full((r,), -1, dtype=torch.int32, device="cuda")
+    val = torch.zeros(r, dtype=torch.float32, device="cuda")
+    nd = u64_scalar()
+    B.sparsify_topr(dev_tensor(g), r, idx, val, nd, ws_for(d))
+    sync()
+    assert int(host(nd)[0]) == r
+    np.testing.assert_array_equal(host(idx).view(np.uint32), ref)
+    np.testing.assert_array_equal(host(val).view(np.uint32), g[ref.astype(np.int64)].view(np.uint32))
+
+
 @pytest.mark.parametrize("d,kind", [(50_000, "sparse"), (10_000, "zeros"), (5000, "normal"), (3 * 4096 + 1, "sparse")])
 def test_support_parity(d, kind):
     import torch
@@ -362,6 +390,56 @@ def test_roundtrip_sparse_value_source_parity(name):
         (ref,) = refs
         assert ref.P.size > ref.S.size
         np.testing.assert_array_equal(out["dense"], ref.dense)
+
+
+LAYOUT_CASES = {
+    # name: (g, offsets, ratio, fpr, D, S): the partitioned filter layout
+    "resnet20_conv_37k": RT_CASES["resnet20_conv_37k"],
+    "ragged_tensors": RT_CASES["ragged_tensors"],
+    "support_50k": RT_CASES["support_50k"],
+    "support_1m": RT_CASES["support_1m"],          # the bucketed insert
+    "many_tensors_3m": RT_CASES["many_tensors_3m"],
+    # filters larger than the probe pass's LDS copy: 1.73 M and 4.3 M bits
+    "normal_12m": (W.normal(12_000_000, 41), [0, 12_000_000], (1, 100), 1e-3, 5, 8),
+    "normal_30m_fpr_1e-4": (W.normal(30_000_001, 42), [0, 30_000_001], (1, 100), 1e-4, 5, 8),
+}
+
+
+@pytest.mark.parametrize("name", list(LAYOUT_CASES))
+def test_roundtrip_partitioned_layout_parity(name):
+    """The partitioned filter (hash j over part j of k): filter words,
+    positives, values and the record's hash id as the oracle's."""
+    g, off, ratio, fpr, D, S = LAYOUT_CASES[name]
+    log(f"roundtrip {name} layout=partitioned d={g.size}")
+    cfg = B.Config(off, ratio, fpr, D, S, filter_layout=B.FILTER_PARTITIONED)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, D, S, layout=oracle.LAYOUT_PARTITIONED)
+    check_roundtrip(g, cfg, out, refs)
+
+
+def test_receiver_reads_the_layout_from_the_record_and_rejects_unknown_ones():
+    import torch
+
+    w = W.Workload("t", 50_000, 1, (1, 100), 1e-3, 5, 8, "normal_1e-3", 12)
+    g = W.generate(w)
+    # a partitioned payload decoded by a receiver whose configuration names
+    # the standard layout: the record decides
+    cfg_p = B.Config.from_workload(w, filter_layout=B.FILTER_PARTITIONED)
+    rt = run_roundtrip(g, cfg_p)
+    cfg_s = B.Config.from_workload(w)
+    dense = torch.full((w.d,), 3.0, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    B.payload_decode(dev_tensor(rt["payload"]), cfg_s, dense, None, None, counts, workspace(w.d))
+    sync()
+    assert int(host(counts)[3]) == 0
+    np.testing.assert_array_equal(host(dense), rt["dense"])
+    # an unknown hash id: the record is invalid and decodes as empty
+    bad = rt["payload"].copy()
+    bad[8 * 4: 8 * 4 + 4] = np.frombuffer(np.uint32(3).tobytes(), np.uint8)
+    B.payload_decode(dev_tensor(bad), cfg_s, dense, None, None, counts, workspace(w.d))
+    sync()
+    assert int(host(counts)[3]) & B.FLAG_DEC_MISMATCH
+    assert np.all(host(dense) == 0)
 
 
 SEG_CASES = {
