@@ -40,6 +40,23 @@ constexpr uint32_t HIST1_SHIFT = 20;
 // filter pass's blocks add to copy (block mod HISTA_COPIES), which spreads
 // their atomics over that many times more cache lines.
 constexpr uint32_t HISTA_COPIES = 8;
+// Sampled top-r: a large tensor whose r is a small share of d takes the
+// first digit's histogram from a sample (segment j of SAMPLE_SEG elements
+// in every srate, at j srate + srate / 2) and reads the tensor once, in a
+// filter pass that keeps the bins of a bracket [bL, bH] (at most NBR bins)
+// around the sample's estimate of the threshold as candidates.  A bracket
+// that the exact counts contradict is redone from a full histogram.
+constexpr uint32_t SAMPLE_SEG = 64;
+constexpr uint32_t SAMPLE_SEGS_PER_BLOCK = 64;   // 16 waves x 4 segments
+constexpr uint64_t SAMPLE_MIN_D = 1ull << 22;
+constexpr uint32_t SHIST_COPIES = 4;             // copies of the sample histogram (block mod 4)
+constexpr uint32_t NBR = 4;                      // most first-digit bins in a bracket
+constexpr uint32_t HISTA_BINS = NBR * 1024;      // candidate histogram: (bin - bL, key bits 19..10)
+// The filter pass's exact counts per sampled tensor: elements above the
+// bracket and candidates in each of its bins, added by block mod
+// FCNT_COPIES.
+constexpr uint32_t FCNT_COPIES = 16;
+constexpr uint32_t FCNT_W = 1 + NBR;
 constexpr uint32_t SORT_BINS = 256;           // 8-bit LSD radix digits
 constexpr uint32_t FIT_CHUNKS = 8;            // partial-moment blocks per fitted run
 constexpr uint32_t MAX_DEG = 7;
@@ -115,6 +132,12 @@ struct TInit {
     uint32_t seg_slot;   // chord segmentation over the whole grid: the tensor's state, or NO_SEG_SLOT
     uint32_t value_src;  // VALUES_DENSE or VALUES_SPARSE
     uint32_t layout;     // LAYOUT_STANDARD or LAYOUT_PARTITIONED
+    // sampled top-r (srate 0: the exact histogram; hb0, hbn then count the
+    // sample's blocks)
+    uint32_t srate;      // one sampled segment in srate (a power of 2)
+    uint32_t nsamp;      // elements in the sample
+    uint32_t slo, shi;   // sample ranks that bound the bracket: rho -/+ delta
+    uint32_t rb0, rbn;   // blocks of the full histogram for a redo
 };
 
 // Chord segmentation over the whole grid (at most SEG_GRID_RUNS runs per
@@ -159,6 +182,8 @@ struct TDesc {
     uint32_t needT;      // top-r: how many elements with key == T to take
     uint32_t ntie;       // top-r: elements with key == T
     uint32_t idx_star;   // top-r: largest index taken among key == T (when ties split)
+    uint32_t bL, bH;     // top-r: the filter pass's bracket of first-digit bins
+    uint32_t sfail;      // top-r: the sampled bracket missed the threshold and was redone
     uint32_t bA;         // top-r: bin of key bits 19..10 holding the threshold (~0: all of b1)
     uint32_t needA;      // top-r: how many to take from bin bA
     uint32_t nsub;       // top-r: candidates in bin bA (the short list)
@@ -180,7 +205,7 @@ struct Glob {
     uint32_t sort_tiles;      // value-sort tiles over all tensors
     uint32_t sigma_words;     // reorder-map words over all tensors
     uint32_t values;          // sum of |P|
-    uint32_t pad_;
+    uint32_t redo;            // top-r: some sampled bracket missed (the redo's filter pass has work)
     uint32_t sort_ticket[4];  // value sort: next tile of each pass, in start order
 };
 
@@ -210,7 +235,9 @@ struct Work {
     uint32_t *selbits;        // selection bitmap (paper's d-bit string B), slots / 32 words
     uint32_t *cand_key;       // top-r candidates (keys), per tensor slot
     uint32_t *cand_idx;       // top-r candidates (indices)
-    uint32_t *histA;          // top-r: per tensor, HISTA_COPIES histograms of the candidates' key bits 19..10 (1024 bins)
+    uint32_t *histA;          // top-r: per tensor, HISTA_COPIES histograms of the candidates' (bin - bL, key bits 19..10)
+    uint32_t *shist;          // sampled top-r: per tensor, SHIST_COPIES first-digit histograms of the sample
+    uint32_t *fcnt;           // sampled top-r: [tensor][FCNT_COPIES][FCNT_W] counts of the filter pass
     uint32_t *sub_key;        // top-r short list (borrows P, which is written later)
     uint32_t *sub_idx;        // top-r short list (borrows V)
     uint32_t *S;              // selected indices, per tensor slot

@@ -33,7 +33,7 @@ int resident_grid(K kernel, int threads, uint32_t work) {
 // each kernel launch; the time between consecutive events is that kernel's.
 void trace_mark(hipStream_t s, const char *kernel);
 
-constexpr int INIT_CHUNK = 15;  // tensors per set-up launch (kernel argument size)
+constexpr int INIT_CHUNK = 14;  // tensors per set-up launch (kernel argument size)
 
 struct InitArgs {
     uint32_t first, count;
@@ -54,7 +54,10 @@ static_assert(sizeof(Work) + sizeof(InitArgs) + sizeof(ZeroArgs) <= 4096, "set-u
 // select.hip
 // descriptors of one chunk of tensors, plus clearing the zero ranges
 hipError_t launch_init(const Work &w, const InitArgs &a, const ZeroArgs &z, hipStream_t s);
-hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int grid_persist, bool any_topr,
+// hist_blocks: the first-digit histograms (exact, or of the samples);
+// redo_blocks: the full histograms of sampled tensors whose bracket missed
+// (0: no tensor is sampled, and the redo passes are not launched)
+hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, uint32_t redo_blocks, bool any_topr,
                        hipStream_t s);
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s);
 hipError_t launch_compact_selection(const Work &w, const float *g, float *val_out, int grid_persist, hipStream_t s);

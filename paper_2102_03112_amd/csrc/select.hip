@@ -58,78 +58,51 @@ hipError_t launch_init(const Work &w, const InitArgs &a, const ZeroArgs &z, hipS
 // top-r step 1: first-digit histogram
 // ---------------------------------------------------------------------------
 
-// histogram block -> tensor (hb0 ascending over top-r tensors)
+// histogram block -> tensor: PHASE 0 blocks by hb0/hbn (exact histograms
+// and samples), PHASE 1 (redo) blocks by rb0/rbn; both ascending over the
+// tensors
+template <int PHASE>
 __device__ __forceinline__ int tensor_of_hist_block(const Work &w, uint32_t b) {
     uint32_t lo = 0, hi = w.ntensors;
     while (hi - lo > 1) {
         uint32_t mid = (lo + hi) >> 1;
-        if (w.td[mid].in.hb0 <= b)
+        if ((PHASE == 0 ? w.td[mid].in.hb0 : w.td[mid].in.rb0) <= b)
             lo = mid;
         else
             hi = mid;
     }
     const TInit &in = w.td[lo].in;
-    if (in.hbn == 0 || b < in.hb0 || b >= in.hb0 + in.hbn) return -1;
+    const uint32_t b0 = PHASE == 0 ? in.hb0 : in.rb0, bn = PHASE == 0 ? in.hbn : in.rbn;
+    if (bn == 0 || b < b0 || b >= b0 + bn) return -1;
     return (int)lo;
 }
 
-constexpr uint32_t HIST_THREADS = 1024;
-constexpr uint32_t HIST_SUB = 4;  // sub-histograms, to spread LDS atomics on popular bins
+// The filter pass's exact counts of sampled top-r tensor t: elements above
+// the bracket, and candidates in each bracket bin.
+__device__ __forceinline__ void filter_counts(const Work &w, uint32_t t, uint32_t *above, uint32_t inb[NBR]) {
+    const uint32_t *c = w.fcnt + (uint64_t)t * FCNT_COPIES * FCNT_W;
+    uint32_t a = 0;
+#pragma unroll
+    for (uint32_t x = 0; x < NBR; ++x) inb[x] = 0;
+    for (uint32_t q = 0; q < FCNT_COPIES; ++q) {
+        a += c[q * FCNT_W];
+#pragma unroll
+        for (uint32_t x = 0; x < NBR; ++x) inb[x] += c[q * FCNT_W + 1 + x];
+    }
+    *above = a;
+}
 
-__global__ __launch_bounds__(HIST_THREADS) void k_topr_hist(Work w, const float *__restrict__ g) {
-    __shared__ uint32_t h[HIST_SUB][HIST1_BINS];
-    __shared__ uint32_t bad;
-    for (uint32_t i = threadIdx.x; i < HIST_SUB * HIST1_BINS; i += HIST_THREADS) (&h[0][0])[i] = 0;
-    if (threadIdx.x == 0) bad = 0;
-    __syncthreads();
-    const int t = tensor_of_hist_block(w, blockIdx.x);
-    if (t < 0) return;
+// A sampled tensor's first filter pass missed the threshold: its exact
+// counts put the r-th largest magnitude above or below the bracket.
+__device__ __forceinline__ bool bracket_missed(const Work &w, uint32_t t) {
     const TInit &in = w.td[t].in;
-    const uint32_t lb = blockIdx.x - in.hb0;
-    const uint64_t span = (uint64_t)((in.ntiles + in.hbn - 1) / in.hbn) * TILE;
-    const uint64_t lo = lb * span;
-    const uint64_t hi = lo + span < in.d ? lo + span : in.d;
-    const float *gt = g + in.off;
-    uint32_t *mine = h[(threadIdx.x >> 6) % HIST_SUB];
-    uint32_t nonfinite = 0;
-    // 8 values per thread per step; the next step's values are in flight
-    // while this step's are counted.  Reads past the block's range return 0
-    // through the buffer view and are not counted.
-    constexpr uint32_t STEP = 8 * HIST_THREADS;
-    const uint32_t n = (uint32_t)(hi > lo ? hi - lo : 0);
-    const __amdgpu_buffer_rsrc_t gv = buffer_view(gt + lo, 4u * n);
-    uint32_t vn[8];
+    if (in.srate == 0 || in.r == 0 || in.r == R_NONZERO) return false;
+    uint32_t above, inb[NBR];
+    filter_counts(w, t, &above, inb);
+    uint64_t tot = above;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) vn[u] = buffer_u32(gv, 4u * (u * HIST_THREADS + threadIdx.x));
-    for (uint32_t b0 = 0; b0 < n; b0 += STEP) {
-        uint32_t v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = vn[u];
-        if (b0 + STEP < n) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) vn[u] = buffer_u32(gv, 4u * (b0 + STEP + u * HIST_THREADS + threadIdx.x));
-        }
-        asm volatile("" ::: "memory");
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const uint32_t i = b0 + u * HIST_THREADS + threadIdx.x;
-            if (i < n) {
-                const uint32_t key = mag_key(__uint_as_float(v[u]));
-                nonfinite |= key >= 0x7f800000u;
-                atomicAdd(&mine[key >> HIST1_SHIFT], 1u);
-            }
-        }
-    }
-    if (nonfinite) bad = 1;
-    __syncthreads();
-    // the tensor's histogram: integer sums, so the order of the adds does
-    // not matter
-    uint32_t *out = w.hist + (uint64_t)t * HIST1_BINS;
-    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += HIST_THREADS) {
-        const uint32_t c = h[0][i] + h[1][i] + h[2][i] + h[3][i];
-        if (c) atomicAdd(&out[i], c);
-    }
-    if (threadIdx.x == 0 && bad) atomicOr(&w.td[t].flags, FLAG_NONFINITE);
+    for (uint32_t x = 0; x < NBR; ++x) tot += inb[x];
+    return above >= in.r || tot < in.r;
 }
 
 // Find, scanning bins from the top, the bin where the running count reaches
@@ -191,17 +164,21 @@ constexpr uint32_t FILTER_STEPS = TILE / FILTER_THREADS;  // elements per thread
 
 struct PickLds {
     uint32_t res_bin, res_above;
-    uint32_t scratch[FILTER_WAVES + 1];  // block scans of up to FILTER_THREADS threads
+    uint32_t scratch[1024 / 64 + 1];  // block scans of up to 1024 threads
 };
 
+// The bracket of an exact top-r tensor: bL = bH = the bin b1 holding the
+// r-th largest magnitude, from the tensor's full histogram (block-wide,
+// every thread gets it; r = 0: an empty bracket past the last bin).  The
+// recording block also writes how many to take from b1 and its size.
+template <uint32_t NT>
 __device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) {
     TDesc &td = w.td[t];
     const uint32_t r = td.in.r;
     if (r == 0) {
         if (record && threadIdx.x == 0) {
-            td.b1 = HIST1_BINS;  // nothing above, nothing in the bin
-            td.need1 = 0;
-            td.ncand = 0;
+            td.bL = td.bH = HIST1_BINS;
+            td.need1 = td.ncand = 0;
         }
         return HIST1_BINS;
     }
@@ -211,10 +188,10 @@ __device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) 
     }
     __syncthreads();
     const uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
-    find_from_top<HIST1_BINS, FILTER_THREADS>(hist, r, &l.res_bin, &l.res_above, l.scratch);
+    find_from_top<HIST1_BINS, NT>(hist, r, &l.res_bin, &l.res_above, l.scratch);
     const uint32_t b1 = l.res_bin;
     if (record && threadIdx.x == 0) {
-        td.b1 = b1;
+        td.bL = td.bH = b1;
         td.need1 = r - l.res_above;
         td.ncand = hist[b1];
     }
@@ -222,15 +199,199 @@ __device__ uint32_t pick_b1(const Work &w, uint32_t t, bool record, PickLds &l) 
     return b1;
 }
 
+// The bracket of a sampled tensor from the sample's histogram hs (summed
+// over its copies into LDS): with rho = r nsamp / d the threshold's
+// expected rank in the sample and delta = 8 sqrt(rho) + 64, bH is the bin
+// holding the sample's (rho - delta)-th largest and bL the one holding its
+// (rho + delta)-th (slo and shi), so that the r-th largest of the tensor
+// lies in [bL, bH] unless the sample is off by more than eight binomial
+// standard deviations (plus a margin for correlated values).  At most NBR
+// bins: a wider bracket keeps its top NBR bins (and the counts decide).
+template <uint32_t NT>
+__device__ void pick_sampled(const Work &w, uint32_t t, bool record, PickLds &l, uint32_t *hs, uint32_t *bL,
+                             uint32_t *bH) {
+    TDesc &td = w.td[t];
+    const uint32_t *sh = w.shist + (uint64_t)t * SHIST_COPIES * HIST1_BINS;
+    for (uint32_t b = threadIdx.x; b < HIST1_BINS; b += NT) {
+        uint32_t c = 0;
+#pragma unroll
+        for (uint32_t q = 0; q < SHIST_COPIES; ++q) c += sh[q * HIST1_BINS + b];
+        hs[b] = c;
+    }
+    if (threadIdx.x == 0) {
+        l.res_bin = 0;
+        l.res_above = 0;
+    }
+    __syncthreads();
+    find_from_top<HIST1_BINS, NT>(hs, td.in.slo, &l.res_bin, &l.res_above, l.scratch);
+    const uint32_t hi = l.res_bin;
+    __syncthreads();  // every thread has read the result
+    if (threadIdx.x == 0) {
+        l.res_bin = 0;
+        l.res_above = 0;
+    }
+    __syncthreads();
+    find_from_top<HIST1_BINS, NT>(hs, td.in.shi, &l.res_bin, &l.res_above, l.scratch);
+    uint32_t lo = l.res_bin;
+    if (lo > hi) lo = hi;  // cannot happen: slo <= shi
+    if (hi - lo >= NBR) lo = hi - (NBR - 1u);
+    if (record && threadIdx.x == 0) {
+        td.bL = lo;
+        td.bH = hi;
+    }
+    __syncthreads();  // l and hs are reused
+    *bL = lo;
+    *bH = hi;
+}
+
+constexpr uint32_t HIST_THREADS = 1024;
+constexpr uint32_t HIST_SUB = 4;  // sub-histograms, to spread LDS atomics on popular bins
+
+// PHASE 0: the histogram of key bits 30..20 of each exact top-r tensor, and
+// of the sample of each sampled one.  PHASE 1: the full histogram of each
+// sampled tensor whose bracket missed (the tensor is marked, and the
+// candidate histogram the redo's filter pass adds to is cleared); the
+// blocks of other tensors return at once.
+template <int PHASE>
+__global__ __launch_bounds__(HIST_THREADS) void k_topr_hist(Work w, const float *__restrict__ g) {
+    __shared__ uint32_t h[HIST_SUB][HIST1_BINS];
+    __shared__ uint32_t bad, miss;
+    const int t = tensor_of_hist_block<PHASE>(w, blockIdx.x);
+    if (t < 0) return;  // block-uniform
+    TDesc &td = w.td[t];
+    const TInit &in = td.in;
+    const uint32_t lb = blockIdx.x - (PHASE == 0 ? in.hb0 : in.rb0);
+    const uint32_t nb = PHASE == 0 ? in.hbn : in.rbn;
+    if (PHASE == 1) {
+        if (threadIdx.x == 0) miss = bracket_missed(w, t) ? 1u : 0u;
+        __syncthreads();
+        if (!miss) return;  // block-uniform
+        if (threadIdx.x == 0) w.glob->redo = 1u;  // the redo's filter pass has work
+        // this block's share of the candidate histogram, cleared for the redo
+        uint32_t *ha = w.histA + (uint64_t)t * HISTA_COPIES * HISTA_BINS;
+        constexpr uint32_t NW = HISTA_COPIES * HISTA_BINS;
+        const uint32_t per = (NW + nb - 1) / nb;
+        for (uint32_t i = lb * per + threadIdx.x; i < min(NW, (lb + 1) * per); i += HIST_THREADS) ha[i] = 0;
+        if (lb == 0 && threadIdx.x == 0) td.sfail = 1;
+    }
+    for (uint32_t i = threadIdx.x; i < HIST_SUB * HIST1_BINS; i += HIST_THREADS) (&h[0][0])[i] = 0;
+    if (threadIdx.x == 0) bad = 0;
+    __syncthreads();
+    const float *gt = g + in.off;
+    uint32_t *mine = h[(threadIdx.x >> 6) % HIST_SUB];
+    uint32_t nonfinite = 0;
+    const bool sample = PHASE == 0 && in.srate != 0;
+    if (sample) {
+        // sampled segments [lb SAMPLE_SEGS_PER_BLOCK, +SAMPLE_SEGS_PER_BLOCK):
+        // wave q reads segments q, q + 16, ... of the block's share, one
+        // element per lane, all its reads in flight together
+        constexpr uint32_t WAVES = HIST_THREADS / 64, PER_WAVE = SAMPLE_SEGS_PER_BLOCK / WAVES;
+        static_assert(PER_WAVE * WAVES == SAMPLE_SEGS_PER_BLOCK, "whole segments per wave");
+        const uint32_t lane = threadIdx.x & 63u, wq = threadIdx.x >> 6;
+        const uint64_t nseg = ((uint64_t)in.d + SAMPLE_SEG - 1) / SAMPLE_SEG;
+        uint32_t v[PER_WAVE];
+        bool in_s[PER_WAVE];
+#pragma unroll
+        for (uint32_t u = 0; u < PER_WAVE; ++u) {
+            const uint64_t j = (uint64_t)lb * SAMPLE_SEGS_PER_BLOCK + u * WAVES + wq;  // sampled segment
+            const uint64_t seg = j * in.srate + in.srate / 2;
+            const uint64_t e = seg * SAMPLE_SEG + lane;
+            in_s[u] = seg < nseg && e < in.d;
+            v[u] = in_s[u] ? __float_as_uint(gt[e]) : 0u;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < PER_WAVE; ++u) {
+            if (in_s[u]) {
+                const uint32_t key = mag_key(__uint_as_float(v[u]));
+                nonfinite |= key >= 0x7f800000u;
+                atomicAdd(&mine[key >> HIST1_SHIFT], 1u);
+            }
+        }
+    } else {
+        const uint64_t span = (uint64_t)((in.ntiles + nb - 1) / nb) * TILE;
+        const uint64_t lo = lb * span;
+        const uint64_t hi = lo + span < in.d ? lo + span : in.d;
+        // 8 values per thread per step; the next step's values are in flight
+        // while this step's are counted.  Reads past the block's range return
+        // 0 through the buffer view and are not counted.
+        constexpr uint32_t STEP = 8 * HIST_THREADS;
+        const uint32_t n = (uint32_t)(hi > lo ? hi - lo : 0);
+        const __amdgpu_buffer_rsrc_t gv = buffer_view(gt + lo, 4u * n);
+        uint32_t vn[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) vn[u] = buffer_u32(gv, 4u * (u * HIST_THREADS + threadIdx.x));
+        for (uint32_t b0 = 0; b0 < n; b0 += STEP) {
+            uint32_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = vn[u];
+            if (b0 + STEP < n) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) vn[u] = buffer_u32(gv, 4u * (b0 + STEP + u * HIST_THREADS + threadIdx.x));
+            }
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const uint32_t i = b0 + u * HIST_THREADS + threadIdx.x;
+                if (i < n) {
+                    const uint32_t key = mag_key(__uint_as_float(v[u]));
+                    nonfinite |= key >= 0x7f800000u;
+                    atomicAdd(&mine[key >> HIST1_SHIFT], 1u);
+                }
+            }
+        }
+    }
+    if (nonfinite) bad = 1;
+    __syncthreads();
+    // the tensor's histogram (the sample's: one of SHIST_COPIES copies):
+    // integer sums, so the order of the adds does not matter
+    uint32_t *out = sample ? w.shist + ((uint64_t)t * SHIST_COPIES + lb % SHIST_COPIES) * HIST1_BINS
+                           : w.hist + (uint64_t)t * HIST1_BINS;
+    for (uint32_t i = threadIdx.x; i < HIST1_BINS; i += HIST_THREADS) {
+        const uint32_t c = h[0][i] + h[1][i] + h[2][i] + h[3][i];
+        if (c) atomicAdd(&out[i], c);
+    }
+    if (threadIdx.x == 0 && bad) atomicOr(&td.flags, FLAG_NONFINITE);
+}
+
+// The filter pass's bracket of each top-r tensor, one block per tensor,
+// from the exact histogram or the sample's (the redo's filter pass picks
+// the exact bin of a tensor whose sampled bracket missed itself).  (A separate
+// launch: inside the filter pass its registers would spill the
+// classification's, and making the histogram pass's last block pick needs
+// device-wide fences that cost more than the launch.)
+__global__ __launch_bounds__(HIST_THREADS) void k_topr_pick(Work w) {
+    __shared__ uint32_t hs[HIST1_BINS];
+    __shared__ PickLds pl;
+    const uint32_t t = blockIdx.x;
+    const TDesc &td = w.td[t];
+    if (td.in.r == R_NONZERO) return;  // block-uniform
+    if (td.in.srate != 0 && td.in.r != 0) {
+        uint32_t bL, bH;
+        pick_sampled<HIST_THREADS>(w, t, true, pl, hs, &bL, &bH);
+    } else {
+        pick_b1<HIST_THREADS>(w, t, true, pl);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // top-r step 2 / support: bitmap of definite selections + per-tile candidates
 // ---------------------------------------------------------------------------
 // Elements of a tile are visited as e = j * 512 + threadIdx.x (j = 0..7):
 // each load instruction reads 512 consecutive floats, and one wave ballot
-// covers 64 consecutive elements, i.e. two whole bitmap words.  Candidates
-// (top-r: key in bin b1) are kept in index order in the tile's own stretch
-// of the candidate arrays, with their number in ccnt[tile].  For the
-// support, tcnt[tile] receives the number of selected elements.
+// covers 64 consecutive elements, i.e. two whole bitmap words.  Top-r
+// elements above the tensor's bracket [bL, bH] are selected; those in it
+// are candidates, kept in index order in the tile's own stretch of the
+// candidate arrays (their number in ccnt[tile]) and counted in the
+// candidate histogram by (bin - bL, key bits 19..10).  Each block adds its
+// exact counts per tensor (above the bracket, and in each bracket bin) to
+// copy (block mod FCNT_COPIES) of the tensor's counts.  For the support,
+// tcnt[tile] receives the number of selected elements.
+// PHASE 0 is the first pass over every tile; PHASE 1 redoes the tiles of
+// the sampled tensors whose bracket missed, with the exact bin b1.  With
+// SAMPLED (some tensor of the call is sampled), PHASE 0 takes the brackets
+// from the pick kernel and counts; without it, and in PHASE 1, each block
+// picks the exact bin b1 itself (the count of the bracket is then known
+// from the histogram).
 // What the filter pass needs of a tile's tensor.  Descriptors are read with
 // vector loads (kernels write them), so a tile's fields are read before the
 // next tile's values are requested: waiting for them afterwards would also
@@ -262,41 +423,53 @@ __device__ __forceinline__ void filter_load(const float *g, const FilterTile &f,
         x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * FILTER_THREADS + threadIdx.x)));
 }
 
+constexpr uint32_t NO_TENSOR = 0xffffffffu;
+
+template <int PHASE, bool SAMPLED>
 __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void k_select_filter(Work w, const float *__restrict__ g) {
+    constexpr bool COUNT = PHASE == 0 && SAMPLED;  // brackets from the pick kernel; exact counts
     static_assert(FILTER_STEPS * FILTER_WAVES == 64, "one wave scans the (step, wave) candidate counts");
     __shared__ uint32_t wcnt[FILTER_STEPS * FILTER_WAVES];
     __shared__ uint32_t woff[FILTER_STEPS * FILTER_WAVES];
     __shared__ uint32_t dcnt[FILTER_WAVES];
     __shared__ uint32_t sbw[TILE_WORDS];
     __shared__ uint32_t bad;
+    __shared__ uint32_t acc[FCNT_W];  // the current tensor's counts: above the bracket, in each bin
     __shared__ PickLds pl;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     const uint32_t hcopy = blockIdx.x % HISTA_COPIES;
     if (threadIdx.x == 0) bad = 0;
+    if (threadIdx.x < FCNT_W) acc[threadIdx.x] = 0;
     __syncthreads();
-    uint32_t b1_t = 0xffffffffu, b1_c = 0;  // tensor whose b1 the block holds, and b1
-    // the next tile's values are in flight while this tile is classified
-    float xn[FILTER_STEPS];
-    FilterTile fn{};
-    if (blockIdx.x < w.ntiles_total) {
-        fn = filter_tile(w, blockIdx.x);
-        filter_load(g, fn, xn);
-    }
-    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-        const FilterTile f = fn;
-        const bool more = tile + gridDim.x < w.ntiles_total;
-        if (more) fn = filter_tile(w, tile + gridDim.x);
-        float x[FILTER_STEPS];
+    uint32_t cur_t = NO_TENSOR, bL = 0, bH = 0;  // tensor whose bracket the block holds, and the bracket
+    // thread 0 adds the block's counts of tensor cur_t to its copy and
+    // clears them; the barriers of the tile before and of the next pick or
+    // tile order this with the other threads' updates
+    auto flush = [&]() {
+        if (COUNT && threadIdx.x == 0 && cur_t != NO_TENSOR) {
+            uint32_t *c = w.fcnt + ((uint64_t)cur_t * FCNT_COPIES + blockIdx.x % FCNT_COPIES) * FCNT_W;
 #pragma unroll
-        for (uint32_t j = 0; j < FILTER_STEPS; ++j) x[j] = xn[j];
-        if (more) filter_load(g, fn, xn);
-        // keeps the scheduler from sinking the loads next to their uses
-        asm volatile("" ::: "memory");
-        if (!f.nz && f.t != b1_t) {
-            b1_c = pick_b1(w, f.t, f.base == 0, pl);
-            b1_t = f.t;
+            for (uint32_t q = 0; q < FCNT_W; ++q) {
+                if (acc[q]) atomicAdd(&c[q], acc[q]);
+                acc[q] = 0;
+            }
         }
-        const uint32_t base = f.base, d = f.d, b1 = f.nz ? 0u : b1_c;
+    };
+    // classify one tile's values
+    auto classify = [&](uint32_t tile, const FilterTile &f, const float (&x)[FILTER_STEPS]) {
+        if (!f.nz && f.t != cur_t) {  // block-uniform
+            flush();
+            cur_t = f.t;
+            if constexpr (COUNT) {
+                // picked by the pick kernel (inside this one its registers
+                // would spill the classification's)
+                bL = w.td[f.t].bL;
+                bH = w.td[f.t].bH;
+            } else {
+                bL = bH = pick_b1<FILTER_THREADS>(w, f.t, f.base == 0, pl);
+            }
+        }
+        const uint32_t base = f.base, d = f.d;
         const uint64_t slot = f.slot;
         const bool nz = f.nz;
         uint32_t keys[FILTER_STEPS];
@@ -313,8 +486,9 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
             nonfinite |= key >= 0x7f800000u;
             const uint32_t bin = key >> HIST1_SHIFT;
             // bitwise, not short-circuit: no branches per step
-            const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > b1)));
-            const bool cand = valid & !nz & (bin == b1);
+            const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > bH)));
+            // (an exact bracket is one bin: bL = bH)
+            const bool cand = COUNT ? valid & !nz & (bin >= bL) & (bin <= bH) : valid & !nz & (bin == bH);
             const uint64_t dm = ballot(def);
             cmask[j] = ballot(cand);
             keys[j] = key;
@@ -340,6 +514,7 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
                 uint32_t nd = 0;
                 for (uint32_t q = 0; q < FILTER_WAVES; ++q) nd += dcnt[q];
                 w.tcnt[tile] = nd;
+                if (COUNT && !nz) acc[0] += nd;
             }
         }
         __syncthreads();
@@ -349,18 +524,55 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
         }
         if (threadIdx.x < TILE_WORDS) w.selbits[((slot + base) >> 5) + threadIdx.x] = sbw[threadIdx.x];
         const uint64_t cbase = slot + base;
-        uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * 1024u;
+        uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * HISTA_BINS;
 #pragma unroll
         for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
             if ((cmask[j] >> lane) & 1ull) {
                 const uint64_t q = cbase + woff[j * FILTER_WAVES + wv] + lanes_below(cmask[j]);
+                // < NBR: a candidate lies in the bracket
+                const uint32_t xb = COUNT ? (keys[j] >> HIST1_SHIFT) - bL : 0u;
                 w.cand_key[q] = keys[j];
                 w.cand_idx[q] = base + j * FILTER_THREADS + threadIdx.x;
-                atomicAdd(&histA[(keys[j] >> 10) & 1023u], 1u);
+                atomicAdd(&histA[xb * 1024u + ((keys[j] >> 10) & 1023u)], 1u);
+                if (COUNT) atomicAdd(&acc[1 + xb], 1u);
             }
         }
         __syncthreads();
+    };
+    if constexpr (PHASE == 0) {
+        // the next tile's values are in flight while this tile is classified
+        float xn[FILTER_STEPS];
+        FilterTile fn{};
+        if (blockIdx.x < w.ntiles_total) {
+            fn = filter_tile(w, blockIdx.x);
+            filter_load(g, fn, xn);
+        }
+        for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+            const FilterTile f = fn;
+            const bool more = tile + gridDim.x < w.ntiles_total;
+            if (more) fn = filter_tile(w, tile + gridDim.x);
+            float x[FILTER_STEPS];
+#pragma unroll
+            for (uint32_t j = 0; j < FILTER_STEPS; ++j) x[j] = xn[j];
+            if (more) filter_load(g, fn, xn);
+            // keeps the scheduler from sinking the loads next to their uses
+            asm volatile("" ::: "memory");
+            classify(tile, f, x);
+        }
+    } else {
+        // the redo: only the tiles of tensors whose sampled bracket missed
+        // (marked by the redo's histogram pass); no read-ahead
+        if (!w.glob->redo) return;  // block-uniform: no tensor missed
+        for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+            const uint32_t t = tensor_of_tile(w, tile);
+            if (!w.td[t].sfail) continue;  // block-uniform
+            const FilterTile f = filter_tile(w, tile);
+            float x[FILTER_STEPS];
+            filter_load(g, f, x);
+            classify(tile, f, x);
+        }
     }
+    flush();
 }
 
 // ---------------------------------------------------------------------------
@@ -384,20 +596,57 @@ constexpr uint32_t ALL_OF_B1 = 0xFFFFFFFFu;  // bA when the whole bin b1 is take
 constexpr uint32_t CP_BATCH = 4;
 constexpr uint32_t CP_TILES = 32;
 
-// bA of top-r tensor t (ALL_OF_B1: the whole bin b1 is taken) from the sum
-// of its histogram copies, and how many to take from bin bA.  Block-wide.
-__device__ uint32_t pick_bA(const Work &w, uint32_t t, uint32_t *hsum, PickLds &l, uint32_t *needA) {
-    const TDesc &td = w.td[t];
-    const uint32_t need1 = td.need1, ncand = td.ncand;
-    if (need1 == ncand) {
-        *needA = 0;
-        return ALL_OF_B1;
+// Where the threshold of top-r tensor t lies among its candidates: the
+// bracket bin x (from the bottom of the bracket) that holds the r-th largest
+// magnitude, the bin bA of key bits 19..10 within it (ALL_OF_B1: the whole
+// bin x is taken) and how many to take from bA; from the filter pass's
+// exact counts (the redo's, if the tensor was redone) and its candidate
+// histogram.  x = NBR takes no candidate.  Block-wide; the block that
+// records also writes the tensor's first-digit bin b1 = bL + x for the
+// final step.
+struct Thr {
+    uint32_t x, bA, needA;
+};
+
+__device__ Thr pick_thr(const Work &w, uint32_t t, uint32_t *hsum, PickLds &l, bool record) {
+    TDesc &td = w.td[t];
+    const uint32_t r = td.in.r;
+    uint32_t above = 0, inb[NBR] = {0, 0, 0, 0};
+    static_assert(NBR == 4, "initialiser");
+    if (td.in.srate == 0 || td.sfail) {
+        // exact bracket (bin b1): from the histogram, through the pick
+        above = r - td.need1;
+        inb[0] = td.ncand;
+    } else {
+        filter_counts(w, t, &above, inb);
     }
-    const uint32_t *histA = w.histA + (uint64_t)t * HISTA_COPIES * 1024u;
+    uint64_t tot = above;
+#pragma unroll
+    for (uint32_t x = 0; x < NBR; ++x) tot += inb[x];
+    Thr th{NBR, ALL_OF_B1, 0};
+    if (r == 0 || above >= r || tot < r) {
+        // r = 0, or counts that contradict the bracket, which the redo
+        // rules out: the selection count then differs from r and says so
+        if (r != 0 && record && threadIdx.x == 0) atomicOr(&td.flags, FLAG_COUNT);
+        return th;
+    }
+    uint32_t need = r - above;
+    uint32_t x = NBR - 1;
+    while (need > inb[x]) {  // ends at x >= 0: the bins hold at least `need`
+        need -= inb[x];
+        --x;
+    }
+    th.x = x;
+    if (record && threadIdx.x == 0) {
+        td.b1 = td.bL + x;
+        td.ncand = inb[x];
+    }
+    if (need == inb[x]) return th;  // the whole bin (bA = ALL_OF_B1)
+    const uint32_t *histA = w.histA + (uint64_t)t * HISTA_COPIES * HISTA_BINS + x * 1024u;
     for (uint32_t b = threadIdx.x; b < 1024u; b += NTHREADS) {
         uint32_t c = 0;
 #pragma unroll
-        for (uint32_t q = 0; q < HISTA_COPIES; ++q) c += histA[q * 1024u + b];
+        for (uint32_t q = 0; q < HISTA_COPIES; ++q) c += histA[q * HISTA_BINS + b];
         hsum[b] = c;
     }
     if (threadIdx.x == 0) {
@@ -405,24 +654,25 @@ __device__ uint32_t pick_bA(const Work &w, uint32_t t, uint32_t *hsum, PickLds &
         l.res_above = 0;
     }
     __syncthreads();
-    find_from_top<1024, NTHREADS>(hsum, need1, &l.res_bin, &l.res_above, l.scratch);
-    const uint32_t bA = l.res_bin;
-    *needA = need1 - l.res_above;
+    find_from_top<1024, NTHREADS>(hsum, need, &l.res_bin, &l.res_above, l.scratch);
+    th.bA = l.res_bin;
+    th.needA = need - l.res_above;
     __syncthreads();  // hsum and l are reused
-    return bA;
+    return th;
 }
 
 __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
     __shared__ uint32_t pre[CP_TILES];
     __shared__ uint32_t tten[CP_TILES];
     __shared__ uint64_t tbase[CP_TILES];  // workspace offset of the tile's first candidate
-    __shared__ uint32_t tbA[CP_TILES];
+    __shared__ uint32_t tbA[CP_TILES], tx[CP_TILES], tbL[CP_TILES];  // the tile's tensor's pick and bracket
     __shared__ uint32_t tpk[CP_TILES];    // the tile's entry in the group's tensor list
-    __shared__ uint32_t gten[CP_TILES], gbA[CP_TILES];  // the group's tensors, in tile order, and their bA
+    __shared__ uint32_t gten[CP_TILES], gbA[CP_TILES], gx[CP_TILES], gbL[CP_TILES];  // the group's tensors, in tile order, and their picks
     __shared__ uint32_t gtot, ngten;
     __shared__ uint32_t hsum[1024];
     __shared__ PickLds pl;
-    uint32_t last_t = 0xFFFFFFFFu, last_bA = 0;  // the block's most recent pick
+    uint32_t last_t = 0xFFFFFFFFu;  // the block's most recent pick
+    Thr last{NBR, ALL_OF_B1, 0};
     for (uint32_t g0 = blockIdx.x * CP_TILES; g0 < w.ntiles_total; g0 += gridDim.x * CP_TILES) {
         if (threadIdx.x < 64) {  // the first wave scans the group's counts and lists its tensors
             const uint32_t tile = g0 + threadIdx.x;
@@ -458,23 +708,33 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
             const uint32_t t = gten[q];
             if (t != last_t) {
                 TDesc &td = w.td[t];
-                uint32_t bA = 0, needA = 0;
-                if (td.in.r != R_NONZERO && td.ncand > 0) {
-                    bA = pick_bA(w, t, hsum, pl, &needA);
+                Thr th{NBR, ALL_OF_B1, 0};
+                if (td.in.r != R_NONZERO) {
                     // the group holding the tensor's first tile records the
                     // pick for the final step
-                    if (td.in.tile0 >= g0 && threadIdx.x == 0) {
-                        td.bA = bA;
-                        td.needA = needA;
+                    const bool record = td.in.tile0 >= g0;
+                    th = pick_thr(w, t, hsum, pl, record);
+                    if (record && threadIdx.x == 0) {
+                        td.bA = th.bA;
+                        td.needA = th.needA;
                     }
                 }
                 last_t = t;
-                last_bA = bA;
+                last = th;
             }
-            if (threadIdx.x == 0) gbA[q] = last_bA;
+            if (threadIdx.x == 0) {
+                gbA[q] = last.bA;
+                gx[q] = last.x;
+                gbL[q] = w.td[t].bL;
+            }
         }
         __syncthreads();
-        if (threadIdx.x < CP_TILES && g0 + threadIdx.x < w.ntiles_total) tbA[threadIdx.x] = gbA[tpk[threadIdx.x]];
+        if (threadIdx.x < CP_TILES && g0 + threadIdx.x < w.ntiles_total) {
+            const uint32_t e = tpk[threadIdx.x];
+            tbA[threadIdx.x] = gbA[e];
+            tx[threadIdx.x] = gx[e];
+            tbL[threadIdx.x] = gbL[e];
+        }
         __syncthreads();
         const uint32_t tot = gtot;
         for (uint32_t e0 = 0; e0 < tot; e0 += NTHREADS * CP_BATCH) {
@@ -503,9 +763,12 @@ __global__ __launch_bounds__(NTHREADS) void k_topr_candpass(Work w) {
                 const bool act = e < tot;
                 const uint32_t x = tix[u];
                 const uint32_t bA = tbA[x], k = key[u], i = idx[u];
+                // the candidate's bracket bin (from the bracket's bottom) and
+                // key bits 19..10
+                const uint32_t xb = (k >> HIST1_SHIFT) - tbL[x], xt = tx[x];
                 const uint32_t dA = (k >> 10) & 1023u;
-                const bool take = act && (bA == ALL_OF_B1 || dA > bA);
-                const bool sub = act && bA != ALL_OF_B1 && dA == bA;
+                const bool take = act && (xb > xt || (xb == xt && (bA == ALL_OF_B1 || dA > bA)));
+                const bool sub = act && xb == xt && bA != ALL_OF_B1 && dA == bA;
                 // i lies in tile x, whose first element sits at slot tbase[x]
                 if (take) atomicOr(&w.selbits[(tbase[x] + (i % TILE)) >> 5], 1u << (i & 31u));
                 if (sub) {
@@ -617,15 +880,31 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_final(Work w) {
     }
 }
 
-hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, int grid_persist, bool any_topr,
+hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, uint32_t redo_blocks, bool any_topr,
                        hipStream_t s) {
-    if (any_topr) {
-        k_topr_hist<<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
+    const bool sampled = redo_blocks > 0;
+    const int fgrid = resident_grid(k_select_filter<0, false>, FILTER_THREADS, w.ntiles_total);
+    if (any_topr && hist_blocks > 0) {
+        k_topr_hist<0><<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
         trace_mark(s, "k_topr_hist");
     }
-    k_select_filter<<<resident_grid(k_select_filter, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
+    if (any_topr && sampled) {
+        k_topr_pick<<<w.ntensors, HIST_THREADS, 0, s>>>(w);
+        trace_mark(s, "k_topr_pick");
+        k_select_filter<0, true><<<fgrid, FILTER_THREADS, 0, s>>>(w, g);
+    } else {
+        k_select_filter<0, false><<<fgrid, FILTER_THREADS, 0, s>>>(w, g);
+    }
     trace_mark(s, "k_select_filter");
     if (any_topr) {
+        if (sampled) {
+            // the exact redo of sampled brackets that missed (blocks of other
+            // tensors return at once)
+            k_topr_hist<1><<<redo_blocks, HIST_THREADS, 0, s>>>(w, g);
+            trace_mark(s, "k_topr_hist_redo");
+            k_select_filter<1, true><<<fgrid, FILTER_THREADS, 0, s>>>(w, g);
+            trace_mark(s, "k_select_filter_redo");
+        }
         k_topr_candpass<<<resident_grid(k_topr_candpass, NTHREADS, (w.ntiles_total + CP_TILES - 1) / CP_TILES), NTHREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_candpass");
         k_topr_final<<<w.ntensors, SEL_THREADS, 0, s>>>(w);
@@ -738,7 +1017,7 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
 
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     (void)grid_persist;
-    k_select_filter<<<resident_grid(k_select_filter, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
+    k_select_filter<0, false><<<resident_grid(k_select_filter<0, false>, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     // |S| from the per-tile counts of the filter pass
     k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w);

@@ -70,8 +70,45 @@ def test_topr_parity(d, r, kind):
     np.testing.assert_array_equal(host(val)[:r], g[ref.astype(np.int64)])
 
 
+SAMPLED_D = (1 << 26) + 4099  # calls of at least 2^26 elements sample; ragged tail
+
+
+def _sample_blind():
+    """Large magnitudes only where the selection's sample does not look.
+    A call of at least 2^26 elements takes the threshold's first digit of
+    each tensor of at least 2^22 elements with r <= d/16 from a sample:
+    segment j srate + srate/2 of 64 elements, srate the largest power of 2
+    leaving max(2^18, 4096 ceil(d/r)) sampled elements, here 128 for r = 1%.
+    Outside the sampled segments 2% of the elements are +-(1..2), so the 1%
+    largest are all there, and the sample's bracket (around the threshold of
+    the N(0, 1e-3) values it sees) is contradicted by the exact counts: the
+    tensor is redone from a full histogram."""
+    rng = np.random.default_rng(41)
+    g = rng.standard_normal(SAMPLED_D).astype(np.float32) * np.float32(1e-3)
+    seg = np.arange(SAMPLED_D) // 64
+    big = (seg % 128 != 64) & (rng.random(SAMPLED_D) < 0.02)
+    nb = int(big.sum())
+    g[big] = (np.sign(rng.standard_normal(nb)) * (1.0 + rng.random(nb))).astype(np.float32)
+    return g
+
+
+def _all_binades():
+    """Magnitudes log-uniform over all normal binades: about 33,000 elements
+    per first-digit bin, so the sample's bracket may span more bins than it
+    keeps (at r = 6%), and the exact counts decide whether it holds."""
+    rng = np.random.default_rng(43)
+    e = rng.uniform(-125.0, 127.0, SAMPLED_D)
+    return (np.sign(rng.standard_normal(e.size)) * np.exp2(e)).astype(np.float32)
+
+
 # large tensors: millions of elements, r from 0.1% to a few %, and heavy ties
+# (in calls of at least 2^26 elements, tensors of at least 2^22 elements
+# with r <= d/16 take the threshold's first digit from a sample, the others
+# from an exact histogram)
 LARGE_TOPR_CASES = [
+    ("sample_blind_67m", _sample_blind, SAMPLED_D // 100),
+    ("all_binades_67m", _all_binades, SAMPLED_D // 100),
+    ("all_binades_67m_r6pct", _all_binades, SAMPLED_D * 6 // 100),
     ("normal_5m", lambda: W.normal(5_000_000, 31), 50_000),
     ("laplace_5m_r0.1pct", lambda: W.generate(W.Workload("t", 5_000_003, 1, (1, 1000), 1e-3, 5, 8, "laplace_5e-4", 32)),
      5001),
