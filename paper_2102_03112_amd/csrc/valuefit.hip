@@ -1371,9 +1371,11 @@ __global__ __launch_bounds__(DEXP_THREADS) void k_dexp_pass(Work w, uint32_t pas
 }
 
 hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s) {
-    // the fit's chunk blocks, then PACK_BLOCKS packing the reorder maps
-    constexpr uint32_t PACK_BLOCKS = 32;
-    k_fit_moments<<<fit_blocks + PACK_BLOCKS, FIT_THREADS, 0, s>>>(w, fit_blocks);
+    // the fit's chunk blocks, then blocks packing the reorder maps: one per
+    // 32 Ki elements of the work's slots (which bound the values), at least
+    // 32 and at most 1024
+    const uint32_t pack_blocks = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(32, w.slots >> 15));
+    k_fit_moments<<<fit_blocks + pack_blocks, FIT_THREADS, 0, s>>>(w, fit_blocks);
     trace_mark(s, "k_fit_moments");
     if (fit_blocks == 0) return hipGetLastError();
     k_fit_solve<<<fit_blocks / FIT_CHUNKS, 64, 0, s>>>(w);
@@ -1411,8 +1413,11 @@ __device__ void pack_sigma_words(const Work &w, uint32_t first, uint32_t stride)
         const uint32_t wl = gw - td.sw0;
         const uint32_t b = td.b, nv = td.nv;
         const uint64_t bit0 = (uint64_t)wl * 32u;
-        const uint64_t qa = bit0 / b;
-        uint64_t qb = (bit0 + 31u) / b;
+        // floor(bit0 / b) in double: exact, since bit0 < 2^53 and a quotient
+        // that is not an integer lies at least 1/b from one
+        const double rb = (double)b;
+        const uint64_t qa = (uint64_t)floor((double)bit0 / rb);
+        uint64_t qb = (uint64_t)floor((double)(bit0 + 31u) / rb);
         if (qb > nv - 1u) qb = nv - 1u;
         const uint32_t *sg = w.sig + td.in.slot;
         uint32_t v = 0;
