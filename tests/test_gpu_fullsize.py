@@ -45,15 +45,27 @@ def test_resnet50_25m_random_policy_full():
     _full("resnet50_25m", oracle.POLICY_RANDOM, 20210205)
 
 
-def test_resnet50_25m_partitioned_layout_full():
-    w = W.WORKLOADS["resnet50_25m"]
+def _full_partitioned(name):
+    w = W.WORKLOADS[name]
     log(f"full-size {w.name} layout=partitioned: generating d={w.d}")
     g = W.generate(w)
     cfg = B.Config.from_workload(w, filter_layout=B.FILTER_PARTITIONED)
     out = run_roundtrip(g, cfg)
+    log(f"full-size {w.name} layout=partitioned: oracle")
     refs = oracle.roundtrip(g, w.offsets(), w.ratio, w.fpr, w.degree, w.n_seg, layout=oracle.LAYOUT_PARTITIONED)
     check_roundtrip(g, cfg, out, refs)
     release_workspace()
+
+
+def test_resnet50_25m_partitioned_layout_full():
+    _full_partitioned("resnet50_25m")
+
+
+@pytest.mark.skip(reason="partitioned filter of 3.7e8 bits: a smaller one (4e7 bits) went silent on the GPU with a "
+                         "build that probed such filters in rounds (cause not found); kept off the GPU")
+def test_ncf_32m_partitioned_layout_full():
+    """The 44.7 MiB partitioned filter of the NCF support."""
+    _full_partitioned("ncf_32m")
 
 
 def test_ncf_32m_support_full():
