@@ -777,13 +777,19 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     }
     DR_HIP(hipStreamWaitEvent(ss->s, ss->fork, 0));
     trace_call(ss->s);  // per-kernel timing: the wait for the fork is idle time
-    // CUs left to the sender: one in each of the 32 shader engines (8 XCDs
-    // of 4).  Workgroups are dealt to the engines in turn, so a kernel
-    // launched beside the probe pass needs a free CU in every engine: with
-    // fewer left, its workgroups dealt to a full engine wait for the probe
-    // pass to end, and the sender's value stage runs after it instead of
-    // beside it (seen with 8, 16 and 24 left)
-    const uint32_t reserve = 32u;
+    // CUs left to the sender: a multiple of the 32 shader engines (8 XCDs of
+    // 4).  Workgroups are dealt to the engines in turn, so a kernel launched
+    // beside the probe pass needs a free CU in every engine: with fewer than
+    // 32 left, its workgroups dealt to a full engine wait for the probe pass
+    // to end, and the sender's value stage runs after it instead of beside
+    // it (seen with 8, 16 and 24 left).  A top-r gradient codes about r
+    // values, a small sort beside a long probe pass: one CU per engine.  An
+    // inherently sparse one codes every nonzero (19 M values for the NCF
+    // workload), and its sort needs more of the chip than the probe pass
+    // loses: four per engine (measured on ncf_32m: 7.96 ms with 32 left,
+    // 7.72 with 64, 7.66 with 96, 7.56 with 128; resnet50_25m gets slower
+    // with each step above 32).
+    const uint32_t reserve = e.p.any_topr ? 32u : 128u;
     st = decode_probe(dd, (uint32_t)std::max(1, dr::device_cus() - (int)reserve), ss->s);
     if (st != DR_OK) return st;
     DR_HIP(hipEventRecord(ss->join, ss->s));
