@@ -148,11 +148,6 @@ __device__ void find_from_top(const uint32_t *cnt, uint32_t need, uint32_t *res_
     __syncthreads();
 }
 
-// The bin b1 that holds the r-th largest magnitude of top-r tensor t, from
-// its histogram (block-wide, every thread gets it).  Every filter block
-// finds it for its own tiles' tensor, hidden under its first tile's reads;
-// the block holding the tensor's first tile records b1, how many to take
-// from it and its size for the passes after.
 // The filter pass's blocks: 512 threads, 8 elements of a tile each, and at
 // most 80 VGPRs so that three blocks (six waves per SIMD) fit on a CU.
 // Measured against 256 threads and 16 elements (120 VGPRs, four waves per
@@ -376,26 +371,23 @@ __global__ __launch_bounds__(HIST_THREADS) void k_topr_pick(Work w) {
 // ---------------------------------------------------------------------------
 // top-r step 2 / support: bitmap of definite selections + per-tile candidates
 // ---------------------------------------------------------------------------
-// Elements of a tile are visited as e = j * 512 + threadIdx.x (j = 0..7):
-// each load instruction reads 512 consecutive floats, and one wave ballot
-// covers 64 consecutive elements, i.e. two whole bitmap words.  Top-r
-// elements above the tensor's bracket [bL, bH] are selected; those in it
-// are candidates, kept in index order in the tile's own stretch of the
+// Each wave owns whole tiles (the tiles gw, gw + waves, ... of the grid's
+// waves), so the pass has no block barriers: a tile is 64 steps of 64
+// consecutive elements, read 8 steps at a time with the next 8 in flight.
+// Top-r elements above the tensor's bracket [bL, bH] are selected; those in
+// it are candidates, written in index order (a running count and the
+// lanes below in the step's ballot) to the tile's own stretch of the
 // candidate arrays (their number in ccnt[tile]) and counted in the
-// candidate histogram by (bin - bL, key bits 19..10).  Each block adds its
-// exact counts per tensor (above the bracket, and in each bracket bin) to
-// copy (block mod FCNT_COPIES) of the tensor's counts.  For the support,
-// tcnt[tile] receives the number of selected elements.
-// PHASE 0 is the first pass over every tile; PHASE 1 redoes the tiles of
-// the sampled tensors whose bracket missed, with the exact bin b1.  With
-// SAMPLED (some tensor of the call is sampled), PHASE 0 takes the brackets
-// from the pick kernel and counts; without it, and in PHASE 1, each block
-// picks the exact bin b1 itself (the count of the bracket is then known
-// from the histogram).
-// What the filter pass needs of a tile's tensor.  Descriptors are read with
-// vector loads (kernels write them), so a tile's fields are read before the
-// next tile's values are requested: waiting for them afterwards would also
-// wait for those values.
+// candidate histogram by (bin - bL, key bits 19..10).  Lane s keeps step
+// s's 64-bit ballot, so the tile's 128 bitmap words leave in one coalesced
+// 8-byte store per lane.  For the support, tcnt[tile] receives the number
+// of selected elements.
+// The calls with a sampled tensor use it.  PHASE 0 is the first pass over
+// every tile, with the brackets of the pick kernel; it adds each wave's
+// exact counts per tensor (above the bracket, in each bracket bin) to copy
+// (wave mod FCNT_COPIES).  PHASE 1 redoes the tiles of the sampled tensors
+// whose bracket missed; each wave picks the exact bin b1 itself from the
+// histogram.
 struct FilterTile {
     uint32_t t, base, d;
     uint64_t slot, off;
@@ -414,6 +406,189 @@ __device__ __forceinline__ FilterTile filter_tile(const Work &w, uint32_t tile) 
     return f;
 }
 
+constexpr uint32_t SF_THREADS = 256;                         // filter blocks: 4 waves, each on tiles of its own
+constexpr uint32_t SF_GROUP = 8;                             // steps of 64 elements read together
+constexpr uint32_t SF_STEPS = TILE / 64;                     // 64 steps per tile: one per lane
+constexpr uint32_t SF_GROUPS = SF_STEPS / SF_GROUP;
+static_assert(SF_STEPS == 64, "lane s keeps the ballot of step s");
+
+// A lane's values of steps [grp SF_GROUP, +SF_GROUP) of a tile, read
+// through a raw buffer view (reads past the tensor's end return 0 and touch
+// no memory).
+__device__ __forceinline__ void sf_load(const float *g, const FilterTile &f, uint32_t grp, float x[SF_GROUP]) {
+    const __amdgpu_buffer_rsrc_t gv = buffer_view(g + f.off + f.base, 4u * min(TILE, f.d - min(f.d, f.base)));
+    const uint32_t lane = threadIdx.x & 63u;
+#pragma unroll
+    for (uint32_t u = 0; u < SF_GROUP; ++u)
+        x[u] = __uint_as_float(buffer_u32(gv, 4u * ((grp * SF_GROUP + u) * 64u + lane)));
+}
+
+// The exact bin b1 of top-r tensor t for one wave (every lane gets it):
+// lane l sums the 32 bins [2016 - 32 l, 2047 - 32 l] (from the top), a
+// wave scan finds the lane whose bins hold the r-th largest magnitude, and
+// that lane walks them.  The recording wave writes the bracket, how many to
+// take from b1 and its size.
+__device__ __noinline__ uint32_t wave_pick_b1(const Work &w, uint32_t t, bool record) {
+    TDesc &td = w.td[t];
+    const uint32_t r = td.in.r, lane = threadIdx.x & 63u;
+    if (r == 0) {
+        if (record && lane == 0) {
+            td.bL = td.bH = HIST1_BINS;  // nothing above, nothing in the bracket
+            td.need1 = td.ncand = 0;
+        }
+        return HIST1_BINS;
+    }
+    constexpr uint32_t PER = HIST1_BINS / 64;
+    const uint32_t *hist = w.hist + (uint64_t)t * HIST1_BINS;
+    uint32_t sum = 0;
+#pragma unroll 8
+    for (uint32_t q = 0; q < PER; ++q) sum += hist[HIST1_BINS - 1 - (lane * PER + q)];
+    const uint32_t incl = wave_incl_scan(sum), excl = incl - sum;
+    const bool mine = excl < r && r <= incl;
+    uint32_t bin = 0, above = 0;
+    if (mine) {
+        uint32_t run = excl;
+        for (uint32_t q = 0; q < PER; ++q) {
+            const uint32_t b = HIST1_BINS - 1 - (lane * PER + q);
+            const uint32_t c = hist[b];
+            if (run + c >= r) {
+                bin = b;
+                above = run;
+                break;
+            }
+            run += c;
+        }
+    }
+    const uint64_t m = ballot(mine);
+    const int src = m ? __ffsll((unsigned long long)m) - 1 : 0;  // one lane (r <= d: the counts reach r)
+    bin = __shfl(bin, src, 64);
+    above = __shfl(above, src, 64);
+    if (record && lane == 0) {
+        td.bL = td.bH = bin;
+        td.need1 = r - above;
+        td.ncand = hist[bin];
+    }
+    return bin;
+}
+
+constexpr uint32_t NO_TENSOR = 0xffffffffu;
+
+template <int PHASE>
+__global__ __launch_bounds__(SF_THREADS) void k_select_filter_wave(Work w, const float *__restrict__ g) {
+    constexpr bool COUNT = PHASE == 0;  // brackets from the pick kernel; exact counts
+    const uint32_t lane = threadIdx.x & 63u;
+    const uint32_t gw = blockIdx.x * (SF_THREADS / 64) + (threadIdx.x >> 6);  // this wave, over the grid
+    const uint32_t nw = gridDim.x * (SF_THREADS / 64);
+    const uint32_t hcopy = gw % HISTA_COPIES, ccopy = gw % FCNT_COPIES;
+    if (PHASE == 1 && !w.glob->redo) return;  // no tensor missed its bracket
+    uint32_t cur_t = NO_TENSOR, bL = 0, bH = 0;  // tensor whose bracket the wave holds, and the bracket
+    uint32_t acc_def = 0, acc_x[NBR];            // COUNT: the wave's counts of tensor cur_t
+#pragma unroll
+    for (uint32_t x = 0; x < NBR; ++x) acc_x[x] = 0;
+    auto flush = [&]() {
+        if (COUNT && cur_t != NO_TENSOR && lane == 0) {
+            uint32_t *c = w.fcnt + ((uint64_t)cur_t * FCNT_COPIES + ccopy) * FCNT_W;
+            if (acc_def) atomicAdd(&c[0], acc_def);
+#pragma unroll
+            for (uint32_t x = 0; x < NBR; ++x)
+                if (acc_x[x]) atomicAdd(&c[1 + x], acc_x[x]);
+        }
+        acc_def = 0;
+#pragma unroll
+        for (uint32_t x = 0; x < NBR; ++x) acc_x[x] = 0;
+    };
+    // PHASE 0 reads the next tile's first values while it classifies a
+    // tile's last ones; the redo reads a tile only once it knows the tile's
+    // tensor was redone
+    float xn[SF_GROUP];
+    FilterTile fn{};
+    if (PHASE == 0 && gw < w.ntiles_total) {
+        fn = filter_tile(w, gw);
+        sf_load(g, fn, 0, xn);
+    }
+    for (uint32_t tile = gw; tile < w.ntiles_total; tile += nw) {
+        const FilterTile f = PHASE == 0 ? fn : filter_tile(w, tile);
+        if (PHASE == 1) {
+            if (!w.td[f.t].sfail) continue;  // wave-uniform
+            sf_load(g, f, 0, xn);
+        }
+        if (!f.nz && f.t != cur_t) {                   // wave-uniform
+            flush();
+            cur_t = f.t;
+            if constexpr (COUNT) {
+                bL = w.td[f.t].bL;
+                bH = w.td[f.t].bH;
+            } else {
+                bL = bH = wave_pick_b1(w, f.t, f.base == 0);
+            }
+        }
+        const uint32_t base = f.base, d = f.d;
+        const bool nz = f.nz;
+        const uint64_t cbase = f.slot + base;
+        uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * HISTA_BINS;
+        uint32_t run = 0, ndef = 0, nonfinite = 0;
+        uint64_t myword = 0;  // lane s: the ballot of step s
+        for (uint32_t grp = 0; grp < SF_GROUPS; ++grp) {
+            float x[SF_GROUP];
+#pragma unroll
+            for (uint32_t u = 0; u < SF_GROUP; ++u) x[u] = xn[u];
+            if (grp + 1 < SF_GROUPS) {
+                sf_load(g, f, grp + 1, xn);
+            } else if (PHASE == 0 && tile + nw < w.ntiles_total) {
+                fn = filter_tile(w, tile + nw);
+                sf_load(g, fn, 0, xn);
+            }
+            // keeps the scheduler from sinking the loads next to their uses
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (uint32_t u = 0; u < SF_GROUP; ++u) {
+                const uint32_t st = grp * SF_GROUP + u;  // elements [64 st, 64 st + 64) of the tile
+                const uint32_t i = base + st * 64u + lane;
+                const bool valid = i < d;
+                const uint32_t key = valid ? mag_key(x[u]) : 0u;
+                nonfinite |= key >= 0x7f800000u;
+                const uint32_t bin = key >> HIST1_SHIFT;
+                // bitwise, not short-circuit: no branches per step; an exact
+                // bracket is one bin (bL = bH)
+                const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > bH)));
+                const bool cand = COUNT ? valid & !nz & (bin >= bL) & (bin <= bH) : valid & !nz & (bin == bH);
+                const uint64_t dm = ballot(def);
+                const uint64_t cm = ballot(cand);
+                ndef += popc64(dm);
+                myword = lane == st ? dm : myword;
+                if (cand) {
+                    const uint64_t q = cbase + run + lanes_below(cm);
+                    const uint32_t xb = COUNT ? bin - bL : 0u;  // < NBR: the candidate lies in the bracket
+                    w.cand_key[q] = key;
+                    w.cand_idx[q] = i;
+                    atomicAdd(&histA[xb * 1024u + ((key >> 10) & 1023u)], 1u);
+                }
+                if (COUNT && cm) {
+#pragma unroll
+                    for (uint32_t x = 0; x < NBR; ++x) acc_x[x] += popc64(ballot(cand && bin - bL == x));
+                }
+                run += popc64(cm);
+            }
+        }
+        // slot + base is a multiple of TILE, so the tile's words are 8-byte aligned
+        uint2 *sb = (uint2 *)(w.selbits + ((f.slot + base) >> 5));
+        sb[lane] = make_uint2((uint32_t)myword, (uint32_t)(myword >> 32));
+        if (lane == 0) {
+            w.ccnt[tile] = run;
+            w.tcnt[tile] = ndef;
+        }
+        if (COUNT && !nz) acc_def += ndef;
+        if (ballot(nonfinite != 0) && lane == 0) atomicOr(&w.td[f.t].flags, FLAG_NONFINITE);
+    }
+    flush();
+}
+
+// The block-wide form of the filter pass: a tile per block at a time, 512
+// threads of 8 elements each; each block finds the exact bin b1 itself.
+// The exact calls use it: with few tiles per wave, the wave-per-tile form
+// above leaves its waves' reads exposed (normal_1m: 19 against 11 µs;
+// resnet50_25m: 46 against 44), where the sampled calls' many tiles
+// amortise them (transformer_355m_x24: 437 against 517 µs).
 // The FILTER_STEPS values of a thread for a tile, read through a raw buffer
 // view (reads past the tensor's end return 0 and touch no memory).
 __device__ __forceinline__ void filter_load(const float *g, const FilterTile &f, float x[FILTER_STEPS]) {
@@ -423,51 +598,24 @@ __device__ __forceinline__ void filter_load(const float *g, const FilterTile &f,
         x[j] = __uint_as_float(buffer_u32(gv, 4u * (j * FILTER_THREADS + threadIdx.x)));
 }
 
-constexpr uint32_t NO_TENSOR = 0xffffffffu;
-
-template <int PHASE, bool SAMPLED>
-__global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void k_select_filter(Work w, const float *__restrict__ g) {
-    constexpr bool COUNT = PHASE == 0 && SAMPLED;  // brackets from the pick kernel; exact counts
+__global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void k_select_filter_blk(Work w, const float *__restrict__ g) {
     static_assert(FILTER_STEPS * FILTER_WAVES == 64, "one wave scans the (step, wave) candidate counts");
     __shared__ uint32_t wcnt[FILTER_STEPS * FILTER_WAVES];
     __shared__ uint32_t woff[FILTER_STEPS * FILTER_WAVES];
     __shared__ uint32_t dcnt[FILTER_WAVES];
     __shared__ uint32_t sbw[TILE_WORDS];
     __shared__ uint32_t bad;
-    __shared__ uint32_t acc[FCNT_W];  // the current tensor's counts: above the bracket, in each bin
     __shared__ PickLds pl;
     const uint32_t lane = threadIdx.x & 63u, wv = threadIdx.x >> 6;
     const uint32_t hcopy = blockIdx.x % HISTA_COPIES;
     if (threadIdx.x == 0) bad = 0;
-    if (threadIdx.x < FCNT_W) acc[threadIdx.x] = 0;
     __syncthreads();
-    uint32_t cur_t = NO_TENSOR, bL = 0, bH = 0;  // tensor whose bracket the block holds, and the bracket
-    // thread 0 adds the block's counts of tensor cur_t to its copy and
-    // clears them; the barriers of the tile before and of the next pick or
-    // tile order this with the other threads' updates
-    auto flush = [&]() {
-        if (COUNT && threadIdx.x == 0 && cur_t != NO_TENSOR) {
-            uint32_t *c = w.fcnt + ((uint64_t)cur_t * FCNT_COPIES + blockIdx.x % FCNT_COPIES) * FCNT_W;
-#pragma unroll
-            for (uint32_t q = 0; q < FCNT_W; ++q) {
-                if (acc[q]) atomicAdd(&c[q], acc[q]);
-                acc[q] = 0;
-            }
-        }
-    };
+    uint32_t cur_t = NO_TENSOR, b1 = 0;  // tensor whose bin b1 the block holds, and b1
     // classify one tile's values
     auto classify = [&](uint32_t tile, const FilterTile &f, const float (&x)[FILTER_STEPS]) {
         if (!f.nz && f.t != cur_t) {  // block-uniform
-            flush();
             cur_t = f.t;
-            if constexpr (COUNT) {
-                // picked by the pick kernel (inside this one its registers
-                // would spill the classification's)
-                bL = w.td[f.t].bL;
-                bH = w.td[f.t].bH;
-            } else {
-                bL = bH = pick_b1<FILTER_THREADS>(w, f.t, f.base == 0, pl);
-            }
+            b1 = pick_b1<FILTER_THREADS>(w, f.t, f.base == 0, pl);
         }
         const uint32_t base = f.base, d = f.d;
         const uint64_t slot = f.slot;
@@ -486,9 +634,8 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
             nonfinite |= key >= 0x7f800000u;
             const uint32_t bin = key >> HIST1_SHIFT;
             // bitwise, not short-circuit: no branches per step
-            const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > bH)));
-            // (an exact bracket is one bin: bL = bH)
-            const bool cand = COUNT ? valid & !nz & (bin >= bL) & (bin <= bH) : valid & !nz & (bin == bH);
+            const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > b1)));
+            const bool cand = valid & !nz & (bin == b1);
             const uint64_t dm = ballot(def);
             cmask[j] = ballot(cand);
             keys[j] = key;
@@ -514,7 +661,6 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
                 uint32_t nd = 0;
                 for (uint32_t q = 0; q < FILTER_WAVES; ++q) nd += dcnt[q];
                 w.tcnt[tile] = nd;
-                if (COUNT && !nz) acc[0] += nd;
             }
         }
         __syncthreads();
@@ -529,50 +675,32 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
         for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
             if ((cmask[j] >> lane) & 1ull) {
                 const uint64_t q = cbase + woff[j * FILTER_WAVES + wv] + lanes_below(cmask[j]);
-                // < NBR: a candidate lies in the bracket
-                const uint32_t xb = COUNT ? (keys[j] >> HIST1_SHIFT) - bL : 0u;
                 w.cand_key[q] = keys[j];
                 w.cand_idx[q] = base + j * FILTER_THREADS + threadIdx.x;
-                atomicAdd(&histA[xb * 1024u + ((keys[j] >> 10) & 1023u)], 1u);
-                if (COUNT) atomicAdd(&acc[1 + xb], 1u);
+                atomicAdd(&histA[(keys[j] >> 10) & 1023u], 1u);  // bracket bin 0
             }
         }
         __syncthreads();
     };
-    if constexpr (PHASE == 0) {
-        // the next tile's values are in flight while this tile is classified
-        float xn[FILTER_STEPS];
-        FilterTile fn{};
-        if (blockIdx.x < w.ntiles_total) {
-            fn = filter_tile(w, blockIdx.x);
-            filter_load(g, fn, xn);
-        }
-        for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-            const FilterTile f = fn;
-            const bool more = tile + gridDim.x < w.ntiles_total;
-            if (more) fn = filter_tile(w, tile + gridDim.x);
-            float x[FILTER_STEPS];
-#pragma unroll
-            for (uint32_t j = 0; j < FILTER_STEPS; ++j) x[j] = xn[j];
-            if (more) filter_load(g, fn, xn);
-            // keeps the scheduler from sinking the loads next to their uses
-            asm volatile("" ::: "memory");
-            classify(tile, f, x);
-        }
-    } else {
-        // the redo: only the tiles of tensors whose sampled bracket missed
-        // (marked by the redo's histogram pass); no read-ahead
-        if (!w.glob->redo) return;  // block-uniform: no tensor missed
-        for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
-            const uint32_t t = tensor_of_tile(w, tile);
-            if (!w.td[t].sfail) continue;  // block-uniform
-            const FilterTile f = filter_tile(w, tile);
-            float x[FILTER_STEPS];
-            filter_load(g, f, x);
-            classify(tile, f, x);
-        }
+    // the next tile's values are in flight while this tile is classified
+    float xn[FILTER_STEPS];
+    FilterTile fn{};
+    if (blockIdx.x < w.ntiles_total) {
+        fn = filter_tile(w, blockIdx.x);
+        filter_load(g, fn, xn);
     }
-    flush();
+    for (uint32_t tile = blockIdx.x; tile < w.ntiles_total; tile += gridDim.x) {
+        const FilterTile f = fn;
+        const bool more = tile + gridDim.x < w.ntiles_total;
+        if (more) fn = filter_tile(w, tile + gridDim.x);
+        float x[FILTER_STEPS];
+#pragma unroll
+        for (uint32_t j = 0; j < FILTER_STEPS; ++j) x[j] = xn[j];
+        if (more) filter_load(g, fn, xn);
+        // keeps the scheduler from sinking the loads next to their uses
+        asm volatile("" ::: "memory");
+        classify(tile, f, x);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -883,7 +1011,9 @@ __global__ __launch_bounds__(SEL_THREADS) void k_topr_final(Work w) {
 hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, uint32_t redo_blocks, bool any_topr,
                        hipStream_t s) {
     const bool sampled = redo_blocks > 0;
-    const int fgrid = resident_grid(k_select_filter<0, false>, FILTER_THREADS, w.ntiles_total);
+    // the wave-per-tile form: at least 8 tiles per wave (vgg16_138m: 193
+    // against 206 µs with a wave per tile; a 16-tile floor was slower again)
+    const int fgrid = resident_grid(k_select_filter_wave<0>, SF_THREADS, (w.ntiles_total + 31) / 32);
     if (any_topr && hist_blocks > 0) {
         k_topr_hist<0><<<hist_blocks, HIST_THREADS, 0, s>>>(w, g);
         trace_mark(s, "k_topr_hist");
@@ -891,9 +1021,10 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, uint
     if (any_topr && sampled) {
         k_topr_pick<<<w.ntensors, HIST_THREADS, 0, s>>>(w);
         trace_mark(s, "k_topr_pick");
-        k_select_filter<0, true><<<fgrid, FILTER_THREADS, 0, s>>>(w, g);
+        k_select_filter_wave<0><<<fgrid, SF_THREADS, 0, s>>>(w, g);
     } else {
-        k_select_filter<0, false><<<fgrid, FILTER_THREADS, 0, s>>>(w, g);
+        k_select_filter_blk<<<resident_grid(k_select_filter_blk, FILTER_THREADS, w.ntiles_total),
+                                         FILTER_THREADS, 0, s>>>(w, g);
     }
     trace_mark(s, "k_select_filter");
     if (any_topr) {
@@ -902,7 +1033,7 @@ hipError_t launch_topr(const Work &w, const float *g, uint32_t hist_blocks, uint
             // tensors return at once)
             k_topr_hist<1><<<redo_blocks, HIST_THREADS, 0, s>>>(w, g);
             trace_mark(s, "k_topr_hist_redo");
-            k_select_filter<1, true><<<fgrid, FILTER_THREADS, 0, s>>>(w, g);
+            k_select_filter_wave<1><<<fgrid, SF_THREADS, 0, s>>>(w, g);
             trace_mark(s, "k_select_filter_redo");
         }
         k_topr_candpass<<<resident_grid(k_topr_candpass, NTHREADS, (w.ntiles_total + CP_TILES - 1) / CP_TILES), NTHREADS, 0, s>>>(w);
@@ -1017,7 +1148,8 @@ hipError_t launch_compact_selection(const Work &w, const float *g, float *val_ou
 
 hipError_t launch_nonzero(const Work &w, const float *g, int grid_persist, hipStream_t s) {
     (void)grid_persist;
-    k_select_filter<0, false><<<resident_grid(k_select_filter<0, false>, FILTER_THREADS, w.ntiles_total), FILTER_THREADS, 0, s>>>(w, g);
+    k_select_filter_blk<<<resident_grid(k_select_filter_blk, FILTER_THREADS, w.ntiles_total),
+                                     FILTER_THREADS, 0, s>>>(w, g);
     trace_mark(s, "k_select_filter");
     // |S| from the per-tile counts of the filter pass
     k_tile_scan<<<w.ntensors, TSCAN_THREADS, 0, s>>>(w);
