@@ -87,11 +87,14 @@ int persist_grid(int per_cu) { return dr::device_cus() * per_cu; }
 struct Carve {
     uint64_t slots = 0, ntiles = 0, ntensors = 0, hist_blocks = 0, redo_blocks = 0, fit_blocks = 0, btab = 0,
              bslices = 0, bnd = 0, segslots = 0;
+    // bucketed query: list entries (the largest such tensor's size), count
+    // table words and round-total words; both carves hold them
+    uint64_t qb_entries = 0, qb_tab = 0, qb_rows = 0;
     bool query_only = false;  // descriptors, tile counts, the positives bitmap and the tile table only
     size_t bytes = 0;
     size_t o_td, o_glob, o_pstat, o_histA, o_shist, o_fcnt, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
         o_V, o_sstat, o_sdig, o_ttab, o_fit, o_btab, o_brow, o_keyA, o_keyB, o_valA, o_valB, o_sig, o_vs, o_bnd,
-        o_segst, o_segpart;
+        o_segst, o_segpart, o_qlist, o_qbkt, o_qtab, o_qrow;
 
     void plan() {
         size_t at = 0;
@@ -108,6 +111,10 @@ struct Carve {
         o_toff = take(4 * ntiles);
         o_pbits = take(slots / 8);
         o_ttab = take(4ull * ntiles);
+        o_qlist = take(4 * qb_entries);
+        o_qbkt = take(4 * qb_entries);
+        o_qtab = take(4 * qb_tab);
+        o_qrow = take(4 * qb_rows);
         o_ccnt = take(all * 4 * ntiles);
         // the selection's counters, contiguous: k_init clears them as one range
         o_hist = take(all * 4ull * HIST1_BINS * ntensors);
@@ -179,6 +186,11 @@ struct Carve {
         w.bounds = (uint32_t *)(ws + o_bnd);
         w.segst = (SegState *)(ws + o_segst);
         w.segpart = (SegPart *)(ws + o_segpart);
+        w.qlist = (uint32_t *)(ws + o_qlist);
+        w.qbkt = (uint32_t *)(ws + o_qbkt);
+        w.qtab = (uint32_t *)(ws + o_qtab);
+        w.qrow = (uint32_t *)(ws + o_qrow);
+        w.qcap = qb_entries;
         return w;
     }
 
@@ -258,6 +270,11 @@ Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     // item count
     c.bslices = 47 * c.slots / (1u << SLICE_LOG2_MIN) + 2 * n_tensors + BL_MAX_SLICES;
     c.btab = c.bslices * MAX_CHUNKS;
+    // the bucketed query of one tensor of at most d elements: at most
+    // QB_MAX_BINS bins of ceil(d / QB_CH) chunks each, rounds for k <= 32
+    c.qb_entries = c.slots;
+    c.qb_tab = (uint64_t)QB_MAX_BINS * (c.slots / QB_CH + 1);
+    c.qb_rows = 33ull * QB_MAX_BINS;
     c.plan();
     return c;
 }
@@ -269,6 +286,8 @@ struct Plan {
     uint32_t bl_chunks = 0, bl_slices = 0, max_slices = 0, hash_per_round = 1, kmax = 0;
     uint64_t bl_items = 0;
     std::vector<uint64_t> bl_mcap;  // planned filter bits per tensor
+    std::vector<QbTensor> qb;       // tensors given the bucketed query
+    uint32_t qb_min_bits = 0, qb_k = 0;
     bool any_topr = false;
     bool direct = false;  // every filter small enough for the direct insert
     bool segment = false; // some tensor needs the segmentation pass (chord, or the heuristic count)
@@ -374,6 +393,54 @@ void plan_bloom_direct(Plan &p, bool from_bitmap) {
     p.dir_slices = (uint32_t)sl;
 }
 
+// The receiver's bucketed query, for tensors whose filter may be larger
+// than an XCD's L2: those of at most QB_MAX_D elements whose largest filter (m for their
+// n_cap items) has at least qb_min_bits() bits, the first QB_MAX_TENSORS of
+// them.  The kernels check the actual filter against the same threshold and
+// leave smaller ones to the probe pass.  The environment variable
+// DR_QUERY_BUCKET_MIN_BITS replaces the threshold (the tests lower it to
+// run the path on small tensors).
+constexpr uint64_t QB_MIN_BITS_DEFAULT = 1ull << 25;  // 4 MiB, an XCD's L2
+constexpr size_t QB_MAX_TENSORS = 16;
+
+uint64_t qb_min_bits() {
+    const char *e = getenv("DR_QUERY_BUCKET_MIN_BITS");
+    if (!e || !*e) return QB_MIN_BITS_DEFAULT;
+    char *end = nullptr;
+    const unsigned long long v = strtoull(e, &end, 10);
+    return (end && *end == 0) ? std::min<uint64_t>(v, 0xffffffffull) : QB_MIN_BITS_DEFAULT;
+}
+
+void plan_query_bucketed(Plan &p, bool allow) {
+    p.qb.clear();
+    p.carve.qb_entries = p.carve.qb_tab = p.carve.qb_rows = 0;
+    if (!allow) return;
+    const uint64_t mb = qb_min_bits();
+    uint64_t ent = 0, tab = 0;
+    uint32_t k = 0;
+    for (size_t t = 0; t < p.t.size() && p.qb.size() < QB_MAX_TENSORS; ++t) {
+        const TInit &in = p.t[t];
+        const uint64_t m = p.bl_mcap[t];
+        if (in.k < 1 || m < mb || in.d < 1 || in.d > QB_MAX_D) continue;
+        QbTensor q;
+        q.t = (uint32_t)t;
+        q.nsl_cap = (uint32_t)ceil_div(m, 1ull << QB_SL);
+        q.nch_cap = (uint32_t)ceil_div(in.d, QB_CH);
+        q.nreg = (uint32_t)ceil_div(in.d, 1ull << QB_RL);
+        if (q.nsl_cap > QB_MAX_BINS || q.nreg > QB_MAX_BINS) continue;
+        p.qb.push_back(q);
+        ent = std::max<uint64_t>(ent, in.d);
+        tab = std::max<uint64_t>(tab, (uint64_t)std::max(q.nsl_cap, q.nreg) * q.nch_cap);
+        k = in.k;
+    }
+    if (p.qb.empty()) return;
+    p.qb_min_bits = (uint32_t)mb;
+    p.qb_k = k;
+    p.carve.qb_entries = align_up(ent, 64);
+    p.carve.qb_tab = tab;
+    p.carve.qb_rows = (uint64_t)(k + 1) * QB_MAX_BINS;
+}
+
 dr_status check_cfg(const dr_config *cfg) {
     if (!cfg) return fail(DR_EINVAL, "cfg is null");
     if (cfg->n_tensors < 1 || cfg->n_tensors > DR_MAX_TENSORS) return fail(DR_EINVAL, "n_tensors out of range");
@@ -417,7 +484,7 @@ uint64_t record_capacity(uint64_t d, uint64_t n_cap, double fpr, uint32_t degree
 }
 
 // The per-tensor plan of a round trip (sender and receiver use the same one).
-dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_off) {
+dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_off, bool allow_qb = true) {
     dr_status st = check_cfg(cfg);
     if (st != DR_OK) return st;
     const uint64_t T = cfg->n_tensors;
@@ -511,6 +578,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
     p.carve.redo_blocks = redo_blocks;
     p.carve.fit_blocks = fit_blocks;
     p.carve.bnd = bnd;
+    plan_query_bucketed(p, allow_qb);
     p.carve.plan();
     plan_bloom_rounds(p, k);
     plan_bloom_direct(p, true);
@@ -559,8 +627,8 @@ struct Encode {
 };
 
 dr_status encode_prepare(const float *g, const dr_config *cfg, uint8_t *payload, size_t payload_bytes,
-                         uint64_t *counts_out, void *ws, size_t ws_bytes, Encode &e) {
-    dr_status st = plan_config(cfg, e.p, e.rec_off);
+                         uint64_t *counts_out, void *ws, size_t ws_bytes, Encode &e, bool allow_qb = true) {
+    dr_status st = plan_config(cfg, e.p, e.rec_off, allow_qb);
     if (st != DR_OK) return st;
     if (!g && cfg->offsets_h[cfg->n_tensors] > 0) return fail(DR_EINVAL, "g is null");
     if (!payload || payload_bytes < e.rec_off.back()) return fail(DR_EINVAL, "payload buffer too small");
@@ -633,8 +701,9 @@ struct Decode {
 };
 
 dr_status decode_prepare(const uint8_t *payload, const dr_config *cfg, float *dense_out, uint32_t *idx_out,
-                         float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, Decode &dd) {
-    dr_status st = plan_config(cfg, dd.p, dd.rec_off);
+                         float *val_out, uint64_t *counts_out, void *ws, size_t ws_bytes, Decode &dd,
+                         bool allow_qb = true) {
+    dr_status st = plan_config(cfg, dd.p, dd.rec_off, allow_qb);
     if (st != DR_OK) return st;
     if (!payload) return fail(DR_EINVAL, "payload is null");
     if (!dense_out && cfg->offsets_h[cfg->n_tensors] > 0) return fail(DR_EINVAL, "dense_out is null");
@@ -655,13 +724,19 @@ dr_status decode_prepare(const uint8_t *payload, const dr_config *cfg, float *de
     return DR_OK;
 }
 
-// Bytes of a receiver's query-only work for the plan's layout.
-Carve query_carve(const Plan &p) {
+// Bytes of a receiver's query-only work for the plan's layout (with or
+// without regions of its own for the bucketed query).
+Carve query_carve(const Plan &p, bool with_qb = true) {
     Carve c;
     c.query_only = true;
     c.ntensors = p.carve.ntensors;
     c.ntiles = p.carve.ntiles;
     c.slots = p.carve.slots;
+    if (with_qb) {
+        c.qb_entries = p.carve.qb_entries;
+        c.qb_tab = p.carve.qb_tab;
+        c.qb_rows = p.carve.qb_rows;
+    }
     c.plan();
     return c;
 }
@@ -672,6 +747,7 @@ dr_status decode_init(Decode &dd, bool query_only, hipStream_t s) {
 }
 
 dr_status decode_probe(Decode &dd, uint32_t max_probe_blocks, hipStream_t s) {
+    for (const QbTensor &q : dd.p.qb) DR_HIP(launch_query_bucketed(dd.w, q, dd.p.qb_k, dd.p.qb_min_bits, s));
     DR_HIP(launch_probe_decode(dd.w, dd.dense_out, dd.counts_out, max_probe_blocks, s));
     return DR_OK;
 }
@@ -743,7 +819,9 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
     Decode dd;
     st = decode_prepare(payload, cfg, dense_out, idx_out, val_out, counts_out, ws, ws_bytes, dd);
     if (st != DR_OK) return st;
-    const Carve qc = query_carve(dd.p);
+    // the receiver's bucketed query borrows the sender's lists and tables,
+    // which the sender does not use
+    const Carve qc = query_carve(dd.p, false);
     const size_t qoff = align_up(e.p.carve.bytes, 256);
     // one fork/join sequence at a time per process, so that the two events
     // are not re-recorded by another thread between a record and its wait
@@ -757,6 +835,11 @@ dr_status roundtrip_impl(const float *g, const dr_config *cfg, uint8_t *payload,
         // stream runs it (once the caller's earlier work on s is done) while
         // the sender selects
         dd.w = qc.view((uint8_t *)ws + qoff);
+        dd.w.qlist = e.w.qlist;
+        dd.w.qbkt = e.w.qbkt;
+        dd.w.qtab = e.w.qtab;
+        dd.w.qrow = e.w.qrow;
+        dd.w.qcap = e.w.qcap;
         DR_HIP(hipEventRecord(ss->start, s));
         DR_HIP(hipStreamWaitEvent(ss->s, ss->start, 0));
         trace_call(ss->s);  // per-kernel timing: the side stream's kernels count from here
@@ -835,7 +918,7 @@ dr_status roundtrip_static_impl(const float *g, const dr_config *cfg, uint8_t *p
     {
         Plan p;
         std::vector<uint64_t> rec_off;
-        dr_status st = plan_config(cfg, p, rec_off);
+        dr_status st = plan_config(cfg, p, rec_off, false);
         if (st != DR_OK) return st;
         if (p.carve.bytes > DR_STATIC_SCRATCH_BYTES)
             return fail(DR_ECAPACITY, "this gradient needs %zu bytes of scratch; the static scratch holds %zu "
@@ -845,10 +928,13 @@ dr_status roundtrip_static_impl(const float *g, const dr_config *cfg, uint8_t *p
     dr_status st = static_scratch(&ws);
     if (st != DR_OK) return st;
     Encode e;
-    st = encode_prepare(g, cfg, payload, payload_bytes, counts_out, ws, DR_STATIC_SCRATCH_BYTES, e);
+    // without the bucketed query, whose lists would take scratch the array
+    // does not have
+    st = encode_prepare(g, cfg, payload, payload_bytes, counts_out, ws, DR_STATIC_SCRATCH_BYTES, e, false);
     if (st != DR_OK) return st;
     Decode dd;
-    st = decode_prepare(payload, cfg, dense_out, idx_out, val_out, counts_out, ws, DR_STATIC_SCRATCH_BYTES, dd);
+    st = decode_prepare(payload, cfg, dense_out, idx_out, val_out, counts_out, ws, DR_STATIC_SCRATCH_BYTES, dd,
+                        false);
     if (st != DR_OK) return st;
     trace_call(s);
     st = encode_front(e, g, counts_out, s);

@@ -882,9 +882,12 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
         const uint32_t nq = (re - rb) * QPT;
         bool ok;
         const RecordView rv = query_filter(w, o, td, MODE, &ok);
+        // a tensor the bucketed query has done: its positives bitmap is
+        // written, and the pass only counts it
+        const bool pre = __builtin_amdgcn_readfirstlane(td.qb) != 0u;
         __syncthreads();  // the previous run is finished with fc, tcl and next
         if (t != cached) {
-            fcw = min(rv.m_bits / 32u, FC_WORDS);
+            fcw = pre ? 0u : min(rv.m_bits / 32u, FC_WORDS);
             for (uint32_t x = threadIdx.x; x < fcw; x += PB_THREADS) fc[x] = rv.bits[x];
             if (rv.layout == LAYOUT_PARTITIONED) fill_part_starts(ps, rv.m_bits, rv.k);
             cached = t;
@@ -925,6 +928,19 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
                     for (uint32_t e = lane; e < QWAVE; e += 64)
                         if (wbase + e < d) dz[e] = 0.0f;
                 }
+            }
+            if (pre) {
+                const uint32_t pw =
+                    lane < QWAVE / 32 ? w.pbits[(uint64_t)tile * TILE_WORDS + (qi % QPT) * (QWAVE / 32) + lane] : 0u;
+                const uint32_t pc = wave_sum(__popc(pw));
+                if (lane == 0) atomicAdd(&tcl[qi / QPT], pc);
+                // the wave reconverges here, before the next step's ticket:
+                // without it the compiler merged this lane-0 branch with
+                // the ticket's (also lane 0), so that lanes 1..63 reached
+                // the ticket's readfirstlane without lane 0, read step 0
+                // from it again and again, and the pass never ended
+                __builtin_amdgcn_wave_barrier();
+                continue;
             }
             if (lane < QWAVE / 32) mw[lane] = 0;
             __builtin_amdgcn_wave_barrier();
@@ -1034,6 +1050,346 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
     }
     __syncthreads();  // the block's tile counts are written; fc is free
     probe_scan<MODE>(w, o, t_begin, t_end, fc);
+}
+
+// ---------------------------------------------------------------------------
+// Bucketed query
+// ---------------------------------------------------------------------------
+// For a filter larger than an XCD's L2, every probe of the probe pass is a
+// random read from the last-level cache, and the pass runs at the fabric's
+// rate for such reads (ncf_32m: the receiver's 273 M probes of a 46 MB
+// filter, most of them the k probes of each of its 19 M positives).  The
+// receiver's bucketed query takes the probes one hash at a time and brings
+// them to the filter instead:
+//  * round j < k: the live indices (round 0: all of the tensor's) are
+//    counted per chunk of the list and per bin, the bin being the filter
+//    slice (2^QB_SL bits) that hash j's bit falls in; a scan of the counts
+//    gives each (bin, chunk) its place, and a scatter writes the indices
+//    bin by bin (qbkt).  One block per slice then loads its slice into LDS
+//    and tests its bin's indices, writing each index, or QB_DEAD where its
+//    bit is clear, to the same place of qlist: the next round's list;
+//  * round k: the survivors, which are the positives, are bucketed the same
+//    way by index region (2^QB_RL indices), and one block per region sets
+//    their bits in an LDS copy of the region's bitmap and writes it out.
+// The probe pass then only counts that bitmap.  Every global access is a
+// stream; the random ones go to LDS.  The kernels are launched per tensor
+// and decide alike, from the record's header, whether the tensor is theirs
+// (k as planned, a filter of at least min_bits that the work has room
+// for); one that is not is left to the probe pass.  The sender keeps its
+// probe pass: it skips its own selection, so it probes far fewer indices,
+// most of them once, and the rounds' fixed costs outweigh what they save
+// there (ncf_32m: 1.17 ms in rounds against 0.76 ms).
+struct QbArgs {
+    uint32_t t;         // tensor
+    uint32_t k;         // hashes planned on the host
+    uint32_t min_bits;  // smallest filter taken this way
+    uint32_t nsl_cap;   // slices the work has room for
+    uint32_t nch_cap;   // chunks per bin row of qtab
+};
+
+constexpr uint32_t QB_TEST_THREADS = 512;
+
+__device__ __forceinline__ uint32_t qb_slices(uint32_t m_bits) {
+    return (uint32_t)(((uint64_t)m_bits + (1u << QB_SL) - 1) >> QB_SL);
+}
+__device__ __forceinline__ uint32_t qb_regions(uint32_t d) {
+    return (uint32_t)(((uint64_t)d + (1u << QB_RL) - 1) >> QB_RL);
+}
+
+__device__ __forceinline__ bool qb_usable(const RecordView &rv, bool ok, const TDesc &td, const QbArgs &a) {
+    return ok && rv.k >= 1 && rv.k == a.k && rv.m_bits >= a.min_bits && qb_slices(rv.m_bits) <= a.nsl_cap &&
+           td.in.d >= 1 && td.in.d <= QB_MAX_D;
+}
+
+// v[0] + ... + v[n-1], for every thread of the block (NT threads)
+template <uint32_t NT>
+__device__ __forceinline__ uint32_t qb_sum(const uint32_t *v, uint32_t n, uint32_t *scratch) {
+    uint32_t s = 0;
+    for (uint32_t b = threadIdx.x; b < n; b += NT) s += v[b];
+    s = wave_sum(s);
+    __syncthreads();  // scratch is free
+    if ((threadIdx.x & 63u) == 0) scratch[threadIdx.x >> 6] = s;
+    __syncthreads();
+    uint32_t tot = 0;
+#pragma unroll
+    for (uint32_t q = 0; q < NT / 64; ++q) tot += scratch[q];
+    __syncthreads();  // every thread has read scratch
+    return tot;
+}
+
+// Round j's list length: the tensor's size in round 0, else the entries the
+// previous round bucketed (the sum of its bin totals).
+template <uint32_t NT>
+__device__ __forceinline__ uint32_t qb_len(const Work &w, const TDesc &td, uint32_t j, uint32_t nsl,
+                                           uint32_t *scratch) {
+    return j == 0 ? td.in.d : qb_sum<NT>(w.qrow + (j - 1) * QB_MAX_BINS, nsl, scratch);
+}
+
+// Entries [b0, b0 + QB_SUB) of round j's list, QB_PER per thread; QB_DEAD
+// past the list's end and for an index that failed a probe.
+__device__ __forceinline__ void qb_load(const Work &w, uint32_t j, uint32_t b0, uint32_t len, uint32_t *e) {
+    const uint32_t x0 = b0 + threadIdx.x;
+    if (j == 0) {
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            const uint32_t x = x0 + u * QB_THREADS;
+            e[u] = x < len ? x : QB_DEAD;
+        }
+    } else {
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            const uint32_t x = x0 + u * QB_THREADS;
+            e[u] = x < len ? w.qlist[x] : QB_DEAD;
+        }
+    }
+}
+
+// bin of index i in round j: the slice of hash j's bit, or (last round) the
+// index region
+__device__ __forceinline__ uint32_t qb_key(const PosMap &pm, uint32_t i, uint32_t j, bool fin) {
+    return fin ? (i >> QB_RL) : (pm(mm3_key(i), j) >> QB_SL);
+}
+
+// Counts of chunk c's entries per bin: column c of qtab.
+template <int MODE>
+__global__ __launch_bounds__(QB_THREADS) void k_qb_count(Work w, QbArgs a, uint32_t j) {
+    __shared__ uint32_t h[QB_MAX_BINS];
+    __shared__ uint32_t ps[33];
+    __shared__ uint32_t scratch[QB_THREADS / 64 + 1];
+    TDesc &td = w.td[a.t];
+    const QueryOut o{};
+    bool ok;
+    const RecordView rv = query_filter(w, o, td, MODE, &ok);
+    if (j == 0) {
+        if (!qb_usable(rv, ok, td, a)) return;
+        if (blockIdx.x == 0 && threadIdx.x == 0) td.qb = 1u;
+    } else if (!td.qb) {
+        return;
+    }
+    const uint32_t d = td.in.d, nsl = qb_slices(rv.m_bits);
+    const bool fin = j == rv.k;
+    const uint32_t nb = fin ? qb_regions(d) : nsl;
+    const uint32_t len = qb_len<QB_THREADS>(w, td, j, nsl, scratch);
+    const uint32_t c = blockIdx.x;
+    if ((uint64_t)c * QB_CH >= len) return;
+    const bool part = rv.layout == LAYOUT_PARTITIONED;
+    if (part) fill_part_starts(ps, rv.m_bits, rv.k);
+    for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) h[b] = 0;
+    __syncthreads();
+    const PosMap pm{rv.m_bits, part ? ps : nullptr};
+    for (uint32_t b0 = c * QB_CH; b0 < min(len, (c + 1) * QB_CH); b0 += QB_SUB) {
+        uint32_t e[QB_PER];
+        qb_load(w, j, b0, len, e);
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            if (e[u] != QB_DEAD) {
+                const uint32_t b = qb_key(pm, e[u], j, fin);
+                if (b < nb) atomicAdd(&h[b], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) w.qtab[(uint64_t)b * a.nch_cap + c] = h[b];
+}
+
+// One block per bin: its row of qtab becomes each chunk's offset within the
+// bin's bucket, and the bin's total goes to qrow.
+template <int MODE>
+__global__ __launch_bounds__(QB_THREADS) void k_qb_scan(Work w, QbArgs a, uint32_t j) {
+    __shared__ uint32_t scratch[QB_THREADS / 64 + 1];
+    TDesc &td = w.td[a.t];
+    if (!td.qb) return;
+    const QueryOut o{};
+    bool ok;
+    const RecordView rv = query_filter(w, o, td, MODE, &ok);
+    const uint32_t d = td.in.d, nsl = qb_slices(rv.m_bits);
+    const uint32_t nb = j == rv.k ? qb_regions(d) : nsl;
+    const uint32_t b = blockIdx.x;
+    if (b >= nb) return;
+    const uint32_t len = qb_len<QB_THREADS>(w, td, j, nsl, scratch);
+    const uint32_t nch = (len + QB_CH - 1) / QB_CH;
+    uint32_t *row = w.qtab + (uint64_t)b * a.nch_cap;
+    uint32_t carry = 0;
+    for (uint32_t c0 = 0; c0 < nch; c0 += QB_THREADS) {
+        const uint32_t c = c0 + threadIdx.x;
+        const uint32_t v = c < nch ? row[c] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan_n<QB_THREADS>(v, scratch, &tot);
+        if (c < nch) row[c] = carry + ex;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) w.qrow[j * QB_MAX_BINS + b] = carry;
+}
+
+// Chunk c's entries into their bins' buckets (qbkt): grouped by bin in LDS
+// (ranks from LDS atomics, a scan of the bins' counts, the placement), then
+// written bin by bin, so that consecutive lanes store to consecutive
+// addresses.  The order within a bucket does not matter: a bucket's
+// indices are tested independently, and the positives end up in a bitmap.
+template <int MODE>
+__global__ __launch_bounds__(QB_THREADS) void k_qb_scatter(Work w, QbArgs a, uint32_t j) {
+    __shared__ uint32_t bst[QB_MAX_BINS];  // where the chunk's entries of each bin go
+    __shared__ uint32_t lc[QB_MAX_BINS];   // the chunk's entries per bin
+    __shared__ uint32_t lo[QB_MAX_BINS];   // their first place in the staging area
+    __shared__ uint32_t stage[QB_SUB];
+    __shared__ uint16_t sb[QB_SUB];
+    __shared__ uint32_t ps[33];
+    __shared__ uint32_t scratch[QB_THREADS / 64 + 1];
+    static_assert(QB_MAX_BINS <= 65536, "bins are staged as 16-bit numbers");
+    TDesc &td = w.td[a.t];
+    if (!td.qb) return;
+    const QueryOut o{};
+    bool ok;
+    const RecordView rv = query_filter(w, o, td, MODE, &ok);
+    const uint32_t d = td.in.d, nsl = qb_slices(rv.m_bits);
+    const bool fin = j == rv.k;
+    const uint32_t nb = fin ? qb_regions(d) : nsl;
+    const uint32_t len = qb_len<QB_THREADS>(w, td, j, nsl, scratch);
+    const uint32_t c = blockIdx.x;
+    if ((uint64_t)c * QB_CH >= len) return;
+    const bool part = rv.layout == LAYOUT_PARTITIONED;
+    if (part) fill_part_starts(ps, rv.m_bits, rv.k);
+    // bucket starts (exclusive scan of the round's bin totals), each plus
+    // this chunk's offset within the bucket
+    const uint32_t *rowj = w.qrow + j * QB_MAX_BINS;
+    uint32_t carry = 0;
+    for (uint32_t b0 = 0; b0 < nb; b0 += QB_THREADS) {
+        const uint32_t b = b0 + threadIdx.x;
+        const uint32_t v = b < nb ? rowj[b] : 0u;
+        uint32_t tot;
+        const uint32_t ex = block_excl_scan_n<QB_THREADS>(v, scratch, &tot);
+        if (b < nb) bst[b] = carry + ex + w.qtab[(uint64_t)b * a.nch_cap + c];
+        carry += tot;
+    }
+    const PosMap pm{rv.m_bits, part ? ps : nullptr};
+    for (uint32_t x0 = c * QB_CH; x0 < min(len, (c + 1) * QB_CH); x0 += QB_SUB) {
+        for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) lc[b] = 0;
+        uint32_t e[QB_PER];
+        qb_load(w, j, x0, len, e);
+        __syncthreads();  // lc is clear (and, the first time, bst and ps are set)
+        uint32_t key[QB_PER], rk[QB_PER];
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            key[u] = QB_DEAD;
+            rk[u] = 0;
+            if (e[u] != QB_DEAD) {
+                const uint32_t b = qb_key(pm, e[u], j, fin);
+                if (b < nb) {
+                    key[u] = b;
+                    rk[u] = atomicAdd(&lc[b], 1u);
+                }
+            }
+        }
+        __syncthreads();
+        carry = 0;
+        for (uint32_t b0 = 0; b0 < nb; b0 += QB_THREADS) {
+            const uint32_t b = b0 + threadIdx.x;
+            const uint32_t v = b < nb ? lc[b] : 0u;
+            uint32_t tot;
+            const uint32_t ex = block_excl_scan_n<QB_THREADS>(v, scratch, &tot);
+            if (b < nb) lo[b] = carry + ex;
+            carry += tot;
+        }
+        const uint32_t total = carry;
+        __syncthreads();
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            if (key[u] != QB_DEAD) {
+                const uint32_t q = lo[key[u]] + rk[u];
+                stage[q] = e[u];
+                sb[q] = (uint16_t)key[u];
+            }
+        }
+        __syncthreads();
+        for (uint32_t q = threadIdx.x; q < total; q += QB_THREADS) {
+            const uint32_t b = sb[q];
+            const uint32_t dst = bst[b] + (q - lo[b]);
+            if (dst < w.qcap) w.qbkt[dst] = stage[q];
+        }
+        __syncthreads();  // the stores have read bst, lo, sb and stage
+        // the next batch's entries of each bin go after this batch's
+        for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) bst[b] += lc[b];
+    }
+}
+
+// Round j's test: block s loads filter slice s into LDS and tests hash j of
+// the indices in its bucket; each goes back to its place in qlist, or
+// QB_DEAD if its bit is clear.
+template <int MODE>
+__global__ __launch_bounds__(QB_TEST_THREADS) void k_qb_test(Work w, QbArgs a, uint32_t j) {
+    __shared__ uint32_t sl[QB_SW];
+    __shared__ uint32_t ps[33];
+    __shared__ uint32_t scratch[QB_TEST_THREADS / 64 + 1];
+    TDesc &td = w.td[a.t];
+    if (!td.qb) return;
+    const QueryOut o{};
+    bool ok;
+    const RecordView rv = query_filter(w, o, td, MODE, &ok);
+    const uint32_t nsl = qb_slices(rv.m_bits);
+    const uint32_t s = blockIdx.x;
+    if (s >= nsl) return;
+    const uint32_t *rowj = w.qrow + j * QB_MAX_BINS;
+    const uint32_t start = qb_sum<QB_TEST_THREADS>(rowj, s, scratch), end = start + rowj[s];
+    const uint32_t w0 = s * QB_SW, nw = min(QB_SW, rv.m_bits / 32u - w0);
+    for (uint32_t q = threadIdx.x; q < nw; q += QB_TEST_THREADS) sl[q] = rv.bits[w0 + q];
+    const bool part = rv.layout == LAYOUT_PARTITIONED;
+    if (part) fill_part_starts(ps, rv.m_bits, rv.k);
+    __syncthreads();
+    const PosMap pm{rv.m_bits, part ? ps : nullptr};
+    const uint32_t p0 = s << QB_SL, nbits = nw * 32u;
+    for (uint32_t x0 = start + threadIdx.x; x0 < end; x0 += QB_TEST_THREADS * QB_PER) {
+        uint32_t e[QB_PER];
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            const uint32_t x = x0 + u * QB_TEST_THREADS;
+            e[u] = x < end ? w.qbkt[x] : QB_DEAD;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            const uint32_t x = x0 + u * QB_TEST_THREADS;
+            if (x < end) {
+                const uint32_t p = pm(mm3_key(e[u]), j) - p0;  // wraps for a bit below the slice
+                const bool alive = p < nbits && ((sl[p >> 5] >> (p & 31u)) & 1u);
+                if (x < w.qcap) w.qlist[x] = alive ? e[u] : QB_DEAD;
+            }
+        }
+    }
+}
+
+// Last step: block r sets the bits of the positives in index region r in an
+// LDS copy of the region's bitmap and writes the region's words of pbits.
+template <int MODE>
+__global__ __launch_bounds__(QB_TEST_THREADS) void k_qb_fill(Work w, QbArgs a) {
+    __shared__ uint32_t bm[QB_RW];
+    __shared__ uint32_t scratch[QB_TEST_THREADS / 64 + 1];
+    TDesc &td = w.td[a.t];
+    if (!td.qb) return;
+    const QueryOut o{};
+    bool ok;
+    const RecordView rv = query_filter(w, o, td, MODE, &ok);
+    const uint32_t d = td.in.d;
+    const uint32_t r = blockIdx.x;
+    if (r >= qb_regions(d)) return;
+    const uint32_t *rowk = w.qrow + rv.k * QB_MAX_BINS;
+    const uint32_t start = qb_sum<QB_TEST_THREADS>(rowk, r, scratch), end = start + rowk[r];
+    const uint32_t w0 = r * QB_RW, nw = min(QB_RW, td.in.ntiles * TILE_WORDS - w0);
+    for (uint32_t q = threadIdx.x; q < QB_RW; q += QB_TEST_THREADS) bm[q] = 0u;
+    __syncthreads();
+    const uint32_t i0 = r << QB_RL;
+    for (uint32_t x0 = start + threadIdx.x; x0 < end; x0 += QB_TEST_THREADS * QB_PER) {
+        uint32_t e[QB_PER];
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u) {
+            const uint32_t x = x0 + u * QB_TEST_THREADS;
+            e[u] = x < end ? w.qbkt[x] - i0 : QB_DEAD;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < QB_PER; ++u)
+            if (e[u] < (1u << QB_RL)) atomicOr(&bm[e[u] >> 5], 1u << (e[u] & 31u));
+    }
+    __syncthreads();
+    uint32_t *out = w.pbits + (uint64_t)td.in.tile0 * TILE_WORDS + w0;
+    for (uint32_t q = threadIdx.x; q < nw; q += QB_TEST_THREADS) out[q] = bm[q];
 }
 
 // The received value of a positive whose value number is vn (NO_SLOT: not
@@ -1335,6 +1691,26 @@ hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, 
     }
     k_emit<Q_ENCODE><<<resident_grid(k_emit<Q_ENCODE>, NTHREADS, w.ntiles_total), NTHREADS, 0, s>>>(w, o);
     trace_mark(s, "k_emit<Q_ENCODE>");
+    return hipGetLastError();
+}
+
+hipError_t launch_query_bucketed(const Work &w, const QbTensor &q, uint32_t k, uint32_t min_bits, hipStream_t s) {
+    if (k < 1 || q.nch_cap == 0 || q.nsl_cap == 0 || q.nreg == 0) return hipSuccess;
+    const QbArgs a{q.t, k, min_bits, q.nsl_cap, q.nch_cap};
+    for (uint32_t j = 0; j <= k; ++j) {
+        k_qb_count<Q_DECODE><<<q.nch_cap, QB_THREADS, 0, s>>>(w, a, j);
+        trace_mark(s, "k_qb_count");
+        k_qb_scan<Q_DECODE><<<j < k ? q.nsl_cap : q.nreg, QB_THREADS, 0, s>>>(w, a, j);
+        trace_mark(s, "k_qb_scan");
+        k_qb_scatter<Q_DECODE><<<q.nch_cap, QB_THREADS, 0, s>>>(w, a, j);
+        trace_mark(s, "k_qb_scatter");
+        if (j < k) {
+            k_qb_test<Q_DECODE><<<q.nsl_cap, QB_TEST_THREADS, 0, s>>>(w, a, j);
+            trace_mark(s, "k_qb_test");
+        }
+    }
+    k_qb_fill<Q_DECODE><<<q.nreg, QB_TEST_THREADS, 0, s>>>(w, a);
+    trace_mark(s, "k_qb_fill");
     return hipGetLastError();
 }
 

@@ -28,6 +28,22 @@ constexpr uint32_t MAX_CHUNKS = 256;           // Bloom insert: most item chunks
 constexpr uint32_t DIR_SLICE_LOG2 = 20;        // direct insert: 2^20-bit (128 KiB) slices in LDS
 constexpr uint32_t DIR_SLICE_WORDS = 1u << (DIR_SLICE_LOG2 - 5);
 constexpr uint64_t DIR_MAX_BITS = 8ull << DIR_SLICE_LOG2;  // at most 8 slices per tensor
+// Bucketed query (filters larger than an XCD's L2): rounds of one hash
+// each route the live indices to filter slices of 2^QB_SL bits held in LDS;
+// the positives are then bucketed by index region of 2^QB_RL indices.  Bins
+// of a round are slices or regions, at most QB_MAX_BINS of either; a chunk
+// is QB_CH list entries, staged QB_SUB at a time.
+constexpr uint32_t QB_SL = 19;                  // filter slice: 2^19 bits (64 KiB)
+constexpr uint32_t QB_SW = 1u << (QB_SL - 5);
+constexpr uint32_t QB_RL = 19;                  // index region: 2^19 indices (64 KiB of bitmap)
+constexpr uint32_t QB_RW = 1u << (QB_RL - 5);
+constexpr uint32_t QB_MAX_BINS = 2048;
+constexpr uint32_t QB_THREADS = 1024;
+constexpr uint32_t QB_PER = 16;                 // entries per thread of a staged batch
+constexpr uint32_t QB_SUB = QB_THREADS * QB_PER;
+constexpr uint32_t QB_CH = 2 * QB_SUB;          // entries per chunk
+constexpr uint32_t QB_MAX_D = 1u << 30;         // largest tensor taken this way (regions <= QB_MAX_BINS)
+constexpr uint32_t QB_DEAD = 0xffffffffu;       // list entry of an index that failed a probe
 constexpr int BUFFER_RSRC_WORD3 = 0x00020000;  // gfx9 buffer descriptor word 3 (32-bit dword format)
 constexpr uint32_t SLICE_LOG2_MIN = 14;       // Bloom fill slices: 2^14 to 2^20 bits (2 to 128 KiB of LDS)
 constexpr uint32_t SLICE_LOG2_MAX = 20;
@@ -196,6 +212,7 @@ struct TDesc {
     uint32_t rec_bytes;  // payload record: bytes in use
     uint32_t bl_end;     // Bloom insert: positions bucketed in the current round
     uint32_t model;      // value model used: FIT_DEXP needs at least 4 values, else FIT_POLY
+    uint32_t qb;         // the bucketed query found this tensor's filter and wrote its positives bitmap
 };
 
 static_assert(sizeof(TInit) % 4 == 0 && sizeof(TDesc) % 4 == 0, "descriptor layout");
@@ -259,6 +276,12 @@ struct Work {
     uint32_t *bounds;         // chord segmentation: segment starts (S_eff + 1 per tensor)
     SegState *segst;          // chord segmentation over the grid: per state slot
     SegPart *segpart;         // and SEG_GRID_BLOCKS partial results per slot
+    // bucketed query (one tensor at a time): the live indices of a round
+    // (qlist, with QB_DEAD for the ones that failed), the same bucketed by
+    // bin (qbkt), per (bin, chunk) counts then offsets (qtab, bins x
+    // qb_nch words) and each round's bin totals (qrow, QB_MAX_BINS per round)
+    uint32_t *qlist, *qbkt, *qtab, *qrow;
+    uint64_t qcap;            // entries of qlist and qbkt
 };
 
 // ---------------------------------------------------------------------------

@@ -75,6 +75,14 @@ hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_c
 // recorded between the two
 hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, uint64_t *counts_out, hipStream_t s,
                                hipEvent_t after_probe = nullptr);
+// The receiver's bucketed query of one tensor (a filter larger than an
+// XCD's L2): rounds of one hash each, then the positives bitmap; the probe
+// pass that follows counts it.  Caps of the work it was planned for:
+// nsl_cap filter slices, nch_cap list chunks, nreg index regions.
+struct QbTensor {
+    uint32_t t, nsl_cap, nch_cap, nreg;
+};
+hipError_t launch_query_bucketed(const Work &w, const QbTensor &q, uint32_t k, uint32_t min_bits, hipStream_t s);
 hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,
                               hipStream_t s);
 // the receiver's query in two halves: the probe pass (at most max_blocks

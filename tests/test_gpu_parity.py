@@ -728,3 +728,46 @@ def test_per_kernel_trace():
     tr = B.trace_end()
     assert "k_probe<Q_ENCODE>" in tr and "k_emit<Q_DECODE>" in tr
     assert all(n >= 1 and ms >= 0 for n, ms in tr.values())
+
+
+# ---------------------------------------------------------------------------
+# The bucketed query (rounds of one hash routed to filter slices in LDS),
+# which the library takes for filters of at least 2^25 bits: with the
+# threshold lowered to 1024 bits it runs on these small cases, for the
+# sender (which skips its own selection) and the receiver, in the round
+# trip and in a standalone decode of the same payload.
+# ---------------------------------------------------------------------------
+QB_CASES = {
+    "resnet20_conv_37k": RT_CASES["resnet20_conv_37k"],
+    "ragged_tensors": RT_CASES["ragged_tensors"],
+    "support_50k": RT_CASES["support_50k"],
+    # several index regions and filter slices, the bucketed insert before it
+    "support_1m": RT_CASES["support_1m"],
+    # more tensors than the path takes (16): the rest are probed as usual
+    "many_tensors_3m": RT_CASES["many_tensors_3m"],
+    # a 1.73 M-bit filter: four slices, 47 regions
+    "normal_12m": LAYOUT_CASES["normal_12m"],
+}
+
+
+@pytest.mark.parametrize("layout", [B.FILTER_STANDARD, B.FILTER_PARTITIONED], ids=["standard", "partitioned"])
+@pytest.mark.parametrize("name", list(QB_CASES))
+def test_roundtrip_bucketed_query_parity(name, layout, monkeypatch):
+    import torch
+
+    monkeypatch.setenv("DR_QUERY_BUCKET_MIN_BITS", "1024")
+    g, off, ratio, fpr, D, S = QB_CASES[name]
+    log(f"roundtrip {name} bucketed query layout={layout} d={g.size} tensors={len(off) - 1}")
+    cfg = B.Config(off, ratio, fpr, D, S, filter_layout=layout)
+    out = run_roundtrip(g, cfg)
+    refs = oracle.roundtrip(g, off, ratio, fpr, D, S,
+                            layout=oracle.LAYOUT_PARTITIONED if layout == B.FILTER_PARTITIONED else oracle.LAYOUT_STANDARD)
+    check_roundtrip(g, cfg, out, refs)
+    # the same payload through the standalone receiver
+    dense = torch.full((g.size,), 3.0, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(4 * cfg.n_tensors, dtype=torch.int64, device="cuda")
+    B.payload_decode(dev_tensor(out["payload"]), cfg, dense, None, None, counts, workspace(g.size, cfg.n_tensors))
+    sync()
+    c = host(counts).reshape(cfg.n_tensors, 4)
+    assert np.all(c[:, 3] == 0)
+    np.testing.assert_array_equal(host(dense), out["dense"])
