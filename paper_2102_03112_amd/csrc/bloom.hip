@@ -1221,13 +1221,18 @@ __global__ __launch_bounds__(QB_THREADS) void k_qb_scan(Work w, QbArgs a, uint32
     if (threadIdx.x == 0) w.qrow[j * QB_MAX_BINS + b] = carry;
 }
 
-// Chunk c's entries into their bins' buckets (qbkt): grouped by bin in LDS
-// (ranks from LDS atomics, a scan of the bins' counts, the placement), then
-// written bin by bin, so that consecutive lanes store to consecutive
-// addresses.  The order within a bucket does not matter: a bucket's
-// indices are tested independently, and the positives end up in a bitmap.
+// Chunk c's entries into their bins' buckets (qbkt), QB_SUB at a time:
+// grouped by bin in LDS (ranks from LDS atomics, a scan of the bins'
+// counts, the placement), then written bin by bin, so that consecutive
+// lanes store to consecutive addresses.  The order within a bucket does not
+// matter: a bucket's indices are tested independently, and the positives
+// end up in a bitmap.  Two blocks per CU (72 KiB of LDS and at most 64
+// VGPRs each): while one waits at a barrier the other's loads and stores
+// are in flight (ncf_32m: 1.57 ms against 2.11 with one block of twice the
+// staging).
 template <int MODE>
-__global__ __launch_bounds__(QB_THREADS) void k_qb_scatter(Work w, QbArgs a, uint32_t j) {
+__global__ __launch_bounds__(QB_THREADS) __attribute__((amdgpu_waves_per_eu(8))) void k_qb_scatter(Work w, QbArgs a,
+                                                                                                  uint32_t j) {
     __shared__ uint32_t bst[QB_MAX_BINS];  // where the chunk's entries of each bin go
     __shared__ uint32_t lc[QB_MAX_BINS];   // the chunk's entries per bin
     __shared__ uint32_t lo[QB_MAX_BINS];   // their first place in the staging area
