@@ -164,19 +164,22 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_bloom_rowbase(Work w, uint32_t
 
 // Scatter: each position goes to its slice's bucket, after the chunk's
 // offset within that bucket, as a 32-bit offset within the slice.  A block
-// takes its chunk's items 4096 at a time and their positions four hashes at
-// a time (16 K positions), groups them by slice in LDS (a counting sort:
+// takes its chunk's items 4096 at a time and their positions two hashes at
+// a time (8 K positions), groups them by slice in LDS (a counting sort:
 // ranks from LDS atomics, a scan of the counts, then the placement), and
 // writes each slice's run with consecutive lanes on consecutive addresses.
 // Stored straight from the hashing lanes, each 4-byte record was an L2
-// request of its own, and the pass ran at the L2 request rate.
+// request of its own, and the pass ran at the L2 request rate.  Two blocks
+// share a CU (76 KiB of LDS and at most 64 VGPRs each; four hashes per
+// group and one block per CU took 0.68 ms on ncf_32m, two 0.585 ms).
 constexpr uint32_t SC_ITEMS = 4096;                      // items per batch
-constexpr uint32_t SC_HASHES = 4;                        // hashes per group
+constexpr uint32_t SC_HASHES = 2;                        // hashes per group
 constexpr uint32_t SC_PER = SC_ITEMS / BL_THREADS;       // items per thread
 constexpr uint32_t SC_STAGE = SC_ITEMS * SC_HASHES;      // positions per group
 
 template <bool FROM_BITMAP>
-__global__ __launch_bounds__(BL_THREADS) void k_bloom_scatter(Work w, uint32_t j0, uint32_t j1) {
+__global__ __launch_bounds__(BL_THREADS) __attribute__((amdgpu_waves_per_eu(8))) void k_bloom_scatter(Work w, uint32_t j0,
+                                                                                                     uint32_t j1) {
     __shared__ uint32_t gcur[BL_MAX_SLICES];  // next record of this chunk in each slice's bucket
     __shared__ uint32_t cnt[BL_MAX_SLICES];   // the group's positions per slice
     __shared__ uint32_t off[BL_MAX_SLICES];   // their start in the staging area

@@ -24,7 +24,7 @@ constexpr uint32_t NTHREADS = 256;            // threads per block (4 waves of 6
 constexpr uint32_t NWAVES = NTHREADS / 64;
 constexpr uint32_t R_NONZERO = 0xFFFFFFFFu;   // select every nonzero
 constexpr uint32_t CHUNK_TILES = 16;          // Bloom insert from the bitmap: fewest tiles per chunk
-constexpr uint32_t MAX_CHUNKS = 256;           // Bloom insert: most item chunks per tensor
+constexpr uint32_t MAX_CHUNKS = 512;           // Bloom insert: most item chunks per tensor (two scatter blocks per CU)
 constexpr uint32_t DIR_SLICE_LOG2 = 20;        // direct insert: 2^20-bit (128 KiB) slices in LDS
 constexpr uint32_t DIR_SLICE_WORDS = 1u << (DIR_SLICE_LOG2 - 5);
 constexpr uint64_t DIR_MAX_BITS = 8ull << DIR_SLICE_LOG2;  // at most 8 slices per tensor
