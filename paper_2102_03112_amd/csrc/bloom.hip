@@ -931,12 +931,17 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
             if (MODE == Q_DECODE) {
                 // the receiver's dense output starts as zeros here, written
                 // while the filter reads (an L2-bound loop) are in flight;
-                // the emit pass then stores only the positives
+                // the emit pass then stores only the positives.  The zeros
+                // are stored non-temporally: they are not read again here,
+                // and the filter's lines keep the L2 to themselves
+                // (resnet50_25m: 192 -> 187.5 us)
                 float *dz = o.dense_out + td.in.off + wbase;
                 if (wbase + QWAVE <= d && ((uintptr_t)dz & 15u) == 0) {
+                    typedef float f4 __attribute__((ext_vector_type(4)));
+                    const f4 zero4 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
                     for (uint32_t u = 0; u < QWAVE / 256; ++u)
-                        ((float4 *)dz)[u * 64 + lane] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                        __builtin_nontemporal_store(zero4, &((f4 *)dz)[u * 64 + lane]);
                 } else {
                     for (uint32_t e = lane; e < QWAVE; e += 64)
                         if (wbase + e < d) dz[e] = 0.0f;
