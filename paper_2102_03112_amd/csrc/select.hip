@@ -476,26 +476,36 @@ constexpr uint32_t NO_TENSOR = 0xffffffffu;
 template <int PHASE>
 __global__ __launch_bounds__(SF_THREADS) void k_select_filter_wave(Work w, const float *__restrict__ g) {
     constexpr bool COUNT = PHASE == 0;  // brackets from the pick kernel; exact counts
+    static_assert(NBR * 16 <= 64, "a lane's bracket-bin counts fit one 64-bit word");
     const uint32_t lane = threadIdx.x & 63u;
     const uint32_t gw = blockIdx.x * (SF_THREADS / 64) + (threadIdx.x >> 6);  // this wave, over the grid
     const uint32_t nw = gridDim.x * (SF_THREADS / 64);
     const uint32_t hcopy = gw % HISTA_COPIES, ccopy = gw % FCNT_COPIES;
     if (PHASE == 1 && !w.glob->redo) return;  // no tensor missed its bracket
     uint32_t cur_t = NO_TENSOR, bL = 0, bH = 0;  // tensor whose bracket the wave holds, and the bracket
-    uint32_t acc_def = 0, acc_x[NBR];            // COUNT: the wave's counts of tensor cur_t
-#pragma unroll
-    for (uint32_t x = 0; x < NBR; ++x) acc_x[x] = 0;
+    // COUNT: the wave's count above the bracket of tensor cur_t, and each
+    // lane's count per bracket bin (16-bit fields, bin bL + x in bits
+    // [16 x, 16 x + 16)); a lane adds at most 64 per tile, so the fields
+    // are emptied at least every FLUSH_TILES tiles
+    constexpr uint32_t FLUSH_TILES = 1000;
+    uint32_t acc_def = 0, since = 0;
+    uint64_t acc_x = 0;
     auto flush = [&]() {
-        if (COUNT && cur_t != NO_TENSOR && lane == 0) {
-            uint32_t *c = w.fcnt + ((uint64_t)cur_t * FCNT_COPIES + ccopy) * FCNT_W;
-            if (acc_def) atomicAdd(&c[0], acc_def);
+        if (COUNT && cur_t != NO_TENSOR) {
+            uint32_t cx[NBR];
 #pragma unroll
-            for (uint32_t x = 0; x < NBR; ++x)
-                if (acc_x[x]) atomicAdd(&c[1 + x], acc_x[x]);
+            for (uint32_t x = 0; x < NBR; ++x) cx[x] = wave_sum((uint32_t)(acc_x >> (16 * x)) & 0xffffu);
+            if (lane == 0) {
+                uint32_t *c = w.fcnt + ((uint64_t)cur_t * FCNT_COPIES + ccopy) * FCNT_W;
+                if (acc_def) atomicAdd(&c[0], acc_def);
+#pragma unroll
+                for (uint32_t x = 0; x < NBR; ++x)
+                    if (cx[x]) atomicAdd(&c[1 + x], cx[x]);
+            }
         }
         acc_def = 0;
-#pragma unroll
-        for (uint32_t x = 0; x < NBR; ++x) acc_x[x] = 0;
+        acc_x = 0;
+        since = 0;
     };
     // PHASE 0 reads the next tile's first values while it classifies a
     // tile's last ones; the redo reads a tile only once it knows the tile's
@@ -512,73 +522,104 @@ __global__ __launch_bounds__(SF_THREADS) void k_select_filter_wave(Work w, const
             if (!w.td[f.t].sfail) continue;  // wave-uniform
             sf_load(g, f, 0, xn);
         }
-        if (!f.nz && f.t != cur_t) {                   // wave-uniform
+        if (!f.nz && (f.t != cur_t || (COUNT && since == FLUSH_TILES))) {  // wave-uniform
             flush();
-            cur_t = f.t;
-            if constexpr (COUNT) {
-                bL = w.td[f.t].bL;
-                bH = w.td[f.t].bH;
+            if (f.t != cur_t) {
+                cur_t = f.t;
+                if constexpr (COUNT) {
+                    bL = w.td[f.t].bL;
+                    bH = w.td[f.t].bH;
+                } else {
+                    bL = bH = wave_pick_b1(w, f.t, f.base == 0);
+                }
+            }
+        }
+        // the tile's fields are wave-uniform: saying so keeps them, and the
+        // addresses below, in scalar registers
+        const uint32_t base = __builtin_amdgcn_readfirstlane(f.base);
+        const uint32_t lim = __builtin_amdgcn_readfirstlane(f.d) - base;  // elements of the tensor here (> 0)
+        const uint32_t span = bH - bL;
+        const uint64_t cb = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(f.slot >> 32)) << 32) |
+                            __builtin_amdgcn_readfirstlane((uint32_t)f.slot);
+        uint32_t *const ckey = w.cand_key + cb + base;  // the tile's stretch of the candidate arrays
+        uint32_t *const cidx = w.cand_idx + cb + base;
+        uint32_t *const histA =
+            w.histA + ((uint64_t)__builtin_amdgcn_readfirstlane(f.t) * HISTA_COPIES + hcopy) * HISTA_BINS;
+        uint32_t run = 0, ndef = 0, kmax = 0;
+        uint32_t wlo = 0, whi = 0;  // lane s: the ballot of step s
+        // one step of 64 elements; MODE 0: top-r, whole tile; 1: top-r, the
+        // tensor's last (partial) tile; 2: support (no candidates).  A value
+        // past the tensor's end reads as 0, so only a bracket reaching bin 0
+        // needs the lane mask.
+        auto step = [&](auto MODE, uint32_t st, float xv) {
+            const uint32_t key = mag_key(xv);
+            kmax = max(kmax, key);
+            const uint32_t bin = key >> HIST1_SHIFT;
+            uint64_t dm, cm = 0;
+            if constexpr (MODE() == 2) {
+                dm = __builtin_amdgcn_ballot_w64(key != 0u);
             } else {
-                bL = bH = wave_pick_b1(w, f.t, f.base == 0);
-            }
-        }
-        const uint32_t base = f.base, d = f.d;
-        const bool nz = f.nz;
-        const uint64_t cbase = f.slot + base;
-        uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * HISTA_BINS;
-        uint32_t run = 0, ndef = 0, nonfinite = 0;
-        uint64_t myword = 0;  // lane s: the ballot of step s
-        for (uint32_t grp = 0; grp < SF_GROUPS; ++grp) {
-            float x[SF_GROUP];
-#pragma unroll
-            for (uint32_t u = 0; u < SF_GROUP; ++u) x[u] = xn[u];
-            if (grp + 1 < SF_GROUPS) {
-                sf_load(g, f, grp + 1, xn);
-            } else if (PHASE == 0 && tile + nw < w.ntiles_total) {
-                fn = filter_tile(w, tile + nw);
-                sf_load(g, fn, 0, xn);
-            }
-            // keeps the scheduler from sinking the loads next to their uses
-            asm volatile("" ::: "memory");
-#pragma unroll
-            for (uint32_t u = 0; u < SF_GROUP; ++u) {
-                const uint32_t st = grp * SF_GROUP + u;  // elements [64 st, 64 st + 64) of the tile
-                const uint32_t i = base + st * 64u + lane;
-                const bool valid = i < d;
-                const uint32_t key = valid ? mag_key(x[u]) : 0u;
-                nonfinite |= key >= 0x7f800000u;
-                const uint32_t bin = key >> HIST1_SHIFT;
-                // bitwise, not short-circuit: no branches per step; an exact
-                // bracket is one bin (bL = bH)
-                const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > bH)));
-                const bool cand = COUNT ? valid & !nz & (bin >= bL) & (bin <= bH) : valid & !nz & (bin == bH);
-                const uint64_t dm = ballot(def);
-                const uint64_t cm = ballot(cand);
-                ndef += popc64(dm);
-                myword = lane == st ? dm : myword;
-                if (cand) {
-                    const uint64_t q = cbase + run + lanes_below(cm);
-                    const uint32_t xb = COUNT ? bin - bL : 0u;  // < NBR: the candidate lies in the bracket
-                    w.cand_key[q] = key;
-                    w.cand_idx[q] = i;
-                    atomicAdd(&histA[xb * 1024u + ((key >> 10) & 1023u)], 1u);
+                dm = __builtin_amdgcn_ballot_w64(bin > bH);
+                // unsigned: bL <= bin <= bH
+                const bool c = bin - bL <= span && (MODE() == 0 || st * 64u + lane < lim);
+                cm = __builtin_amdgcn_ballot_w64(c);
+                if (cm) {  // wave-uniform
+                    if (c) {
+                        const uint32_t q = __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32),
+                                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)cm, run));
+                        const uint32_t xb = bin - bL;  // < NBR: the candidate lies in the bracket
+                        ckey[q] = key;
+                        cidx[q] = base + st * 64u + lane;
+                        atomicAdd(&histA[(xb << 10) | ((key >> 10) & 1023u)], 1u);
+                        if (COUNT) acc_x += 1ull << (xb << 4);
+                    }
+                    run += popc64(cm);
                 }
-                if (COUNT && cm) {
-#pragma unroll
-                    for (uint32_t x = 0; x < NBR; ++x) acc_x[x] += popc64(ballot(cand && bin - bL == x));
-                }
-                run += popc64(cm);
             }
-        }
+            ndef += popc64(dm);
+            // lane st of wlo / whi takes the ballot's halves (wave-uniform
+            // operands: the ballot and the lane number)
+            uint32_t lo = wlo, hi = whi;
+            asm("v_writelane_b32 %0, %1, m0" : "+v"(lo) : "s"((uint32_t)dm), "{m0}"(st));
+            asm("v_writelane_b32 %0, %1, m0" : "+v"(hi) : "s"((uint32_t)(dm >> 32)), "{m0}"(st));
+            wlo = lo;
+            whi = hi;
+        };
+        auto steps = [&](auto MODE) {
+            for (uint32_t grp = 0; grp < SF_GROUPS; ++grp) {
+                float x[SF_GROUP];
+#pragma unroll
+                for (uint32_t u = 0; u < SF_GROUP; ++u) x[u] = xn[u];
+                if (grp + 1 < SF_GROUPS) {
+                    sf_load(g, f, grp + 1, xn);
+                } else if (PHASE == 0 && tile + nw < w.ntiles_total) {
+                    fn = filter_tile(w, tile + nw);
+                    sf_load(g, fn, 0, xn);
+                }
+                // keeps the scheduler from sinking the loads next to their uses
+                asm volatile("" ::: "memory");
+#pragma unroll
+                for (uint32_t u = 0; u < SF_GROUP; ++u) step(MODE, grp * SF_GROUP + u, x[u]);
+            }
+        };
+        if (f.nz)
+            steps(std::integral_constant<int, 2>());
+        else if (lim >= TILE)
+            steps(std::integral_constant<int, 0>());
+        else
+            steps(std::integral_constant<int, 1>());
         // slot + base is a multiple of TILE, so the tile's words are 8-byte aligned
         uint2 *sb = (uint2 *)(w.selbits + ((f.slot + base) >> 5));
-        sb[lane] = make_uint2((uint32_t)myword, (uint32_t)(myword >> 32));
+        sb[lane] = make_uint2(wlo, whi);
         if (lane == 0) {
             w.ccnt[tile] = run;
             w.tcnt[tile] = ndef;
         }
-        if (COUNT && !nz) acc_def += ndef;
-        if (ballot(nonfinite != 0) && lane == 0) atomicOr(&w.td[f.t].flags, FLAG_NONFINITE);
+        if (COUNT && !f.nz) {
+            acc_def += ndef;
+            ++since;
+        }
+        if (__builtin_amdgcn_ballot_w64(kmax >= 0x7f800000u) && lane == 0) atomicOr(&w.td[f.t].flags, FLAG_NONFINITE);
     }
     flush();
 }
