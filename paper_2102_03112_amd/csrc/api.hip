@@ -90,6 +90,9 @@ struct Carve {
     // bucketed query: list entries (the largest such tensor's size), count
     // table words and round-total words; both carves hold them
     uint64_t qb_entries = 0, qb_tab = 0, qb_rows = 0;
+    // values the sender expects to code (r per top-r tensor, doubled for its
+    // false positives; d for the support): sizes the reorder-map packing grid
+    uint64_t vals_est = 0;
     bool query_only = false;  // descriptors, tile counts, the positives bitmap and the tile table only
     size_t bytes = 0;
     size_t o_td, o_glob, o_pstat, o_histA, o_shist, o_fcnt, o_tcnt, o_toff, o_ccnt, o_hist, o_sel, o_pbits, o_ckey, o_cidx, o_S, o_P,
@@ -510,6 +513,7 @@ dr_status plan_config(const dr_config *cfg, Plan &p, std::vector<uint64_t> &rec_
         const uint64_t d = cfg->offsets_h[t + 1] - cfg->offsets_h[t];
         const uint64_t r = nz ? 0 : ceil_div(d * cfg->ratio_num, cfg->ratio_den);
         const uint64_t n_cap = nz ? d : r;
+        p.carve.vals_est += nz ? d : std::min<uint64_t>(d, 2 * r + TILE);
         uint64_t m_cap = 0;
         uint32_t kk = 0;
         if (!bloom_params_host(n_cap, cfg->fpr, &m_cap, &kk))
@@ -672,7 +676,7 @@ dr_status encode_back(Encode &e, hipStream_t s) {
     const Work &w = e.w;
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
     if (p.segment) DR_HIP(launch_segment(w, p.seg_grid_req, p.seg_block_pass, s));
-    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
+    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.carve.vals_est, p.dexp, s));
     return DR_OK;
 }
 
@@ -1004,6 +1008,7 @@ Plan single_plan(uint64_t d) {
     p.carve.ntensors = 1;
     p.carve.ntiles = in.ntiles;
     p.carve.slots = (uint64_t)in.ntiles * TILE;
+    p.carve.vals_est = d;
     return p;
 }
 
@@ -1475,7 +1480,7 @@ dr_status dr_curvefit_encode(const float *vals, const uint64_t *n, uint64_t n_ca
     DR_HIP(launch_keygen(w, vals, n, n_cap, flags_out, persist_grid(4), s));
     DR_HIP(launch_value_setup(w, false, nullptr, s));
     DR_HIP(launch_sort(w, (uint32_t)p.carve.ntiles, s));
-    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.dexp, s));
+    DR_HIP(launch_fit(w, (uint32_t)p.carve.fit_blocks, p.carve.vals_est, p.dexp, s));
     return DR_OK;
 }
 

@@ -106,7 +106,7 @@ hipError_t launch_sort(const Work &w, uint32_t cap_tiles, hipStream_t s);
 hipError_t launch_segment(const Work &w, uint32_t grid_req, bool block_pass, hipStream_t s);
 // the fit's moments with the packing of the reorder maps (one launch), the
 // solve, then the double-exponential passes if any tensor asks for them
-hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s);
+hipError_t launch_fit(const Work &w, uint32_t fit_blocks, uint64_t vals_est, bool dexp, hipStream_t s);
 hipError_t launch_curvefit_decode(const Work &w, const float *coef, const uint32_t *sigma, const uint64_t *n,
                                   uint64_t n_cap, float *vals_out, uint64_t *flags_out, int grid_persist,
                                   hipStream_t s);

@@ -892,6 +892,17 @@ __device__ __forceinline__ uint32_t tensor_of_fit_block(const Work &w, uint32_t 
 constexpr uint32_t FIT_THREADS = 1024;
 constexpr uint32_t FIT_BATCH = 8;
 
+// Chunks a run of ns points is cut into: at most FIT_CHUNKS, each at least
+// a batch per thread.  A block reduces its 3 D + 2 sums over all its waves
+// whatever its chunk's size, so eight chunks of a short run are mostly
+// reductions (transformer_355m_x24: 192 runs of 18.5 K points, now three
+// chunks each).  The blocks of unused chunks write zero partials.
+constexpr uint64_t FIT_MIN_CHUNK = (uint64_t)FIT_THREADS * FIT_BATCH;
+__device__ __forceinline__ uint32_t fit_chunks(uint64_t ns) {
+    const uint64_t c = (ns + FIT_MIN_CHUNK - 1) / FIT_MIN_CHUNK;
+    return (uint32_t)(c < 1 ? 1 : (c > FIT_CHUNKS ? FIT_CHUNKS : c));
+}
+
 template <int D>
 __device__ void fit_moments_body(const float *y, uint64_t lo_run, uint64_t ns, uint64_t j0, uint64_t j1,
                                  double *out) {
@@ -967,9 +978,14 @@ __global__ __launch_bounds__(FIT_THREADS) void k_fit_moments(Work w, uint32_t fi
     uint64_t lo, hi;
     run_range(w, td, s, &lo, &hi);
     const uint64_t ns = hi - lo;
-    const uint64_t j0 = ns * ch / FIT_CHUNKS, j1 = ns * (ch + 1) / FIT_CHUNKS;
-    const float *y = w.vsorted + td.in.slot;
+    const uint32_t nch = fit_chunks(ns);
     double *out = w.fit_part + (uint64_t)blockIdx.x * NMOM;
+    if (ch >= nch) {  // block-uniform: the run has fewer chunks; this one adds nothing
+        if (threadIdx.x < NMOM) out[threadIdx.x] = 0.0;
+        return;
+    }
+    const uint64_t j0 = ns * ch / nch, j1 = ns * (ch + 1) / nch;
+    const float *y = w.vsorted + td.in.slot;
     switch (td.deff) {
         case 0: fit_moments_body<0>(y, lo, ns, j0, j1, out); break;
         case 1: fit_moments_body<1>(y, lo, ns, j0, j1, out); break;
@@ -1370,11 +1386,16 @@ __global__ __launch_bounds__(DEXP_THREADS) void k_dexp_pass(Work w, uint32_t pas
     }
 }
 
-hipError_t launch_fit(const Work &w, uint32_t fit_blocks, bool dexp, hipStream_t s) {
+hipError_t launch_fit(const Work &w, uint32_t fit_blocks, uint64_t vals_est, bool dexp, hipStream_t s) {
     // the fit's chunk blocks, then blocks packing the reorder maps: one per
-    // 32 Ki elements of the work's slots (which bound the values), at least
-    // 32 and at most 1024
-    const uint32_t pack_blocks = (uint32_t)std::min<uint64_t>(1024, std::max<uint64_t>(32, w.slots >> 15));
+    // PACK_PER_BLOCK of the values the plan expects (each takes at most 32
+    // bits, so as many words), at least 8 and at most 512.  Sized by the
+    // work's slots instead (one per 32 Ki, at most 1024), resnet50_25m
+    // launched 780 blocks for 166 K words; with the words found by a cursor
+    // instead of a search per word, ncf_32m's launch went from 0.45 to 0.25 ms.
+    constexpr uint64_t PACK_PER_BLOCK = 4ull * FIT_THREADS;
+    const uint32_t pack_blocks =
+        (uint32_t)std::min<uint64_t>(512, std::max<uint64_t>(8, (vals_est + PACK_PER_BLOCK - 1) / PACK_PER_BLOCK));
     k_fit_moments<<<fit_blocks + pack_blocks, FIT_THREADS, 0, s>>>(w, fit_blocks);
     trace_mark(s, "k_fit_moments");
     if (fit_blocks == 0) return hipGetLastError();
@@ -1404,33 +1425,93 @@ __device__ __forceinline__ uint32_t tensor_of_sword(const Work &w, uint32_t g) {
     return lo;
 }
 
-// Words first, first + stride, ... of the reorder maps of all tensors.
+// Words first, first + stride, ... of the reorder maps of all tensors.  A
+// thread's words ascend, so its tensor only moves forward: the tensor's
+// fields are read when it changes, not per word.  Words of a tensor with
+// b >= 16 overlap at most three entries; four such words have all their
+// entries' reads in flight together.
 __device__ void pack_sigma_words(const Work &w, uint32_t first, uint32_t stride) {
+    constexpr uint32_t U = 4;
     const uint32_t total = w.glob->sigma_words;
-    for (uint32_t gw = first; gw < total; gw += stride) {
-        const uint32_t t = tensor_of_sword(w, gw);
+    if (first >= total) return;
+    uint32_t t = tensor_of_sword(w, first);
+    uint32_t sw0 = 0, swn = 0, b = 0, nv = 0;
+    const uint32_t *sg = nullptr;
+    uint32_t *out = nullptr;
+    auto enter = [&]() {  // tensor t's fields
         const TDesc &td = w.td[t];
-        const uint32_t wl = gw - td.sw0;
-        const uint32_t b = td.b, nv = td.nv;
+        sw0 = td.sw0;
+        swn = t + 1 < w.ntensors ? w.td[t + 1].sw0 : total;
+        b = td.b;
+        nv = td.nv;
+        sg = w.sig + td.in.slot;
+        out = td.in.sigma ? td.in.sigma : (uint32_t *)(td.in.rec + td.sigma_off);
+    };
+    enter();
+    // floor(bit0 / b) in double: exact, since bit0 < 2^53 and a quotient that
+    // is not an integer lies at least 1/b from one
+    auto first_entry = [&](uint64_t bit0) { return (uint64_t)floor((double)bit0 / (double)b); };
+    // one word from its entries qa..qb, all read here
+    auto word_of = [&](uint32_t wl) {
         const uint64_t bit0 = (uint64_t)wl * 32u;
-        // floor(bit0 / b) in double: exact, since bit0 < 2^53 and a quotient
-        // that is not an integer lies at least 1/b from one
-        const double rb = (double)b;
-        const uint64_t qa = (uint64_t)floor((double)bit0 / rb);
-        uint64_t qb = (uint64_t)floor((double)(bit0 + 31u) / rb);
+        const uint64_t qa = first_entry(bit0);
+        uint64_t qb = first_entry(bit0 + 31u);
         if (qb > nv - 1u) qb = nv - 1u;
-        const uint32_t *sg = w.sig + td.in.slot;
         uint32_t v = 0;
         for (uint64_t q = qa; q <= qb; ++q) {
             const int64_t sh = (int64_t)(q * b) - (int64_t)bit0;
             const uint64_t e = sg[q];
-            if (sh >= 0)
-                v |= (uint32_t)(e << sh);
-            else
-                v |= (uint32_t)(e >> (-sh));
+            v |= sh >= 0 ? (uint32_t)(e << sh) : (uint32_t)(e >> (-sh));
         }
-        uint32_t *out = td.in.sigma ? td.in.sigma : (uint32_t *)(td.in.rec + td.sigma_off);
-        out[wl] = v;
+        return v;
+    };
+    for (uint32_t g0 = first; g0 < total; g0 += U * stride) {
+        while (g0 >= swn) {  // the thread's next word lies in a later tensor
+            ++t;
+            enter();
+        }
+        const uint32_t glast = (uint32_t)min<uint64_t>((uint64_t)g0 + (U - 1) * (uint64_t)stride, total - 1u);
+        if (glast < swn && b >= 16u) {
+            // U words of tensor t (the last ones may lie past the maps' end)
+            uint32_t e[U][3], wl[U];
+            int32_t sh[U];
+#pragma unroll
+            for (uint32_t u = 0; u < U; ++u) {
+                const uint64_t gw = (uint64_t)g0 + u * (uint64_t)stride;
+                wl[u] = gw < total ? (uint32_t)(gw - sw0) : 0u;
+                const uint64_t bit0 = (uint64_t)wl[u] * 32u;
+                const uint64_t qa = first_entry(bit0);
+                sh[u] = (int32_t)((int64_t)(qa * b) - (int64_t)bit0);  // in (-b, 0]
+#pragma unroll
+                for (uint32_t k = 0; k < 3; ++k) {
+                    // an entry past the map's last is 0 (the last word's
+                    // bits past the map are clear)
+                    const bool in = gw < total && qa + k < nv;
+                    const uint32_t x = sg[in ? qa + k : 0u];
+                    e[u][k] = in ? x : 0u;
+                }
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < U; ++u) {
+                if ((uint64_t)g0 + u * (uint64_t)stride >= total) break;
+                const int32_t s0 = sh[u];
+                uint32_t v = (uint32_t)(e[u][0] >> (uint32_t)(-s0));
+                const int32_t s1 = s0 + (int32_t)b, s2 = s1 + (int32_t)b;
+                v |= s1 < 32 ? e[u][1] << (uint32_t)s1 : 0u;
+                v |= s2 < 32 ? e[u][2] << (uint32_t)s2 : 0u;
+                out[wl[u]] = v;
+            }
+        } else {
+            for (uint32_t u = 0; u < U; ++u) {
+                const uint64_t gw = (uint64_t)g0 + u * (uint64_t)stride;
+                if (gw >= total) break;
+                while (gw >= swn) {
+                    ++t;
+                    enter();
+                }
+                out[gw - sw0] = word_of((uint32_t)(gw - sw0));
+            }
+        }
     }
 }
 
