@@ -274,9 +274,13 @@ Carve bound_carve(uint64_t d, uint64_t n_tensors) {
     c.bslices = 47 * c.slots / (1u << SLICE_LOG2_MIN) + 2 * n_tensors + BL_MAX_SLICES;
     c.btab = c.bslices * MAX_CHUNKS;
     // the bucketed query of one tensor of at most d elements: at most
-    // QB_MAX_BINS bins of ceil(d / QB_CH) chunks each, rounds for k <= 32
+    // QB_MAX_BINS bins of max(ceil(d / QB_CH), slices) chunks each (slices
+    // of 2^QB_SL bits of a filter of at most 47 n + 32 bits), rounds for
+    // k <= 32
     c.qb_entries = c.slots;
-    c.qb_tab = (uint64_t)QB_MAX_BINS * (c.slots / QB_CH + 1);
+    c.qb_tab = (uint64_t)QB_MAX_BINS *
+               std::max<uint64_t>(c.slots / QB_CH + 1,
+                                  std::min<uint64_t>(QB_MAX_BINS, (47 * c.slots + 32) / (1ull << QB_SL) + 1));
     c.qb_rows = 33ull * QB_MAX_BINS;
     c.plan();
     return c;
@@ -431,9 +435,11 @@ void plan_query_bucketed(Plan &p, bool allow) {
         q.nch_cap = (uint32_t)ceil_div(in.d, QB_CH);
         q.nreg = (uint32_t)ceil_div(in.d, 1ull << QB_RL);
         if (q.nsl_cap > QB_MAX_BINS || q.nreg > QB_MAX_BINS) continue;
+        // round 0's chunks are QB_CH indices, later rounds' the slices
+        q.ncol = std::max(q.nch_cap, q.nsl_cap);
         p.qb.push_back(q);
         ent = std::max<uint64_t>(ent, in.d);
-        tab = std::max<uint64_t>(tab, (uint64_t)std::max(q.nsl_cap, q.nreg) * q.nch_cap);
+        tab = std::max<uint64_t>(tab, (uint64_t)std::max(q.nsl_cap, q.nreg) * q.ncol);
         k = in.k;
     }
     if (p.qb.empty()) return;

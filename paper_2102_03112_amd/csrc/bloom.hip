@@ -1103,7 +1103,11 @@ __global__ __launch_bounds__(PB_THREADS) void k_probe(Work w, QueryOut o) {
 //    gives each (bin, chunk) its place, and a scatter writes the indices
 //    bin by bin (qbkt).  One block per slice then loads its slice into LDS
 //    and tests its bin's indices, writing each index, or QB_DEAD where its
-//    bit is clear, to the same place of qlist: the next round's list;
+//    bit is clear, to the same place of qlist: the next round's list.  In
+//    round 0 the chunks are QB_CH consecutive indices and a count pass
+//    counts them; in later rounds chunk s is what test block s wrote, and
+//    that block counts its survivors by their next bin itself (a count
+//    pass per round cost about 0.85 ms on ncf_32m);
 //  * round k: the survivors, which are the positives, are bucketed the same
 //    way by index region (2^QB_RL indices), and one block per region sets
 //    their bits in an LDS copy of the region's bitmap and writes it out.
@@ -1120,7 +1124,7 @@ struct QbArgs {
     uint32_t k;         // hashes planned on the host
     uint32_t min_bits;  // smallest filter taken this way
     uint32_t nsl_cap;   // slices the work has room for
-    uint32_t nch_cap;   // chunks per bin row of qtab
+    uint32_t ncol;      // columns of qtab: at least round 0's chunks and nsl_cap
 };
 
 constexpr uint32_t QB_TEST_THREADS = 512;
@@ -1153,16 +1157,8 @@ __device__ __forceinline__ uint32_t qb_sum(const uint32_t *v, uint32_t n, uint32
     return tot;
 }
 
-// Round j's list length: the tensor's size in round 0, else the entries the
-// previous round bucketed (the sum of its bin totals).
-template <uint32_t NT>
-__device__ __forceinline__ uint32_t qb_len(const Work &w, const TDesc &td, uint32_t j, uint32_t nsl,
-                                           uint32_t *scratch) {
-    return j == 0 ? td.in.d : qb_sum<NT>(w.qrow + (j - 1) * QB_MAX_BINS, nsl, scratch);
-}
-
 // Entries [b0, b0 + QB_SUB) of round j's list, QB_PER per thread; QB_DEAD
-// past the list's end and for an index that failed a probe.
+// at and past `len` and for an index that failed a probe.
 __device__ __forceinline__ void qb_load(const Work &w, uint32_t j, uint32_t b0, uint32_t len, uint32_t *e) {
     const uint32_t x0 = b0 + threadIdx.x;
     if (j == 0) {
@@ -1186,46 +1182,45 @@ __device__ __forceinline__ uint32_t qb_key(const PosMap &pm, uint32_t i, uint32_
     return fin ? (i >> QB_RL) : (pm(mm3_key(i), j) >> QB_SL);
 }
 
-// Counts of chunk c's entries per bin: column c of qtab.
+// Round 0: counts of chunk c's indices (QB_CH consecutive ones) per bin:
+// column c of qtab.  The first block marks the tensor as taken this way.
 template <int MODE>
-__global__ __launch_bounds__(QB_THREADS) void k_qb_count(Work w, QbArgs a, uint32_t j) {
+__global__ __launch_bounds__(QB_THREADS) void k_qb_count(Work w, QbArgs a) {
     __shared__ uint32_t h[QB_MAX_BINS];
     __shared__ uint32_t ps[33];
-    __shared__ uint32_t scratch[QB_THREADS / 64 + 1];
     TDesc &td = w.td[a.t];
     const QueryOut o{};
     bool ok;
     const RecordView rv = query_filter(w, o, td, MODE, &ok);
-    if (j == 0) {
-        if (!qb_usable(rv, ok, td, a)) return;
-        if (blockIdx.x == 0 && threadIdx.x == 0) td.qb = 1u;
-    } else if (!td.qb) {
-        return;
-    }
-    const uint32_t d = td.in.d, nsl = qb_slices(rv.m_bits);
-    const bool fin = j == rv.k;
-    const uint32_t nb = fin ? qb_regions(d) : nsl;
-    const uint32_t len = qb_len<QB_THREADS>(w, td, j, nsl, scratch);
+    if (!qb_usable(rv, ok, td, a)) return;
+    if (blockIdx.x == 0 && threadIdx.x == 0) td.qb = 1u;
+    const uint32_t d = td.in.d, nb = qb_slices(rv.m_bits);
     const uint32_t c = blockIdx.x;
-    if ((uint64_t)c * QB_CH >= len) return;
+    if ((uint64_t)c * QB_CH >= d) return;
     const bool part = rv.layout == LAYOUT_PARTITIONED;
     if (part) fill_part_starts(ps, rv.m_bits, rv.k);
     for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) h[b] = 0;
     __syncthreads();
     const PosMap pm{rv.m_bits, part ? ps : nullptr};
-    for (uint32_t b0 = c * QB_CH; b0 < min(len, (c + 1) * QB_CH); b0 += QB_SUB) {
+    for (uint32_t b0 = c * QB_CH; b0 < min(d, (c + 1) * QB_CH); b0 += QB_SUB) {
         uint32_t e[QB_PER];
-        qb_load(w, j, b0, len, e);
+        qb_load(w, 0, b0, d, e);
 #pragma unroll
         for (uint32_t u = 0; u < QB_PER; ++u) {
             if (e[u] != QB_DEAD) {
-                const uint32_t b = qb_key(pm, e[u], j, fin);
+                const uint32_t b = qb_key(pm, e[u], 0, false);
                 if (b < nb) atomicAdd(&h[b], 1u);
             }
         }
     }
     __syncthreads();
-    for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) w.qtab[(uint64_t)b * a.nch_cap + c] = h[b];
+    for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) w.qtab[(uint64_t)b * a.ncol + c] = h[b];
+}
+
+// Round j's chunks: QB_CH consecutive indices in round 0, else the buckets
+// of round j - 1 (chunk s: the places test block s wrote in qlist).
+__device__ __forceinline__ uint32_t qb_chunks(const TDesc &td, uint32_t j, uint32_t nsl) {
+    return j == 0 ? (td.in.d + QB_CH - 1) / QB_CH : nsl;
 }
 
 // One block per bin: its row of qtab becomes each chunk's offset within the
@@ -1242,9 +1237,8 @@ __global__ __launch_bounds__(QB_THREADS) void k_qb_scan(Work w, QbArgs a, uint32
     const uint32_t nb = j == rv.k ? qb_regions(d) : nsl;
     const uint32_t b = blockIdx.x;
     if (b >= nb) return;
-    const uint32_t len = qb_len<QB_THREADS>(w, td, j, nsl, scratch);
-    const uint32_t nch = (len + QB_CH - 1) / QB_CH;
-    uint32_t *row = w.qtab + (uint64_t)b * a.nch_cap;
+    const uint32_t nch = qb_chunks(td, j, nsl);
+    uint32_t *row = w.qtab + (uint64_t)b * a.ncol;
     uint32_t carry = 0;
     for (uint32_t c0 = 0; c0 < nch; c0 += QB_THREADS) {
         const uint32_t c = c0 + threadIdx.x;
@@ -1285,9 +1279,18 @@ __global__ __launch_bounds__(QB_THREADS) __attribute__((amdgpu_waves_per_eu(8)))
     const uint32_t d = td.in.d, nsl = qb_slices(rv.m_bits);
     const bool fin = j == rv.k;
     const uint32_t nb = fin ? qb_regions(d) : nsl;
-    const uint32_t len = qb_len<QB_THREADS>(w, td, j, nsl, scratch);
     const uint32_t c = blockIdx.x;
-    if ((uint64_t)c * QB_CH >= len) return;
+    if (c >= qb_chunks(td, j, nsl)) return;
+    // the chunk's places [xa, xb) in round j's list
+    uint32_t xa, xb;
+    if (j == 0) {
+        xa = c * QB_CH;
+        xb = min(d, xa + QB_CH);
+    } else {
+        const uint32_t *prev = w.qrow + (j - 1) * QB_MAX_BINS;
+        xa = qb_sum<QB_THREADS>(prev, c, scratch);
+        xb = xa + prev[c];
+    }
     const bool part = rv.layout == LAYOUT_PARTITIONED;
     if (part) fill_part_starts(ps, rv.m_bits, rv.k);
     // bucket starts (exclusive scan of the round's bin totals), each plus
@@ -1299,14 +1302,14 @@ __global__ __launch_bounds__(QB_THREADS) __attribute__((amdgpu_waves_per_eu(8)))
         const uint32_t v = b < nb ? rowj[b] : 0u;
         uint32_t tot;
         const uint32_t ex = block_excl_scan_n<QB_THREADS>(v, scratch, &tot);
-        if (b < nb) bst[b] = carry + ex + w.qtab[(uint64_t)b * a.nch_cap + c];
+        if (b < nb) bst[b] = carry + ex + w.qtab[(uint64_t)b * a.ncol + c];
         carry += tot;
     }
     const PosMap pm{rv.m_bits, part ? ps : nullptr};
-    for (uint32_t x0 = c * QB_CH; x0 < min(len, (c + 1) * QB_CH); x0 += QB_SUB) {
+    for (uint32_t x0 = xa; x0 < xb; x0 += QB_SUB) {
         for (uint32_t b = threadIdx.x; b < nb; b += QB_THREADS) lc[b] = 0;
         uint32_t e[QB_PER];
-        qb_load(w, j, x0, len, e);
+        qb_load(w, j, x0, xb, e);
         __syncthreads();  // lc is clear (and, the first time, bst and ps are set)
         uint32_t key[QB_PER], rk[QB_PER];
 #pragma unroll
@@ -1355,10 +1358,13 @@ __global__ __launch_bounds__(QB_THREADS) __attribute__((amdgpu_waves_per_eu(8)))
 
 // Round j's test: block s loads filter slice s into LDS and tests hash j of
 // the indices in its bucket; each goes back to its place in qlist, or
-// QB_DEAD if its bit is clear.
+// QB_DEAD if its bit is clear.  The block also counts its survivors by
+// their bin in round j + 1 (the slice of hash j + 1, or after the last hash
+// the index region): column s of qtab, for round j + 1's chunk s.
 template <int MODE>
 __global__ __launch_bounds__(QB_TEST_THREADS) void k_qb_test(Work w, QbArgs a, uint32_t j) {
     __shared__ uint32_t sl[QB_SW];
+    __shared__ uint32_t h[QB_MAX_BINS];
     __shared__ uint32_t ps[33];
     __shared__ uint32_t scratch[QB_TEST_THREADS / 64 + 1];
     TDesc &td = w.td[a.t];
@@ -1373,6 +1379,9 @@ __global__ __launch_bounds__(QB_TEST_THREADS) void k_qb_test(Work w, QbArgs a, u
     const uint32_t start = qb_sum<QB_TEST_THREADS>(rowj, s, scratch), end = start + rowj[s];
     const uint32_t w0 = s * QB_SW, nw = min(QB_SW, rv.m_bits / 32u - w0);
     for (uint32_t q = threadIdx.x; q < nw; q += QB_TEST_THREADS) sl[q] = rv.bits[w0 + q];
+    const bool fin = j + 1 == rv.k;  // round j + 1 bins by index region
+    const uint32_t nb = fin ? qb_regions(td.in.d) : nsl;
+    for (uint32_t b = threadIdx.x; b < nb; b += QB_TEST_THREADS) h[b] = 0;
     const bool part = rv.layout == LAYOUT_PARTITIONED;
     if (part) fill_part_starts(ps, rv.m_bits, rv.k);
     __syncthreads();
@@ -1389,12 +1398,19 @@ __global__ __launch_bounds__(QB_TEST_THREADS) void k_qb_test(Work w, QbArgs a, u
         for (uint32_t u = 0; u < QB_PER; ++u) {
             const uint32_t x = x0 + u * QB_TEST_THREADS;
             if (x < end) {
-                const uint32_t p = pm(mm3_key(e[u]), j) - p0;  // wraps for a bit below the slice
+                const uint32_t key = mm3_key(e[u]);
+                const uint32_t p = pm(key, j) - p0;  // wraps for a bit below the slice
                 const bool alive = p < nbits && ((sl[p >> 5] >> (p & 31u)) & 1u);
                 if (x < w.qcap) w.qlist[x] = alive ? e[u] : QB_DEAD;
+                if (alive) {
+                    const uint32_t b = fin ? e[u] >> QB_RL : pm(key, j + 1) >> QB_SL;
+                    if (b < nb) atomicAdd(&h[b], 1u);
+                }
             }
         }
     }
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < nb; b += QB_TEST_THREADS) w.qtab[(uint64_t)b * a.ncol + s] = h[b];
 }
 
 // Last step: block r sets the bits of the positives in index region r in an
@@ -1742,14 +1758,16 @@ hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, 
 }
 
 hipError_t launch_query_bucketed(const Work &w, const QbTensor &q, uint32_t k, uint32_t min_bits, hipStream_t s) {
-    if (k < 1 || q.nch_cap == 0 || q.nsl_cap == 0 || q.nreg == 0) return hipSuccess;
-    const QbArgs a{q.t, k, min_bits, q.nsl_cap, q.nch_cap};
+    if (k < 1 || q.nch_cap == 0 || q.nsl_cap == 0 || q.nreg == 0 || q.ncol < q.nch_cap || q.ncol < q.nsl_cap)
+        return hipSuccess;
+    const QbArgs a{q.t, k, min_bits, q.nsl_cap, q.ncol};
+    // round 0's counts; each later round's are its previous test's
+    k_qb_count<Q_DECODE><<<q.nch_cap, QB_THREADS, 0, s>>>(w, a);
+    trace_mark(s, "k_qb_count");
     for (uint32_t j = 0; j <= k; ++j) {
-        k_qb_count<Q_DECODE><<<q.nch_cap, QB_THREADS, 0, s>>>(w, a, j);
-        trace_mark(s, "k_qb_count");
         k_qb_scan<Q_DECODE><<<j < k ? q.nsl_cap : q.nreg, QB_THREADS, 0, s>>>(w, a, j);
         trace_mark(s, "k_qb_scan");
-        k_qb_scatter<Q_DECODE><<<q.nch_cap, QB_THREADS, 0, s>>>(w, a, j);
+        k_qb_scatter<Q_DECODE><<<q.ncol, QB_THREADS, 0, s>>>(w, a, j);
         trace_mark(s, "k_qb_scatter");
         if (j < k) {
             k_qb_test<Q_DECODE><<<q.nsl_cap, QB_TEST_THREADS, 0, s>>>(w, a, j);

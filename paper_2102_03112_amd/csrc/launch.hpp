@@ -78,9 +78,10 @@ hipError_t launch_query_encode(const Work &w, const float *g, int grid_persist, 
 // The receiver's bucketed query of one tensor (a filter larger than an
 // XCD's L2): rounds of one hash each, then the positives bitmap; the probe
 // pass that follows counts it.  Caps of the work it was planned for:
-// nsl_cap filter slices, nch_cap list chunks, nreg index regions.
+// nsl_cap filter slices, nch_cap round-0 list chunks, nreg index regions.
 struct QbTensor {
     uint32_t t, nsl_cap, nch_cap, nreg;
+    uint32_t ncol;  // columns of the count table: max(nch_cap, nsl_cap)
 };
 hipError_t launch_query_bucketed(const Work &w, const QbTensor &q, uint32_t k, uint32_t min_bits, hipStream_t s);
 hipError_t launch_query_plain(const Work &w, uint32_t *idx_out, uint64_t cap, uint64_t *n_out, int grid_persist,

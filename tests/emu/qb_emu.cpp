@@ -71,8 +71,8 @@ int main(int argc, char **argv) {
     memcpy(&rec[16], filt.data(), filt.size() * 4);
     // the plan's caps (api.hip plan_query_bucketed)
     const uint32_t nsl_cap = (uint32_t)cdiv(m, 1u << QB_SL), nch_cap = (uint32_t)cdiv(d, QB_CH),
-                   nreg = (uint32_t)cdiv(d, 1u << QB_RL);
-    const uint64_t qcap = cdiv(d, 64) * 64, tab = (uint64_t)std::max(nsl_cap, nreg) * nch_cap,
+                   nreg = (uint32_t)cdiv(d, 1u << QB_RL), ncol = std::max(nch_cap, nsl_cap);
+    const uint64_t qcap = cdiv(d, 64) * 64, tab = (uint64_t)std::max(nsl_cap, nreg) * ncol,
                    rows = (uint64_t)(k + 1) * QB_MAX_BINS;
     std::vector<uint32_t> qlist(qcap, 0xA5A5A5A5u), qbkt(qcap, 0x5A5A5A5Au), qtab(tab, 0xDEADBEEFu),
         qrow(rows, 0xDEADBEEFu), pbits(ntiles * TILE_WORDS, 0xCCCCCCCCu), ttab(ntiles, 0);
@@ -97,11 +97,11 @@ int main(int argc, char **argv) {
     w.qtab = qtab.data();
     w.qrow = qrow.data();
     w.qcap = qcap;
-    const QbArgs a{0, k, 1024, nsl_cap, nch_cap};
+    const QbArgs a{0, k, 1024, nsl_cap, ncol};
+    emu_launch(nch_cap, QB_THREADS, [&] { k_qb_count<Q_DECODE>(w, a); });
     for (uint32_t j = 0; j <= k; ++j) {
-        emu_launch(nch_cap, QB_THREADS, [&] { k_qb_count<Q_DECODE>(w, a, j); });
         emu_launch(j < k ? nsl_cap : nreg, QB_THREADS, [&] { k_qb_scan<Q_DECODE>(w, a, j); });
-        emu_launch(nch_cap, QB_THREADS, [&] { k_qb_scatter<Q_DECODE>(w, a, j); });
+        emu_launch(ncol, QB_THREADS, [&] { k_qb_scatter<Q_DECODE>(w, a, j); });
         if (j < k) emu_launch(nsl_cap, QB_TEST_THREADS, [&] { k_qb_test<Q_DECODE>(w, a, j); });
     }
     emu_launch(nreg, QB_TEST_THREADS, [&] { k_qb_fill<Q_DECODE>(w, a); });

@@ -52,6 +52,9 @@ CASES = [
     # three slices (the last one partial), two regions (the last one
     # partial), 17 chunks
     (530_001, 120_000, 1_050_016, 2, 0),
+    # more slices (4) than round 0 has chunks (2): the count table is as
+    # wide as the slices
+    (40_000, 30_000, 3 * (1 << 19) + 1024, 3, 0),
 ]
 
 
