@@ -658,32 +658,54 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
             cur_t = f.t;
             b1 = pick_b1<FILTER_THREADS>(w, f.t, f.base == 0, pl);
         }
-        const uint32_t base = f.base, d = f.d;
-        const uint64_t slot = f.slot;
-        const bool nz = f.nz;
+        // the tile's fields are block-uniform: saying so keeps them in
+        // scalar registers
+        const uint32_t base = __builtin_amdgcn_readfirstlane(f.base);
+        const uint32_t lim = __builtin_amdgcn_readfirstlane(f.d) - base;  // elements of the tensor here (> 0)
+        const uint64_t slot = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(f.slot >> 32)) << 32) |
+                              __builtin_amdgcn_readfirstlane((uint32_t)f.slot);
         uint32_t keys[FILTER_STEPS];
         uint64_t cmask[FILTER_STEPS];
-        uint32_t nonfinite = 0, ndef = 0;
+        uint32_t kmax = 0, ndef = 0;
         // lane 2j + h ends up holding half h of step j's bitmap ballot, and
-        // lane j the candidate count of step j: selects, not branches
+        // lane j the candidate count of step j (lane writes of wave-uniform
+        // values)
         uint32_t myword = 0, mycand = 0;
+        // MODE 0: top-r, whole tile; 1: top-r, the tensor's last (partial)
+        // tile; 2: support.  A value past the tensor's end reads as 0, so
+        // only a bin b1 of 0 needs the lane mask.
+        auto steps = [&](auto MODE) {
 #pragma unroll
-        for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
-            const uint32_t i = base + j * FILTER_THREADS + threadIdx.x;
-            const bool valid = i < d;
-            const uint32_t key = valid ? mag_key(x[j]) : 0u;
-            nonfinite |= key >= 0x7f800000u;
-            const uint32_t bin = key >> HIST1_SHIFT;
-            // bitwise, not short-circuit: no branches per step
-            const bool def = valid & ((nz & (key != 0u)) | (!nz & (bin > b1)));
-            const bool cand = valid & !nz & (bin == b1);
-            const uint64_t dm = ballot(def);
-            cmask[j] = ballot(cand);
-            keys[j] = key;
-            ndef += popc64(dm);
-            myword = lane == 2u * j ? (uint32_t)dm : (lane == 2u * j + 1u ? (uint32_t)(dm >> 32) : myword);
-            mycand = lane == j ? popc64(cmask[j]) : mycand;
-        }
+            for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
+                const uint32_t key = mag_key(x[j]);
+                kmax = max(kmax, key);
+                const uint32_t bin = key >> HIST1_SHIFT;
+                uint64_t dm, cm = 0;
+                if constexpr (MODE() == 2) {
+                    dm = __builtin_amdgcn_ballot_w64(key != 0u);
+                } else {
+                    dm = __builtin_amdgcn_ballot_w64(bin > b1);
+                    cm = __builtin_amdgcn_ballot_w64(bin == b1 &&
+                                                     (MODE() == 0 || j * FILTER_THREADS + threadIdx.x < lim));
+                }
+                cmask[j] = cm;
+                keys[j] = key;
+                ndef += popc64(dm);
+                uint32_t mw = myword, mc = mycand;
+                asm("v_writelane_b32 %0, %1, m0" : "+v"(mw) : "s"((uint32_t)dm), "{m0}"(2u * j));
+                asm("v_writelane_b32 %0, %1, m0" : "+v"(mw) : "s"((uint32_t)(dm >> 32)), "{m0}"(2u * j + 1u));
+                asm("v_writelane_b32 %0, %1, m0" : "+v"(mc) : "s"(popc64(cm)), "{m0}"(j));
+                myword = mw;
+                mycand = mc;
+            }
+        };
+        if (f.nz)
+            steps(std::integral_constant<int, 2>());
+        else if (lim >= TILE)
+            steps(std::integral_constant<int, 0>());
+        else
+            steps(std::integral_constant<int, 1>());
+        const bool nonfinite = kmax >= 0x7f800000u;
         // the tile's bitmap words are staged in LDS and written by one
         // coalesced store after the barrier (two-lane stores per step cost a
         // third of the pass's read bandwidth)
@@ -714,7 +736,7 @@ __global__ __launch_bounds__(FILTER_THREADS) __attribute__((amdgpu_waves_per_eu(
         uint32_t *histA = w.histA + ((uint64_t)f.t * HISTA_COPIES + hcopy) * HISTA_BINS;
 #pragma unroll
         for (uint32_t j = 0; j < FILTER_STEPS; ++j) {
-            if ((cmask[j] >> lane) & 1ull) {
+            if (cmask[j] && ((cmask[j] >> lane) & 1ull)) {  // the first test is wave-uniform
                 const uint64_t q = cbase + woff[j * FILTER_WAVES + wv] + lanes_below(cmask[j]);
                 w.cand_key[q] = keys[j];
                 w.cand_idx[q] = base + j * FILTER_THREADS + threadIdx.x;
