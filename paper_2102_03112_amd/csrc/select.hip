@@ -371,9 +371,9 @@ __global__ __launch_bounds__(HIST_THREADS) void k_topr_pick(Work w) {
 // ---------------------------------------------------------------------------
 // top-r step 2 / support: bitmap of definite selections + per-tile candidates
 // ---------------------------------------------------------------------------
-// Each wave owns whole tiles (the tiles gw, gw + waves, ... of the grid's
-// waves), so the pass has no block barriers: a tile is 64 steps of 64
-// consecutive elements, read 8 steps at a time with the next 8 in flight.
+// Each wave owns whole tiles (a run of consecutive ones), so the pass has
+// no block barriers: a tile is 64 steps of 64 consecutive elements, read 8
+// steps at a time with the next 8 in flight.
 // Top-r elements above the tensor's bracket [bL, bH] are selected; those in
 // it are candidates, written in index order (a running count and the
 // lanes below in the step's ballot) to the tile's own stretch of the
@@ -510,13 +510,19 @@ __global__ __launch_bounds__(SF_THREADS) void k_select_filter_wave(Work w, const
     // PHASE 0 reads the next tile's first values while it classifies a
     // tile's last ones; the redo reads a tile only once it knows the tile's
     // tensor was redone
+    // wave gw takes tiles [t_lo, t_hi), consecutive ones.  Measured against
+    // tiles gw, gw + waves, ... (and runs of 4 or 16 tiles taken that way):
+    // transformer_355m_x24 350 against 427 us (384, 437), vgg16_138m 168
+    // against 159 us (163, 163)
+    const uint32_t per = (w.ntiles_total + nw - 1) / nw;
+    const uint32_t t_lo = min(w.ntiles_total, gw * per), t_hi = min(w.ntiles_total, t_lo + per);
     float xn[SF_GROUP];
     FilterTile fn{};
-    if (PHASE == 0 && gw < w.ntiles_total) {
-        fn = filter_tile(w, gw);
+    if (PHASE == 0 && t_lo < t_hi) {
+        fn = filter_tile(w, t_lo);
         sf_load(g, fn, 0, xn);
     }
-    for (uint32_t tile = gw; tile < w.ntiles_total; tile += nw) {
+    for (uint32_t tile = t_lo; tile < t_hi; ++tile) {
         const FilterTile f = PHASE == 0 ? fn : filter_tile(w, tile);
         if (PHASE == 1) {
             if (!w.td[f.t].sfail) continue;  // wave-uniform
@@ -592,8 +598,8 @@ __global__ __launch_bounds__(SF_THREADS) void k_select_filter_wave(Work w, const
                 for (uint32_t u = 0; u < SF_GROUP; ++u) x[u] = xn[u];
                 if (grp + 1 < SF_GROUPS) {
                     sf_load(g, f, grp + 1, xn);
-                } else if (PHASE == 0 && tile + nw < w.ntiles_total) {
-                    fn = filter_tile(w, tile + nw);
+                } else if (PHASE == 0 && tile + 1 < t_hi) {
+                    fn = filter_tile(w, tile + 1);
                     sf_load(g, fn, 0, xn);
                 }
                 // keeps the scheduler from sinking the loads next to their uses
