@@ -39,7 +39,7 @@ constexpr uint32_t QB_RL = 19;                  // index region: 2^19 indices (6
 constexpr uint32_t QB_RW = 1u << (QB_RL - 5);
 constexpr uint32_t QB_MAX_BINS = 2048;
 constexpr uint32_t QB_THREADS = 1024;
-constexpr uint32_t QB_PER = 8;                  // entries per thread of a staged batch
+constexpr uint32_t QB_PER = 9;                  // entries per thread of a staged batch
 constexpr uint32_t QB_SUB = QB_THREADS * QB_PER;
 constexpr uint32_t QB_CH = 4 * QB_SUB;          // entries per chunk
 constexpr uint32_t QB_MAX_D = 1u << 30;         // largest tensor taken this way (regions <= QB_MAX_BINS)

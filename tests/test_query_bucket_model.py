@@ -28,7 +28,7 @@ import pytest
 import oracle
 
 QB_SL, QB_RL = 19, 19
-QB_CH = 2 * 1024 * 16
+QB_CH = 4 * 1024 * 9  # 4 batches of 1024 threads x 9 entries
 QB_MAX_BINS = 2048
 TILE = 4096
 TILE_WORDS = TILE // 32
