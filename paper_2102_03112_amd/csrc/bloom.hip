@@ -81,18 +81,38 @@ __device__ __forceinline__ uint32_t active_chunks(const TDesc &td, bool from_bit
     return (td.n + td.in.bl_chunk - 1) / td.in.bl_chunk;
 }
 
+// The hashes [*a, *b) of tensor td in round r of the bucketed insert.  The
+// plan gives rounds of hpr hashes, for the most items a tensor may have;
+// a tensor with fewer (a support's count is known only on the device) takes
+// as many hashes per round as its position region holds, so that it may
+// finish in fewer rounds, and the later rounds' kernels skip it (ncf_32m,
+// 13 hashes: two rounds of 10 and 3 instead of three of 6, 6 and 1).
+__device__ __forceinline__ void bl_round(const TDesc &td, uint32_t r, uint32_t hpr, uint32_t *a, uint32_t *b) {
+    const uint32_t k = td.in.k;
+    uint64_t h = td.n ? td.in.bl_poscap / td.n : k;
+    if (h < hpr) h = hpr;
+    if (h > k) h = k;
+    const uint64_t a64 = (uint64_t)r * h;
+    *a = (uint32_t)(a64 < k ? a64 : k);
+    *b = (uint32_t)min<uint64_t>(k, (uint64_t)*a + h);
+}
+
 // The bucketed insert's kernels run 1024 threads per block: a chunk's
 // items are hashed one after another per thread, and the LDS atomics of the
 // count and scatter passes need many waves in flight to hide their latency.
+// Each takes round r of hpr planned hashes per round.
 constexpr uint32_t BL_THREADS = 1024;
 
 template <bool FROM_BITMAP>
-__global__ __launch_bounds__(BL_THREADS) void k_bloom_count(Work w, uint32_t j0, uint32_t j1) {
+__global__ __launch_bounds__(BL_THREADS) void k_bloom_count(Work w, uint32_t r, uint32_t hpr) {
     extern __shared__ uint32_t lh[];
     const uint32_t t = tensor_of_chunk(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t c = blockIdx.x - td.in.bl_chunk0;
     if (c >= td.in.bl_nchunks || c >= active_chunks(td, FROM_BITMAP)) return;
+    uint32_t j0, je;
+    bl_round(td, r, hpr, &j0, &je);
+    if (j0 >= je) return;  // the tensor has had all its hashes
     const uint32_t m_bits = td.m_words * 32u;
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (m_bits + (1u << sl2) - 1) >> sl2;
@@ -102,13 +122,10 @@ __global__ __launch_bounds__(BL_THREADS) void k_bloom_count(Work w, uint32_t j0,
     const PosMap pm{m_bits, part ? ps : nullptr};
     for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) lh[s] = 0;
     __syncthreads();
-    const uint32_t je = min(j1, td.in.k);
-    if (je > j0) {
-        for_chunk_items<FROM_BITMAP, BL_THREADS>(w, td, c, [&](uint32_t x) {
-            const uint32_t km = mm3_key(x);
-            for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[pm(km, j) >> sl2], 1u);
-        });
-    }
+    for_chunk_items<FROM_BITMAP, BL_THREADS>(w, td, c, [&](uint32_t x) {
+        const uint32_t km = mm3_key(x);
+        for (uint32_t j = j0; j < je; ++j) atomicAdd(&lh[pm(km, j) >> sl2], 1u);
+    });
     __syncthreads();
     uint32_t *tab = w.btab + td.in.bl_tab0;
     for (uint32_t s = threadIdx.x; s < nsl; s += BL_THREADS) tab[(uint64_t)s * td.in.bl_nchunks + c] = lh[s];
@@ -116,12 +133,14 @@ __global__ __launch_bounds__(BL_THREADS) void k_bloom_count(Work w, uint32_t j0,
 
 // Row scan: for slice s of a tensor (one block each), offsets of its chunks
 // within the slice's bucket, and the bucket's size.
-__global__ __launch_bounds__(NTHREADS) void k_bloom_rowscan(Work w, uint32_t j0, int from_bitmap) {
+__global__ __launch_bounds__(NTHREADS) void k_bloom_rowscan(Work w, uint32_t r, uint32_t hpr, int from_bitmap) {
     __shared__ uint32_t scratch[NWAVES + 1];
     const uint32_t t = tensor_of_slice(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t s = blockIdx.x - td.in.bl_slice0;
-    if (s >= td.in.bl_nslices || j0 >= td.in.k) return;
+    uint32_t j0, je;
+    bl_round(td, r, hpr, &j0, &je);
+    if (s >= td.in.bl_nslices || j0 >= je) return;
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (td.m_words * 32u + (1u << sl2) - 1) >> sl2;
     if (s >= nsl) return;
@@ -142,9 +161,11 @@ __global__ __launch_bounds__(NTHREADS) void k_bloom_rowscan(Work w, uint32_t j0,
 constexpr uint32_t SCAN_THREADS = 1024;
 
 // per tensor: start of each slice's bucket; the end of the last goes to bl_end
-__global__ __launch_bounds__(SCAN_THREADS) void k_bloom_rowbase(Work w, uint32_t j0) {
+__global__ __launch_bounds__(SCAN_THREADS) void k_bloom_rowbase(Work w, uint32_t r, uint32_t hpr) {
     TDesc &td = w.td[blockIdx.x];
-    if (j0 >= td.in.k) return;
+    uint32_t j0, je;
+    bl_round(td, r, hpr, &j0, &je);
+    if (j0 >= je) return;
     __shared__ uint32_t scratch[SCAN_THREADS / 64 + 1];
     const uint32_t sl2 = td.in.slice_log2;
     const uint32_t nsl = (td.m_words * 32u + (1u << sl2) - 1) >> sl2;
@@ -178,8 +199,8 @@ constexpr uint32_t SC_PER = SC_ITEMS / BL_THREADS;       // items per thread
 constexpr uint32_t SC_STAGE = SC_ITEMS * SC_HASHES;      // positions per group
 
 template <bool FROM_BITMAP>
-__global__ __launch_bounds__(BL_THREADS) __attribute__((amdgpu_waves_per_eu(8))) void k_bloom_scatter(Work w, uint32_t j0,
-                                                                                                     uint32_t j1) {
+__global__ __launch_bounds__(BL_THREADS) __attribute__((amdgpu_waves_per_eu(8))) void k_bloom_scatter(Work w, uint32_t r,
+                                                                                                     uint32_t hpr) {
     __shared__ uint32_t gcur[BL_MAX_SLICES];  // next record of this chunk in each slice's bucket
     __shared__ uint32_t cnt[BL_MAX_SLICES];   // the group's positions per slice
     __shared__ uint32_t off[BL_MAX_SLICES];   // their start in the staging area
@@ -192,7 +213,8 @@ __global__ __launch_bounds__(BL_THREADS) __attribute__((amdgpu_waves_per_eu(8)))
     TDesc &td = w.td[t];
     const uint32_t c = blockIdx.x - td.in.bl_chunk0;
     if (c >= td.in.bl_nchunks || c >= active_chunks(td, FROM_BITMAP)) return;
-    const uint32_t je = min(j1, td.in.k);
+    uint32_t j0, je;
+    bl_round(td, r, hpr, &j0, &je);
     if (je <= j0) return;
     const uint32_t m_bits = td.m_words * 32u;
     __shared__ uint32_t ps[33];
@@ -320,12 +342,17 @@ __global__ __launch_bounds__(BL_THREADS) __attribute__((amdgpu_waves_per_eu(8)))
 
 // Fill: one block per slice sets its bucket's bits in an LDS copy of the
 // slice (up to 128 KiB) and writes the slice out.
-__global__ __launch_bounds__(BL_THREADS) void k_bloom_fill(Work w, uint32_t j0, uint32_t j1) {
+__global__ __launch_bounds__(BL_THREADS) void k_bloom_fill(Work w, uint32_t r, uint32_t hpr) {
     __shared__ uint32_t words[SLICE_WORDS_MAX];
     const uint32_t t = tensor_of_slice(w, blockIdx.x);
     const TDesc &td = w.td[t];
     const uint32_t s = blockIdx.x - td.in.bl_slice0;
     if (s >= td.in.bl_nslices) return;
+    uint32_t j0, je;
+    bl_round(td, r, hpr, &j0, &je);
+    // a round past the tensor's last leaves its filter alone; round 0 of a
+    // tensor with no hashes (k = 0) still writes its empty slices
+    if (r > 0 && j0 >= je) return;
     const uint32_t m_words = td.m_words;
     const uint32_t m_bits = m_words * 32u;
     const uint32_t sl2 = td.in.slice_log2;
@@ -335,9 +362,8 @@ __global__ __launch_bounds__(BL_THREADS) void k_bloom_fill(Work w, uint32_t j0, 
     uint32_t *out = td.in.bits + (uint64_t)s * slice_words;
     const uint32_t lim = min(slice_words, m_words - s * slice_words);
     // the first round starts from an empty slice, later rounds add to it
-    for (uint32_t i = threadIdx.x; i < slice_words; i += BL_THREADS) words[i] = (j0 > 0 && i < lim) ? out[i] : 0u;
+    for (uint32_t i = threadIdx.x; i < slice_words; i += BL_THREADS) words[i] = (r > 0 && i < lim) ? out[i] : 0u;
     __syncthreads();
-    const uint32_t je = min(j1, td.in.k);
     if (je > j0) {
         const uint32_t start = w.brow[w.bslices + blockIdx.x];
         uint32_t end = start + w.brow[blockIdx.x];
@@ -540,29 +566,30 @@ hipError_t launch_bloom_insert(const Work &w, bool from_bitmap, uint32_t total_c
                                uint32_t max_slices, uint32_t hash_per_round, uint32_t kmax, hipStream_t s) {
     // LDS for one counter per slice of the largest filter
     const size_t lds = (size_t)max_slices * 4u;
-    uint32_t j0 = 0;
-    do {
-        const uint32_t j1 = j0 + hash_per_round;
+    // the rounds the plan needs; a tensor with fewer items than planned may
+    // need fewer (bl_round), and later rounds' kernels skip it
+    const uint32_t hpr = std::max<uint32_t>(1, hash_per_round);
+    const uint32_t rounds = std::max<uint32_t>(1, (kmax + hpr - 1) / hpr);
+    for (uint32_t r = 0; r < rounds; ++r) {
         if (total_chunks) {
             if (from_bitmap)
-                k_bloom_count<true><<<total_chunks, BL_THREADS, lds, s>>>(w, j0, j1);
+                k_bloom_count<true><<<total_chunks, BL_THREADS, lds, s>>>(w, r, hpr);
             else
-                k_bloom_count<false><<<total_chunks, BL_THREADS, lds, s>>>(w, j0, j1);
+                k_bloom_count<false><<<total_chunks, BL_THREADS, lds, s>>>(w, r, hpr);
             trace_mark(s, "k_bloom_count");
-            k_bloom_rowscan<<<total_slices, NTHREADS, 0, s>>>(w, j0, from_bitmap ? 1 : 0);
+            k_bloom_rowscan<<<total_slices, NTHREADS, 0, s>>>(w, r, hpr, from_bitmap ? 1 : 0);
             trace_mark(s, "k_bloom_rowscan");
-            k_bloom_rowbase<<<w.ntensors, SCAN_THREADS, 0, s>>>(w, j0);
+            k_bloom_rowbase<<<w.ntensors, SCAN_THREADS, 0, s>>>(w, r, hpr);
             trace_mark(s, "k_bloom_rowbase");
             if (from_bitmap)
-                k_bloom_scatter<true><<<total_chunks, BL_THREADS, 0, s>>>(w, j0, j1);
+                k_bloom_scatter<true><<<total_chunks, BL_THREADS, 0, s>>>(w, r, hpr);
             else
-                k_bloom_scatter<false><<<total_chunks, BL_THREADS, 0, s>>>(w, j0, j1);
+                k_bloom_scatter<false><<<total_chunks, BL_THREADS, 0, s>>>(w, r, hpr);
             trace_mark(s, "k_bloom_scatter");
         }
-        k_bloom_fill<<<total_slices, BL_THREADS, 0, s>>>(w, j0, j1);
+        k_bloom_fill<<<total_slices, BL_THREADS, 0, s>>>(w, r, hpr);
         trace_mark(s, "k_bloom_fill");
-        j0 = j1;
-    } while (j0 < kmax);
+    }
     return hipGetLastError();
 }
 
