@@ -624,6 +624,36 @@ struct RecordView {
     uint32_t layout;  // LAYOUT_* of the filter (from the record's hash id)
 };
 
+// A record's fields, and a tensor's, are the same in every lane of a block:
+// readfirstlane states it, so that a loop over many tiles keeps them in
+// scalar registers rather than in a vector register each.
+__device__ __forceinline__ uint32_t uni(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ uint64_t uni(uint64_t x) {
+    return ((uint64_t)uni((uint32_t)(x >> 32)) << 32) | uni((uint32_t)x);
+}
+template <typename T>
+__device__ __forceinline__ T *uni(T *p) {
+    return (T *)uni((uint64_t)p);
+}
+__device__ __forceinline__ void uniform_record(RecordView &v) {
+    v.bits = uni(v.bits);
+    v.coef = uni(v.coef);
+    v.knots = uni(v.knots);
+    v.sigma = uni(v.sigma);
+    v.m_bits = uni(v.m_bits);
+    v.k = uni(v.k);
+    v.npos = uni(v.npos);
+    v.nv = uni(v.nv);
+    v.policy = uni(v.policy);
+    v.seed = uni(v.seed);
+    v.deff = uni(v.deff);
+    v.seff = uni(v.seff);
+    v.b = uni(v.b);
+    v.segmode = uni(v.segmode);
+    v.model = uni(v.model);
+    v.layout = uni(v.layout);
+}
+
 // Reads a record header and checks it against the record's capacity and
 // the tensor's size; an invalid record decodes as empty (k = 0) and is
 // flagged, so a damaged payload cannot send reads past its record.
@@ -1527,6 +1557,14 @@ constexpr uint32_t EMIT_KNOTS = 256;  // chord run starts staged in LDS (else re
 // pass: transformer_355m_x24 0.284 -> 0.227 ms, vgg16_138m 93 -> 71 us).
 constexpr uint32_t EMIT_THREADS = 128;
 static_assert(EMIT_THREADS >= TILE_WORDS, "each thread of an emit block reads one word of the tile's positives bitmap");
+// A tile's wait is mostly memory latency, so the passes want many blocks per
+// CU: six waves per SIMD (80 VGPRs, with the record and tensor fields in
+// scalar registers) give 12 blocks, as many as the LDS holds, instead of the
+// 8 that the receiver's pass got at 128 VGPRs (its time on
+// transformer_355m_x24 0.233 -> 0.216 ms, vgg16_138m 69 -> 59 us).  The
+// general decoder (chord runs, the double exponential) takes five, which it
+// fits without spilling.
+#define EMIT_WAVES_PER_EU(GEN) __attribute__((amdgpu_waves_per_eu((GEN) ? 5 : 6)))
 
 // Stage a record's coefficients and run starts in LDS when they fit (the
 // caller synchronises before use); the pointers to read them from: LDS or
@@ -1562,7 +1600,7 @@ __device__ __forceinline__ void match_layout(RecordView &rv, TDesc &td, uint64_t
 }
 
 template <int MODE, bool GEN = false>
-__global__ __launch_bounds__(EMIT_THREADS) void k_emit(Work w, QueryOut o) {
+__global__ __launch_bounds__(EMIT_THREADS) EMIT_WAVES_PER_EU(GEN) void k_emit(Work w, QueryOut o) {
     __shared__ uint32_t scratch[EMIT_THREADS / 64 + 1];
     __shared__ uint32_t pw[TILE_WORDS];
     __shared__ uint32_t pre[TILE_WORDS];
@@ -1598,23 +1636,24 @@ __global__ __launch_bounds__(EMIT_THREADS) void k_emit(Work w, QueryOut o) {
         const uint32_t t = tn;
         TDesc &td = w.td[t];
         if (t != cur_t) {
-            tile0 = td.in.tile0;
-            d = td.in.d;
-            toff_el = td.in.off;
-            tslot = td.in.slot;
+            tile0 = uni(td.in.tile0);
+            d = uni(td.in.d);
+            toff_el = uni(td.in.off);
+            tslot = uni(td.in.slot);
             if (MODE == Q_ENCODE) {
-                npos = td.npos;
-                ncoded = td.nv;
-                policy = td.in.policy;
-                pseed = td.in.seed;
-                sparse_vals = td.in.value_src == VALUES_SPARSE;
+                npos = uni(td.npos);
+                ncoded = uni(td.nv);
+                policy = uni(td.in.policy);
+                pseed = uni(td.in.seed);
+                sparse_vals = uni(td.in.value_src) == VALUES_SPARSE;
             }
             if (MODE == Q_DECODE) {
                 bool ok = true;
                 rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
                 match_layout<GEN>(rv, td, o.counts_out, t);
+                uniform_record(rv);
                 // the receiver's own positives, and the header's values count
-                npos = td.nv_dec;
+                npos = uni(td.nv_dec);
                 ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
                 policy = rv.policy;
                 pseed = rv.seed;
