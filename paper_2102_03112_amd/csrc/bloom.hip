@@ -1740,20 +1740,21 @@ __global__ __launch_bounds__(NTHREADS) void k_emit_sum(Work w, QueryOut o) {
     __shared__ uint32_t kn[EMIT_KNOTS];
     constexpr uint32_t GROUPS = TILE / (4 * NTHREADS);
     for (uint32_t tile = blockIdx.x; tile < o.ntiles1; tile += gridDim.x) {
-        const uint32_t t = tensor_of_tile(w, tile);  // payload 0's descriptor of the tensor
-        const uint32_t lt = tile - w.td[t].in.tile0;
-        const uint32_t d = w.td[t].in.d;
-        const uint64_t toff_el = w.td[t].in.off;
+        const uint32_t t = uni(tensor_of_tile(w, tile));  // payload 0's descriptor of the tensor
+        const uint32_t lt = tile - uni(w.td[t].in.tile0);
+        const uint32_t d = uni(w.td[t].in.d);
+        const uint64_t toff_el = uni(w.td[t].in.off);
         for (uint32_t e = threadIdx.x; e < TILE; e += NTHREADS) acc[e] = 0.0f;
         for (uint32_t p = 0; p < o.npay; ++p) {
             const uint32_t v = p * o.ntens + t;
             TDesc &td = w.td[v];
             const uint32_t ptile = p * o.ntiles1 + tile;
             const uint32_t word = threadIdx.x < TILE_WORDS ? w.pbits[(uint64_t)ptile * TILE_WORDS + threadIdx.x] : 0u;
-            const uint32_t q0 = w.toff[ptile];
+            const uint32_t q0 = uni(w.toff[ptile]);
             bool ok = true;
-            const RecordView rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
-            const uint32_t npos = td.nv_dec;
+            RecordView rv = read_record(td.in.rec, td.in.rec_cap, d, &ok);
+            uniform_record(rv);
+            const uint32_t npos = uni(td.nv_dec);
             const uint32_t ncoded = rv.policy == POLICY_P0 ? npos : min(rv.nv, npos);
             uint32_t tot;
             const uint32_t ex = block_excl_scan(__popc(word), scratch, &tot);
