@@ -888,15 +888,21 @@ __device__ __forceinline__ uint32_t tensor_of_fit_block(const Work &w, uint32_t 
 
 // Moments of one chunk of a run: sums of t^e (e <= 2D) and t^e y (e <= D)
 // over local ranks [j0, j1) of a run of ns points starting at lo_run.
-// Each thread reads FIT_BATCH values before it uses any.
-constexpr uint32_t FIT_THREADS = 1024;
+// Each thread reads FIT_BATCH values before it uses any.  Blocks of four
+// waves: beside the receiver's probe pass the launch has 32 CUs, and
+// 1024-thread blocks (one per CU at 120 VGPRs) left them idle between
+// rounds of blocks; at 256 threads (146 VGPRs, three blocks per CU) the
+// launch took resnet50_25m 33 -> 22 us, vgg16_138m 73 -> 31 us and
+// transformer_355m_x24 600 -> 391 us.  Long runs get fewer threads
+// (FIT_CHUNKS blocks each): ncf_32m's launch went from 0.22 to 0.48 ms,
+// inside the slack its sender's branch has beside the receiver's query.
+constexpr uint32_t FIT_THREADS = 256;
 constexpr uint32_t FIT_BATCH = 8;
 
 // Chunks a run of ns points is cut into: at most FIT_CHUNKS, each at least
 // a batch per thread.  A block reduces its 3 D + 2 sums over all its waves
-// whatever its chunk's size, so eight chunks of a short run are mostly
-// reductions (transformer_355m_x24: 192 runs of 18.5 K points, now three
-// chunks each).  The blocks of unused chunks write zero partials.
+// whatever its chunk's size, so many chunks of a short run would be mostly
+// reductions.  The blocks of unused chunks write zero partials.
 constexpr uint64_t FIT_MIN_CHUNK = (uint64_t)FIT_THREADS * FIT_BATCH;
 __device__ __forceinline__ uint32_t fit_chunks(uint64_t ns) {
     const uint64_t c = (ns + FIT_MIN_CHUNK - 1) / FIT_MIN_CHUNK;
@@ -1393,6 +1399,8 @@ hipError_t launch_fit(const Work &w, uint32_t fit_blocks, uint64_t vals_est, boo
     // work's slots instead (one per 32 Ki, at most 1024), resnet50_25m
     // launched 780 blocks for 166 K words; with the words found by a cursor
     // instead of a search per word, ncf_32m's launch went from 0.45 to 0.25 ms.
+    // (At most 512 Ki threads instead of 512 blocks, as many threads as
+    // before the fit's blocks shrank to 256, changed no workload's step.)
     constexpr uint64_t PACK_PER_BLOCK = 4ull * FIT_THREADS;
     const uint32_t pack_blocks =
         (uint32_t)std::min<uint64_t>(512, std::max<uint64_t>(8, (vals_est + PACK_PER_BLOCK - 1) / PACK_PER_BLOCK));
